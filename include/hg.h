@@ -1,0 +1,230 @@
+/*
+ * hg.h -- C ABI of libhg.so, the MI355X (gfx950) hot path of risk-aware
+ * overlapping-subgraph GNN training.
+ *
+ * Paper: "Empowering Credit Risk Detection in Weixin Pay with Billion-Scale
+ * Deep Graph Learning" (RAOS).  Each worker trains on one overlapping
+ * subgraph; this library runs one worker's share on one GPU:
+ *
+ *   hg_build_csr            overlapping-subgraph construction (Methodology,
+ *                           "Risk-Aware Subgraph Construction": candidate-set
+ *                           and union equations; Algorithm 1, construction loop)
+ *   hg_layer_fwd/_bwd       one relation-typed message-passing layer
+ *                           (message, aggregation and update equations of the
+ *                           "Heterogeneous Graph Transformer" paragraph, in the
+ *                           relation-typed mean-aggregation form)
+ *   hg_align_loss_fwd_bwd   the CCA consistency-alignment loss on the overlap
+ *                           nodes and its gradient (Section "Cross-Subgraph
+ *                           Consistency Alignment", standardisation, invariance,
+ *                           decorrelation and CCA-loss equations; the lambda_CCA
+ *                           weight of the joint objective)
+ *
+ * Conventions (all entry points):
+ *  - Pointers named in a struct or argument list are DEVICE pointers unless
+ *    the comment says "host".  Matrices are row-major and contiguous.
+ *  - The caller owns every buffer.  The library never allocates or frees
+ *    device memory, keeps no pointer past a call and holds no mutable global
+ *    state apart from a per-device property cache and the optional timing
+ *    log (hg_timing_*).  Calls on disjoint buffers are re-entrant.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *    Everything except hg_build_csr is asynchronous on that stream.
+ *  - Return value: HG_OK (0) or a negative HG_ERR_* code.  Arguments are
+ *    validated on the host before any device work; on error nothing is
+ *    launched (except HG_ERR_RANGE / HG_ERR_HIP, see hg_build_csr) and
+ *    hg_last_error_detail() describes the cause.  No C++ exception crosses
+ *    the ABI.
+ *  - Ids are int32, counts int64, features float32 or bfloat16 (dtype),
+ *    weights and weight gradients always float32.
+ */
+#ifndef HG_H_
+#define HG_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ------------------------------------------------------ */
+#define HG_OK               0
+#define HG_ERR_ARG         -1  /* null pointer, bad size or option          */
+#define HG_ERR_RANGE       -2  /* an id >= n_nodes, rel >= n_rel, ntype >= n_ntype */
+#define HG_ERR_CAPACITY    -3  /* workspace / plan too small (needed size in detail) */
+#define HG_ERR_HIP         -4  /* a HIP runtime or launch error             */
+#define HG_ERR_UNSUPPORTED -5  /* valid but not implemented (dtype, d, sizes) */
+
+/* ---- options ----------------------------------------------------------- */
+#define HG_KEY_OUTDEG  0   /* node key = out-degree over all relations      */
+#define HG_KEY_HINDEX  1   /* node key = h-index of the out-neighbour multiset */
+#define HG_KEYDIR_OUT  0   /* only direction implemented                    */
+#define HG_THETA_NONE  2147483647
+#define HG_DTYPE_F32   0
+#define HG_DTYPE_BF16  1
+#define HG_MAX_REL     255
+#define HG_MAX_NTYPE   255
+
+/* Input graph: one snapshot, typed nodes and typed directed edges
+ * (Problem Formulation: node-type and edge-type maps).  Edge e goes from
+ * src[e] to dst[e] with relation rel[e].  The base set is
+ * V_k = { v : part[v] == k } (one block of the base partition, Graph
+ * Partition paragraph).  Limits: 0 <= n_edges < 2^31, 1 <= n_nodes < 2^31,
+ * n_nodes * n_rel < 2^31, 1 <= n_rel <= 255, 1 <= n_ntype <= 255. */
+typedef struct hg_graph_desc {
+  int64_t n_nodes;
+  int64_t n_edges;
+  int32_t n_rel;
+  int32_t n_ntype;
+  const int32_t* src;     /* [n_edges] */
+  const int32_t* dst;     /* [n_edges] */
+  const uint8_t* rel;     /* [n_edges] */
+  const uint8_t* ntype;   /* [n_nodes] */
+  const int32_t* part;    /* [n_nodes] partition id of every node */
+  int32_t k;              /* this worker's partition */
+  const float* edge_w;    /* must be NULL: weighted edges are not implemented */
+} hg_graph_desc;
+
+/* Budgeted long-tail overlap selection (h-index filter and TopM steps of
+ * Algorithm 1).  Candidates C_k are nodes outside V_k joined to V_k by an
+ * edge in either direction; C'_k keeps those with key <= theta; the first
+ * min(budget_M, |C'_k|) of C'_k in ascending (key, splitmix64(seed ^ gid),
+ * gid) order are selected, where splitmix64(x) is the first output of the
+ * SplitMix64 generator (Steele, Lea and Flood 2014) started from state x. */
+typedef struct hg_overlap_desc {
+  int64_t budget_M;       /* >= 0 */
+  int32_t key;            /* HG_KEY_OUTDEG or HG_KEY_HINDEX */
+  int32_t key_dir;        /* HG_KEYDIR_OUT */
+  int32_t theta;          /* >= 0; HG_THETA_NONE = no filter */
+  int32_t reserved;
+  uint64_t seed;
+} hg_overlap_desc;
+
+/* Overlapping subgraph G[V_k u C_{k,M}] (union equation; induced subgraph of
+ * Algorithm 1).  Local ids order the nodes by (node type, global id), so each
+ * type is a contiguous range [type_off[t], type_off[t+1]).  Row (v, r) of the
+ * CSR holds the in-edges of relation r of local node v (index v*n_rel + r),
+ * entries in ascending original edge index; the CSC likewise holds
+ * out-edges.  csc_scale[p] = 1 / deg_r(csc_row[p]), the mean-aggregation
+ * weight, as a correctly rounded float32 quotient.
+ *
+ * The caller allocates every device array to CAPACITY: node arrays n_nodes,
+ * overlap arrays min(budget_M, n_nodes), type_off n_ntype + 1, pointer arrays
+ * n_nodes * n_rel + 1, edge arrays n_edges, plan hg_plan_size() bytes.
+ * csr_eid may be NULL.  hg_build_csr fills the host fields. */
+typedef struct hg_subgraph {
+  /* device outputs */
+  int32_t* local2global;  /* [n_sub]  */
+  int32_t* global2local;  /* [n_nodes], -1 for nodes outside the subgraph */
+  int32_t* type_off;      /* [n_ntype + 1] */
+  int32_t* overlap;       /* [m_sel] local ids of C_{k,M}, ascending */
+  int32_t* overlap_home;  /* [m_sel] part[] of each overlap node */
+  uint8_t* overlap_rel;   /* [m_sel] relation of the lowest-index edge joining it to V_k */
+  int32_t* csr_ptr;       /* [n_sub * n_rel + 1] */
+  int32_t* csr_col;       /* [e_sub] source local id */
+  int32_t* csr_eid;       /* [e_sub] original edge index, or NULL */
+  int32_t* csc_ptr;       /* [n_sub * n_rel + 1] */
+  int32_t* csc_row;       /* [e_sub] destination local id */
+  float*   csc_scale;     /* [e_sub] */
+  void*    plan;          /* opaque execution plan used by the layer kernels */
+  size_t   plan_bytes;    /* capacity of plan */
+  /* host outputs */
+  int64_t n_nodes;        /* input graph sizes, copied from the descriptor */
+  int64_t n_edges;
+  int64_t n_sub;          /* |V_k u C_{k,M}| */
+  int64_t e_sub;          /* edges of the induced subgraph */
+  int64_t m_sel;          /* |C_{k,M}| */
+  int32_t n_rel;
+  int32_t n_ntype;
+  int64_t type_off_host[HG_MAX_NTYPE + 1];
+  int64_t n_active[HG_MAX_REL];   /* sources with >= 1 out-edge of relation r */
+  int64_t plan_items;     /* backward work items (internal) */
+  int64_t plan_heavy;     /* split CSC rows (internal) */
+  int64_t plan_partials;  /* partial rows of split CSC rows (internal) */
+} hg_subgraph;
+
+/* Bytes of `plan` for a graph with these input sizes. */
+size_t hg_plan_size(int64_t n_nodes, int64_t n_edges, int32_t n_rel);
+
+/* Scratch bytes hg_build_csr needs for this input (host call, no device work). */
+size_t hg_build_csr_workspace_size(const hg_graph_desc* g, const hg_overlap_desc* o);
+
+/* Build the overlapping subgraph of partition g->k.  SYNCHRONOUS: it
+ * synchronises `stream` once at the end, checks the device-side range flag
+ * and fills the host fields of *out.  Returns HG_ERR_RANGE if any src/dst is
+ * outside [0, n_nodes), rel >= n_rel or ntype >= n_ntype (device arrays are
+ * then unspecified).  ws: ws_bytes >= hg_build_csr_workspace_size(). */
+int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg_subgraph* out,
+                 void* ws, size_t ws_bytes, void* stream);
+
+/* One layer (the update equation with sigma = ReLU and the residual):
+ *   z_j  = sum_r (1/|N_r(j)|) sum_{i in N_r(j)} h_i W_r + h_j W_self[type(j)] + b[type(j)]
+ *   h'_j = (relu ? max(z_j, 0) : z_j) + (residual ? h_j : 0)
+ * (an empty N_r(j) contributes 0).  d_in == d_out == d. */
+typedef struct hg_layer_desc {
+  int32_t d_in;
+  int32_t d_out;
+  int32_t dtype;     /* HG_DTYPE_F32 (d in {64,128}) or HG_DTYPE_BF16 (d in {64,128,256}) */
+  int32_t relu;      /* 0 or 1 */
+  int32_t residual;  /* 0 or 1 */
+} hg_layer_desc;
+
+/* Bytes of `saved` (the ReLU mask: bit c of row j, at 32-bit word
+ * j*(d/32) + c/32, bit c%32, is 1 iff z[j][c] > 0). */
+size_t hg_layer_saved_size(const hg_subgraph* s, const hg_layer_desc* L);
+size_t hg_layer_fwd_workspace_size(const hg_subgraph* s, const hg_layer_desc* L);
+size_t hg_layer_bwd_workspace_size(const hg_subgraph* s, const hg_layer_desc* L);
+
+/* Forward.  H_in, H_out: [n_sub, d] of dtype; W_rel [n_rel, d, d],
+ * W_self [n_ntype, d, d] (row-vector convention y = x W), bias [n_ntype, d]
+ * (may be NULL = 0).  saved receives the ReLU mask.  H_out must not alias H_in. */
+int hg_layer_fwd(const hg_subgraph* s, const hg_layer_desc* L, const void* H_in,
+                 const float* W_rel, const float* W_self, const float* bias,
+                 void* H_out, void* saved, void* ws, size_t ws_bytes, void* stream);
+
+/* Backward of hg_layer_fwd for upstream gradient dH_out = dL/dH_out:
+ *   dZ = dH_out * mask,  dH_in = dH_out (residual) + dZ W_self^T + sum_r A_r^T dZ W_r^T,
+ *   dW_r = (A_r H_in)^T dZ,  dW_self[t] = H_t^T dZ_t,  dbias[t] = sum_t dZ_t.
+ * Every output is OVERWRITTEN.  dbias may be NULL.  Deterministic: no
+ * floating-point atomics, fixed reduction orders. */
+int hg_layer_bwd(const hg_subgraph* s, const hg_layer_desc* L, const void* H_in,
+                 const float* W_rel, const float* W_self, const void* saved,
+                 const void* dH_out, void* dH_in, float* dW_rel, float* dW_self,
+                 float* dbias, void* ws, size_t ws_bytes, void* stream);
+
+/* CCA alignment on the overlap batch B (|B| = M):
+ *   X = H[overlap] (local view), Y = H_ref (the other subgraph's view, row b
+ *   for overlap[b]); per column mu and sigma = sqrt(var + eps), var with
+ *   divisor M - ddof; Xh = (X - mu) / (sigma sqrt(M)), same for Y;
+ *   L_inv = sum_b w_b ||Xh_b - Yh_b||^2 (w = 1 if NULL),
+ *   L_dec = ||Xh^T Xh - I||_F^2 + ||Yh^T Yh - I||_F^2,  L = L_inv + lambda_n L_dec.
+ * Writes loss3[0..2] = (L_inv, L_dec, L) (device float32) and ADDS
+ * scale * dL/dX into rows overlap[b] of dH (scale = lambda_CCA).  If dH_ref is
+ * not NULL it is OVERWRITTEN with scale * dL/dY.  H, dH: [n_rows, d];
+ * H_ref, dH_ref: [M, d]; overlap entries distinct and in [0, n_rows).
+ * M = 0 writes zeros.  Requires M > ddof, d in {64, 128, 256}. */
+size_t hg_align_workspace_size(int64_t M, int32_t d);
+int hg_align_loss_fwd_bwd(int64_t M, int32_t d, int32_t dtype, int64_t n_rows,
+                          const void* H, const int32_t* overlap, const void* H_ref,
+                          const float* w, float lambda_n, float scale, float eps,
+                          int32_t ddof, float* loss3, void* dH, void* dH_ref,
+                          void* ws, size_t ws_bytes, void* stream);
+
+/* ---- diagnostics ------------------------------------------------------- */
+const char* hg_status_string(int status);
+/* Thread-local description of the last error (host memory, valid until the
+ * next call on this thread). */
+const char* hg_last_error_detail(void);
+
+/* ---- kernel timing (instrumentation, off by default) --------------------
+ * While enabled, every kernel launch of this library is bracketed by two
+ * hipEvents recorded on the launch stream.  hg_timing_collect synchronises
+ * those events and returns, per kernel name, the number of launches and the
+ * summed duration in milliseconds; it then clears the log. */
+int hg_timing_enable(int on);
+/* Fills up to `cap` entries; returns the number of kernel names (may exceed cap). */
+int hg_timing_collect(char (*names)[64], int64_t* launches, double* total_ms, int cap);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* HG_H_ */

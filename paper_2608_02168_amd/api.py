@@ -1,0 +1,345 @@
+"""ctypes binding of libhg.so with the same entry-point names as include/hg.h.
+
+Argument marshalling only: torch tensors provide device memory and the
+current stream; every step of the computation runs in the library's HIP
+kernels.  If libhg.so is missing this module raises on first use -- there
+is no fallback implementation.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from dataclasses import dataclass, field
+from typing import Optional
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libhg.so")
+
+HG_OK = 0
+HG_ERR_ARG = -1
+HG_ERR_RANGE = -2
+HG_ERR_CAPACITY = -3
+HG_ERR_HIP = -4
+HG_ERR_UNSUPPORTED = -5
+HG_KEY_OUTDEG = 0
+HG_KEY_HINDEX = 1
+HG_KEYDIR_OUT = 0
+HG_THETA_NONE = 2**31 - 1
+HG_DTYPE_F32 = 0
+HG_DTYPE_BF16 = 1
+HG_MAX_REL = 255
+HG_MAX_NTYPE = 255
+
+EXPORTS = [
+    "hg_plan_size", "hg_build_csr_workspace_size", "hg_build_csr",
+    "hg_layer_saved_size", "hg_layer_fwd_workspace_size", "hg_layer_bwd_workspace_size",
+    "hg_layer_fwd", "hg_layer_bwd", "hg_align_workspace_size", "hg_align_loss_fwd_bwd",
+    "hg_status_string", "hg_last_error_detail", "hg_timing_enable", "hg_timing_collect",
+]
+
+
+class HgError(RuntimeError):
+    def __init__(self, status: int, where: str, detail: str):
+        super().__init__(f"{where}: {status_string(status)} ({detail})")
+        self.status = status
+
+
+class GraphDesc(C.Structure):
+    _fields_ = [("n_nodes", C.c_int64), ("n_edges", C.c_int64), ("n_rel", C.c_int32),
+                ("n_ntype", C.c_int32), ("src", C.c_void_p), ("dst", C.c_void_p),
+                ("rel", C.c_void_p), ("ntype", C.c_void_p), ("part", C.c_void_p),
+                ("k", C.c_int32), ("edge_w", C.c_void_p)]
+
+
+class OverlapDesc(C.Structure):
+    _fields_ = [("budget_M", C.c_int64), ("key", C.c_int32), ("key_dir", C.c_int32),
+                ("theta", C.c_int32), ("reserved", C.c_int32), ("seed", C.c_uint64)]
+
+
+class SubgraphStruct(C.Structure):
+    _fields_ = [("local2global", C.c_void_p), ("global2local", C.c_void_p),
+                ("type_off", C.c_void_p), ("overlap", C.c_void_p), ("overlap_home", C.c_void_p),
+                ("overlap_rel", C.c_void_p), ("csr_ptr", C.c_void_p), ("csr_col", C.c_void_p),
+                ("csr_eid", C.c_void_p), ("csc_ptr", C.c_void_p), ("csc_row", C.c_void_p),
+                ("csc_scale", C.c_void_p), ("plan", C.c_void_p), ("plan_bytes", C.c_size_t),
+                ("n_nodes", C.c_int64), ("n_edges", C.c_int64), ("n_sub", C.c_int64),
+                ("e_sub", C.c_int64), ("m_sel", C.c_int64), ("n_rel", C.c_int32),
+                ("n_ntype", C.c_int32), ("type_off_host", C.c_int64 * (HG_MAX_NTYPE + 1)),
+                ("n_active", C.c_int64 * HG_MAX_REL), ("plan_items", C.c_int64),
+                ("plan_heavy", C.c_int64), ("plan_partials", C.c_int64)]
+
+
+class LayerDesc(C.Structure):
+    _fields_ = [("d_in", C.c_int32), ("d_out", C.c_int32), ("dtype", C.c_int32),
+                ("relu", C.c_int32), ("residual", C.c_int32)]
+
+
+_lib = None
+
+
+def lib() -> C.CDLL:
+    """Load libhg.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: run __graft_entry__.build() "
+                          "(python -m paper_2608_02168_amd.build)")
+    L = C.CDLL(LIB_PATH)
+    vp, sz, i64, i32, f32 = C.c_void_p, C.c_size_t, C.c_int64, C.c_int32, C.c_float
+    sig = {
+        "hg_plan_size": (sz, [i64, i64, i32]),
+        "hg_build_csr_workspace_size": (sz, [vp, vp]),
+        "hg_build_csr": (C.c_int, [vp, vp, vp, vp, sz, vp]),
+        "hg_layer_saved_size": (sz, [vp, vp]),
+        "hg_layer_fwd_workspace_size": (sz, [vp, vp]),
+        "hg_layer_bwd_workspace_size": (sz, [vp, vp]),
+        "hg_layer_fwd": (C.c_int, [vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "hg_layer_bwd": (C.c_int, [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "hg_align_workspace_size": (sz, [i64, i32]),
+        "hg_align_loss_fwd_bwd": (C.c_int, [i64, i32, i32, i64, vp, vp, vp, vp, f32, f32, f32,
+                                            i32, vp, vp, vp, vp, sz, vp]),
+        "hg_status_string": (C.c_char_p, [C.c_int]),
+        "hg_last_error_detail": (C.c_char_p, []),
+        "hg_timing_enable": (C.c_int, [C.c_int]),
+        "hg_timing_collect": (C.c_int, [vp, vp, vp, C.c_int]),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(L, name)
+        f.restype = res
+        f.argtypes = args
+    _lib = L
+    return L
+
+
+def status_string(status: int) -> str:
+    return lib().hg_status_string(status).decode()
+
+
+def last_error_detail() -> str:
+    return lib().hg_last_error_detail().decode()
+
+
+def _check(status: int, where: str):
+    if status != HG_OK:
+        raise HgError(status, where, last_error_detail())
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else C.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return C.c_void_p(stream.cuda_stream)
+
+
+def _ws(nbytes: int, device) -> torch.Tensor:
+    return torch.empty(max(1, int(nbytes)), dtype=torch.uint8, device=device)
+
+
+@dataclass
+class Subgraph:
+    """Device arrays of hg_subgraph plus the host counts the build returned."""
+    c: SubgraphStruct
+    device: torch.device
+    arrays: dict = field(default_factory=dict)
+
+    @property
+    def n_sub(self) -> int:
+        return int(self.c.n_sub)
+
+    @property
+    def e_sub(self) -> int:
+        return int(self.c.e_sub)
+
+    @property
+    def m_sel(self) -> int:
+        return int(self.c.m_sel)
+
+    @property
+    def n_rel(self) -> int:
+        return int(self.c.n_rel)
+
+    @property
+    def n_ntype(self) -> int:
+        return int(self.c.n_ntype)
+
+    def view(self, name: str) -> torch.Tensor:
+        """The valid prefix of one output array."""
+        n_ptr = self.n_sub * self.n_rel + 1
+        length = {"local2global": self.n_sub, "global2local": int(self.c.n_nodes),
+                  "type_off": self.n_ntype + 1, "overlap": self.m_sel,
+                  "overlap_home": self.m_sel, "overlap_rel": self.m_sel, "csr_ptr": n_ptr,
+                  "csc_ptr": n_ptr, "csr_col": self.e_sub, "csr_eid": self.e_sub,
+                  "csc_row": self.e_sub, "csc_scale": self.e_sub}[name]
+        return self.arrays[name][:length]
+
+    def n_active(self):
+        return [int(self.c.n_active[r]) for r in range(self.n_rel)]
+
+    def type_off_host(self):
+        return [int(self.c.type_off_host[t]) for t in range(self.n_ntype + 1)]
+
+
+def hg_plan_size(n_nodes: int, n_edges: int, n_rel: int) -> int:
+    return int(lib().hg_plan_size(n_nodes, n_edges, n_rel))
+
+
+def hg_build_csr(src, dst, rel, ntype, part, k: int, n_rel: int, n_ntype: int, budget_M: int,
+                 key: int = HG_KEY_OUTDEG, theta: int = HG_THETA_NONE, seed: int = 0,
+                 want_eid: bool = True, stream=None, ws: Optional[torch.Tensor] = None,
+                 out: Optional[Subgraph] = None) -> Subgraph:
+    """Overlapping-subgraph construction; inputs are device tensors
+    (src/dst/part int32, rel/ntype uint8).  Synchronous.  ``out`` reuses the
+    arrays of an earlier build of the same input sizes."""
+    dev = ntype.device
+    n, e = int(ntype.shape[0]), int(src.shape[0])
+    g = GraphDesc(n, e, n_rel, n_ntype, _ptr(src), _ptr(dst), _ptr(rel), _ptr(ntype), _ptr(part),
+                  k, None)
+    o = OverlapDesc(budget_M, key, HG_KEYDIR_OUT, theta, 0, seed)
+    L = lib()
+    if out is not None:
+        if ws is None:
+            ws = _ws(int(L.hg_build_csr_workspace_size(C.byref(g), C.byref(o))), dev)
+        _check(L.hg_build_csr(C.byref(g), C.byref(o), C.byref(out.c), _ptr(ws), ws.numel(),
+                              _stream(stream)), "hg_build_csr")
+        return out
+    i32 = dict(dtype=torch.int32, device=dev)
+    m_cap = max(1, min(budget_M, n))
+    nq = n * n_rel + 1
+    arrays = {
+        "local2global": torch.empty(n, **i32), "global2local": torch.empty(n, **i32),
+        "type_off": torch.empty(n_ntype + 1, **i32), "overlap": torch.empty(m_cap, **i32),
+        "overlap_home": torch.empty(m_cap, **i32),
+        "overlap_rel": torch.empty(m_cap, dtype=torch.uint8, device=dev),
+        "csr_ptr": torch.empty(nq, **i32), "csr_col": torch.empty(max(1, e), **i32),
+        "csr_eid": torch.empty(max(1, e), **i32) if want_eid else None,
+        "csc_ptr": torch.empty(nq, **i32), "csc_row": torch.empty(max(1, e), **i32),
+        "csc_scale": torch.empty(max(1, e), dtype=torch.float32, device=dev),
+    }
+    plan_bytes = hg_plan_size(n, e, n_rel)
+    arrays["plan"] = _ws(plan_bytes, dev)
+    s = SubgraphStruct()
+    for name in ("local2global", "global2local", "type_off", "overlap", "overlap_home",
+                 "overlap_rel", "csr_ptr", "csr_col", "csr_eid", "csc_ptr", "csc_row",
+                 "csc_scale", "plan"):
+        setattr(s, name, _ptr(arrays[name]))
+    s.plan_bytes = plan_bytes
+    need = int(L.hg_build_csr_workspace_size(C.byref(g), C.byref(o)))
+    if need == 0:
+        _check(L.hg_build_csr(C.byref(g), C.byref(o), C.byref(s), None, 0, _stream(stream)),
+               "hg_build_csr")
+    if ws is None or ws.numel() < need:
+        ws = _ws(need, dev)
+    _check(L.hg_build_csr(C.byref(g), C.byref(o), C.byref(s), _ptr(ws), ws.numel(),
+                          _stream(stream)), "hg_build_csr")
+    return Subgraph(s, dev, arrays)
+
+
+def _layer_desc(d: int, dtype, relu: bool, residual: bool) -> LayerDesc:
+    code = HG_DTYPE_BF16 if dtype == torch.bfloat16 else HG_DTYPE_F32
+    return LayerDesc(d, d, code, int(relu), int(residual))
+
+
+def hg_layer_saved_size(sub: Subgraph, d: int, dtype=torch.float32) -> int:
+    desc = _layer_desc(d, dtype, True, True)
+    return int(lib().hg_layer_saved_size(C.byref(sub.c), C.byref(desc)))
+
+
+def hg_layer_fwd_workspace_size(sub: Subgraph, d: int, dtype=torch.float32) -> int:
+    desc = _layer_desc(d, dtype, True, True)
+    return int(lib().hg_layer_fwd_workspace_size(C.byref(sub.c), C.byref(desc)))
+
+
+def hg_layer_bwd_workspace_size(sub: Subgraph, d: int, dtype=torch.float32) -> int:
+    desc = _layer_desc(d, dtype, True, True)
+    return int(lib().hg_layer_bwd_workspace_size(C.byref(sub.c), C.byref(desc)))
+
+
+def hg_layer_fwd(sub: Subgraph, H_in, W_rel, W_self, bias=None, relu=True, residual=True,
+                 H_out=None, saved=None, ws=None, stream=None):
+    """Returns (H_out, saved); saved is the ReLU bitmask [n_sub, d/32] int32."""
+    d = int(H_in.shape[1])
+    desc = _layer_desc(d, H_in.dtype, relu, residual)
+    L = lib()
+    if H_out is None:
+        H_out = torch.empty_like(H_in)
+    if saved is None:
+        saved = torch.empty((max(1, sub.n_sub), (d + 31) // 32), dtype=torch.int32, device=H_in.device)
+    if ws is None:
+        need = int(L.hg_layer_fwd_workspace_size(C.byref(sub.c), C.byref(desc)))
+        ws = _ws(need, H_in.device)
+    _check(L.hg_layer_fwd(C.byref(sub.c), C.byref(desc), _ptr(H_in), _ptr(W_rel), _ptr(W_self),
+                          _ptr(bias), _ptr(H_out), _ptr(saved), _ptr(ws), ws.numel(),
+                          _stream(stream)), "hg_layer_fwd")
+    return H_out, saved
+
+
+def hg_layer_bwd(sub: Subgraph, H_in, W_rel, W_self, saved, dH_out, relu=True, residual=True,
+                 dH_in=None, dW_rel=None, dW_self=None, dbias=None, want_dbias=True, ws=None,
+                 stream=None):
+    """Returns (dH_in, dW_rel, dW_self, dbias)."""
+    d = int(H_in.shape[1])
+    desc = _layer_desc(d, H_in.dtype, relu, residual)
+    L = lib()
+    dev = H_in.device
+    if dH_in is None:
+        dH_in = torch.empty_like(H_in)
+    if dW_rel is None:
+        dW_rel = torch.empty_like(W_rel)
+    if dW_self is None:
+        dW_self = torch.empty_like(W_self)
+    if dbias is None and want_dbias:
+        dbias = torch.empty((W_self.shape[0], d), dtype=torch.float32, device=dev)
+    if ws is None:
+        need = int(L.hg_layer_bwd_workspace_size(C.byref(sub.c), C.byref(desc)))
+        ws = _ws(need, dev)
+    _check(L.hg_layer_bwd(C.byref(sub.c), C.byref(desc), _ptr(H_in), _ptr(W_rel), _ptr(W_self),
+                          _ptr(saved), _ptr(dH_out), _ptr(dH_in), _ptr(dW_rel), _ptr(dW_self),
+                          _ptr(dbias), _ptr(ws), ws.numel(), _stream(stream)), "hg_layer_bwd")
+    return dH_in, dW_rel, dW_self, dbias
+
+
+def hg_align_workspace_size(M: int, d: int) -> int:
+    return int(lib().hg_align_workspace_size(M, d))
+
+
+def hg_align_loss_fwd_bwd(H, overlap, H_ref, dH, w=None, lambda_n=2e-4, scale=0.1, eps=1e-5,
+                          ddof=0, dH_ref=None, loss3=None, ws=None, stream=None):
+    """CCA alignment: returns loss3 (device float32 [3] = L_inv, L_dec, L);
+    adds scale * dL/dX into dH[overlap] and overwrites dH_ref if given."""
+    M = int(overlap.shape[0])
+    d = int(H.shape[1])
+    L = lib()
+    code = HG_DTYPE_BF16 if H.dtype == torch.bfloat16 else HG_DTYPE_F32
+    if loss3 is None:
+        loss3 = torch.empty(3, dtype=torch.float32, device=H.device)
+    if ws is None:
+        ws = _ws(int(L.hg_align_workspace_size(M, d)), H.device)
+    _check(L.hg_align_loss_fwd_bwd(M, d, code, int(H.shape[0]), _ptr(H), _ptr(overlap), _ptr(H_ref),
+                                   _ptr(w), lambda_n, scale, eps, ddof, _ptr(loss3), _ptr(dH),
+                                   _ptr(dH_ref), _ptr(ws), ws.numel(), _stream(stream)),
+           "hg_align_loss_fwd_bwd")
+    return loss3
+
+
+def hg_timing_enable(on: bool = True):
+    _check(lib().hg_timing_enable(int(on)), "hg_timing_enable")
+
+
+def hg_timing_collect(cap: int = 256) -> dict:
+    """{kernel name: (launches, total_ms)} since the last collect."""
+    names = (C.c_char * 64 * cap)()
+    launches = (C.c_int64 * cap)()
+    total = (C.c_double * cap)()
+    n = lib().hg_timing_collect(names, launches, total, cap)
+    if n < 0:
+        _check(n, "hg_timing_collect")
+    out = {}
+    for i in range(min(n, cap)):
+        out[bytes(names[i]).split(b"\0", 1)[0].decode()] = (int(launches[i]), float(total[i]))
+    return out

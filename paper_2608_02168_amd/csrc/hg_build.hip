@@ -1,0 +1,686 @@
+// hg_build_csr: risk-aware overlapping-subgraph construction on the GPU.
+//
+// Steps (Methodology, "Risk-Aware Subgraph Construction"; Algorithm 1,
+// construction loop):
+//   1. one pass over the edges: range checks, out-degrees, and for every node
+//      outside V_k the smallest index of an edge joining it to V_k (either
+//      direction) -- a node is a candidate of C_k iff that index exists;
+//   2. node keys: out-degree, or the h-index of the out-neighbour multiset;
+//   3. C'_k = candidates with key <= theta, compacted in gid order;
+//   4. TopM: an exact radix select of the min(M, |C'_k|) smallest 128-bit
+//      composites (key, splitmix64(seed ^ gid), gid) -- unique by gid, so the
+//      selected set is unique;
+//   5. local ids in (node type, gid) order by a stable bucket partition;
+//   6. induced-subgraph edge compaction in original edge order;
+//   7. stable LSD radix sorts by (dst, r) and (src, r) give the CSR and CSC;
+//      row pointers from run-length counts; csc_scale = 1/deg_r(dst);
+//   8. the execution plan: per-relation active-source lists and the chunked
+//      work list of the atomic-free transposed SpMM.
+#include <vector>
+
+#include "hg_internal.h"
+
+namespace hg {
+
+namespace {
+
+constexpr int kBT = 256;  // threads per block for the elementwise passes
+constexpr int kChunk = 1024;  // max CSC entries handled by one backward work item
+
+inline unsigned grid_for(int64_t n, int64_t cap = 16384) {
+  int64_t b = cdiv(n > 0 ? n : 1, kBT);
+  return (unsigned)(b < cap ? b : cap);
+}
+
+#define GRID_STRIDE(i, n)                                                        \
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < (n);     \
+       i += (int64_t)gridDim.x * blockDim.x)
+
+// Device counters written by the build.
+enum : int { C_ERR = 0, C_NSUB, C_ESUB, C_MSEL, C_ITEMS, C_HEAVY, C_PARTS, C_CPRIME, C_COUNT };
+
+struct SelectState {
+  uint32_t k_rem;   // how many more to take from the current prefix bucket
+  uint32_t mode;    // 0 = searching, 1 = done (take composite prefix <= digits), 2 = take none
+  uint32_t npass;   // number of fixed leading digits
+  uint32_t pad;
+  uint32_t digits[16];
+  int32_t hist[256];
+};
+
+__device__ __forceinline__ uint64_t splitmix64_first(uint64_t state) {
+  // SplitMix64 (Steele, Lea, Flood 2014): advance by the golden gamma, then
+  // the variant-13 finaliser.
+  uint64_t z = state + 0x9E3779B97F4A7C15ull;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+// Byte p (0 = most significant) of the 128-bit composite (key, hash, gid).
+__device__ __forceinline__ uint32_t composite_digit(uint32_t key, uint64_t h, uint32_t gid, int p) {
+  uint32_t w;
+  switch (p >> 2) {
+    case 0: w = key; break;
+    case 1: w = (uint32_t)(h >> 32); break;
+    case 2: w = (uint32_t)h; break;
+    default: w = gid; break;
+  }
+  return (w >> (8 * (3 - (p & 3)))) & 0xFFu;
+}
+
+__global__ void k_edges_pass(const int32_t* __restrict__ src, const int32_t* __restrict__ dst,
+                             const uint8_t* __restrict__ rel, const int32_t* __restrict__ part,
+                             int32_t k, int64_t n_nodes, int64_t n_edges, int32_t n_rel,
+                             int32_t* __restrict__ outdeg, int32_t* __restrict__ first,
+                             int32_t* __restrict__ cnt) {
+  GRID_STRIDE(e, n_edges) {
+    const int32_t s = src[e], d = dst[e];
+    const int r = rel[e];
+    if (s < 0 || s >= n_nodes || d < 0 || d >= n_nodes || r >= n_rel) {
+      atomicOr(&cnt[C_ERR], 1);
+      continue;
+    }
+    atomicAdd(&outdeg[s], 1);
+    const bool ps = part[s] == k, pd = part[d] == k;
+    if (pd && !ps) atomicMin(&first[s], (int32_t)e);
+    if (ps && !pd) atomicMin(&first[d], (int32_t)e);
+  }
+}
+
+__global__ void k_check_ntype(const uint8_t* __restrict__ ntype, int64_t n, int32_t n_ntype,
+                              int32_t* __restrict__ cnt) {
+  GRID_STRIDE(v, n) {
+    if (ntype[v] >= n_ntype) atomicOr(&cnt[C_ERR], 2);
+  }
+}
+
+// h-index histogram sizes: D+1 bins for every candidate of out-degree D.
+__global__ void k_hindex_sizes(const int32_t* __restrict__ outdeg, const int32_t* __restrict__ first,
+                               int64_t n, int32_t n_edges, int32_t* __restrict__ sz) {
+  GRID_STRIDE(v, n) { sz[v] = (first[v] < n_edges) ? outdeg[v] + 1 : 0; }
+}
+
+__global__ void k_hindex_hist(const int32_t* __restrict__ src, const int32_t* __restrict__ dst,
+                              int64_t n_edges, const int32_t* __restrict__ outdeg,
+                              const int32_t* __restrict__ first, const int32_t* __restrict__ hoff,
+                              int32_t* __restrict__ hist) {
+  GRID_STRIDE(e, n_edges) {
+    const int32_t s = src[e];
+    if (first[s] < (int32_t)n_edges) {
+      const int32_t ds = outdeg[s];
+      const int32_t c = min(outdeg[dst[e]], ds);
+      atomicAdd(&hist[(int64_t)hoff[s] + c], 1);
+    }
+  }
+}
+
+// key[v] = max h with #{neighbour degrees >= h} >= h, scanning h upwards.
+__global__ void k_hindex_final(const int32_t* __restrict__ outdeg, const int32_t* __restrict__ first,
+                               const int32_t* __restrict__ hoff, const int32_t* __restrict__ hist,
+                               int64_t n, int32_t n_edges, int32_t* __restrict__ key) {
+  GRID_STRIDE(v, n) {
+    if (first[v] >= n_edges) continue;
+    const int32_t D = outdeg[v];
+    const int32_t* hv = hist + hoff[v];
+    int32_t h = 0, ge = D;  // ge = #{values >= h}
+    while (h < D) {
+      const int32_t nxt = ge - hv[h];
+      if (nxt >= h + 1) {
+        ++h;
+        ge = nxt;
+      } else {
+        break;
+      }
+    }
+    key[v] = h;
+  }
+}
+
+__global__ void k_copy_key(const int32_t* __restrict__ outdeg, int64_t n, int32_t* __restrict__ key) {
+  GRID_STRIDE(v, n) { key[v] = outdeg[v]; }
+}
+
+__global__ void k_filter_flags(const int32_t* __restrict__ first, const int32_t* __restrict__ key,
+                               int64_t n, int32_t n_edges, int32_t theta, int32_t* __restrict__ flag) {
+  GRID_STRIDE(v, n) { flag[v] = (first[v] < n_edges && key[v] <= theta) ? 1 : 0; }
+}
+
+__global__ void k_compact_nodes(const int32_t* __restrict__ first, const int32_t* __restrict__ key,
+                                const int32_t* __restrict__ pos, int64_t n, int32_t n_edges,
+                                int32_t theta, int32_t* __restrict__ list) {
+  GRID_STRIDE(v, n) {
+    if (first[v] < n_edges && key[v] <= theta) list[pos[v]] = (int32_t)v;
+  }
+}
+
+__global__ void k_select_init(SelectState* st, const int32_t* __restrict__ cprime, int64_t budget) {
+  const int t = threadIdx.x;
+  st->hist[t] = 0;
+  if (t == 0) {
+    const int64_t c = *cprime;
+    const int64_t take = budget < c ? budget : c;
+    st->k_rem = (uint32_t)take;
+    st->npass = 0;
+    st->mode = (take == 0) ? 2u : ((take == c) ? 1u : 0u);
+  }
+  if (t < 16) st->digits[t] = 0;
+}
+
+__device__ __forceinline__ bool prefix_match(const SelectState* st, uint32_t key, uint64_t h,
+                                             uint32_t gid, int npass) {
+  for (int p = 0; p < npass; ++p)
+    if (composite_digit(key, h, gid, p) != st->digits[p]) return false;
+  return true;
+}
+
+__global__ void k_select_hist(SelectState* st, const int32_t* __restrict__ list,
+                              const int32_t* __restrict__ cprime, const int32_t* __restrict__ key,
+                              uint64_t seed) {
+  __shared__ int lh[256];
+  if (st->mode != 0) return;
+  lh[threadIdx.x] = 0;
+  __syncthreads();
+  const int npass = (int)st->npass;
+  const int64_t c = *cprime;
+  GRID_STRIDE(i, c) {
+    const uint32_t gid = (uint32_t)list[i];
+    const uint32_t kv = (uint32_t)key[gid];
+    const uint64_t h = splitmix64_first(seed ^ (uint64_t)gid);
+    if (prefix_match(st, kv, h, gid, npass)) atomicAdd(&lh[composite_digit(kv, h, gid, npass)], 1);
+  }
+  __syncthreads();
+  if (lh[threadIdx.x]) atomicAdd(&st->hist[threadIdx.x], lh[threadIdx.x]);
+}
+
+// One block of 256 threads: pick the bucket holding the k_rem-th smallest.
+__global__ void k_select_pick(SelectState* st) {
+  __shared__ int cnt[256];
+  __shared__ int pre[256];
+  if (st->mode != 0) return;
+  const int t = threadIdx.x;
+  cnt[t] = st->hist[t];
+  __syncthreads();
+  if (t == 0) {
+    int run = 0;
+    for (int b = 0; b < 256; ++b) {
+      pre[b] = run;
+      run += cnt[b];
+    }
+  }
+  __syncthreads();
+  const uint32_t k = st->k_rem;
+  const uint32_t lo = (uint32_t)pre[t], c = (uint32_t)cnt[t];
+  __syncthreads();
+  if (c > 0 && lo < k && k <= lo + c) {
+    const uint32_t p = st->npass;
+    st->digits[p] = (uint32_t)t;
+    st->npass = p + 1;
+    st->k_rem = k - lo;
+    if (k - lo == c) st->mode = 1;
+  }
+  st->hist[t] = 0;
+}
+
+__global__ void k_select_mark(const SelectState* st, const int32_t* __restrict__ list,
+                              const int32_t* __restrict__ cprime, const int32_t* __restrict__ key,
+                              uint64_t seed, uint8_t* __restrict__ sel) {
+  const uint32_t mode = st->mode;
+  if (mode == 2) return;
+  const int npass = (int)st->npass;
+  const int64_t c = *cprime;
+  GRID_STRIDE(i, c) {
+    const uint32_t gid = (uint32_t)list[i];
+    const uint32_t kv = (uint32_t)key[gid];
+    const uint64_t h = splitmix64_first(seed ^ (uint64_t)gid);
+    bool le = true;
+    for (int p = 0; p < npass; ++p) {
+      const uint32_t dg = composite_digit(kv, h, gid, p);
+      if (dg != st->digits[p]) {
+        le = dg < st->digits[p];
+        break;
+      }
+    }
+    if (le) sel[gid] = 1;
+  }
+}
+
+__global__ void k_member_digit(const int32_t* __restrict__ part, int32_t k,
+                               const uint8_t* __restrict__ sel, const uint8_t* __restrict__ ntype,
+                               int64_t n, uint8_t* __restrict__ digit, int32_t* __restrict__ iota) {
+  GRID_STRIDE(v, n) {
+    digit[v] = (part[v] == k || sel[v]) ? ntype[v] : (uint8_t)255;
+    iota[v] = (int32_t)v;
+  }
+}
+
+__global__ void k_global2local(const int32_t* __restrict__ l2g, const int32_t* __restrict__ type_off,
+                               int32_t n_ntype, int32_t* __restrict__ g2l, int32_t* __restrict__ cnt) {
+  const int64_t ns = type_off[n_ntype];
+  if (blockIdx.x == 0 && threadIdx.x == 0) cnt[C_NSUB] = (int32_t)ns;
+  GRID_STRIDE(i, ns) { g2l[l2g[i]] = (int32_t)i; }
+}
+
+__global__ void k_overlap_flags(const int32_t* __restrict__ l2g, const uint8_t* __restrict__ sel,
+                                const int32_t* __restrict__ cnt, int64_t n, int32_t* __restrict__ flag) {
+  const int64_t ns = cnt[C_NSUB];
+  GRID_STRIDE(i, n) { flag[i] = (i < ns && sel[l2g[i]]) ? 1 : 0; }
+}
+
+__global__ void k_overlap_fill(const int32_t* __restrict__ l2g, const int32_t* __restrict__ flag,
+                               const int32_t* __restrict__ pos, const int32_t* __restrict__ cnt,
+                               const int32_t* __restrict__ part, const int32_t* __restrict__ first,
+                               const uint8_t* __restrict__ rel, int32_t* __restrict__ overlap,
+                               int32_t* __restrict__ home, uint8_t* __restrict__ orel) {
+  const int64_t ns = cnt[C_NSUB];
+  GRID_STRIDE(i, ns) {
+    if (flag[i]) {
+      const int32_t p = pos[i];
+      const int32_t g = l2g[i];
+      overlap[p] = (int32_t)i;
+      home[p] = part[g];
+      orel[p] = rel[first[g]];
+    }
+  }
+}
+
+__global__ void k_edge_keep(const int32_t* __restrict__ src, const int32_t* __restrict__ dst,
+                            const int32_t* __restrict__ g2l, int64_t n_edges, int32_t* __restrict__ keep) {
+  GRID_STRIDE(e, n_edges) { keep[e] = (g2l[src[e]] >= 0 && g2l[dst[e]] >= 0) ? 1 : 0; }
+}
+
+__global__ void k_edge_compact(const int32_t* __restrict__ src, const int32_t* __restrict__ dst,
+                               const uint8_t* __restrict__ rel, const int32_t* __restrict__ g2l,
+                               const int32_t* __restrict__ pos, int64_t n_edges, int32_t n_rel,
+                               uint32_t* __restrict__ kcsr, uint32_t* __restrict__ kcsc,
+                               int32_t* __restrict__ vsrc, int32_t* __restrict__ vdst,
+                               int32_t* __restrict__ veid) {
+  GRID_STRIDE(e, n_edges) {
+    const int32_t s = g2l[src[e]], d = g2l[dst[e]];
+    if (s >= 0 && d >= 0) {
+      const int32_t p = pos[e];
+      const uint32_t r = rel[e];
+      kcsr[p] = (uint32_t)d * (uint32_t)n_rel + r;
+      kcsc[p] = (uint32_t)s * (uint32_t)n_rel + r;
+      vsrc[p] = s;
+      vdst[p] = d;
+      veid[p] = (int32_t)e;
+    }
+  }
+}
+
+// Row lengths of sorted keys: one atomic per run of equal keys inside a wave.
+__global__ void k_row_count(const uint32_t* __restrict__ keys, int64_t n, int32_t* __restrict__ cnt) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int lane = threadIdx.x & (kWave - 1);
+  const bool valid = i < n;
+  const uint32_t k = valid ? keys[i] : 0xFFFFFFFFu;
+  const uint32_t kp = __shfl_up(k, 1, kWave);
+  const bool start = valid && (lane == 0 || k != kp);
+  const uint64_t starts = __ballot(start);
+  const int nvalid = __popcll(__ballot(valid));
+  if (start) {
+    const uint64_t above = (lane == kWave - 1) ? 0ull : (starts & ~((2ull << lane) - 1ull));
+    int next = above ? __ffsll((long long)above) - 1 : kWave;
+    if (next > nvalid) next = nvalid;
+    atomicAdd(&cnt[k], next - lane);
+  }
+}
+
+__global__ void k_csc_scale(const uint32_t* __restrict__ kcsc, const int32_t* __restrict__ csc_row,
+                            const int32_t* __restrict__ csr_ptr, int64_t n, int32_t n_rel,
+                            float* __restrict__ scale) {
+  GRID_STRIDE(p, n) {
+    const int64_t row = (int64_t)csc_row[p] * n_rel + (int64_t)(kcsc[p] % (uint32_t)n_rel);
+    const int32_t deg = csr_ptr[row + 1] - csr_ptr[row];
+    scale[p] = 1.0f / (float)deg;
+  }
+}
+
+__global__ void k_active_digit(const int32_t* __restrict__ csc_ptr, int64_t nq, int32_t n_rel,
+                               uint8_t* __restrict__ digit, int32_t* __restrict__ srcid,
+                               int32_t* __restrict__ n_items, int32_t* __restrict__ n_heavy,
+                               int32_t* __restrict__ n_parts) {
+  GRID_STRIDE(q, nq) {
+    const int32_t len = csc_ptr[q + 1] - csc_ptr[q];
+    digit[q] = len > 0 ? (uint8_t)(q % n_rel) : (uint8_t)255;
+    srcid[q] = (int32_t)(q / n_rel);
+    const int32_t nch = (len + kChunk - 1) / kChunk;
+    n_items[q] = nch;
+    n_heavy[q] = nch > 1 ? 1 : 0;
+    n_parts[q] = nch > 1 ? nch : 0;
+  }
+}
+
+__global__ void k_plan_items(const int32_t* __restrict__ csc_ptr, int64_t nq,
+                             const int32_t* __restrict__ item_off, const int32_t* __restrict__ heavy_off,
+                             const int32_t* __restrict__ part_off, int4* __restrict__ items,
+                             int4* __restrict__ heavy) {
+  GRID_STRIDE(q, nq) {
+    const int32_t beg = csc_ptr[q], end = csc_ptr[q + 1];
+    const int32_t len = end - beg;
+    if (len <= 0) continue;
+    const int32_t nch = (len + kChunk - 1) / kChunk;
+    const int32_t io = item_off[q];
+    if (nch == 1) {
+      items[io] = make_int4((int32_t)q, beg, end, -1);
+    } else {
+      const int32_t so = part_off[q];
+      for (int32_t c = 0; c < nch; ++c) {
+        const int32_t b = beg + c * kChunk;
+        const int32_t e2 = min(end, b + kChunk);
+        items[io + c] = make_int4((int32_t)q, b, e2, so + c);
+      }
+      heavy[heavy_off[q]] = make_int4((int32_t)q, so, nch, 0);
+    }
+  }
+}
+
+int bits_for(int64_t nvals) {
+  int b = 0;
+  while (b < 32 && ((int64_t)1 << b) < nvals) ++b;
+  return b;
+}
+
+// Workspace layout, shared by the sizing and the run.
+template <class A>
+struct BuildWs {
+  int32_t *cnt, *outdeg, *first, *key, *flag, *pos, *list, *iota, *hoff, *hist;
+  uint8_t *sel, *digit;
+  SelectState* st;
+  int32_t *keep, *vsrc, *vdst, *veid, *alt1, *alt2, *alt3, *rowcnt, *q_items, *q_heavy, *q_parts,
+      *q_src, *scratch;
+  uint32_t *kcsr, *kcsc, *kalt;
+  void layout(A& a, int64_t N, int64_t E, int64_t R, bool hindex) {
+    const int64_t NQ = N * R + 1;
+    cnt = a.template take<int32_t>(C_COUNT + 8);
+    outdeg = a.template take<int32_t>(N);
+    first = a.template take<int32_t>(N);
+    key = a.template take<int32_t>(N);
+    flag = a.template take<int32_t>(N + 1);
+    pos = a.template take<int32_t>(N + 1);
+    list = a.template take<int32_t>(N);
+    iota = a.template take<int32_t>(N);
+    hoff = a.template take<int32_t>(hindex ? N + 1 : 0);
+    hist = a.template take<int32_t>(hindex ? E + N : 0);
+    sel = a.template take<uint8_t>(N);
+    digit = a.template take<uint8_t>(NQ > N ? NQ : N);
+    st = a.template take<SelectState>(1);
+    keep = a.template take<int32_t>(E + 1);
+    kcsr = a.template take<uint32_t>(E);
+    kcsc = a.template take<uint32_t>(E);
+    kalt = a.template take<uint32_t>(E);
+    vsrc = a.template take<int32_t>(E);
+    vdst = a.template take<int32_t>(E);
+    veid = a.template take<int32_t>(E);
+    alt1 = a.template take<int32_t>(E);
+    alt2 = a.template take<int32_t>(E);
+    alt3 = a.template take<int32_t>(E);
+    rowcnt = a.template take<int32_t>(NQ);
+    q_items = a.template take<int32_t>(NQ);
+    q_heavy = a.template take<int32_t>(NQ);
+    q_parts = a.template take<int32_t>(NQ);
+    q_src = a.template take<int32_t>(NQ);
+    int64_t sc = scan_scratch_elems(E + N + NQ + 1);
+    int64_t rs = radix_scratch_elems(E > NQ ? E : NQ);
+    scratch = a.template take<int32_t>(sc > rs ? sc : rs);
+  }
+};
+
+struct PlanLayout {
+  size_t s_off, soff_off, items_off, heavy_off, total;
+  int64_t cap_s, cap_items, cap_heavy;
+  PlanLayout(int64_t N, int64_t E, int64_t R) {
+    const int64_t nq = N * R;
+    cap_s = nq < E ? nq : E;
+    cap_heavy = E / kChunk + 1;
+    cap_items = cap_s + cap_heavy;
+    size_t o = 0;
+    s_off = o; o = align_up(o + sizeof(int32_t) * (size_t)(cap_s > 0 ? cap_s : 1));
+    soff_off = o; o = align_up(o + sizeof(int32_t) * (size_t)(R + 1));
+    items_off = o; o = align_up(o + sizeof(int4) * (size_t)cap_items);
+    heavy_off = o; o = align_up(o + sizeof(int4) * (size_t)cap_heavy);
+    total = o;
+  }
+};
+
+}  // namespace
+
+PlanView plan_view(const hg_subgraph* s) {
+  PlanLayout pl(s->n_nodes, s->n_edges, s->n_rel);
+  const char* b = static_cast<const char*>(s->plan);
+  PlanView v;
+  v.active = reinterpret_cast<const int32_t*>(b + pl.s_off);
+  v.items = reinterpret_cast<const int4*>(b + pl.items_off);
+  v.heavy = reinterpret_cast<const int4*>(b + pl.heavy_off);
+  return v;
+}
+
+}  // namespace hg
+
+using namespace hg;
+
+extern "C" size_t hg_plan_size(int64_t n_nodes, int64_t n_edges, int32_t n_rel) {
+  if (n_nodes < 0 || n_edges < 0 || n_rel < 1) return 0;
+  return PlanLayout(n_nodes, n_edges, n_rel).total;
+}
+
+static int validate_build(const hg_graph_desc* g, const hg_overlap_desc* o) {
+  if (!g || !o) return fail(HG_ERR_ARG, "null descriptor");
+  if (g->n_nodes < 1 || g->n_nodes >= ((int64_t)1 << 31))
+    return fail(HG_ERR_ARG, "n_nodes %lld outside [1, 2^31)", (long long)g->n_nodes);
+  if (g->n_edges < 0) return fail(HG_ERR_ARG, "n_edges %lld < 0", (long long)g->n_edges);
+  if (g->n_edges >= ((int64_t)1 << 31))
+    return fail(HG_ERR_UNSUPPORTED, "n_edges %lld >= 2^31", (long long)g->n_edges);
+  if (g->n_rel < 1 || g->n_rel > HG_MAX_REL) return fail(HG_ERR_UNSUPPORTED, "n_rel %d", g->n_rel);
+  if (g->n_ntype < 1 || g->n_ntype > HG_MAX_NTYPE)
+    return fail(HG_ERR_UNSUPPORTED, "n_ntype %d", g->n_ntype);
+  if (g->n_nodes * (int64_t)g->n_rel >= ((int64_t)1 << 31) - 1)
+    return fail(HG_ERR_UNSUPPORTED, "n_nodes * n_rel >= 2^31");
+  if (g->n_edges > 0 && (!g->src || !g->dst || !g->rel))
+    return fail(HG_ERR_ARG, "null edge array");
+  if (!g->ntype || !g->part) return fail(HG_ERR_ARG, "null node array");
+  if (g->edge_w) return fail(HG_ERR_UNSUPPORTED, "edge weights are not implemented");
+  if (o->budget_M < 0) return fail(HG_ERR_ARG, "budget_M < 0");
+  if (o->key != HG_KEY_OUTDEG && o->key != HG_KEY_HINDEX) return fail(HG_ERR_ARG, "key %d", o->key);
+  if (o->key_dir != HG_KEYDIR_OUT) return fail(HG_ERR_UNSUPPORTED, "key_dir %d", o->key_dir);
+  if (o->theta < 0) return fail(HG_ERR_ARG, "theta < 0");
+  return HG_OK;
+}
+
+extern "C" size_t hg_build_csr_workspace_size(const hg_graph_desc* g, const hg_overlap_desc* o) {
+  if (validate_build(g, o) != HG_OK) return 0;
+  Sizer sz;
+  BuildWs<Sizer> w;
+  w.layout(sz, g->n_nodes, g->n_edges, g->n_rel, o->key == HG_KEY_HINDEX);
+  return sz.used + 256;
+}
+
+extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg_subgraph* out,
+                            void* ws, size_t ws_bytes, void* stream) {
+  HG_TRY(validate_build(g, o));
+  if (!out) return fail(HG_ERR_ARG, "null output");
+  if (!out->local2global || !out->global2local || !out->type_off || !out->csr_ptr ||
+      !out->csc_ptr || !out->plan || (!out->overlap && o->budget_M > 0) ||
+      (!out->overlap_home && o->budget_M > 0) || (!out->overlap_rel && o->budget_M > 0) ||
+      (g->n_edges > 0 && (!out->csr_col || !out->csc_row || !out->csc_scale)))
+    return fail(HG_ERR_ARG, "null output array");
+  const int64_t N = g->n_nodes, E = g->n_edges, R = g->n_rel, T = g->n_ntype;
+  const size_t need_plan = hg_plan_size(N, E, (int32_t)R);
+  if (out->plan_bytes < need_plan)
+    return fail(HG_ERR_CAPACITY, "plan needs %zu bytes, got %zu", need_plan, out->plan_bytes);
+  const size_t need = hg_build_csr_workspace_size(g, o);
+  if (!ws || ws_bytes < need) return fail(HG_ERR_CAPACITY, "workspace needs %zu bytes, got %zu", need, ws_bytes);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const bool hindex = o->key == HG_KEY_HINDEX;
+
+  Arena arena(ws, ws_bytes);
+  BuildWs<Arena> w;
+  w.layout(arena, N, E, R, hindex);
+  if (!arena.ok()) return fail(HG_ERR_CAPACITY, "workspace layout overflow");
+
+  const unsigned gN = grid_for(N), gE = grid_for(E);
+  // 1. degrees, base-edge index, range checks
+  HG_TRY(fill_i32(w.cnt, 0, C_COUNT + 8, s));
+  HG_TRY(fill_i32(w.outdeg, 0, N, s));
+  HG_TRY(fill_i32(w.first, (int32_t)E, N, s));
+  HG_TRY(fill_u8(w.sel, 0, N, s));
+  if (E > 0)
+    HG_LAUNCH("build_edges_pass", k_edges_pass, dim3(gE), dim3(kBT), 0, s, g->src, g->dst, g->rel,
+              g->part, g->k, N, E, (int32_t)R, w.outdeg, w.first, w.cnt);
+  HG_LAUNCH("build_check_ntype", k_check_ntype, dim3(gN), dim3(kBT), 0, s, g->ntype, N, (int32_t)T, w.cnt);
+  {
+    int32_t herr = 0;
+    HG_HIP_TRY(hipMemcpyAsync(&herr, w.cnt + C_ERR, sizeof(int32_t), hipMemcpyDeviceToHost, s));
+    HG_HIP_TRY(hipStreamSynchronize(s));
+    if (herr) return fail(HG_ERR_RANGE, "input ids out of range (flags 0x%x)", herr);
+  }
+  // 2. keys
+  if (hindex) {
+    HG_LAUNCH("build_hindex_sizes", k_hindex_sizes, dim3(gN), dim3(kBT), 0, s,
+              (const int32_t*)w.outdeg, (const int32_t*)w.first, N, (int32_t)E, w.flag);
+    HG_TRY(fill_i32(w.flag + N, 0, 1, s));
+    HG_TRY(scan_exclusive_i32(w.flag, w.hoff, N + 1, nullptr, w.scratch, s));
+    HG_TRY(fill_i32(w.hist, 0, E + N, s));
+    if (E > 0)
+      HG_LAUNCH("build_hindex_hist", k_hindex_hist, dim3(gE), dim3(kBT), 0, s, g->src, g->dst, E,
+                (const int32_t*)w.outdeg, (const int32_t*)w.first, (const int32_t*)w.hoff, w.hist);
+    HG_LAUNCH("build_hindex_final", k_hindex_final, dim3(gN), dim3(kBT), 0, s,
+              (const int32_t*)w.outdeg, (const int32_t*)w.first, (const int32_t*)w.hoff,
+              (const int32_t*)w.hist, N, (int32_t)E, w.key);
+  } else {
+    HG_LAUNCH("build_copy_key", k_copy_key, dim3(gN), dim3(kBT), 0, s, (const int32_t*)w.outdeg, N, w.key);
+  }
+  // 3. filtered candidates, compacted in gid order
+  HG_LAUNCH("build_filter_flags", k_filter_flags, dim3(gN), dim3(kBT), 0, s, (const int32_t*)w.first,
+            (const int32_t*)w.key, N, (int32_t)E, o->theta, w.flag);
+  HG_TRY(scan_exclusive_i32(w.flag, w.pos, N, w.cnt + C_CPRIME, w.scratch, s));
+  HG_LAUNCH("build_compact_nodes", k_compact_nodes, dim3(gN), dim3(kBT), 0, s, (const int32_t*)w.first,
+            (const int32_t*)w.key, (const int32_t*)w.pos, N, (int32_t)E, o->theta, w.list);
+  // 4. TopM by exact radix select over the 128-bit composite
+  {
+    const int64_t budget = o->budget_M;
+    HG_LAUNCH("build_select_init", k_select_init, dim3(1), dim3(256), 0, s, w.st,
+              (const int32_t*)(w.cnt + C_CPRIME), budget);
+    for (int p = 0; p < 16; ++p) {
+      HG_LAUNCH("build_select_hist", k_select_hist, dim3(grid_for(N, 2048)), dim3(256), 0, s, w.st,
+                (const int32_t*)w.list, (const int32_t*)(w.cnt + C_CPRIME), (const int32_t*)w.key,
+                o->seed);
+      HG_LAUNCH("build_select_pick", k_select_pick, dim3(1), dim3(256), 0, s, w.st);
+    }
+    HG_LAUNCH("build_select_mark", k_select_mark, dim3(grid_for(N, 2048)), dim3(256), 0, s,
+              (const SelectState*)w.st, (const int32_t*)w.list, (const int32_t*)(w.cnt + C_CPRIME),
+              (const int32_t*)w.key, o->seed, w.sel);
+  }
+  // 5. local ids in (ntype, gid) order
+  HG_LAUNCH("build_member_digit", k_member_digit, dim3(gN), dim3(kBT), 0, s, g->part, g->k,
+            (const uint8_t*)w.sel, g->ntype, N, w.digit, w.iota);
+  HG_TRY(bucket_partition(w.digit, w.iota, N, (int)T, out->local2global, out->type_off, w.scratch, s));
+  HG_TRY(fill_i32(out->global2local, -1, N, s));
+  HG_LAUNCH("build_global2local", k_global2local, dim3(gN), dim3(kBT), 0, s,
+            (const int32_t*)out->local2global, (const int32_t*)out->type_off, (int32_t)T,
+            out->global2local, w.cnt);
+  // overlap list (local ids ascending)
+  HG_LAUNCH("build_overlap_flags", k_overlap_flags, dim3(gN), dim3(kBT), 0, s,
+            (const int32_t*)out->local2global, (const uint8_t*)w.sel, (const int32_t*)w.cnt, N, w.flag);
+  HG_TRY(scan_exclusive_i32(w.flag, w.pos, N, w.cnt + C_MSEL, w.scratch, s));
+  if (o->budget_M > 0)
+    HG_LAUNCH("build_overlap_fill", k_overlap_fill, dim3(gN), dim3(kBT), 0, s,
+              (const int32_t*)out->local2global, (const int32_t*)w.flag, (const int32_t*)w.pos,
+              (const int32_t*)w.cnt, g->part, (const int32_t*)w.first, g->rel, out->overlap,
+              out->overlap_home, out->overlap_rel);
+  // 6. induced-subgraph edges in original order
+  if (E > 0) {
+    HG_LAUNCH("build_edge_keep", k_edge_keep, dim3(gE), dim3(kBT), 0, s, g->src, g->dst,
+              (const int32_t*)out->global2local, E, w.keep);
+    HG_TRY(scan_exclusive_i32(w.keep, w.keep, E, w.cnt + C_ESUB, w.scratch, s));
+    HG_LAUNCH("build_edge_compact", k_edge_compact, dim3(gE), dim3(kBT), 0, s, g->src, g->dst, g->rel,
+              (const int32_t*)out->global2local, (const int32_t*)w.keep, E, (int32_t)R, w.kcsr,
+              w.kcsc, w.vsrc, w.vdst, w.veid);
+  } else {
+    HG_TRY(fill_i32(w.cnt + C_ESUB, 0, 1, s));
+  }
+  // counts needed to size the sorts
+  int32_t hc[C_COUNT];
+  HG_HIP_TRY(hipMemcpyAsync(hc, w.cnt, sizeof(hc), hipMemcpyDeviceToHost, s));
+  HG_HIP_TRY(hipStreamSynchronize(s));
+  const int64_t NS = hc[C_NSUB], ES = hc[C_ESUB];
+  const int64_t NQ = NS * R;
+  // 7. CSR: stable sort by dst*R + r; CSC: stable sort by src*R + r
+  const int bits = bits_for(NQ);
+  {
+    uint32_t* ko;
+    int32_t *v1o, *v2o;
+    const bool want_eid = out->csr_eid != nullptr;
+    HG_TRY(radix_sort_pairs(w.kcsr, w.kalt, w.vsrc, w.alt1, want_eid ? w.veid : nullptr,
+                            want_eid ? w.alt2 : nullptr, ES, bits, w.scratch, s, &ko, &v1o, &v2o));
+    if (ES > 0) {
+      HG_HIP_TRY(hipMemcpyAsync(out->csr_col, v1o, sizeof(int32_t) * ES, hipMemcpyDeviceToDevice, s));
+      if (want_eid)
+        HG_HIP_TRY(hipMemcpyAsync(out->csr_eid, v2o, sizeof(int32_t) * ES, hipMemcpyDeviceToDevice, s));
+    }
+    HG_TRY(fill_i32(w.rowcnt, 0, NQ + 1, s));
+    if (ES > 0)
+      HG_LAUNCH("build_row_count", k_row_count, dim3((unsigned)cdiv(ES, kBT)), dim3(kBT), 0, s,
+                (const uint32_t*)ko, ES, w.rowcnt);
+    HG_TRY(scan_exclusive_i32(w.rowcnt, out->csr_ptr, NQ + 1, nullptr, w.scratch, s));
+  }
+  {
+    uint32_t* ko;
+    int32_t *v1o, *v2o;
+    HG_TRY(radix_sort_pairs(w.kcsc, w.kalt, w.vdst, w.alt3, nullptr, nullptr, ES, bits, w.scratch, s,
+                            &ko, &v1o, &v2o));
+    if (ES > 0)
+      HG_HIP_TRY(hipMemcpyAsync(out->csc_row, v1o, sizeof(int32_t) * ES, hipMemcpyDeviceToDevice, s));
+    HG_TRY(fill_i32(w.rowcnt, 0, NQ + 1, s));
+    if (ES > 0)
+      HG_LAUNCH("build_row_count", k_row_count, dim3((unsigned)cdiv(ES, kBT)), dim3(kBT), 0, s,
+                (const uint32_t*)ko, ES, w.rowcnt);
+    HG_TRY(scan_exclusive_i32(w.rowcnt, out->csc_ptr, NQ + 1, nullptr, w.scratch, s));
+    if (ES > 0)
+      HG_LAUNCH("build_csc_scale", k_csc_scale, dim3(grid_for(ES)), dim3(kBT), 0, s,
+                (const uint32_t*)ko, (const int32_t*)out->csc_row, (const int32_t*)out->csr_ptr, ES,
+                (int32_t)R, out->csc_scale);
+  }
+  // 8. plan: active-source lists and backward work items
+  PlanLayout pl(N, E, R);
+  char* pb = static_cast<char*>(out->plan);
+  int32_t* act = reinterpret_cast<int32_t*>(pb + pl.s_off);
+  int32_t* act_off = reinterpret_cast<int32_t*>(pb + pl.soff_off);
+  int4* items = reinterpret_cast<int4*>(pb + pl.items_off);
+  int4* heavy = reinterpret_cast<int4*>(pb + pl.heavy_off);
+  if (NQ > 0) {
+    HG_LAUNCH("build_active_digit", k_active_digit, dim3(grid_for(NQ)), dim3(kBT), 0, s,
+              (const int32_t*)out->csc_ptr, NQ, (int32_t)R, w.digit, w.q_src, w.q_items, w.q_heavy,
+              w.q_parts);
+    HG_TRY(bucket_partition(w.digit, w.q_src, NQ, (int)R, act, act_off, w.scratch, s));
+    HG_TRY(scan_exclusive_i32(w.q_items, w.q_items, NQ, w.cnt + C_ITEMS, w.scratch, s));
+    HG_TRY(scan_exclusive_i32(w.q_heavy, w.q_heavy, NQ, w.cnt + C_HEAVY, w.scratch, s));
+    HG_TRY(scan_exclusive_i32(w.q_parts, w.q_parts, NQ, w.cnt + C_PARTS, w.scratch, s));
+    HG_LAUNCH("build_plan_items", k_plan_items, dim3(grid_for(NQ)), dim3(kBT), 0, s,
+              (const int32_t*)out->csc_ptr, NQ, (const int32_t*)w.q_items, (const int32_t*)w.q_heavy,
+              (const int32_t*)w.q_parts, items, heavy);
+  } else {
+    HG_TRY(fill_i32(act_off, 0, R + 1, s));
+    HG_TRY(fill_i32(w.cnt + C_ITEMS, 0, 3, s));
+  }
+  // final sync: host counts
+  std::vector<int32_t> tof(T + 1), aof(R + 1);
+  HG_HIP_TRY(hipMemcpyAsync(hc, w.cnt, sizeof(hc), hipMemcpyDeviceToHost, s));
+  HG_HIP_TRY(hipMemcpyAsync(tof.data(), out->type_off, sizeof(int32_t) * (T + 1), hipMemcpyDeviceToHost, s));
+  HG_HIP_TRY(hipMemcpyAsync(aof.data(), act_off, sizeof(int32_t) * (R + 1), hipMemcpyDeviceToHost, s));
+  HG_HIP_TRY(hipStreamSynchronize(s));
+  out->n_nodes = N;
+  out->n_edges = E;
+  out->n_sub = NS;
+  out->e_sub = ES;
+  out->m_sel = hc[C_MSEL];
+  out->n_rel = (int32_t)R;
+  out->n_ntype = (int32_t)T;
+  for (int t = 0; t <= HG_MAX_NTYPE; ++t) out->type_off_host[t] = t <= T ? tof[t] : 0;
+  for (int r = 0; r < HG_MAX_REL; ++r) out->n_active[r] = r < R ? (int64_t)aof[r + 1] - aof[r] : 0;
+  out->plan_items = hc[C_ITEMS];
+  out->plan_heavy = hc[C_HEAVY];
+  out->plan_partials = hc[C_PARTS];
+  return HG_OK;
+}

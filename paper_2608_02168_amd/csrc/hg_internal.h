@@ -1,0 +1,118 @@
+// Internal declarations shared by the libhg.so translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <cstdio>
+#include <string>
+
+#include "../../include/hg.h"
+
+namespace hg {
+
+constexpr int kWave = 64;
+
+// ---- host-side error reporting -----------------------------------------
+void set_detail(const char* fmt, ...);
+int fail(int code, const char* fmt, ...);
+
+#define HG_HIP_TRY(expr)                                                     \
+  do {                                                                       \
+    hipError_t e_ = (expr);                                                  \
+    if (e_ != hipSuccess)                                                    \
+      return ::hg::fail(HG_ERR_HIP, "%s failed: %s (%s:%d)", #expr,          \
+                        hipGetErrorString(e_), __FILE__, __LINE__);          \
+  } while (0)
+
+#define HG_TRY(expr)              \
+  do {                            \
+    int s_ = (expr);              \
+    if (s_ != HG_OK) return s_;   \
+  } while (0)
+
+// ---- kernel timing log ----------------------------------------------------
+bool timing_on();
+void timing_begin(const char* name, hipStream_t s, void** tok);
+void timing_end(void* tok, hipStream_t s);
+
+// Launch a kernel, optionally bracketed by timing events; returns HG status.
+#define HG_LAUNCH(name, kernel, grid, block, shmem, stream, ...)             \
+  do {                                                                       \
+    void* tok_ = nullptr;                                                    \
+    if (::hg::timing_on()) ::hg::timing_begin(name, stream, &tok_);          \
+    hipLaunchKernelGGL(kernel, grid, block, shmem, stream, __VA_ARGS__);     \
+    if (tok_) ::hg::timing_end(tok_, stream);                                \
+    hipError_t le_ = hipGetLastError();                                      \
+    if (le_ != hipSuccess)                                                   \
+      return ::hg::fail(HG_ERR_HIP, "launch of %s failed: %s", name,        \
+                        hipGetErrorString(le_));                             \
+  } while (0)
+
+inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+inline size_t align_up(size_t x, size_t a = 256) { return (x + a - 1) / a * a; }
+
+// Bump allocator over a caller-provided workspace.
+struct Arena {
+  char* base;
+  size_t cap;
+  size_t used = 0;
+  Arena(void* p, size_t c) : base(static_cast<char*>(p)), cap(c) {}
+  template <class T>
+  T* take(int64_t n) {
+    size_t off = align_up(used);
+    used = off + align_up(sizeof(T) * (size_t)(n > 0 ? n : 0));
+    return (used <= cap && base) ? reinterpret_cast<T*>(base + off) : nullptr;
+  }
+  bool ok() const { return used <= cap; }
+};
+
+// Sizing pass: same sequence of takes without memory.
+struct Sizer {
+  size_t used = 0;
+  template <class T>
+  T* take(int64_t n) {
+    used = align_up(used) + align_up(sizeof(T) * (size_t)(n > 0 ? n : 0));
+    return nullptr;
+  }
+};
+
+int num_cus();
+
+// Execution plan written by hg_build_csr (laid out for the input capacities).
+struct PlanView {
+  const int32_t* active;  // concatenated S_r lists: sources with >= 1 out-edge of relation r, ascending
+  const int4* items;      // backward work items (csc row q, begin, end, partial slot or -1)
+  const int4* heavy;      // split rows (q, first partial slot, number of slots, 0)
+};
+PlanView plan_view(const hg_subgraph* s);
+
+// ---- primitives (hg_scan.hip) -------------------------------------------
+// Exclusive prefix sum of n int32 values into out (out may equal in).
+// Writes the total into *total_dev (device int32) if non-null.  Scratch:
+// scan_scratch_elems(n) int32.
+int64_t scan_scratch_elems(int64_t n);
+int scan_exclusive_i32(const int32_t* in, int32_t* out, int64_t n, int32_t* total_dev,
+                       int32_t* scratch, hipStream_t s);
+
+// Stable LSD radix sort of (key, value[, value2]) by the low `bits` bits of
+// key (uint32).  Ping-pong buffers must hold n elements; the result ends in
+// the *_out buffers (the call copies as needed).  Scratch: radix_scratch_elems(n).
+int64_t radix_scratch_elems(int64_t n);
+int radix_sort_pairs(uint32_t* keys, uint32_t* keys_alt, int32_t* v1, int32_t* v1_alt,
+                     int32_t* v2, int32_t* v2_alt, int64_t n, int bits,
+                     int32_t* scratch, hipStream_t s, uint32_t** keys_out,
+                     int32_t** v1_out, int32_t** v2_out);
+
+// Stable partition of n items into `nbins` (<= 256) buckets by a digit array
+// (uint8, 255 = drop).  Writes out[off[bin] + rank] = val[i] and bin_off[0..nbins]
+// (device int32).  Scratch: radix_scratch_elems(n).
+int bucket_partition(const uint8_t* digit, const int32_t* val, int64_t n, int nbins,
+                     int32_t* out, int32_t* bin_off, int32_t* scratch, hipStream_t s);
+
+// Fill helpers (used instead of hipMemsetAsync so the kernels can be captured).
+int fill_i32(int32_t* p, int32_t v, int64_t n, hipStream_t s);
+int fill_u8(uint8_t* p, uint8_t v, int64_t n, hipStream_t s);
+int fill_f32(float* p, float v, int64_t n, hipStream_t s);
+
+}  // namespace hg

@@ -1,0 +1,425 @@
+// hg_layer_fwd / hg_layer_bwd: one relation-typed mean-aggregation layer.
+//
+// Forward (message, aggregation and update equations of the "Heterogeneous
+// Graph Transformer" paragraph in relation-typed mean form):
+//   (c) MFMA transforms  Y_self = H W_self[t] + b[t]   per contiguous type range
+//                        Y[i*R + r] = H_i W_r           for i in S_r (active sources)
+//   (b) SpMM             z_j = Y_self[j] + sum_{edges i->j of relation r} Y[i*R+r] / deg_r(j)
+//                        h'_j = ReLU(z_j) + h_j, ReLU mask saved as bits
+// Backward:
+//   dZ = G * mask
+//   (b) transposed SpMM  dY[i*R + r] = sum_{edges i->j of r} csc_scale * dZ_j  (no atomics;
+//                        rows longer than the chunk size are split, then summed in order)
+//   (c) MFMA             dH = G + dZ W_self^T, then dH[S_r] += dY_r W_r^T for r = 0..R-1
+//                        dW_self[t] = H_t^T dZ_t, db[t] = colsum dZ_t, dW_r = H[S_r]^T dY_r
+//                        (split-K with a fixed-order reduction)
+#include "hg_internal.h"
+#include "hg_mfma.h"
+
+namespace hg {
+
+namespace {
+
+// ---- forward SpMM + epilogue --------------------------------------------------
+// One wave per destination row.  Lanes form EPW slots of LPR lanes; a slot
+// gathers one source row (D floats as LPR float4s), so a wave step covers EPW
+// edges; neighbour ids and weights of up to 64 entries sit one per lane and are
+// broadcast with ds_bpermute.
+template <int D>
+__global__ void __launch_bounds__(256) k_spmm_fwd(int64_t n_sub, int32_t R, const int32_t* __restrict__ csr_ptr,
+                                                  const int32_t* __restrict__ csr_col,
+                                                  const float* __restrict__ Y, const float* __restrict__ Yself,
+                                                  const float* __restrict__ Hin, float* __restrict__ Hout,
+                                                  uint32_t* __restrict__ mask, int relu, int residual) {
+  constexpr int LPR = D / 4;
+  constexpr int EPW = 64 / LPR;
+  constexpr int U = 4;
+  const int l = threadIdx.x & 63;
+  const int slot = l / LPR;
+  const int c4 = l % LPR;
+  const int64_t wave0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+  const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
+  for (int64_t j = wave0; j < n_sub; j += nwaves) {
+    const int64_t rb = j * R;
+    const int32_t p0 = csr_ptr[rb];
+    const int32_t pe = csr_ptr[rb + R];
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int32_t base = p0; base < pe; base += 64) {
+      const int32_t pos = base + l;
+      const bool valid = pos < pe;
+      int32_t rowi = 0;
+      float wgt = 0.f;
+      if (valid) {
+        const int32_t src = csr_col[pos];
+        int32_t r = 0, lo = p0, hi = pe;
+        for (int t = 1; t < R; ++t) {
+          const int32_t pt = csr_ptr[rb + t];
+          if (pt <= pos) {
+            r = t;
+            lo = pt;
+          } else if (pt < hi) {
+            hi = pt;
+          }
+        }
+        rowi = src * R + r;
+        wgt = 1.0f / (float)(hi - lo);
+      }
+      const int cnt = (pe - base) < 64 ? (pe - base) : 64;
+      for (int e = 0; e < cnt; e += EPW * U) {
+        f32x4 v[U];
+        float ww[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const int my = e + u * EPW + slot;
+          const int32_t q = __shfl(rowi, my & 63, 64);
+          const float wq = __shfl(wgt, my & 63, 64);
+          ww[u] = (my < cnt) ? wq : 0.f;
+          if (my < cnt) {
+            v[u] = *reinterpret_cast<const f32x4*>(Y + (int64_t)q * D + 4 * c4);
+          } else {
+            v[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) acc += ww[u] * v[u];
+      }
+    }
+#pragma unroll
+    for (int o = LPR; o < 64; o <<= 1) {
+      acc[0] += __shfl_xor(acc[0], o, 64);
+      acc[1] += __shfl_xor(acc[1], o, 64);
+      acc[2] += __shfl_xor(acc[2], o, 64);
+      acc[3] += __shfl_xor(acc[3], o, 64);
+    }
+    const int64_t off = j * D + 4 * c4;
+    f32x4 z = acc;
+    uint32_t word = 0;
+    if (slot == 0) {
+      z += *reinterpret_cast<const f32x4*>(Yself + off);
+      f32x4 h = z;
+      if (relu) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) h[q] = z[q] > 0.f ? z[q] : 0.f;
+      }
+      if (residual) h += *reinterpret_cast<const f32x4*>(Hin + off);
+      *reinterpret_cast<f32x4*>(Hout + off) = h;
+      uint32_t nib = 0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) nib |= ((!relu || z[q] > 0.f) ? 1u : 0u) << q;
+      word = nib << (4 * (c4 & 7));
+    }
+    word |= __shfl_xor(word, 1, 64);
+    word |= __shfl_xor(word, 2, 64);
+    word |= __shfl_xor(word, 4, 64);
+    if (slot == 0 && (c4 & 7) == 0) mask[j * (D / 32) + (c4 >> 3)] = word;
+  }
+}
+
+// dZ = G * mask
+template <int D>
+__global__ void k_relu_grad(int64_t n_sub, const float* __restrict__ G, const uint32_t* __restrict__ mask,
+                            float* __restrict__ dZ) {
+  constexpr int C4 = D / 4;
+  const int64_t total = n_sub * C4;
+  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < total;
+       t += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t j = t / C4;
+    const int c4 = (int)(t % C4);
+    const uint32_t nib = (mask[j * (D / 32) + (c4 >> 3)] >> (4 * (c4 & 7))) & 0xFu;
+    f32x4 g = *reinterpret_cast<const f32x4*>(G + j * D + 4 * c4);
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      if (!((nib >> q) & 1u)) g[q] = 0.f;
+    *reinterpret_cast<f32x4*>(dZ + j * D + 4 * c4) = g;
+  }
+}
+
+// ---- backward transposed SpMM over the CSC work items ---------------------------
+template <int D>
+__global__ void __launch_bounds__(256) k_spmm_bwd(int64_t n_items, const int4* __restrict__ items,
+                                                  const int32_t* __restrict__ csc_row,
+                                                  const float* __restrict__ csc_scale,
+                                                  const float* __restrict__ dZ, float* __restrict__ dY,
+                                                  float* __restrict__ partial) {
+  constexpr int LPR = D / 4;
+  constexpr int EPW = 64 / LPR;
+  constexpr int U = 4;
+  const int l = threadIdx.x & 63;
+  const int slot = l / LPR;
+  const int c4 = l % LPR;
+  const int64_t wave0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+  const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
+  for (int64_t it = wave0; it < n_items; it += nwaves) {
+    const int4 item = items[it];
+    const int32_t beg = item.y, end = item.z;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int32_t base = beg; base < end; base += 64) {
+      const int32_t pos = base + l;
+      int32_t dst = 0;
+      float sc = 0.f;
+      if (pos < end) {
+        dst = csc_row[pos];
+        sc = csc_scale[pos];
+      }
+      const int cnt = (end - base) < 64 ? (end - base) : 64;
+      for (int e = 0; e < cnt; e += EPW * U) {
+        f32x4 v[U];
+        float ww[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const int my = e + u * EPW + slot;
+          const int32_t q = __shfl(dst, my & 63, 64);
+          const float wq = __shfl(sc, my & 63, 64);
+          ww[u] = (my < cnt) ? wq : 0.f;
+          if (my < cnt) {
+            v[u] = *reinterpret_cast<const f32x4*>(dZ + (int64_t)q * D + 4 * c4);
+          } else {
+            v[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) acc += ww[u] * v[u];
+      }
+    }
+#pragma unroll
+    for (int o = LPR; o < 64; o <<= 1) {
+      acc[0] += __shfl_xor(acc[0], o, 64);
+      acc[1] += __shfl_xor(acc[1], o, 64);
+      acc[2] += __shfl_xor(acc[2], o, 64);
+      acc[3] += __shfl_xor(acc[3], o, 64);
+    }
+    if (slot == 0) {
+      float* out = (item.w < 0) ? dY + (int64_t)item.x * D : partial + (int64_t)item.w * D;
+      *reinterpret_cast<f32x4*>(out + 4 * c4) = acc;
+    }
+  }
+}
+
+// Split rows: dY[q] = sum of its partial rows, in chunk order.
+template <int D>
+__global__ void k_heavy_reduce(int64_t n_heavy, const int4* __restrict__ heavy,
+                               const float* __restrict__ partial, float* __restrict__ dY) {
+  constexpr int LPR = D / 4;
+  const int l = threadIdx.x & 63;
+  const int64_t wave0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+  const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
+  for (int64_t h = wave0; h < n_heavy; h += nwaves) {
+    const int4 hv = heavy[h];
+    if (l < LPR) {
+      f32x4 s = {0.f, 0.f, 0.f, 0.f};
+      for (int32_t k = 0; k < hv.z; ++k)
+        s += *reinterpret_cast<const f32x4*>(partial + (int64_t)(hv.y + k) * D + 4 * l);
+      *reinterpret_cast<f32x4*>(dY + (int64_t)hv.x * D + 4 * l) = s;
+    }
+  }
+}
+
+inline unsigned wave_grid(int64_t n_waves) {
+  int64_t blocks = cdiv(n_waves, 4);
+  const int64_t cap = (int64_t)num_cus() * 64;
+  if (blocks > cap) blocks = cap;
+  return (unsigned)(blocks > 0 ? blocks : 1);
+}
+
+int validate_layer(const hg_subgraph* s, const hg_layer_desc* L) {
+  if (!s || !L) return fail(HG_ERR_ARG, "null subgraph or layer descriptor");
+  if (L->d_in != L->d_out) return fail(HG_ERR_UNSUPPORTED, "d_in %d != d_out %d", L->d_in, L->d_out);
+  if (L->dtype != HG_DTYPE_F32 && L->dtype != HG_DTYPE_BF16)
+    return fail(HG_ERR_ARG, "dtype %d", L->dtype);
+  if (L->dtype == HG_DTYPE_F32 && L->d_in != 64 && L->d_in != 128)
+    return fail(HG_ERR_UNSUPPORTED, "float32 layers support d in {64, 128}, got %d", L->d_in);
+  if (L->dtype == HG_DTYPE_BF16)
+    return fail(HG_ERR_UNSUPPORTED, "bfloat16 layers are not implemented");
+  if ((L->relu != 0 && L->relu != 1) || (L->residual != 0 && L->residual != 1))
+    return fail(HG_ERR_ARG, "relu/residual must be 0 or 1");
+  if (s->n_sub < 0 || s->n_rel < 1 || s->n_ntype < 1 || !s->csr_ptr || !s->csc_ptr || !s->plan)
+    return fail(HG_ERR_ARG, "subgraph not built");
+  return HG_OK;
+}
+
+template <int D>
+struct FwdWs {
+  float *Y, *Yself;
+  template <class A>
+  void layout(A& a, const hg_subgraph* s) {
+    Y = a.template take<float>(s->n_sub * s->n_rel * (int64_t)D);
+    Yself = a.template take<float>(s->n_sub * (int64_t)D);
+  }
+};
+
+template <int D>
+struct BwdWs {
+  float *dZ, *dY, *part, *splitk, *colsum;
+  template <class A>
+  void layout(A& a, const hg_subgraph* s) {
+    dZ = a.template take<float>(s->n_sub * (int64_t)D);
+    dY = a.template take<float>(s->n_sub * s->n_rel * (int64_t)D);
+    part = a.template take<float>(s->plan_partials * (int64_t)D);
+    splitk = a.template take<float>(splitk_max_chunks() * (int64_t)D * D);
+    colsum = a.template take<float>(splitk_max_chunks() * (int64_t)D);
+  }
+};
+
+template <int D>
+int layer_fwd_impl(const hg_subgraph* s, const hg_layer_desc* L, const float* Hin, const float* W_rel,
+                   const float* W_self, const float* bias, float* Hout, uint32_t* mask, void* ws,
+                   size_t ws_bytes, hipStream_t st) {
+  Arena a(ws, ws_bytes);
+  FwdWs<D> w;
+  w.layout(a, s);
+  if (!a.ok()) return fail(HG_ERR_CAPACITY, "forward workspace needs %zu bytes, got %zu", a.used, ws_bytes);
+  const int32_t R = s->n_rel;
+  const PlanView pv = plan_view(s);
+  // (c) self transform per node type, bias folded in
+  for (int t = 0; t < s->n_ntype; ++t) {
+    const int64_t lo = s->type_off_host[t], hi = s->type_off_host[t + 1];
+    LoadRows<D> la{Hin, rows_contig(lo)};
+    StoreRows<D> ep{w.Yself, rows_contig(lo), bias ? bias + (int64_t)t * D : nullptr, nullptr};
+    HG_TRY((launch_gemm_rows<D, false>("gemm_fwd_self", hi - lo, W_self + (int64_t)t * D * D, la, ep, st)));
+  }
+  // (c) relation transforms over the active sources
+  int64_t off = 0;
+  for (int r = 0; r < R; ++r) {
+    const int64_t n = s->n_active[r];
+    LoadRows<D> la{Hin, rows_list(pv.active + off)};
+    StoreRows<D> ep{w.Y, rows_list(pv.active + off, R, r), nullptr, nullptr};
+    HG_TRY((launch_gemm_rows<D, false>("gemm_fwd_rel", n, W_rel + (int64_t)r * D * D, la, ep, st)));
+    off += n;
+  }
+  // (b) aggregation + epilogue
+  if (s->n_sub > 0)
+    HG_LAUNCH("spmm_fwd", k_spmm_fwd<D>, dim3(wave_grid(s->n_sub)), dim3(256), 0, st, s->n_sub, R,
+              (const int32_t*)s->csr_ptr, (const int32_t*)s->csr_col, (const float*)w.Y,
+              (const float*)w.Yself, Hin, Hout, mask, L->relu, L->residual);
+  return HG_OK;
+}
+
+template <int D>
+int layer_bwd_impl(const hg_subgraph* s, const hg_layer_desc* L, const float* Hin, const float* W_rel,
+                   const float* W_self, const uint32_t* mask, const float* G, float* dHin, float* dW_rel,
+                   float* dW_self, float* dbias, void* ws, size_t ws_bytes, hipStream_t st) {
+  Arena a(ws, ws_bytes);
+  BwdWs<D> w;
+  w.layout(a, s);
+  if (!a.ok()) return fail(HG_ERR_CAPACITY, "backward workspace needs %zu bytes, got %zu", a.used, ws_bytes);
+  const int32_t R = s->n_rel;
+  const PlanView pv = plan_view(s);
+  const int64_t ns = s->n_sub;
+  if (ns > 0) {
+    const int64_t n4 = ns * (D / 4);
+    HG_LAUNCH("relu_grad", k_relu_grad<D>, dim3((unsigned)(cdiv(n4, 256) < 65536 ? cdiv(n4, 256) : 65536)),
+              dim3(256), 0, st, ns, G, mask, w.dZ);
+  }
+  // (b) transposed SpMM
+  if (s->plan_items > 0)
+    HG_LAUNCH("spmm_bwd", k_spmm_bwd<D>, dim3(wave_grid(s->plan_items)), dim3(256), 0, st,
+              (int64_t)s->plan_items, pv.items, (const int32_t*)s->csc_row, (const float*)s->csc_scale,
+              (const float*)w.dZ, w.dY, w.part);
+  if (s->plan_heavy > 0)
+    HG_LAUNCH("spmm_bwd_reduce", k_heavy_reduce<D>, dim3(wave_grid(s->plan_heavy)), dim3(256), 0, st,
+              (int64_t)s->plan_heavy, pv.heavy, (const float*)w.part, w.dY);
+  // (c) dH = G (residual) + dZ W_self^T per type, then += dY_r W_r^T per relation in order
+  for (int t = 0; t < s->n_ntype; ++t) {
+    const int64_t lo = s->type_off_host[t], hi = s->type_off_host[t + 1];
+    LoadRows<D> la{w.dZ, rows_contig(lo)};
+    StoreRows<D> ep{dHin, rows_contig(lo), nullptr, L->residual ? G : nullptr};
+    HG_TRY((launch_gemm_rows<D, true>("gemm_bwd_dx_self", hi - lo, W_self + (int64_t)t * D * D, la, ep, st)));
+    if (!L->residual && hi > lo) {
+      // nothing else to add
+    }
+  }
+  int64_t off = 0;
+  for (int r = 0; r < R; ++r) {
+    const int64_t n = s->n_active[r];
+    LoadRows<D> la{w.dY, rows_list(pv.active + off, R, r)};
+    StoreRows<D> ep{dHin, rows_list(pv.active + off), nullptr, dHin};
+    HG_TRY((launch_gemm_rows<D, true>("gemm_bwd_dx_rel", n, W_rel + (int64_t)r * D * D, la, ep, st)));
+    off += n;
+  }
+  // (c) weight gradients, split-K
+  for (int t = 0; t < s->n_ntype; ++t) {
+    const int64_t lo = s->type_off_host[t], hi = s->type_off_host[t + 1];
+    LoadRows<D> la{Hin, rows_contig(lo)};
+    LoadRows<D> lb{w.dZ, rows_contig(lo)};
+    HG_TRY((launch_gemm_tn<D>("gemm_bwd_dw_self", hi - lo, la, lb, w.splitk, w.colsum,
+                              dW_self + (int64_t)t * D * D, dbias ? dbias + (int64_t)t * D : nullptr, 0, st)));
+  }
+  off = 0;
+  for (int r = 0; r < R; ++r) {
+    const int64_t n = s->n_active[r];
+    LoadRows<D> la{Hin, rows_list(pv.active + off)};
+    LoadRows<D> lb{w.dY, rows_list(pv.active + off, R, r)};
+    HG_TRY((launch_gemm_tn<D>("gemm_bwd_dw_rel", n, la, lb, w.splitk, w.colsum, dW_rel + (int64_t)r * D * D,
+                              nullptr, 0, st)));
+    off += n;
+  }
+  return HG_OK;
+}
+
+}  // namespace
+
+}  // namespace hg
+
+using namespace hg;
+
+extern "C" size_t hg_layer_saved_size(const hg_subgraph* s, const hg_layer_desc* L) {
+  if (!s || !L || L->d_out <= 0) return 0;
+  return sizeof(uint32_t) * (size_t)s->n_sub * (size_t)((L->d_out + 31) / 32);
+}
+
+extern "C" size_t hg_layer_fwd_workspace_size(const hg_subgraph* s, const hg_layer_desc* L) {
+  if (validate_layer(s, L) != HG_OK) return 0;
+  Sizer z;
+  if (L->d_in == 64) {
+    FwdWs<64> w;
+    w.layout(z, s);
+  } else {
+    FwdWs<128> w;
+    w.layout(z, s);
+  }
+  return z.used + 256;
+}
+
+extern "C" size_t hg_layer_bwd_workspace_size(const hg_subgraph* s, const hg_layer_desc* L) {
+  if (validate_layer(s, L) != HG_OK) return 0;
+  Sizer z;
+  if (L->d_in == 64) {
+    BwdWs<64> w;
+    w.layout(z, s);
+  } else {
+    BwdWs<128> w;
+    w.layout(z, s);
+  }
+  return z.used + 256;
+}
+
+extern "C" int hg_layer_fwd(const hg_subgraph* s, const hg_layer_desc* L, const void* H_in,
+                            const float* W_rel, const float* W_self, const float* bias, void* H_out,
+                            void* saved, void* ws, size_t ws_bytes, void* stream) {
+  HG_TRY(validate_layer(s, L));
+  if (s->n_sub > 0 && (!H_in || !H_out || !saved || !W_rel || !W_self))
+    return fail(HG_ERR_ARG, "null layer argument");
+  if (H_in == H_out && s->n_sub > 0) return fail(HG_ERR_ARG, "H_out must not alias H_in");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (L->d_in == 64)
+    return layer_fwd_impl<64>(s, L, (const float*)H_in, W_rel, W_self, bias, (float*)H_out,
+                              (uint32_t*)saved, ws, ws_bytes, st);
+  return layer_fwd_impl<128>(s, L, (const float*)H_in, W_rel, W_self, bias, (float*)H_out,
+                             (uint32_t*)saved, ws, ws_bytes, st);
+}
+
+extern "C" int hg_layer_bwd(const hg_subgraph* s, const hg_layer_desc* L, const void* H_in,
+                            const float* W_rel, const float* W_self, const void* saved,
+                            const void* dH_out, void* dH_in, float* dW_rel, float* dW_self,
+                            float* dbias, void* ws, size_t ws_bytes, void* stream) {
+  HG_TRY(validate_layer(s, L));
+  if (!W_rel || !W_self || !dW_rel || !dW_self) return fail(HG_ERR_ARG, "null weight argument");
+  if (s->n_sub > 0 && (!H_in || !saved || !dH_out || !dH_in)) return fail(HG_ERR_ARG, "null layer argument");
+  if (dH_in == dH_out && s->n_sub > 0) return fail(HG_ERR_ARG, "dH_in must not alias dH_out");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (L->d_in == 64)
+    return layer_bwd_impl<64>(s, L, (const float*)H_in, W_rel, W_self, (const uint32_t*)saved,
+                              (const float*)dH_out, (float*)dH_in, dW_rel, dW_self, dbias, ws, ws_bytes, st);
+  return layer_bwd_impl<128>(s, L, (const float*)H_in, W_rel, W_self, (const uint32_t*)saved,
+                             (const float*)dH_out, (float*)dH_in, dW_rel, dW_self, dbias, ws, ws_bytes, st);
+}

@@ -1,0 +1,297 @@
+// Device-wide primitives: exclusive scan, stable LSD radix sort, stable
+// bucket partition and fills.  All of them are deterministic: counts use
+// integer atomics only where the result does not depend on their order.
+#include "hg_internal.h"
+
+namespace hg {
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kItems = 16;
+constexpr int kTile = kThreads * kItems;  // 4096
+constexpr int kWaves = kThreads / kWave;
+
+__device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
+
+// Inclusive wave scan of one int per lane.
+__device__ __forceinline__ int wave_incl_scan(int v) {
+  const int l = lane_id();
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    int t = __shfl_up(v, o, kWave);
+    if (l >= o) v += t;
+  }
+  return v;
+}
+
+// Exclusive block scan of one int per thread; returns the block total in *total.
+__device__ __forceinline__ int block_excl_scan(int v, int* total) {
+  __shared__ int wsum[kWaves];
+  const int w = threadIdx.x / kWave;
+  int inc = wave_incl_scan(v);
+  if (lane_id() == kWave - 1) wsum[w] = inc;
+  __syncthreads();
+  int off = 0, tot = 0;
+#pragma unroll
+  for (int i = 0; i < kWaves; ++i) {
+    int x = wsum[i];
+    off += (i < w) ? x : 0;
+    tot += x;
+  }
+  __syncthreads();
+  *total = tot;
+  return off + inc - v;
+}
+
+__global__ void k_tile_sums(const int32_t* __restrict__ in, int64_t n, int32_t* __restrict__ sums) {
+  const int64_t base = (int64_t)blockIdx.x * kTile;
+  int s = 0;
+#pragma unroll
+  for (int j = 0; j < kItems; ++j) {
+    int64_t i = base + (int64_t)j * kThreads + threadIdx.x;
+    s += (i < n) ? in[i] : 0;
+  }
+  int tot;
+  (void)block_excl_scan(s, &tot);
+  if (threadIdx.x == 0) sums[blockIdx.x] = tot;
+}
+
+// Single block: exclusive scan of sums[0..m) in place, carrying across chunks.
+__global__ void k_scan_sums(int32_t* __restrict__ sums, int64_t m, int32_t* __restrict__ total) {
+  int carry = 0;
+  for (int64_t base = 0; base < m; base += kThreads) {
+    int64_t i = base + threadIdx.x;
+    int v = (i < m) ? sums[i] : 0;
+    int tot;
+    int ex = block_excl_scan(v, &tot);
+    if (i < m) sums[i] = carry + ex;
+    carry += tot;
+  }
+  if (threadIdx.x == 0 && total) *total = carry;
+}
+
+// Per tile: blocked arrangement (thread t owns items [t*16, t*16+16) of the tile).
+__global__ void k_scan_tiles(const int32_t* __restrict__ in, int32_t* __restrict__ out, int64_t n,
+                             const int32_t* __restrict__ tile_off) {
+  const int64_t base = (int64_t)blockIdx.x * kTile + (int64_t)threadIdx.x * kItems;
+  int v[kItems];
+  int s = 0;
+#pragma unroll
+  for (int j = 0; j < kItems; ++j) {
+    int64_t i = base + j;
+    v[j] = (i < n) ? in[i] : 0;
+    s += v[j];
+  }
+  int tot;
+  int ex = block_excl_scan(s, &tot) + tile_off[blockIdx.x];
+#pragma unroll
+  for (int j = 0; j < kItems; ++j) {
+    int64_t i = base + j;
+    if (i < n) out[i] = ex;
+    ex += v[j];
+  }
+}
+
+// ---- radix sort -------------------------------------------------------------
+
+// Digit histogram of one tile: hist[d * ntiles + tile].
+template <bool kDigitArray>
+__global__ void k_radix_upsweep(const uint32_t* __restrict__ keys, const uint8_t* __restrict__ digits,
+                                int64_t n, int shift, uint32_t dmask, int32_t* __restrict__ hist,
+                                int64_t ntiles) {
+  __shared__ int cnt[256];
+  cnt[threadIdx.x] = 0;
+  __syncthreads();
+  const int64_t base = (int64_t)blockIdx.x * kTile;
+#pragma unroll 4
+  for (int j = 0; j < kItems; ++j) {
+    int64_t i = base + (int64_t)j * kThreads + threadIdx.x;
+    if (i < n) {
+      uint32_t d = kDigitArray ? (uint32_t)digits[i] : ((keys[i] >> shift) & dmask);
+      if (!kDigitArray || d != 255u) atomicAdd(&cnt[d], 1);
+    }
+  }
+  __syncthreads();
+  hist[(int64_t)threadIdx.x * ntiles + blockIdx.x] = cnt[threadIdx.x];
+}
+
+// Stable scatter of one tile.  Items are visited in 16 rounds of 256
+// consecutive items; inside a round the order is (wave, lane).  An item's
+// destination is the tile's global offset for its digit plus the number of
+// earlier items of the tile with the same digit.
+template <bool kDigitArray, bool kHasV1, bool kHasV2>
+__global__ void k_radix_downsweep(const uint32_t* __restrict__ keys, const uint8_t* __restrict__ digits,
+                                  const int32_t* __restrict__ v1, const int32_t* __restrict__ v2,
+                                  int64_t n, int shift, uint32_t dmask,
+                                  const int32_t* __restrict__ offs, int64_t ntiles,
+                                  uint32_t* __restrict__ keys_out, int32_t* __restrict__ v1_out,
+                                  int32_t* __restrict__ v2_out) {
+  __shared__ int base_d[256];
+  __shared__ int wcnt[kWaves][256];
+  __shared__ int wpre[kWaves][256];
+  const int t = threadIdx.x;
+  const int w = t / kWave;
+  const int l = lane_id();
+  base_d[t] = offs[(int64_t)t * ntiles + blockIdx.x];
+#pragma unroll
+  for (int i = 0; i < kWaves; ++i) wcnt[i][t] = 0;
+  __syncthreads();
+  const uint64_t lt_mask = (l == 0) ? 0ull : (~0ull >> (kWave - l));
+  const int64_t tile_base = (int64_t)blockIdx.x * kTile;
+  for (int j = 0; j < kItems; ++j) {
+    const int64_t i = tile_base + (int64_t)j * kThreads + t;
+    const bool valid0 = i < n;
+    uint32_t k = 0, d = 0;
+    if (valid0) {
+      if (kDigitArray) {
+        d = digits[i];
+      } else {
+        k = keys[i];
+        d = (k >> shift) & dmask;
+      }
+    }
+    const bool valid = valid0 && (!kDigitArray || d != 255u);
+    uint64_t m = __ballot(valid);
+#pragma unroll
+    for (int b = 0; b < 8; ++b) {
+      const bool bit = (d >> b) & 1u;
+      const uint64_t bal = __ballot(bit);
+      m &= bit ? bal : ~bal;
+    }
+    int rank = 0;
+    if (valid) {
+      rank = __popcll(m & lt_mask);
+      if ((m & lt_mask) == 0) wcnt[w][d] = __popcll(m);
+    }
+    __syncthreads();
+    {
+      int run = base_d[t];
+#pragma unroll
+      for (int q = 0; q < kWaves; ++q) {
+        wpre[q][t] = run;
+        run += wcnt[q][t];
+        wcnt[q][t] = 0;
+      }
+      base_d[t] = run;
+    }
+    __syncthreads();
+    if (valid) {
+      const int pos = wpre[w][d] + rank;
+      if (!kDigitArray) keys_out[pos] = k;
+      if (kHasV1) v1_out[pos] = v1[i];
+      if (kHasV2) v2_out[pos] = v2[i];
+    }
+  }
+}
+
+__global__ void k_bin_offsets(const int32_t* __restrict__ offs, int64_t ntiles, int nbins,
+                              const int32_t* __restrict__ total, int32_t* __restrict__ bin_off) {
+  int b = threadIdx.x;
+  if (b < nbins) bin_off[b] = offs[(int64_t)b * ntiles];
+  if (b == nbins) bin_off[b] = *total;
+}
+
+template <class T>
+__global__ void k_fill(T* __restrict__ p, T v, int64_t n) {
+  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (; i < n; i += stride) p[i] = v;
+}
+
+template <class T>
+int fill_impl(T* p, T v, int64_t n, hipStream_t s) {
+  if (n <= 0) return HG_OK;
+  int64_t blocks = cdiv(n, 256);
+  if (blocks > 65536) blocks = 65536;
+  HG_LAUNCH("fill", (k_fill<T>), dim3((unsigned)blocks), dim3(256), 0, s, p, v, n);
+  return HG_OK;
+}
+
+}  // namespace
+
+int64_t scan_scratch_elems(int64_t n) { return cdiv(n > 0 ? n : 1, kTile) + 64; }
+
+int scan_exclusive_i32(const int32_t* in, int32_t* out, int64_t n, int32_t* total_dev,
+                       int32_t* scratch, hipStream_t s) {
+  if (n <= 0) {
+    if (total_dev) HG_TRY(fill_i32(total_dev, 0, 1, s));
+    return HG_OK;
+  }
+  const int64_t tiles = cdiv(n, kTile);
+  HG_LAUNCH("scan_tile_sums", k_tile_sums, dim3((unsigned)tiles), dim3(kThreads), 0, s, in, n, scratch);
+  HG_LAUNCH("scan_sums", k_scan_sums, dim3(1), dim3(kThreads), 0, s, scratch, tiles, total_dev);
+  HG_LAUNCH("scan_tiles", k_scan_tiles, dim3((unsigned)tiles), dim3(kThreads), 0, s, in, out, n,
+            (const int32_t*)scratch);
+  return HG_OK;
+}
+
+int64_t radix_scratch_elems(int64_t n) {
+  const int64_t tiles = cdiv(n > 0 ? n : 1, kTile);
+  const int64_t h = 256 * tiles;
+  return h + scan_scratch_elems(h) + 64;
+}
+
+int radix_sort_pairs(uint32_t* keys, uint32_t* keys_alt, int32_t* v1, int32_t* v1_alt,
+                     int32_t* v2, int32_t* v2_alt, int64_t n, int bits, int32_t* scratch,
+                     hipStream_t s, uint32_t** keys_out, int32_t** v1_out, int32_t** v2_out) {
+  *keys_out = keys;
+  *v1_out = v1;
+  if (v2_out) *v2_out = v2;
+  if (n <= 0 || bits <= 0) return HG_OK;
+  const int64_t tiles = cdiv(n, kTile);
+  int32_t* hist = scratch;
+  int32_t* sscr = scratch + 256 * tiles;
+  uint32_t *ka = keys, *kb = keys_alt;
+  int32_t *a1 = v1, *b1 = v1_alt, *a2 = v2, *b2 = v2_alt;
+  for (int shift = 0; shift < bits; shift += 8) {
+    const int nb = (bits - shift) < 8 ? (bits - shift) : 8;
+    const uint32_t dmask = (1u << nb) - 1u;
+    HG_LAUNCH("radix_upsweep", (k_radix_upsweep<false>), dim3((unsigned)tiles), dim3(kThreads), 0, s,
+              (const uint32_t*)ka, (const uint8_t*)nullptr, n, shift, dmask, hist, tiles);
+    HG_TRY(scan_exclusive_i32(hist, hist, 256 * tiles, nullptr, sscr, s));
+    if (v2) {
+      HG_LAUNCH("radix_downsweep", (k_radix_downsweep<false, true, true>), dim3((unsigned)tiles),
+                dim3(kThreads), 0, s, (const uint32_t*)ka, (const uint8_t*)nullptr,
+                (const int32_t*)a1, (const int32_t*)a2, n, shift, dmask, (const int32_t*)hist,
+                tiles, kb, b1, b2);
+    } else {
+      HG_LAUNCH("radix_downsweep", (k_radix_downsweep<false, true, false>), dim3((unsigned)tiles),
+                dim3(kThreads), 0, s, (const uint32_t*)ka, (const uint8_t*)nullptr,
+                (const int32_t*)a1, (const int32_t*)nullptr, n, shift, dmask,
+                (const int32_t*)hist, tiles, kb, b1, (int32_t*)nullptr);
+    }
+    uint32_t* tk = ka; ka = kb; kb = tk;
+    int32_t* t1 = a1; a1 = b1; b1 = t1;
+    int32_t* t2 = a2; a2 = b2; b2 = t2;
+  }
+  *keys_out = ka;
+  *v1_out = a1;
+  if (v2_out) *v2_out = a2;
+  return HG_OK;
+}
+
+int bucket_partition(const uint8_t* digit, const int32_t* val, int64_t n, int nbins, int32_t* out,
+                     int32_t* bin_off, int32_t* scratch, hipStream_t s) {
+  if (nbins < 1 || nbins > 255) return fail(HG_ERR_ARG, "bucket_partition: nbins %d", nbins);
+  if (n <= 0) return fill_i32(bin_off, 0, nbins + 1, s);
+  const int64_t tiles = cdiv(n, kTile);
+  int32_t* hist = scratch;
+  int32_t* sscr = scratch + 256 * tiles;
+  int32_t* total = sscr + scan_scratch_elems(256 * tiles);
+  HG_LAUNCH("partition_upsweep", (k_radix_upsweep<true>), dim3((unsigned)tiles), dim3(kThreads), 0, s,
+            (const uint32_t*)nullptr, digit, n, 0, 0xFFu, hist, tiles);
+  HG_TRY(scan_exclusive_i32(hist, hist, 256 * tiles, total, sscr, s));
+  HG_LAUNCH("partition_downsweep", (k_radix_downsweep<true, true, false>), dim3((unsigned)tiles),
+            dim3(kThreads), 0, s, (const uint32_t*)nullptr, digit, val, (const int32_t*)nullptr, n,
+            0, 0xFFu, (const int32_t*)hist, tiles, (uint32_t*)nullptr, out, (int32_t*)nullptr);
+  HG_LAUNCH("partition_offsets", k_bin_offsets, dim3(1), dim3(256), 0, s, (const int32_t*)hist,
+            tiles, nbins, (const int32_t*)total, bin_off);
+  return HG_OK;
+}
+
+int fill_i32(int32_t* p, int32_t v, int64_t n, hipStream_t s) { return fill_impl(p, v, n, s); }
+int fill_u8(uint8_t* p, uint8_t v, int64_t n, hipStream_t s) { return fill_impl(p, v, n, s); }
+int fill_f32(float* p, float v, int64_t n, hipStream_t s) { return fill_impl(p, v, n, s); }
+
+}  // namespace hg

@@ -1,0 +1,121 @@
+"""One training step of the hot path through the C ABI: subgraph build,
+L layers forward, the CCA alignment on the overlap rows, L layers backward.
+
+This module only allocates buffers (torch) and sequences library calls; all
+arithmetic runs in libhg.so.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+from typing import List, Optional
+
+import numpy as np
+import torch
+
+from . import api, synth
+
+
+@dataclass
+class StepInputs:
+    wl: synth.Workload
+    graph: dict                 # device tensors src, dst, rel, ntype, part
+    k: int
+    sub: api.Subgraph
+    build_ws: torch.Tensor
+    h0: torch.Tensor            # [n_sub, d] features in local order
+    weights: List[tuple]        # per layer (w_rel, w_self, bias) device float32
+    weights_np: list
+    href: torch.Tensor          # [m_sel, d]
+    gext: torch.Tensor          # [n_sub, d]
+    omega: Optional[torch.Tensor]
+    feats_np: np.ndarray
+    href_np: np.ndarray
+    gext_np: np.ndarray
+    # preallocated per-step buffers
+    H: List[torch.Tensor] = field(default_factory=list)
+    saved: List[torch.Tensor] = field(default_factory=list)
+    dH: List[torch.Tensor] = field(default_factory=list)
+    grads: List[tuple] = field(default_factory=list)
+    fwd_ws: Optional[torch.Tensor] = None
+    bwd_ws: Optional[torch.Tensor] = None
+    align_ws: Optional[torch.Tensor] = None
+    loss: Optional[torch.Tensor] = None
+
+
+@dataclass
+class StepResult:
+    loss: torch.Tensor
+    dH0: torch.Tensor
+    grads: List[tuple]
+
+
+def _dev(x, device):
+    return torch.from_numpy(np.ascontiguousarray(x)).to(device)
+
+
+def make_inputs(wl: synth.Workload, g: synth.Graph, device="cuda", feats: Optional[np.ndarray] = None
+                ) -> StepInputs:
+    cfg, mc = wl.graph, wl.model
+    d = mc.d
+    gd = {k: _dev(getattr(g, k), device) for k in ("src", "dst", "rel", "ntype", "part")}
+    sub = api.hg_build_csr(gd["src"], gd["dst"], gd["rel"], gd["ntype"], gd["part"], g.k, cfg.n_rel,
+                           g.n_ntype, cfg.budget, key=cfg.key, theta=cfg.theta, seed=cfg.seed)
+    import ctypes as C
+    gdesc = api.GraphDesc(g.n_nodes, g.n_edges, cfg.n_rel, g.n_ntype, None, None, None, None, None, 0, None)
+    odesc = api.OverlapDesc(cfg.budget, cfg.key, 0, cfg.theta, 0, cfg.seed)
+    build_ws = api._ws(int(api.lib().hg_build_csr_workspace_size(C.byref(gdesc), C.byref(odesc))), device)
+    feats = synth.features(mc.seed, g.n_nodes, d) if feats is None else feats
+    l2g = sub.view("local2global").long()
+    h0 = _dev(feats, device).index_select(0, l2g).contiguous()
+    weights_np = [synth.layer_weights(mc.seed, li, cfg.n_rel, g.n_ntype, d, mc.bias_range)
+                  for li in range(mc.n_layers)]
+    weights = [(_dev(w.w_rel, device), _dev(w.w_self, device), _dev(w.bias, device)) for w in weights_np]
+    m = sub.m_sel
+    href_np = synth.reference_embeddings(mc.seed, max(m, 1), d)
+    gext_np = synth.upstream_grad(mc.seed, max(sub.n_sub, 1), d)
+    omega = None
+    if mc.weighted_align and m > 0:
+        orel = sub.view("overlap_rel").cpu().numpy()
+        omega = _dev(synth.align_weights(orel, g.rel, cfg.n_rel), device)
+    inp = StepInputs(wl, gd, g.k, sub, build_ws, h0, weights, weights_np, _dev(href_np[:m], device),
+                     _dev(gext_np[: sub.n_sub], device), omega, feats, href_np, gext_np)
+    ns = sub.n_sub
+    f32 = dict(dtype=torch.float32, device=device)
+    inp.H = [h0] + [torch.empty((ns, d), **f32) for _ in range(mc.n_layers)]
+    inp.saved = [torch.empty((max(ns, 1), d // 32), dtype=torch.int32, device=device)
+                 for _ in range(mc.n_layers)]
+    inp.dH = [torch.empty((ns, d), **f32) for _ in range(2)]
+    inp.grads = [(torch.empty_like(w[0]), torch.empty_like(w[1]), torch.empty_like(w[2])) for w in weights]
+    inp.fwd_ws = api._ws(api.hg_layer_fwd_workspace_size(sub, d), device)
+    inp.bwd_ws = api._ws(api.hg_layer_bwd_workspace_size(sub, d), device)
+    inp.align_ws = api._ws(api.hg_align_workspace_size(m, d), device)
+    inp.loss = torch.empty(3, **f32)
+    return inp
+
+
+def run_step(inp: StepInputs, rebuild: bool = True) -> StepResult:
+    cfg, mc = inp.wl.graph, inp.wl.model
+    gd = inp.graph
+    if rebuild:
+        api.hg_build_csr(gd["src"], gd["dst"], gd["rel"], gd["ntype"], gd["part"], inp.k, cfg.n_rel, 2,
+                         cfg.budget, key=cfg.key, theta=cfg.theta, seed=cfg.seed, ws=inp.build_ws,
+                         out=inp.sub)
+    sub = inp.sub
+    for li in range(mc.n_layers):
+        w_rel, w_self, bias = inp.weights[li]
+        api.hg_layer_fwd(sub, inp.H[li], w_rel, w_self, bias, H_out=inp.H[li + 1], saved=inp.saved[li],
+                         ws=inp.fwd_ws)
+    g = inp.dH[0]
+    g.copy_(inp.gext)
+    overlap = sub.view("overlap")
+    api.hg_align_loss_fwd_bwd(inp.H[-1], overlap, inp.href, g, w=inp.omega, lambda_n=mc.lambda_n,
+                              scale=mc.lambda_cca, eps=mc.eps, ddof=mc.ddof, loss3=inp.loss,
+                              ws=inp.align_ws)
+    cur, nxt = 0, 1
+    for li in reversed(range(mc.n_layers)):
+        w_rel, w_self, _ = inp.weights[li]
+        gw = inp.grads[li]
+        api.hg_layer_bwd(sub, inp.H[li], w_rel, w_self, inp.saved[li], inp.dH[cur], dH_in=inp.dH[nxt],
+                         dW_rel=gw[0], dW_self=gw[1], dbias=gw[2], ws=inp.bwd_ws)
+        cur, nxt = nxt, cur
+    return StepResult(inp.loss, inp.dH[cur], inp.grads)

@@ -1,0 +1,175 @@
+"""The C ABI on the host: the library loads, exports every symbol the
+header declares, and rejects invalid arguments before any device work
+(no GPU is needed for any of these)."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+from paper_2608_02168_amd import api
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "hg.h")
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(api.LIB_PATH):
+        pytest.skip("libhg.so not built")
+    return api.lib()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(hg_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol(L):
+    names = declared_functions()
+    assert len(names) >= 14
+    for n in names:
+        assert hasattr(L, n), n
+    assert set(names) == set(api.EXPORTS)
+
+
+def test_status_strings(L):
+    for code in (0, -1, -2, -3, -4, -5):
+        assert api.status_string(code).startswith("HG_")
+    assert "unknown" in api.status_string(7)
+
+
+def _graph(n=10, e=5, R=2, T=2, **kw):
+    fake = C.c_void_p(0x1000)  # never dereferenced: validation fails first
+    d = dict(n_nodes=n, n_edges=e, n_rel=R, n_ntype=T, src=fake, dst=fake, rel=fake, ntype=fake,
+             part=fake, k=0, edge_w=None)
+    d.update(kw)
+    return api.GraphDesc(**d)
+
+
+def _ov(**kw):
+    d = dict(budget_M=3, key=0, key_dir=0, theta=api.HG_THETA_NONE, reserved=0, seed=1)
+    d.update(kw)
+    return api.OverlapDesc(**d)
+
+
+@pytest.mark.parametrize("gkw,okw,code", [
+    (dict(n_nodes=0), {}, api.HG_ERR_ARG),
+    (dict(n_edges=-1), {}, api.HG_ERR_ARG),
+    (dict(n_edges=2**31), {}, api.HG_ERR_UNSUPPORTED),
+    (dict(n_rel=0), {}, api.HG_ERR_UNSUPPORTED),
+    (dict(n_rel=256), {}, api.HG_ERR_UNSUPPORTED),
+    (dict(n_ntype=0), {}, api.HG_ERR_UNSUPPORTED),
+    (dict(n_nodes=2**30, n_rel=4), {}, api.HG_ERR_UNSUPPORTED),
+    (dict(src=None), {}, api.HG_ERR_ARG),
+    (dict(part=None), {}, api.HG_ERR_ARG),
+    (dict(edge_w=C.c_void_p(0x1000)), {}, api.HG_ERR_UNSUPPORTED),
+    ({}, dict(budget_M=-1), api.HG_ERR_ARG),
+    ({}, dict(key=7), api.HG_ERR_ARG),
+    ({}, dict(key_dir=1), api.HG_ERR_UNSUPPORTED),
+    ({}, dict(theta=-3), api.HG_ERR_ARG),
+])
+def test_build_validation(L, gkw, okw, code):
+    g, o = _graph(**gkw), _ov(**okw)
+    s = api.SubgraphStruct()
+    assert L.hg_build_csr_workspace_size(C.byref(g), C.byref(o)) == 0
+    assert L.hg_build_csr(C.byref(g), C.byref(o), C.byref(s), None, 0, None) == code
+    assert len(api.last_error_detail()) > 0
+
+
+def test_build_capacity_checks(L):
+    g, o = _graph(), _ov()
+    fake = C.c_void_p(0x1000)
+    s = api.SubgraphStruct()
+    for name in ("local2global", "global2local", "type_off", "overlap", "overlap_home",
+                 "overlap_rel", "csr_ptr", "csr_col", "csc_ptr", "csc_row", "csc_scale", "plan"):
+        setattr(s, name, fake)
+    s.plan_bytes = 1
+    assert L.hg_build_csr(C.byref(g), C.byref(o), C.byref(s), fake, 1 << 30, None) == api.HG_ERR_CAPACITY
+    assert "plan" in api.last_error_detail()
+    s.plan_bytes = api.hg_plan_size(10, 5, 2)
+    need = L.hg_build_csr_workspace_size(C.byref(g), C.byref(o))
+    assert need > 0
+    assert L.hg_build_csr(C.byref(g), C.byref(o), C.byref(s), fake, need - 1, None) == api.HG_ERR_CAPACITY
+    s.overlap = None
+    assert L.hg_build_csr(C.byref(g), C.byref(o), C.byref(s), fake, need, None) == api.HG_ERR_ARG
+
+
+def test_plan_size_monotone(L):
+    assert api.hg_plan_size(10, 10, 1) > 0
+    assert api.hg_plan_size(1000, 10**5, 3) > api.hg_plan_size(1000, 10**4, 3)
+    assert L.hg_plan_size(-1, 0, 1) == 0
+
+
+def _sub(n_sub=10, R=2, T=2):
+    s = api.SubgraphStruct()
+    fake = C.c_void_p(0x1000)
+    s.csr_ptr = s.csc_ptr = s.plan = fake
+    s.n_sub, s.n_rel, s.n_ntype = n_sub, R, T
+    return s
+
+
+@pytest.mark.parametrize("desc,code", [
+    (dict(d_in=64, d_out=128), api.HG_ERR_UNSUPPORTED),
+    (dict(d_in=96, d_out=96), api.HG_ERR_UNSUPPORTED),
+    (dict(d_in=64, d_out=64, dtype=9), api.HG_ERR_ARG),
+    (dict(d_in=64, d_out=64, relu=2), api.HG_ERR_ARG),
+])
+def test_layer_validation(L, desc, code):
+    full = dict(d_in=64, d_out=64, dtype=0, relu=1, residual=1)
+    full.update(desc)
+    ld = api.LayerDesc(**full)
+    s = _sub()
+    fake = C.c_void_p(0x1000)
+    assert L.hg_layer_fwd(C.byref(s), C.byref(ld), fake, fake, fake, None, C.c_void_p(0x2000), fake,
+                          fake, 1, None) == code
+    assert L.hg_layer_fwd_workspace_size(C.byref(s), C.byref(ld)) == 0
+
+
+def test_layer_alias_and_null_checks(L):
+    ld = api.LayerDesc(64, 64, 0, 1, 1)
+    s = _sub()
+    fake = C.c_void_p(0x1000)
+    assert L.hg_layer_fwd(C.byref(s), C.byref(ld), fake, fake, fake, None, fake, fake, fake, 1,
+                          None) == api.HG_ERR_ARG
+    assert L.hg_layer_fwd(C.byref(s), C.byref(ld), None, fake, fake, None, C.c_void_p(8), fake, fake,
+                          1, None) == api.HG_ERR_ARG
+    assert L.hg_layer_bwd(C.byref(s), C.byref(ld), fake, None, fake, fake, fake, fake, fake, fake,
+                          None, fake, 1, None) == api.HG_ERR_ARG
+    assert L.hg_layer_fwd(None, C.byref(ld), fake, fake, fake, None, fake, fake, fake, 1,
+                          None) == api.HG_ERR_ARG
+
+
+def test_layer_workspace_sizes_scale_with_graph(L):
+    ld = api.LayerDesc(128, 128, 0, 1, 1)
+    a, b = _sub(n_sub=100), _sub(n_sub=1000)
+    assert L.hg_layer_fwd_workspace_size(C.byref(b), C.byref(ld)) > \
+        L.hg_layer_fwd_workspace_size(C.byref(a), C.byref(ld))
+    assert L.hg_layer_saved_size(C.byref(b), C.byref(ld)) == 1000 * 4 * 4
+
+
+@pytest.mark.parametrize("args,code", [
+    (dict(M=-1), api.HG_ERR_ARG),
+    (dict(d=96), api.HG_ERR_UNSUPPORTED),
+    (dict(dtype=1), api.HG_ERR_UNSUPPORTED),
+    (dict(M=20, n_rows=10), api.HG_ERR_ARG),
+    (dict(M=1, ddof=1), api.HG_ERR_ARG),
+    (dict(eps=-1.0), api.HG_ERR_ARG),
+    (dict(H=None), api.HG_ERR_ARG),
+])
+def test_align_validation(L, args, code):
+    fake = C.c_void_p(0x1000)
+    a = dict(M=5, d=64, dtype=0, n_rows=10, H=fake, overlap=fake, H_ref=fake, w=None, lambda_n=2e-4,
+             scale=0.1, eps=1e-5, ddof=0, loss3=fake, dH=fake, dH_ref=None, ws=fake, ws_bytes=1 << 20,
+             stream=None)
+    a.update(args)
+    assert L.hg_align_loss_fwd_bwd(*a.values()) == code
+    assert L.hg_align_workspace_size(5, 96) == 0
+    assert L.hg_align_workspace_size(5, 64) > 0
+
+
+def test_product_path_fails_loudly_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(api, "_lib", None)
+    monkeypatch.setattr(api, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(ImportError):
+        api.lib()

@@ -1,0 +1,105 @@
+"""GPU parity of hg_build_csr against the oracle: every integer output
+bit-exact (csc_scale bit-exact as a correctly rounded quotient), run-twice
+determinism, and the device range check."""
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+from oracle import select
+from paper_2608_02168_amd import api, synth
+from tests.helpers import graph_to_dev
+
+pytestmark = pytest.mark.gpu
+
+CASES = {
+    # name: (graph config, key, theta, budget override)
+    "tiny": (synth.WORKLOADS["tiny"].graph, 0, select.THETA_NONE, None),
+    "tiny_hindex_theta2": (synth.WORKLOADS["tiny"].graph, 1, 2, None),
+    "tiny_budget_cut": (synth.WORKLOADS["tiny"].graph, 0, select.THETA_NONE, 137),
+    "tiny_hindex_budget_cut": (synth.WORKLOADS["tiny"].graph, 1, select.THETA_NONE, 211),
+    "skew_small_theta3": (synth.scaled(synth.WORKLOADS["skew"].graph, 0.002), 0, 3, None),
+    "medium_small": (synth.scaled(synth.WORKLOADS["medium"].graph, 0.01), 0, select.THETA_NONE, 900),
+}
+
+
+def run_both(cfg, key, theta, budget, seed=12345, n_ntype=2):
+    g = synth.make_graph(cfg)
+    budget = cfg.budget if budget is None else budget
+    ref = select.build(g.src, g.dst, g.rel, g.ntype, g.part, g.k, cfg.n_rel, n_ntype, budget,
+                       key, theta, seed)
+    d = graph_to_dev(g)
+    sub = api.hg_build_csr(d["src"], d["dst"], d["rel"], d["ntype"], d["part"], g.k, cfg.n_rel,
+                           n_ntype, budget, key=key, theta=theta, seed=seed)
+    return g, ref, sub
+
+
+def assert_same(ref, sub):
+    assert sub.n_sub == ref.n_sub and sub.e_sub == ref.e_sub
+    assert sub.m_sel == ref.overlap.shape[0]
+    for name in ("local2global", "global2local", "type_off", "overlap", "overlap_home",
+                 "overlap_rel", "csr_ptr", "csr_col", "csr_eid", "csc_ptr", "csc_row"):
+        got = sub.view(name).cpu().numpy()
+        exp = getattr(ref, name)
+        assert got.shape == exp.shape, name
+        assert np.array_equal(got, exp.astype(got.dtype)), name
+    sc = sub.view("csc_scale").cpu().numpy()
+    assert np.array_equal(sc.view(np.uint32), ref.csc_scale.view(np.uint32))
+    assert sub.n_active() == list(ref.n_active)
+    assert sub.type_off_host() == list(ref.type_off)
+
+
+@pytest.mark.parametrize("case", sorted(CASES))
+def test_build_bit_exact(case):
+    cfg, key, theta, budget = CASES[case]
+    _, ref, sub = run_both(cfg, key, theta, budget)
+    assert_same(ref, sub)
+
+
+def test_build_deterministic():
+    cfg, key, theta, budget = CASES["tiny_hindex_budget_cut"]
+    _, _, a = run_both(cfg, key, theta, budget)
+    _, _, b = run_both(cfg, key, theta, budget)
+    for name in ("local2global", "overlap", "csr_col", "csc_row", "csc_scale"):
+        assert torch.equal(a.view(name), b.view(name))
+    pa = a.arrays["plan"].cpu().numpy()
+    pb = b.arrays["plan"].cpu().numpy()
+    assert np.array_equal(pa, pb)
+
+
+def test_build_single_type_single_relation_and_ragged():
+    rng = np.random.default_rng(4)
+    n, e = 1537, 9001
+    src = rng.integers(0, n, e).astype(np.int32)
+    dst = rng.integers(0, n, e).astype(np.int32)
+    rel = np.zeros(e, np.uint8)
+    ntype = np.zeros(n, np.uint8)
+    part = (rng.random(n) < 0.3).astype(np.int32)
+    ref = select.build(src, dst, rel, ntype, part, 1, 1, 1, 77, 0, select.THETA_NONE, 3)
+    t = lambda x: torch.from_numpy(x).cuda()
+    sub = api.hg_build_csr(t(src), t(dst), t(rel), t(ntype), t(part), 1, 1, 1, 77, seed=3)
+    assert_same(ref, sub)
+
+
+def test_build_no_edges_and_zero_budget():
+    n = 100
+    z32 = torch.zeros(0, dtype=torch.int32, device="cuda")
+    z8 = torch.zeros(0, dtype=torch.uint8, device="cuda")
+    ntype = torch.zeros(n, dtype=torch.uint8, device="cuda")
+    part = (torch.arange(n, device="cuda") >= 60).to(torch.int32)
+    sub = api.hg_build_csr(z32, z32, z8, ntype, part, 0, 2, 1, 0)
+    assert sub.n_sub == 60 and sub.e_sub == 0 and sub.m_sel == 0
+    assert torch.equal(sub.view("local2global").cpu(), torch.arange(60, dtype=torch.int32))
+    assert int(sub.view("csr_ptr").abs().sum()) == 0
+
+
+def test_build_range_error_is_reported():
+    n = 50
+    src = torch.tensor([1, 2, 70], dtype=torch.int32, device="cuda")  # 70 >= n
+    dst = torch.tensor([3, 4, 5], dtype=torch.int32, device="cuda")
+    rel = torch.zeros(3, dtype=torch.uint8, device="cuda")
+    ntype = torch.zeros(n, dtype=torch.uint8, device="cuda")
+    part = torch.zeros(n, dtype=torch.int32, device="cuda")
+    with pytest.raises(api.HgError) as ei:
+        api.hg_build_csr(src, dst, rel, ntype, part, 0, 1, 1, 5)
+    assert ei.value.status == api.HG_ERR_RANGE

@@ -1,0 +1,103 @@
+"""GPU parity of hg_layer_fwd / hg_layer_bwd against the oracle (float64),
+element-wise relative error <= 1e-4 for float32 features."""
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+from oracle import layer, select
+from paper_2608_02168_amd import api, synth
+from tests.helpers import graph_to_dev, pack_mask, parity_err, unpack_mask, to_dev
+
+pytestmark = pytest.mark.gpu
+TOL = 1e-4
+
+
+def setup(cfg, d, seed=7, bias_range=0.1):
+    g = synth.make_graph(cfg)
+    ref = select.build(g.src, g.dst, g.rel, g.ntype, g.part, g.k, cfg.n_rel, 2, cfg.budget)
+    dev = graph_to_dev(g)
+    sub = api.hg_build_csr(dev["src"], dev["dst"], dev["rel"], dev["ntype"], dev["part"], g.k,
+                           cfg.n_rel, 2, cfg.budget)
+    X = synth.features(seed, g.n_nodes, d)[ref.local2global]
+    w = synth.layer_weights(seed, 0, cfg.n_rel, 2, d, bias_range)
+    return g, ref, sub, X, w
+
+
+CFGS = {
+    "tiny_d64": (synth.WORKLOADS["tiny"].graph, 64),
+    "tiny_d128": (synth.WORKLOADS["tiny"].graph, 128),
+    "skew_small_d64": (synth.scaled(synth.WORKLOADS["skew"].graph, 0.002), 64),
+}
+
+
+@pytest.mark.parametrize("name", sorted(CFGS))
+@pytest.mark.parametrize("relu,residual", [(1, 1), (0, 1), (1, 0)])
+def test_layer_forward(name, relu, residual):
+    cfg, d = CFGS[name]
+    g, ref, sub, X, w = setup(cfg, d)
+    out, Z = layer.forward(ref.n_sub, ref.src_l, ref.dst_l, ref.rel_l, ref.ntype_l, X, w.w_rel,
+                           w.w_self, w.bias)
+    expect = (np.maximum(Z, 0) if relu else Z) + (X if residual else 0)
+    H, saved = api.hg_layer_fwd(sub, to_dev(X), to_dev(w.w_rel), to_dev(w.w_self), to_dev(w.bias),
+                                relu=bool(relu), residual=bool(residual))
+    assert parity_err(H.cpu().numpy(), expect) <= TOL
+    got_mask = unpack_mask(saved.cpu().numpy(), d)
+    exp_mask = (Z > 0) if relu else np.ones_like(Z, dtype=bool)
+    diff = got_mask != exp_mask
+    # only elements whose z lies within rounding of 0 may decide differently
+    band = 1e-4 * np.sqrt(np.mean(Z * Z))
+    assert np.all(np.abs(Z[diff]) <= band)
+
+
+@pytest.mark.parametrize("name", sorted(CFGS))
+@pytest.mark.parametrize("relu,residual", [(1, 1), (1, 0), (0, 1)])
+def test_layer_backward(name, relu, residual):
+    cfg, d = CFGS[name]
+    g, ref, sub, X, w = setup(cfg, d)
+    G = synth.upstream_grad(3, ref.n_sub, d)
+    _, Z = layer.forward(ref.n_sub, ref.src_l, ref.dst_l, ref.rel_l, ref.ntype_l, X, w.w_rel,
+                         w.w_self, w.bias)
+    mask = (Z > 0) if relu else np.ones_like(Z, dtype=bool)
+    dH, dWr, dWs, db = layer.backward(ref.n_sub, ref.src_l, ref.dst_l, ref.rel_l, ref.ntype_l, X,
+                                      w.w_rel, w.w_self, w.bias, G, mask=mask)
+    if not residual:
+        dH = dH - G
+    saved = to_dev(pack_mask(mask))
+    out = api.hg_layer_bwd(sub, to_dev(X), to_dev(w.w_rel), to_dev(w.w_self), saved, to_dev(G),
+                           relu=bool(relu), residual=bool(residual))
+    for got, exp, nm in zip(out, (dH, dWr, dWs, db), ("dH", "dW_rel", "dW_self", "dbias")):
+        err = parity_err(got.cpu().numpy(), exp)
+        assert err <= TOL, (nm, err)
+
+
+def test_layer_backward_deterministic():
+    cfg, d = CFGS["tiny_d128"]
+    g, ref, sub, X, w = setup(cfg, d)
+    G = to_dev(synth.upstream_grad(3, ref.n_sub, d))
+    Xd = to_dev(X)
+    _, saved = api.hg_layer_fwd(sub, Xd, to_dev(w.w_rel), to_dev(w.w_self), to_dev(w.bias))
+    a = api.hg_layer_bwd(sub, Xd, to_dev(w.w_rel), to_dev(w.w_self), saved, G)
+    b = api.hg_layer_bwd(sub, Xd, to_dev(w.w_rel), to_dev(w.w_self), saved, G)
+    for x, y in zip(a, b):
+        assert torch.equal(x, y)
+
+
+def test_forward_backward_chain_uses_own_mask():
+    """Forward then backward with the mask the forward saved: equal to the
+    oracle wherever no z sits at the ReLU kink."""
+    cfg, d = CFGS["tiny_d64"]
+    g, ref, sub, X, w = setup(cfg, d)
+    G = synth.upstream_grad(5, ref.n_sub, d)
+    _, Z = layer.forward(ref.n_sub, ref.src_l, ref.dst_l, ref.rel_l, ref.ntype_l, X, w.w_rel,
+                         w.w_self, w.bias)
+    band = 1e-4 * np.sqrt(np.mean(Z * Z))
+    if np.any(np.abs(Z) <= band):
+        pytest.skip("a z value sits at the ReLU kink for this seed")
+    Xd = to_dev(X)
+    _, saved = api.hg_layer_fwd(sub, Xd, to_dev(w.w_rel), to_dev(w.w_self), to_dev(w.bias))
+    out = api.hg_layer_bwd(sub, Xd, to_dev(w.w_rel), to_dev(w.w_self), saved, to_dev(G))
+    exp = layer.backward(ref.n_sub, ref.src_l, ref.dst_l, ref.rel_l, ref.ntype_l, X, w.w_rel,
+                         w.w_self, w.bias, G)
+    for got, e in zip(out, exp):
+        assert parity_err(got.cpu().numpy(), e) <= TOL
