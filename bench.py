@@ -1,0 +1,161 @@
+"""Benchmark of one training step of the hot path on one MI355X.
+
+A step = subgraph build (selection, relabel, CSR/CSC, plan), L layers
+forward, the CCA alignment loss + gradient on the overlap rows, L layers
+backward -- every step of it in libhg.so's HIP kernels, inputs resident in
+HBM before the timed region.
+
+Prints one JSON line: value = L * E_sub / t_step in GTEPS (edges x layers
+per second, forward + backward of every layer, build and alignment included),
+plus the roofline of the dominant kernel (algorithmic bytes per launch /
+average launch time from HIP events recorded around each launch on its own
+stream) and the oracle timed on the host cores on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+FP32_MFMA_PEAK_TFLOPS = 157.3
+
+
+def algorithmic_cost(kind: str, info: dict):
+    """(bytes, flops) per launch, counted without cache reuse.  E = subgraph
+    edges, N = subgraph nodes, A = active (source, relation) rows, s = bytes
+    per feature element, d = width, R = relations."""
+    E, N, A, d, s, R = info["E"], info["N"], info["A"], info["d"], info["s"], info["R"]
+    if kind == "spmm_fwd":
+        # per edge: one gathered row of Y plus its 4-byte column id; per node:
+        # R+1 row pointers, Y_self and H_in rows read, H_out row and d/8 mask bytes written
+        return E * (d * s + 4) + N * (4 * (R + 1) + 3 * d * s + d / 8), 2.0 * E * d
+    if kind == "spmm_bwd":
+        # per edge: one gathered dZ row, destination id and scale; per work
+        # item 16 bytes; per active row one dY row written
+        return E * (d * s + 8) + A * (d * s + 16), 2.0 * E * d
+    raise KeyError(kind)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--config", default="large", help="tiny | medium | large | skew")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample", type=float, default=0.01,
+                    help="fraction of the workload's node/edge counts the oracle runs on")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus})",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2608_02168_amd import api, runner, synth
+
+    wl = synth.WORKLOADS[args.config]
+    t0 = time.time()
+    g = synth.make_graph(wl.graph)
+    print(f"[bench] graph {wl.graph.name}: N={g.n_nodes} E={g.n_edges} generated in {time.time() - t0:.1f}s",
+          file=sys.stderr, flush=True)
+    inp = runner.make_inputs(wl, g, device="cuda")
+    sub = inp.sub
+    print(f"[bench] subgraph N_s={sub.n_sub} E_s={sub.e_sub} M_sel={sub.m_sel}", file=sys.stderr, flush=True)
+    L = wl.model.n_layers
+    for _ in range(args.warmup):
+        runner.run_step(inp)
+    torch.cuda.synchronize()
+    api.hg_timing_collect()
+    api.hg_timing_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        runner.run_step(inp)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    api.hg_timing_enable(False)
+    kern = api.hg_timing_collect()
+    ms = (t1 - t0) * 1e3 / args.steps
+    edges = L * sub.e_sub
+    value = edges / (ms * 1e-3) / 1e9
+
+    info = dict(E=sub.e_sub, N=sub.n_sub, A=sum(sub.n_active()), d=wl.model.d,
+                s=2 if wl.model.dtype == "bf16" else 4, R=sub.n_rel)
+    spmm = {k: v for k, v in kern.items() if k in ("spmm_fwd", "spmm_bwd")}
+    dom = max(spmm, key=lambda k: spmm[k][1])
+    launches, total_ms = spmm[dom]
+    avg_ms = total_ms / launches
+    nbytes, _ = algorithmic_cost(dom, info)
+    achieved = nbytes / (avg_ms * 1e-3) / 1e9
+    roofline = {"kernel": dom, "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                "avg_launch_ms": round(avg_ms, 4), "algorithmic_bytes_per_launch": int(nbytes)}
+    layer_ms = sum(v[1] for k, v in kern.items()
+                   if k.startswith(("spmm", "gemm_fwd", "gemm_bwd", "relu_grad", "splitk"))) / args.steps
+    breakdown = {k: round(v[1] / args.steps, 3) for k, v in sorted(kern.items(), key=lambda kv: -kv[1][1])}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(wl, args.cpu_sample)
+
+    out = {
+        "metric": "GNN layer fwd+bwd edges/sec (GTEPS) + achieved HBM GB/s fraction, 1 GPU",
+        "value": round(value, 4), "unit": "GTEPS", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 3), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32" if wl.model.dtype == "f32" else "bf16",
+        "data": "synthetic",
+        "config": {"workload": wl.desc, "name": args.config, "n_nodes": g.n_nodes, "n_edges": g.n_edges,
+                   "n_sub": sub.n_sub, "e_sub": sub.e_sub, "m_sel": sub.m_sel, "n_rel": sub.n_rel,
+                   "d": wl.model.d, "layers": L, "parallelism": "none (1 GPU)"},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "layer_gteps": round(edges / (layer_ms * 1e-3) / 1e9, 4) if layer_ms > 0 else None,
+        "kernel_ms_per_step": breakdown,
+    }
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(wl, frac):
+    """The oracle (oracle/step.py, unchanged) on the same recipe at a fraction
+    of the node and edge counts; reported in the same unit."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    from oracle import step as oracle_step
+    from paper_2608_02168_amd import synth
+
+    cfg = synth.scaled(wl.graph, frac)
+    g = synth.make_graph(cfg)
+    mc = wl.model
+    feats = synth.features(mc.seed, g.n_nodes, mc.d)
+    if mc.dtype == "bf16":
+        feats = synth.round_bf16(feats)
+    weights = [synth.layer_weights(mc.seed, li, cfg.n_rel, 2, mc.d, mc.bias_range) for li in range(mc.n_layers)]
+    href = synth.reference_embeddings(mc.seed, max(cfg.budget, 1), mc.d)
+    gext = synth.upstream_grad(mc.seed, g.n_nodes, mc.d)
+    t0 = time.perf_counter()
+    sub, *_ = oracle_step.run(dict(src=g.src, dst=g.dst, rel=g.rel, ntype=g.ntype, part=g.part),
+                              dict(k=g.k, n_rel=cfg.n_rel, n_ntype=2, budget=cfg.budget, key=cfg.key,
+                                   theta=cfg.theta, seed=cfg.seed),
+                              feats, weights, href, gext, lambda_n=mc.lambda_n, scale=mc.lambda_cca,
+                              eps=mc.eps, ddof=mc.ddof)
+    dt = time.perf_counter() - t0
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    return {"value": round(mc.n_layers * sub.e_sub / dt / 1e9, 6), "unit": "GTEPS", "cores": threads,
+            "kind": "oracle",
+            "sample": f"same recipe at {frac:g} of the node/edge counts: N={g.n_nodes}, E={g.n_edges}, "
+                      f"E_sub={sub.e_sub}; one full step (build, {mc.n_layers} layers fwd+bwd, alignment) "
+                      f"in {dt:.1f}s; float64; scipy sparse products single-threaded, BLAS {threads} threads"}
+
+
+if __name__ == "__main__":
+    main()

@@ -204,6 +204,8 @@ def hg_build_csr(src, dst, rel, ntype, part, k: int, n_rel: int, n_ntype: int, b
     L = lib()
     if out is not None:
         if ws is None:
+            ws = out.arrays.get("ws")
+        if ws is None:
             ws = _ws(int(L.hg_build_csr_workspace_size(C.byref(g), C.byref(o))), dev)
         _check(L.hg_build_csr(C.byref(g), C.byref(o), C.byref(out.c), _ptr(ws), ws.numel(),
                               _stream(stream)), "hg_build_csr")
@@ -237,6 +239,7 @@ def hg_build_csr(src, dst, rel, ntype, part, k: int, n_rel: int, n_ntype: int, b
         ws = _ws(need, dev)
     _check(L.hg_build_csr(C.byref(g), C.byref(o), C.byref(s), _ptr(ws), ws.numel(),
                           _stream(stream)), "hg_build_csr")
+    arrays["ws"] = ws
     return Subgraph(s, dev, arrays)
 
 

@@ -60,10 +60,7 @@ def make_inputs(wl: synth.Workload, g: synth.Graph, device="cuda", feats: Option
     gd = {k: _dev(getattr(g, k), device) for k in ("src", "dst", "rel", "ntype", "part")}
     sub = api.hg_build_csr(gd["src"], gd["dst"], gd["rel"], gd["ntype"], gd["part"], g.k, cfg.n_rel,
                            g.n_ntype, cfg.budget, key=cfg.key, theta=cfg.theta, seed=cfg.seed)
-    import ctypes as C
-    gdesc = api.GraphDesc(g.n_nodes, g.n_edges, cfg.n_rel, g.n_ntype, None, None, None, None, None, 0, None)
-    odesc = api.OverlapDesc(cfg.budget, cfg.key, 0, cfg.theta, 0, cfg.seed)
-    build_ws = api._ws(int(api.lib().hg_build_csr_workspace_size(C.byref(gdesc), C.byref(odesc))), device)
+    build_ws = sub.arrays["ws"]
     feats = synth.features(mc.seed, g.n_nodes, d) if feats is None else feats
     l2g = sub.view("local2global").long()
     h0 = _dev(feats, device).index_select(0, l2g).contiguous()
