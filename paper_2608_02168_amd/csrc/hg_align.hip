@@ -148,9 +148,13 @@ struct GradEpi {
   const float* w;
   float four_lambda;
   float two_sign;
-  __device__ __forceinline__ void operator()(int64_t b, int c, float v) const {
+  __device__ __forceinline__ int64_t row(int64_t b) const { return b; }
+  __device__ __forceinline__ float pre(int64_t b, int64_t, int c) const {
     const float diff = self.at(b, c) - other.at(b, c);
-    G[b * D + c] = four_lambda * v + two_sign * (w ? w[b] : 1.f) * diff;
+    return two_sign * (w ? w[b] : 1.f) * diff;
+  }
+  __device__ __forceinline__ void store(int64_t b, int64_t, int c, float acc, float pre) const {
+    G[b * D + c] = four_lambda * acc + pre;
   }
 };
 
@@ -188,7 +192,7 @@ struct AlignWs {
     shy = a.template take<float>(D);
     cx = a.template take<float>(D * D);
     cy = a.template take<float>(D * D);
-    cpart = a.template take<float>(nchunks * D);
+    cpart = a.template take<float>((nchunks + kSplitGroups + 1) * D);
     gpart = a.template take<float>(splitk_max_chunks() * (int64_t)D * D);
     invc = a.template take<float>(D);
     s1 = a.template take<float>(D);
@@ -207,8 +211,7 @@ int colsum(const char* name, int64_t m, F f, float* part, float* out, hipStream_
   const int64_t nch = align_chunks(m);
   const int64_t rpc = cdiv(m, nch);
   HG_LAUNCH(name, (k_colsum<D, F>), dim3((unsigned)nch), dim3(256), 0, s, m, rpc, f, part);
-  HG_LAUNCH("align_colsum_reduce", k_sum_partials, dim3(1), dim3(256), 0, s, (const float*)part, nch,
-            (int64_t)D, out, 0);
+  HG_TRY(reduce_partials(part, nch, (int64_t)D, part + nch * D, out, 0, s));
   return HG_OK;
 }
 

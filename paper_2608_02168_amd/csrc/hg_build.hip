@@ -32,6 +32,8 @@ inline unsigned grid_for(int64_t n, int64_t cap = 16384) {
   return (unsigned)(b < cap ? b : cap);
 }
 
+__device__ __forceinline__ int64_t cdiv_dev(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
 #define GRID_STRIDE(i, n)                                                        \
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < (n);     \
        i += (int64_t)gridDim.x * blockDim.x)
@@ -69,9 +71,42 @@ __device__ __forceinline__ uint32_t composite_digit(uint32_t key, uint64_t h, ui
   return (w >> (8 * (3 - (p & 3)))) & 0xFFu;
 }
 
+// bits[v / 32] bit v % 32 = pred(v); one wave covers 64 nodes (two words).
+__global__ void k_base_bits(const int32_t* __restrict__ part, int32_t k, int64_t n,
+                            uint32_t* __restrict__ bits) {
+  GRID_STRIDE(v0, cdiv_dev(n, 64) * 64) {
+    const bool in = v0 < n && part[v0] == k;
+    const uint64_t m = __ballot(in);
+    if ((threadIdx.x & 63) == 0) {
+      const int64_t wd = v0 >> 5;
+      bits[wd] = (uint32_t)m;
+      if ((v0 + 32) < n) bits[wd + 1] = (uint32_t)(m >> 32);
+    }
+  }
+}
+
+__global__ void k_cand_bits(const int32_t* __restrict__ first, int32_t n_edges, int64_t n,
+                            uint32_t* __restrict__ bits) {
+  GRID_STRIDE(v0, cdiv_dev(n, 64) * 64) {
+    const bool in = v0 < n && first[v0] < n_edges;
+    const uint64_t m = __ballot(in);
+    if ((threadIdx.x & 63) == 0) {
+      const int64_t wd = v0 >> 5;
+      bits[wd] = (uint32_t)m;
+      if ((v0 + 32) < n) bits[wd + 1] = (uint32_t)(m >> 32);
+    }
+  }
+}
+
+__device__ __forceinline__ bool bit_of(const uint32_t* __restrict__ bits, int32_t v) {
+  return (bits[v >> 5] >> (v & 31)) & 1u;
+}
+
+// Range checks and, for every node outside V_k, the smallest index of an edge
+// joining it to V_k; all out-degrees when count_all (needed by the h-index).
 __global__ void k_edges_pass(const int32_t* __restrict__ src, const int32_t* __restrict__ dst,
-                             const uint8_t* __restrict__ rel, const int32_t* __restrict__ part,
-                             int32_t k, int64_t n_nodes, int64_t n_edges, int32_t n_rel,
+                             const uint8_t* __restrict__ rel, const uint32_t* __restrict__ base_bits,
+                             int64_t n_nodes, int64_t n_edges, int32_t n_rel, int count_all,
                              int32_t* __restrict__ outdeg, int32_t* __restrict__ first,
                              int32_t* __restrict__ cnt) {
   GRID_STRIDE(e, n_edges) {
@@ -81,10 +116,19 @@ __global__ void k_edges_pass(const int32_t* __restrict__ src, const int32_t* __r
       atomicOr(&cnt[C_ERR], 1);
       continue;
     }
-    atomicAdd(&outdeg[s], 1);
-    const bool ps = part[s] == k, pd = part[d] == k;
+    if (count_all) atomicAdd(&outdeg[s], 1);
+    const bool ps = bit_of(base_bits, s), pd = bit_of(base_bits, d);
     if (pd && !ps) atomicMin(&first[s], (int32_t)e);
     if (ps && !pd) atomicMin(&first[d], (int32_t)e);
+  }
+}
+
+// Out-degrees of the candidate nodes only (the out-degree key needs no other).
+__global__ void k_cand_outdeg(const int32_t* __restrict__ src, int64_t n_edges,
+                              const uint32_t* __restrict__ cand_bits, int32_t* __restrict__ outdeg) {
+  GRID_STRIDE(e, n_edges) {
+    const int32_t s = src[e];
+    if (bit_of(cand_bits, s)) atomicAdd(&outdeg[s], 1);
   }
 }
 
@@ -284,9 +328,21 @@ __global__ void k_overlap_fill(const int32_t* __restrict__ l2g, const int32_t* _
   }
 }
 
+__global__ void k_member_bits(const int32_t* __restrict__ g2l, int64_t n, uint32_t* __restrict__ bits) {
+  GRID_STRIDE(v0, cdiv_dev(n, 64) * 64) {
+    const bool in = v0 < n && g2l[v0] >= 0;
+    const uint64_t m = __ballot(in);
+    if ((threadIdx.x & 63) == 0) {
+      const int64_t wd = v0 >> 5;
+      bits[wd] = (uint32_t)m;
+      if ((v0 + 32) < n) bits[wd + 1] = (uint32_t)(m >> 32);
+    }
+  }
+}
+
 __global__ void k_edge_keep(const int32_t* __restrict__ src, const int32_t* __restrict__ dst,
-                            const int32_t* __restrict__ g2l, int64_t n_edges, int32_t* __restrict__ keep) {
-  GRID_STRIDE(e, n_edges) { keep[e] = (g2l[src[e]] >= 0 && g2l[dst[e]] >= 0) ? 1 : 0; }
+                            const uint32_t* __restrict__ mbits, int64_t n_edges, int32_t* __restrict__ keep) {
+  GRID_STRIDE(e, n_edges) { keep[e] = (bit_of(mbits, src[e]) && bit_of(mbits, dst[e])) ? 1 : 0; }
 }
 
 __global__ void k_edge_compact(const int32_t* __restrict__ src, const int32_t* __restrict__ dst,
@@ -390,7 +446,7 @@ struct BuildWs {
   SelectState* st;
   int32_t *keep, *vsrc, *vdst, *veid, *alt1, *alt2, *alt3, *rowcnt, *q_items, *q_heavy, *q_parts,
       *q_src, *scratch;
-  uint32_t *kcsr, *kcsc, *kalt;
+  uint32_t *kcsr, *kcsc, *kalt, *bbits, *cbits, *mbits;
   void layout(A& a, int64_t N, int64_t E, int64_t R, bool hindex) {
     const int64_t NQ = N * R + 1;
     cnt = a.template take<int32_t>(C_COUNT + 8);
@@ -404,6 +460,9 @@ struct BuildWs {
     hoff = a.template take<int32_t>(hindex ? N + 1 : 0);
     hist = a.template take<int32_t>(hindex ? E + N : 0);
     sel = a.template take<uint8_t>(N);
+    bbits = a.template take<uint32_t>(N / 32 + 2);
+    cbits = a.template take<uint32_t>(N / 32 + 2);
+    mbits = a.template take<uint32_t>(N / 32 + 2);
     digit = a.template take<uint8_t>(NQ > N ? NQ : N);
     st = a.template take<SelectState>(1);
     keep = a.template take<int32_t>(E + 1);
@@ -525,9 +584,11 @@ extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg
   HG_TRY(fill_i32(w.outdeg, 0, N, s));
   HG_TRY(fill_i32(w.first, (int32_t)E, N, s));
   HG_TRY(fill_u8(w.sel, 0, N, s));
+  const unsigned gB = grid_for(cdiv(N, 64) * 64);
+  HG_LAUNCH("build_base_bits", k_base_bits, dim3(gB), dim3(kBT), 0, s, g->part, g->k, N, w.bbits);
   if (E > 0)
     HG_LAUNCH("build_edges_pass", k_edges_pass, dim3(gE), dim3(kBT), 0, s, g->src, g->dst, g->rel,
-              g->part, g->k, N, E, (int32_t)R, w.outdeg, w.first, w.cnt);
+              (const uint32_t*)w.bbits, N, E, (int32_t)R, hindex ? 1 : 0, w.outdeg, w.first, w.cnt);
   HG_LAUNCH("build_check_ntype", k_check_ntype, dim3(gN), dim3(kBT), 0, s, g->ntype, N, (int32_t)T, w.cnt);
   {
     int32_t herr = 0;
@@ -549,6 +610,11 @@ extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg
               (const int32_t*)w.outdeg, (const int32_t*)w.first, (const int32_t*)w.hoff,
               (const int32_t*)w.hist, N, (int32_t)E, w.key);
   } else {
+    HG_LAUNCH("build_cand_bits", k_cand_bits, dim3(gB), dim3(kBT), 0, s, (const int32_t*)w.first, (int32_t)E, N,
+              w.cbits);
+    if (E > 0)
+      HG_LAUNCH("build_cand_outdeg", k_cand_outdeg, dim3(gE), dim3(kBT), 0, s, g->src, E,
+                (const uint32_t*)w.cbits, w.outdeg);
     HG_LAUNCH("build_copy_key", k_copy_key, dim3(gN), dim3(kBT), 0, s, (const int32_t*)w.outdeg, N, w.key);
   }
   // 3. filtered candidates, compacted in gid order
@@ -591,8 +657,10 @@ extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg
               out->overlap_home, out->overlap_rel);
   // 6. induced-subgraph edges in original order
   if (E > 0) {
+    HG_LAUNCH("build_member_bits", k_member_bits, dim3(gB), dim3(kBT), 0, s, (const int32_t*)out->global2local,
+              N, w.mbits);
     HG_LAUNCH("build_edge_keep", k_edge_keep, dim3(gE), dim3(kBT), 0, s, g->src, g->dst,
-              (const int32_t*)out->global2local, E, w.keep);
+              (const uint32_t*)w.mbits, E, w.keep);
     HG_TRY(scan_exclusive_i32(w.keep, w.keep, E, w.cnt + C_ESUB, w.scratch, s));
     HG_LAUNCH("build_edge_compact", k_edge_compact, dim3(gE), dim3(kBT), 0, s, g->src, g->dst, g->rel,
               (const int32_t*)out->global2local, (const int32_t*)w.keep, E, (int32_t)R, w.kcsr,

@@ -7,7 +7,7 @@
 //   (b) SpMM             z_j = Y_self[j] + sum_{edges i->j of relation r} Y[i*R+r] / deg_r(j)
 //                        h'_j = ReLU(z_j) + h_j, ReLU mask saved as bits
 // Backward:
-//   dZ = G * mask
+//   dZ = G * mask, formed while the dX self-transform loads G (and written out)
 //   (b) transposed SpMM  dY[i*R + r] = sum_{edges i->j of r} csc_scale * dZ_j  (no atomics;
 //                        rows longer than the chunk size are split, then summed in order)
 //   (c) MFMA             dH = G + dZ W_self^T, then dH[S_r] += dY_r W_r^T for r = 0..R-1
@@ -115,32 +115,13 @@ __global__ void __launch_bounds__(256) k_spmm_fwd(int64_t n_sub, int32_t R, cons
   }
 }
 
-// dZ = G * mask
-template <int D>
-__global__ void k_relu_grad(int64_t n_sub, const float* __restrict__ G, const uint32_t* __restrict__ mask,
-                            float* __restrict__ dZ) {
-  constexpr int C4 = D / 4;
-  const int64_t total = n_sub * C4;
-  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < total;
-       t += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t j = t / C4;
-    const int c4 = (int)(t % C4);
-    const uint32_t nib = (mask[j * (D / 32) + (c4 >> 3)] >> (4 * (c4 & 7))) & 0xFu;
-    f32x4 g = *reinterpret_cast<const f32x4*>(G + j * D + 4 * c4);
-#pragma unroll
-    for (int q = 0; q < 4; ++q)
-      if (!((nib >> q) & 1u)) g[q] = 0.f;
-    *reinterpret_cast<f32x4*>(dZ + j * D + 4 * c4) = g;
-  }
-}
-
 // ---- backward transposed SpMM over the CSC work items ---------------------------
 template <int D>
 __global__ void __launch_bounds__(256) k_spmm_bwd(int64_t n_items, const int4* __restrict__ items,
                                                   const int32_t* __restrict__ csc_row,
                                                   const float* __restrict__ csc_scale,
-                                                  const float* __restrict__ dZ, float* __restrict__ dY,
-                                                  float* __restrict__ partial) {
+                                                  const float* __restrict__ dZ,
+                                                  float* __restrict__ dY, float* __restrict__ partial) {
   constexpr int LPR = D / 4;
   constexpr int EPW = 64 / LPR;
   constexpr int U = 4;
@@ -304,11 +285,13 @@ int layer_bwd_impl(const hg_subgraph* s, const hg_layer_desc* L, const float* Hi
   if (!a.ok()) return fail(HG_ERR_CAPACITY, "backward workspace needs %zu bytes, got %zu", a.used, ws_bytes);
   const int32_t R = s->n_rel;
   const PlanView pv = plan_view(s);
-  const int64_t ns = s->n_sub;
-  if (ns > 0) {
-    const int64_t n4 = ns * (D / 4);
-    HG_LAUNCH("relu_grad", k_relu_grad<D>, dim3((unsigned)(cdiv(n4, 256) < 65536 ? cdiv(n4, 256) : 65536)),
-              dim3(256), 0, st, ns, G, mask, w.dZ);
+  // (c) dH = G (residual) + dZ W_self^T per type; the A-operand load forms
+  // dZ = G * mask and also writes it out for the SpMM and dW_self
+  for (int t = 0; t < s->n_ntype; ++t) {
+    const int64_t lo = s->type_off_host[t], hi = s->type_off_host[t + 1];
+    LoadMasked<D> la{G, mask, rows_contig(lo), w.dZ};
+    StoreRows<D> ep{dHin, rows_contig(lo), nullptr, L->residual ? G : nullptr};
+    HG_TRY((launch_gemm_rows<D, true>("gemm_bwd_dx_self", hi - lo, W_self + (int64_t)t * D * D, la, ep, st)));
   }
   // (b) transposed SpMM
   if (s->plan_items > 0)
@@ -318,16 +301,7 @@ int layer_bwd_impl(const hg_subgraph* s, const hg_layer_desc* L, const float* Hi
   if (s->plan_heavy > 0)
     HG_LAUNCH("spmm_bwd_reduce", k_heavy_reduce<D>, dim3(wave_grid(s->plan_heavy)), dim3(256), 0, st,
               (int64_t)s->plan_heavy, pv.heavy, (const float*)w.part, w.dY);
-  // (c) dH = G (residual) + dZ W_self^T per type, then += dY_r W_r^T per relation in order
-  for (int t = 0; t < s->n_ntype; ++t) {
-    const int64_t lo = s->type_off_host[t], hi = s->type_off_host[t + 1];
-    LoadRows<D> la{w.dZ, rows_contig(lo)};
-    StoreRows<D> ep{dHin, rows_contig(lo), nullptr, L->residual ? G : nullptr};
-    HG_TRY((launch_gemm_rows<D, true>("gemm_bwd_dx_self", hi - lo, W_self + (int64_t)t * D * D, la, ep, st)));
-    if (!L->residual && hi > lo) {
-      // nothing else to add
-    }
-  }
+  // (c) dH += dY_r W_r^T per relation, in relation order
   int64_t off = 0;
   for (int r = 0; r < R; ++r) {
     const int64_t n = s->n_active[r];

@@ -43,15 +43,18 @@ inline RowMap rows_list(const int32_t* list, int32_t mul = 1, int32_t add = 0) {
   return RowMap{list, 0, mul, add};
 }
 
-// ---- A loaders: return 4 consecutive columns [c, c+4) of segment row i ----
+// ---- A loaders: rowp(i) = address of segment row i; load4 / load1 read
+// columns of that row (with an optional per-column transform) ------------------
 template <int D>
 struct LoadRows {
   const float* base;
   RowMap map;
-  __device__ __forceinline__ f32x4 row4(int64_t i, int c) const {
-    return *reinterpret_cast<const f32x4*>(base + map(i) * D + c);
+  __device__ __forceinline__ const float* rowp(int64_t i) const { return base + map(i) * D; }
+  __device__ __forceinline__ f32x4 load4(const float* p, int c) const {
+    return *reinterpret_cast<const f32x4*>(p + c);
   }
-  __device__ __forceinline__ float at(int64_t i, int c) const { return base[map(i) * D + c]; }
+  __device__ __forceinline__ float load1(const float* p, int c) const { return p[c]; }
+  __device__ __forceinline__ float at(int64_t i, int c) const { return rowp(i)[c]; }
 };
 
 // (x - mu[c]) * sc[c]: the per-column standardisation of the alignment loss.
@@ -61,43 +64,89 @@ struct LoadStd {
   RowMap map;
   const float* mu;
   const float* sc;
-  __device__ __forceinline__ f32x4 row4(int64_t i, int c) const {
-    f32x4 x = *reinterpret_cast<const f32x4*>(base + map(i) * D + c);
+  __device__ __forceinline__ const float* rowp(int64_t i) const { return base + map(i) * D; }
+  __device__ __forceinline__ f32x4 load4(const float* p, int c) const {
+    f32x4 x = *reinterpret_cast<const f32x4*>(p + c);
     f32x4 m = *reinterpret_cast<const f32x4*>(mu + c);
     f32x4 s = *reinterpret_cast<const f32x4*>(sc + c);
-    return (x - m) * s;
+    f32x4 r;
+    r[0] = (x[0] - m[0]) * s[0];
+    r[1] = (x[1] - m[1]) * s[1];
+    r[2] = (x[2] - m[2]) * s[2];
+    r[3] = (x[3] - m[3]) * s[3];
+    return r;
   }
-  __device__ __forceinline__ float at(int64_t i, int c) const {
-    return (base[map(i) * D + c] - mu[c]) * sc[c];
-  }
+  __device__ __forceinline__ float load1(const float* p, int c) const { return (p[c] - mu[c]) * sc[c]; }
+  __device__ __forceinline__ float at(int64_t i, int c) const { return load1(rowp(i), c); }
 };
 
-// ---- epilogue: out[row] = acc + bias + addend[row] --------------------------
+// dZ = G * mask read on the fly: the ReLU mask row of G row r holds bit c of
+// column c at word r*(D/32) + c/32.
+template <int D>
+struct LoadMasked {
+  const float* G;
+  const uint32_t* mask;
+  RowMap map;
+  float* tee;  // if set, load4 also stores the masked values here (same offsets as G)
+  __device__ __forceinline__ const float* rowp(int64_t i) const { return G + map(i) * D; }
+  __device__ __forceinline__ uint32_t word(const float* p, int c) const {
+    const int64_t r = (p - G) / D;
+    return mask[r * (D / 32) + (c >> 5)];
+  }
+  __device__ __forceinline__ f32x4 load4(const float* p, int c) const {
+    f32x4 x = *reinterpret_cast<const f32x4*>(p + c);
+    const uint32_t nib = word(p, c) >> (c & 31);
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      if (!((nib >> q) & 1u)) x[q] = 0.f;
+    if (tee) *reinterpret_cast<f32x4*>(tee + (p - G) + c) = x;
+    return x;
+  }
+  __device__ __forceinline__ float load1(const float* p, int c) const {
+    return ((word(p, c) >> (c & 31)) & 1u) ? p[c] : 0.f;
+  }
+  __device__ __forceinline__ float at(int64_t i, int c) const { return load1(rowp(i), c); }
+};
+
+// ---- epilogues ------------------------------------------------------------
+// The kernel calls row(i) once per output row, then pre(i, ro, c) for every
+// element of the tile (all loads), then store(i, ro, c, acc, pre) (all stores):
+// the two phases keep loads from waiting behind stores when the addend is the
+// output itself (dH += ...).
 template <int D>
 struct StoreRows {
   float* out;
   RowMap map;
   const float* bias;    // [D] or null
   const float* addend;  // rows through the same map, or null (may equal out)
-  __device__ __forceinline__ void operator()(int64_t i, int c, float v) const {
-    const int64_t o = map(i) * D + c;
-    if (bias) v += bias[c];
-    if (addend) v += addend[o];
-    out[o] = v;
+  __device__ __forceinline__ int64_t row(int64_t i) const { return map(i); }
+  __device__ __forceinline__ float pre(int64_t, int64_t ro, int c) const {
+    float v = bias ? bias[c] : 0.f;
+    if (addend) v += addend[ro * D + c];
+    return v;
+  }
+  __device__ __forceinline__ void store(int64_t, int64_t ro, int c, float acc, float pre) const {
+    out[ro * D + c] = acc + pre;
   }
 };
 
 // ---- gemm_rows --------------------------------------------------------------
-// Block = 4 waves, tile = 64 rows (16 per wave); persistent over tiles.
-// LDS holds op(W) in fragment order: element ((kb*NB + nb)*64 + lane)*4 + s is
-// op(W)[16 kb + 4 (lane/16) + s][16 nb + lane%16].
+// Block = 8 waves sharing one LDS copy of op(W); a wave owns 16 rows, a block
+// 128 rows; persistent over tiles.  About 100 registers per lane keep four
+// waves per SIMD resident, which hides the A-row loads behind other waves'
+// MFMAs.  LDS holds op(W) in fragment order: f32x4 element (kb*NB + nb)*64 +
+// lane is op(W)[16 kb + 4 (lane/16) + s][16 nb + lane%16], s = 0..3.
+constexpr int kGemmThreads = 512;
+
 template <int D, bool kTransW, class ALoad, class Epi>
-__global__ void __launch_bounds__(256) k_gemm_rows(int64_t n_rows, const float* __restrict__ W,
-                                                   ALoad aload, Epi epi) {
+__global__ void __launch_bounds__(kGemmThreads) k_gemm_rows(int64_t n_rows, const float* __restrict__ W,
+                                                            ALoad aload, Epi epi) {
   constexpr int NB = D / 16;
+  constexpr int kWavesPerBlock = kGemmThreads / 64;
+  constexpr int kRowsPerTile = 16 * kWavesPerBlock;
   extern __shared__ f32x4 wl[];
   const int tid = threadIdx.x;
-  for (int e = tid; e < NB * NB * 64; e += 256) {
+  for (int e = tid; e < NB * NB * 64; e += kGemmThreads) {
     const int l = e & 63;
     const int nb = (e >> 6) % NB;
     const int kb = (e >> 6) / NB;
@@ -118,17 +167,19 @@ __global__ void __launch_bounds__(256) k_gemm_rows(int64_t n_rows, const float* 
   const int w = tid >> 6;
   const int l = lane64();
   const int g = l >> 4, c = l & 15;
-  const int64_t ntiles = (n_rows + 63) / 64;
+  const int64_t ntiles = (n_rows + kRowsPerTile - 1) / kRowsPerTile;
   for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
-    const int64_t r0 = t * 64 + 16 * w;
-    const int64_t ia = r0 + c;
+    const int64_t r0 = t * kRowsPerTile + 16 * w;
     f32x4 a[NB];
-#pragma unroll
-    for (int kb = 0; kb < NB; ++kb) {
+    {
+      const int64_t ia = r0 + c;
       if (ia < n_rows) {
-        a[kb] = aload.row4(ia, 16 * kb + 4 * g);
+        const float* p = aload.rowp(ia);
+#pragma unroll
+        for (int kb = 0; kb < NB; ++kb) a[kb] = aload.load4(p, 16 * kb + 4 * g);
       } else {
-        a[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kb = 0; kb < NB; ++kb) a[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
       }
     }
     f32x4 acc[NB];
@@ -136,21 +187,33 @@ __global__ void __launch_bounds__(256) k_gemm_rows(int64_t n_rows, const float* 
     for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kb = 0; kb < NB; ++kb) {
+      // keep each K block's B fragments local (no hoisting of all LDS reads)
+      __builtin_amdgcn_sched_barrier(0);
+      f32x4 b[NB];
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
-        const f32x4 b = wl[(kb * NB + nb) * 64 + l];
-        acc[nb] = mfma4(a[kb][0], b[0], acc[nb]);
-        acc[nb] = mfma4(a[kb][1], b[1], acc[nb]);
-        acc[nb] = mfma4(a[kb][2], b[2], acc[nb]);
-        acc[nb] = mfma4(a[kb][3], b[3], acc[nb]);
-      }
+      for (int nb = 0; nb < NB; ++nb) b[nb] = wl[(kb * NB + nb) * 64 + l];
+#pragma unroll
+      for (int s = 0; s < 4; ++s)
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) acc[nb] = mfma4(a[kb][s], b[nb][s], acc[nb]);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    // epilogue: lane holds rows r0 + 4 g + v, columns 16 nb + c
+    int64_t ro[4];
+    float pre[4][NB];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int64_t i = r0 + 4 * g + v;
+      ro[v] = (i < n_rows) ? epi.row(i) : 0;
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) pre[v][nb] = (i < n_rows) ? epi.pre(i, ro[v], 16 * nb + c) : 0.f;
     }
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
       const int64_t i = r0 + 4 * g + v;
       if (i < n_rows) {
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) epi(i, 16 * nb + c, acc[nb][v]);
+        for (int nb = 0; nb < NB; ++nb) epi.store(i, ro[v], 16 * nb + c, acc[nb][v], pre[v][nb]);
       }
     }
   }
@@ -160,11 +223,11 @@ template <int D, bool kTransW, class ALoad, class Epi>
 int launch_gemm_rows(const char* name, int64_t n_rows, const float* W, ALoad aload, Epi epi,
                      hipStream_t s) {
   if (n_rows <= 0) return HG_OK;
-  const int64_t tiles = cdiv(n_rows, 64);
+  const int64_t tiles = cdiv(n_rows, 16 * (kGemmThreads / 64));
   const int64_t cap = (int64_t)num_cus() * 2;
   const int64_t grid = tiles < cap ? tiles : cap;
   const size_t lds = sizeof(float) * D * D;
-  HG_LAUNCH(name, (k_gemm_rows<D, kTransW, ALoad, Epi>), dim3((unsigned)grid), dim3(256), lds, s,
+  HG_LAUNCH(name, (k_gemm_rows<D, kTransW, ALoad, Epi>), dim3((unsigned)grid), dim3(kGemmThreads), lds, s,
             n_rows, W, aload, epi);
   return HG_OK;
 }
@@ -172,15 +235,20 @@ int launch_gemm_rows(const char* name, int64_t n_rows, const float* W, ALoad alo
 // ---- gemm_tn split-K ----------------------------------------------------------
 // partial[chunk][i][j] = sum_{rows k of the chunk} A[k][i] * B[k][j]
 // colsum[chunk][j]    = sum_{rows k of the chunk} B[k][j]        (if colsum)
-// D = 128: wave w owns the 64 x 64 quadrant (w/2, w%2) over all rows of the
-// chunk.  D = 64: every wave owns the whole 64 x 64 output over every fourth
-// group of 4 rows; the four waves are summed in LDS in wave order.
+// A wave owns a 64 x 64 block of the output (D = 128: wave w takes quadrant
+// (w/2, w%2) over every row of the chunk; D = 64: every wave takes the whole
+// output over every fourth group of 4 rows, and the waves are summed in LDS
+// in wave order).  Lane (c, g) reads one float4 of A and of B per row
+// (features q0 + 4c .. 4c+3) and feeds component b of it to MFMA block b, so
+// block b, MFMA index c stands for feature q0 + 4c + b: in the output, the
+// lane's register v of block (bi, bj) is element [4 (4 g + v) + bi][4 c + bj].
 template <int D, class LA, class LB>
 __global__ void __launch_bounds__(256) k_gemm_tn(int64_t n_rows, int64_t kc, LA la, LB lb,
                                                  float* __restrict__ partial,
                                                  float* __restrict__ colsum) {
   static_assert(D == 64 || D == 128, "gemm_tn: d must be 64 or 128");
   constexpr bool kQuad = (D == 128);
+  constexpr int U = 4;
   const int w = threadIdx.x >> 6;
   const int l = lane64();
   const int g = l >> 4, c = l & 15;
@@ -191,33 +259,33 @@ __global__ void __launch_bounds__(256) k_gemm_tn(int64_t n_rows, int64_t kc, LA 
   const int qj = kQuad ? (w & 1) : 0;
   const int64_t step0 = kQuad ? 0 : 4 * w;
   const int64_t stride = kQuad ? 4 : 16;
+  const int ca = 64 * qi + 4 * c, cb = 64 * qj + 4 * c;
   f32x4 acc[4][4];
-  float bs[4];
+  f32x4 bs = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int bi = 0; bi < 4; ++bi) {
-    bs[bi] = 0.f;
+  for (int bi = 0; bi < 4; ++bi)
 #pragma unroll
     for (int bj = 0; bj < 4; ++bj) acc[bi][bj] = f32x4{0.f, 0.f, 0.f, 0.f};
-  }
-  for (int64_t k0 = k_beg + step0; k0 < k_end; k0 += stride) {
-    const int64_t row = k0 + g;
-    float a[4], b[4];
-    if (row < k_end) {
+  for (int64_t k0 = k_beg + step0; k0 < k_end; k0 += stride * U) {
+    f32x4 a[U], b[U];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        a[q] = la.at(row, 64 * qi + 16 * q + c);
-        b[q] = lb.at(row, 64 * qj + 16 * q + c);
+    for (int u = 0; u < U; ++u) {
+      const int64_t row = k0 + u * stride + g;
+      if (row < k_end) {
+        a[u] = la.load4(la.rowp(row), ca);
+        b[u] = lb.load4(lb.rowp(row), cb);
+      } else {
+        a[u] = b[u] = f32x4{0.f, 0.f, 0.f, 0.f};
       }
-    } else {
-#pragma unroll
-      for (int q = 0; q < 4; ++q) a[q] = b[q] = 0.f;
     }
 #pragma unroll
-    for (int q = 0; q < 4; ++q) bs[q] += b[q];
+    for (int u = 0; u < U; ++u) {
+      bs += b[u];
 #pragma unroll
-    for (int bi = 0; bi < 4; ++bi)
+      for (int bi = 0; bi < 4; ++bi)
 #pragma unroll
-      for (int bj = 0; bj < 4; ++bj) acc[bi][bj] = mfma4(a[bi], b[bj], acc[bi][bj]);
+        for (int bj = 0; bj < 4; ++bj) acc[bi][bj] = mfma4(a[u][bi], b[u][bj], acc[bi][bj]);
+    }
   }
   // column sums: reduce the 4 row groups of the wave
 #pragma unroll
@@ -230,14 +298,14 @@ __global__ void __launch_bounds__(256) k_gemm_tn(int64_t n_rows, int64_t kc, LA 
 #pragma unroll
     for (int bi = 0; bi < 4; ++bi)
 #pragma unroll
-      for (int bj = 0; bj < 4; ++bj)
+      for (int v = 0; v < 4; ++v) {
+        const int64_t i = 64 * qi + 4 * (4 * g + v) + bi;
+        f32x4 row4;
 #pragma unroll
-        for (int v = 0; v < 4; ++v)
-          out[(int64_t)(64 * qi + 16 * bi + 4 * g + v) * D + 64 * qj + 16 * bj + c] = acc[bi][bj][v];
-    if (colsum && qi == 0 && g == 0) {
-#pragma unroll
-      for (int q = 0; q < 4; ++q) colsum[chunk * D + 64 * qj + 16 * q + c] = bs[q];
-    }
+        for (int bj = 0; bj < 4; ++bj) row4[bj] = acc[bi][bj][v];
+        *reinterpret_cast<f32x4*>(out + i * D + cb) = row4;
+      }
+    if (colsum && qi == 0 && g == 0) *reinterpret_cast<f32x4*>(colsum + chunk * D + cb) = bs;
   } else {
     __shared__ float red[64 * 64];
     __shared__ float cred[64];
@@ -246,15 +314,15 @@ __global__ void __launch_bounds__(256) k_gemm_tn(int64_t n_rows, int64_t kc, LA 
 #pragma unroll
         for (int bi = 0; bi < 4; ++bi)
 #pragma unroll
-          for (int bj = 0; bj < 4; ++bj)
+          for (int v = 0; v < 4; ++v)
 #pragma unroll
-            for (int v = 0; v < 4; ++v) {
-              const int idx = (16 * bi + 4 * g + v) * 64 + 16 * bj + c;
+            for (int bj = 0; bj < 4; ++bj) {
+              const int idx = (4 * (4 * g + v) + bi) * 64 + 4 * c + bj;
               red[idx] = (ww == 0 ? 0.f : red[idx]) + acc[bi][bj][v];
             }
         if (g == 0) {
 #pragma unroll
-          for (int q = 0; q < 4; ++q) cred[16 * q + c] = (ww == 0 ? 0.f : cred[16 * q + c]) + bs[q];
+          for (int q = 0; q < 4; ++q) cred[4 * c + q] = (ww == 0 ? 0.f : cred[4 * c + q]) + bs[q];
         }
       }
       __syncthreads();
@@ -262,6 +330,23 @@ __global__ void __launch_bounds__(256) k_gemm_tn(int64_t n_rows, int64_t kc, LA 
     for (int e = threadIdx.x; e < 64 * 64; e += 256) out[e] = red[e];
     if (colsum && threadIdx.x < 64) colsum[chunk * D + threadIdx.x] = cred[threadIdx.x];
   }
+}
+
+// Fixed-order reduction of nchunks partial arrays of n floats, in two stages:
+// group g sums chunks [g*per, (g+1)*per) in order into tmp[g], then the groups
+// are summed in order: out[i] (+)= sum_g tmp[g][i].
+constexpr int kSplitGroups = 16;
+
+static __global__ void k_sum_partials_grouped(const float* __restrict__ partial, int64_t nchunks,
+                                              int64_t n, int64_t per, float* __restrict__ tmp) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t grp = blockIdx.y;
+  if (i >= n) return;
+  const int64_t c0 = grp * per;
+  const int64_t c1 = (c0 + per < nchunks) ? c0 + per : nchunks;
+  float s = 0.f;
+  for (int64_t c = c0; c < c1; ++c) s += partial[c * n + i];
+  tmp[grp * n + i] = s;
 }
 
 // out[i] (+)= sum_{c < nchunks} partial[c][i]   (fixed order)
@@ -281,10 +366,28 @@ inline int64_t splitk_chunk(int64_t n) {
   if (chunks > cap) chunks = cap;
   if (chunks < 1) chunks = 1;
   int64_t kc = cdiv(n, chunks);
-  kc = cdiv(kc, 16) * 16;
-  return kc > 16 ? kc : 16;
+  kc = cdiv(kc, 64) * 64;
+  return kc > 64 ? kc : 64;
 }
-inline int64_t splitk_max_chunks() { return (int64_t)num_cus() * 4 + 1; }
+inline int64_t splitk_max_chunks() { return (int64_t)num_cus() * 4 + kSplitGroups + 1; }
+
+// partial must hold splitk_max_chunks() * D * D floats: the grouped stage
+// writes its kSplitGroups rows after the chunk rows.
+inline int reduce_partials(const float* partial, int64_t chunks, int64_t n, float* tmp, float* out,
+                           int accumulate, hipStream_t s) {
+  if (chunks <= 2 * kSplitGroups) {
+    HG_LAUNCH("splitk_reduce", k_sum_partials, dim3((unsigned)cdiv(n, 256)), dim3(256), 0, s, partial,
+              chunks, n, out, accumulate);
+    return HG_OK;
+  }
+  const int64_t per = cdiv(chunks, kSplitGroups);
+  const int64_t groups = cdiv(chunks, per);
+  HG_LAUNCH("splitk_reduce", k_sum_partials_grouped, dim3((unsigned)cdiv(n, 256), (unsigned)groups), dim3(256),
+            0, s, partial, chunks, n, per, tmp);
+  HG_LAUNCH("splitk_reduce", k_sum_partials, dim3((unsigned)cdiv(n, 256)), dim3(256), 0, s, (const float*)tmp,
+            groups, n, out, accumulate);
+  return HG_OK;
+}
 
 template <int D, class LA, class LB>
 int launch_gemm_tn(const char* name, int64_t n_rows, LA la, LB lb, float* partial, float* colsum,
@@ -300,11 +403,10 @@ int launch_gemm_tn(const char* name, int64_t n_rows, LA la, LB lb, float* partia
   const int64_t chunks = cdiv(n_rows, kc);
   HG_LAUNCH(name, (k_gemm_tn<D, LA, LB>), dim3((unsigned)chunks), dim3(256), 0, s, n_rows, kc, la,
             lb, partial, out_colsum ? colsum : nullptr);
-  HG_LAUNCH("splitk_reduce", k_sum_partials, dim3((unsigned)cdiv((int64_t)D * D, 256)), dim3(256), 0, s,
-            (const float*)partial, chunks, (int64_t)D * D, out, accumulate);
+  const int64_t cap = (int64_t)num_cus() * 4 + 1;
+  HG_TRY(reduce_partials(partial, chunks, (int64_t)D * D, partial + cap * D * D, out, accumulate, s));
   if (out_colsum)
-    HG_LAUNCH("splitk_reduce", k_sum_partials, dim3(1), dim3(256), 0, s, (const float*)colsum, chunks,
-              (int64_t)D, out_colsum, accumulate);
+    HG_TRY(reduce_partials(colsum, chunks, (int64_t)D, colsum + cap * D, out_colsum, accumulate, s));
   return HG_OK;
 }
 

@@ -116,24 +116,39 @@ __global__ void k_radix_upsweep(const uint32_t* __restrict__ keys, const uint8_t
   hist[(int64_t)threadIdx.x * ntiles + blockIdx.x] = cnt[threadIdx.x];
 }
 
-// Stable scatter of one tile.  Items are visited in 16 rounds of 256
-// consecutive items; inside a round the order is (wave, lane).  An item's
-// destination is the tile's global offset for its digit plus the number of
-// earlier items of the tile with the same digit.
-template <bool kDigitArray, bool kHasV1, bool kHasV2>
-__global__ void k_radix_downsweep(const uint32_t* __restrict__ keys, const uint8_t* __restrict__ digits,
-                                  const int32_t* __restrict__ v1, const int32_t* __restrict__ v2,
-                                  int64_t n, int shift, uint32_t dmask,
-                                  const int32_t* __restrict__ offs, int64_t ntiles,
-                                  uint32_t* __restrict__ keys_out, int32_t* __restrict__ v1_out,
-                                  int32_t* __restrict__ v2_out) {
-  __shared__ int base_d[256];
+// Stable scatter of one tile, staged through LDS.  Items are visited in 16
+// rounds of 256 consecutive items, inside a round in (wave, lane) order; an
+// item's tile-local rank among equal digits gives its slot in an LDS copy of
+// the tile sorted by digit, which is then written out in slot order, so each
+// digit's run of the tile lands in consecutive global addresses.
+// offs is the digit-major exclusive scan of the per-tile counts with the
+// grand total at offs[256 * ntiles].
+template <bool kDigitArray, bool kHasV2>
+__global__ void __launch_bounds__(256) k_radix_downsweep(
+    const uint32_t* __restrict__ keys, const uint8_t* __restrict__ digits,
+    const int32_t* __restrict__ v1, const int32_t* __restrict__ v2, int64_t n, int shift, uint32_t dmask,
+    const int32_t* __restrict__ offs, int64_t ntiles, uint32_t* __restrict__ keys_out,
+    int32_t* __restrict__ v1_out, int32_t* __restrict__ v2_out) {
+  __shared__ int gbase[256];
+  __shared__ int loff[256];
+  __shared__ int run[256];
   __shared__ int wcnt[kWaves][256];
   __shared__ int wpre[kWaves][256];
+  __shared__ uint32_t sk[kDigitArray ? 1 : kTile];
+  __shared__ int32_t sv1[kTile];
+  __shared__ int32_t sv2[kHasV2 ? kTile : 1];
+  __shared__ uint8_t sd[kTile];
   const int t = threadIdx.x;
   const int w = t / kWave;
   const int l = lane_id();
-  base_d[t] = offs[(int64_t)t * ntiles + blockIdx.x];
+  const int64_t fi = (int64_t)t * ntiles + blockIdx.x;
+  const int base = offs[fi];
+  const int cnt = offs[fi + 1] - base;
+  gbase[t] = base;
+  int kept;
+  const int lo = block_excl_scan(cnt, &kept);
+  loff[t] = lo;
+  run[t] = lo;
 #pragma unroll
   for (int i = 0; i < kWaves; ++i) wcnt[i][t] = 0;
   __syncthreads();
@@ -166,22 +181,31 @@ __global__ void k_radix_downsweep(const uint32_t* __restrict__ keys, const uint8
     }
     __syncthreads();
     {
-      int run = base_d[t];
+      int r = run[t];
 #pragma unroll
       for (int q = 0; q < kWaves; ++q) {
-        wpre[q][t] = run;
-        run += wcnt[q][t];
+        wpre[q][t] = r;
+        r += wcnt[q][t];
         wcnt[q][t] = 0;
       }
-      base_d[t] = run;
+      run[t] = r;
     }
     __syncthreads();
     if (valid) {
-      const int pos = wpre[w][d] + rank;
-      if (!kDigitArray) keys_out[pos] = k;
-      if (kHasV1) v1_out[pos] = v1[i];
-      if (kHasV2) v2_out[pos] = v2[i];
+      const int lpos = wpre[w][d] + rank;
+      if (!kDigitArray) sk[lpos] = k;
+      sv1[lpos] = v1[i];
+      if (kHasV2) sv2[lpos] = v2[i];
+      sd[lpos] = (uint8_t)d;
     }
+  }
+  __syncthreads();
+  for (int idx = t; idx < kept; idx += kThreads) {
+    const int d = sd[idx];
+    const int pos = gbase[d] + (idx - loff[d]);
+    if (!kDigitArray) keys_out[pos] = sk[idx];
+    v1_out[pos] = sv1[idx];
+    if (kHasV2) v2_out[pos] = sv2[idx];
   }
 }
 
@@ -229,7 +253,7 @@ int scan_exclusive_i32(const int32_t* in, int32_t* out, int64_t n, int32_t* tota
 int64_t radix_scratch_elems(int64_t n) {
   const int64_t tiles = cdiv(n > 0 ? n : 1, kTile);
   const int64_t h = 256 * tiles;
-  return h + scan_scratch_elems(h) + 64;
+  return h + 1 + scan_scratch_elems(h) + 64;
 }
 
 int radix_sort_pairs(uint32_t* keys, uint32_t* keys_alt, int32_t* v1, int32_t* v1_alt,
@@ -241,7 +265,7 @@ int radix_sort_pairs(uint32_t* keys, uint32_t* keys_alt, int32_t* v1, int32_t* v
   if (n <= 0 || bits <= 0) return HG_OK;
   const int64_t tiles = cdiv(n, kTile);
   int32_t* hist = scratch;
-  int32_t* sscr = scratch + 256 * tiles;
+  int32_t* sscr = scratch + 256 * tiles + 1;
   uint32_t *ka = keys, *kb = keys_alt;
   int32_t *a1 = v1, *b1 = v1_alt, *a2 = v2, *b2 = v2_alt;
   for (int shift = 0; shift < bits; shift += 8) {
@@ -249,14 +273,14 @@ int radix_sort_pairs(uint32_t* keys, uint32_t* keys_alt, int32_t* v1, int32_t* v
     const uint32_t dmask = (1u << nb) - 1u;
     HG_LAUNCH("radix_upsweep", (k_radix_upsweep<false>), dim3((unsigned)tiles), dim3(kThreads), 0, s,
               (const uint32_t*)ka, (const uint8_t*)nullptr, n, shift, dmask, hist, tiles);
-    HG_TRY(scan_exclusive_i32(hist, hist, 256 * tiles, nullptr, sscr, s));
+    HG_TRY(scan_exclusive_i32(hist, hist, 256 * tiles, hist + 256 * tiles, sscr, s));
     if (v2) {
-      HG_LAUNCH("radix_downsweep", (k_radix_downsweep<false, true, true>), dim3((unsigned)tiles),
+      HG_LAUNCH("radix_downsweep", (k_radix_downsweep<false, true>), dim3((unsigned)tiles),
                 dim3(kThreads), 0, s, (const uint32_t*)ka, (const uint8_t*)nullptr,
                 (const int32_t*)a1, (const int32_t*)a2, n, shift, dmask, (const int32_t*)hist,
                 tiles, kb, b1, b2);
     } else {
-      HG_LAUNCH("radix_downsweep", (k_radix_downsweep<false, true, false>), dim3((unsigned)tiles),
+      HG_LAUNCH("radix_downsweep", (k_radix_downsweep<false, false>), dim3((unsigned)tiles),
                 dim3(kThreads), 0, s, (const uint32_t*)ka, (const uint8_t*)nullptr,
                 (const int32_t*)a1, (const int32_t*)nullptr, n, shift, dmask,
                 (const int32_t*)hist, tiles, kb, b1, (int32_t*)nullptr);
@@ -277,12 +301,12 @@ int bucket_partition(const uint8_t* digit, const int32_t* val, int64_t n, int nb
   if (n <= 0) return fill_i32(bin_off, 0, nbins + 1, s);
   const int64_t tiles = cdiv(n, kTile);
   int32_t* hist = scratch;
-  int32_t* sscr = scratch + 256 * tiles;
-  int32_t* total = sscr + scan_scratch_elems(256 * tiles);
+  int32_t* sscr = scratch + 256 * tiles + 1;
+  int32_t* total = hist + 256 * tiles;
   HG_LAUNCH("partition_upsweep", (k_radix_upsweep<true>), dim3((unsigned)tiles), dim3(kThreads), 0, s,
             (const uint32_t*)nullptr, digit, n, 0, 0xFFu, hist, tiles);
   HG_TRY(scan_exclusive_i32(hist, hist, 256 * tiles, total, sscr, s));
-  HG_LAUNCH("partition_downsweep", (k_radix_downsweep<true, true, false>), dim3((unsigned)tiles),
+  HG_LAUNCH("partition_downsweep", (k_radix_downsweep<true, false>), dim3((unsigned)tiles),
             dim3(kThreads), 0, s, (const uint32_t*)nullptr, digit, val, (const int32_t*)nullptr, n,
             0, 0xFFu, (const int32_t*)hist, tiles, (uint32_t*)nullptr, out, (int32_t*)nullptr);
   HG_LAUNCH("partition_offsets", k_bin_offsets, dim3(1), dim3(256), 0, s, (const int32_t*)hist,

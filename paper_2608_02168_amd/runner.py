@@ -59,7 +59,8 @@ def make_inputs(wl: synth.Workload, g: synth.Graph, device="cuda", feats: Option
     d = mc.d
     gd = {k: _dev(getattr(g, k), device) for k in ("src", "dst", "rel", "ntype", "part")}
     sub = api.hg_build_csr(gd["src"], gd["dst"], gd["rel"], gd["ntype"], gd["part"], g.k, cfg.n_rel,
-                           g.n_ntype, cfg.budget, key=cfg.key, theta=cfg.theta, seed=cfg.seed)
+                           g.n_ntype, cfg.budget, key=cfg.key, theta=cfg.theta, seed=cfg.seed,
+                           want_eid=False)
     build_ws = sub.arrays["ws"]
     feats = synth.features(mc.seed, g.n_nodes, d) if feats is None else feats
     l2g = sub.view("local2global").long()
