@@ -36,11 +36,9 @@ def algorithmic_cost(kind: str, info: dict):
         # R+1 row pointers, Y_self and H_in rows read, H_out row and d/8 mask bytes written
         return E * (d * s + 4) + N * (4 * (R + 1) + 3 * d * s + d / 8), 2.0 * E * d
     if kind == "spmm_bwd":
-        # per edge: one gathered row of the upstream gradient G with its d/8
-        # ReLU-mask bytes (dZ = G * mask is formed while gathering), the
-        # destination id and scale; per work item 16 bytes; per active row one
-        # dY row written
-        return E * (d * s + d / 8 + 8) + A * (d * s + 16), 2.0 * E * d
+        # per edge: one gathered dZ row, destination id and scale; per work
+        # item 16 bytes; per active row one dY row written
+        return E * (d * s + 8) + A * (d * s + 16), 2.0 * E * d
     raise KeyError(kind)
 
 
