@@ -116,12 +116,15 @@ __global__ void __launch_bounds__(256) k_spmm_fwd(int64_t n_sub, int32_t R, cons
 }
 
 // ---- backward transposed SpMM over the CSC work items ---------------------------
+// CSC rows of hub sources hold up to millions of entries, so each lane
+// accumulates in float64 (the kernel is bound by the gathers, not the adds);
+// split rows keep float64 partial rows.
 template <int D>
 __global__ void __launch_bounds__(256) k_spmm_bwd(int64_t n_items, const int4* __restrict__ items,
                                                   const int32_t* __restrict__ csc_row,
                                                   const float* __restrict__ csc_scale,
                                                   const float* __restrict__ dZ,
-                                                  float* __restrict__ dY, float* __restrict__ partial) {
+                                                  float* __restrict__ dY, double* __restrict__ partial) {
   constexpr int LPR = D / 4;
   constexpr int EPW = 64 / LPR;
   constexpr int U = 4;
@@ -133,7 +136,7 @@ __global__ void __launch_bounds__(256) k_spmm_bwd(int64_t n_items, const int4* _
   for (int64_t it = wave0; it < n_items; it += nwaves) {
     const int4 item = items[it];
     const int32_t beg = item.y, end = item.z;
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    f64x4 acc = {0.0, 0.0, 0.0, 0.0};
     for (int32_t base = beg; base < end; base += 64) {
       const int32_t pos = base + l;
       int32_t dst = 0;
@@ -159,7 +162,9 @@ __global__ void __launch_bounds__(256) k_spmm_bwd(int64_t n_items, const int4* _
           }
         }
 #pragma unroll
-        for (int u = 0; u < U; ++u) acc += ww[u] * v[u];
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) acc[q] += (double)ww[u] * (double)v[u][q];
       }
     }
 #pragma unroll
@@ -170,8 +175,14 @@ __global__ void __launch_bounds__(256) k_spmm_bwd(int64_t n_items, const int4* _
       acc[3] += __shfl_xor(acc[3], o, 64);
     }
     if (slot == 0) {
-      float* out = (item.w < 0) ? dY + (int64_t)item.x * D : partial + (int64_t)item.w * D;
-      *reinterpret_cast<f32x4*>(out + 4 * c4) = acc;
+      if (item.w < 0) {
+        f32x4 o;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) o[q] = (float)acc[q];
+        *reinterpret_cast<f32x4*>(dY + (int64_t)item.x * D + 4 * c4) = o;
+      } else {
+        *reinterpret_cast<f64x4*>(partial + (int64_t)item.w * D + 4 * c4) = acc;
+      }
     }
   }
 }
@@ -179,7 +190,7 @@ __global__ void __launch_bounds__(256) k_spmm_bwd(int64_t n_items, const int4* _
 // Split rows: dY[q] = sum of its partial rows, in chunk order.
 template <int D>
 __global__ void k_heavy_reduce(int64_t n_heavy, const int4* __restrict__ heavy,
-                               const float* __restrict__ partial, float* __restrict__ dY) {
+                               const double* __restrict__ partial, float* __restrict__ dY) {
   constexpr int LPR = D / 4;
   const int l = threadIdx.x & 63;
   const int64_t wave0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
@@ -187,10 +198,16 @@ __global__ void k_heavy_reduce(int64_t n_heavy, const int4* __restrict__ heavy,
   for (int64_t h = wave0; h < n_heavy; h += nwaves) {
     const int4 hv = heavy[h];
     if (l < LPR) {
-      f32x4 s = {0.f, 0.f, 0.f, 0.f};
-      for (int32_t k = 0; k < hv.z; ++k)
-        s += *reinterpret_cast<const f32x4*>(partial + (int64_t)(hv.y + k) * D + 4 * l);
-      *reinterpret_cast<f32x4*>(dY + (int64_t)hv.x * D + 4 * l) = s;
+      f64x4 s = {0.0, 0.0, 0.0, 0.0};
+      for (int32_t k = 0; k < hv.z; ++k) {
+        const f64x4 p = *reinterpret_cast<const f64x4*>(partial + (int64_t)(hv.y + k) * D + 4 * l);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) s[q] += p[q];
+      }
+      f32x4 o;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) o[q] = (float)s[q];
+      *reinterpret_cast<f32x4*>(dY + (int64_t)hv.x * D + 4 * l) = o;
     }
   }
 }
@@ -230,12 +247,13 @@ struct FwdWs {
 
 template <int D>
 struct BwdWs {
-  float *dZ, *dY, *part, *splitk, *colsum;
+  float *dZ, *dY, *splitk, *colsum;
+  double* part;
   template <class A>
   void layout(A& a, const hg_subgraph* s) {
     dZ = a.template take<float>(s->n_sub * (int64_t)D);
     dY = a.template take<float>(s->n_sub * s->n_rel * (int64_t)D);
-    part = a.template take<float>(s->plan_partials * (int64_t)D);
+    part = a.template take<double>(s->plan_partials * (int64_t)D);
     splitk = a.template take<float>(splitk_max_chunks() * (int64_t)D * D);
     colsum = a.template take<float>(splitk_max_chunks() * (int64_t)D);
   }
@@ -300,7 +318,7 @@ int layer_bwd_impl(const hg_subgraph* s, const hg_layer_desc* L, const float* Hi
               (const float*)w.dZ, w.dY, w.part);
   if (s->plan_heavy > 0)
     HG_LAUNCH("spmm_bwd_reduce", k_heavy_reduce<D>, dim3(wave_grid(s->plan_heavy)), dim3(256), 0, st,
-              (int64_t)s->plan_heavy, pv.heavy, (const float*)w.part, w.dY);
+              (int64_t)s->plan_heavy, pv.heavy, (const double*)w.part, w.dY);
   // (c) dH += dY_r W_r^T per relation, in relation order
   int64_t off = 0;
   for (int r = 0; r < R; ++r) {

@@ -1,0 +1,265 @@
+"""Parity at the benchmark's full sizes, in the launch configuration bench.py
+times (same library calls, same workspaces).
+
+The oracle cannot redo a 200M-edge step in float64 within a test, so:
+  * the overlap selection, relabel and counts are recomputed exactly from the
+    oracle's O(E) pieces (keys, candidates, TopM, base edges);
+  * the CSR is pinned by properties that fix it uniquely: every entry's
+    original edge id maps to its row (dst, r) and to its column, rows are in
+    ascending edge id, and every kept edge appears exactly once; the CSC by
+    exact row counts, per-row destination fingerprints and bit-exact
+    csc_scale;
+  * the layer forward on sampled destination rows (plus the heaviest rows),
+    the layer backward on sampled dH rows, computed one by one from the
+    edge list in float64; the alignment on the full overlap batch;
+  * a complete forward/backward (all rows, dW included) on the 1M-node /
+    20M-edge workload, where the oracle runs in seconds.
+"""
+import gc
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+from oracle import align, layer, select, splitmix
+from paper_2608_02168_amd import api, runner, synth
+from tests.helpers import pack_mask, parity_err, to_dev, unpack_mask
+
+pytestmark = pytest.mark.gpu
+TOL = 1e-4
+
+
+def oracle_selection(g):
+    cfg = g.cfg
+    keys = select.node_keys(g.n_nodes, g.src, g.dst, cfg.key)
+    cand = select.candidates(g.part, g.k, g.src, g.dst)
+    sel = select.top_m(cand, keys, cfg.theta, cfg.budget, cfg.seed)
+    first = select.base_edge(g.part, g.k, g.src, g.dst)
+    member = g.part == g.k
+    member[sel] = True
+    ids = np.nonzero(member)[0]
+    l2g = ids[np.lexsort((ids, g.ntype[ids]))]
+    g2l = np.full(g.n_nodes, -1, np.int64)
+    g2l[l2g] = np.arange(l2g.shape[0])
+    return dict(sel=sel, first=first, member=member, l2g=l2g, g2l=g2l)
+
+
+class Full:
+    """One full-size workload built and stepped on the GPU once."""
+
+    def __init__(self, name):
+        wl = synth.WORKLOADS[name]
+        self.wl = wl
+        self.g = synth.make_graph(wl.graph)
+        self.ref = oracle_selection(self.g)
+        g = self.g
+        gd = {k: to_dev(getattr(g, k)) for k in ("src", "dst", "rel", "ntype", "part")}
+        cfg = wl.graph
+        self.sub = api.hg_build_csr(gd["src"], gd["dst"], gd["rel"], gd["ntype"], gd["part"], g.k,
+                                    cfg.n_rel, 2, cfg.budget, key=cfg.key, theta=cfg.theta, seed=cfg.seed,
+                                    want_eid=True)
+        del gd
+        keep = self.ref["member"][g.src] & self.ref["member"][g.dst]
+        self.eid = np.nonzero(keep)[0]
+        g2l = self.ref["g2l"]
+        self.src_l = g2l[g.src[self.eid]]
+        self.dst_l = g2l[g.dst[self.eid]]
+        self.rel_l = g.rel[self.eid].astype(np.int64)
+        self.R = cfg.n_rel
+        self.ns = self.ref["l2g"].shape[0]
+
+    def free(self):
+        del self.sub
+        gc.collect()
+        torch.cuda.empty_cache()
+
+
+@pytest.fixture(scope="module", params=["large", "skew"])
+def full(request):
+    f = Full(request.param)
+    yield f
+    f.free()
+
+
+def test_fullsize_selection_exact(full):
+    sub, ref, g = full.sub, full.ref, full.g
+    assert sub.n_sub == full.ns and sub.e_sub == full.eid.shape[0]
+    assert np.array_equal(sub.view("local2global").cpu().numpy(), ref["l2g"])
+    ov = sub.view("overlap").cpu().numpy()
+    assert np.array_equal(ov, np.sort(ref["g2l"][ref["sel"]]))
+    og = ref["l2g"][ov]
+    assert np.array_equal(sub.view("overlap_home").cpu().numpy(), g.part[og])
+    assert np.array_equal(sub.view("overlap_rel").cpu().numpy(), g.rel[ref["first"][og]])
+    tof = np.concatenate([[0], np.cumsum(np.bincount(g.ntype[ref["l2g"]], minlength=2))])
+    assert sub.type_off_host() == list(tof)
+
+
+def test_fullsize_csr_csc_properties(full):
+    sub, g, R, ns = full.sub, full.g, full.R, full.ns
+    nq = ns * R
+    key_csr = full.dst_l * R + full.rel_l
+    key_csc = full.src_l * R + full.rel_l
+    cnt_csr = np.bincount(key_csr, minlength=nq)
+    cnt_csc = np.bincount(key_csc, minlength=nq)
+    ptr = sub.view("csr_ptr").cpu().numpy().astype(np.int64)
+    assert np.array_equal(np.diff(ptr), cnt_csr)
+    eid = sub.view("csr_eid").cpu().numpy().astype(np.int64)
+    col = sub.view("csr_col").cpu().numpy().astype(np.int64)
+    row = np.repeat(np.arange(nq), cnt_csr)
+    g2l = full.ref["g2l"]
+    # every entry's edge belongs to its row and column
+    assert np.array_equal(g2l[g.dst[eid]] * R + g.rel[eid], row)
+    assert np.array_equal(g2l[g.src[eid]], col)
+    # ascending edge id inside each row
+    same = row[1:] == row[:-1]
+    assert np.all(np.diff(eid)[same] > 0)
+    # every kept edge exactly once
+    seen = np.bincount(eid, minlength=g.n_edges)
+    expect = np.zeros(g.n_edges, np.int64)
+    expect[full.eid] = 1
+    assert np.array_equal(seen, expect)
+    del eid, col, row, seen, expect
+    # CSC: counts, destination fingerprints per row, exact scale
+    cptr = sub.view("csc_ptr").cpu().numpy().astype(np.int64)
+    assert np.array_equal(np.diff(cptr), cnt_csc)
+    crow = sub.view("csc_row").cpu().numpy().astype(np.int64)
+    # per-row sums of two 24-bit hashes of the destination ids (exact in float64)
+    h = splitmix.mix(crow.astype(np.uint64))
+    rows = np.repeat(np.arange(nq), cnt_csc)
+    hs = splitmix.mix(full.dst_l.astype(np.uint64))
+    for shift in (40, 16):
+        a = ((h >> np.uint64(shift)) & np.uint64(0xFFFFFF)).astype(np.float64)
+        b = ((hs >> np.uint64(shift)) & np.uint64(0xFFFFFF)).astype(np.float64)
+        got = np.bincount(rows, weights=a, minlength=nq)
+        exp = np.bincount(key_csc, weights=b, minlength=nq)
+        assert np.array_equal(got, exp)
+    scale = sub.view("csc_scale").cpu().numpy()
+    deg = cnt_csr[crow * R + (rows % R)].astype(np.float32)
+    assert np.array_equal(scale.view(np.uint32), (np.float32(1.0) / deg).view(np.uint32))
+
+
+def _in_edges(full, rows):
+    """Edges (src, rel, dst) of the subgraph whose destination is in rows."""
+    m = np.isin(full.dst_l, rows)
+    return full.src_l[m], full.rel_l[m], full.dst_l[m]
+
+
+def _z_rows(full, rows, H, w):
+    """float64 pre-activations z for the given destination rows."""
+    R = full.R
+    s, r, t = _in_edges(full, rows)
+    pos = {v: i for i, v in enumerate(rows)}
+    idx = np.array([pos[x] for x in t], dtype=np.int64) if t.size else np.zeros(0, np.int64)
+    n, d = rows.shape[0], H.shape[1]
+    agg = np.zeros((n, R, d))
+    cnt = np.zeros((n, R))
+    np.add.at(agg, (idx, r), H[s].astype(np.float64))
+    np.add.at(cnt, (idx, r), 1.0)
+    mean = np.divide(agg, cnt[:, :, None], out=np.zeros_like(agg), where=cnt[:, :, None] > 0)
+    z = np.einsum("nrd,rde->ne", mean, w.w_rel.astype(np.float64))
+    typ = full.g.ntype[full.ref["l2g"][rows]].astype(np.int64)
+    z += np.einsum("nd,nde->ne", H[rows].astype(np.float64), w.w_self.astype(np.float64)[typ])
+    z += w.bias.astype(np.float64)[typ]
+    return z
+
+
+def test_fullsize_layer_sampled_rows(full):
+    sub, wl = full.sub, full.wl
+    d, R = wl.model.d, full.R
+    H = synth.features(wl.model.seed, full.g.n_nodes, d)[full.ref["l2g"]]
+    w = synth.layer_weights(wl.model.seed, 0, R, 2, d, 0.1)
+    Hd = to_dev(H)
+    wr, wsf, b = to_dev(w.w_rel), to_dev(w.w_self), to_dev(w.bias)
+    out, saved = api.hg_layer_fwd(sub, Hd, wr, wsf, b)
+    rng = np.random.default_rng(0)
+    indeg = np.bincount(full.dst_l, minlength=full.ns)
+    rows = np.unique(np.concatenate([rng.choice(full.ns, 3000, replace=False),
+                                     np.argsort(indeg)[-16:]]))
+    z = _z_rows(full, rows, H, w)
+    got = out[torch.from_numpy(rows).cuda()].cpu().numpy()
+    assert parity_err(got, np.maximum(z, 0) + H[rows]) <= TOL
+    band = 1e-4 * np.sqrt(np.mean(z * z))
+    gm = unpack_mask(saved.cpu().numpy()[rows], d)
+    diff = gm != (z > 0)
+    assert np.all(np.abs(z[diff]) <= band)
+
+    # backward, sampled dH rows: dH_i = G_i + dZ_i W_self^T + sum_{i->j, r} dZ_j / deg_r(j) W_r^T
+    G = synth.upstream_grad(wl.model.seed, full.ns, d)
+    dH, dWr, dWs, db = api.hg_layer_bwd(sub, Hd, wr, wsf, saved, to_dev(G))
+    srcs = np.unique(rng.choice(full.ns, 300, replace=False))
+    mo = np.isin(full.src_l, srcs)
+    es, er, ed = full.src_l[mo], full.rel_l[mo], full.dst_l[mo]
+    need = np.unique(np.concatenate([ed, srcs]))
+    zn = _z_rows(full, need, H, w)
+    pos = {v: i for i, v in enumerate(need)}
+    dz = G[need] * (zn > 0)
+    near = np.abs(zn) <= band
+    key_csr = full.dst_l * R + full.rel_l
+    deg = np.bincount(key_csr, minlength=full.ns * R)
+    typ = full.g.ntype[full.ref["l2g"][srcs]].astype(np.int64)
+    exp = G[srcs].astype(np.float64).copy()
+    ok = np.ones(srcs.shape[0], bool)
+    for k, i in enumerate(srcs):
+        p = pos[i]
+        exp[k] += dz[p] @ w.w_self[typ[k]].astype(np.float64).T
+        ok[k] &= not near[p].any()
+        sel = es == i
+        for j, r in zip(ed[sel], er[sel]):
+            q = pos[j]
+            exp[k] += dz[q] / deg[j * R + r] @ w.w_rel[r].astype(np.float64).T
+            ok[k] &= not near[q].any()
+    assert ok.sum() > 0.8 * ok.shape[0]
+    got = dH[torch.from_numpy(srcs).cuda()].cpu().numpy()
+    assert parity_err(got[ok], exp[ok]) <= TOL
+    del Hd, out, saved, dH
+
+
+def test_fullsize_alignment(full):
+    sub, wl = full.sub, full.wl
+    d = wl.model.d
+    ov = sub.view("overlap").cpu().numpy()
+    m = ov.shape[0]
+    H = synth.features(wl.model.seed + 1, full.g.n_nodes, d)[full.ref["l2g"]]
+    Href = synth.reference_embeddings(wl.model.seed, m, d)
+    omega = None
+    if wl.model.weighted_align:
+        omega = synth.align_weights(sub.view("overlap_rel").cpu().numpy(), full.g.rel, full.R)
+    (li, ld, L), dX, _ = align.loss_and_grad(H[ov], Href, omega, wl.model.lambda_n, wl.model.lambda_cca,
+                                            wl.model.eps, wl.model.ddof)
+    dH = torch.zeros((full.ns, d), dtype=torch.float32, device="cuda")
+    loss = api.hg_align_loss_fwd_bwd(to_dev(H), sub.view("overlap"), to_dev(Href), dH,
+                                     w=None if omega is None else to_dev(omega),
+                                     lambda_n=wl.model.lambda_n, scale=wl.model.lambda_cca,
+                                     eps=wl.model.eps, ddof=wl.model.ddof).cpu().numpy()
+    for a, b in zip(loss, (li, ld, L)):
+        assert abs(a - b) <= TOL * abs(b)
+    assert parity_err(dH.cpu().numpy()[ov], dX) <= TOL
+
+
+def test_medium_full_layer_and_weight_gradients():
+    """Every output of one layer forward and backward on the 1M/20M workload."""
+    wl = synth.WORKLOADS["medium"]
+    g = synth.make_graph(wl.graph)
+    inp = runner.make_inputs(wl, g)
+    sub = inp.sub
+    ref = oracle_selection(g)
+    keep = ref["member"][g.src] & ref["member"][g.dst]
+    eid = np.nonzero(keep)[0]
+    src_l, dst_l = ref["g2l"][g.src[eid]], ref["g2l"][g.dst[eid]]
+    rel_l = g.rel[eid]
+    ntype_l = g.ntype[ref["l2g"]]
+    d = wl.model.d
+    H = inp.feats_np[ref["l2g"]]
+    w = inp.weights_np[0]
+    out, Z = layer.forward(sub.n_sub, src_l, dst_l, rel_l, ntype_l, H, w.w_rel, w.w_self, w.bias)
+    Hd = inp.H[0]
+    Ho, saved = api.hg_layer_fwd(sub, Hd, *inp.weights[0])
+    assert parity_err(Ho.cpu().numpy(), out) <= TOL
+    mask = Z > 0
+    G = synth.upstream_grad(3, sub.n_sub, d)
+    exp = layer.backward(sub.n_sub, src_l, dst_l, rel_l, ntype_l, H, w.w_rel, w.w_self, w.bias, G, mask=mask)
+    got = api.hg_layer_bwd(sub, Hd, inp.weights[0][0], inp.weights[0][1], to_dev(pack_mask(mask)), to_dev(G))
+    for a, b, nm in zip(got, exp, ("dH", "dW_rel", "dW_self", "dbias")):
+        err = parity_err(a.cpu().numpy(), b)
+        assert err <= TOL, (nm, err)
