@@ -38,27 +38,27 @@ __global__ void __launch_bounds__(256) k_colsum(int64_t m, int64_t rows_per_chun
   }
 }
 
-template <int D>
+template <int D, class T>
 struct FRow {  // value of a gathered / contiguous row
-  const float* base;
+  const T* base;
   RowMap map;
-  __device__ __forceinline__ float operator()(int64_t b, int c) const { return base[map(b) * D + c]; }
+  __device__ __forceinline__ float operator()(int64_t b, int c) const { return Elt<T>::get(base + map(b) * D + c); }
 };
 
-template <int D>
+template <int D, class T>
 struct FCentredSq {
-  const float* base;
+  const T* base;
   RowMap map;
   const float* mu;
   __device__ __forceinline__ float operator()(int64_t b, int c) const {
-    const float x = base[map(b) * D + c] - mu[c];
+    const float x = Elt<T>::get(base + map(b) * D + c) - mu[c];
     return x * x;
   }
 };
 
-template <int D>
+template <int D, class T>
 struct FInv {  // w_b (xh - yh)^2
-  LoadStd<D> x, y;
+  LoadStd<D, T> x, y;
   const float* w;
   __device__ __forceinline__ float operator()(int64_t b, int c) const {
     const float d = x.at(b, c) - y.at(b, c);
@@ -73,11 +73,11 @@ struct FGrad {  // g' = G / sqrt(M)  (gradient w.r.t. the centred, 1/sigma-scale
   __device__ __forceinline__ float operator()(int64_t b, int c) const { return G[b * D + c] * inv_sqrt_m; }
 };
 
-template <int D>
+template <int D, class T>
 struct FGradX {  // g' * xt, xt = (x - mu) / sigma
   const float* G;
   float inv_sqrt_m;
-  LoadStd<D> xt;
+  LoadStd<D, T> xt;
   __device__ __forceinline__ float operator()(int64_t b, int c) const {
     return G[b * D + c] * inv_sqrt_m * xt.at(b, c);
   }
@@ -141,10 +141,10 @@ __global__ void k_loss_final(const float* __restrict__ inv_cols, float* __restri
 }
 
 // Epilogue of the gradient GEMM: G[b][c] = 4 lambda_n acc + sign * 2 w_b (xh - yh).
-template <int D>
+template <int D, class T>
 struct GradEpi {
   float* G;
-  LoadStd<D> self, other;
+  LoadStd<D, T> self, other;
   const float* w;
   float four_lambda;
   float two_sign;
@@ -159,11 +159,11 @@ struct GradEpi {
 };
 
 // dX = (1/sigma)(g' - S1/M - xt * S2/(M - ddof)); dst[row] (+)= scale * dX.
-template <int D>
-__global__ void k_std_backward(int64_t m, const float* __restrict__ G, float inv_sqrt_m, LoadStd<D> xt,
+template <int D, class T>
+__global__ void k_std_backward(int64_t m, const float* __restrict__ G, float inv_sqrt_m, LoadStd<D, T> xt,
                                const float* __restrict__ inv_sig, const float* __restrict__ S1,
                                const float* __restrict__ S2, int32_t ddof, float scale,
-                               float* __restrict__ dst, RowMap dmap, int accumulate) {
+                               T* __restrict__ dst, RowMap dmap, int accumulate) {
   const int64_t total = m * D;
   const float inv_m = 1.0f / (float)m;
   const float inv_md = 1.0f / (float)(m - ddof);
@@ -174,7 +174,12 @@ __global__ void k_std_backward(int64_t m, const float* __restrict__ G, float inv
     const float g = G[e] * inv_sqrt_m;
     const float dx = inv_sig[c] * (g - S1[c] * inv_m - xt.at(b, c) * S2[c] * inv_md);
     const int64_t o = dmap(b) * D + c;
-    dst[o] = (accumulate ? dst[o] : 0.f) + scale * dx;
+    const float v = (accumulate ? Elt<T>::get(dst + o) : 0.f) + scale * dx;
+    if constexpr (sizeof(T) == 4) {
+      dst[o] = v;
+    } else {
+      dst[o] = f2bf(v);
+    }
   }
 }
 
@@ -215,53 +220,62 @@ int colsum(const char* name, int64_t m, F f, float* part, float* out, hipStream_
   return HG_OK;
 }
 
-template <int D>
-int align_impl(int64_t m, const float* H, const int32_t* overlap, const float* Href, const float* w,
-               float lambda_n, float scale, float eps, int32_t ddof, float* loss3, float* dH,
-               float* dHref, void* ws, size_t ws_bytes, hipStream_t s) {
+template <int D, class T, class ALoad, class Epi>
+int grad_gemm(int64_t m, const float* W, ALoad la, Epi ep, hipStream_t s) {
+  if constexpr (D <= 128) {
+    return launch_gemm_rows<D, false>("align_grad_gemm", m, W, la, ep, s);
+  } else {
+    return launch_gemm_rows_bf16<D, false>("align_grad_gemm", m, W, la, ep, s);
+  }
+}
+
+template <int D, class T>
+int align_impl(int64_t m, const T* H, const int32_t* overlap, const T* Href, const float* w, float lambda_n,
+               float scale, float eps, int32_t ddof, float* loss3, T* dH, T* dHref, void* ws, size_t ws_bytes,
+               hipStream_t s) {
   Arena a(ws, ws_bytes);
   AlignWs<D> q;
   q.layout(a, m, align_chunks(m));
   if (!a.ok()) return fail(HG_ERR_CAPACITY, "alignment workspace needs %zu bytes, got %zu", a.used, ws_bytes);
   const RowMap mx = rows_list(overlap), my = rows_contig(0);
   // (d1) statistics
-  HG_TRY(colsum<D>("align_stats", m, FRow<D>{H, mx}, q.cpart, q.sum, s));
+  HG_TRY((colsum<D>("align_stats", m, FRow<D, T>{H, mx}, q.cpart, q.sum, s)));
   HG_LAUNCH("align_mean", k_stats_mean<D>, dim3(1), dim3(256), 0, s, (const float*)q.sum, m, q.mux);
-  HG_TRY(colsum<D>("align_stats", m, FCentredSq<D>{H, mx, q.mux}, q.cpart, q.sum, s));
+  HG_TRY((colsum<D>("align_stats", m, FCentredSq<D, T>{H, mx, q.mux}, q.cpart, q.sum, s)));
   HG_LAUNCH("align_sigma", k_stats_sigma<D>, dim3(1), dim3(256), 0, s, (const float*)q.sum, m, ddof, eps,
             q.isx, q.shx);
-  HG_TRY(colsum<D>("align_stats", m, FRow<D>{Href, my}, q.cpart, q.sum, s));
+  HG_TRY((colsum<D>("align_stats", m, FRow<D, T>{Href, my}, q.cpart, q.sum, s)));
   HG_LAUNCH("align_mean", k_stats_mean<D>, dim3(1), dim3(256), 0, s, (const float*)q.sum, m, q.muy);
-  HG_TRY(colsum<D>("align_stats", m, FCentredSq<D>{Href, my, q.muy}, q.cpart, q.sum, s));
+  HG_TRY((colsum<D>("align_stats", m, FCentredSq<D, T>{Href, my, q.muy}, q.cpart, q.sum, s)));
   HG_LAUNCH("align_sigma", k_stats_sigma<D>, dim3(1), dim3(256), 0, s, (const float*)q.sum, m, ddof, eps,
             q.isy, q.shy);
-  const LoadStd<D> xh{H, mx, q.mux, q.shx}, yh{Href, my, q.muy, q.shy};
+  const LoadStd<D, T> xh{H, mx, q.mux, q.shx}, yh{Href, my, q.muy, q.shy};
   // (d2) Grams and loss
   HG_TRY((launch_gemm_tn<D>("align_gram", m, xh, xh, q.gpart, nullptr, q.cx, nullptr, 0, s)));
   HG_TRY((launch_gemm_tn<D>("align_gram", m, yh, yh, q.gpart, nullptr, q.cy, nullptr, 0, s)));
-  HG_TRY(colsum<D>("align_inv", m, FInv<D>{xh, yh, w}, q.cpart, q.invc, s));
+  HG_TRY((colsum<D>("align_inv", m, FInv<D, T>{xh, yh, w}, q.cpart, q.invc, s)));
   HG_LAUNCH("align_loss", k_loss_final<D>, dim3(1), dim3(256), 0, s, (const float*)q.invc, q.cx, q.cy,
             lambda_n, loss3);
   // (d3) gradient of the local view
   const float inv_sqrt_m = 1.0f / sqrtf((float)m);
   const unsigned ge = (unsigned)(cdiv(m * D, 256) < 65536 ? cdiv(m * D, 256) : 65536);
   {
-    GradEpi<D> ep{q.gx, xh, yh, w, 4.0f * lambda_n, 2.0f};
-    HG_TRY((launch_gemm_rows<D, false>("align_grad_gemm", m, q.cx, xh, ep, s)));
-    const LoadStd<D> xt{H, mx, q.mux, q.isx};
-    HG_TRY(colsum<D>("align_grad_stats", m, FGrad<D>{q.gx, inv_sqrt_m}, q.cpart, q.s1, s));
-    HG_TRY(colsum<D>("align_grad_stats", m, FGradX<D>{q.gx, inv_sqrt_m, xt}, q.cpart, q.s2, s));
-    HG_LAUNCH("align_std_backward", k_std_backward<D>, dim3(ge), dim3(256), 0, s, m, (const float*)q.gx,
+    GradEpi<D, T> ep{q.gx, xh, yh, w, 4.0f * lambda_n, 2.0f};
+    HG_TRY((grad_gemm<D, T>(m, q.cx, xh, ep, s)));
+    const LoadStd<D, T> xt{H, mx, q.mux, q.isx};
+    HG_TRY((colsum<D>("align_grad_stats", m, FGrad<D>{q.gx, inv_sqrt_m}, q.cpart, q.s1, s)));
+    HG_TRY((colsum<D>("align_grad_stats", m, FGradX<D, T>{q.gx, inv_sqrt_m, xt}, q.cpart, q.s2, s)));
+    HG_LAUNCH("align_std_backward", (k_std_backward<D, T>), dim3(ge), dim3(256), 0, s, m, (const float*)q.gx,
               inv_sqrt_m, xt, (const float*)q.isx, (const float*)q.s1, (const float*)q.s2, ddof, scale, dH,
               mx, 1);
   }
   if (dHref) {
-    GradEpi<D> ep{q.gx, yh, xh, w, 4.0f * lambda_n, 2.0f};
-    HG_TRY((launch_gemm_rows<D, false>("align_grad_gemm", m, q.cy, yh, ep, s)));
-    const LoadStd<D> yt{Href, my, q.muy, q.isy};
-    HG_TRY(colsum<D>("align_grad_stats", m, FGrad<D>{q.gx, inv_sqrt_m}, q.cpart, q.s1, s));
-    HG_TRY(colsum<D>("align_grad_stats", m, FGradX<D>{q.gx, inv_sqrt_m, yt}, q.cpart, q.s2, s));
-    HG_LAUNCH("align_std_backward", k_std_backward<D>, dim3(ge), dim3(256), 0, s, m, (const float*)q.gx,
+    GradEpi<D, T> ep{q.gx, yh, xh, w, 4.0f * lambda_n, 2.0f};
+    HG_TRY((grad_gemm<D, T>(m, q.cy, yh, ep, s)));
+    const LoadStd<D, T> yt{Href, my, q.muy, q.isy};
+    HG_TRY((colsum<D>("align_grad_stats", m, FGrad<D>{q.gx, inv_sqrt_m}, q.cpart, q.s1, s)));
+    HG_TRY((colsum<D>("align_grad_stats", m, FGradX<D, T>{q.gx, inv_sqrt_m, yt}, q.cpart, q.s2, s)));
+    HG_LAUNCH("align_std_backward", (k_std_backward<D, T>), dim3(ge), dim3(256), 0, s, m, (const float*)q.gx,
               inv_sqrt_m, yt, (const float*)q.isy, (const float*)q.s1, (const float*)q.s2, ddof, scale,
               dHref, my, 0);
   }
@@ -283,6 +297,9 @@ extern "C" size_t hg_align_workspace_size(int64_t M, int32_t d) {
   } else if (d == 128) {
     AlignWs<128> w;
     w.layout(z, M, align_chunks(M));
+  } else if (d == 256) {
+    AlignWs<256> w;
+    w.layout(z, M, align_chunks(M));
   } else {
     return 0;
   }
@@ -295,8 +312,11 @@ extern "C" int hg_align_loss_fwd_bwd(int64_t M, int32_t d, int32_t dtype, int64_
                                      void* dH, void* dH_ref, void* ws, size_t ws_bytes, void* stream) {
   if (M < 0 || n_rows < 0) return fail(HG_ERR_ARG, "negative size");
   if (!loss3) return fail(HG_ERR_ARG, "null loss3");
-  if (dtype != HG_DTYPE_F32) return fail(HG_ERR_UNSUPPORTED, "alignment supports float32 only");
-  if (d != 64 && d != 128) return fail(HG_ERR_UNSUPPORTED, "alignment supports d in {64, 128}, got %d", d);
+  if (dtype != HG_DTYPE_F32 && dtype != HG_DTYPE_BF16) return fail(HG_ERR_ARG, "dtype %d", dtype);
+  if (dtype == HG_DTYPE_F32 && d != 64 && d != 128)
+    return fail(HG_ERR_UNSUPPORTED, "float32 alignment supports d in {64, 128}, got %d", d);
+  if (dtype == HG_DTYPE_BF16 && d != 64 && d != 128 && d != 256)
+    return fail(HG_ERR_UNSUPPORTED, "bfloat16 alignment supports d in {64, 128, 256}, got %d", d);
   if (ddof < 0) return fail(HG_ERR_ARG, "ddof < 0");
   if (!(eps >= 0.f)) return fail(HG_ERR_ARG, "eps must be >= 0");
   if (M > n_rows) return fail(HG_ERR_ARG, "M %lld > n_rows %lld", (long long)M, (long long)n_rows);
@@ -304,9 +324,15 @@ extern "C" int hg_align_loss_fwd_bwd(int64_t M, int32_t d, int32_t dtype, int64_
   if (M == 0) return fill_f32(loss3, 0.f, 3, s);
   if (M <= ddof) return fail(HG_ERR_ARG, "M %lld <= ddof %d", (long long)M, ddof);
   if (!H || !overlap || !H_ref || !dH) return fail(HG_ERR_ARG, "null alignment argument");
-  if (d == 64)
-    return align_impl<64>(M, (const float*)H, overlap, (const float*)H_ref, w, lambda_n, scale, eps, ddof,
-                          loss3, (float*)dH, (float*)dH_ref, ws, ws_bytes, s);
-  return align_impl<128>(M, (const float*)H, overlap, (const float*)H_ref, w, lambda_n, scale, eps, ddof,
-                         loss3, (float*)dH, (float*)dH_ref, ws, ws_bytes, s);
+  if (dtype == HG_DTYPE_BF16) {
+    const bf16_t *h = (const bf16_t*)H, *r = (const bf16_t*)H_ref;
+    bf16_t *dh = (bf16_t*)dH, *dr = (bf16_t*)dH_ref;
+    if (d == 64) return align_impl<64, bf16_t>(M, h, overlap, r, w, lambda_n, scale, eps, ddof, loss3, dh, dr, ws, ws_bytes, s);
+    if (d == 128) return align_impl<128, bf16_t>(M, h, overlap, r, w, lambda_n, scale, eps, ddof, loss3, dh, dr, ws, ws_bytes, s);
+    return align_impl<256, bf16_t>(M, h, overlap, r, w, lambda_n, scale, eps, ddof, loss3, dh, dr, ws, ws_bytes, s);
+  }
+  const float *h = (const float*)H, *r = (const float*)H_ref;
+  float *dh = (float*)dH, *dr = (float*)dH_ref;
+  if (d == 64) return align_impl<64, float>(M, h, overlap, r, w, lambda_n, scale, eps, ddof, loss3, dh, dr, ws, ws_bytes, s);
+  return align_impl<128, float>(M, h, overlap, r, w, lambda_n, scale, eps, ddof, loss3, dh, dr, ws, ws_bytes, s);
 }

@@ -21,35 +21,39 @@ namespace hg {
 namespace {
 
 // ---- forward SpMM + epilogue --------------------------------------------------
-// One wave per destination row.  Lanes form EPW slots of LPR lanes; a slot
-// gathers one source row (D floats as LPR float4s), so a wave step covers EPW
-// edges; neighbour ids and weights of up to 64 entries sit one per lane and are
-// broadcast with ds_bpermute.
-template <int D>
+// One wave per destination row.  A row of D elements of T is read as LPR
+// 16-byte chunks (EL elements each); lanes form EPW = 64/LPR slots, a slot
+// gathers one source row, so one wave step covers EPW edges.  Neighbour ids
+// and weights of up to 64 entries sit one per lane and are broadcast with
+// ds_bpermute.  Accumulation is float32.
+template <int D, class T>
 __global__ void __launch_bounds__(256) k_spmm_fwd(int64_t n_sub, int32_t R, const int32_t* __restrict__ csr_ptr,
                                                   const int32_t* __restrict__ csr_col,
-                                                  const float* __restrict__ Y, const float* __restrict__ Yself,
-                                                  const float* __restrict__ Hin, float* __restrict__ Hout,
+                                                  const T* __restrict__ Y, const T* __restrict__ Yself,
+                                                  const T* __restrict__ Hin, T* __restrict__ Hout,
                                                   uint32_t* __restrict__ mask, int relu, int residual) {
-  constexpr int LPR = D / 4;
+  constexpr int EL = Elt<T>::EL;
+  constexpr int LPR = D / EL;
   constexpr int EPW = 64 / LPR;
   constexpr int U = 4;
+  static_assert(LPR <= 64 && EPW * LPR == 64, "row must span a power-of-two number of lanes");
   const int l = threadIdx.x & 63;
   const int slot = l / LPR;
-  const int c4 = l % LPR;
+  const int c0 = (l % LPR) * EL;
   const int64_t wave0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
   const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
   for (int64_t j = wave0; j < n_sub; j += nwaves) {
     const int64_t rb = j * R;
     const int32_t p0 = csr_ptr[rb];
     const int32_t pe = csr_ptr[rb + R];
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    float acc[EL];
+#pragma unroll
+    for (int q = 0; q < EL; ++q) acc[q] = 0.f;
     for (int32_t base = p0; base < pe; base += 64) {
       const int32_t pos = base + l;
-      const bool valid = pos < pe;
       int32_t rowi = 0;
       float wgt = 0.f;
-      if (valid) {
+      if (pos < pe) {
         const int32_t src = csr_col[pos];
         int32_t r = 0, lo = p0, hi = pe;
         for (int t = 1; t < R; ++t) {
@@ -66,7 +70,7 @@ __global__ void __launch_bounds__(256) k_spmm_fwd(int64_t n_sub, int32_t R, cons
       }
       const int cnt = (pe - base) < 64 ? (pe - base) : 64;
       for (int e = 0; e < cnt; e += EPW * U) {
-        f32x4 v[U];
+        float v[U][EL];
         float ww[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
@@ -75,43 +79,44 @@ __global__ void __launch_bounds__(256) k_spmm_fwd(int64_t n_sub, int32_t R, cons
           const float wq = __shfl(wgt, my & 63, 64);
           ww[u] = (my < cnt) ? wq : 0.f;
           if (my < cnt) {
-            v[u] = *reinterpret_cast<const f32x4*>(Y + (int64_t)q * D + 4 * c4);
+            Elt<T>::load(Y + (int64_t)q * D + c0, v[u]);
           } else {
-            v[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int k = 0; k < EL; ++k) v[u][k] = 0.f;
           }
         }
 #pragma unroll
-        for (int u = 0; u < U; ++u) acc += ww[u] * v[u];
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+          for (int k = 0; k < EL; ++k) acc[k] += ww[u] * v[u][k];
       }
     }
 #pragma unroll
-    for (int o = LPR; o < 64; o <<= 1) {
-      acc[0] += __shfl_xor(acc[0], o, 64);
-      acc[1] += __shfl_xor(acc[1], o, 64);
-      acc[2] += __shfl_xor(acc[2], o, 64);
-      acc[3] += __shfl_xor(acc[3], o, 64);
-    }
-    const int64_t off = j * D + 4 * c4;
-    f32x4 z = acc;
+    for (int o = LPR; o < 64; o <<= 1)
+#pragma unroll
+      for (int k = 0; k < EL; ++k) acc[k] += __shfl_xor(acc[k], o, 64);
+    const int64_t off = j * D + c0;
     uint32_t word = 0;
     if (slot == 0) {
-      z += *reinterpret_cast<const f32x4*>(Yself + off);
-      f32x4 h = z;
-      if (relu) {
+      float ys[EL], h[EL], z[EL];
+      Elt<T>::load(Yself + off, ys);
+      float hin[EL];
+      if (residual) Elt<T>::load(Hin + off, hin);
+      uint32_t bits = 0;
 #pragma unroll
-        for (int q = 0; q < 4; ++q) h[q] = z[q] > 0.f ? z[q] : 0.f;
+      for (int k = 0; k < EL; ++k) {
+        z[k] = acc[k] + ys[k];
+        h[k] = (relu && !(z[k] > 0.f)) ? 0.f : z[k];
+        if (residual) h[k] += hin[k];
+        bits |= ((!relu || z[k] > 0.f) ? 1u : 0u) << k;
       }
-      if (residual) h += *reinterpret_cast<const f32x4*>(Hin + off);
-      *reinterpret_cast<f32x4*>(Hout + off) = h;
-      uint32_t nib = 0;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) nib |= ((!relu || z[q] > 0.f) ? 1u : 0u) << q;
-      word = nib << (4 * (c4 & 7));
+      Elt<T>::store(Hout + off, h);
+      word = bits << (c0 & 31);
     }
-    word |= __shfl_xor(word, 1, 64);
-    word |= __shfl_xor(word, 2, 64);
-    word |= __shfl_xor(word, 4, 64);
-    if (slot == 0 && (c4 & 7) == 0) mask[j * (D / 32) + (c4 >> 3)] = word;
+    // OR the EL-bit groups of the 32/EL lanes that share a mask word
+#pragma unroll
+    for (int o = 1; o < 32 / EL; o <<= 1) word |= __shfl_xor(word, o, 64);
+    if (slot == 0 && (c0 & 31) == 0) mask[j * (D / 32) + (c0 >> 5)] = word;
   }
 }
 
@@ -119,24 +124,27 @@ __global__ void __launch_bounds__(256) k_spmm_fwd(int64_t n_sub, int32_t R, cons
 // CSC rows of hub sources hold up to millions of entries, so each lane
 // accumulates in float64 (the kernel is bound by the gathers, not the adds);
 // split rows keep float64 partial rows.
-template <int D>
+template <int D, class T>
 __global__ void __launch_bounds__(256) k_spmm_bwd(int64_t n_items, const int4* __restrict__ items,
                                                   const int32_t* __restrict__ csc_row,
                                                   const float* __restrict__ csc_scale,
-                                                  const float* __restrict__ dZ,
-                                                  float* __restrict__ dY, double* __restrict__ partial) {
-  constexpr int LPR = D / 4;
+                                                  const T* __restrict__ dZ,
+                                                  T* __restrict__ dY, double* __restrict__ partial) {
+  constexpr int EL = Elt<T>::EL;
+  constexpr int LPR = D / EL;
   constexpr int EPW = 64 / LPR;
   constexpr int U = 4;
   const int l = threadIdx.x & 63;
   const int slot = l / LPR;
-  const int c4 = l % LPR;
+  const int c0 = (l % LPR) * EL;
   const int64_t wave0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
   const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
   for (int64_t it = wave0; it < n_items; it += nwaves) {
     const int4 item = items[it];
     const int32_t beg = item.y, end = item.z;
-    f64x4 acc = {0.0, 0.0, 0.0, 0.0};
+    double acc[EL];
+#pragma unroll
+    for (int k = 0; k < EL; ++k) acc[k] = 0.0;
     for (int32_t base = beg; base < end; base += 64) {
       const int32_t pos = base + l;
       int32_t dst = 0;
@@ -147,7 +155,7 @@ __global__ void __launch_bounds__(256) k_spmm_bwd(int64_t n_items, const int4* _
       }
       const int cnt = (end - base) < 64 ? (end - base) : 64;
       for (int e = 0; e < cnt; e += EPW * U) {
-        f32x4 v[U];
+        float v[U][EL];
         float ww[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
@@ -156,58 +164,61 @@ __global__ void __launch_bounds__(256) k_spmm_bwd(int64_t n_items, const int4* _
           const float wq = __shfl(sc, my & 63, 64);
           ww[u] = (my < cnt) ? wq : 0.f;
           if (my < cnt) {
-            v[u] = *reinterpret_cast<const f32x4*>(dZ + (int64_t)q * D + 4 * c4);
+            Elt<T>::load(dZ + (int64_t)q * D + c0, v[u]);
           } else {
-            v[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int k = 0; k < EL; ++k) v[u][k] = 0.f;
           }
         }
 #pragma unroll
         for (int u = 0; u < U; ++u)
 #pragma unroll
-          for (int q = 0; q < 4; ++q) acc[q] += (double)ww[u] * (double)v[u][q];
+          for (int k = 0; k < EL; ++k) acc[k] += (double)ww[u] * (double)v[u][k];
       }
     }
 #pragma unroll
-    for (int o = LPR; o < 64; o <<= 1) {
-      acc[0] += __shfl_xor(acc[0], o, 64);
-      acc[1] += __shfl_xor(acc[1], o, 64);
-      acc[2] += __shfl_xor(acc[2], o, 64);
-      acc[3] += __shfl_xor(acc[3], o, 64);
-    }
+    for (int o = LPR; o < 64; o <<= 1)
+#pragma unroll
+      for (int k = 0; k < EL; ++k) acc[k] += __shfl_xor(acc[k], o, 64);
     if (slot == 0) {
       if (item.w < 0) {
-        f32x4 o;
+        float o[EL];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) o[q] = (float)acc[q];
-        *reinterpret_cast<f32x4*>(dY + (int64_t)item.x * D + 4 * c4) = o;
+        for (int k = 0; k < EL; ++k) o[k] = (float)acc[k];
+        Elt<T>::store(dY + (int64_t)item.x * D + c0, o);
       } else {
-        *reinterpret_cast<f64x4*>(partial + (int64_t)item.w * D + 4 * c4) = acc;
+        double* p = partial + (int64_t)item.w * D + c0;
+#pragma unroll
+        for (int k = 0; k < EL; ++k) p[k] = acc[k];
       }
     }
   }
 }
 
-// Split rows: dY[q] = sum of its partial rows, in chunk order.
-template <int D>
+// Split rows: dY[q] = sum of its partial rows, in chunk order (float64).
+template <int D, class T>
 __global__ void k_heavy_reduce(int64_t n_heavy, const int4* __restrict__ heavy,
-                               const double* __restrict__ partial, float* __restrict__ dY) {
-  constexpr int LPR = D / 4;
+                               const double* __restrict__ partial, T* __restrict__ dY) {
+  constexpr int EL = Elt<T>::EL;
+  constexpr int LPR = D / EL;
   const int l = threadIdx.x & 63;
   const int64_t wave0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
   const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
   for (int64_t h = wave0; h < n_heavy; h += nwaves) {
     const int4 hv = heavy[h];
     if (l < LPR) {
-      f64x4 s = {0.0, 0.0, 0.0, 0.0};
-      for (int32_t k = 0; k < hv.z; ++k) {
-        const f64x4 p = *reinterpret_cast<const f64x4*>(partial + (int64_t)(hv.y + k) * D + 4 * l);
+      double s[EL];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) s[q] += p[q];
+      for (int k = 0; k < EL; ++k) s[k] = 0.0;
+      for (int32_t i = 0; i < hv.z; ++i) {
+        const double* p = partial + (int64_t)(hv.y + i) * D + l * EL;
+#pragma unroll
+        for (int k = 0; k < EL; ++k) s[k] += p[k];
       }
-      f32x4 o;
+      float o[EL];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) o[q] = (float)s[q];
-      *reinterpret_cast<f32x4*>(dY + (int64_t)hv.x * D + 4 * l) = o;
+      for (int k = 0; k < EL; ++k) o[k] = (float)s[k];
+      Elt<T>::store(dY + (int64_t)hv.x * D + l * EL, o);
     }
   }
 }
@@ -226,8 +237,8 @@ int validate_layer(const hg_subgraph* s, const hg_layer_desc* L) {
     return fail(HG_ERR_ARG, "dtype %d", L->dtype);
   if (L->dtype == HG_DTYPE_F32 && L->d_in != 64 && L->d_in != 128)
     return fail(HG_ERR_UNSUPPORTED, "float32 layers support d in {64, 128}, got %d", L->d_in);
-  if (L->dtype == HG_DTYPE_BF16)
-    return fail(HG_ERR_UNSUPPORTED, "bfloat16 layers are not implemented");
+  if (L->dtype == HG_DTYPE_BF16 && L->d_in != 64 && L->d_in != 128 && L->d_in != 256)
+    return fail(HG_ERR_UNSUPPORTED, "bfloat16 layers support d in {64, 128, 256}, got %d", L->d_in);
   if ((L->relu != 0 && L->relu != 1) || (L->residual != 0 && L->residual != 1))
     return fail(HG_ERR_ARG, "relu/residual must be 0 or 1");
   if (s->n_sub < 0 || s->n_rel < 1 || s->n_ntype < 1 || !s->csr_ptr || !s->csc_ptr || !s->plan)
@@ -235,36 +246,47 @@ int validate_layer(const hg_subgraph* s, const hg_layer_desc* L) {
   return HG_OK;
 }
 
-template <int D>
+template <int D, class T>
 struct FwdWs {
-  float *Y, *Yself;
+  T *Y, *Yself;
   template <class A>
   void layout(A& a, const hg_subgraph* s) {
-    Y = a.template take<float>(s->n_sub * s->n_rel * (int64_t)D);
-    Yself = a.template take<float>(s->n_sub * (int64_t)D);
+    Y = a.template take<T>(s->n_sub * s->n_rel * (int64_t)D);
+    Yself = a.template take<T>(s->n_sub * (int64_t)D);
   }
 };
 
-template <int D>
+template <int D, class T>
 struct BwdWs {
-  float *dZ, *dY, *splitk, *colsum;
+  T *dZ, *dY;
+  float *splitk, *colsum;
   double* part;
   template <class A>
   void layout(A& a, const hg_subgraph* s) {
-    dZ = a.template take<float>(s->n_sub * (int64_t)D);
-    dY = a.template take<float>(s->n_sub * s->n_rel * (int64_t)D);
+    dZ = a.template take<T>(s->n_sub * (int64_t)D);
+    dY = a.template take<T>(s->n_sub * s->n_rel * (int64_t)D);
     part = a.template take<double>(s->plan_partials * (int64_t)D);
     splitk = a.template take<float>(splitk_max_chunks() * (int64_t)D * D);
     colsum = a.template take<float>(splitk_max_chunks() * (int64_t)D);
   }
 };
 
-template <int D>
-int layer_fwd_impl(const hg_subgraph* s, const hg_layer_desc* L, const float* Hin, const float* W_rel,
-                   const float* W_self, const float* bias, float* Hout, uint32_t* mask, void* ws,
+// fp32 features use the fp32 MFMA transform, bf16 features the bf16 one.
+template <int D, class T, bool kTransW, class ALoad, class Epi>
+int transform(const char* name, int64_t n, const float* W, ALoad la, Epi ep, hipStream_t st) {
+  if constexpr (sizeof(T) == 4) {
+    return launch_gemm_rows<D, kTransW>(name, n, W, la, ep, st);
+  } else {
+    return launch_gemm_rows_bf16<D, kTransW>(name, n, W, la, ep, st);
+  }
+}
+
+template <int D, class T>
+int layer_fwd_impl(const hg_subgraph* s, const hg_layer_desc* L, const T* Hin, const float* W_rel,
+                   const float* W_self, const float* bias, T* Hout, uint32_t* mask, void* ws,
                    size_t ws_bytes, hipStream_t st) {
   Arena a(ws, ws_bytes);
-  FwdWs<D> w;
+  FwdWs<D, T> w;
   w.layout(a, s);
   if (!a.ok()) return fail(HG_ERR_CAPACITY, "forward workspace needs %zu bytes, got %zu", a.used, ws_bytes);
   const int32_t R = s->n_rel;
@@ -272,33 +294,33 @@ int layer_fwd_impl(const hg_subgraph* s, const hg_layer_desc* L, const float* Hi
   // (c) self transform per node type, bias folded in
   for (int t = 0; t < s->n_ntype; ++t) {
     const int64_t lo = s->type_off_host[t], hi = s->type_off_host[t + 1];
-    LoadRows<D> la{Hin, rows_contig(lo)};
-    StoreRows<D> ep{w.Yself, rows_contig(lo), bias ? bias + (int64_t)t * D : nullptr, nullptr};
-    HG_TRY((launch_gemm_rows<D, false>("gemm_fwd_self", hi - lo, W_self + (int64_t)t * D * D, la, ep, st)));
+    LoadRows<D, T> la{Hin, rows_contig(lo)};
+    StoreRows<D, T> ep{w.Yself, rows_contig(lo), bias ? bias + (int64_t)t * D : nullptr, nullptr};
+    HG_TRY((transform<D, T, false>("gemm_fwd_self", hi - lo, W_self + (int64_t)t * D * D, la, ep, st)));
   }
   // (c) relation transforms over the active sources
   int64_t off = 0;
   for (int r = 0; r < R; ++r) {
     const int64_t n = s->n_active[r];
-    LoadRows<D> la{Hin, rows_list(pv.active + off)};
-    StoreRows<D> ep{w.Y, rows_list(pv.active + off, R, r), nullptr, nullptr};
-    HG_TRY((launch_gemm_rows<D, false>("gemm_fwd_rel", n, W_rel + (int64_t)r * D * D, la, ep, st)));
+    LoadRows<D, T> la{Hin, rows_list(pv.active + off)};
+    StoreRows<D, T> ep{w.Y, rows_list(pv.active + off, R, r), nullptr, nullptr};
+    HG_TRY((transform<D, T, false>("gemm_fwd_rel", n, W_rel + (int64_t)r * D * D, la, ep, st)));
     off += n;
   }
   // (b) aggregation + epilogue
   if (s->n_sub > 0)
-    HG_LAUNCH("spmm_fwd", k_spmm_fwd<D>, dim3(wave_grid(s->n_sub)), dim3(256), 0, st, s->n_sub, R,
-              (const int32_t*)s->csr_ptr, (const int32_t*)s->csr_col, (const float*)w.Y,
-              (const float*)w.Yself, Hin, Hout, mask, L->relu, L->residual);
+    HG_LAUNCH("spmm_fwd", (k_spmm_fwd<D, T>), dim3(wave_grid(s->n_sub)), dim3(256), 0, st, s->n_sub, R,
+              (const int32_t*)s->csr_ptr, (const int32_t*)s->csr_col, (const T*)w.Y, (const T*)w.Yself, Hin,
+              Hout, mask, L->relu, L->residual);
   return HG_OK;
 }
 
-template <int D>
-int layer_bwd_impl(const hg_subgraph* s, const hg_layer_desc* L, const float* Hin, const float* W_rel,
-                   const float* W_self, const uint32_t* mask, const float* G, float* dHin, float* dW_rel,
+template <int D, class T>
+int layer_bwd_impl(const hg_subgraph* s, const hg_layer_desc* L, const T* Hin, const float* W_rel,
+                   const float* W_self, const uint32_t* mask, const T* G, T* dHin, float* dW_rel,
                    float* dW_self, float* dbias, void* ws, size_t ws_bytes, hipStream_t st) {
   Arena a(ws, ws_bytes);
-  BwdWs<D> w;
+  BwdWs<D, T> w;
   w.layout(a, s);
   if (!a.ok()) return fail(HG_ERR_CAPACITY, "backward workspace needs %zu bytes, got %zu", a.used, ws_bytes);
   const int32_t R = s->n_rel;
@@ -307,45 +329,57 @@ int layer_bwd_impl(const hg_subgraph* s, const hg_layer_desc* L, const float* Hi
   // dZ = G * mask and also writes it out for the SpMM and dW_self
   for (int t = 0; t < s->n_ntype; ++t) {
     const int64_t lo = s->type_off_host[t], hi = s->type_off_host[t + 1];
-    LoadMasked<D> la{G, mask, rows_contig(lo), w.dZ};
-    StoreRows<D> ep{dHin, rows_contig(lo), nullptr, L->residual ? G : nullptr};
-    HG_TRY((launch_gemm_rows<D, true>("gemm_bwd_dx_self", hi - lo, W_self + (int64_t)t * D * D, la, ep, st)));
+    LoadMasked<D, T> la{G, mask, rows_contig(lo), w.dZ};
+    StoreRows<D, T> ep{dHin, rows_contig(lo), nullptr, L->residual ? G : nullptr};
+    HG_TRY((transform<D, T, true>("gemm_bwd_dx_self", hi - lo, W_self + (int64_t)t * D * D, la, ep, st)));
   }
   // (b) transposed SpMM
   if (s->plan_items > 0)
-    HG_LAUNCH("spmm_bwd", k_spmm_bwd<D>, dim3(wave_grid(s->plan_items)), dim3(256), 0, st,
+    HG_LAUNCH("spmm_bwd", (k_spmm_bwd<D, T>), dim3(wave_grid(s->plan_items)), dim3(256), 0, st,
               (int64_t)s->plan_items, pv.items, (const int32_t*)s->csc_row, (const float*)s->csc_scale,
-              (const float*)w.dZ, w.dY, w.part);
+              (const T*)w.dZ, w.dY, w.part);
   if (s->plan_heavy > 0)
-    HG_LAUNCH("spmm_bwd_reduce", k_heavy_reduce<D>, dim3(wave_grid(s->plan_heavy)), dim3(256), 0, st,
+    HG_LAUNCH("spmm_bwd_reduce", (k_heavy_reduce<D, T>), dim3(wave_grid(s->plan_heavy)), dim3(256), 0, st,
               (int64_t)s->plan_heavy, pv.heavy, (const double*)w.part, w.dY);
   // (c) dH += dY_r W_r^T per relation, in relation order
   int64_t off = 0;
   for (int r = 0; r < R; ++r) {
     const int64_t n = s->n_active[r];
-    LoadRows<D> la{w.dY, rows_list(pv.active + off, R, r)};
-    StoreRows<D> ep{dHin, rows_list(pv.active + off), nullptr, dHin};
-    HG_TRY((launch_gemm_rows<D, true>("gemm_bwd_dx_rel", n, W_rel + (int64_t)r * D * D, la, ep, st)));
+    LoadRows<D, T> la{w.dY, rows_list(pv.active + off, R, r)};
+    StoreRows<D, T> ep{dHin, rows_list(pv.active + off), nullptr, dHin};
+    HG_TRY((transform<D, T, true>("gemm_bwd_dx_rel", n, W_rel + (int64_t)r * D * D, la, ep, st)));
     off += n;
   }
   // (c) weight gradients, split-K
   for (int t = 0; t < s->n_ntype; ++t) {
     const int64_t lo = s->type_off_host[t], hi = s->type_off_host[t + 1];
-    LoadRows<D> la{Hin, rows_contig(lo)};
-    LoadRows<D> lb{w.dZ, rows_contig(lo)};
+    LoadRows<D, T> la{Hin, rows_contig(lo)};
+    LoadRows<D, T> lb{w.dZ, rows_contig(lo)};
     HG_TRY((launch_gemm_tn<D>("gemm_bwd_dw_self", hi - lo, la, lb, w.splitk, w.colsum,
                               dW_self + (int64_t)t * D * D, dbias ? dbias + (int64_t)t * D : nullptr, 0, st)));
   }
   off = 0;
   for (int r = 0; r < R; ++r) {
     const int64_t n = s->n_active[r];
-    LoadRows<D> la{Hin, rows_list(pv.active + off)};
-    LoadRows<D> lb{w.dY, rows_list(pv.active + off, R, r)};
+    LoadRows<D, T> la{Hin, rows_list(pv.active + off)};
+    LoadRows<D, T> lb{w.dY, rows_list(pv.active + off, R, r)};
     HG_TRY((launch_gemm_tn<D>("gemm_bwd_dw_rel", n, la, lb, w.splitk, w.colsum, dW_rel + (int64_t)r * D * D,
                               nullptr, 0, st)));
     off += n;
   }
   return HG_OK;
+}
+
+template <template <int, class> class WS>
+size_t ws_size(const hg_subgraph* s, const hg_layer_desc* L) {
+  Sizer z;
+  const bool bf = L->dtype == HG_DTYPE_BF16;
+  switch (L->d_in) {
+    case 64: if (bf) { WS<64, bf16_t> w; w.layout(z, s); } else { WS<64, float> w; w.layout(z, s); } break;
+    case 128: if (bf) { WS<128, bf16_t> w; w.layout(z, s); } else { WS<128, float> w; w.layout(z, s); } break;
+    default: { WS<256, bf16_t> w; w.layout(z, s); } break;
+  }
+  return z.used + 256;
 }
 
 }  // namespace
@@ -361,28 +395,12 @@ extern "C" size_t hg_layer_saved_size(const hg_subgraph* s, const hg_layer_desc*
 
 extern "C" size_t hg_layer_fwd_workspace_size(const hg_subgraph* s, const hg_layer_desc* L) {
   if (validate_layer(s, L) != HG_OK) return 0;
-  Sizer z;
-  if (L->d_in == 64) {
-    FwdWs<64> w;
-    w.layout(z, s);
-  } else {
-    FwdWs<128> w;
-    w.layout(z, s);
-  }
-  return z.used + 256;
+  return ws_size<FwdWs>(s, L);
 }
 
 extern "C" size_t hg_layer_bwd_workspace_size(const hg_subgraph* s, const hg_layer_desc* L) {
   if (validate_layer(s, L) != HG_OK) return 0;
-  Sizer z;
-  if (L->d_in == 64) {
-    BwdWs<64> w;
-    w.layout(z, s);
-  } else {
-    BwdWs<128> w;
-    w.layout(z, s);
-  }
-  return z.used + 256;
+  return ws_size<BwdWs>(s, L);
 }
 
 extern "C" int hg_layer_fwd(const hg_subgraph* s, const hg_layer_desc* L, const void* H_in,
@@ -393,11 +411,18 @@ extern "C" int hg_layer_fwd(const hg_subgraph* s, const hg_layer_desc* L, const 
     return fail(HG_ERR_ARG, "null layer argument");
   if (H_in == H_out && s->n_sub > 0) return fail(HG_ERR_ARG, "H_out must not alias H_in");
   hipStream_t st = static_cast<hipStream_t>(stream);
-  if (L->d_in == 64)
-    return layer_fwd_impl<64>(s, L, (const float*)H_in, W_rel, W_self, bias, (float*)H_out,
-                              (uint32_t*)saved, ws, ws_bytes, st);
-  return layer_fwd_impl<128>(s, L, (const float*)H_in, W_rel, W_self, bias, (float*)H_out,
-                             (uint32_t*)saved, ws, ws_bytes, st);
+  uint32_t* m = (uint32_t*)saved;
+  if (L->dtype == HG_DTYPE_BF16) {
+    const bf16_t* hi = (const bf16_t*)H_in;
+    bf16_t* ho = (bf16_t*)H_out;
+    if (L->d_in == 64) return layer_fwd_impl<64, bf16_t>(s, L, hi, W_rel, W_self, bias, ho, m, ws, ws_bytes, st);
+    if (L->d_in == 128) return layer_fwd_impl<128, bf16_t>(s, L, hi, W_rel, W_self, bias, ho, m, ws, ws_bytes, st);
+    return layer_fwd_impl<256, bf16_t>(s, L, hi, W_rel, W_self, bias, ho, m, ws, ws_bytes, st);
+  }
+  const float* hi = (const float*)H_in;
+  float* ho = (float*)H_out;
+  if (L->d_in == 64) return layer_fwd_impl<64, float>(s, L, hi, W_rel, W_self, bias, ho, m, ws, ws_bytes, st);
+  return layer_fwd_impl<128, float>(s, L, hi, W_rel, W_self, bias, ho, m, ws, ws_bytes, st);
 }
 
 extern "C" int hg_layer_bwd(const hg_subgraph* s, const hg_layer_desc* L, const void* H_in,
@@ -409,9 +434,21 @@ extern "C" int hg_layer_bwd(const hg_subgraph* s, const hg_layer_desc* L, const 
   if (s->n_sub > 0 && (!H_in || !saved || !dH_out || !dH_in)) return fail(HG_ERR_ARG, "null layer argument");
   if (dH_in == dH_out && s->n_sub > 0) return fail(HG_ERR_ARG, "dH_in must not alias dH_out");
   hipStream_t st = static_cast<hipStream_t>(stream);
+  const uint32_t* m = (const uint32_t*)saved;
+  if (L->dtype == HG_DTYPE_BF16) {
+    const bf16_t* hi = (const bf16_t*)H_in;
+    const bf16_t* g = (const bf16_t*)dH_out;
+    bf16_t* dh = (bf16_t*)dH_in;
+    if (L->d_in == 64)
+      return layer_bwd_impl<64, bf16_t>(s, L, hi, W_rel, W_self, m, g, dh, dW_rel, dW_self, dbias, ws, ws_bytes, st);
+    if (L->d_in == 128)
+      return layer_bwd_impl<128, bf16_t>(s, L, hi, W_rel, W_self, m, g, dh, dW_rel, dW_self, dbias, ws, ws_bytes, st);
+    return layer_bwd_impl<256, bf16_t>(s, L, hi, W_rel, W_self, m, g, dh, dW_rel, dW_self, dbias, ws, ws_bytes, st);
+  }
+  const float* hi = (const float*)H_in;
+  const float* g = (const float*)dH_out;
+  float* dh = (float*)dH_in;
   if (L->d_in == 64)
-    return layer_bwd_impl<64>(s, L, (const float*)H_in, W_rel, W_self, (const uint32_t*)saved,
-                              (const float*)dH_out, (float*)dH_in, dW_rel, dW_self, dbias, ws, ws_bytes, st);
-  return layer_bwd_impl<128>(s, L, (const float*)H_in, W_rel, W_self, (const uint32_t*)saved,
-                             (const float*)dH_out, (float*)dH_in, dW_rel, dW_self, dbias, ws, ws_bytes, st);
+    return layer_bwd_impl<64, float>(s, L, hi, W_rel, W_self, m, g, dh, dW_rel, dW_self, dbias, ws, ws_bytes, st);
+  return layer_bwd_impl<128, float>(s, L, hi, W_rel, W_self, m, g, dh, dW_rel, dW_self, dbias, ws, ws_bytes, st);
 }

@@ -20,6 +20,71 @@ namespace hg {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef double f64x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef uint16_t bf16_t;  // bfloat16 storage
+
+__device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
+
+// float -> bfloat16, round to nearest even (NaN kept quiet).
+__device__ __forceinline__ uint16_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7FFFFFFFu) > 0x7F800000u) return (uint16_t)((u >> 16) | 0x40u);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+__device__ __forceinline__ uint32_t pack2bf(float a, float b) {
+  return (uint32_t)f2bf(a) | ((uint32_t)f2bf(b) << 16);
+}
+
+// Element types of feature rows: 16-byte chunks hold EL elements.
+template <class T>
+struct Elt;
+template <>
+struct Elt<float> {
+  static constexpr int EL = 4;
+  __device__ static __forceinline__ void load(const float* p, float (&v)[4]) {
+    const f32x4 x = *reinterpret_cast<const f32x4*>(p);
+    v[0] = x[0]; v[1] = x[1]; v[2] = x[2]; v[3] = x[3];
+  }
+  __device__ static __forceinline__ void store(float* p, const float (&v)[4]) {
+    *reinterpret_cast<f32x4*>(p) = f32x4{v[0], v[1], v[2], v[3]};
+  }
+  __device__ static __forceinline__ float get(const float* p) { return *p; }
+  __device__ static __forceinline__ f32x4 load4(const float* p) { return *reinterpret_cast<const f32x4*>(p); }
+};
+template <>
+struct Elt<bf16_t> {
+  static constexpr int EL = 8;
+  __device__ static __forceinline__ void load(const bf16_t* p, float (&v)[8]) {
+    const uint4 x = *reinterpret_cast<const uint4*>(p);
+    const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      v[2 * q] = __uint_as_float(w[q] << 16);
+      v[2 * q + 1] = __uint_as_float(w[q] & 0xFFFF0000u);
+    }
+  }
+  __device__ static __forceinline__ void store(bf16_t* p, const float (&v)[8]) {
+    uint4 x;
+    x.x = pack2bf(v[0], v[1]);
+    x.y = pack2bf(v[2], v[3]);
+    x.z = pack2bf(v[4], v[5]);
+    x.w = pack2bf(v[6], v[7]);
+    *reinterpret_cast<uint4*>(p) = x;
+  }
+  __device__ static __forceinline__ float get(const bf16_t* p) { return bf2f(*p); }
+  __device__ static __forceinline__ f32x4 load4(const bf16_t* p) {
+    const uint2 x = *reinterpret_cast<const uint2*>(p);
+    return f32x4{__uint_as_float(x.x << 16), __uint_as_float(x.x & 0xFFFF0000u),
+                 __uint_as_float(x.y << 16), __uint_as_float(x.y & 0xFFFF0000u)};
+  }
+};
+
+__device__ __forceinline__ f32x4 mfma_bf16(uint4 a, uint4 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b),
+                                                 c, 0, 0, 0);
+}
 
 __device__ __forceinline__ f32x4 mfma4(float a, float b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
@@ -46,28 +111,39 @@ inline RowMap rows_list(const int32_t* list, int32_t mul = 1, int32_t add = 0) {
 
 // ---- A loaders: rowp(i) = address of segment row i; load4 / load1 read
 // columns of that row (with an optional per-column transform) ------------------
-template <int D>
+template <int D, class T = float>
 struct LoadRows {
-  const float* base;
+  const T* base;
   RowMap map;
-  __device__ __forceinline__ const float* rowp(int64_t i) const { return base + map(i) * D; }
-  __device__ __forceinline__ f32x4 load4(const float* p, int c) const {
-    return *reinterpret_cast<const f32x4*>(p + c);
+  __device__ __forceinline__ const T* rowp(int64_t i) const { return base + map(i) * D; }
+  __device__ __forceinline__ f32x4 load4(const T* p, int c) const { return Elt<T>::load4(p + c); }
+  // 8 consecutive columns as bfloat16 (the bf16 MFMA operand)
+  __device__ __forceinline__ uint4 load8bf(const T* p, int c) const {
+    if constexpr (sizeof(T) == 2) {
+      return *reinterpret_cast<const uint4*>(p + c);
+    } else {
+      const f32x4 x = load4(p, c), y = load4(p, c + 4);
+      return uint4{pack2bf(x[0], x[1]), pack2bf(x[2], x[3]), pack2bf(y[0], y[1]), pack2bf(y[2], y[3])};
+    }
   }
-  __device__ __forceinline__ float load1(const float* p, int c) const { return p[c]; }
-  __device__ __forceinline__ float at(int64_t i, int c) const { return rowp(i)[c]; }
+  __device__ __forceinline__ float load1(const T* p, int c) const { return Elt<T>::get(p + c); }
+  __device__ __forceinline__ float at(int64_t i, int c) const { return load1(rowp(i), c); }
 };
 
 // (x - mu[c]) * sc[c]: the per-column standardisation of the alignment loss.
-template <int D>
+template <int D, class T = float>
 struct LoadStd {
-  const float* base;
+  const T* base;
   RowMap map;
   const float* mu;
   const float* sc;
-  __device__ __forceinline__ const float* rowp(int64_t i) const { return base + map(i) * D; }
-  __device__ __forceinline__ f32x4 load4(const float* p, int c) const {
-    f32x4 x = *reinterpret_cast<const f32x4*>(p + c);
+  __device__ __forceinline__ const T* rowp(int64_t i) const { return base + map(i) * D; }
+  __device__ __forceinline__ uint4 load8bf(const T* p, int c) const {
+    const f32x4 x = load4(p, c), y = load4(p, c + 4);
+    return uint4{pack2bf(x[0], x[1]), pack2bf(x[2], x[3]), pack2bf(y[0], y[1]), pack2bf(y[2], y[3])};
+  }
+  __device__ __forceinline__ f32x4 load4(const T* p, int c) const {
+    f32x4 x = Elt<T>::load4(p + c);
     f32x4 m = *reinterpret_cast<const f32x4*>(mu + c);
     f32x4 s = *reinterpret_cast<const f32x4*>(sc + c);
     f32x4 r;
@@ -77,34 +153,51 @@ struct LoadStd {
     r[3] = (x[3] - m[3]) * s[3];
     return r;
   }
-  __device__ __forceinline__ float load1(const float* p, int c) const { return (p[c] - mu[c]) * sc[c]; }
+  __device__ __forceinline__ float load1(const T* p, int c) const { return (Elt<T>::get(p + c) - mu[c]) * sc[c]; }
   __device__ __forceinline__ float at(int64_t i, int c) const { return load1(rowp(i), c); }
 };
 
 // dZ = G * mask read on the fly: the ReLU mask row of G row r holds bit c of
 // column c at word r*(D/32) + c/32.
-template <int D>
+template <int D, class T = float>
 struct LoadMasked {
-  const float* G;
+  const T* G;
   const uint32_t* mask;
   RowMap map;
-  float* tee;  // if set, load4 also stores the masked values here (same offsets as G)
-  __device__ __forceinline__ const float* rowp(int64_t i) const { return G + map(i) * D; }
-  __device__ __forceinline__ uint32_t word(const float* p, int c) const {
+  T* tee;  // if set, loads also store the masked values here (same offsets as G)
+  __device__ __forceinline__ const T* rowp(int64_t i) const { return G + map(i) * D; }
+  __device__ __forceinline__ uint32_t word(const T* p, int c) const {
     const int64_t r = (p - G) / D;
     return mask[r * (D / 32) + (c >> 5)];
   }
-  __device__ __forceinline__ f32x4 load4(const float* p, int c) const {
-    f32x4 x = *reinterpret_cast<const f32x4*>(p + c);
+  __device__ __forceinline__ f32x4 load4(const T* p, int c) const {
+    f32x4 x = Elt<T>::load4(p + c);
     const uint32_t nib = word(p, c) >> (c & 31);
 #pragma unroll
     for (int q = 0; q < 4; ++q)
       if (!((nib >> q) & 1u)) x[q] = 0.f;
-    if (tee) *reinterpret_cast<f32x4*>(tee + (p - G) + c) = x;
+    if constexpr (sizeof(T) == 4) {
+      if (tee) *reinterpret_cast<f32x4*>(tee + (p - G) + c) = x;
+    }
     return x;
   }
-  __device__ __forceinline__ float load1(const float* p, int c) const {
-    return ((word(p, c) >> (c & 31)) & 1u) ? p[c] : 0.f;
+  __device__ __forceinline__ uint4 load8bf(const T* p, int c) const {
+    static_assert(sizeof(T) == 2, "load8bf of masked rows is the bfloat16 path");
+    uint4 x = *reinterpret_cast<const uint4*>(p + c);
+    const uint32_t byte = (word(p, c) >> (c & 31)) & 0xFFu;
+    uint32_t w[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const uint32_t lo = ((byte >> (2 * q)) & 1u) ? 0x0000FFFFu : 0u;
+      const uint32_t hi = ((byte >> (2 * q + 1)) & 1u) ? 0xFFFF0000u : 0u;
+      w[q] &= (lo | hi);
+    }
+    x = uint4{w[0], w[1], w[2], w[3]};
+    if (tee) *reinterpret_cast<uint4*>(tee + (p - G) + c) = x;
+    return x;
+  }
+  __device__ __forceinline__ float load1(const T* p, int c) const {
+    return ((word(p, c) >> (c & 31)) & 1u) ? Elt<T>::get(p + c) : 0.f;
   }
   __device__ __forceinline__ float at(int64_t i, int c) const { return load1(rowp(i), c); }
 };
@@ -114,20 +207,24 @@ struct LoadMasked {
 // element of the tile (all loads), then store(i, ro, c, acc, pre) (all stores):
 // the two phases keep loads from waiting behind stores when the addend is the
 // output itself (dH += ...).
-template <int D>
+template <int D, class T = float>
 struct StoreRows {
-  float* out;
+  T* out;
   RowMap map;
-  const float* bias;    // [D] or null
-  const float* addend;  // rows through the same map, or null (may equal out)
+  const float* bias;  // [D] or null
+  const T* addend;    // rows through the same map, or null (may equal out)
   __device__ __forceinline__ int64_t row(int64_t i) const { return map(i); }
   __device__ __forceinline__ float pre(int64_t, int64_t ro, int c) const {
     float v = bias ? bias[c] : 0.f;
-    if (addend) v += addend[ro * D + c];
+    if (addend) v += Elt<T>::get(addend + ro * D + c);
     return v;
   }
   __device__ __forceinline__ void store(int64_t, int64_t ro, int c, float acc, float pre) const {
-    out[ro * D + c] = acc + pre;
+    if constexpr (sizeof(T) == 4) {
+      out[ro * D + c] = acc + pre;
+    } else {
+      out[ro * D + c] = f2bf(acc + pre);
+    }
   }
 };
 
@@ -175,7 +272,7 @@ __global__ void __launch_bounds__(kGemmThreads) k_gemm_rows(int64_t n_rows, cons
     {
       const int64_t ia = r0 + c;
       if (ia < n_rows) {
-        const float* p = aload.rowp(ia);
+        const auto p = aload.rowp(ia);
 #pragma unroll
         for (int kb = 0; kb < NB; ++kb) a[kb] = aload.load4(p, 16 * kb + 4 * g);
       } else {
@@ -233,6 +330,116 @@ int launch_gemm_rows(const char* name, int64_t n_rows, const float* W, ALoad alo
   return HG_OK;
 }
 
+// ---- gemm_rows, bfloat16 MFMA ----------------------------------------------------
+// v_mfma_f32_16x16x32_bf16: lane (c, g) supplies A[row c][32 kb + 8 g + e],
+// e = 0..7 -- eight consecutive columns, one 16-byte load -- and
+// op(W)[32 kb + 8 g + e][16 nb + c] from LDS, where op(W) is staged rounded to
+// bfloat16 in fragment order (uint4 element (kb*NB + nb)*64 + lane).  A block
+// is RG row groups x CG column groups of waves; a wave owns 16 rows and D/CG
+// columns.  Accumulation is float32.
+template <int D>
+struct BfShape {
+  static constexpr int CG = D >= 256 ? 4 : 1;
+  static constexpr int RG = D >= 256 ? 4 : 8;
+  static constexpr int kThreads = 64 * CG * RG;
+};
+
+template <int D, bool kTransW, class ALoad, class Epi>
+__global__ void __launch_bounds__(BfShape<D>::kThreads) k_gemm_rows_bf16(int64_t n_rows, const float* __restrict__ W,
+                                                                       ALoad aload, Epi epi) {
+  constexpr int NB = D / 16, KB = D / 32;
+  constexpr int CG = BfShape<D>::CG, RG = BfShape<D>::RG, NT = BfShape<D>::kThreads;
+  constexpr int NBW = NB / CG;
+  extern __shared__ uint4 wlb[];
+  const int tid = threadIdx.x;
+  for (int e = tid; e < KB * NB * 64; e += NT) {
+    const int l = e & 63;
+    const int nb = (e >> 6) % NB;
+    const int kb = (e >> 6) / NB;
+    const int j = 16 * nb + (l & 15);
+    const int k0 = 32 * kb + 8 * (l >> 4);
+    float v[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) v[q] = kTransW ? W[(int64_t)j * D + k0 + q] : W[(int64_t)(k0 + q) * D + j];
+    wlb[e] = uint4{pack2bf(v[0], v[1]), pack2bf(v[2], v[3]), pack2bf(v[4], v[5]), pack2bf(v[6], v[7])};
+  }
+  __syncthreads();
+  const int w = tid >> 6;
+  const int rg = w / CG, cg = w % CG;
+  const int l = lane64();
+  const int g = l >> 4, c = l & 15;
+  constexpr int kRowsPerTile = 16 * RG;
+  const int64_t ntiles = (n_rows + kRowsPerTile - 1) / kRowsPerTile;
+  for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
+    const int64_t r0 = t * kRowsPerTile + 16 * rg;
+    uint4 a[KB];
+    {
+      const int64_t ia = r0 + c;
+      if (ia < n_rows) {
+        const auto p = aload.rowp(ia);
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb) a[kb] = aload.load8bf(p, 32 * kb + 8 * g);
+      } else {
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb) a[kb] = uint4{0u, 0u, 0u, 0u};
+      }
+    }
+    f32x4 acc[NBW];
+#pragma unroll
+    for (int nb = 0; nb < NBW; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+      __builtin_amdgcn_sched_barrier(0);
+      uint4 b[NBW];
+#pragma unroll
+      for (int nb = 0; nb < NBW; ++nb) b[nb] = wlb[(kb * NB + cg * NBW + nb) * 64 + l];
+#pragma unroll
+      for (int nb = 0; nb < NBW; ++nb) acc[nb] = mfma_bf16(a[kb], b[nb], acc[nb]);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    int64_t ro[4];
+    float pre[4][NBW];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int64_t i = r0 + 4 * g + v;
+      ro[v] = (i < n_rows) ? epi.row(i) : 0;
+#pragma unroll
+      for (int nb = 0; nb < NBW; ++nb)
+        pre[v][nb] = (i < n_rows) ? epi.pre(i, ro[v], 16 * (cg * NBW + nb) + c) : 0.f;
+    }
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int64_t i = r0 + 4 * g + v;
+      if (i < n_rows) {
+#pragma unroll
+        for (int nb = 0; nb < NBW; ++nb)
+          epi.store(i, ro[v], 16 * (cg * NBW + nb) + c, acc[nb][v], pre[v][nb]);
+      }
+    }
+  }
+}
+
+template <int D, bool kTransW, class ALoad, class Epi>
+int launch_gemm_rows_bf16(const char* name, int64_t n_rows, const float* W, ALoad aload, Epi epi,
+                          hipStream_t s) {
+  if (n_rows <= 0) return HG_OK;
+  const int64_t tiles = cdiv(n_rows, 16 * BfShape<D>::RG);
+  const int64_t cap = (int64_t)num_cus() * (D >= 256 ? 1 : 2);
+  const int64_t grid = tiles < cap ? tiles : cap;
+  const size_t lds = sizeof(uint16_t) * D * D;
+  auto kern = k_gemm_rows_bf16<D, kTransW, ALoad, Epi>;
+  if (lds > 65536) {
+    static bool attr_set = false;
+    if (!attr_set) {
+      HG_HIP_TRY(hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
+      attr_set = true;
+    }
+  }
+  HG_LAUNCH(name, kern, dim3((unsigned)grid), dim3(BfShape<D>::kThreads), lds, s, n_rows, W, aload, epi);
+  return HG_OK;
+}
+
 // ---- gemm_tn split-K ----------------------------------------------------------
 // partial[chunk][i][j] = sum_{rows k of the chunk} A[k][i] * B[k][j]
 // colsum[chunk][j]    = sum_{rows k of the chunk} B[k][j]        (if colsum)
@@ -247,8 +454,8 @@ template <int D, class LA, class LB>
 __global__ void __launch_bounds__(256) k_gemm_tn(int64_t n_rows, int64_t kc, LA la, LB lb,
                                                  float* __restrict__ partial,
                                                  float* __restrict__ colsum) {
-  static_assert(D == 64 || D == 128, "gemm_tn: d must be 64 or 128");
-  constexpr bool kQuad = (D == 128);
+  static_assert(D == 64 || D == 128 || D == 256, "gemm_tn: d must be 64, 128 or 256");
+  constexpr bool kQuad = (D >= 128);
   constexpr int U = 4;
   const int w = threadIdx.x >> 6;
   const int l = lane64();
@@ -260,7 +467,10 @@ __global__ void __launch_bounds__(256) k_gemm_tn(int64_t n_rows, int64_t kc, LA 
   const int qj = kQuad ? (w & 1) : 0;
   const int64_t step0 = kQuad ? 0 : 4 * w;
   const int64_t stride = kQuad ? 4 : 16;
-  const int ca = 64 * qi + 4 * c, cb = 64 * qj + 4 * c;
+  // D = 256: blockIdx.y picks the 128 x 128 output tile (ti, tj)
+  const int ti = (D == 256) ? (int)(blockIdx.y >> 1) : 0;
+  const int tj = (D == 256) ? (int)(blockIdx.y & 1) : 0;
+  const int ca = 128 * ti + 64 * qi + 4 * c, cb = 128 * tj + 64 * qj + 4 * c;
   f32x4 acc[4][4];
   f32x4 bs = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -273,8 +483,10 @@ __global__ void __launch_bounds__(256) k_gemm_tn(int64_t n_rows, int64_t kc, LA 
     for (int u = 0; u < U; ++u) {
       const int64_t row = k0 + u * stride + g;
       if (row < k_end) {
-        a[u] = la.load4(la.rowp(row), ca);
-        b[u] = lb.load4(lb.rowp(row), cb);
+        const auto pa = la.rowp(row);
+        const auto pb = lb.rowp(row);
+        a[u] = la.load4(pa, ca);
+        b[u] = lb.load4(pb, cb);
       } else {
         a[u] = b[u] = f32x4{0.f, 0.f, 0.f, 0.f};
       }
@@ -300,13 +512,13 @@ __global__ void __launch_bounds__(256) k_gemm_tn(int64_t n_rows, int64_t kc, LA 
     for (int bi = 0; bi < 4; ++bi)
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
-        const int64_t i = 64 * qi + 4 * (4 * g + v) + bi;
+        const int64_t i = 128 * ti + 64 * qi + 4 * (4 * g + v) + bi;
         f32x4 row4;
 #pragma unroll
         for (int bj = 0; bj < 4; ++bj) row4[bj] = acc[bi][bj][v];
         *reinterpret_cast<f32x4*>(out + i * D + cb) = row4;
       }
-    if (colsum && qi == 0 && g == 0) *reinterpret_cast<f32x4*>(colsum + chunk * D + cb) = bs;
+    if (colsum && ti == 0 && qi == 0 && g == 0) *reinterpret_cast<f32x4*>(colsum + chunk * D + cb) = bs;
   } else {
     __shared__ float red[64 * 64];
     __shared__ float cred[64];
@@ -402,7 +614,8 @@ int launch_gemm_tn(const char* name, int64_t n_rows, LA la, LB lb, float* partia
   }
   const int64_t kc = splitk_chunk(n_rows);
   const int64_t chunks = cdiv(n_rows, kc);
-  HG_LAUNCH(name, (k_gemm_tn<D, LA, LB>), dim3((unsigned)chunks), dim3(256), 0, s, n_rows, kc, la,
+  const unsigned tiles = D == 256 ? 4u : 1u;
+  HG_LAUNCH(name, (k_gemm_tn<D, LA, LB>), dim3((unsigned)chunks, tiles), dim3(256), 0, s, n_rows, kc, la,
             lb, partial, out_colsum ? colsum : nullptr);
   const int64_t cap = (int64_t)num_cus() * 4 + 1;
   HG_TRY(reduce_partials(partial, chunks, (int64_t)D * D, partial + cap * D * D, out, accumulate, s));

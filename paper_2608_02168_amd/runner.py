@@ -63,29 +63,36 @@ def make_inputs(wl: synth.Workload, g: synth.Graph, device="cuda", feats: Option
                            want_eid=False)
     build_ws = sub.arrays["ws"]
     feats = synth.features(mc.seed, g.n_nodes, d) if feats is None else feats
+    fdt = torch.bfloat16 if mc.dtype == "bf16" else torch.float32
+    if mc.dtype == "bf16":
+        feats = synth.round_bf16(feats)
     l2g = sub.view("local2global").long()
-    h0 = _dev(feats, device).index_select(0, l2g).contiguous()
+    h0 = _dev(feats, device).index_select(0, l2g).to(fdt).contiguous()
     weights_np = [synth.layer_weights(mc.seed, li, cfg.n_rel, g.n_ntype, d, mc.bias_range)
                   for li in range(mc.n_layers)]
     weights = [(_dev(w.w_rel, device), _dev(w.w_self, device), _dev(w.bias, device)) for w in weights_np]
     m = sub.m_sel
     href_np = synth.reference_embeddings(mc.seed, max(m, 1), d)
     gext_np = synth.upstream_grad(mc.seed, max(sub.n_sub, 1), d)
+    if mc.dtype == "bf16":
+        href_np, gext_np = synth.round_bf16(href_np), synth.round_bf16(gext_np)
     omega = None
     if mc.weighted_align and m > 0:
         orel = sub.view("overlap_rel").cpu().numpy()
         omega = _dev(synth.align_weights(orel, g.rel, cfg.n_rel), device)
-    inp = StepInputs(wl, gd, g.k, sub, build_ws, h0, weights, weights_np, _dev(href_np[:m], device),
-                     _dev(gext_np[: sub.n_sub], device), omega, feats, href_np, gext_np)
+    inp = StepInputs(wl, gd, g.k, sub, build_ws, h0, weights, weights_np,
+                     _dev(href_np[:m], device).to(fdt), _dev(gext_np[: sub.n_sub], device).to(fdt),
+                     omega, feats, href_np, gext_np)
     ns = sub.n_sub
     f32 = dict(dtype=torch.float32, device=device)
-    inp.H = [h0] + [torch.empty((ns, d), **f32) for _ in range(mc.n_layers)]
+    act = dict(dtype=fdt, device=device)
+    inp.H = [h0] + [torch.empty((ns, d), **act) for _ in range(mc.n_layers)]
     inp.saved = [torch.empty((max(ns, 1), d // 32), dtype=torch.int32, device=device)
                  for _ in range(mc.n_layers)]
-    inp.dH = [torch.empty((ns, d), **f32) for _ in range(2)]
+    inp.dH = [torch.empty((ns, d), **act) for _ in range(2)]
     inp.grads = [(torch.empty_like(w[0]), torch.empty_like(w[1]), torch.empty_like(w[2])) for w in weights]
-    inp.fwd_ws = api._ws(api.hg_layer_fwd_workspace_size(sub, d), device)
-    inp.bwd_ws = api._ws(api.hg_layer_bwd_workspace_size(sub, d), device)
+    inp.fwd_ws = api._ws(api.hg_layer_fwd_workspace_size(sub, d, fdt), device)
+    inp.bwd_ws = api._ws(api.hg_layer_bwd_workspace_size(sub, d, fdt), device)
     inp.align_ws = api._ws(api.hg_align_workspace_size(m, d), device)
     inp.loss = torch.empty(3, **f32)
     return inp

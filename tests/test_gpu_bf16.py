@@ -1,0 +1,96 @@
+"""bfloat16 storage path (fp32 accumulation, fp32 weights): GPU against the
+oracle in float64 on the same bf16-rounded inputs, element-wise relative
+error <= 2e-2 with the RMS floor."""
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+from oracle import align, layer, select
+from paper_2608_02168_amd import api, runner, synth
+from tests.helpers import graph_to_dev, pack_mask, parity_err, unpack_mask, to_dev
+
+pytestmark = pytest.mark.gpu
+TOL = 2e-2
+
+
+def bf(x):
+    return torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).cuda().to(torch.bfloat16)
+
+
+def setup(cfg, d, seed=7):
+    g = synth.make_graph(cfg)
+    ref = select.build(g.src, g.dst, g.rel, g.ntype, g.part, g.k, cfg.n_rel, 2, cfg.budget)
+    dev = graph_to_dev(g)
+    sub = api.hg_build_csr(dev["src"], dev["dst"], dev["rel"], dev["ntype"], dev["part"], g.k,
+                           cfg.n_rel, 2, cfg.budget)
+    X = synth.round_bf16(synth.features(seed, g.n_nodes, d)[ref.local2global])
+    w = synth.layer_weights(seed, 0, cfg.n_rel, 2, d, 0.1)
+    return g, ref, sub, X, w
+
+
+@pytest.mark.parametrize("d", [64, 128, 256])
+def test_bf16_layer_forward_backward(d):
+    cfg = synth.WORKLOADS["tiny"].graph
+    g, ref, sub, X, w = setup(cfg, d)
+    out, Z = layer.forward(ref.n_sub, ref.src_l, ref.dst_l, ref.rel_l, ref.ntype_l, X, w.w_rel,
+                           w.w_self, w.bias)
+    H, saved = api.hg_layer_fwd(sub, bf(X), to_dev(w.w_rel), to_dev(w.w_self), to_dev(w.bias))
+    assert H.dtype == torch.bfloat16
+    assert parity_err(H.float().cpu().numpy(), out) <= TOL
+    got = unpack_mask(saved.cpu().numpy(), d)
+    diff = got != (Z > 0)
+    assert np.all(np.abs(Z[diff]) <= 2e-2 * np.sqrt(np.mean(Z * Z)))
+    G = synth.round_bf16(synth.upstream_grad(3, ref.n_sub, d))
+    mask = Z > 0
+    exp = layer.backward(ref.n_sub, ref.src_l, ref.dst_l, ref.rel_l, ref.ntype_l, X, w.w_rel, w.w_self,
+                         w.bias, G, mask=mask)
+    res = api.hg_layer_bwd(sub, bf(X), to_dev(w.w_rel), to_dev(w.w_self), to_dev(pack_mask(mask)), bf(G))
+    assert res[0].dtype == torch.bfloat16
+    for a, b, nm in zip(res, exp, ("dH", "dW_rel", "dW_self", "dbias")):
+        err = parity_err(a.float().cpu().numpy(), b)
+        assert err <= TOL, (nm, err)
+
+
+@pytest.mark.parametrize("d", [64, 256])
+def test_bf16_alignment(d):
+    rng = np.random.default_rng(d)
+    n, m = 6000, 3001
+    H = synth.round_bf16(synth.features(d, n, d) * rng.uniform(0.5, 2, d).astype(np.float32))
+    ov = np.sort(rng.choice(n, m, replace=False)).astype(np.int32)
+    Href = synth.round_bf16(0.5 * H[ov] + synth.reference_embeddings(d, m, d))
+    (li, ld, L), dX, dY = align.loss_and_grad(H[ov], Href, None, 2e-4, 0.1, 1e-5, 0)
+    G0 = synth.round_bf16(synth.upstream_grad(1, n, d))
+    dH = bf(G0)
+    dHref = torch.empty((m, d), dtype=torch.bfloat16, device="cuda")
+    loss = api.hg_align_loss_fwd_bwd(bf(H), to_dev(ov), bf(Href), dH, dH_ref=dHref).cpu().numpy()
+    for a, b in zip(loss, (li, ld, L)):
+        assert abs(a - b) <= TOL * abs(b)
+    exp = G0.astype(np.float64)
+    exp[ov] += dX
+    assert parity_err(dH.float().cpu().numpy()[ov], exp[ov]) <= TOL
+    # the increment itself, against the oracle's gradient scale
+    inc = dH.float().cpu().numpy()[ov] - G0[ov]
+    assert np.max(np.abs(inc - dX)) <= TOL * np.max(np.abs(dX)) + 1e-2 * np.max(np.abs(G0[ov])) * 2**-8
+    assert parity_err(dHref.float().cpu().numpy(), dY) <= TOL
+
+
+def test_bf16_step_runs_and_matches_layerwise():
+    """The d=256, 3-layer bf16 workload's recipe at reduced size through the
+    runner: first-layer output against the oracle on the same bf16 input."""
+    base = synth.WORKLOADS["large_bf16"]
+    wl = synth.Workload(synth.scaled(base.graph, 0.0005), base.model, "bf16-small")
+    g = synth.make_graph(wl.graph)
+    inp = runner.make_inputs(wl, g)
+    res = runner.run_step(inp)
+    torch.cuda.synchronize()
+    assert np.all(np.isfinite(res.loss.cpu().numpy()))
+    sub = inp.sub
+    ref = select.build(g.src, g.dst, g.rel, g.ntype, g.part, g.k, wl.graph.n_rel, 2, wl.graph.budget)
+    X = inp.h0.float().cpu().numpy()
+    w = inp.weights_np[0]
+    out, _ = layer.forward(ref.n_sub, ref.src_l, ref.dst_l, ref.rel_l, ref.ntype_l, X, w.w_rel, w.w_self, w.bias)
+    assert parity_err(inp.H[1].float().cpu().numpy(), out) <= TOL
+    for gw in res.grads:
+        for t in gw:
+            assert torch.isfinite(t).all()
