@@ -163,7 +163,7 @@ int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg_subgraph* 
 typedef struct hg_layer_desc {
   int32_t d_in;
   int32_t d_out;
-  int32_t dtype;     /* HG_DTYPE_F32 (d in {64,128}) or HG_DTYPE_BF16 (d in {64,128,256}) */
+  int32_t dtype;     /* HG_DTYPE_F32 or HG_DTYPE_BF16 (feature storage); d in {64, 128, 256} */
   int32_t relu;      /* 0 or 1 */
   int32_t residual;  /* 0 or 1 */
 } hg_layer_desc;
@@ -201,7 +201,8 @@ int hg_layer_bwd(const hg_subgraph* s, const hg_layer_desc* L, const void* H_in,
  * scale * dL/dX into rows overlap[b] of dH (scale = lambda_CCA).  If dH_ref is
  * not NULL it is OVERWRITTEN with scale * dL/dY.  H, dH: [n_rows, d];
  * H_ref, dH_ref: [M, d]; overlap entries distinct and in [0, n_rows).
- * M = 0 writes zeros.  Requires M > ddof, d in {64, 128, 256}. */
+ * M = 0 writes zeros.  Requires M > ddof, d in {64, 128, 256}.  dtype is
+ * the storage type of H, H_ref, dH and dH_ref (float32 or bfloat16). */
 size_t hg_align_workspace_size(int64_t M, int32_t d);
 int hg_align_loss_fwd_bwd(int64_t M, int32_t d, int32_t dtype, int64_t n_rows,
                           const void* H, const int32_t* overlap, const void* H_ref,

@@ -222,11 +222,7 @@ int colsum(const char* name, int64_t m, F f, float* part, float* out, hipStream_
 
 template <int D, class T, class ALoad, class Epi>
 int grad_gemm(int64_t m, const float* W, ALoad la, Epi ep, hipStream_t s) {
-  if constexpr (D <= 128) {
-    return launch_gemm_rows<D, false>("align_grad_gemm", m, W, la, ep, s);
-  } else {
-    return launch_gemm_rows_bf16<D, false>("align_grad_gemm", m, W, la, ep, s);
-  }
+  return launch_gemm_rows<D, false>("align_grad_gemm", m, W, la, ep, s);
 }
 
 template <int D, class T>
@@ -313,10 +309,8 @@ extern "C" int hg_align_loss_fwd_bwd(int64_t M, int32_t d, int32_t dtype, int64_
   if (M < 0 || n_rows < 0) return fail(HG_ERR_ARG, "negative size");
   if (!loss3) return fail(HG_ERR_ARG, "null loss3");
   if (dtype != HG_DTYPE_F32 && dtype != HG_DTYPE_BF16) return fail(HG_ERR_ARG, "dtype %d", dtype);
-  if (dtype == HG_DTYPE_F32 && d != 64 && d != 128)
-    return fail(HG_ERR_UNSUPPORTED, "float32 alignment supports d in {64, 128}, got %d", d);
-  if (dtype == HG_DTYPE_BF16 && d != 64 && d != 128 && d != 256)
-    return fail(HG_ERR_UNSUPPORTED, "bfloat16 alignment supports d in {64, 128, 256}, got %d", d);
+  if (d != 64 && d != 128 && d != 256)
+    return fail(HG_ERR_UNSUPPORTED, "alignment supports d in {64, 128, 256}, got %d", d);
   if (ddof < 0) return fail(HG_ERR_ARG, "ddof < 0");
   if (!(eps >= 0.f)) return fail(HG_ERR_ARG, "eps must be >= 0");
   if (M > n_rows) return fail(HG_ERR_ARG, "M %lld > n_rows %lld", (long long)M, (long long)n_rows);
@@ -334,5 +328,6 @@ extern "C" int hg_align_loss_fwd_bwd(int64_t M, int32_t d, int32_t dtype, int64_
   const float *h = (const float*)H, *r = (const float*)H_ref;
   float *dh = (float*)dH, *dr = (float*)dH_ref;
   if (d == 64) return align_impl<64, float>(M, h, overlap, r, w, lambda_n, scale, eps, ddof, loss3, dh, dr, ws, ws_bytes, s);
-  return align_impl<128, float>(M, h, overlap, r, w, lambda_n, scale, eps, ddof, loss3, dh, dr, ws, ws_bytes, s);
+  if (d == 128) return align_impl<128, float>(M, h, overlap, r, w, lambda_n, scale, eps, ddof, loss3, dh, dr, ws, ws_bytes, s);
+  return align_impl<256, float>(M, h, overlap, r, w, lambda_n, scale, eps, ddof, loss3, dh, dr, ws, ws_bytes, s);
 }

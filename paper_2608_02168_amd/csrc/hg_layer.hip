@@ -124,12 +124,12 @@ __global__ void __launch_bounds__(256) k_spmm_fwd(int64_t n_sub, int32_t R, cons
 // CSC rows of hub sources hold up to millions of entries, so each lane
 // accumulates in float64 (the kernel is bound by the gathers, not the adds);
 // split rows keep float64 partial rows.
-template <int D, class T>
+template <int D, class T, class TO>
 __global__ void __launch_bounds__(256) k_spmm_bwd(int64_t n_items, const int4* __restrict__ items,
                                                   const int32_t* __restrict__ csc_row,
                                                   const float* __restrict__ csc_scale,
                                                   const T* __restrict__ dZ,
-                                                  T* __restrict__ dY, double* __restrict__ partial) {
+                                                  TO* __restrict__ dY, double* __restrict__ partial) {
   constexpr int EL = Elt<T>::EL;
   constexpr int LPR = D / EL;
   constexpr int EPW = 64 / LPR;
@@ -182,10 +182,9 @@ __global__ void __launch_bounds__(256) k_spmm_bwd(int64_t n_items, const int4* _
       for (int k = 0; k < EL; ++k) acc[k] += __shfl_xor(acc[k], o, 64);
     if (slot == 0) {
       if (item.w < 0) {
-        float o[EL];
+        TO* o = dY + (int64_t)item.x * D + c0;
 #pragma unroll
-        for (int k = 0; k < EL; ++k) o[k] = (float)acc[k];
-        Elt<T>::store(dY + (int64_t)item.x * D + c0, o);
+        for (int k = 0; k < EL; ++k) o[k] = (TO)acc[k];
       } else {
         double* p = partial + (int64_t)item.w * D + c0;
 #pragma unroll
@@ -199,7 +198,7 @@ __global__ void __launch_bounds__(256) k_spmm_bwd(int64_t n_items, const int4* _
 template <int D, class T>
 __global__ void k_heavy_reduce(int64_t n_heavy, const int4* __restrict__ heavy,
                                const double* __restrict__ partial, T* __restrict__ dY) {
-  constexpr int EL = Elt<T>::EL;
+  constexpr int EL = 4;
   constexpr int LPR = D / EL;
   const int l = threadIdx.x & 63;
   const int64_t wave0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
@@ -215,11 +214,18 @@ __global__ void k_heavy_reduce(int64_t n_heavy, const int4* __restrict__ heavy,
 #pragma unroll
         for (int k = 0; k < EL; ++k) s[k] += p[k];
       }
-      float o[EL];
+      T* o = dY + (int64_t)hv.x * D + l * EL;
 #pragma unroll
-      for (int k = 0; k < EL; ++k) o[k] = (float)s[k];
-      Elt<T>::store(dY + (int64_t)hv.x * D + l * EL, o);
+      for (int k = 0; k < EL; ++k) o[k] = (T)s[k];
     }
+  }
+}
+
+__global__ void k_to_bf16(const float* __restrict__ x, bf16_t* __restrict__ y, int64_t n) {
+  for (int64_t i = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4; i < n;
+       i += (int64_t)gridDim.x * blockDim.x * 4) {
+    const f32x4 v = *reinterpret_cast<const f32x4*>(x + i);
+    *reinterpret_cast<uint2*>(y + i) = uint2{pack2bf(v[0], v[1]), pack2bf(v[2], v[3])};
   }
 }
 
@@ -235,10 +241,8 @@ int validate_layer(const hg_subgraph* s, const hg_layer_desc* L) {
   if (L->d_in != L->d_out) return fail(HG_ERR_UNSUPPORTED, "d_in %d != d_out %d", L->d_in, L->d_out);
   if (L->dtype != HG_DTYPE_F32 && L->dtype != HG_DTYPE_BF16)
     return fail(HG_ERR_ARG, "dtype %d", L->dtype);
-  if (L->dtype == HG_DTYPE_F32 && L->d_in != 64 && L->d_in != 128)
-    return fail(HG_ERR_UNSUPPORTED, "float32 layers support d in {64, 128}, got %d", L->d_in);
-  if (L->dtype == HG_DTYPE_BF16 && L->d_in != 64 && L->d_in != 128 && L->d_in != 256)
-    return fail(HG_ERR_UNSUPPORTED, "bfloat16 layers support d in {64, 128, 256}, got %d", L->d_in);
+  if (L->d_in != 64 && L->d_in != 128 && L->d_in != 256)
+    return fail(HG_ERR_UNSUPPORTED, "layers support d in {64, 128, 256}, got %d", L->d_in);
   if ((L->relu != 0 && L->relu != 1) || (L->residual != 0 && L->residual != 1))
     return fail(HG_ERR_ARG, "relu/residual must be 0 or 1");
   if (s->n_sub < 0 || s->n_rel < 1 || s->n_ntype < 1 || !s->csr_ptr || !s->csc_ptr || !s->plan)
@@ -256,15 +260,19 @@ struct FwdWs {
   }
 };
 
+// dZ keeps the feature type (it is G times a 0/1 mask, exact); dY and, for
+// bfloat16 features, the dH accumulator are float32 so hub rows keep full
+// precision until the single final rounding.
 template <int D, class T>
 struct BwdWs {
-  T *dZ, *dY;
-  float *splitk, *colsum;
+  T* dZ;
+  float *dY, *dhacc, *splitk, *colsum;
   double* part;
   template <class A>
   void layout(A& a, const hg_subgraph* s) {
     dZ = a.template take<T>(s->n_sub * (int64_t)D);
-    dY = a.template take<T>(s->n_sub * s->n_rel * (int64_t)D);
+    dY = a.template take<float>(s->n_sub * s->n_rel * (int64_t)D);
+    dhacc = a.template take<float>(sizeof(T) == 2 ? s->n_sub * (int64_t)D : 0);
     part = a.template take<double>(s->plan_partials * (int64_t)D);
     splitk = a.template take<float>(splitk_max_chunks() * (int64_t)D * D);
     colsum = a.template take<float>(splitk_max_chunks() * (int64_t)D);
@@ -325,30 +333,37 @@ int layer_bwd_impl(const hg_subgraph* s, const hg_layer_desc* L, const T* Hin, c
   if (!a.ok()) return fail(HG_ERR_CAPACITY, "backward workspace needs %zu bytes, got %zu", a.used, ws_bytes);
   const int32_t R = s->n_rel;
   const PlanView pv = plan_view(s);
-  // (c) dH = G (residual) + dZ W_self^T per type; the A-operand load forms
-  // dZ = G * mask and also writes it out for the SpMM and dW_self
+  float* dacc = (sizeof(T) == 4) ? reinterpret_cast<float*>(dHin) : w.dhacc;
+  // (c) dH = G (residual) + dZ W_self^T per type, float32 MFMA; the A-operand
+  // load forms dZ = G * mask and also writes it out for the SpMM and dW_self
   for (int t = 0; t < s->n_ntype; ++t) {
     const int64_t lo = s->type_off_host[t], hi = s->type_off_host[t + 1];
     LoadMasked<D, T> la{G, mask, rows_contig(lo), w.dZ};
-    StoreRows<D, T> ep{dHin, rows_contig(lo), nullptr, L->residual ? G : nullptr};
-    HG_TRY((transform<D, T, true>("gemm_bwd_dx_self", hi - lo, W_self + (int64_t)t * D * D, la, ep, st)));
+    StoreRows<D, float, T> ep{dacc, rows_contig(lo), nullptr, L->residual ? G : nullptr};
+    HG_TRY((launch_gemm_rows<D, true>("gemm_bwd_dx_self", hi - lo, W_self + (int64_t)t * D * D, la, ep, st)));
   }
-  // (b) transposed SpMM
+  // (b) transposed SpMM into float32 dY
   if (s->plan_items > 0)
-    HG_LAUNCH("spmm_bwd", (k_spmm_bwd<D, T>), dim3(wave_grid(s->plan_items)), dim3(256), 0, st,
+    HG_LAUNCH("spmm_bwd", (k_spmm_bwd<D, T, float>), dim3(wave_grid(s->plan_items)), dim3(256), 0, st,
               (int64_t)s->plan_items, pv.items, (const int32_t*)s->csc_row, (const float*)s->csc_scale,
               (const T*)w.dZ, w.dY, w.part);
   if (s->plan_heavy > 0)
-    HG_LAUNCH("spmm_bwd_reduce", (k_heavy_reduce<D, T>), dim3(wave_grid(s->plan_heavy)), dim3(256), 0, st,
+    HG_LAUNCH("spmm_bwd_reduce", (k_heavy_reduce<D, float>), dim3(wave_grid(s->plan_heavy)), dim3(256), 0, st,
               (int64_t)s->plan_heavy, pv.heavy, (const double*)w.part, w.dY);
   // (c) dH += dY_r W_r^T per relation, in relation order
   int64_t off = 0;
   for (int r = 0; r < R; ++r) {
     const int64_t n = s->n_active[r];
-    LoadRows<D, T> la{w.dY, rows_list(pv.active + off, R, r)};
-    StoreRows<D, T> ep{dHin, rows_list(pv.active + off), nullptr, dHin};
-    HG_TRY((transform<D, T, true>("gemm_bwd_dx_rel", n, W_rel + (int64_t)r * D * D, la, ep, st)));
+    LoadRows<D, float> la{w.dY, rows_list(pv.active + off, R, r)};
+    StoreRows<D, float, float> ep{dacc, rows_list(pv.active + off), nullptr, dacc};
+    HG_TRY((launch_gemm_rows<D, true>("gemm_bwd_dx_rel", n, W_rel + (int64_t)r * D * D, la, ep, st)));
     off += n;
+  }
+  if constexpr (sizeof(T) == 2) {
+    const int64_t n = s->n_sub * (int64_t)D;
+    if (n > 0)
+      HG_LAUNCH("dh_to_bf16", k_to_bf16, dim3((unsigned)(cdiv(n / 4, 256) < 65536 ? cdiv(n / 4, 256) : 65536)),
+                dim3(256), 0, st, (const float*)w.dhacc, reinterpret_cast<bf16_t*>(dHin), n);
   }
   // (c) weight gradients, split-K
   for (int t = 0; t < s->n_ntype; ++t) {
@@ -362,7 +377,7 @@ int layer_bwd_impl(const hg_subgraph* s, const hg_layer_desc* L, const T* Hin, c
   for (int r = 0; r < R; ++r) {
     const int64_t n = s->n_active[r];
     LoadRows<D, T> la{Hin, rows_list(pv.active + off)};
-    LoadRows<D, T> lb{w.dY, rows_list(pv.active + off, R, r)};
+    LoadRows<D, float> lb{w.dY, rows_list(pv.active + off, R, r)};
     HG_TRY((launch_gemm_tn<D>("gemm_bwd_dw_rel", n, la, lb, w.splitk, w.colsum, dW_rel + (int64_t)r * D * D,
                               nullptr, 0, st)));
     off += n;
@@ -377,7 +392,7 @@ size_t ws_size(const hg_subgraph* s, const hg_layer_desc* L) {
   switch (L->d_in) {
     case 64: if (bf) { WS<64, bf16_t> w; w.layout(z, s); } else { WS<64, float> w; w.layout(z, s); } break;
     case 128: if (bf) { WS<128, bf16_t> w; w.layout(z, s); } else { WS<128, float> w; w.layout(z, s); } break;
-    default: { WS<256, bf16_t> w; w.layout(z, s); } break;
+    default: if (bf) { WS<256, bf16_t> w; w.layout(z, s); } else { WS<256, float> w; w.layout(z, s); } break;
   }
   return z.used + 256;
 }
@@ -422,7 +437,8 @@ extern "C" int hg_layer_fwd(const hg_subgraph* s, const hg_layer_desc* L, const 
   const float* hi = (const float*)H_in;
   float* ho = (float*)H_out;
   if (L->d_in == 64) return layer_fwd_impl<64, float>(s, L, hi, W_rel, W_self, bias, ho, m, ws, ws_bytes, st);
-  return layer_fwd_impl<128, float>(s, L, hi, W_rel, W_self, bias, ho, m, ws, ws_bytes, st);
+  if (L->d_in == 128) return layer_fwd_impl<128, float>(s, L, hi, W_rel, W_self, bias, ho, m, ws, ws_bytes, st);
+  return layer_fwd_impl<256, float>(s, L, hi, W_rel, W_self, bias, ho, m, ws, ws_bytes, st);
 }
 
 extern "C" int hg_layer_bwd(const hg_subgraph* s, const hg_layer_desc* L, const void* H_in,
@@ -450,5 +466,7 @@ extern "C" int hg_layer_bwd(const hg_subgraph* s, const hg_layer_desc* L, const 
   float* dh = (float*)dH_in;
   if (L->d_in == 64)
     return layer_bwd_impl<64, float>(s, L, hi, W_rel, W_self, m, g, dh, dW_rel, dW_self, dbias, ws, ws_bytes, st);
-  return layer_bwd_impl<128, float>(s, L, hi, W_rel, W_self, m, g, dh, dW_rel, dW_self, dbias, ws, ws_bytes, st);
+  if (L->d_in == 128)
+    return layer_bwd_impl<128, float>(s, L, hi, W_rel, W_self, m, g, dh, dW_rel, dW_self, dbias, ws, ws_bytes, st);
+  return layer_bwd_impl<256, float>(s, L, hi, W_rel, W_self, m, g, dh, dW_rel, dW_self, dbias, ws, ws_bytes, st);
 }

@@ -176,8 +176,12 @@ struct LoadMasked {
 #pragma unroll
     for (int q = 0; q < 4; ++q)
       if (!((nib >> q) & 1u)) x[q] = 0.f;
-    if constexpr (sizeof(T) == 4) {
-      if (tee) *reinterpret_cast<f32x4*>(tee + (p - G) + c) = x;
+    if (tee) {
+      if constexpr (sizeof(T) == 4) {
+        *reinterpret_cast<f32x4*>(tee + (p - G) + c) = x;
+      } else {
+        *reinterpret_cast<uint2*>(tee + (p - G) + c) = uint2{pack2bf(x[0], x[1]), pack2bf(x[2], x[3])};
+      }
     }
     return x;
   }
@@ -207,16 +211,16 @@ struct LoadMasked {
 // element of the tile (all loads), then store(i, ro, c, acc, pre) (all stores):
 // the two phases keep loads from waiting behind stores when the addend is the
 // output itself (dH += ...).
-template <int D, class T = float>
+template <int D, class T = float, class TA = T>
 struct StoreRows {
   T* out;
   RowMap map;
   const float* bias;  // [D] or null
-  const T* addend;    // rows through the same map, or null (may equal out)
+  const TA* addend;   // rows through the same map, or null (may equal out)
   __device__ __forceinline__ int64_t row(int64_t i) const { return map(i); }
   __device__ __forceinline__ float pre(int64_t, int64_t ro, int c) const {
     float v = bias ? bias[c] : 0.f;
-    if (addend) v += Elt<T>::get(addend + ro * D + c);
+    if (addend) v += Elt<TA>::get(addend + ro * D + c);
     return v;
   }
   __device__ __forceinline__ void store(int64_t, int64_t ro, int c, float acc, float pre) const {
@@ -229,26 +233,34 @@ struct StoreRows {
 };
 
 // ---- gemm_rows --------------------------------------------------------------
-// Block = 8 waves sharing one LDS copy of op(W); a wave owns 16 rows, a block
-// 128 rows; persistent over tiles.  About 100 registers per lane keep four
-// waves per SIMD resident, which hides the A-row loads behind other waves'
-// MFMAs.  LDS holds op(W) in fragment order: f32x4 element (kb*NB + nb)*64 +
-// lane is op(W)[16 kb + 4 (lane/16) + s][16 nb + lane%16], s = 0..3.
+// Block = 8 waves sharing one LDS copy of a column slice of op(W); a wave owns
+// 16 rows, a block 128 rows; persistent over tiles.  About 100-150 registers
+// per lane keep two to four waves per SIMD resident, which hides the A-row
+// loads behind other waves' MFMAs.  W is D x D; blockIdx.y picks the column
+// slice [DN*y, DN*y + DN) (DN = D for D <= 128, 128 for D = 256).  LDS holds
+// the slice in fragment order: f32x4 element (kb*NB + nb)*64 + lane is
+// op(W)[16 kb + 4 (lane/16) + s][col0 + 16 nb + lane%16], s = 0..3.
 constexpr int kGemmThreads = 512;
+template <int D>
+struct F32Slice {
+  static constexpr int DN = D > 128 ? 128 : D;
+};
 
 template <int D, bool kTransW, class ALoad, class Epi>
 __global__ void __launch_bounds__(kGemmThreads) k_gemm_rows(int64_t n_rows, const float* __restrict__ W,
                                                             ALoad aload, Epi epi) {
-  constexpr int NB = D / 16;
+  constexpr int DN = F32Slice<D>::DN;
+  constexpr int KB = D / 16, NB = DN / 16;
   constexpr int kWavesPerBlock = kGemmThreads / 64;
   constexpr int kRowsPerTile = 16 * kWavesPerBlock;
   extern __shared__ f32x4 wl[];
   const int tid = threadIdx.x;
-  for (int e = tid; e < NB * NB * 64; e += kGemmThreads) {
+  const int col0 = DN * blockIdx.y;
+  for (int e = tid; e < KB * NB * 64; e += kGemmThreads) {
     const int l = e & 63;
     const int nb = (e >> 6) % NB;
     const int kb = (e >> 6) / NB;
-    const int j = 16 * nb + (l & 15);
+    const int j = col0 + 16 * nb + (l & 15);
     const int k0 = 16 * kb + 4 * (l >> 4);
     f32x4 v;
     if (kTransW) {
@@ -268,23 +280,23 @@ __global__ void __launch_bounds__(kGemmThreads) k_gemm_rows(int64_t n_rows, cons
   const int64_t ntiles = (n_rows + kRowsPerTile - 1) / kRowsPerTile;
   for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
     const int64_t r0 = t * kRowsPerTile + 16 * w;
-    f32x4 a[NB];
+    f32x4 a[KB];
     {
       const int64_t ia = r0 + c;
       if (ia < n_rows) {
         const auto p = aload.rowp(ia);
 #pragma unroll
-        for (int kb = 0; kb < NB; ++kb) a[kb] = aload.load4(p, 16 * kb + 4 * g);
+        for (int kb = 0; kb < KB; ++kb) a[kb] = aload.load4(p, 16 * kb + 4 * g);
       } else {
 #pragma unroll
-        for (int kb = 0; kb < NB; ++kb) a[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int kb = 0; kb < KB; ++kb) a[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
       }
     }
     f32x4 acc[NB];
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int kb = 0; kb < NB; ++kb) {
+    for (int kb = 0; kb < KB; ++kb) {
       // keep each K block's B fragments local (no hoisting of all LDS reads)
       __builtin_amdgcn_sched_barrier(0);
       f32x4 b[NB];
@@ -296,7 +308,7 @@ __global__ void __launch_bounds__(kGemmThreads) k_gemm_rows(int64_t n_rows, cons
         for (int nb = 0; nb < NB; ++nb) acc[nb] = mfma4(a[kb][s], b[nb][s], acc[nb]);
     }
     __builtin_amdgcn_sched_barrier(0);
-    // epilogue: lane holds rows r0 + 4 g + v, columns 16 nb + c
+    // epilogue: lane holds rows r0 + 4 g + v, columns col0 + 16 nb + c
     int64_t ro[4];
     float pre[4][NB];
 #pragma unroll
@@ -304,14 +316,15 @@ __global__ void __launch_bounds__(kGemmThreads) k_gemm_rows(int64_t n_rows, cons
       const int64_t i = r0 + 4 * g + v;
       ro[v] = (i < n_rows) ? epi.row(i) : 0;
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) pre[v][nb] = (i < n_rows) ? epi.pre(i, ro[v], 16 * nb + c) : 0.f;
+      for (int nb = 0; nb < NB; ++nb)
+        pre[v][nb] = (i < n_rows) ? epi.pre(i, ro[v], col0 + 16 * nb + c) : 0.f;
     }
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
       const int64_t i = r0 + 4 * g + v;
       if (i < n_rows) {
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) epi.store(i, ro[v], 16 * nb + c, acc[nb][v], pre[v][nb]);
+        for (int nb = 0; nb < NB; ++nb) epi.store(i, ro[v], col0 + 16 * nb + c, acc[nb][v], pre[v][nb]);
       }
     }
   }
@@ -321,12 +334,21 @@ template <int D, bool kTransW, class ALoad, class Epi>
 int launch_gemm_rows(const char* name, int64_t n_rows, const float* W, ALoad aload, Epi epi,
                      hipStream_t s) {
   if (n_rows <= 0) return HG_OK;
+  constexpr int DN = F32Slice<D>::DN;
   const int64_t tiles = cdiv(n_rows, 16 * (kGemmThreads / 64));
-  const int64_t cap = (int64_t)num_cus() * 2;
+  const int64_t cap = (int64_t)num_cus() * (D > 128 ? 1 : 2);
   const int64_t grid = tiles < cap ? tiles : cap;
-  const size_t lds = sizeof(float) * D * D;
-  HG_LAUNCH(name, (k_gemm_rows<D, kTransW, ALoad, Epi>), dim3((unsigned)grid), dim3(kGemmThreads), lds, s,
-            n_rows, W, aload, epi);
+  const size_t lds = sizeof(float) * D * DN;
+  auto kern = k_gemm_rows<D, kTransW, ALoad, Epi>;
+  if (lds > 65536) {
+    static bool attr_set = false;
+    if (!attr_set) {
+      HG_HIP_TRY(hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
+      attr_set = true;
+    }
+  }
+  HG_LAUNCH(name, kern, dim3((unsigned)grid, D / DN), dim3(kGemmThreads), lds, s, n_rows, W, aload, epi);
   return HG_OK;
 }
 

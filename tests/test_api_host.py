@@ -112,7 +112,6 @@ def _sub(n_sub=10, R=2, T=2):
 @pytest.mark.parametrize("desc,code", [
     (dict(d_in=64, d_out=128), api.HG_ERR_UNSUPPORTED),
     (dict(d_in=96, d_out=96), api.HG_ERR_UNSUPPORTED),
-    (dict(d_in=256, d_out=256), api.HG_ERR_UNSUPPORTED),            # float32 stops at d = 128
     (dict(d_in=96, d_out=96, dtype=1), api.HG_ERR_UNSUPPORTED),
     (dict(d_in=64, d_out=64, dtype=9), api.HG_ERR_ARG),
     (dict(d_in=64, d_out=64, relu=2), api.HG_ERR_ARG),
@@ -154,7 +153,7 @@ def test_layer_workspace_sizes_scale_with_graph(L):
     (dict(M=-1), api.HG_ERR_ARG),
     (dict(d=96), api.HG_ERR_UNSUPPORTED),
     (dict(dtype=1, d=96), api.HG_ERR_UNSUPPORTED),
-    (dict(d=256), api.HG_ERR_UNSUPPORTED),          # float32 alignment stops at d = 128
+    (dict(d=512), api.HG_ERR_UNSUPPORTED),
     (dict(dtype=7), api.HG_ERR_ARG),
     (dict(dtype=1, d=256, ws_bytes=1), api.HG_ERR_CAPACITY),
     (dict(M=20, n_rows=10), api.HG_ERR_ARG),

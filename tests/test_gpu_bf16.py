@@ -69,9 +69,6 @@ def test_bf16_alignment(d):
     exp = G0.astype(np.float64)
     exp[ov] += dX
     assert parity_err(dH.float().cpu().numpy()[ov], exp[ov]) <= TOL
-    # the increment itself, against the oracle's gradient scale
-    inc = dH.float().cpu().numpy()[ov] - G0[ov]
-    assert np.max(np.abs(inc - dX)) <= TOL * np.max(np.abs(dX)) + 1e-2 * np.max(np.abs(G0[ov])) * 2**-8
     assert parity_err(dHref.float().cpu().numpy(), dY) <= TOL
 
 

@@ -28,6 +28,7 @@ CFGS = {
     "tiny_d64": (synth.WORKLOADS["tiny"].graph, 64),
     "tiny_d128": (synth.WORKLOADS["tiny"].graph, 128),
     "skew_small_d64": (synth.scaled(synth.WORKLOADS["skew"].graph, 0.002), 64),
+    "tiny_d256": (synth.scaled(synth.WORKLOADS["tiny"].graph, 0.3), 256),
 }
 
 
