@@ -340,19 +340,26 @@ __global__ void k_member_bits(const int32_t* __restrict__ g2l, int64_t n, uint32
   }
 }
 
+// Local ids of both endpoints (one random gather each) and the keep flag.
 __global__ void k_edge_keep(const int32_t* __restrict__ src, const int32_t* __restrict__ dst,
-                            const uint32_t* __restrict__ mbits, int64_t n_edges, int32_t* __restrict__ keep) {
-  GRID_STRIDE(e, n_edges) { keep[e] = (bit_of(mbits, src[e]) && bit_of(mbits, dst[e])) ? 1 : 0; }
-}
-
-__global__ void k_edge_compact(const int32_t* __restrict__ src, const int32_t* __restrict__ dst,
-                               const uint8_t* __restrict__ rel, const int32_t* __restrict__ g2l,
-                               const int32_t* __restrict__ pos, int64_t n_edges, int32_t n_rel,
-                               uint32_t* __restrict__ kcsr, uint32_t* __restrict__ kcsc,
-                               int32_t* __restrict__ vsrc, int32_t* __restrict__ vdst,
-                               int32_t* __restrict__ veid) {
+                            const int32_t* __restrict__ g2l, int64_t n_edges, int32_t* __restrict__ keep,
+                            int32_t* __restrict__ sl, int32_t* __restrict__ dl) {
   GRID_STRIDE(e, n_edges) {
     const int32_t s = g2l[src[e]], d = g2l[dst[e]];
+    sl[e] = s;
+    dl[e] = d;
+    keep[e] = (s >= 0 && d >= 0) ? 1 : 0;
+  }
+}
+
+// Stable compaction of the kept edges (pos = exclusive scan of keep).
+__global__ void k_edge_compact(const int32_t* __restrict__ sl, const int32_t* __restrict__ dl,
+                               const uint8_t* __restrict__ rel, const int32_t* __restrict__ pos,
+                               int64_t n_edges, int32_t n_rel, uint32_t* __restrict__ kcsr,
+                               uint32_t* __restrict__ kcsc, int32_t* __restrict__ vsrc,
+                               int32_t* __restrict__ vdst, int32_t* __restrict__ veid) {
+  GRID_STRIDE(e, n_edges) {
+    const int32_t s = sl[e], d = dl[e];
     if (s >= 0 && d >= 0) {
       const int32_t p = pos[e];
       const uint32_t r = rel[e];
@@ -657,14 +664,13 @@ extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg
               out->overlap_home, out->overlap_rel);
   // 6. induced-subgraph edges in original order
   if (E > 0) {
-    HG_LAUNCH("build_member_bits", k_member_bits, dim3(gB), dim3(kBT), 0, s, (const int32_t*)out->global2local,
-              N, w.mbits);
+    // local ids land in the sort's ping-pong buffers (free until the sorts)
     HG_LAUNCH("build_edge_keep", k_edge_keep, dim3(gE), dim3(kBT), 0, s, g->src, g->dst,
-              (const uint32_t*)w.mbits, E, w.keep);
+              (const int32_t*)out->global2local, E, w.keep, w.alt1, w.alt2);
     HG_TRY(scan_exclusive_i32(w.keep, w.keep, E, w.cnt + C_ESUB, w.scratch, s));
-    HG_LAUNCH("build_edge_compact", k_edge_compact, dim3(gE), dim3(kBT), 0, s, g->src, g->dst, g->rel,
-              (const int32_t*)out->global2local, (const int32_t*)w.keep, E, (int32_t)R, w.kcsr,
-              w.kcsc, w.vsrc, w.vdst, w.veid);
+    HG_LAUNCH("build_edge_compact", k_edge_compact, dim3(gE), dim3(kBT), 0, s, (const int32_t*)w.alt1,
+              (const int32_t*)w.alt2, g->rel, (const int32_t*)w.keep, E, (int32_t)R, w.kcsr, w.kcsc, w.vsrc,
+              w.vdst, w.veid);
   } else {
     HG_TRY(fill_i32(w.cnt + C_ESUB, 0, 1, s));
   }

@@ -26,8 +26,9 @@ namespace {
 // gathers one source row, so one wave step covers EPW edges.  Neighbour ids
 // and weights of up to 64 entries sit one per lane and are broadcast with
 // ds_bpermute.  Accumulation is float32.
+// fp32 rows: 8 waves per SIMD (<= 64 VGPRs) keep the most gathers in flight.
 template <int D, class T>
-__global__ void __launch_bounds__(256) k_spmm_fwd(int64_t n_sub, int32_t R, const int32_t* __restrict__ csr_ptr,
+__global__ void __launch_bounds__(256, (sizeof(T) == 4 && D <= 128) ? 8 : 4) k_spmm_fwd(int64_t n_sub, int32_t R, const int32_t* __restrict__ csr_ptr,
                                                   const int32_t* __restrict__ csr_col,
                                                   const T* __restrict__ Y, const T* __restrict__ Yself,
                                                   const T* __restrict__ Hin, T* __restrict__ Hout,
@@ -125,7 +126,7 @@ __global__ void __launch_bounds__(256) k_spmm_fwd(int64_t n_sub, int32_t R, cons
 // accumulates in float64 (the kernel is bound by the gathers, not the adds);
 // split rows keep float64 partial rows.
 template <int D, class T, class TO>
-__global__ void __launch_bounds__(256) k_spmm_bwd(int64_t n_items, const int4* __restrict__ items,
+__global__ void __launch_bounds__(256, (sizeof(T) == 4 && D <= 128) ? 8 : 4) k_spmm_bwd(int64_t n_items, const int4* __restrict__ items,
                                                   const int32_t* __restrict__ csc_row,
                                                   const float* __restrict__ csc_scale,
                                                   const T* __restrict__ dZ,
@@ -139,56 +140,109 @@ __global__ void __launch_bounds__(256) k_spmm_bwd(int64_t n_items, const int4* _
   const int c0 = (l % LPR) * EL;
   const int64_t wave0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
   const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
-  for (int64_t it = wave0; it < n_items; it += nwaves) {
-    const int4 item = items[it];
-    const int32_t beg = item.y, end = item.z;
-    double acc[EL];
-#pragma unroll
-    for (int k = 0; k < EL; ++k) acc[k] = 0.0;
-    for (int32_t base = beg; base < end; base += 64) {
-      const int32_t pos = base + l;
-      int32_t dst = 0;
-      float sc = 0.f;
-      if (pos < end) {
-        dst = csc_row[pos];
-        sc = csc_scale[pos];
-      }
-      const int cnt = (end - base) < 64 ? (end - base) : 64;
-      for (int e = 0; e < cnt; e += EPW * U) {
-        float v[U][EL];
-        float ww[U];
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-          const int my = e + u * EPW + slot;
-          const int32_t q = __shfl(dst, my & 63, 64);
-          const float wq = __shfl(sc, my & 63, 64);
-          ww[u] = (my < cnt) ? wq : 0.f;
-          if (my < cnt) {
-            Elt<T>::load(dZ + (int64_t)q * D + c0, v[u]);
-          } else {
-#pragma unroll
-            for (int k = 0; k < EL; ++k) v[u][k] = 0.f;
-          }
+  if constexpr (sizeof(T) == 4) {
+    // float32 rows: one float4 per lane, float64 accumulators (54 VGPRs)
+    for (int64_t it = wave0; it < n_items; it += nwaves) {
+      const int4 item = items[it];
+      const int32_t beg = item.y, end = item.z;
+      f64x4 acc = {0.0, 0.0, 0.0, 0.0};
+      for (int32_t base = beg; base < end; base += 64) {
+        const int32_t pos = base + l;
+        int32_t dst = 0;
+        float sc = 0.f;
+        if (pos < end) {
+          dst = csc_row[pos];
+          sc = csc_scale[pos];
         }
+        const int cnt = (end - base) < 64 ? (end - base) : 64;
+        for (int e = 0; e < cnt; e += EPW * U) {
+          f32x4 v[U];
+          float ww[U];
 #pragma unroll
-        for (int u = 0; u < U; ++u)
+          for (int u = 0; u < U; ++u) {
+            const int my = e + u * EPW + slot;
+            const int32_t q = __shfl(dst, my & 63, 64);
+            const float wq = __shfl(sc, my & 63, 64);
+            ww[u] = (my < cnt) ? wq : 0.f;
+            if (my < cnt) {
+              v[u] = *reinterpret_cast<const f32x4*>(reinterpret_cast<const float*>(dZ) + (int64_t)q * D + c0);
+            } else {
+              v[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+            }
+          }
 #pragma unroll
-          for (int k = 0; k < EL; ++k) acc[k] += (double)ww[u] * (double)v[u][k];
+          for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) acc[q] += (double)ww[u] * (double)v[u][q];
+        }
+      }
+#pragma unroll
+      for (int o = LPR; o < 64; o <<= 1) {
+        acc[0] += __shfl_xor(acc[0], o, 64);
+        acc[1] += __shfl_xor(acc[1], o, 64);
+        acc[2] += __shfl_xor(acc[2], o, 64);
+        acc[3] += __shfl_xor(acc[3], o, 64);
+      }
+      if (slot == 0) {
+        if (item.w < 0) {
+          f32x4 o;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) o[q] = (float)acc[q];
+          *reinterpret_cast<f32x4*>(dY + (int64_t)item.x * D + c0) = o;
+        } else {
+          *reinterpret_cast<f64x4*>(partial + (int64_t)item.w * D + c0) = acc;
+        }
       }
     }
-#pragma unroll
-    for (int o = LPR; o < 64; o <<= 1)
-#pragma unroll
-      for (int k = 0; k < EL; ++k) acc[k] += __shfl_xor(acc[k], o, 64);
-    if (slot == 0) {
-      if (item.w < 0) {
-        TO* o = dY + (int64_t)item.x * D + c0;
-#pragma unroll
-        for (int k = 0; k < EL; ++k) o[k] = (TO)acc[k];
-      } else {
-        double* p = partial + (int64_t)item.w * D + c0;
-#pragma unroll
-        for (int k = 0; k < EL; ++k) p[k] = acc[k];
+  } else {
+    typedef typename Elt<T>::vf vf;
+    typedef typename Elt<T>::vd vd;
+    for (int64_t it = wave0; it < n_items; it += nwaves) {
+      const int4 item = items[it];
+      const int32_t beg = item.y, end = item.z;
+      vd acc = (vd)0.0;
+      for (int32_t base = beg; base < end; base += 64) {
+        const int32_t pos = base + l;
+        int32_t dst = 0;
+        float sc = 0.f;
+        if (pos < end) {
+          dst = csc_row[pos];
+          sc = csc_scale[pos];
+        }
+        const int cnt = (end - base) < 64 ? (end - base) : 64;
+        for (int e = 0; e < cnt; e += EPW * U) {
+          vf v[U];
+          float ww[U];
+  #pragma unroll
+          for (int u = 0; u < U; ++u) {
+            const int my = e + u * EPW + slot;
+            const int32_t q = __shfl(dst, my & 63, 64);
+            const float wq = __shfl(sc, my & 63, 64);
+            ww[u] = (my < cnt) ? wq : 0.f;
+            v[u] = (my < cnt) ? Elt<T>::loadv(dZ + (int64_t)q * D + c0) : (vf)0.f;
+          }
+  #pragma unroll
+          for (int u = 0; u < U; ++u) acc += __builtin_convertvector(v[u], vd) * (double)ww[u];
+        }
+      }
+  #pragma unroll
+      for (int o = LPR; o < 64; o <<= 1)
+  #pragma unroll
+        for (int k = 0; k < EL; ++k) acc[k] += __shfl_xor(acc[k], o, 64);
+      if (slot == 0) {
+        if (item.w < 0) {
+          static_assert(sizeof(TO) == 4, "dY is float32");
+          float* o = dY + (int64_t)item.x * D + c0;
+  #pragma unroll
+          for (int k = 0; k < EL; k += 4)
+            *reinterpret_cast<f32x4*>(o + k) =
+                f32x4{(float)acc[k], (float)acc[k + 1], (float)acc[k + 2], (float)acc[k + 3]};
+        } else {
+          double* p = partial + (int64_t)item.w * D + c0;
+  #pragma unroll
+          for (int k = 0; k < EL; k += 4)
+            *reinterpret_cast<f64x4*>(p + k) = f64x4{acc[k], acc[k + 1], acc[k + 2], acc[k + 3]};
+        }
       }
     }
   }
@@ -214,9 +268,8 @@ __global__ void k_heavy_reduce(int64_t n_heavy, const int4* __restrict__ heavy,
 #pragma unroll
         for (int k = 0; k < EL; ++k) s[k] += p[k];
       }
-      T* o = dY + (int64_t)hv.x * D + l * EL;
-#pragma unroll
-      for (int k = 0; k < EL; ++k) o[k] = (T)s[k];
+      *reinterpret_cast<f32x4*>(dY + (int64_t)hv.x * D + l * EL) =
+          f32x4{(float)s[0], (float)s[1], (float)s[2], (float)s[3]};
     }
   }
 }
@@ -340,7 +393,7 @@ int layer_bwd_impl(const hg_subgraph* s, const hg_layer_desc* L, const T* Hin, c
     const int64_t lo = s->type_off_host[t], hi = s->type_off_host[t + 1];
     LoadMasked<D, T> la{G, mask, rows_contig(lo), w.dZ};
     StoreRows<D, float, T> ep{dacc, rows_contig(lo), nullptr, L->residual ? G : nullptr};
-    HG_TRY((launch_gemm_rows<D, true>("gemm_bwd_dx_self", hi - lo, W_self + (int64_t)t * D * D, la, ep, st)));
+    HG_TRY((launch_gemm_rows<D, true, false>("gemm_bwd_dx_self", hi - lo, W_self + (int64_t)t * D * D, la, ep, st)));
   }
   // (b) transposed SpMM into float32 dY
   if (s->plan_items > 0)
@@ -356,7 +409,7 @@ int layer_bwd_impl(const hg_subgraph* s, const hg_layer_desc* L, const T* Hin, c
     const int64_t n = s->n_active[r];
     LoadRows<D, float> la{w.dY, rows_list(pv.active + off, R, r)};
     StoreRows<D, float, float> ep{dacc, rows_list(pv.active + off), nullptr, dacc};
-    HG_TRY((launch_gemm_rows<D, true>("gemm_bwd_dx_rel", n, W_rel + (int64_t)r * D * D, la, ep, st)));
+    HG_TRY((launch_gemm_rows<D, true, false>("gemm_bwd_dx_rel", n, W_rel + (int64_t)r * D * D, la, ep, st)));
     off += n;
   }
   if constexpr (sizeof(T) == 2) {

@@ -43,6 +43,9 @@ struct Elt;
 template <>
 struct Elt<float> {
   static constexpr int EL = 4;
+  typedef float vf __attribute__((ext_vector_type(4)));
+  typedef double vd __attribute__((ext_vector_type(4)));
+  __device__ static __forceinline__ vf loadv(const float* p) { return *reinterpret_cast<const vf*>(p); }
   __device__ static __forceinline__ void load(const float* p, float (&v)[4]) {
     const f32x4 x = *reinterpret_cast<const f32x4*>(p);
     v[0] = x[0]; v[1] = x[1]; v[2] = x[2]; v[3] = x[3];
@@ -56,6 +59,17 @@ struct Elt<float> {
 template <>
 struct Elt<bf16_t> {
   static constexpr int EL = 8;
+  typedef float vf __attribute__((ext_vector_type(8)));
+  typedef double vd __attribute__((ext_vector_type(8)));
+  __device__ static __forceinline__ vf loadv(const bf16_t* p) {
+    const uint4 x = *reinterpret_cast<const uint4*>(p);
+    vf v;
+    v[0] = __uint_as_float(x.x << 16); v[1] = __uint_as_float(x.x & 0xFFFF0000u);
+    v[2] = __uint_as_float(x.y << 16); v[3] = __uint_as_float(x.y & 0xFFFF0000u);
+    v[4] = __uint_as_float(x.z << 16); v[5] = __uint_as_float(x.z & 0xFFFF0000u);
+    v[6] = __uint_as_float(x.w << 16); v[7] = __uint_as_float(x.w & 0xFFFF0000u);
+    return v;
+  }
   __device__ static __forceinline__ void load(const bf16_t* p, float (&v)[8]) {
     const uint4 x = *reinterpret_cast<const uint4*>(p);
     const uint32_t w[4] = {x.x, x.y, x.z, x.w};
@@ -246,7 +260,7 @@ struct F32Slice {
   static constexpr int DN = D > 128 ? 128 : D;
 };
 
-template <int D, bool kTransW, class ALoad, class Epi>
+template <int D, bool kTransW, class ALoad, class Epi, bool kPrefetchArg>
 __global__ void __launch_bounds__(kGemmThreads) k_gemm_rows(int64_t n_rows, const float* __restrict__ W,
                                                             ALoad aload, Epi epi) {
   constexpr int DN = F32Slice<D>::DN;
@@ -278,20 +292,43 @@ __global__ void __launch_bounds__(kGemmThreads) k_gemm_rows(int64_t n_rows, cons
   const int l = lane64();
   const int g = l >> 4, c = l & 15;
   const int64_t ntiles = (n_rows + kRowsPerTile - 1) / kRowsPerTile;
+  // A rows of the next tile are loaded into registers before the current
+  // tile's MFMAs (software pipelining; two waves per SIMD at D = 128).
+  auto load_a = [&](int64_t tt, f32x4 (&dst)[KB]) {
+    const int64_t ia = tt * kRowsPerTile + 16 * w + c;
+    if (tt < ntiles && ia < n_rows) {
+      const auto p = aload.rowp(ia);
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) dst[kb] = aload.load4(p, 16 * kb + 4 * g);
+    } else {
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) dst[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+  };
+  // at D = 256 the next tile's registers do not fit: no prefetch there
+  constexpr bool kPrefetch = kPrefetchArg && D <= 128;
+  f32x4 a[KB];
+  if (kPrefetch) load_a(blockIdx.x, a);
   for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
     const int64_t r0 = t * kRowsPerTile + 16 * w;
-    f32x4 a[KB];
-    {
-      const int64_t ia = r0 + c;
-      if (ia < n_rows) {
-        const auto p = aload.rowp(ia);
+    if (!kPrefetch) load_a(t, a);
+    // epilogue operands of this tile (bias, addend): loaded before the MFMAs
+    // when registers allow, after them otherwise
+    int64_t ro[4];
+    float pre[4][NB];
+    auto load_pre = [&]() {
 #pragma unroll
-        for (int kb = 0; kb < KB; ++kb) a[kb] = aload.load4(p, 16 * kb + 4 * g);
-      } else {
+      for (int v = 0; v < 4; ++v) {
+        const int64_t i = r0 + 4 * g + v;
+        ro[v] = (i < n_rows) ? epi.row(i) : 0;
 #pragma unroll
-        for (int kb = 0; kb < KB; ++kb) a[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int nb = 0; nb < NB; ++nb)
+          pre[v][nb] = (i < n_rows) ? epi.pre(i, ro[v], col0 + 16 * nb + c) : 0.f;
       }
-    }
+    };
+    if constexpr (kPrefetch) load_pre();
+    f32x4 an[kPrefetch ? KB : 1];
+    if constexpr (kPrefetch) load_a(t + gridDim.x, an);
     f32x4 acc[NB];
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -308,17 +345,7 @@ __global__ void __launch_bounds__(kGemmThreads) k_gemm_rows(int64_t n_rows, cons
         for (int nb = 0; nb < NB; ++nb) acc[nb] = mfma4(a[kb][s], b[nb][s], acc[nb]);
     }
     __builtin_amdgcn_sched_barrier(0);
-    // epilogue: lane holds rows r0 + 4 g + v, columns col0 + 16 nb + c
-    int64_t ro[4];
-    float pre[4][NB];
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int64_t i = r0 + 4 * g + v;
-      ro[v] = (i < n_rows) ? epi.row(i) : 0;
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb)
-        pre[v][nb] = (i < n_rows) ? epi.pre(i, ro[v], col0 + 16 * nb + c) : 0.f;
-    }
+    if constexpr (!kPrefetch) load_pre();
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
       const int64_t i = r0 + 4 * g + v;
@@ -327,19 +354,26 @@ __global__ void __launch_bounds__(kGemmThreads) k_gemm_rows(int64_t n_rows, cons
         for (int nb = 0; nb < NB; ++nb) epi.store(i, ro[v], col0 + 16 * nb + c, acc[nb][v], pre[v][nb]);
       }
     }
+    if constexpr (kPrefetch) {
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) a[kb] = an[kb];
+    }
   }
 }
 
-template <int D, bool kTransW, class ALoad, class Epi>
+// kPrefetch: pipeline the next tile's A rows and this tile's epilogue operands
+// (two waves per SIMD); without it four waves per SIMD hide the latency, which
+// is the better trade when the epilogue reads an addend.
+template <int D, bool kTransW, bool kPrefetch = true, class ALoad, class Epi>
 int launch_gemm_rows(const char* name, int64_t n_rows, const float* W, ALoad aload, Epi epi,
                      hipStream_t s) {
   if (n_rows <= 0) return HG_OK;
   constexpr int DN = F32Slice<D>::DN;
   const int64_t tiles = cdiv(n_rows, 16 * (kGemmThreads / 64));
-  const int64_t cap = (int64_t)num_cus() * (D > 128 ? 1 : 2);
+  const int64_t cap = (int64_t)num_cus() * ((kPrefetch || D > 128) ? 1 : 2);
   const int64_t grid = tiles < cap ? tiles : cap;
   const size_t lds = sizeof(float) * D * DN;
-  auto kern = k_gemm_rows<D, kTransW, ALoad, Epi>;
+  auto kern = k_gemm_rows<D, kTransW, ALoad, Epi, kPrefetch>;
   if (lds > 65536) {
     static bool attr_set = false;
     if (!attr_set) {

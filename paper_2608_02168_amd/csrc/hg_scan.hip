@@ -71,25 +71,25 @@ __global__ void k_scan_sums(int32_t* __restrict__ sums, int64_t m, int32_t* __re
   if (threadIdx.x == 0 && total) *total = carry;
 }
 
-// Per tile: blocked arrangement (thread t owns items [t*16, t*16+16) of the tile).
+// Per tile: 16 rounds of 256 consecutive items (coalesced loads and stores),
+// each an exclusive block scan carried over from the previous round.
 __global__ void k_scan_tiles(const int32_t* __restrict__ in, int32_t* __restrict__ out, int64_t n,
                              const int32_t* __restrict__ tile_off) {
-  const int64_t base = (int64_t)blockIdx.x * kTile + (int64_t)threadIdx.x * kItems;
+  const int64_t base = (int64_t)blockIdx.x * kTile;
+  int carry = tile_off[blockIdx.x];
   int v[kItems];
-  int s = 0;
 #pragma unroll
   for (int j = 0; j < kItems; ++j) {
-    int64_t i = base + j;
+    const int64_t i = base + (int64_t)j * kThreads + threadIdx.x;
     v[j] = (i < n) ? in[i] : 0;
-    s += v[j];
   }
-  int tot;
-  int ex = block_excl_scan(s, &tot) + tile_off[blockIdx.x];
 #pragma unroll
   for (int j = 0; j < kItems; ++j) {
-    int64_t i = base + j;
-    if (i < n) out[i] = ex;
-    ex += v[j];
+    const int64_t i = base + (int64_t)j * kThreads + threadIdx.x;
+    int tot;
+    const int ex = block_excl_scan(v[j], &tot);
+    if (i < n) out[i] = carry + ex;
+    carry += tot;
   }
 }
 
