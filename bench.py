@@ -42,6 +42,27 @@ def algorithmic_cost(kind: str, info: dict):
     raise KeyError(kind)
 
 
+def counted_traffic(kernel: str):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 counter
+    summary, or None if that summary was taken on different kernel source."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"{kernel}_large_counters.md")
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    for line in open(path):
+        if ":" in line and not line.startswith((" ", "|", "#")):
+            k, v = line.split(":", 1)
+            vals[k.strip()] = v.strip()
+    src = os.path.join(ROOT, vals.get("source", ""))
+    if not os.path.isfile(src) or "traffic_bytes_per_launch" not in vals:
+        return None
+    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    if sha != vals.get("source_sha256_16"):
+        return None
+    return int(vals["traffic_bytes_per_launch"])
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -96,8 +117,10 @@ def main():
     avg_ms = total_ms / launches
     nbytes, _ = algorithmic_cost(dom, info)
     achieved = nbytes / (avg_ms * 1e-3) / 1e9
+    traffic = counted_traffic(dom) if args.config == "large" else None
     roofline = {"kernel": dom, "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
-                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+                "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE x2 + WRITE_SIZE, copy-calibrated)",
                 "avg_launch_ms": round(avg_ms, 4), "algorithmic_bytes_per_launch": int(nbytes)}
     layer_ms = sum(v[1] for k, v in kern.items()
                    if k.startswith(("spmm", "gemm_fwd", "gemm_bwd", "relu_grad", "splitk"))) / args.steps
