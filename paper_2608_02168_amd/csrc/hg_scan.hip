@@ -116,11 +116,14 @@ __global__ void k_radix_upsweep(const uint32_t* __restrict__ keys, const uint8_t
   hist[(int64_t)threadIdx.x * ntiles + blockIdx.x] = cnt[threadIdx.x];
 }
 
-// Stable scatter of one tile, staged through LDS.  Items are visited in 16
-// rounds of 256 consecutive items, inside a round in (wave, lane) order; an
-// item's tile-local rank among equal digits gives its slot in an LDS copy of
-// the tile sorted by digit, which is then written out in slot order, so each
-// digit's run of the tile lands in consecutive global addresses.
+// Stable scatter of one tile, staged through LDS.  Wave w owns the 1024
+// consecutive items [1024 w, 1024 w + 1024) of the tile and visits them in 16
+// rounds of 64 (lane order), so the tile order is (wave, round, lane).  An
+// item's rank among equal digits inside its wave comes from wave-private LDS
+// counters (no block barrier per round); one barrier later the per-digit
+// offsets of the waves are known, each item is written to its slot of an LDS
+// copy of the tile sorted by digit, and that copy is written out in slot
+// order, so every digit's run lands in consecutive global addresses.
 // offs is the digit-major exclusive scan of the per-tile counts with the
 // grand total at offs[256 * ntiles].
 template <bool kDigitArray, bool kHasV2>
@@ -131,9 +134,7 @@ __global__ void __launch_bounds__(256) k_radix_downsweep(
     int32_t* __restrict__ v1_out, int32_t* __restrict__ v2_out) {
   __shared__ int gbase[256];
   __shared__ int loff[256];
-  __shared__ int run[256];
   __shared__ int wcnt[kWaves][256];
-  __shared__ int wpre[kWaves][256];
   __shared__ uint32_t sk[kDigitArray ? 1 : kTile];
   __shared__ int32_t sv1[kTile];
   __shared__ int32_t sv2[kHasV2 ? kTile : 1];
@@ -145,28 +146,36 @@ __global__ void __launch_bounds__(256) k_radix_downsweep(
   const int base = offs[fi];
   const int cnt = offs[fi + 1] - base;
   gbase[t] = base;
-  int kept;
-  const int lo = block_excl_scan(cnt, &kept);
-  loff[t] = lo;
-  run[t] = lo;
 #pragma unroll
   for (int i = 0; i < kWaves; ++i) wcnt[i][t] = 0;
-  __syncthreads();
   const uint64_t lt_mask = (l == 0) ? 0ull : (~0ull >> (kWave - l));
-  const int64_t tile_base = (int64_t)blockIdx.x * kTile;
+  const int64_t wbase = (int64_t)blockIdx.x * kTile + (int64_t)w * (kItems * kWave);
+  // all loads of the wave's slice first
+  uint32_t kd[kItems];  // key, or digit
+  int32_t a1[kItems], a2[kHasV2 ? kItems : 1];
+#pragma unroll
   for (int j = 0; j < kItems; ++j) {
-    const int64_t i = tile_base + (int64_t)j * kThreads + t;
-    const bool valid0 = i < n;
-    uint32_t k = 0, d = 0;
-    if (valid0) {
-      if (kDigitArray) {
-        d = digits[i];
-      } else {
-        k = keys[i];
-        d = (k >> shift) & dmask;
-      }
+    const int64_t i = wbase + (int64_t)j * kWave + l;
+    if (i < n) {
+      kd[j] = kDigitArray ? (uint32_t)digits[i] : keys[i];
+      a1[j] = v1[i];
+      if (kHasV2) a2[j] = v2[i];
+    } else {
+      kd[j] = kDigitArray ? 255u : 0u;
+      a1[j] = 0;
+      if (kHasV2) a2[j] = 0;
     }
-    const bool valid = valid0 && (!kDigitArray || d != 255u);
+  }
+  int lo = 0, kept = 0;
+  lo = block_excl_scan(cnt, &kept);  // includes a barrier: wcnt zeroing is visible after it
+  loff[t] = lo;
+  // ranks inside the wave
+  uint16_t rk[kItems];
+#pragma unroll
+  for (int j = 0; j < kItems; ++j) {
+    const int64_t i = wbase + (int64_t)j * kWave + l;
+    const uint32_t d = kDigitArray ? kd[j] : ((kd[j] >> shift) & dmask);
+    const bool valid = i < n && (!kDigitArray || d != 255u);
     uint64_t m = __ballot(valid);
 #pragma unroll
     for (int b = 0; b < 8; ++b) {
@@ -174,28 +183,34 @@ __global__ void __launch_bounds__(256) k_radix_downsweep(
       const uint64_t bal = __ballot(bit);
       m &= bit ? bal : ~bal;
     }
-    int rank = 0;
-    if (valid) {
-      rank = __popcll(m & lt_mask);
-      if ((m & lt_mask) == 0) wcnt[w][d] = __popcll(m);
-    }
-    __syncthreads();
-    {
-      int r = run[t];
+    int r = 0;
+    if (valid) r = wcnt[w][d] + __popcll(m & lt_mask);
+    // every lane has read the counter before the group's leader advances it
+    __builtin_amdgcn_wave_barrier();
+    if (valid && (m & lt_mask) == 0) wcnt[w][d] += __popcll(m);
+    __builtin_amdgcn_wave_barrier();
+    rk[j] = valid ? (uint16_t)r : (uint16_t)0xFFFFu;
+  }
+  __syncthreads();
+  // per digit: exclusive prefix over the waves, added to the tile-local offset
+  {
+    int run = loff[t];
 #pragma unroll
-      for (int q = 0; q < kWaves; ++q) {
-        wpre[q][t] = r;
-        r += wcnt[q][t];
-        wcnt[q][t] = 0;
-      }
-      run[t] = r;
+    for (int q = 0; q < kWaves; ++q) {
+      const int c = wcnt[q][t];
+      wcnt[q][t] = run;
+      run += c;
     }
-    __syncthreads();
-    if (valid) {
-      const int lpos = wpre[w][d] + rank;
-      if (!kDigitArray) sk[lpos] = k;
-      sv1[lpos] = v1[i];
-      if (kHasV2) sv2[lpos] = v2[i];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < kItems; ++j) {
+    if (rk[j] != 0xFFFFu) {
+      const uint32_t d = kDigitArray ? kd[j] : ((kd[j] >> shift) & dmask);
+      const int lpos = wcnt[w][d] + rk[j];
+      if (!kDigitArray) sk[lpos] = kd[j];
+      sv1[lpos] = a1[j];
+      if (kHasV2) sv2[lpos] = a2[j];
       sd[lpos] = (uint8_t)d;
     }
   }
