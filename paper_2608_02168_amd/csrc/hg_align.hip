@@ -156,6 +156,15 @@ struct GradEpi {
   __device__ __forceinline__ void store(int64_t b, int64_t, int c, float acc, float pre) const {
     G[b * D + c] = four_lambda * acc + pre;
   }
+  __device__ __forceinline__ f32x4 pre4(int64_t b, int64_t, int c) const {
+    const auto ps = self.rowp(b);
+    const auto po = other.rowp(b);
+    const f32x4 diff = self.load4(ps, c) - other.load4(po, c);
+    return (two_sign * (w ? w[b] : 1.f)) * diff;
+  }
+  __device__ __forceinline__ void store4(int64_t b, int64_t, int c, f32x4 acc, f32x4 pre) const {
+    *reinterpret_cast<f32x4*>(G + b * D + c) = four_lambda * acc + pre;
+  }
 };
 
 // dX = (1/sigma)(g' - S1/M - xt * S2/(M - ddof)); dst[row] (+)= scale * dX.
@@ -222,7 +231,7 @@ int colsum(const char* name, int64_t m, F f, float* part, float* out, hipStream_
 
 template <int D, class T, class ALoad, class Epi>
 int grad_gemm(int64_t m, const float* W, ALoad la, Epi ep, hipStream_t s) {
-  return launch_gemm_rows<D, false>("align_grad_gemm", m, W, la, ep, s);
+  return launch_gemm_rows<D, false, false>("align_grad_gemm", m, W, la, ep, s);
 }
 
 template <int D, class T>

@@ -244,6 +244,20 @@ struct StoreRows {
       out[ro * D + c] = f2bf(acc + pre);
     }
   }
+  // four consecutive columns [c, c + 4) of one row
+  __device__ __forceinline__ f32x4 pre4(int64_t, int64_t ro, int c) const {
+    f32x4 v = bias ? *reinterpret_cast<const f32x4*>(bias + c) : f32x4{0.f, 0.f, 0.f, 0.f};
+    if (addend) v += Elt<TA>::load4(addend + ro * D + c);
+    return v;
+  }
+  __device__ __forceinline__ void store4(int64_t, int64_t ro, int c, f32x4 acc, f32x4 pre) const {
+    const f32x4 r = acc + pre;
+    if constexpr (sizeof(T) == 4) {
+      *reinterpret_cast<f32x4*>(out + ro * D + c) = r;
+    } else {
+      *reinterpret_cast<uint2*>(out + ro * D + c) = uint2{pack2bf(r[0], r[1]), pack2bf(r[2], r[3])};
+    }
+  }
 };
 
 // ---- gemm_rows --------------------------------------------------------------
@@ -312,19 +326,19 @@ __global__ void __launch_bounds__(kGemmThreads) k_gemm_rows(int64_t n_rows, cons
   for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
     const int64_t r0 = t * kRowsPerTile + 16 * w;
     if (!kPrefetch) load_a(t, a);
-    // epilogue operands of this tile (bias, addend): loaded before the MFMAs
-    // when registers allow, after them otherwise
-    int64_t ro[4];
-    float pre[4][NB];
+    // The MFMA computes the transpose, out^T = op(W)^T A^T (W fragments as the
+    // A operand, A rows as the B operand), so lane (c, g) ends up holding
+    // row r0 + c, columns col0 + 16 nb + 4 g .. + 3 of the output: the
+    // epilogue reads and writes 16 bytes per lane per column block.
+    const int64_t i = r0 + c;
+    const bool live = i < n_rows;
+    int64_t ro = 0;
+    f32x4 pre[NB];
     auto load_pre = [&]() {
+      ro = live ? epi.row(i) : 0;
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int64_t i = r0 + 4 * g + v;
-        ro[v] = (i < n_rows) ? epi.row(i) : 0;
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb)
-          pre[v][nb] = (i < n_rows) ? epi.pre(i, ro[v], col0 + 16 * nb + c) : 0.f;
-      }
+      for (int nb = 0; nb < NB; ++nb)
+        pre[nb] = live ? epi.pre4(i, ro, col0 + 16 * nb + 4 * g) : f32x4{0.f, 0.f, 0.f, 0.f};
     };
     if constexpr (kPrefetch) load_pre();
     f32x4 an[kPrefetch ? KB : 1];
@@ -334,7 +348,7 @@ __global__ void __launch_bounds__(kGemmThreads) k_gemm_rows(int64_t n_rows, cons
     for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb) {
-      // keep each K block's B fragments local (no hoisting of all LDS reads)
+      // keep each K block's W fragments local (no hoisting of all LDS reads)
       __builtin_amdgcn_sched_barrier(0);
       f32x4 b[NB];
 #pragma unroll
@@ -342,17 +356,13 @@ __global__ void __launch_bounds__(kGemmThreads) k_gemm_rows(int64_t n_rows, cons
 #pragma unroll
       for (int s = 0; s < 4; ++s)
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) acc[nb] = mfma4(a[kb][s], b[nb][s], acc[nb]);
+        for (int nb = 0; nb < NB; ++nb) acc[nb] = mfma4(b[nb][s], a[kb][s], acc[nb]);
     }
     __builtin_amdgcn_sched_barrier(0);
     if constexpr (!kPrefetch) load_pre();
+    if (live) {
 #pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int64_t i = r0 + 4 * g + v;
-      if (i < n_rows) {
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb) epi.store(i, ro[v], col0 + 16 * nb + c, acc[nb][v], pre[v][nb]);
-      }
+      for (int nb = 0; nb < NB; ++nb) epi.store4(i, ro, col0 + 16 * nb + 4 * g, acc[nb], pre[nb]);
     }
     if constexpr (kPrefetch) {
 #pragma unroll
@@ -361,9 +371,6 @@ __global__ void __launch_bounds__(kGemmThreads) k_gemm_rows(int64_t n_rows, cons
   }
 }
 
-// kPrefetch: pipeline the next tile's A rows and this tile's epilogue operands
-// (two waves per SIMD); without it four waves per SIMD hide the latency, which
-// is the better trade when the epilogue reads an addend.
 template <int D, bool kTransW, bool kPrefetch = true, class ALoad, class Epi>
 int launch_gemm_rows(const char* name, int64_t n_rows, const float* W, ALoad aload, Epi epi,
                      hipStream_t s) {
@@ -449,28 +456,20 @@ __global__ void __launch_bounds__(BfShape<D>::kThreads) k_gemm_rows_bf16(int64_t
       uint4 b[NBW];
 #pragma unroll
       for (int nb = 0; nb < NBW; ++nb) b[nb] = wlb[(kb * NB + cg * NBW + nb) * 64 + l];
+      // transposed product: W fragments as the A operand, A rows as the B operand
 #pragma unroll
-      for (int nb = 0; nb < NBW; ++nb) acc[nb] = mfma_bf16(a[kb], b[nb], acc[nb]);
+      for (int nb = 0; nb < NBW; ++nb) acc[nb] = mfma_bf16(b[nb], a[kb], acc[nb]);
     }
     __builtin_amdgcn_sched_barrier(0);
-    int64_t ro[4];
-    float pre[4][NBW];
+    // lane (c, g) holds row r0 + c, columns 16 (cg*NBW + nb) + 4 g .. + 3
+    const int64_t i = r0 + c;
+    if (i < n_rows) {
+      const int64_t ro = epi.row(i);
+      f32x4 pre[NBW];
 #pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int64_t i = r0 + 4 * g + v;
-      ro[v] = (i < n_rows) ? epi.row(i) : 0;
+      for (int nb = 0; nb < NBW; ++nb) pre[nb] = epi.pre4(i, ro, 16 * (cg * NBW + nb) + 4 * g);
 #pragma unroll
-      for (int nb = 0; nb < NBW; ++nb)
-        pre[v][nb] = (i < n_rows) ? epi.pre(i, ro[v], 16 * (cg * NBW + nb) + c) : 0.f;
-    }
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int64_t i = r0 + 4 * g + v;
-      if (i < n_rows) {
-#pragma unroll
-        for (int nb = 0; nb < NBW; ++nb)
-          epi.store(i, ro[v], 16 * (cg * NBW + nb) + c, acc[nb][v], pre[v][nb]);
-      }
+      for (int nb = 0; nb < NBW; ++nb) epi.store4(i, ro, 16 * (cg * NBW + nb) + 4 * g, acc[nb], pre[nb]);
     }
   }
 }
