@@ -72,6 +72,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=float, default=0.01,
                     help="fraction of the workload's node/edge counts the oracle runs on")
+    ap.add_argument("--no-ceiling", action="store_true",
+                    help="skip the random-row gather ceiling measurement")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus})",
@@ -122,6 +124,9 @@ def main():
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
                 "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE x2 + WRITE_SIZE, copy-calibrated)",
                 "avg_launch_ms": round(avg_ms, 4), "algorithmic_bytes_per_launch": int(nbytes)}
+    if not args.no_ceiling:
+        groups = info["E"] / max(info["A"] if dom == "spmm_bwd" else info["N"], 1)
+        roofline["ceiling"] = gather_ceiling(info["N"], info["E"], info["d"] * info["s"], groups, achieved)
     layer_ms = sum(v[1] for k, v in kern.items()
                    if k.startswith(("spmm", "gemm_fwd", "gemm_bwd", "relu_grad", "splitk"))) / args.steps
     breakdown = {k: round(v[1] / args.steps, 3) for k, v in sorted(kern.items(), key=lambda kv: -kv[1][1])}
@@ -145,6 +150,43 @@ def main():
         "kernel_ms_per_step": breakdown,
     }
     print(json.dumps(out), flush=True)
+
+
+def gather_ceiling(n_rows, n_idx, row_bytes, group, achieved):
+    """What the memory system delivers for the SpMM access pattern at this
+    shape: rows of row_bytes fetched through uniform random ids (n_idx of them
+    over n_rows rows), summed in groups of `group`, without and with one row
+    written per group (csrc/hg_ceiling.hip).  Bytes are counted like the
+    kernels' algorithmic bytes: rows + 4-byte ids + written rows."""
+    import torch
+
+    from paper_2608_02168_amd import ceiling
+
+    g = int(min(max(round(group), 1), 64))
+    dc = row_bytes // 4
+    table = torch.randn((n_rows, dc), device="cuda")
+    idx = torch.empty(n_idx, dtype=torch.int32, device="cuda")
+    ceiling.random_rows(idx, n_rows, 12345)
+    out = torch.empty((n_idx // g, dc), device="cuda")
+    res = {}
+    for write in (False, True):
+        ceiling.gather(table, idx, g, out, write)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(3):
+            ceiling.gather(table, idx, g, out, write)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / 3
+        ng = n_idx // g
+        nbytes = ng * g * (row_bytes + 4) + (ng * row_bytes if write else 0)
+        res["with_writes" if write else "gather_only"] = round(nbytes / (ms * 1e-3) / 1e9, 1)
+    del table, idx, out
+    torch.cuda.empty_cache()
+    return {"pattern": f"uniform random {row_bytes}-byte rows, {n_idx} ids over {n_rows} rows, "
+                       f"groups of {g}, one row written per group",
+            "gather_only": res["gather_only"], "with_writes": res["with_writes"], "unit": "GB/s",
+            "frac": round(achieved / res["with_writes"], 4)}
 
 
 def cpu_baseline(wl, frac):
