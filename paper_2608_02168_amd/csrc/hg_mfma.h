@@ -14,6 +14,8 @@
 //               a deterministic split-K for weight gradients and Gram matrices.
 #pragma once
 
+#include <type_traits>
+
 #include "hg_internal.h"
 
 namespace hg {
@@ -55,6 +57,10 @@ struct Elt<float> {
   }
   __device__ static __forceinline__ float get(const float* p) { return *p; }
   __device__ static __forceinline__ f32x4 load4(const float* p) { return *reinterpret_cast<const f32x4*>(p); }
+  // four elements as loaded (issue) and as used (after the data arrived)
+  typedef f32x4 raw4_t;
+  __device__ static __forceinline__ raw4_t raw4(const float* p) { return *reinterpret_cast<const f32x4*>(p); }
+  __device__ static __forceinline__ f32x4 cook4(raw4_t r) { return r; }
 };
 template <>
 struct Elt<bf16_t> {
@@ -93,6 +99,12 @@ struct Elt<bf16_t> {
     return f32x4{__uint_as_float(x.x << 16), __uint_as_float(x.x & 0xFFFF0000u),
                  __uint_as_float(x.y << 16), __uint_as_float(x.y & 0xFFFF0000u)};
   }
+  typedef uint2 raw4_t;
+  __device__ static __forceinline__ raw4_t raw4(const bf16_t* p) { return *reinterpret_cast<const uint2*>(p); }
+  __device__ static __forceinline__ f32x4 cook4(raw4_t x) {
+    return f32x4{__uint_as_float(x.x << 16), __uint_as_float(x.x & 0xFFFF0000u),
+                 __uint_as_float(x.y << 16), __uint_as_float(x.y & 0xFFFF0000u)};
+  }
 };
 
 __device__ __forceinline__ f32x4 mfma_bf16(uint4 a, uint4 b, f32x4 c) {
@@ -115,6 +127,27 @@ struct RowMap {
   __device__ __forceinline__ int64_t operator()(int64_t i) const {
     const int64_t b = list ? (int64_t)list[i] : first + i;
     return b * mul + add;
+  }
+  // The same split in two with the list/contiguous choice fixed at compile
+  // time: key(i) is the raw list entry (a load whose value is not touched) or
+  // i itself; row_of(key) does the arithmetic once the entry has arrived.
+  template <bool kList>
+  using Key = typename std::conditional<kList, int32_t, int64_t>::type;
+  template <bool kList>
+  __device__ __forceinline__ Key<kList> key(int64_t i) const {
+    if constexpr (kList) {
+      return list[i];
+    } else {
+      return i;
+    }
+  }
+  template <bool kList>
+  __device__ __forceinline__ int64_t row_of(Key<kList> k) const {
+    if constexpr (kList) {
+      return (int64_t)k * mul + add;
+    } else {
+      return (first + k) * mul + add;
+    }
   }
 };
 
@@ -142,6 +175,12 @@ struct LoadRows {
   }
   __device__ __forceinline__ float load1(const T* p, int c) const { return Elt<T>::get(p + c); }
   __device__ __forceinline__ float at(int64_t i, int c) const { return load1(rowp(i), c); }
+  // split form for prefetching: base row, raw load, transform at use
+  typedef typename Elt<T>::raw4_t Raw;
+  struct Prep {};
+  __device__ __forceinline__ Raw raw4b(int64_t b, int c) const { return Elt<T>::raw4(base + b * D + c); }
+  __device__ __forceinline__ Prep prep(int) const { return Prep{}; }
+  __device__ __forceinline__ f32x4 cook4(Raw r, const Prep&) const { return Elt<T>::cook4(r); }
 };
 
 // (x - mu[c]) * sc[c]: the per-column standardisation of the alignment loss.
@@ -169,6 +208,23 @@ struct LoadStd {
   }
   __device__ __forceinline__ float load1(const T* p, int c) const { return (Elt<T>::get(p + c) - mu[c]) * sc[c]; }
   __device__ __forceinline__ float at(int64_t i, int c) const { return load1(rowp(i), c); }
+  typedef typename Elt<T>::raw4_t Raw;
+  struct Prep {
+    f32x4 m, s;
+  };
+  __device__ __forceinline__ Raw raw4b(int64_t b, int c) const { return Elt<T>::raw4(base + b * D + c); }
+  __device__ __forceinline__ Prep prep(int c) const {
+    return Prep{*reinterpret_cast<const f32x4*>(mu + c), *reinterpret_cast<const f32x4*>(sc + c)};
+  }
+  __device__ __forceinline__ f32x4 cook4(Raw raw, const Prep& q) const {
+    const f32x4 x = Elt<T>::cook4(raw);
+    f32x4 r;
+    r[0] = (x[0] - q.m[0]) * q.s[0];
+    r[1] = (x[1] - q.m[1]) * q.s[1];
+    r[2] = (x[2] - q.m[2]) * q.s[2];
+    r[3] = (x[3] - q.m[3]) * q.s[3];
+    return r;
+  }
 };
 
 // dZ = G * mask read on the fly: the ReLU mask row of G row r holds bit c of
@@ -505,13 +561,12 @@ int launch_gemm_rows_bf16(const char* name, int64_t n_rows, const float* W, ALoa
 // (features q0 + 4c .. 4c+3) and feeds component b of it to MFMA block b, so
 // block b, MFMA index c stands for feature q0 + 4c + b: in the output, the
 // lane's register v of block (bi, bj) is element [4 (4 g + v) + bi][4 c + bj].
-template <int D, class LA, class LB>
+template <int D, class LA, class LB, bool kListA, bool kListB>
 __global__ void __launch_bounds__(256) k_gemm_tn(int64_t n_rows, int64_t kc, LA la, LB lb,
                                                  float* __restrict__ partial,
                                                  float* __restrict__ colsum) {
   static_assert(D == 64 || D == 128 || D == 256, "gemm_tn: d must be 64, 128 or 256");
   constexpr bool kQuad = (D >= 128);
-  constexpr int U = 4;
   const int w = threadIdx.x >> 6;
   const int l = lane64();
   const int g = l >> 4, c = l & 15;
@@ -532,27 +587,74 @@ __global__ void __launch_bounds__(256) k_gemm_tn(int64_t n_rows, int64_t kc, LA 
   for (int bi = 0; bi < 4; ++bi)
 #pragma unroll
     for (int bj = 0; bj < 4; ++bj) acc[bi][bj] = f32x4{0.f, 0.f, 0.f, 0.f};
-  for (int64_t k0 = k_beg + step0; k0 < k_end; k0 += stride * U) {
-    f32x4 a[U], b[U];
+  // Software pipeline over steps of U row groups: the rows of step s + 1 are
+  // loaded and the row-list entries of step s + 2 looked up while step s is
+  // multiplied.  Two register sets alternate (the loop body is unrolled by
+  // two), so no prefetched value is ever copied.  Rows past the chunk end are
+  // read from its last row and zeroed before use.
+  constexpr int U = 4;
+  typedef typename LA::Raw RA;
+  typedef typename LB::Raw RB;
+  const int64_t S = stride * U;
+  const typename LA::Prep pa = la.prep(ca);
+  const typename LB::Prep pb = lb.prep(cb);
+  typedef RowMap::Key<kListA> KA;
+  typedef RowMap::Key<kListB> KB;
+  auto keys = [&](int64_t k0, KA (&ka)[U], KB (&kb)[U]) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int64_t row = k0 + u * stride + g;
-      if (row < k_end) {
-        const auto pa = la.rowp(row);
-        const auto pb = lb.rowp(row);
-        a[u] = la.load4(pa, ca);
-        b[u] = lb.load4(pb, cb);
-      } else {
-        a[u] = b[u] = f32x4{0.f, 0.f, 0.f, 0.f};
-      }
+      int64_t r = k0 + u * stride + g;
+      r = r < k_end ? r : k_end - 1;
+      ka[u] = la.map.template key<kListA>(r);
+      kb[u] = lb.map.template key<kListB>(r);
     }
+  };
+  auto fetch = [&](const KA (&ka)[U], const KB (&kb)[U], RA (&xa)[U], RB (&xb)[U]) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      bs += b[u];
+      xa[u] = la.raw4b(la.map.template row_of<kListA>(ka[u]), ca);
+      xb[u] = lb.raw4b(lb.map.template row_of<kListB>(kb[u]), cb);
+    }
+  };
+  auto compute = [&](int64_t k0, const RA (&xa)[U], const RB (&xb)[U]) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const bool ok = k0 + u * stride + g < k_end;
+      f32x4 a = la.cook4(xa[u], pa), b = lb.cook4(xb[u], pb);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        a[q] = ok ? a[q] : 0.f;
+        b[q] = ok ? b[q] : 0.f;
+      }
+      bs += b;
 #pragma unroll
       for (int bi = 0; bi < 4; ++bi)
 #pragma unroll
-        for (int bj = 0; bj < 4; ++bj) acc[bi][bj] = mfma4(a[u][bi], b[u][bj], acc[bi][bj]);
+        for (int bj = 0; bj < 4; ++bj) acc[bi][bj] = mfma4(a[bi], b[bj], acc[bi][bj]);
+    }
+  };
+  int64_t k0 = k_beg + step0;
+  if (k0 < k_end) {
+    KA k0a[U], k1a[U];
+    KB k0b[U], k1b[U];
+    RA x0a[U], x1a[U];
+    RB x0b[U], x1b[U];
+    keys(k0, k0a, k0b);
+    fetch(k0a, k0b, x0a, x0b);
+    keys(k0 + S, k1a, k1b);
+    // one basic block per pair of steps (a second step past the chunk end
+    // multiplies zeroed rows); the barriers keep each phase where it is
+    for (; k0 < k_end; k0 += 2 * S) {
+      fetch(k1a, k1b, x1a, x1b);
+      keys(k0 + 2 * S, k0a, k0b);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(k0, x0a, x0b);
+      __builtin_amdgcn_sched_barrier(0);
+      fetch(k0a, k0b, x0a, x0b);
+      keys(k0 + 3 * S, k1a, k1b);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(k0 + S, x1a, x1b);
+      __builtin_amdgcn_sched_barrier(0);
     }
   }
   // column sums: reduce the 4 row groups of the wave
@@ -627,17 +729,19 @@ static __global__ void k_sum_partials(const float* __restrict__ partial, int64_t
   out[i] = s;
 }
 
-// Chunking of a K-reduction of n rows (deterministic in n).
+// Chunking of a K-reduction of n rows (deterministic in n): at most
+// kSplitPerCu chunks per compute unit, one resident block each.
+constexpr int kSplitPerCu = 2;
 inline int64_t splitk_chunk(int64_t n) {
   int64_t chunks = cdiv(n, 512);
-  const int64_t cap = (int64_t)num_cus() * 4;
+  const int64_t cap = (int64_t)num_cus() * kSplitPerCu;
   if (chunks > cap) chunks = cap;
   if (chunks < 1) chunks = 1;
   int64_t kc = cdiv(n, chunks);
   kc = cdiv(kc, 64) * 64;
   return kc > 64 ? kc : 64;
 }
-inline int64_t splitk_max_chunks() { return (int64_t)num_cus() * 4 + kSplitGroups + 1; }
+inline int64_t splitk_max_chunks() { return (int64_t)num_cus() * kSplitPerCu + kSplitGroups + 1; }
 
 // partial must hold splitk_max_chunks() * D * D floats: the grouped stage
 // writes its kSplitGroups rows after the chunk rows.
@@ -670,9 +774,19 @@ int launch_gemm_tn(const char* name, int64_t n_rows, LA la, LB lb, float* partia
   const int64_t kc = splitk_chunk(n_rows);
   const int64_t chunks = cdiv(n_rows, kc);
   const unsigned tiles = D == 256 ? 4u : 1u;
-  HG_LAUNCH(name, (k_gemm_tn<D, LA, LB>), dim3((unsigned)chunks, tiles), dim3(256), 0, s, n_rows, kc, la,
-            lb, partial, out_colsum ? colsum : nullptr);
-  const int64_t cap = (int64_t)num_cus() * 4 + 1;
+  const bool list_a = la.map.list != nullptr, list_b = lb.map.list != nullptr;
+  float* cs = out_colsum ? colsum : nullptr;
+  const dim3 grid((unsigned)chunks, tiles);
+  if (list_a && list_b) {
+    HG_LAUNCH(name, (k_gemm_tn<D, LA, LB, true, true>), grid, dim3(256), 0, s, n_rows, kc, la, lb, partial, cs);
+  } else if (!list_a && !list_b) {
+    HG_LAUNCH(name, (k_gemm_tn<D, LA, LB, false, false>), grid, dim3(256), 0, s, n_rows, kc, la, lb, partial, cs);
+  } else if (list_a) {
+    HG_LAUNCH(name, (k_gemm_tn<D, LA, LB, true, false>), grid, dim3(256), 0, s, n_rows, kc, la, lb, partial, cs);
+  } else {
+    HG_LAUNCH(name, (k_gemm_tn<D, LA, LB, false, true>), grid, dim3(256), 0, s, n_rows, kc, la, lb, partial, cs);
+  }
+  const int64_t cap = (int64_t)num_cus() * kSplitPerCu + 1;
   HG_TRY(reduce_partials(partial, chunks, (int64_t)D * D, partial + cap * D * D, out, accumulate, s));
   if (out_colsum)
     HG_TRY(reduce_partials(colsum, chunks, (int64_t)D, colsum + cap * D, out_colsum, accumulate, s));
