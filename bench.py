@@ -42,10 +42,21 @@ def algorithmic_cost(kind: str, info: dict):
     raise KeyError(kind)
 
 
+def kernel_source_sha(path: str, kernel: str) -> str:
+    """SHA-256 (16 hex digits) of a kernel's own source text: from the
+    template line before `kernel(` to the closing brace at column 0."""
+    import hashlib
+    lines = open(path).read().split("\n")
+    start = next(i for i, l in enumerate(lines) if f" {kernel}(" in l and "__global__" in l)
+    while start > 0 and not lines[start].startswith("template"):
+        start -= 1
+    end = next(i for i in range(start, len(lines)) if lines[i] == "}")
+    return hashlib.sha256("\n".join(lines[start:end + 1]).encode()).hexdigest()[:16]
+
+
 def counted_traffic(kernel: str):
     """HBM bytes per launch of `kernel` from the committed rocprofv3 counter
-    summary, or None if that summary was taken on different kernel source."""
-    import hashlib
+    summary, or None if the kernel's source has changed since."""
     path = os.path.join(ROOT, "profiles", f"{kernel}_large_counters.md")
     if not os.path.exists(path):
         return None
@@ -55,10 +66,9 @@ def counted_traffic(kernel: str):
             k, v = line.split(":", 1)
             vals[k.strip()] = v.strip()
     src = os.path.join(ROOT, vals.get("source", ""))
-    if not os.path.isfile(src) or "traffic_bytes_per_launch" not in vals:
+    if not os.path.isfile(src) or "traffic_bytes_per_launch" not in vals or "kernel_function" not in vals:
         return None
-    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
-    if sha != vals.get("source_sha256_16"):
+    if kernel_source_sha(src, vals["kernel_function"]) != vals.get("kernel_source_sha256_16"):
         return None
     return int(vals["traffic_bytes_per_launch"])
 

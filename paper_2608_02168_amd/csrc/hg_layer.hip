@@ -332,11 +332,22 @@ struct BwdWs {
   }
 };
 
+// fp32 MFMA row transform: the software-pipelined kernel up to d = 128,
+// the column-sliced one at d = 256.
+template <int D, bool kTransW, class ALoad, class Epi>
+int rows_f32(const char* name, int64_t n, const float* W, ALoad la, Epi ep, hipStream_t st) {
+  if constexpr (D <= 128) {
+    return launch_gemm_rows_pp<D, kTransW>(name, n, W, la, ep, st);
+  } else {
+    return launch_gemm_rows<D, kTransW, false>(name, n, W, la, ep, st);
+  }
+}
+
 // fp32 features use the fp32 MFMA transform, bf16 features the bf16 one.
 template <int D, class T, bool kTransW, class ALoad, class Epi>
 int transform(const char* name, int64_t n, const float* W, ALoad la, Epi ep, hipStream_t st) {
   if constexpr (sizeof(T) == 4) {
-    return launch_gemm_rows<D, kTransW>(name, n, W, la, ep, st);
+    return rows_f32<D, kTransW>(name, n, W, la, ep, st);
   } else {
     return launch_gemm_rows_bf16<D, kTransW>(name, n, W, la, ep, st);
   }
@@ -392,8 +403,9 @@ int layer_bwd_impl(const hg_subgraph* s, const hg_layer_desc* L, const T* Hin, c
   for (int t = 0; t < s->n_ntype; ++t) {
     const int64_t lo = s->type_off_host[t], hi = s->type_off_host[t + 1];
     LoadMasked<D, T> la{G, mask, rows_contig(lo), w.dZ};
-    StoreRows<D, float, T> ep{dacc, rows_contig(lo), nullptr, L->residual ? G : nullptr};
-    HG_TRY((launch_gemm_rows<D, true, false>("gemm_bwd_dx_self", hi - lo, W_self + (int64_t)t * D * D, la, ep, st)));
+    // the residual addend G is A's own rows before masking
+    StoreRows<D, float, T, true> ep{dacc, rows_contig(lo), nullptr, L->residual ? G : nullptr};
+    HG_TRY((rows_f32<D, true>("gemm_bwd_dx_self", hi - lo, W_self + (int64_t)t * D * D, la, ep, st)));
   }
   // (b) transposed SpMM into float32 dY
   if (s->plan_items > 0)
@@ -409,7 +421,7 @@ int layer_bwd_impl(const hg_subgraph* s, const hg_layer_desc* L, const T* Hin, c
     const int64_t n = s->n_active[r];
     LoadRows<D, float> la{w.dY, rows_list(pv.active + off, R, r)};
     StoreRows<D, float, float> ep{dacc, rows_list(pv.active + off), nullptr, dacc};
-    HG_TRY((launch_gemm_rows<D, true, false>("gemm_bwd_dx_rel", n, W_rel + (int64_t)r * D * D, la, ep, st)));
+    HG_TRY((rows_f32<D, true>("gemm_bwd_dx_rel", n, W_rel + (int64_t)r * D * D, la, ep, st)));
     off += n;
   }
   if constexpr (sizeof(T) == 2) {

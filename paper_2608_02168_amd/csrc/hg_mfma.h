@@ -181,6 +181,23 @@ struct LoadRows {
   __device__ __forceinline__ Raw raw4b(int64_t b, int c) const { return Elt<T>::raw4(base + b * D + c); }
   __device__ __forceinline__ Prep prep(int) const { return Prep{}; }
   __device__ __forceinline__ f32x4 cook4(Raw r, const Prep&) const { return Elt<T>::cook4(r); }
+  // whole-row form of the split (lane group g holds columns 16 kb + 4 g)
+  struct RowRaw {
+    Raw x[D / 16];
+  };
+  __device__ __forceinline__ void fetch_row(int64_t b, int g, RowRaw& r) const {
+#pragma unroll
+    for (int kb = 0; kb < D / 16; ++kb) r.x[kb] = raw4b(b, 16 * kb + 4 * g);
+  }
+  __device__ __forceinline__ void cook_row(const RowRaw& r, int64_t, int, bool, f32x4 (&a)[D / 16]) const {
+#pragma unroll
+    for (int kb = 0; kb < D / 16; ++kb) a[kb] = Elt<T>::cook4(r.x[kb]);
+  }
+  // per-K-block form: the row as stored, and the MFMA operand
+  __device__ __forceinline__ f32x4 stored4(const RowRaw& r, int kb) const { return Elt<T>::cook4(r.x[kb]); }
+  __device__ __forceinline__ f32x4 operand4(const RowRaw& r, int kb, int) const { return Elt<T>::cook4(r.x[kb]); }
+  static constexpr bool kTee = false;
+  __device__ __forceinline__ void tee4(int64_t, int, int, f32x4) const {}
 };
 
 // (x - mu[c]) * sc[c]: the per-column standardisation of the alignment loss.
@@ -274,6 +291,65 @@ struct LoadMasked {
     return ((word(p, c) >> (c & 31)) & 1u) ? Elt<T>::get(p + c) : 0.f;
   }
   __device__ __forceinline__ float at(int64_t i, int c) const { return load1(rowp(i), c); }
+  // Whole-row split: the row's elements and its D/32 mask words are loaded
+  // first; the mask is applied (and the masked values written to tee) when
+  // they are used.  Lane group g holds columns 16 kb + 4 g.
+  typedef typename Elt<T>::raw4_t Raw;
+  struct RowRaw {
+    Raw x[D / 16];
+    uint32_t m[D / 32];
+  };
+  __device__ __forceinline__ void fetch_row(int64_t b, int g, RowRaw& r) const {
+#pragma unroll
+    for (int kb = 0; kb < D / 16; ++kb) r.x[kb] = Elt<T>::raw4(G + b * D + 16 * kb + 4 * g);
+    const uint32_t* mw = mask + b * (D / 32);
+    if constexpr (D == 64) {
+      const uint2 v = *reinterpret_cast<const uint2*>(mw);
+      r.m[0] = v.x; r.m[1] = v.y;
+    } else {
+#pragma unroll
+      for (int q = 0; q < D / 128; ++q) {
+        const uint4 v = *reinterpret_cast<const uint4*>(mw + 4 * q);
+        r.m[4 * q] = v.x; r.m[4 * q + 1] = v.y; r.m[4 * q + 2] = v.z; r.m[4 * q + 3] = v.w;
+      }
+    }
+  }
+  __device__ __forceinline__ void cook_row(const RowRaw& r, int64_t b, int g, bool live, f32x4 (&a)[D / 16]) const {
+#pragma unroll
+    for (int kb = 0; kb < D / 16; ++kb) {
+      f32x4 x = Elt<T>::cook4(r.x[kb]);
+      const uint32_t nib = r.m[kb >> 1] >> (16 * (kb & 1) + 4 * g);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) x[q] = ((nib >> q) & 1u) ? x[q] : 0.f;
+      if (tee && live) {
+        T* o = tee + b * D + 16 * kb + 4 * g;
+        if constexpr (sizeof(T) == 4) {
+          *reinterpret_cast<f32x4*>(o) = x;
+        } else {
+          *reinterpret_cast<uint2*>(o) = uint2{pack2bf(x[0], x[1]), pack2bf(x[2], x[3])};
+        }
+      }
+      a[kb] = x;
+    }
+  }
+  __device__ __forceinline__ f32x4 stored4(const RowRaw& r, int kb) const { return Elt<T>::cook4(r.x[kb]); }
+  __device__ __forceinline__ f32x4 operand4(const RowRaw& r, int kb, int g) const {
+    f32x4 x = Elt<T>::cook4(r.x[kb]);
+    const uint32_t nib = r.m[kb >> 1] >> (16 * (kb & 1) + 4 * g);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) x[q] = ((nib >> q) & 1u) ? x[q] : 0.f;
+    return x;
+  }
+  static constexpr bool kTee = true;
+  __device__ __forceinline__ void tee4(int64_t b, int kb, int g, f32x4 x) const {
+    if (!tee) return;
+    T* o = tee + b * D + 16 * kb + 4 * g;
+    if constexpr (sizeof(T) == 4) {
+      *reinterpret_cast<f32x4*>(o) = x;
+    } else {
+      *reinterpret_cast<uint2*>(o) = uint2{pack2bf(x[0], x[1]), pack2bf(x[2], x[3])};
+    }
+  }
 };
 
 // ---- epilogues ------------------------------------------------------------
@@ -281,8 +357,12 @@ struct LoadMasked {
 // element of the tile (all loads), then store(i, ro, c, acc, pre) (all stores):
 // the two phases keep loads from waiting behind stores when the addend is the
 // output itself (dH += ...).
-template <int D, class T = float, class TA = T>
+// kAddendIsA: the addend rows are the A operand's rows as stored (before the
+// loader's transform), at the same row index; a kernel holding those rows in
+// registers may use them instead of reading the addend again.
+template <int D, class T = float, class TA = T, bool kAddendIsA = false>
 struct StoreRows {
+  static constexpr bool kAddA = kAddendIsA;
   T* out;
   RowMap map;
   const float* bias;  // [D] or null
@@ -305,6 +385,9 @@ struct StoreRows {
     f32x4 v = bias ? *reinterpret_cast<const f32x4*>(bias + c) : f32x4{0.f, 0.f, 0.f, 0.f};
     if (addend) v += Elt<TA>::load4(addend + ro * D + c);
     return v;
+  }
+  __device__ __forceinline__ f32x4 bias4(int c) const {
+    return bias ? *reinterpret_cast<const f32x4*>(bias + c) : f32x4{0.f, 0.f, 0.f, 0.f};
   }
   __device__ __forceinline__ void store4(int64_t, int64_t ro, int c, f32x4 acc, f32x4 pre) const {
     const f32x4 r = acc + pre;
@@ -446,6 +529,167 @@ int launch_gemm_rows(const char* name, int64_t n_rows, const float* W, ALoad alo
     }
   }
   HG_LAUNCH(name, kern, dim3((unsigned)grid, D / DN), dim3(kGemmThreads), lds, s, n_rows, W, aload, epi);
+  return HG_OK;
+}
+
+// ---- gemm_rows, software-pipelined (d <= 128) ---------------------------------------
+// Same tiles, LDS layout and transposed MFMA as k_gemm_rows, with the memory
+// traffic spread over the tile instead of bunched at its ends:
+//  - the next tile's A rows are loaded while the current tile is multiplied,
+//    into the other of two register sets (the tile loop is unrolled by two,
+//    so no prefetched value is copied: a copy would wait for the load);
+//  - row-list entries of A are read two tiles ahead, the output rows' one
+//    tile ahead, so no address waits on a load issued just before;
+//  - output columns go in groups of NG blocks: a group's epilogue operands
+//    are loaded before its MFMAs and its results stored right after them.
+// The loader's fetch_row issues the loads; cook_row turns them into MFMA
+// operands (mask, conversion) when they are used.
+template <int D, bool kTransW, class ALoad, class Epi, bool kListA, bool kListO, int NG>
+__global__ void __launch_bounds__(kGemmThreads, 4) k_gemm_rows_pp(int64_t n_rows, const float* __restrict__ W,
+                                                               ALoad aload, Epi epi) {
+  static_assert(D == 64 || D == 128, "pipelined gemm_rows: d = 64 or 128");
+  constexpr int KB = D / 16, NB = D / 16;
+  static_assert(NB % NG == 0, "column groups must divide the column blocks");
+  static_assert(!Epi::kAddA || !kListO, "an addend taken from A needs the output rows to be the A rows");
+  constexpr int kRowsPerTile = 16 * (kGemmThreads / 64);
+  extern __shared__ f32x4 wl[];
+  const int tid = threadIdx.x;
+  for (int e = tid; e < KB * NB * 64; e += kGemmThreads) {
+    const int l = e & 63;
+    const int nb = (e >> 6) % NB;
+    const int kb = (e >> 6) / NB;
+    const int j = 16 * nb + (l & 15);
+    const int k0 = 16 * kb + 4 * (l >> 4);
+    f32x4 v;
+    if (kTransW) {
+      v = *reinterpret_cast<const f32x4*>(W + (int64_t)j * D + k0);
+    } else {
+      v[0] = W[(int64_t)(k0 + 0) * D + j];
+      v[1] = W[(int64_t)(k0 + 1) * D + j];
+      v[2] = W[(int64_t)(k0 + 2) * D + j];
+      v[3] = W[(int64_t)(k0 + 3) * D + j];
+    }
+    wl[e] = v;
+  }
+  __syncthreads();
+  const int w = tid >> 6;
+  const int l = lane64();
+  const int g = l >> 4, c = l & 15;
+  const int64_t ntiles = (n_rows + kRowsPerTile - 1) / kRowsPerTile;
+  const int64_t G = gridDim.x;
+  typedef RowMap::Key<kListA> KA;
+  typedef RowMap::Key<kListO> KO;
+  typedef typename ALoad::RowRaw RR;
+  // lane (c, g) of wave w owns row 16 w + c of a tile; rows past the end are
+  // read from the last row and never stored
+  auto row_in = [&](int64_t t) -> int64_t {
+    const int64_t i = t * kRowsPerTile + 16 * w + c;
+    return i < n_rows ? i : n_rows - 1;
+  };
+  auto tile = [&](int64_t t, const RR& x, KA ka, KO ko) {
+    const int64_t i = t * kRowsPerTile + 16 * w + c;
+    const bool live = i < n_rows;
+    const int64_t ro = epi.map.template row_of<kListO>(ko);
+    const int64_t ra = aload.map.template row_of<kListA>(ka);
+#pragma unroll
+    for (int p = 0; p < NB / NG; ++p) {
+      f32x4 pre[NG];
+#pragma unroll
+      for (int q = 0; q < NG; ++q) {
+        const int col = 16 * (p * NG + q) + 4 * g;
+        if constexpr (Epi::kAddA) {
+          // output column block p NG + q covers the lane's A columns of K block p NG + q
+          pre[q] = epi.addend ? epi.bias4(col) + aload.stored4(x, p * NG + q) : epi.bias4(col);
+        } else {
+          pre[q] = epi.pre4(i, ro, col);
+        }
+      }
+      f32x4 acc[NG];
+#pragma unroll
+      for (int q = 0; q < NG; ++q) acc[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) {
+        const f32x4 a = aload.operand4(x, kb, g);
+        if (ALoad::kTee && p == 0 && live) aload.tee4(ra, kb, g, a);
+        f32x4 b[NG];
+#pragma unroll
+        for (int q = 0; q < NG; ++q) b[q] = wl[(kb * NB + p * NG + q) * 64 + l];
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+#pragma unroll
+          for (int q = 0; q < NG; ++q) acc[q] = mfma4(b[q][s], a[s], acc[q]);
+      }
+      if (live) {
+#pragma unroll
+        for (int q = 0; q < NG; ++q) epi.store4(i, ro, 16 * (p * NG + q) + 4 * g, acc[q], pre[q]);
+      }
+    }
+  };
+  int64_t t = blockIdx.x;
+  if (t >= ntiles) return;
+  KA ka0 = aload.map.template key<kListA>(row_in(t));
+  KA ka1 = aload.map.template key<kListA>(row_in(t + G));
+  KO ko0 = epi.map.template key<kListO>(row_in(t));
+  KO ko1;
+  RR x0, x1;
+  aload.fetch_row(aload.map.template row_of<kListA>(ka0), g, x0);
+  // the body handles tiles t and t + G (the second may lie past the end: its
+  // rows are clamped and nothing is stored)
+  for (; t < ntiles; t += 2 * G) {
+    {
+      const KA kc = ka0;
+      aload.fetch_row(aload.map.template row_of<kListA>(ka1), g, x1);
+      ka0 = aload.map.template key<kListA>(row_in(t + 2 * G));
+      ko1 = epi.map.template key<kListO>(row_in(t + G));
+      __builtin_amdgcn_sched_barrier(0);
+      tile(t, x0, kc, ko0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    {
+      const KA kc = ka1;
+      aload.fetch_row(aload.map.template row_of<kListA>(ka0), g, x0);
+      ka1 = aload.map.template key<kListA>(row_in(t + 3 * G));
+      ko0 = epi.map.template key<kListO>(row_in(t + 2 * G));
+      __builtin_amdgcn_sched_barrier(0);
+      tile(t + G, x1, kc, ko1);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+}
+
+constexpr int kGemmPPBlocksPerCu = 2;
+template <int D, bool kTransW, class ALoad, class Epi>
+int launch_gemm_rows_pp(const char* name, int64_t n_rows, const float* W, ALoad aload, Epi epi, hipStream_t s) {
+  if (n_rows <= 0) return HG_OK;
+  // the masked fp32 loader keeps its raw rows live through the tile (they are
+  // the residual addend): one column block per group keeps it in 128 VGPRs
+  constexpr int NG = (Epi::kAddA && ALoad::kTee && sizeof(typename ALoad::Raw) == 16) ? 1 : 2;
+  const int64_t tiles = cdiv(n_rows, 16 * (kGemmThreads / 64));
+  const int64_t cap = (int64_t)num_cus() * kGemmPPBlocksPerCu;
+  const int64_t grid = tiles < cap ? tiles : cap;
+  const size_t lds = sizeof(float) * D * D;
+  const bool la = aload.map.list != nullptr, lo = epi.map.list != nullptr;
+#define HG_PP_LAUNCH(LA_, LO_) \
+  HG_LAUNCH(name, (k_gemm_rows_pp<D, kTransW, ALoad, Epi, LA_, LO_, NG>), dim3((unsigned)grid), \
+            dim3(kGemmThreads), lds, s, n_rows, W, aload, epi)
+  if constexpr (Epi::kAddA) {
+    // the addend is read from the A registers: output row i must be A row i
+    if (la || lo || aload.map.first != epi.map.first || aload.map.mul != epi.map.mul ||
+        aload.map.add != epi.map.add)
+      return fail(HG_ERR_ARG, "%s: an addend taken from A needs identical contiguous row maps", name);
+    HG_PP_LAUNCH(false, false);
+  } else {
+    if (la && lo) {
+      HG_PP_LAUNCH(true, true);
+    } else if (la) {
+      HG_PP_LAUNCH(true, false);
+    } else if (lo) {
+      HG_PP_LAUNCH(false, true);
+    } else {
+      HG_PP_LAUNCH(false, false);
+    }
+  }
+#undef HG_PP_LAUNCH
   return HG_OK;
 }
 
