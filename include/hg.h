@@ -13,6 +13,9 @@
  *                           (message, aggregation and update equations of the
  *                           "Heterogeneous Graph Transformer" paragraph, in the
  *                           relation-typed mean-aggregation form)
+ *   hg_hgt_fwd/_bwd         the attention form of that layer: multi-head
+ *                           mutual attention, per-destination softmax and
+ *                           weighted aggregation (E6-E11)
  *   hg_align_loss_fwd_bwd   the CCA consistency-alignment loss on the overlap
  *                           nodes and its gradient (Section "Cross-Subgraph
  *                           Consistency Alignment", standardisation, invariance,
@@ -190,6 +193,64 @@ int hg_layer_bwd(const hg_subgraph* s, const hg_layer_desc* L, const void* H_in,
                  const float* W_rel, const float* W_self, const void* saved,
                  const void* dH_out, void* dH_in, float* dW_rel, float* dW_self,
                  float* dbias, void* ws, size_t ws_bytes, void* stream);
+
+/* ---- heterogeneous graph transformer layer (E6-E11) ------------------------
+ * S heads of width dk = d / S.  For an edge e = (i -> j) of relation r:
+ *   K = H W_K[type] + b_K[type], Q = H W_Q[type] + b_Q[type], V = H W_V[type] + b_V[type]
+ *   score^s(e) = (K^s_i W_att[r, s]) . Q^s_j * mu[type(i)][r][type(j)] / sqrt(dk)   (E6)
+ *   msg^s(e)   = V^s_i W_msg[r, s]                                                   (E7)
+ *   alpha^s(e) = softmax of score^s over the in-edges of j, all relations          (E8)
+ *   h~_j       = concat_s sum_e alpha^s(e) msg^s(e)   (0 without in-edges)   (E9, E10)
+ *   z_j = h~_j W_agg[type(j)] + b_agg[type(j)],
+ *   h'_j = (relu ? max(z_j, 0) : z_j) + (residual ? h_j : 0)                       (E11)
+ * x^s is columns [s dk, s dk + dk) of x.  Weights are float32 in the
+ * row-vector convention: W_K, W_Q, W_V, W_agg [n_ntype, d, d]; b_K, b_Q, b_V,
+ * b_agg [n_ntype, d] (each bias may be NULL = 0); W_att, W_msg
+ * [n_rel, S, dk, dk]; mu [n_ntype, n_rel, n_ntype].  Passing W_V = W_K and
+ * b_V = b_K makes the message reuse the key projection. */
+typedef struct hg_hgt_desc {
+  int32_t d;         /* 64 or 128 */
+  int32_t heads;     /* S: d / S a power of two >= 4 */
+  int32_t dtype;     /* HG_DTYPE_F32 */
+  int32_t relu;      /* 0 or 1 */
+  int32_t residual;  /* 0 or 1 */
+} hg_hgt_desc;
+
+typedef struct hg_hgt_weights {
+  const float *W_K, *b_K, *W_Q, *b_Q, *W_V, *b_V;
+  const float *W_att, *W_msg, *mu;
+  const float *W_agg, *b_agg;
+} hg_hgt_weights;
+
+/* Gradients, same shapes as hg_hgt_weights; all OVERWRITTEN.  A bias
+ * gradient may be NULL (not computed). */
+typedef struct hg_hgt_grads {
+  float *W_K, *b_K, *W_Q, *b_Q, *W_V, *b_V;
+  float *W_att, *W_msg, *mu;
+  float *W_agg, *b_agg;
+} hg_hgt_grads;
+
+/* Bytes of `saved`: the forward's intermediates for the backward (K, Q, V,
+ * the relation transforms of K and V, h~ and the per-head log-sum-exp of the
+ * scores); its layout is internal.  The ReLU mask is a separate argument. */
+size_t hg_hgt_saved_size(const hg_subgraph* s, const hg_hgt_desc* L);
+size_t hg_hgt_fwd_workspace_size(const hg_subgraph* s, const hg_hgt_desc* L);
+size_t hg_hgt_bwd_workspace_size(const hg_subgraph* s, const hg_hgt_desc* L);
+
+/* Forward.  H_in, H_out: [n_sub, d] float32, H_out must not alias H_in.
+ * mask [n_sub, d / 32] uint32 receives the ReLU decisions (bit c of row j at
+ * word j*(d/32) + c/32, bit c%32, is 1 iff z[j][c] > 0; all ones when
+ * relu = 0).  Asynchronous. */
+int hg_hgt_fwd(const hg_subgraph* s, const hg_hgt_desc* L, const void* H_in, const hg_hgt_weights* W,
+               void* H_out, void* mask, void* saved, void* ws, size_t ws_bytes, void* stream);
+
+/* Backward of hg_hgt_fwd for dH_out = dL/dH_out, from the mask and `saved`
+ * of the forward call with the same inputs (dZ = dH_out * mask).  dH_in
+ * [n_sub, d] and every gradient are OVERWRITTEN.  Deterministic: no
+ * floating-point atomics. */
+int hg_hgt_bwd(const hg_subgraph* s, const hg_hgt_desc* L, const void* H_in, const hg_hgt_weights* W,
+               const void* mask, const void* saved, const void* dH_out, void* dH_in, const hg_hgt_grads* dW,
+               void* ws, size_t ws_bytes, void* stream);
 
 /* CCA alignment on the overlap batch B (|B| = M):
  *   X = H[overlap] (local view), Y = H_ref (the other subgraph's view, row b

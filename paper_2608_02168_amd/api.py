@@ -35,7 +35,8 @@ HG_MAX_NTYPE = 255
 EXPORTS = [
     "hg_plan_size", "hg_build_csr_workspace_size", "hg_build_csr",
     "hg_layer_saved_size", "hg_layer_fwd_workspace_size", "hg_layer_bwd_workspace_size",
-    "hg_layer_fwd", "hg_layer_bwd", "hg_align_workspace_size", "hg_align_loss_fwd_bwd",
+    "hg_layer_fwd", "hg_layer_bwd", "hg_hgt_saved_size", "hg_hgt_fwd_workspace_size",
+    "hg_hgt_bwd_workspace_size", "hg_hgt_fwd", "hg_hgt_bwd", "hg_align_workspace_size", "hg_align_loss_fwd_bwd",
     "hg_status_string", "hg_last_error_detail", "hg_timing_enable", "hg_timing_collect",
 ]
 
@@ -76,6 +77,18 @@ class LayerDesc(C.Structure):
                 ("relu", C.c_int32), ("residual", C.c_int32)]
 
 
+HGT_PARAMS = ("W_K", "b_K", "W_Q", "b_Q", "W_V", "b_V", "W_att", "W_msg", "mu", "W_agg", "b_agg")
+
+
+class HgtDesc(C.Structure):
+    _fields_ = [("d", C.c_int32), ("heads", C.c_int32), ("dtype", C.c_int32), ("relu", C.c_int32),
+                ("residual", C.c_int32)]
+
+
+class HgtWeights(C.Structure):
+    _fields_ = [(n, C.c_void_p) for n in HGT_PARAMS]
+
+
 _lib = None
 
 
@@ -98,6 +111,11 @@ def lib() -> C.CDLL:
         "hg_layer_bwd_workspace_size": (sz, [vp, vp]),
         "hg_layer_fwd": (C.c_int, [vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
         "hg_layer_bwd": (C.c_int, [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "hg_hgt_saved_size": (sz, [vp, vp]),
+        "hg_hgt_fwd_workspace_size": (sz, [vp, vp]),
+        "hg_hgt_bwd_workspace_size": (sz, [vp, vp]),
+        "hg_hgt_fwd": (C.c_int, [vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "hg_hgt_bwd": (C.c_int, [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
         "hg_align_workspace_size": (sz, [i64, i32]),
         "hg_align_loss_fwd_bwd": (C.c_int, [i64, i32, i32, i64, vp, vp, vp, vp, f32, f32, f32,
                                             i32, vp, vp, vp, vp, sz, vp]),
@@ -305,6 +323,71 @@ def hg_layer_bwd(sub: Subgraph, H_in, W_rel, W_self, saved, dH_out, relu=True, r
                           _ptr(saved), _ptr(dH_out), _ptr(dH_in), _ptr(dW_rel), _ptr(dW_self),
                           _ptr(dbias), _ptr(ws), ws.numel(), _stream(stream)), "hg_layer_bwd")
     return dH_in, dW_rel, dW_self, dbias
+
+
+def _hgt_desc(d: int, heads: int, relu: bool, residual: bool) -> HgtDesc:
+    return HgtDesc(d, heads, HG_DTYPE_F32, int(relu), int(residual))
+
+
+def _hgt_struct(weights: dict) -> HgtWeights:
+    """weights: name -> device float32 tensor (biases may be missing or None)."""
+    return HgtWeights(*[_ptr(weights.get(n)) for n in HGT_PARAMS])
+
+
+def hg_hgt_saved_size(sub: Subgraph, d: int, heads: int) -> int:
+    desc = _hgt_desc(d, heads, True, True)
+    return int(lib().hg_hgt_saved_size(C.byref(sub.c), C.byref(desc)))
+
+
+def hg_hgt_fwd_workspace_size(sub: Subgraph, d: int, heads: int) -> int:
+    desc = _hgt_desc(d, heads, True, True)
+    return int(lib().hg_hgt_fwd_workspace_size(C.byref(sub.c), C.byref(desc)))
+
+
+def hg_hgt_bwd_workspace_size(sub: Subgraph, d: int, heads: int) -> int:
+    desc = _hgt_desc(d, heads, True, True)
+    return int(lib().hg_hgt_bwd_workspace_size(C.byref(sub.c), C.byref(desc)))
+
+
+def hg_hgt_fwd(sub: Subgraph, H_in, weights: dict, heads: int, relu=True, residual=True, H_out=None,
+               mask=None, saved=None, ws=None, stream=None):
+    """Attention layer forward; returns (H_out, mask, saved): mask is the ReLU
+    bitmask [n_sub, d/32] int32, saved a uint8 buffer for the backward."""
+    d = int(H_in.shape[1])
+    desc = _hgt_desc(d, heads, relu, residual)
+    L = lib()
+    if H_out is None:
+        H_out = torch.empty_like(H_in)
+    if mask is None:
+        mask = torch.empty((max(1, sub.n_sub), d // 32), dtype=torch.int32, device=H_in.device)
+    if saved is None:
+        saved = _ws(int(L.hg_hgt_saved_size(C.byref(sub.c), C.byref(desc))), H_in.device)
+    if ws is None:
+        ws = _ws(int(L.hg_hgt_fwd_workspace_size(C.byref(sub.c), C.byref(desc))), H_in.device)
+    W = _hgt_struct(weights)
+    _check(L.hg_hgt_fwd(C.byref(sub.c), C.byref(desc), _ptr(H_in), C.byref(W), _ptr(H_out), _ptr(mask),
+                        _ptr(saved), _ptr(ws), ws.numel(), _stream(stream)), "hg_hgt_fwd")
+    return H_out, mask, saved
+
+
+def hg_hgt_bwd(sub: Subgraph, H_in, weights: dict, heads: int, mask, saved, dH_out, relu=True, residual=True,
+               dH_in=None, grads: Optional[dict] = None, ws=None, stream=None):
+    """Attention layer backward; returns (dH_in, grads) with grads a dict of
+    the same names as the weights (bias gradients for the biases given)."""
+    d = int(H_in.shape[1])
+    desc = _hgt_desc(d, heads, relu, residual)
+    L = lib()
+    if dH_in is None:
+        dH_in = torch.empty_like(H_in)
+    if grads is None:
+        grads = {n: torch.empty_like(w) for n, w in weights.items() if w is not None}
+    if ws is None:
+        ws = _ws(int(L.hg_hgt_bwd_workspace_size(C.byref(sub.c), C.byref(desc))), H_in.device)
+    G = _hgt_struct(grads)
+    W = _hgt_struct(weights)
+    _check(L.hg_hgt_bwd(C.byref(sub.c), C.byref(desc), _ptr(H_in), C.byref(W), _ptr(mask), _ptr(saved),
+                        _ptr(dH_out), _ptr(dH_in), C.byref(G), _ptr(ws), ws.numel(), _stream(stream)), "hg_hgt_bwd")
+    return dH_in, grads
 
 
 def hg_align_workspace_size(M: int, d: int) -> int:

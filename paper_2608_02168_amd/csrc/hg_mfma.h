@@ -363,6 +363,7 @@ struct LoadMasked {
 template <int D, class T = float, class TA = T, bool kAddendIsA = false>
 struct StoreRows {
   static constexpr bool kAddA = kAddendIsA;
+  static constexpr bool kMask = false;
   T* out;
   RowMap map;
   const float* bias;  // [D] or null
@@ -619,7 +620,20 @@ __global__ void __launch_bounds__(kGemmThreads, 4) k_gemm_rows_pp(int64_t n_rows
 #pragma unroll
           for (int q = 0; q < NG; ++q) acc[q] = mfma4(b[q][s], a[s], acc[q]);
       }
-      if (live) {
+      if constexpr (Epi::kMask) {
+        // store4 returns the 4 output-decision bits of its columns; the lanes
+        // (c, 0..3) of a 32-column group hold one 32-bit mask word together
+        static_assert(NG == 2, "mask words need 32-column groups");
+        uint32_t word = 0;
+#pragma unroll
+        for (int q = 0; q < NG; ++q) {
+          const uint32_t nib = live ? epi.store4(i, ro, 16 * (p * NG + q) + 4 * g, acc[q], pre[q]) : 0u;
+          word |= nib << (16 * q + 4 * g);
+        }
+        word |= __shfl_xor(word, 16, 64);
+        word |= __shfl_xor(word, 32, 64);
+        if (live && g == 0) epi.mask_word(ro, p, word);
+      } else if (live) {
 #pragma unroll
         for (int q = 0; q < NG; ++q) epi.store4(i, ro, 16 * (p * NG + q) + 4 * g, acc[q], pre[q]);
       }

@@ -217,6 +217,27 @@ def layer_weights(seed: int, layer: int, n_rel: int, n_ntype: int, d: int,
     return LayerWeights(w_rel, w_self, bias)
 
 
+def hgt_weights(seed: int, layer: int, n_rel: int, n_ntype: int, d: int, heads: int,
+                bias_range: float = 0.0, mu_range=(0.5, 1.5)) -> dict:
+    """Attention-layer weights: Xavier-uniform d x d projections and per-head
+    dk x dk relation matrices, biases U(+-bias_range), mu U(mu_range); float32."""
+    rng = _rng(seed, 200 + layer)
+    dk = d // heads
+    a, ak = np.sqrt(6.0 / (2 * d)), np.sqrt(6.0 / (2 * dk))
+    out = {}
+    for name in ("W_K", "W_Q", "W_V", "W_agg"):
+        out[name] = rng.uniform(-a, a, size=(n_ntype, d, d)).astype(np.float32)
+    for name in ("W_att", "W_msg"):
+        out[name] = rng.uniform(-ak, ak, size=(n_rel, heads, dk, dk)).astype(np.float32)
+    out["mu"] = rng.uniform(mu_range[0], mu_range[1], size=(n_ntype, n_rel, n_ntype)).astype(np.float32)
+    for name in ("b_K", "b_Q", "b_V", "b_agg"):
+        if bias_range > 0:
+            out[name] = rng.uniform(-bias_range, bias_range, size=(n_ntype, d)).astype(np.float32)
+        else:
+            out[name] = np.zeros((n_ntype, d), dtype=np.float32)
+    return out
+
+
 def round_bf16(x: np.ndarray) -> np.ndarray:
     """float32 -> nearest-even bfloat16 value, returned as float32 (storage rounding)."""
     u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
