@@ -296,6 +296,418 @@ int hgt_fwd_impl(const hg_subgraph* s, const hg_hgt_desc* L, const float* Hin, c
   return HG_OK;
 }
 
+
+// ---- backward ------------------------------------------------------------------
+// With alpha^s(e) recomputed from the saved log-sum-exp, dalpha = dh~_j . msg
+// and D_j^s = dh~_j^s . h~_j^s (= sum_e alpha dalpha):
+//   dscore^s(e) = alpha (dalpha - D_j^s)
+//   dQ_j   += dscore c Kt(e),  dKt(e) += dscore c Q_j,  dVt(e) += alpha dh~_j
+//   dmu    += dscore (Kt(e) . Q_j) / sqrt(dk)
+// The destination pass (CSR rows) produces dQ, D and per-row sums for dmu;
+// the source pass (CSC work items of the plan) produces dKt and dVt.
+constexpr int kMaxTypesBwd = 4;
+
+struct HgtBwdWs {
+  float *dZ, *dht, *dQ, *dK, *dV;  // [n_sub, d]
+  float* Dsum;                     // [n_sub, S]
+  float *dKt, *dVt;                // [n_sub * R, d]
+  double *pk, *pv;                 // [plan_partials, d]
+  float* rowpart;                  // [n_sub * R * T]: dmu sums of each CSR row, by source type
+  float* mupart;                   // [T * R * T, kMuChunks]
+  float *Watt, *Wmsg;              // [R, d, d] block-diagonal expansions
+  float *gatt, *gmsg;              // [R, d, d] full gradients before the block extraction
+  float *splitk, *colsum;          // split-K partials
+  template <class A>
+  void layout(A& a, const hg_subgraph* s, int d, int S);
+};
+constexpr int kMuChunks = 64;
+
+template <class A>
+void HgtBwdWs::layout(A& a, const hg_subgraph* s, int d, int S) {
+  const int64_t n = s->n_sub, R = s->n_rel, T = s->n_ntype;
+  dZ = a.template take<float>(n * d);
+  dht = a.template take<float>(n * d);
+  dQ = a.template take<float>(n * d);
+  dK = a.template take<float>(n * d);
+  dV = a.template take<float>(n * d);
+  Dsum = a.template take<float>(n * S);
+  dKt = a.template take<float>(n * R * d);
+  dVt = a.template take<float>(n * R * d);
+  pk = a.template take<double>(s->plan_partials * d);
+  pv = a.template take<double>(s->plan_partials * d);
+  rowpart = a.template take<float>(n * R * T);
+  mupart = a.template take<float>(T * R * T * kMuChunks);
+  Watt = a.template take<float>(R * d * d);
+  Wmsg = a.template take<float>(R * d * d);
+  gatt = a.template take<float>(R * d * d);
+  gmsg = a.template take<float>(R * d * d);
+  splitk = a.template take<float>(splitk_max_chunks() * (int64_t)d * d);
+  colsum = a.template take<float>(splitk_max_chunks() * (int64_t)d);
+}
+
+template <int LPH>
+__device__ __forceinline__ float head_sum(float v) {
+#pragma unroll
+  for (int o = 1; o < LPH; o <<= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+// Destination pass: one wave per node j, its CSR rows one relation at a time.
+template <int D, int S>
+__global__ void __launch_bounds__(kAttnThreads) k_hgt_attn_bwd_dst(
+    int64_t n_sub, int32_t R, int32_t T, const int32_t* __restrict__ type_off, const int32_t* __restrict__ csr_ptr,
+    const int32_t* __restrict__ csr_col, const float* __restrict__ Q, const float* __restrict__ Kt,
+    const float* __restrict__ Vt, const float* __restrict__ ht, const float* __restrict__ dht,
+    const float* __restrict__ lse, const float* __restrict__ mu, float inv_sqrt_dk, float* __restrict__ dQ,
+    float* __restrict__ Dsum, float* __restrict__ rowpart) {
+  constexpr int LPR = D / 4, EPW = 64 / LPR, DK = D / S, LPH = DK / 4, U = 2;
+  const int l = threadIdx.x & 63;
+  const int slot = l / LPR, lr = l % LPR, c0 = lr * 4, head = lr / LPH;
+  const bool head_lead = (lr % LPH) == 0;
+  const int64_t wave0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+  const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
+  for (int64_t j = wave0; j < n_sub; j += nwaves) {
+    const int tj = type_of(j, T, type_off);
+    const f32x4 q = *reinterpret_cast<const f32x4*>(Q + j * D + c0);
+    const f32x4 g = *reinterpret_cast<const f32x4*>(dht + j * D + c0);
+    const f32x4 h = *reinterpret_cast<const f32x4*>(ht + j * D + c0);
+    const float dsum = head_sum<LPH>(g[0] * h[0] + g[1] * h[1] + g[2] * h[2] + g[3] * h[3]);
+    const float lj = lse[j * S + head];
+    if (slot == 0 && head_lead) Dsum[j * S + head] = dsum;
+    f32x4 dq = {0.f, 0.f, 0.f, 0.f};
+    const int64_t rb = j * R;
+    for (int r = 0; r < R; ++r) {
+      const int32_t b0 = csr_ptr[rb + r], b1 = csr_ptr[rb + r + 1];
+      float dm[kMaxTypesBwd] = {0.f, 0.f, 0.f, 0.f};
+      for (int32_t base = b0; base < b1; base += 64) {
+        const int32_t pos = base + l;
+        int32_t rowi = 0, ti = 0;
+        float cf = 0.f;
+        if (pos < b1) {
+          const int32_t src = csr_col[pos];
+          ti = type_of(src, T, type_off);
+          rowi = src * R + r;
+          cf = mu[((int64_t)ti * R + r) * T + tj] * inv_sqrt_dk;
+        }
+        const int cnt = (b1 - base) < 64 ? (b1 - base) : 64;
+        for (int e = 0; e < cnt; e += EPW * U) {
+          f32x4 kv[U], vv[U];
+          float cc[U];
+          int tt[U];
+          bool ok[U];
+#pragma unroll
+          for (int u = 0; u < U; ++u) {
+            const int my = e + u * EPW + slot;
+            const int32_t qi = __shfl(rowi, my & 63, 64);
+            cc[u] = __shfl(cf, my & 63, 64);
+            tt[u] = __shfl(ti, my & 63, 64);
+            ok[u] = my < cnt;
+            if (ok[u]) {
+              kv[u] = *reinterpret_cast<const f32x4*>(Kt + (int64_t)qi * D + c0);
+              vv[u] = *reinterpret_cast<const f32x4*>(Vt + (int64_t)qi * D + c0);
+            } else {
+              kv[u] = vv[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+            }
+          }
+#pragma unroll
+          for (int u = 0; u < U; ++u) {
+            const float dot = head_sum<LPH>(kv[u][0] * q[0] + kv[u][1] * q[1] + kv[u][2] * q[2] + kv[u][3] * q[3]);
+            const float dal = head_sum<LPH>(vv[u][0] * g[0] + vv[u][1] * g[1] + vv[u][2] * g[2] + vv[u][3] * g[3]);
+            if (ok[u]) {
+              const float a = __expf(dot * cc[u] - lj);
+              const float ds = a * (dal - dsum);
+              dq += (ds * cc[u]) * kv[u];
+              const float cm = head_lead ? ds * dot * inv_sqrt_dk : 0.f;
+#pragma unroll
+              for (int t = 0; t < kMaxTypesBwd; ++t) dm[t] += (tt[u] == t) ? cm : 0.f;
+            }
+          }
+        }
+      }
+      for (int t = 0; t < T; ++t) {
+        const float v = wave_sum(dm[t]);
+        if (l == 0) rowpart[(rb + r) * T + t] = v;
+      }
+    }
+#pragma unroll
+    for (int o = LPR; o < 64; o <<= 1)
+#pragma unroll
+      for (int k = 0; k < 4; ++k) dq[k] += __shfl_xor(dq[k], o, 64);
+    if (slot == 0) *reinterpret_cast<f32x4*>(dQ + j * D + c0) = dq;
+  }
+}
+
+// Source pass: one wave per work item (CSC row q = i * R + r or a chunk of
+// it); Kt and Vt of the row are read once, Q and dh~ gathered per out-edge.
+template <int D, int S>
+__global__ void __launch_bounds__(kAttnThreads) k_hgt_attn_bwd_src(
+    int64_t n_items, const int4* __restrict__ items, int32_t R, int32_t T, const int32_t* __restrict__ type_off,
+    const int32_t* __restrict__ csc_row, const float* __restrict__ Q, const float* __restrict__ Kt,
+    const float* __restrict__ Vt, const float* __restrict__ dht, const float* __restrict__ lse,
+    const float* __restrict__ Dsum, const float* __restrict__ mu, float inv_sqrt_dk, float* __restrict__ dKt,
+    float* __restrict__ dVt, double* __restrict__ pk, double* __restrict__ pv) {
+  constexpr int LPR = D / 4, EPW = 64 / LPR, DK = D / S, LPH = DK / 4, U = 2;
+  const int l = threadIdx.x & 63;
+  const int slot = l / LPR, lr = l % LPR, c0 = lr * 4, head = lr / LPH;
+  const int64_t wave0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+  const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
+  for (int64_t it = wave0; it < n_items; it += nwaves) {
+    const int4 item = items[it];
+    const int64_t qrow = item.x;
+    const int32_t i = (int32_t)(qrow / R), r = (int32_t)(qrow % R);
+    const int ti = type_of(i, T, type_off);
+    const f32x4 kt = *reinterpret_cast<const f32x4*>(Kt + qrow * D + c0);
+    const f32x4 vt = *reinterpret_cast<const f32x4*>(Vt + qrow * D + c0);
+    f64x4 dk = {0.0, 0.0, 0.0, 0.0}, dv = {0.0, 0.0, 0.0, 0.0};
+    for (int32_t base = item.y; base < item.z; base += 64) {
+      const int32_t pos = base + l;
+      int32_t jj = 0;
+      float cf = 0.f;
+      if (pos < item.z) {
+        jj = csc_row[pos];
+        cf = mu[((int64_t)ti * R + r) * T + type_of(jj, T, type_off)] * inv_sqrt_dk;
+      }
+      const int cnt = (item.z - base) < 64 ? (item.z - base) : 64;
+      for (int e = 0; e < cnt; e += EPW * U) {
+        f32x4 qv[U], gv[U];
+        float cc[U], lj[U], dj[U];
+        bool ok[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const int my = e + u * EPW + slot;
+          const int64_t j = __shfl(jj, my & 63, 64);
+          cc[u] = __shfl(cf, my & 63, 64);
+          ok[u] = my < cnt;
+          if (ok[u]) {
+            qv[u] = *reinterpret_cast<const f32x4*>(Q + j * D + c0);
+            gv[u] = *reinterpret_cast<const f32x4*>(dht + j * D + c0);
+            lj[u] = lse[j * S + head];
+            dj[u] = Dsum[j * S + head];
+          } else {
+            qv[u] = gv[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+            lj[u] = dj[u] = 0.f;
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const float dot = head_sum<LPH>(kt[0] * qv[u][0] + kt[1] * qv[u][1] + kt[2] * qv[u][2] + kt[3] * qv[u][3]);
+          const float dal = head_sum<LPH>(vt[0] * gv[u][0] + vt[1] * gv[u][1] + vt[2] * gv[u][2] + vt[3] * gv[u][3]);
+          if (ok[u]) {
+            const float a = __expf(dot * cc[u] - lj[u]);
+            const float ds = a * (dal - dj[u]);
+            const double wk = (double)(ds * cc[u]), wv = (double)a;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+              dk[k] += wk * (double)qv[u][k];
+              dv[k] += wv * (double)gv[u][k];
+            }
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int o = LPR; o < 64; o <<= 1)
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        dk[k] += __shfl_xor(dk[k], o, 64);
+        dv[k] += __shfl_xor(dv[k], o, 64);
+      }
+    if (slot == 0) {
+      if (item.w < 0) {
+        *reinterpret_cast<f32x4*>(dKt + qrow * D + c0) = f32x4{(float)dk[0], (float)dk[1], (float)dk[2], (float)dk[3]};
+        *reinterpret_cast<f32x4*>(dVt + qrow * D + c0) = f32x4{(float)dv[0], (float)dv[1], (float)dv[2], (float)dv[3]};
+      } else {
+        *reinterpret_cast<f64x4*>(pk + (int64_t)item.w * D + c0) = dk;
+        *reinterpret_cast<f64x4*>(pv + (int64_t)item.w * D + c0) = dv;
+      }
+    }
+  }
+}
+
+// Split rows: sum their float64 partial rows in chunk order.
+template <int D>
+__global__ void k_hgt_heavy_reduce(int64_t n_heavy, const int4* __restrict__ heavy, const double* __restrict__ pk,
+                                   const double* __restrict__ pv, float* __restrict__ dKt, float* __restrict__ dVt) {
+  constexpr int LPR = D / 4;
+  const int l = threadIdx.x & 63;
+  const int64_t wave0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+  const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
+  for (int64_t h = wave0; h < n_heavy; h += nwaves) {
+    const int4 hv = heavy[h];
+    if (l < LPR) {
+      f64x4 a = {0.0, 0.0, 0.0, 0.0}, b = {0.0, 0.0, 0.0, 0.0};
+      for (int32_t c = 0; c < hv.z; ++c) {
+        a += *reinterpret_cast<const f64x4*>(pk + (int64_t)(hv.y + c) * D + 4 * l);
+        b += *reinterpret_cast<const f64x4*>(pv + (int64_t)(hv.y + c) * D + 4 * l);
+      }
+      *reinterpret_cast<f32x4*>(dKt + (int64_t)hv.x * D + 4 * l) = f32x4{(float)a[0], (float)a[1], (float)a[2], (float)a[3]};
+      *reinterpret_cast<f32x4*>(dVt + (int64_t)hv.x * D + 4 * l) = f32x4{(float)b[0], (float)b[1], (float)b[2], (float)b[3]};
+    }
+  }
+}
+
+// [R, d, d] -> its diagonal blocks [R, S, dk, dk].
+__global__ void k_diagblocks(const float* __restrict__ full, int64_t R, int d, int S, float* __restrict__ out) {
+  const int dk = d / S;
+  const int64_t total = R * S * dk * dk;
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t r = e / ((int64_t)S * dk * dk);
+    const int s = (int)((e / ((int64_t)dk * dk)) % S);
+    const int a = (int)((e / dk) % dk), b = (int)(e % dk);
+    out[e] = full[(r * d + s * dk + a) * d + s * dk + b];
+  }
+}
+
+// dmu[ti][r][tj] = sum over destinations j of type tj of rowpart[(j R + r) T + ti]:
+// block (c, m) sums chunk c of the type range in a fixed tree order.
+__global__ void __launch_bounds__(256) k_dmu_partial(const float* __restrict__ rowpart, const int32_t* __restrict__ type_off,
+                                                    int32_t R, int32_t T, float* __restrict__ mupart) {
+  __shared__ float red[256];
+  const int m = blockIdx.y;  // (ti * R + r) * T + tj
+  const int tj = m % T, r = (m / T) % R, ti = m / (T * R);
+  const int64_t lo = type_off[tj], hi = type_off[tj + 1];
+  const int64_t per = (hi - lo + kMuChunks - 1) / kMuChunks;
+  const int64_t c0 = lo + per * blockIdx.x, c1 = (c0 + per < hi) ? c0 + per : hi;
+  float acc = 0.f;
+  for (int64_t j = c0 + threadIdx.x; j < c1; j += blockDim.x) acc += rowpart[(j * R + r) * T + ti];
+  red[threadIdx.x] = acc;
+  __syncthreads();
+  for (int o = 128; o > 0; o >>= 1) {
+    if (threadIdx.x < o) red[threadIdx.x] += red[threadIdx.x + o];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) mupart[(int64_t)m * kMuChunks + blockIdx.x] = red[0];
+}
+
+__global__ void k_dmu_final(const float* __restrict__ mupart, int M, float* __restrict__ dmu) {
+  const int m = blockIdx.x * blockDim.x + threadIdx.x;
+  if (m >= M) return;
+  float s = 0.f;
+  for (int c = 0; c < kMuChunks; ++c) s += mupart[(int64_t)m * kMuChunks + c];
+  dmu[m] = s;
+}
+
+template <int D>
+int hgt_bwd_impl(const hg_subgraph* s, const hg_hgt_desc* L, const float* Hin, const hg_hgt_weights* W,
+                 const uint32_t* mask, const void* saved, const float* G, float* dHin, const hg_hgt_grads* dW,
+                 void* ws, size_t ws_bytes, hipStream_t st) {
+  const int S = L->heads;
+  const int32_t R = s->n_rel, T = s->n_ntype;
+  Arena as(const_cast<void*>(saved), (size_t)-1);
+  HgtSaved sv;
+  sv.layout(as, s, D, S);
+  Arena a(ws, ws_bytes);
+  HgtBwdWs w;
+  w.layout(a, s, D, S);
+  if (!a.ok()) return fail(HG_ERR_CAPACITY, "attention backward workspace needs %zu bytes, got %zu", a.used, ws_bytes);
+  const PlanView pv = plan_view(s);
+  const float inv_sqrt_dk = 1.0f / std::sqrt((float)(D / S));
+  {
+    const int64_t n = (int64_t)R * D * D;
+    const unsigned g = (unsigned)(cdiv(n, 256) < 4096 ? cdiv(n, 256) : 4096);
+    HG_LAUNCH("hgt_blockdiag", k_blockdiag, dim3(g), dim3(256), 0, st, W->W_att, (int64_t)R, D, S, w.Watt);
+    HG_LAUNCH("hgt_blockdiag", k_blockdiag, dim3(g), dim3(256), 0, st, W->W_msg, (int64_t)R, D, S, w.Wmsg);
+  }
+  // (1) dZ = G * mask (written by the A load), dh~ = dZ W_agg^T; dW_agg, db_agg
+  for (int t = 0; t < T; ++t) {
+    const int64_t lo = s->type_off_host[t], hi = s->type_off_host[t + 1];
+    LoadMasked<D, float> la{G, mask, rows_contig(lo), w.dZ};
+    HG_TRY((launch_gemm_rows_pp<D, true>("hgt_bwd_dht", hi - lo, W->W_agg + (int64_t)t * D * D, la,
+                                         StoreRows<D, float>{w.dht, rows_contig(lo), nullptr, nullptr}, st)));
+    HG_TRY((launch_gemm_tn<D>("hgt_bwd_dw", hi - lo, LoadRows<D, float>{sv.ht, rows_contig(lo)},
+                              LoadRows<D, float>{w.dZ, rows_contig(lo)}, w.splitk, w.colsum,
+                              dW->W_agg + (int64_t)t * D * D, dW->b_agg ? dW->b_agg + (int64_t)t * D : nullptr, 0, st)));
+  }
+  // (2) destination pass, (3) source pass
+  if (s->n_sub > 0) {
+#define HG_ATTN_BWD(S_)                                                                                               \
+  do {                                                                                                                \
+    HG_LAUNCH("hgt_attn_bwd_dst", (k_hgt_attn_bwd_dst<D, S_>), dim3(attn_grid(s->n_sub)), dim3(kAttnThreads), 0, st, \
+              s->n_sub, R, T, (const int32_t*)s->type_off, (const int32_t*)s->csr_ptr, (const int32_t*)s->csr_col,   \
+              (const float*)sv.Q, (const float*)sv.Kt, (const float*)sv.Vt, (const float*)sv.ht,                     \
+              (const float*)w.dht, (const float*)sv.lse, W->mu, inv_sqrt_dk, w.dQ, w.Dsum, w.rowpart);               \
+    if (s->plan_items > 0)                                                                                            \
+      HG_LAUNCH("hgt_attn_bwd_src", (k_hgt_attn_bwd_src<D, S_>), dim3(attn_grid(s->plan_items)), dim3(kAttnThreads),  \
+                0, st, (int64_t)s->plan_items, pv.items, R, T, (const int32_t*)s->type_off,                           \
+                (const int32_t*)s->csc_row, (const float*)sv.Q, (const float*)sv.Kt, (const float*)sv.Vt,             \
+                (const float*)w.dht, (const float*)sv.lse, (const float*)w.Dsum, W->mu, inv_sqrt_dk, w.dKt, w.dVt,    \
+                w.pk, w.pv);                                                                                          \
+  } while (0)
+    switch (D / S) {
+      case 4: HG_ATTN_BWD(D / 4); break;
+      case 8: HG_ATTN_BWD(D / 8); break;
+      case 16: HG_ATTN_BWD(D / 16); break;
+      case 32: HG_ATTN_BWD(D / 32); break;
+      case 64: HG_ATTN_BWD(D / 64); break;
+      case 128: if constexpr (D >= 128) { HG_ATTN_BWD(D / 128); } break;
+      default: return fail(HG_ERR_UNSUPPORTED, "attention layer: head width %d", D / S);
+    }
+#undef HG_ATTN_BWD
+    if (s->plan_heavy > 0)
+      HG_LAUNCH("hgt_bwd_heavy", k_hgt_heavy_reduce<D>, dim3(attn_grid(s->plan_heavy)), dim3(kAttnThreads), 0, st,
+                (int64_t)s->plan_heavy, pv.heavy, (const double*)w.pk, (const double*)w.pv, w.dKt, w.dVt);
+  }
+  // (4) dK += dKt_r W_att[r]^T, dV += dVt_r W_msg[r]^T; full dW_att, dW_msg
+  HG_TRY(fill_f32(w.dK, 0.f, s->n_sub * (int64_t)D, st));
+  HG_TRY(fill_f32(w.dV, 0.f, s->n_sub * (int64_t)D, st));
+  int64_t off = 0;
+  for (int r = 0; r < R; ++r) {
+    const int64_t n = s->n_active[r];
+    const int64_t wo = (int64_t)r * D * D;
+    HG_TRY((launch_gemm_rows_pp<D, true>("hgt_bwd_dx_rel", n, w.Watt + wo,
+                                         LoadRows<D, float>{w.dKt, rows_list(pv.active + off, R, r)},
+                                         StoreRows<D, float>{w.dK, rows_list(pv.active + off), nullptr, w.dK}, st)));
+    HG_TRY((launch_gemm_rows_pp<D, true>("hgt_bwd_dx_rel", n, w.Wmsg + wo,
+                                         LoadRows<D, float>{w.dVt, rows_list(pv.active + off, R, r)},
+                                         StoreRows<D, float>{w.dV, rows_list(pv.active + off), nullptr, w.dV}, st)));
+    HG_TRY((launch_gemm_tn<D>("hgt_bwd_dw", n, LoadRows<D, float>{sv.K, rows_list(pv.active + off)},
+                              LoadRows<D, float>{w.dKt, rows_list(pv.active + off, R, r)}, w.splitk, w.colsum,
+                              w.gatt + wo, nullptr, 0, st)));
+    HG_TRY((launch_gemm_tn<D>("hgt_bwd_dw", n, LoadRows<D, float>{sv.V, rows_list(pv.active + off)},
+                              LoadRows<D, float>{w.dVt, rows_list(pv.active + off, R, r)}, w.splitk, w.colsum,
+                              w.gmsg + wo, nullptr, 0, st)));
+    off += n;
+  }
+  {
+    const int64_t n = (int64_t)R * D * D / S;
+    const unsigned g = (unsigned)(cdiv(n, 256) < 4096 ? cdiv(n, 256) : 4096);
+    HG_LAUNCH("hgt_diagblocks", k_diagblocks, dim3(g), dim3(256), 0, st, (const float*)w.gatt, (int64_t)R, D, S, dW->W_att);
+    HG_LAUNCH("hgt_diagblocks", k_diagblocks, dim3(g), dim3(256), 0, st, (const float*)w.gmsg, (int64_t)R, D, S, dW->W_msg);
+  }
+  // (5) dH = G (residual) + dK W_K^T + dQ W_Q^T + dV W_V^T per type; projection gradients
+  for (int t = 0; t < T; ++t) {
+    const int64_t lo = s->type_off_host[t], hi = s->type_off_host[t + 1];
+    const int64_t wo = (int64_t)t * D * D, bo = (int64_t)t * D;
+    const float* srcs[3] = {w.dK, w.dQ, w.dV};
+    const float* Ws[3] = {W->W_K, W->W_Q, W->W_V};
+    float* dWs[3] = {dW->W_K, dW->W_Q, dW->W_V};
+    float* dbs[3] = {dW->b_K, dW->b_Q, dW->b_V};
+    for (int k = 0; k < 3; ++k) {
+      const float* addend = (k == 0) ? (L->residual ? G : nullptr) : dHin;
+      HG_TRY((launch_gemm_rows_pp<D, true>("hgt_bwd_dx", hi - lo, Ws[k] + wo, LoadRows<D, float>{srcs[k], rows_contig(lo)},
+                                           StoreRows<D, float>{dHin, rows_contig(lo), nullptr, addend}, st)));
+      HG_TRY((launch_gemm_tn<D>("hgt_bwd_dw", hi - lo, LoadRows<D, float>{Hin, rows_contig(lo)},
+                                LoadRows<D, float>{srcs[k], rows_contig(lo)}, w.splitk, w.colsum, dWs[k] + wo,
+                                dbs[k] ? dbs[k] + bo : nullptr, 0, st)));
+    }
+  }
+  // (6) dmu
+  {
+    const int M = T * R * T;
+    HG_LAUNCH("hgt_bwd_dmu", k_dmu_partial, dim3(kMuChunks, M), dim3(256), 0, st, (const float*)w.rowpart,
+              (const int32_t*)s->type_off, R, T, w.mupart);
+    HG_LAUNCH("hgt_bwd_dmu", k_dmu_final, dim3((unsigned)cdiv(M, 256)), dim3(256), 0, st, (const float*)w.mupart, M,
+              dW->mu);
+  }
+  return HG_OK;
+}
+
 size_t saved_size(const hg_subgraph* s, int d, int S) {
   Sizer z;
   HgtSaved sv;
@@ -325,7 +737,10 @@ size_t hg_hgt_fwd_workspace_size(const hg_subgraph* s, const hg_hgt_desc* L) {
 
 size_t hg_hgt_bwd_workspace_size(const hg_subgraph* s, const hg_hgt_desc* L) {
   if (!s || !L || !hgt_shape_ok(L->d, L->heads)) return 0;
-  return 0;
+  Sizer z;
+  HgtBwdWs w;
+  w.layout(z, s, L->d, L->heads);
+  return z.used;
 }
 
 int hg_hgt_fwd(const hg_subgraph* s, const hg_hgt_desc* L, const void* H_in, const hg_hgt_weights* W, void* H_out,
@@ -344,10 +759,27 @@ int hg_hgt_fwd(const hg_subgraph* s, const hg_hgt_desc* L, const void* H_in, con
                            static_cast<uint32_t*>(mask), saved, ws, ws_bytes, st);
 }
 
-int hg_hgt_bwd(const hg_subgraph* s, const hg_hgt_desc* L, const void*, const hg_hgt_weights*, const void*,
-               const void*, const void*, void*, const hg_hgt_grads*, void*, size_t, void*) {
+int hg_hgt_bwd(const hg_subgraph* s, const hg_hgt_desc* L, const void* H_in, const hg_hgt_weights* W,
+               const void* mask, const void* saved, const void* dH_out, void* dH_in, const hg_hgt_grads* dW, void* ws,
+               size_t ws_bytes, void* stream) {
   HG_TRY(validate_hgt(s, L));
-  return fail(HG_ERR_UNSUPPORTED, "attention-layer backward is not built yet");
+  if (s->n_ntype > kMaxTypesBwd)
+    return fail(HG_ERR_UNSUPPORTED, "attention-layer backward: at most %d node types (got %d)", kMaxTypesBwd,
+                s->n_ntype);
+  if (!H_in || !mask || !saved || !dH_out || !dH_in || !W || !dW)
+    return fail(HG_ERR_ARG, "null input, mask, saved, gradient or weights pointer");
+  if (!W->W_K || !W->W_Q || !W->W_V || !W->W_att || !W->W_msg || !W->mu || !W->W_agg)
+    return fail(HG_ERR_ARG, "null weight pointer (only biases may be NULL)");
+  if (!dW->W_K || !dW->W_Q || !dW->W_V || !dW->W_att || !dW->W_msg || !dW->mu || !dW->W_agg)
+    return fail(HG_ERR_ARG, "null weight-gradient pointer (only bias gradients may be NULL)");
+  if (dH_in == dH_out || dH_in == H_in) return fail(HG_ERR_ARG, "dH_in must not alias dH_out or H_in");
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  const float* Hin = static_cast<const float*>(H_in);
+  const uint32_t* m = static_cast<const uint32_t*>(mask);
+  const float* G = static_cast<const float*>(dH_out);
+  float* dH = static_cast<float*>(dH_in);
+  if (L->d == 64) return hgt_bwd_impl<64>(s, L, Hin, W, m, saved, G, dH, dW, ws, ws_bytes, st);
+  return hgt_bwd_impl<128>(s, L, Hin, W, m, saved, G, dH, dW, ws, ws_bytes, st);
 }
 
 }  // extern "C"

@@ -86,3 +86,44 @@ def test_hgt_forward_isolated_nodes_and_null_biases():
     H, mask, _ = api.hg_hgt_fwd(sub, to_dev(X), wd, heads)
     torch.cuda.synchronize()
     assert parity_err(H.cpu().numpy(), np.maximum(Z, 0) + X) <= TOL
+
+
+@pytest.mark.parametrize("name", sorted(CFGS))
+@pytest.mark.parametrize("relu,residual", [(1, 1), (0, 1), (1, 0)])
+def test_hgt_backward(name, relu, residual):
+    cfg, d, heads = CFGS[name]
+    ref, sub, X, w = setup(cfg, d, heads)
+    G = synth.upstream_grad(3, ref.n_sub, d)
+    p = oracle_params(w)
+    _, Z, _, _ = hgt.forward(ref.n_sub, ref.src_l, ref.dst_l, ref.rel_l, ref.ntype_l, X, p, heads)
+    mask = (Z > 0) if relu else np.ones_like(Z, dtype=bool)
+    dH, g = hgt.backward(ref.n_sub, ref.src_l, ref.dst_l, ref.rel_l, ref.ntype_l, X, p, heads, G, mask=mask)
+    if not residual:
+        dH = dH - G
+    Xd, wd = to_dev(X), dev_weights(w)
+    _, _, saved = api.hg_hgt_fwd(sub, Xd, wd, heads, relu=bool(relu), residual=bool(residual))
+    dHg, grads = api.hg_hgt_bwd(sub, Xd, wd, heads, to_dev(pack_mask(mask)), saved, to_dev(G), relu=bool(relu),
+                                residual=bool(residual))
+    torch.cuda.synchronize()
+    errs = {"dH": parity_err(dHg.cpu().numpy(), dH)}
+    for n in hgt.PARAM_NAMES:
+        errs[n] = parity_err(grads[n].cpu().numpy(), getattr(g, n))
+    assert max(errs.values()) <= TOL, errs
+
+
+def test_hgt_backward_deterministic_and_null_bias_grads():
+    cfg, d, heads = CFGS["tiny_d64_h4"]
+    ref, sub, X, w = setup(cfg, d, heads)
+    Xd, wd = to_dev(X), dev_weights(w)
+    G = to_dev(synth.upstream_grad(4, ref.n_sub, d))
+    _, mask, saved = api.hg_hgt_fwd(sub, Xd, wd, heads)
+    runs = []
+    for _ in range(2):
+        grads = {n: torch.full_like(v, float("nan")) for n, v in wd.items() if not n.startswith("b_")}
+        dH, grads = api.hg_hgt_bwd(sub, Xd, wd, heads, mask, saved, G, grads=grads)
+        torch.cuda.synchronize()
+        runs.append((dH.cpu().numpy().copy(), {n: v.cpu().numpy().copy() for n, v in grads.items()}))
+    assert np.array_equal(runs[0][0], runs[1][0])
+    for n in runs[0][1]:
+        assert np.array_equal(runs[0][1][n], runs[1][1][n]), n
+        assert np.all(np.isfinite(runs[0][1][n])), n
