@@ -26,11 +26,30 @@ HBM_PEAK_GBS = 8000.0
 FP32_MFMA_PEAK_TFLOPS = 157.3
 
 
+SPARSE_KERNELS = {"mean": ("spmm_fwd", "spmm_bwd"),
+                  "hgt": ("hgt_attn_fwd", "hgt_attn_bwd_dst", "hgt_attn_bwd_src")}
+
+
 def algorithmic_cost(kind: str, info: dict):
     """(bytes, flops) per launch, counted without cache reuse.  E = subgraph
     edges, N = subgraph nodes, A = active (source, relation) rows, s = bytes
-    per feature element, d = width, R = relations."""
+    per feature element, d = width, R = relations, T = node types, S = heads."""
     E, N, A, d, s, R = info["E"], info["N"], info["A"], info["d"], info["s"], info["R"]
+    T, S = info.get("T", 2), info.get("S", 1)
+    if kind == "hgt_attn_fwd":
+        # per edge: Kt and Vt rows of the source plus its column id; per node:
+        # Q read, h~ written, S log-sum-exps, R+1 row pointers
+        return E * (2 * d * s + 4) + N * (2 * d * s + 4 * S + 4 * (R + 1)), 4.0 * E * d
+    if kind == "hgt_attn_bwd_dst":
+        # per edge: Kt and Vt rows plus the column id; per node: Q, dh~ and h~
+        # read, dQ written, S log-sum-exps read and S sums written, R+1 row
+        # pointers, R*T partial sums of the mu gradient
+        return E * (2 * d * s + 4) + N * (4 * d * s + 8 * S + 4 * (R + 1) + 4 * R * T), 6.0 * E * d
+    if kind == "hgt_attn_bwd_src":
+        # per edge: Q and dh~ rows of the destination, its id and its S
+        # log-sum-exps and S sums; per work item: Kt, Vt read, dKt, dVt
+        # written, 16-byte item
+        return E * (2 * d * s + 4 + 8 * S) + A * (4 * d * s + 16), 6.0 * E * d
     if kind == "spmm_fwd":
         # per edge: one gathered row of Y plus its 4-byte column id; per node:
         # R+1 row pointers, Y_self and H_in rows read, H_out row and d/8 mask bytes written
@@ -78,7 +97,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--config", default="large", help="tiny | medium | large | skew")
+    ap.add_argument("--config", default="large",
+                    help="tiny | medium | large | large_bf16 | skew | large_hgt | tiny_hgt")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=float, default=0.01,
                     help="fraction of the workload's node/edge counts the oracle runs on")
@@ -122,8 +142,8 @@ def main():
     value = edges / (ms * 1e-3) / 1e9
 
     info = dict(E=sub.e_sub, N=sub.n_sub, A=sum(sub.n_active()), d=wl.model.d,
-                s=2 if wl.model.dtype == "bf16" else 4, R=sub.n_rel)
-    spmm = {k: v for k, v in kern.items() if k in ("spmm_fwd", "spmm_bwd")}
+                s=2 if wl.model.dtype == "bf16" else 4, R=sub.n_rel, T=sub.n_ntype, S=wl.model.heads)
+    spmm = {k: v for k, v in kern.items() if k in SPARSE_KERNELS[wl.model.kind]}
     dom = max(spmm, key=lambda k: spmm[k][1])
     launches, total_ms = spmm[dom]
     avg_ms = total_ms / launches
@@ -135,10 +155,10 @@ def main():
                 "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE x2 + WRITE_SIZE, copy-calibrated)",
                 "avg_launch_ms": round(avg_ms, 4), "algorithmic_bytes_per_launch": int(nbytes)}
     if not args.no_ceiling:
-        groups = info["E"] / max(info["A"] if dom == "spmm_bwd" else info["N"], 1)
+        groups = info["E"] / max(info["A"] if dom in ("spmm_bwd", "hgt_attn_bwd_src") else info["N"], 1)
         roofline["ceiling"] = gather_ceiling(info["N"], info["E"], info["d"] * info["s"], groups, achieved)
     layer_ms = sum(v[1] for k, v in kern.items()
-                   if k.startswith(("spmm", "gemm_fwd", "gemm_bwd", "relu_grad", "splitk"))) / args.steps
+                   if k.startswith(("spmm", "gemm_fwd", "gemm_bwd", "relu_grad", "splitk", "hgt_"))) / args.steps
     breakdown = {k: round(v[1] / args.steps, 3) for k, v in sorted(kern.items(), key=lambda kv: -kv[1][1])}
 
     cpu = None
@@ -151,9 +171,11 @@ def main():
         "warmup": args.warmup, "ms_per_step": round(ms, 3), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "f32" if wl.model.dtype == "f32" else "bf16",
         "data": "synthetic",
-        "config": {"workload": wl.desc, "name": args.config, "n_nodes": g.n_nodes, "n_edges": g.n_edges,
-                   "n_sub": sub.n_sub, "e_sub": sub.e_sub, "m_sel": sub.m_sel, "n_rel": sub.n_rel,
-                   "d": wl.model.d, "layers": L, "parallelism": "none (1 GPU)"},
+        "config": {"workload": wl.desc, "name": args.config, "layer": wl.model.kind, "n_nodes": g.n_nodes,
+                   "n_edges": g.n_edges, "n_sub": sub.n_sub, "e_sub": sub.e_sub, "m_sel": sub.m_sel,
+                   "n_rel": sub.n_rel, "d": wl.model.d, "layers": L,
+                   **({"heads": wl.model.heads} if wl.model.kind == "hgt" else {}),
+                   "parallelism": "none (1 GPU)"},
         "roofline": roofline,
         "cpu_baseline": cpu,
         "layer_gteps": round(edges / (layer_ms * 1e-3) / 1e9, 4) if layer_ms > 0 else None,
@@ -214,7 +236,11 @@ def cpu_baseline(wl, frac):
     feats = synth.features(mc.seed, g.n_nodes, mc.d)
     if mc.dtype == "bf16":
         feats = synth.round_bf16(feats)
-    weights = [synth.layer_weights(mc.seed, li, cfg.n_rel, 2, mc.d, mc.bias_range) for li in range(mc.n_layers)]
+    if mc.kind == "hgt":
+        weights = [synth.hgt_weights(mc.seed, li, cfg.n_rel, 2, mc.d, mc.heads, mc.bias_range)
+                   for li in range(mc.n_layers)]
+    else:
+        weights = [synth.layer_weights(mc.seed, li, cfg.n_rel, 2, mc.d, mc.bias_range) for li in range(mc.n_layers)]
     href = synth.reference_embeddings(mc.seed, max(cfg.budget, 1), mc.d)
     gext = synth.upstream_grad(mc.seed, g.n_nodes, mc.d)
     t0 = time.perf_counter()
@@ -222,7 +248,7 @@ def cpu_baseline(wl, frac):
                               dict(k=g.k, n_rel=cfg.n_rel, n_ntype=2, budget=cfg.budget, key=cfg.key,
                                    theta=cfg.theta, seed=cfg.seed),
                               feats, weights, href, gext, lambda_n=mc.lambda_n, scale=mc.lambda_cca,
-                              eps=mc.eps, ddof=mc.ddof)
+                              eps=mc.eps, ddof=mc.ddof, heads=mc.heads)
     dt = time.perf_counter() - t0
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
     return {"value": round(mc.n_layers * sub.e_sub / dt / 1e9, 6), "unit": "GTEPS", "cores": threads,

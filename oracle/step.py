@@ -1,5 +1,7 @@
 """One whole step of the hot path on the CPU: build, L layers forward, the
-alignment loss on the overlap rows, L layers backward.
+alignment loss on the overlap rows, L layers backward.  Layers are the
+mean-aggregation layer (weights with w_rel / w_self / bias) or the attention
+layer (weights as a dict of the oracle.hgt parameter names, with `heads`).
 
 TEST INFRASTRUCTURE ONLY (see the package docstring).  Used by the smoke
 check and the benchmark's CPU-baseline leg.
@@ -8,17 +10,20 @@ from __future__ import annotations
 
 import numpy as np
 
-from . import align, layer, select
+from . import align, hgt, layer, select
 
 
 def run(graph_arrays: dict, build_args: dict, feats_global: np.ndarray, weights: list,
         h_ref: np.ndarray, g_ext: np.ndarray, omega=None, lambda_n=2e-4, scale=0.1,
-        eps=1e-5, ddof=0):
+        eps=1e-5, ddof=0, heads=None):
     sub = select.build(**graph_arrays, **build_args)
+    edges = (sub.n_sub, sub.src_l, sub.dst_l, sub.rel_l, sub.ntype_l)
     h = [np.asarray(feats_global, dtype=np.float64)[sub.local2global]]
     for w in weights:
-        out, _ = layer.forward(sub.n_sub, sub.src_l, sub.dst_l, sub.rel_l, sub.ntype_l,
-                               h[-1], w.w_rel, w.w_self, w.bias)
+        if isinstance(w, dict):
+            out = hgt.forward(*edges, h[-1], hgt.Params(*[w[n] for n in hgt.PARAM_NAMES]), heads)[0]
+        else:
+            out, _ = layer.forward(*edges, h[-1], w.w_rel, w.w_self, w.bias)
         h.append(out)
     losses, dX, _ = align.loss_and_grad(h[-1][sub.overlap], h_ref[: sub.overlap.shape[0]],
                                         omega, lambda_n, scale, eps, ddof)
@@ -27,7 +32,10 @@ def run(graph_arrays: dict, build_args: dict, feats_global: np.ndarray, weights:
     grads = []
     for li in reversed(range(len(weights))):
         w = weights[li]
-        g, dwr, dws, db = layer.backward(sub.n_sub, sub.src_l, sub.dst_l, sub.rel_l,
-                                         sub.ntype_l, h[li], w.w_rel, w.w_self, w.bias, g)
+        if isinstance(w, dict):
+            g, gp = hgt.backward(*edges, h[li], hgt.Params(*[w[n] for n in hgt.PARAM_NAMES]), heads, g)
+            grads.append({n: getattr(gp, n) for n in hgt.PARAM_NAMES})
+            continue
+        g, dwr, dws, db = layer.backward(*edges, h[li], w.w_rel, w.w_self, w.bias, g)
         grads.append((dwr, dws, db))
     return sub, h, losses, g, grads[::-1]

@@ -309,7 +309,8 @@ constexpr int kMaxTypesBwd = 4;
 
 struct HgtBwdWs {
   float *dZ, *dht, *dQ, *dK, *dV;  // [n_sub, d]
-  float* Dsum;                     // [n_sub, S]
+  float* ld;                       // [n_sub, 2S]: per head the log-sum-exp, then per head D_j
+  float* contrib;                  // [e_sub]: each CSR entry's term of the mu gradient (summed over heads)
   float *dKt, *dVt;                // [n_sub * R, d]
   double *pk, *pv;                 // [plan_partials, d]
   float* rowpart;                  // [n_sub * R * T]: dmu sums of each CSR row, by source type
@@ -330,7 +331,8 @@ void HgtBwdWs::layout(A& a, const hg_subgraph* s, int d, int S) {
   dQ = a.template take<float>(n * d);
   dK = a.template take<float>(n * d);
   dV = a.template take<float>(n * d);
-  Dsum = a.template take<float>(n * S);
+  ld = a.template take<float>(n * 2 * S);
+  contrib = a.template take<float>(s->e_sub);
   dKt = a.template take<float>(n * R * d);
   dVt = a.template take<float>(n * R * d);
   pk = a.template take<double>(s->plan_partials * d);
@@ -358,14 +360,17 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
-// Destination pass: one wave per node j, its CSR rows one relation at a time.
+// Destination pass: one wave per node j over all its in-edges (the relation
+// of each entry is found from the row pointers, as in the forward).  Writes
+// dQ_j, the packed per-head (log-sum-exp, D_j) record of j, and each CSR
+// entry's mu-gradient term (summed over the heads) for k_dmu_rows.
 template <int D, int S>
 __global__ void __launch_bounds__(kAttnThreads) k_hgt_attn_bwd_dst(
     int64_t n_sub, int32_t R, int32_t T, const int32_t* __restrict__ type_off, const int32_t* __restrict__ csr_ptr,
     const int32_t* __restrict__ csr_col, const float* __restrict__ Q, const float* __restrict__ Kt,
     const float* __restrict__ Vt, const float* __restrict__ ht, const float* __restrict__ dht,
     const float* __restrict__ lse, const float* __restrict__ mu, float inv_sqrt_dk, float* __restrict__ dQ,
-    float* __restrict__ Dsum, float* __restrict__ rowpart) {
+    float* __restrict__ ld, float* __restrict__ contrib) {
   constexpr int LPR = D / 4, EPW = 64 / LPR, DK = D / S, LPH = DK / 4, U = 2;
   const int l = threadIdx.x & 63;
   const int slot = l / LPR, lr = l % LPR, c0 = lr * 4, head = lr / LPH;
@@ -379,60 +384,58 @@ __global__ void __launch_bounds__(kAttnThreads) k_hgt_attn_bwd_dst(
     const f32x4 h = *reinterpret_cast<const f32x4*>(ht + j * D + c0);
     const float dsum = head_sum<LPH>(g[0] * h[0] + g[1] * h[1] + g[2] * h[2] + g[3] * h[3]);
     const float lj = lse[j * S + head];
-    if (slot == 0 && head_lead) Dsum[j * S + head] = dsum;
+    if (slot == 0 && head_lead) {
+      ld[j * 2 * S + head] = lj;
+      ld[j * 2 * S + S + head] = dsum;
+    }
     f32x4 dq = {0.f, 0.f, 0.f, 0.f};
     const int64_t rb = j * R;
-    for (int r = 0; r < R; ++r) {
-      const int32_t b0 = csr_ptr[rb + r], b1 = csr_ptr[rb + r + 1];
-      float dm[kMaxTypesBwd] = {0.f, 0.f, 0.f, 0.f};
-      for (int32_t base = b0; base < b1; base += 64) {
-        const int32_t pos = base + l;
-        int32_t rowi = 0, ti = 0;
-        float cf = 0.f;
-        if (pos < b1) {
-          const int32_t src = csr_col[pos];
-          ti = type_of(src, T, type_off);
-          rowi = src * R + r;
-          cf = mu[((int64_t)ti * R + r) * T + tj] * inv_sqrt_dk;
-        }
-        const int cnt = (b1 - base) < 64 ? (b1 - base) : 64;
-        for (int e = 0; e < cnt; e += EPW * U) {
-          f32x4 kv[U], vv[U];
-          float cc[U];
-          int tt[U];
-          bool ok[U];
-#pragma unroll
-          for (int u = 0; u < U; ++u) {
-            const int my = e + u * EPW + slot;
-            const int32_t qi = __shfl(rowi, my & 63, 64);
-            cc[u] = __shfl(cf, my & 63, 64);
-            tt[u] = __shfl(ti, my & 63, 64);
-            ok[u] = my < cnt;
-            if (ok[u]) {
-              kv[u] = *reinterpret_cast<const f32x4*>(Kt + (int64_t)qi * D + c0);
-              vv[u] = *reinterpret_cast<const f32x4*>(Vt + (int64_t)qi * D + c0);
-            } else {
-              kv[u] = vv[u] = f32x4{0.f, 0.f, 0.f, 0.f};
-            }
-          }
-#pragma unroll
-          for (int u = 0; u < U; ++u) {
-            const float dot = head_sum<LPH>(kv[u][0] * q[0] + kv[u][1] * q[1] + kv[u][2] * q[2] + kv[u][3] * q[3]);
-            const float dal = head_sum<LPH>(vv[u][0] * g[0] + vv[u][1] * g[1] + vv[u][2] * g[2] + vv[u][3] * g[3]);
-            if (ok[u]) {
-              const float a = __expf(dot * cc[u] - lj);
-              const float ds = a * (dal - dsum);
-              dq += (ds * cc[u]) * kv[u];
-              const float cm = head_lead ? ds * dot * inv_sqrt_dk : 0.f;
-#pragma unroll
-              for (int t = 0; t < kMaxTypesBwd; ++t) dm[t] += (tt[u] == t) ? cm : 0.f;
-            }
-          }
-        }
+    const int32_t p0 = csr_ptr[rb], pe = csr_ptr[rb + R];
+    for (int32_t base = p0; base < pe; base += 64) {
+      const int32_t pos = base + l;
+      int32_t rowi = 0;
+      float cf = 0.f;
+      if (pos < pe) {
+        const int32_t src = csr_col[pos];
+        int r = 0;
+        for (int t = 1; t < R; ++t) r += (csr_ptr[rb + t] <= pos) ? 1 : 0;
+        rowi = src * R + r;
+        cf = mu[((int64_t)type_of(src, T, type_off) * R + r) * T + tj] * inv_sqrt_dk;
       }
-      for (int t = 0; t < T; ++t) {
-        const float v = wave_sum(dm[t]);
-        if (l == 0) rowpart[(rb + r) * T + t] = v;
+      const int cnt = (pe - base) < 64 ? (pe - base) : 64;
+      for (int e = 0; e < cnt; e += EPW * U) {
+        f32x4 kv[U], vv[U];
+        float cc[U];
+        bool ok[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const int my = e + u * EPW + slot;
+          const int32_t qi = __shfl(rowi, my & 63, 64);
+          cc[u] = __shfl(cf, my & 63, 64);
+          ok[u] = my < cnt;
+          if (ok[u]) {
+            kv[u] = *reinterpret_cast<const f32x4*>(Kt + (int64_t)qi * D + c0);
+            vv[u] = *reinterpret_cast<const f32x4*>(Vt + (int64_t)qi * D + c0);
+          } else {
+            kv[u] = vv[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const float dot = head_sum<LPH>(kv[u][0] * q[0] + kv[u][1] * q[1] + kv[u][2] * q[2] + kv[u][3] * q[3]);
+          const float dal = head_sum<LPH>(vv[u][0] * g[0] + vv[u][1] * g[1] + vv[u][2] * g[2] + vv[u][3] * g[3]);
+          float cm = 0.f;
+          if (ok[u]) {
+            const float a = __expf(dot * cc[u] - lj);
+            const float ds = a * (dal - dsum);
+            dq += (ds * cc[u]) * kv[u];
+            cm = head_lead ? ds * dot * inv_sqrt_dk : 0.f;
+          }
+          // the mu term of this entry: sum over the heads of the slot
+#pragma unroll
+          for (int o = LPH; o < LPR; o <<= 1) cm += __shfl_xor(cm, o, 64);
+          if (ok[u] && lr == 0) contrib[base + e + u * EPW + slot] = cm;
+        }
       }
     }
 #pragma unroll
@@ -443,14 +446,31 @@ __global__ void __launch_bounds__(kAttnThreads) k_hgt_attn_bwd_dst(
   }
 }
 
+// rowpart[(j R + r) T + ti] = sum of the mu terms of CSR row (j, r) whose
+// source has type ti (one thread per row, entries in order).
+__global__ void k_dmu_rows(int64_t n_rows, int32_t T, const int32_t* __restrict__ type_off,
+                           const int32_t* __restrict__ csr_ptr, const int32_t* __restrict__ csr_col,
+                           const float* __restrict__ contrib, float* __restrict__ rowpart) {
+  for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < n_rows; q += (int64_t)gridDim.x * blockDim.x) {
+    float acc[kMaxTypesBwd] = {0.f, 0.f, 0.f, 0.f};
+    for (int32_t p = csr_ptr[q]; p < csr_ptr[q + 1]; ++p) {
+      const int ti = type_of(csr_col[p], T, type_off);
+      const float v = contrib[p];
+#pragma unroll
+      for (int t = 0; t < kMaxTypesBwd; ++t) acc[t] += (ti == t) ? v : 0.f;
+    }
+    for (int t = 0; t < T; ++t) rowpart[q * T + t] = acc[t];
+  }
+}
+
 // Source pass: one wave per work item (CSC row q = i * R + r or a chunk of
 // it); Kt and Vt of the row are read once, Q and dh~ gathered per out-edge.
 template <int D, int S>
 __global__ void __launch_bounds__(kAttnThreads) k_hgt_attn_bwd_src(
     int64_t n_items, const int4* __restrict__ items, int32_t R, int32_t T, const int32_t* __restrict__ type_off,
     const int32_t* __restrict__ csc_row, const float* __restrict__ Q, const float* __restrict__ Kt,
-    const float* __restrict__ Vt, const float* __restrict__ dht, const float* __restrict__ lse,
-    const float* __restrict__ Dsum, const float* __restrict__ mu, float inv_sqrt_dk, float* __restrict__ dKt,
+    const float* __restrict__ Vt, const float* __restrict__ dht, const float* __restrict__ ld,
+    const float* __restrict__ mu, float inv_sqrt_dk, float* __restrict__ dKt,
     float* __restrict__ dVt, double* __restrict__ pk, double* __restrict__ pv) {
   constexpr int LPR = D / 4, EPW = 64 / LPR, DK = D / S, LPH = DK / 4, U = 2;
   const int l = threadIdx.x & 63;
@@ -487,8 +507,8 @@ __global__ void __launch_bounds__(kAttnThreads) k_hgt_attn_bwd_src(
           if (ok[u]) {
             qv[u] = *reinterpret_cast<const f32x4*>(Q + j * D + c0);
             gv[u] = *reinterpret_cast<const f32x4*>(dht + j * D + c0);
-            lj[u] = lse[j * S + head];
-            dj[u] = Dsum[j * S + head];
+            lj[u] = ld[j * 2 * S + head];
+            dj[u] = ld[j * 2 * S + S + head];
           } else {
             qv[u] = gv[u] = f32x4{0.f, 0.f, 0.f, 0.f};
             lj[u] = dj[u] = 0.f;
@@ -631,12 +651,12 @@ int hgt_bwd_impl(const hg_subgraph* s, const hg_hgt_desc* L, const float* Hin, c
     HG_LAUNCH("hgt_attn_bwd_dst", (k_hgt_attn_bwd_dst<D, S_>), dim3(attn_grid(s->n_sub)), dim3(kAttnThreads), 0, st, \
               s->n_sub, R, T, (const int32_t*)s->type_off, (const int32_t*)s->csr_ptr, (const int32_t*)s->csr_col,   \
               (const float*)sv.Q, (const float*)sv.Kt, (const float*)sv.Vt, (const float*)sv.ht,                     \
-              (const float*)w.dht, (const float*)sv.lse, W->mu, inv_sqrt_dk, w.dQ, w.Dsum, w.rowpart);               \
+              (const float*)w.dht, (const float*)sv.lse, W->mu, inv_sqrt_dk, w.dQ, w.ld, w.contrib);                 \
     if (s->plan_items > 0)                                                                                            \
       HG_LAUNCH("hgt_attn_bwd_src", (k_hgt_attn_bwd_src<D, S_>), dim3(attn_grid(s->plan_items)), dim3(kAttnThreads),  \
                 0, st, (int64_t)s->plan_items, pv.items, R, T, (const int32_t*)s->type_off,                           \
                 (const int32_t*)s->csc_row, (const float*)sv.Q, (const float*)sv.Kt, (const float*)sv.Vt,             \
-                (const float*)w.dht, (const float*)sv.lse, (const float*)w.Dsum, W->mu, inv_sqrt_dk, w.dKt, w.dVt,    \
+                (const float*)w.dht, (const float*)w.ld, W->mu, inv_sqrt_dk, w.dKt, w.dVt,                            \
                 w.pk, w.pv);                                                                                          \
   } while (0)
     switch (D / S) {
@@ -697,8 +717,13 @@ int hgt_bwd_impl(const hg_subgraph* s, const hg_hgt_desc* L, const float* Hin, c
                                 dbs[k] ? dbs[k] + bo : nullptr, 0, st)));
     }
   }
-  // (6) dmu
+  // (6) dmu: per CSR row by source type, then per meta relation over each type range
   {
+    const int64_t nq = s->n_sub * (int64_t)R;
+    if (nq > 0)
+      HG_LAUNCH("hgt_bwd_dmu", k_dmu_rows, dim3((unsigned)(cdiv(nq, 256) < 65536 ? cdiv(nq, 256) : 65536)), dim3(256), 0,
+                st, nq, T, (const int32_t*)s->type_off, (const int32_t*)s->csr_ptr, (const int32_t*)s->csr_col,
+                (const float*)w.contrib, w.rowpart);
     const int M = T * R * T;
     HG_LAUNCH("hgt_bwd_dmu", k_dmu_partial, dim3(kMuChunks, M), dim3(256), 0, st, (const float*)w.rowpart,
               (const int32_t*)s->type_off, R, T, w.mupart);

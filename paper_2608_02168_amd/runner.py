@@ -40,6 +40,7 @@ class StepInputs:
     bwd_ws: Optional[torch.Tensor] = None
     align_ws: Optional[torch.Tensor] = None
     loss: Optional[torch.Tensor] = None
+    hgt_saved: List[torch.Tensor] = field(default_factory=list)
 
 
 @dataclass
@@ -68,9 +69,14 @@ def make_inputs(wl: synth.Workload, g: synth.Graph, device="cuda", feats: Option
         feats = synth.round_bf16(feats)
     l2g = sub.view("local2global").long()
     h0 = _dev(feats, device).index_select(0, l2g).to(fdt).contiguous()
-    weights_np = [synth.layer_weights(mc.seed, li, cfg.n_rel, g.n_ntype, d, mc.bias_range)
-                  for li in range(mc.n_layers)]
-    weights = [(_dev(w.w_rel, device), _dev(w.w_self, device), _dev(w.bias, device)) for w in weights_np]
+    if mc.kind == "hgt":
+        weights_np = [synth.hgt_weights(mc.seed, li, cfg.n_rel, g.n_ntype, d, mc.heads, mc.bias_range)
+                      for li in range(mc.n_layers)]
+        weights = [{n: _dev(v, device) for n, v in w.items()} for w in weights_np]
+    else:
+        weights_np = [synth.layer_weights(mc.seed, li, cfg.n_rel, g.n_ntype, d, mc.bias_range)
+                      for li in range(mc.n_layers)]
+        weights = [(_dev(w.w_rel, device), _dev(w.w_self, device), _dev(w.bias, device)) for w in weights_np]
     m = sub.m_sel
     href_np = synth.reference_embeddings(mc.seed, max(m, 1), d)
     gext_np = synth.upstream_grad(mc.seed, max(sub.n_sub, 1), d)
@@ -90,9 +96,15 @@ def make_inputs(wl: synth.Workload, g: synth.Graph, device="cuda", feats: Option
     inp.saved = [torch.empty((max(ns, 1), d // 32), dtype=torch.int32, device=device)
                  for _ in range(mc.n_layers)]
     inp.dH = [torch.empty((ns, d), **act) for _ in range(2)]
-    inp.grads = [(torch.empty_like(w[0]), torch.empty_like(w[1]), torch.empty_like(w[2])) for w in weights]
-    inp.fwd_ws = api._ws(api.hg_layer_fwd_workspace_size(sub, d, fdt), device)
-    inp.bwd_ws = api._ws(api.hg_layer_bwd_workspace_size(sub, d, fdt), device)
+    if mc.kind == "hgt":
+        inp.grads = [{n: torch.empty_like(v) for n, v in w.items()} for w in weights]
+        inp.hgt_saved = [api._ws(api.hg_hgt_saved_size(sub, d, mc.heads), device) for _ in range(mc.n_layers)]
+        inp.fwd_ws = api._ws(api.hg_hgt_fwd_workspace_size(sub, d, mc.heads), device)
+        inp.bwd_ws = api._ws(api.hg_hgt_bwd_workspace_size(sub, d, mc.heads), device)
+    else:
+        inp.grads = [(torch.empty_like(w[0]), torch.empty_like(w[1]), torch.empty_like(w[2])) for w in weights]
+        inp.fwd_ws = api._ws(api.hg_layer_fwd_workspace_size(sub, d, fdt), device)
+        inp.bwd_ws = api._ws(api.hg_layer_bwd_workspace_size(sub, d, fdt), device)
     inp.align_ws = api._ws(api.hg_align_workspace_size(m, d), device)
     inp.loss = torch.empty(3, **f32)
     return inp
@@ -106,7 +118,12 @@ def run_step(inp: StepInputs, rebuild: bool = True) -> StepResult:
                          cfg.budget, key=cfg.key, theta=cfg.theta, seed=cfg.seed, ws=inp.build_ws,
                          out=inp.sub)
     sub = inp.sub
+    hgt = mc.kind == "hgt"
     for li in range(mc.n_layers):
+        if hgt:
+            api.hg_hgt_fwd(sub, inp.H[li], inp.weights[li], mc.heads, H_out=inp.H[li + 1], mask=inp.saved[li],
+                           saved=inp.hgt_saved[li], ws=inp.fwd_ws)
+            continue
         w_rel, w_self, bias = inp.weights[li]
         api.hg_layer_fwd(sub, inp.H[li], w_rel, w_self, bias, H_out=inp.H[li + 1], saved=inp.saved[li],
                          ws=inp.fwd_ws)
@@ -118,6 +135,11 @@ def run_step(inp: StepInputs, rebuild: bool = True) -> StepResult:
                               ws=inp.align_ws)
     cur, nxt = 0, 1
     for li in reversed(range(mc.n_layers)):
+        if hgt:
+            api.hg_hgt_bwd(sub, inp.H[li], inp.weights[li], mc.heads, inp.saved[li], inp.hgt_saved[li], inp.dH[cur],
+                           dH_in=inp.dH[nxt], grads=inp.grads[li], ws=inp.bwd_ws)
+            cur, nxt = nxt, cur
+            continue
         w_rel, w_self, _ = inp.weights[li]
         gw = inp.grads[li]
         api.hg_layer_bwd(sub, inp.H[li], w_rel, w_self, inp.saved[li], inp.dH[cur], dH_in=inp.dH[nxt],

@@ -63,6 +63,8 @@ class ModelConfig:
     eps: float = 1e-5
     ddof: int = 0
     weighted_align: bool = False
+    kind: str = "mean"      # "mean" (relation-typed mean aggregation) or "hgt" (attention)
+    heads: int = 4          # attention heads (kind == "hgt")
 
 
 @dataclass(frozen=True)
@@ -89,6 +91,14 @@ WORKLOADS = {
         GraphConfig("large", 10_000_000, 200_000_000, 5, 1.3, 634.0, 9_200_000, 800_000, seed=3),
         ModelConfig(256, 3, dtype="bf16", seed=4),
         "the 10M/200M graph with bf16 features at d=256, fp32 accumulation, L=3"),
+    "large_hgt": Workload(
+        GraphConfig("large", 10_000_000, 200_000_000, 5, 1.3, 634.0, 9_200_000, 800_000, seed=3),
+        ModelConfig(64, 2, seed=3, kind="hgt", heads=4),
+        "the 10M/200M graph with attention layers (4 heads) at d=64 fp32, L=2"),
+    "tiny_hgt": Workload(
+        GraphConfig("tiny", 10_000, 100_000, 3, 1.1, 0.0, 9_500, 500, seed=0),
+        ModelConfig(64, 2, seed=0, kind="hgt", heads=4),
+        "10k nodes, 100k edges, 3 relations, attention layers (4 heads), d=64 fp32, L=2"),
     "skew": Workload(
         GraphConfig("skew", 5_000_000, 150_000_000, 8, 1.6, 6339.0, 4_250_000, 750_000,
                     theta=3, rel_split=SKEW_SPLIT, seed=5),

@@ -10,14 +10,14 @@ import pytest
 torch = pytest.importorskip("torch")
 
 from oracle import step as oracle_step
-from oracle import layer
+from oracle import hgt, layer
 from paper_2608_02168_amd import runner, synth
 from tests.helpers import parity_err, unpack_mask
 
 pytestmark = pytest.mark.gpu
 
 
-@pytest.mark.parametrize("name,factor", [("tiny", 0.3), ("tiny", 0.1), ("skew", 0.001)])
+@pytest.mark.parametrize("name,factor", [("tiny", 0.3), ("tiny", 0.1), ("skew", 0.001), ("tiny_hgt", 0.3)])
 def test_step_matches_oracle(name, factor):
     base = synth.WORKLOADS[name]
     wl = synth.Workload(synth.scaled(base.graph, factor), base.model, name)
@@ -33,12 +33,16 @@ def test_step_matches_oracle(name, factor):
         dict(k=g.k, n_rel=wl.graph.n_rel, n_ntype=2, budget=wl.graph.budget, theta=wl.graph.theta,
              seed=wl.graph.seed),
         inp.feats_np, inp.weights_np, inp.href_np[:m], inp.gext_np, omega=omega,
-        lambda_n=wl.model.lambda_n, scale=wl.model.lambda_cca, eps=wl.model.eps, ddof=wl.model.ddof)
+        lambda_n=wl.model.lambda_n, scale=wl.model.lambda_cca, eps=wl.model.eps, ddof=wl.model.ddof,
+        heads=wl.model.heads)
     masks_agree = True
     d = wl.model.d
+    edges = (ref_sub.n_sub, ref_sub.src_l, ref_sub.dst_l, ref_sub.rel_l, ref_sub.ntype_l)
     for li, w in enumerate(inp.weights_np):
-        _, Z = layer.forward(ref_sub.n_sub, ref_sub.src_l, ref_sub.dst_l, ref_sub.rel_l,
-                             ref_sub.ntype_l, h[li], w.w_rel, w.w_self, w.bias)
+        if isinstance(w, dict):
+            Z = hgt.forward(*edges, h[li], hgt.Params(*[w[n] for n in hgt.PARAM_NAMES]), wl.model.heads)[1]
+        else:
+            _, Z = layer.forward(*edges, h[li], w.w_rel, w.w_self, w.bias)
         got = unpack_mask(inp.saved[li][: sub.n_sub].cpu().numpy(), d)
         diff = got != (Z > 0)
         assert np.all(np.abs(Z[diff]) <= 1e-4 * np.sqrt(np.mean(Z * Z)))
@@ -52,5 +56,9 @@ def test_step_matches_oracle(name, factor):
         pytest.skip("a pre-activation within rounding of zero was decided differently")
     assert parity_err(res.dH0.cpu().numpy(), dH0) <= 1e-4
     for gw, rw in zip(res.grads, grads):
+        if isinstance(rw, dict):
+            for n in rw:
+                assert parity_err(gw[n].cpu().numpy(), rw[n]) <= 1e-4, n
+            continue
         for a, b in zip(gw, rw):
             assert parity_err(a.cpu().numpy(), b) <= 1e-4
