@@ -263,3 +263,70 @@ def test_medium_full_layer_and_weight_gradients():
     for a, b, nm in zip(got, exp, ("dH", "dW_rel", "dW_self", "dbias")):
         err = parity_err(a.cpu().numpy(), b)
         assert err <= TOL, (nm, err)
+
+
+def _closure(full, dsts):
+    """The sub-graph of all in-edges of `dsts`, relabelled: (nodes, src, dst, rel)
+    with nodes the sorted global-local ids involved."""
+    m = np.isin(full.dst_l, dsts)
+    s, r, t = full.src_l[m], full.rel_l[m], full.dst_l[m]
+    nodes = np.unique(np.concatenate([s, t, dsts]))
+    return nodes, np.searchsorted(nodes, s), np.searchsorted(nodes, t), r
+
+
+def test_fullsize_attention_layer_sampled_rows(full):
+    """The attention layer at the benchmark's attention width (d = 64, 4 heads)
+    on the full graph: forward on sampled destination rows, backward dH on
+    sampled sources and the heaviest hub sources, each from the oracle on the
+    closed sub-graph that determines those rows exactly."""
+    from oracle import hgt
+    sub, wl = full.sub, full.wl
+    d, heads, R = 64, 4, full.R
+    H = synth.features(wl.model.seed + 2, full.g.n_nodes, d)[full.ref["l2g"]]
+    w = synth.hgt_weights(wl.model.seed, 0, R, 2, d, heads, 0.1)
+    p = hgt.Params(*[w[n] for n in hgt.PARAM_NAMES])
+    ntype_l = full.g.ntype[full.ref["l2g"]].astype(np.int64)
+    Hd, wd = to_dev(H), {n: to_dev(v) for n, v in w.items()}
+    out, mask, saved = api.hg_hgt_fwd(sub, Hd, wd, heads)
+    rng = np.random.default_rng(1)
+    rows = np.unique(rng.choice(full.ns, 3000, replace=False))
+    nodes, s, t, r = _closure(full, rows)
+    Ho, Z, _, _ = hgt.forward(nodes.shape[0], s, t, r, ntype_l[nodes], H[nodes], p, heads)
+    at = np.searchsorted(nodes, rows)
+    got = out[torch.from_numpy(rows).cuda()].cpu().numpy()
+    assert parity_err(got, Ho[at]) <= TOL
+    band = 1e-4 * np.sqrt(np.mean(Z[at] * Z[at]))
+    diff = unpack_mask(mask.cpu().numpy()[rows], d) != (Z[at] > 0)
+    assert np.all(np.abs(Z[at][diff]) <= band)
+    del Ho, Z
+
+    G = synth.upstream_grad(wl.model.seed + 5, full.ns, d)
+    dH, _ = api.hg_hgt_bwd(sub, Hd, wd, heads, mask, saved, to_dev(G))
+    outdeg = np.bincount(full.src_l, minlength=full.ns)
+    small = np.nonzero((outdeg >= 1) & (outdeg <= 40))[0]
+    # hub sources whose CSC rows are split into several work items, with a
+    # closure the oracle handles in seconds
+    split = np.nonzero((outdeg >= 6000) & (outdeg <= 12000))[0]
+    hubs = split[np.argsort(outdeg[split])[-2:]]
+    srcs = np.unique(np.concatenate([rng.choice(small, 150, replace=False), hubs]))
+    mo = np.isin(full.src_l, srcs)
+    es, ed = full.src_l[mo], full.dst_l[mo]
+    dsts = np.unique(np.concatenate([ed, srcs]))
+    nodes, s, t, r = _closure(full, dsts)
+    Gl = np.zeros((nodes.shape[0], d))
+    inside = np.searchsorted(nodes, dsts)
+    Gl[inside] = G[dsts]
+    _, Z, _, _ = hgt.forward(nodes.shape[0], s, t, r, ntype_l[nodes], H[nodes], p, heads)
+    dHl, _ = hgt.backward(nodes.shape[0], s, t, r, ntype_l[nodes], H[nodes], p, heads, Gl, mask=Z > 0)
+    # rows whose own z, or the z of a destination of theirs, lies within rounding of zero may differ
+    zb = 1e-5 * np.sqrt(np.mean(Z[inside] ** 2))
+    near = np.zeros(full.ns, bool)
+    near[dsts] = np.any(np.abs(Z[inside]) <= zb, axis=1)
+    bad = np.zeros(full.ns, bool)
+    np.logical_or.at(bad, es, near[ed])
+    ok = ~(near[srcs] | bad[srcs])
+    assert hubs.shape[0] >= 1 and ok.sum() > 0.7 * ok.shape[0]
+    got = dH[torch.from_numpy(srcs).cuda()].cpu().numpy()
+    exp = dHl[np.searchsorted(nodes, srcs)]
+    assert parity_err(got[ok], exp[ok]) <= TOL
+    del Hd, out, mask, saved, dH
