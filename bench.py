@@ -73,10 +73,10 @@ def kernel_source_sha(path: str, kernel: str) -> str:
     return hashlib.sha256("\n".join(lines[start:end + 1]).encode()).hexdigest()[:16]
 
 
-def counted_traffic(kernel: str):
+def counted_traffic(kernel: str, config: str):
     """HBM bytes per launch of `kernel` from the committed rocprofv3 counter
-    summary, or None if the kernel's source has changed since."""
-    path = os.path.join(ROOT, "profiles", f"{kernel}_large_counters.md")
+    summary of this workload, or None if the kernel's source has changed since."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{config}_counters.md")
     if not os.path.exists(path):
         return None
     vals = {}
@@ -100,8 +100,9 @@ def main():
     ap.add_argument("--config", default="large",
                     help="tiny | medium | large | large_bf16 | skew | large_hgt | tiny_hgt")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample", type=float, default=0.01,
-                    help="fraction of the workload's node/edge counts the oracle runs on")
+    ap.add_argument("--cpu-sample", type=float, default=None,
+                    help="fraction of the workload's node/edge counts the oracle runs on "
+                         "(default 0.01, or 0.001 for attention layers, about 10-30 s of CPU work)")
     ap.add_argument("--no-ceiling", action="store_true",
                     help="skip the random-row gather ceiling measurement")
     args = ap.parse_args()
@@ -149,7 +150,7 @@ def main():
     avg_ms = total_ms / launches
     nbytes, _ = algorithmic_cost(dom, info)
     achieved = nbytes / (avg_ms * 1e-3) / 1e9
-    traffic = counted_traffic(dom) if args.config == "large" else None
+    traffic = counted_traffic(dom, args.config)
     roofline = {"kernel": dom, "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
                 "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE x2 + WRITE_SIZE, copy-calibrated)",
@@ -163,7 +164,8 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(wl, args.cpu_sample)
+        frac = args.cpu_sample if args.cpu_sample is not None else (0.001 if wl.model.kind == "hgt" else 0.01)
+        cpu = cpu_baseline(wl, frac)
 
     out = {
         "metric": "GNN layer fwd+bwd edges/sec (GTEPS) + achieved HBM GB/s fraction, 1 GPU",
