@@ -16,6 +16,8 @@
  *   hg_hgt_fwd/_bwd         the attention form of that layer: multi-head
  *                           mutual attention, per-destination softmax and
  *                           weighted aggregation (E6-E11)
+ *   hg_mlp_bce_fwd_bwd,     the prediction head, masked BCE loss and Adam update
+ *   hg_adam_step            of the joint objective (E18-E20)
  *   hg_align_loss_fwd_bwd   the CCA consistency-alignment loss on the overlap
  *                           nodes and its gradient (Section "Cross-Subgraph
  *                           Consistency Alignment", standardisation, invariance,
@@ -270,6 +272,33 @@ int hg_align_loss_fwd_bwd(int64_t M, int32_t d, int32_t dtype, int64_t n_rows,
                           const float* w, float lambda_n, float scale, float eps,
                           int32_t ddof, float* loss3, void* dH, void* dH_ref,
                           void* ws, size_t ws_bytes, void* stream);
+
+/* ---- prediction head, masked BCE and Adam ("Prediction and Optimization":
+ * the two-layer MLP E18, the BCE loss E19, the joint objective E20) ---------
+ *   a = H W1 + b1, hid = ReLU(a), o = hid W2 + b2, p = sigmoid(o)
+ *   L_BCE = -(1/N_m) sum_{labels[i] >= 0} [y_i log p_i + (1 - y_i) log(1 - p_i)]
+ * with y_i = labels[i] in {0, 1}; labels[i] = -1 marks an unlabelled row
+ * (N_m = number of labelled rows; L_BCE = 0 and no gradient when N_m = 0).
+ * H [n_rows, d], W1 [d, d_hidden], b1 [d_hidden], W2 [d_hidden, 1], b2 [1],
+ * float32, row-vector convention; labels int8 [n_rows].  Writes loss[0]
+ * (device), prob [n_rows] (p, may be NULL), OVERWRITES dH = dL_BCE/dH and
+ * the weight gradients (db1, db2 may be NULL).  The joint objective adds
+ * lambda_CCA * dL_CCA/dH with hg_align_loss_fwd_bwd into the same dH.
+ * Requires d_hidden == d in {64, 128}; H, labels, dH may be NULL when
+ * n_rows = 0.  Deterministic (fixed reduction order). */
+size_t hg_mlp_bce_workspace_size(int64_t n_rows, int32_t d, int32_t d_hidden);
+int hg_mlp_bce_fwd_bwd(int64_t n_rows, int32_t d, int32_t d_hidden, const float* H, const float* W1,
+                       const float* b1, const float* W2, const float* b2, const int8_t* labels, float* loss,
+                       float* prob, float* dH, float* dW1, float* db1, float* dW2, float* db2, void* ws,
+                       size_t ws_bytes, void* stream);
+
+/* One Adam update (the optimiser paragraph; weight decay added to the
+ * gradient, bias-corrected moments), in place on n float32 values:
+ *   g = grad + weight_decay * param;  m = beta1 m + (1 - beta1) g;  v = beta2 v + (1 - beta2) g^2
+ *   param -= lr * (m / (1 - beta1^step)) / (sqrt(v / (1 - beta2^step)) + eps)
+ * step >= 1 counts updates (m = v = 0 before the first).  Asynchronous. */
+int hg_adam_step(int64_t n, float* param, const float* grad, float* m, float* v, int64_t step, float lr,
+                 float beta1, float beta2, float eps, float weight_decay, void* stream);
 
 /* ---- diagnostics ------------------------------------------------------- */
 const char* hg_status_string(int status);

@@ -37,6 +37,7 @@ EXPORTS = [
     "hg_layer_saved_size", "hg_layer_fwd_workspace_size", "hg_layer_bwd_workspace_size",
     "hg_layer_fwd", "hg_layer_bwd", "hg_hgt_saved_size", "hg_hgt_fwd_workspace_size",
     "hg_hgt_bwd_workspace_size", "hg_hgt_fwd", "hg_hgt_bwd", "hg_align_workspace_size", "hg_align_loss_fwd_bwd",
+    "hg_mlp_bce_workspace_size", "hg_mlp_bce_fwd_bwd", "hg_adam_step",
     "hg_status_string", "hg_last_error_detail", "hg_timing_enable", "hg_timing_collect",
 ]
 
@@ -119,6 +120,9 @@ def lib() -> C.CDLL:
         "hg_align_workspace_size": (sz, [i64, i32]),
         "hg_align_loss_fwd_bwd": (C.c_int, [i64, i32, i32, i64, vp, vp, vp, vp, f32, f32, f32,
                                             i32, vp, vp, vp, vp, sz, vp]),
+        "hg_mlp_bce_workspace_size": (sz, [i64, i32, i32]),
+        "hg_mlp_bce_fwd_bwd": (C.c_int, [i64, i32, i32] + [vp] * 14 + [sz, vp]),
+        "hg_adam_step": (C.c_int, [i64, vp, vp, vp, vp, i64, f32, f32, f32, f32, f32, vp]),
         "hg_status_string": (C.c_char_p, [C.c_int]),
         "hg_last_error_detail": (C.c_char_p, []),
         "hg_timing_enable": (C.c_int, [C.c_int]),
@@ -388,6 +392,38 @@ def hg_hgt_bwd(sub: Subgraph, H_in, weights: dict, heads: int, mask, saved, dH_o
     _check(L.hg_hgt_bwd(C.byref(sub.c), C.byref(desc), _ptr(H_in), C.byref(W), _ptr(mask), _ptr(saved),
                         _ptr(dH_out), _ptr(dH_in), C.byref(G), _ptr(ws), ws.numel(), _stream(stream)), "hg_hgt_bwd")
     return dH_in, grads
+
+
+def hg_mlp_bce_workspace_size(n_rows: int, d: int) -> int:
+    return int(lib().hg_mlp_bce_workspace_size(n_rows, d, d))
+
+
+def hg_mlp_bce_fwd_bwd(H, W1, b1, W2, b2, labels, dH=None, grads: Optional[dict] = None, loss=None, prob=None,
+                       ws=None, stream=None):
+    """Prediction head + masked BCE: returns (loss [1], dH, grads) with grads
+    {W1, b1, W2, b2}; dH is overwritten with dL_BCE/dH."""
+    n, d = int(H.shape[0]), int(H.shape[1])
+    L = lib()
+    if dH is None:
+        dH = torch.empty_like(H)
+    if grads is None:
+        grads = {"W1": torch.empty_like(W1), "b1": torch.empty_like(b1), "W2": torch.empty_like(W2),
+                 "b2": torch.empty_like(b2)}
+    if loss is None:
+        loss = torch.empty(1, dtype=torch.float32, device=H.device)
+    if ws is None:
+        ws = _ws(int(L.hg_mlp_bce_workspace_size(n, d, d)), H.device)
+    _check(L.hg_mlp_bce_fwd_bwd(n, d, d, _ptr(H), _ptr(W1), _ptr(b1), _ptr(W2), _ptr(b2), _ptr(labels), _ptr(loss),
+                                _ptr(prob), _ptr(dH), _ptr(grads["W1"]), _ptr(grads.get("b1")), _ptr(grads["W2"]),
+                                _ptr(grads.get("b2")), _ptr(ws), ws.numel(), _stream(stream)), "hg_mlp_bce_fwd_bwd")
+    return loss, dH, grads
+
+
+def hg_adam_step(param, grad, m, v, step: int, lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=1e-5,
+                 stream=None):
+    """In-place Adam update of one float32 tensor."""
+    _check(lib().hg_adam_step(param.numel(), _ptr(param), _ptr(grad), _ptr(m), _ptr(v), step, lr, beta1, beta2, eps,
+                              weight_decay, _stream(stream)), "hg_adam_step")
 
 
 def hg_align_workspace_size(M: int, d: int) -> int:

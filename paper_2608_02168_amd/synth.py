@@ -248,6 +248,28 @@ def hgt_weights(seed: int, layer: int, n_rel: int, n_ntype: int, d: int, heads: 
     return out
 
 
+def labels(seed: int, ntype: np.ndarray, label_rate: float = 0.117, positive_rate: float = 0.1) -> np.ndarray:
+    """int8 labels: users (type 0) labelled with probability label_rate, each
+    labelled one positive with probability positive_rate; -1 = unlabelled
+    (the paper's dataset leaves 88.3% of users unlabelled)."""
+    rng = _rng(seed, 300)
+    n = ntype.shape[0]
+    lab = rng.random(n) < label_rate
+    pos = rng.random(n) < positive_rate
+    out = np.where(lab & (ntype == 0), pos.astype(np.int8), np.int8(-1)).astype(np.int8)
+    return out
+
+
+def head_weights(seed: int, d: int) -> dict:
+    """Prediction head: W1 [d, d], b1 [d], W2 [d, 1], b2 [1], Xavier-uniform and zero biases."""
+    rng = _rng(seed, 301)
+    a1, a2 = np.sqrt(6.0 / (2 * d)), np.sqrt(6.0 / (d + 1))
+    return {"W1": rng.uniform(-a1, a1, size=(d, d)).astype(np.float32),
+            "b1": np.zeros(d, dtype=np.float32),
+            "W2": rng.uniform(-a2, a2, size=(d, 1)).astype(np.float32),
+            "b2": np.zeros(1, dtype=np.float32)}
+
+
 def round_bf16(x: np.ndarray) -> np.ndarray:
     """float32 -> nearest-even bfloat16 value, returned as float32 (storage rounding)."""
     u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
