@@ -98,7 +98,7 @@ def main():
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--config", default="large",
-                    help="tiny | medium | large | large_bf16 | skew | large_hgt | tiny_hgt")
+                    help="tiny | medium | large | large_bf16 | skew | large_hgt | tiny_hgt | large_full | tiny_full")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=float, default=None,
                     help="fraction of the workload's node/edge counts the oracle runs on "
@@ -245,18 +245,22 @@ def cpu_baseline(wl, frac):
         weights = [synth.layer_weights(mc.seed, li, cfg.n_rel, 2, mc.d, mc.bias_range) for li in range(mc.n_layers)]
     href = synth.reference_embeddings(mc.seed, max(cfg.budget, 1), mc.d)
     gext = synth.upstream_grad(mc.seed, g.n_nodes, mc.d)
+    extra = {}
+    if mc.objective == "bce":
+        extra = dict(head=synth.head_weights(mc.seed, mc.d), labels_global=synth.labels(mc.seed, g.ntype))
     t0 = time.perf_counter()
     sub, *_ = oracle_step.run(dict(src=g.src, dst=g.dst, rel=g.rel, ntype=g.ntype, part=g.part),
                               dict(k=g.k, n_rel=cfg.n_rel, n_ntype=2, budget=cfg.budget, key=cfg.key,
                                    theta=cfg.theta, seed=cfg.seed),
                               feats, weights, href, gext, lambda_n=mc.lambda_n, scale=mc.lambda_cca,
-                              eps=mc.eps, ddof=mc.ddof, heads=mc.heads)
+                              eps=mc.eps, ddof=mc.ddof, heads=mc.heads, **extra)
     dt = time.perf_counter() - t0
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
     return {"value": round(mc.n_layers * sub.e_sub / dt / 1e9, 6), "unit": "GTEPS", "cores": threads,
             "kind": "oracle",
             "sample": f"same recipe at {frac:g} of the node/edge counts: N={g.n_nodes}, E={g.n_edges}, "
-                      f"E_sub={sub.e_sub}; one full step (build, {mc.n_layers} layers fwd+bwd, alignment) "
+                      f"E_sub={sub.e_sub}; one full step (build, {mc.n_layers} layers fwd+bwd, alignment"
+                      f"{', prediction head and BCE' if mc.objective == 'bce' else ''}) "
                       f"in {dt:.1f}s; float64; scipy sparse products single-threaded, BLAS {threads} threads"}
 
 

@@ -41,6 +41,16 @@ class StepInputs:
     align_ws: Optional[torch.Tensor] = None
     loss: Optional[torch.Tensor] = None
     hgt_saved: List[torch.Tensor] = field(default_factory=list)
+    # full objective (prediction head, masked BCE, Adam)
+    labels: Optional[torch.Tensor] = None
+    labels_np: Optional[np.ndarray] = None
+    head: Optional[dict] = None
+    head_np: Optional[dict] = None
+    head_grads: Optional[dict] = None
+    head_ws: Optional[torch.Tensor] = None
+    loss_bce: Optional[torch.Tensor] = None
+    adam: list = field(default_factory=list)   # (param, grad, m, v) for every trained tensor
+    t: int = 0
 
 
 @dataclass
@@ -107,6 +117,23 @@ def make_inputs(wl: synth.Workload, g: synth.Graph, device="cuda", feats: Option
         inp.bwd_ws = api._ws(api.hg_layer_bwd_workspace_size(sub, d, fdt), device)
     inp.align_ws = api._ws(api.hg_align_workspace_size(m, d), device)
     inp.loss = torch.empty(3, **f32)
+    if mc.objective == "bce":
+        inp.labels_np = synth.labels(mc.seed, g.ntype)
+        inp.labels = _dev(inp.labels_np, device).index_select(0, l2g).contiguous()
+        inp.head_np = synth.head_weights(mc.seed, d)
+        inp.head = {k: _dev(v, device) for k, v in inp.head_np.items()}
+        inp.head_grads = {k: torch.empty_like(v) for k, v in inp.head.items()}
+        inp.head_ws = api._ws(api.hg_mlp_bce_workspace_size(ns, d), device)
+        inp.loss_bce = torch.empty(1, **f32)
+        pairs = []
+        for li, w in enumerate(inp.weights):
+            gw = inp.grads[li]
+            if isinstance(w, dict):
+                pairs += [(w[k], gw[k]) for k in w]
+            else:
+                pairs += list(zip(w, gw))
+        pairs += [(inp.head[k], inp.head_grads[k]) for k in inp.head]
+        inp.adam = [(p, gr, torch.zeros_like(p), torch.zeros_like(p)) for p, gr in pairs]
     return inp
 
 
@@ -128,7 +155,12 @@ def run_step(inp: StepInputs, rebuild: bool = True) -> StepResult:
         api.hg_layer_fwd(sub, inp.H[li], w_rel, w_self, bias, H_out=inp.H[li + 1], saved=inp.saved[li],
                          ws=inp.fwd_ws)
     g = inp.dH[0]
-    g.copy_(inp.gext)
+    if mc.objective == "bce":
+        # dL_BCE/dH of the prediction head on the labelled rows (overwrites g)
+        api.hg_mlp_bce_fwd_bwd(inp.H[-1], inp.head["W1"], inp.head["b1"], inp.head["W2"], inp.head["b2"],
+                               inp.labels, dH=g, grads=inp.head_grads, loss=inp.loss_bce, ws=inp.head_ws)
+    else:
+        g.copy_(inp.gext)
     overlap = sub.view("overlap")
     api.hg_align_loss_fwd_bwd(inp.H[-1], overlap, inp.href, g, w=inp.omega, lambda_n=mc.lambda_n,
                               scale=mc.lambda_cca, eps=mc.eps, ddof=mc.ddof, loss3=inp.loss,
@@ -145,4 +177,8 @@ def run_step(inp: StepInputs, rebuild: bool = True) -> StepResult:
         api.hg_layer_bwd(sub, inp.H[li], w_rel, w_self, inp.saved[li], inp.dH[cur], dH_in=inp.dH[nxt],
                          dW_rel=gw[0], dW_self=gw[1], dbias=gw[2], ws=inp.bwd_ws)
         cur, nxt = nxt, cur
+    if mc.objective == "bce":
+        inp.t += 1
+        for p, gr, m1, m2 in inp.adam:
+            api.hg_adam_step(p, gr, m1, m2, inp.t, lr=mc.lr, weight_decay=mc.weight_decay)
     return StepResult(inp.loss, inp.dH[cur], inp.grads)

@@ -65,6 +65,9 @@ class ModelConfig:
     weighted_align: bool = False
     kind: str = "mean"      # "mean" (relation-typed mean aggregation) or "hgt" (attention)
     heads: int = 4          # attention heads (kind == "hgt")
+    objective: str = "synthetic"  # "synthetic" (seeded upstream gradient) or "bce" (head, BCE, Adam)
+    lr: float = 1e-3
+    weight_decay: float = 1e-5
 
 
 @dataclass(frozen=True)
@@ -91,6 +94,14 @@ WORKLOADS = {
         GraphConfig("large", 10_000_000, 200_000_000, 5, 1.3, 634.0, 9_200_000, 800_000, seed=3),
         ModelConfig(256, 3, dtype="bf16", seed=4),
         "the 10M/200M graph with bf16 features at d=256, fp32 accumulation, L=3"),
+    "large_full": Workload(
+        GraphConfig("large", 10_000_000, 200_000_000, 5, 1.3, 634.0, 9_200_000, 800_000, seed=3),
+        ModelConfig(128, 2, seed=3, objective="bce"),
+        "the 10M/200M graph, mean layers d=128 fp32, L=2, with the prediction head, masked BCE and Adam"),
+    "tiny_full": Workload(
+        GraphConfig("tiny", 10_000, 100_000, 3, 1.1, 0.0, 9_500, 500, seed=0),
+        ModelConfig(64, 2, seed=0, objective="bce"),
+        "10k nodes, 100k edges, mean layers d=64, with the prediction head, masked BCE and Adam"),
     "large_hgt": Workload(
         GraphConfig("large", 10_000_000, 200_000_000, 5, 1.3, 634.0, 9_200_000, 800_000, seed=3),
         ModelConfig(64, 2, seed=3, kind="hgt", heads=4),
