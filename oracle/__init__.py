@@ -20,10 +20,19 @@ reordering beyond what the definition states:
 * ``align``   -- the CCA consistency-alignment loss and its gradient
   (Section "Cross-Subgraph Consistency Alignment": standardisation,
   invariance, decorrelation and CCA-loss equations).
+* ``hgt``     -- the heterogeneous attention layer: per-type K/Q/V, relation
+  attention and message matrices with the learned prior, edge softmax per
+  destination, aggregation and typed update, forward and backward (the
+  attention, message, softmax, aggregation and update equations of the
+  "Heterogeneous Graph Transformer" paragraph).
+* ``objective`` -- the two-layer prediction head, the masked BCE loss and the
+  Adam update ("Prediction and Optimization").
+* ``temporal`` -- attention over the w previous states and the GRU update,
+  forward and backward ("Temporal Graph Learning").
 * ``splitmix`` -- the SplitMix64 mixer used as the seeded tie-break of the
   budgeted sampling.
 
 Every function is pinned by tests under ``tests/`` against brute force,
 closed forms, finite differences or published test vectors.
 """
-from . import splitmix, select, layer, align, step  # noqa: F401
+from . import splitmix, select, layer, align, step, hgt, objective, temporal  # noqa: F401
