@@ -18,6 +18,7 @@ in row-vector form with gate order (reset, update, new):
     gh_n = Ht Wh[2] + bh[2],  n = tanh(h Wi[2] + bi[2] + r * gh_n)
     H = (1 - z) * n + z * Ht
 
+With no earlier state (w = 0) Ht = 0: the GRU starts from a zero hidden state.
 Backward by the chain rule (written out in `backward`).  Float64 throughout.
 """
 from __future__ import annotations
@@ -38,11 +39,15 @@ def forward(h, C, p):
     C = np.asarray(C, dtype=np.float64)
     p = {k: np.asarray(v, dtype=np.float64) for k, v in p.items()}
     u = np.tanh(np.einsum("knj,ij->kni", C, p["Q"]))        # u_k = tanh(Q c_k)
-    s = np.einsum("kni,i->nk", u, p["r"])
-    s = s - s.max(axis=1, keepdims=True)
-    a = np.exp(s)
-    a /= a.sum(axis=1, keepdims=True)
-    Ht = np.einsum("nk,knd->nd", a, C)
+    if C.shape[0] == 0:
+        a = np.zeros((h.shape[0], 0))
+        Ht = np.zeros_like(h)
+    else:
+        s = np.einsum("kni,i->nk", u, p["r"])
+        s = s - s.max(axis=1, keepdims=True)
+        a = np.exp(s)
+        a /= a.sum(axis=1, keepdims=True)
+        Ht = np.einsum("nk,knd->nd", a, C)
     Wi, Wh, bi, bh = p["Wi"], p["Wh"], p["bi"], p["bh"]
     r = _sig(h @ Wi[0] + bi[0] + Ht @ Wh[0] + bh[0])
     z = _sig(h @ Wi[1] + bi[1] + Ht @ Wh[1] + bh[1])

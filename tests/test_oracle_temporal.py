@@ -23,9 +23,12 @@ def torch_reference(h, C, p, dH):
     t = {k: torch.tensor(v, dtype=torch.float64, requires_grad=True) for k, v in p.items()}
     th = torch.tensor(h, dtype=torch.float64, requires_grad=True)
     tC = torch.tensor(C, dtype=torch.float64, requires_grad=True)
-    u = torch.tanh(torch.einsum("knj,ij->kni", tC, t["Q"]))
-    a = torch.softmax(torch.einsum("kni,i->nk", u, t["r"]), dim=1)
-    Ht = torch.einsum("nk,knd->nd", a, tC)
+    if C.shape[0] == 0:
+        Ht = None                       # GRUCell's default: a zero hidden state
+    else:
+        u = torch.tanh(torch.einsum("knj,ij->kni", tC, t["Q"]))
+        a = torch.softmax(torch.einsum("kni,i->nk", u, t["r"]), dim=1)
+        Ht = torch.einsum("nk,knd->nd", a, tC)
     d = h.shape[1]
     cell = torch.nn.GRUCell(d, d).double()
     with torch.no_grad():
@@ -36,16 +39,20 @@ def torch_reference(h, C, p, dH):
         cell.bias_hh.copy_(torch.tensor(p["bh"].reshape(-1)))
     H = cell(th, Ht)
     (H * torch.tensor(dH)).sum().backward()
-    grads = {"Q": t["Q"].grad, "r": t["r"].grad,
+    z = torch.zeros_like
+    grads = {"Q": t["Q"].grad if t["Q"].grad is not None else z(t["Q"]),
+             "r": t["r"].grad if t["r"].grad is not None else z(t["r"]),
              "Wi": torch.stack([g.T for g in cell.weight_ih.grad.chunk(3)]),
              "Wh": torch.stack([g.T for g in cell.weight_hh.grad.chunk(3)]),
              "bi": cell.bias_ih.grad.view(3, d), "bh": cell.bias_hh.grad.view(3, d)}
-    return H.detach().numpy(), th.grad.numpy(), tC.grad.numpy(), {k: v.numpy() for k, v in grads.items()}
+    dC = tC.grad.numpy() if tC.grad is not None else np.zeros_like(C)
+    return H.detach().numpy(), th.grad.numpy(), dC, {k: v.detach().numpy() for k, v in grads.items()}
 
 
-def test_matches_torch_gru_cell_and_autograd():
-    rng = np.random.default_rng(0)
-    h, C, p = rand_case(rng)
+@pytest.mark.parametrize("w", [0, 1, 3])
+def test_matches_torch_gru_cell_and_autograd(w):
+    rng = np.random.default_rng(w)
+    h, C, p = rand_case(rng, w=w)
     dH = rng.normal(0, 1, h.shape)
     H, _ = temporal.forward(h, C, p)
     dh, dC, g = temporal.backward(h, C, p, dH)
