@@ -18,6 +18,8 @@
  *                           weighted aggregation (E6-E11)
  *   hg_mlp_bce_fwd_bwd,     the prediction head, masked BCE loss and Adam update
  *   hg_adam_step            of the joint objective (E18-E20)
+ *   hg_temporal_fwd,        the temporal module: attention over the w previous
+ *   hg_temporal_bwd         states and the GRU update (E12, E13)
  *   hg_align_loss_fwd_bwd   the CCA consistency-alignment loss on the overlap
  *                           nodes and its gradient (Section "Cross-Subgraph
  *                           Consistency Alignment", standardisation, invariance,
@@ -299,6 +301,55 @@ int hg_mlp_bce_fwd_bwd(int64_t n_rows, int32_t d, int32_t d_hidden, const float*
  * step >= 1 counts updates (m = v = 0 before the first).  Asynchronous. */
 int hg_adam_step(int64_t n, float* param, const float* grad, float* m, float* v, int64_t step, float lr,
                  float beta1, float beta2, float eps, float weight_decay, void* stream);
+
+/* ---- temporal module ("Temporal Graph Learning": attention over the w
+ * previous states E12, GRU update E13) ---------------------------------------
+ * Per row (node) i, with c_0 .. c_{w-1} its w previous states, oldest first,
+ * and h its spatial embedding at the current snapshot:
+ *   u_k = tanh(Q c_k)  (Q applied to the column vector; row form c_k Q^T)
+ *   s_k = r . u_k,  a = softmax_k(s),  Ht = sum_k a_k c_k                  (E12)
+ *   g_r = sigmoid(h Wi[0] + bi[0] + Ht Wh[0] + bh[0])
+ *   g_z = sigmoid(h Wi[1] + bi[1] + Ht Wh[1] + bh[1])
+ *   g_n = tanh(h Wi[2] + bi[2] + g_r * (Ht Wh[2] + bh[2]))
+ *   H   = (1 - g_z) * g_n + g_z * Ht                                        (E13)
+ * w = 0 (no earlier state) gives Ht = 0.  Weights are float32: Q [d, d],
+ * r [d], Wi, Wh [3, d, d] in the row-vector convention with the gates in the
+ * order (reset, update, new) -- Wi[k] is the transpose of the k-th d x d
+ * block of a GRU cell's stacked input weight, likewise Wh -- and bi, bh
+ * [3, d] (either may be NULL = 0).  Rows (h, every c_k, H, dH, dh, dC_k) are
+ * [n, d] in dtype (float32 or bfloat16).  C and dC are HOST arrays of w
+ * DEVICE pointers.  Requires d = 64 and 0 <= w <= 4. */
+typedef struct hg_temporal_weights {
+  const float *Q, *r, *Wi, *bi, *Wh, *bh;
+} hg_temporal_weights;
+
+/* Gradients, same shapes as hg_temporal_weights.  bi and bh may be NULL
+ * (not computed). */
+typedef struct hg_temporal_grads {
+  float *Q, *r, *Wi, *bi, *Wh, *bh;
+} hg_temporal_grads;
+
+/* Forward: writes H.  H must not alias h or a context state.  No workspace.
+ * Asynchronous. */
+int hg_temporal_fwd(int64_t n, int32_t d, int32_t w, int32_t dtype, const void* h, const void* const* C,
+                    const hg_temporal_weights* W, void* H, void* stream);
+
+/* Bytes of the backward workspace. */
+size_t hg_temporal_bwd_workspace_size(int64_t n, int32_t d, int32_t w);
+
+/* Backward of hg_temporal_fwd for dH = dL/dH (the forward is recomputed:
+ * nothing is kept between the calls).  dh = dL/dh is OVERWRITTEN.  dL/dc_k is
+ * ADDED into dC[k] (dC may be NULL, or any entry, for no gradient of that
+ * state; callers zero a buffer before its first contribution), so one state
+ * can collect the gradients of every later snapshot whose context holds it.
+ * The weight gradients are OVERWRITTEN when accumulate = 0 and added into
+ * when accumulate = 1 (weights shared over the snapshots).  dh and the dC[k]
+ * must not alias each other or any input.  Deterministic: fixed reduction
+ * orders, no floating-point atomics.  ws: ws_bytes >=
+ * hg_temporal_bwd_workspace_size(n, d, w). */
+int hg_temporal_bwd(int64_t n, int32_t d, int32_t w, int32_t dtype, const void* h, const void* const* C,
+                    const hg_temporal_weights* W, const void* dH, void* dh, void* const* dC, int32_t accumulate,
+                    const hg_temporal_grads* G, void* ws, size_t ws_bytes, void* stream);
 
 /* ---- diagnostics ------------------------------------------------------- */
 const char* hg_status_string(int status);

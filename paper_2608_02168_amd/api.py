@@ -38,6 +38,7 @@ EXPORTS = [
     "hg_layer_fwd", "hg_layer_bwd", "hg_hgt_saved_size", "hg_hgt_fwd_workspace_size",
     "hg_hgt_bwd_workspace_size", "hg_hgt_fwd", "hg_hgt_bwd", "hg_align_workspace_size", "hg_align_loss_fwd_bwd",
     "hg_mlp_bce_workspace_size", "hg_mlp_bce_fwd_bwd", "hg_adam_step",
+    "hg_temporal_fwd", "hg_temporal_bwd_workspace_size", "hg_temporal_bwd",
     "hg_status_string", "hg_last_error_detail", "hg_timing_enable", "hg_timing_collect",
 ]
 
@@ -90,6 +91,13 @@ class HgtWeights(C.Structure):
     _fields_ = [(n, C.c_void_p) for n in HGT_PARAMS]
 
 
+TEMPORAL_PARAMS = ("Q", "r", "Wi", "bi", "Wh", "bh")
+
+
+class TemporalWeights(C.Structure):
+    _fields_ = [(n, C.c_void_p) for n in TEMPORAL_PARAMS]
+
+
 _lib = None
 
 
@@ -123,6 +131,9 @@ def lib() -> C.CDLL:
         "hg_mlp_bce_workspace_size": (sz, [i64, i32, i32]),
         "hg_mlp_bce_fwd_bwd": (C.c_int, [i64, i32, i32] + [vp] * 14 + [sz, vp]),
         "hg_adam_step": (C.c_int, [i64, vp, vp, vp, vp, i64, f32, f32, f32, f32, f32, vp]),
+        "hg_temporal_fwd": (C.c_int, [i64, i32, i32, i32, vp, vp, vp, vp, vp]),
+        "hg_temporal_bwd_workspace_size": (sz, [i64, i32, i32]),
+        "hg_temporal_bwd": (C.c_int, [i64, i32, i32, i32, vp, vp, vp, vp, vp, vp, i32, vp, vp, sz, vp]),
         "hg_status_string": (C.c_char_p, [C.c_int]),
         "hg_last_error_detail": (C.c_char_p, []),
         "hg_timing_enable": (C.c_int, [C.c_int]),
@@ -424,6 +435,58 @@ def hg_adam_step(param, grad, m, v, step: int, lr=1e-3, beta1=0.9, beta2=0.999, 
     """In-place Adam update of one float32 tensor."""
     _check(lib().hg_adam_step(param.numel(), _ptr(param), _ptr(grad), _ptr(m), _ptr(v), step, lr, beta1, beta2, eps,
                               weight_decay, _stream(stream)), "hg_adam_step")
+
+
+def _host_ptrs(tensors):
+    """A host array of device pointers (None entries stay NULL)."""
+    arr = (C.c_void_p * max(1, len(tensors)))(*[None if t is None else t.data_ptr() for t in tensors])
+    return arr
+
+
+def _dtype_code(t) -> int:
+    return HG_DTYPE_BF16 if t.dtype == torch.bfloat16 else HG_DTYPE_F32
+
+
+def hg_temporal_fwd(h, states, weights: dict, H=None, stream=None):
+    """Temporal module forward: h [n, d] and the w context states (oldest
+    first, each [n, d], same dtype); returns H."""
+    n, d = int(h.shape[0]), int(h.shape[1])
+    if H is None:
+        H = torch.empty_like(h)
+    ctx = _host_ptrs(states)
+    W = TemporalWeights(*[_ptr(weights.get(k)) for k in TEMPORAL_PARAMS])
+    _check(lib().hg_temporal_fwd(n, d, len(states), _dtype_code(h), _ptr(h), C.cast(ctx, C.c_void_p), C.byref(W),
+                                 _ptr(H), _stream(stream)), "hg_temporal_fwd")
+    return H
+
+
+def hg_temporal_bwd_workspace_size(n: int, d: int, w: int) -> int:
+    return int(lib().hg_temporal_bwd_workspace_size(n, d, w))
+
+
+def hg_temporal_bwd(h, states, weights: dict, dH, dh=None, dstates=None, grads: Optional[dict] = None,
+                    accumulate: bool = False, ws=None, stream=None):
+    """Temporal module backward: returns (dh, grads).  dL/dc_k is ADDED into
+    dstates[k] (a list of tensors or None entries; None = no state
+    gradients); grads are overwritten, or added into when accumulate."""
+    n, d = int(h.shape[0]), int(h.shape[1])
+    w = len(states)
+    L = lib()
+    if dh is None:
+        dh = torch.empty_like(h)
+    if grads is None:
+        grads = {k: torch.empty_like(v) for k, v in weights.items() if v is not None}
+    if ws is None:
+        ws = _ws(int(L.hg_temporal_bwd_workspace_size(n, d, w)), h.device)
+    ctx = _host_ptrs(states)
+    darr = None if dstates is None else _host_ptrs(dstates)  # kept alive through the call
+    dctx = None if darr is None else C.cast(darr, C.c_void_p)
+    W = TemporalWeights(*[_ptr(weights.get(k)) for k in TEMPORAL_PARAMS])
+    G = TemporalWeights(*[_ptr(grads.get(k)) for k in TEMPORAL_PARAMS])
+    _check(L.hg_temporal_bwd(n, d, w, _dtype_code(h), _ptr(h), C.cast(ctx, C.c_void_p), C.byref(W), _ptr(dH),
+                             _ptr(dh), dctx, int(accumulate), C.byref(G), _ptr(ws), ws.numel(), _stream(stream)),
+           "hg_temporal_bwd")
+    return dh, grads
 
 
 def hg_align_workspace_size(M: int, d: int) -> int:

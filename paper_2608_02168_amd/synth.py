@@ -218,6 +218,17 @@ def upstream_grad(seed: int, n_rows: int, d: int) -> np.ndarray:
     return _normal_f32(seed, 13, (n_rows, d))
 
 
+def context_states(seed: int, w: int, n_rows: int, d: int) -> list:
+    """w earlier states of every node, oldest first, N(0, 0.5^2) float32
+    [n_rows, d] each (a GRU's states lie mostly inside (-1, 1))."""
+    out = []
+    for k in range(w):
+        x = _normal_f32(seed, 20 + k, (n_rows, d))
+        x *= np.float32(0.5)
+        out.append(x)
+    return out
+
+
 @dataclass
 class LayerWeights:
     w_rel: np.ndarray   # float32 [R, d, d]   (row-vector convention: y = x @ W)
@@ -279,6 +290,23 @@ def head_weights(seed: int, d: int) -> dict:
             "b1": np.zeros(d, dtype=np.float32),
             "W2": rng.uniform(-a2, a2, size=(d, 1)).astype(np.float32),
             "b2": np.zeros(1, dtype=np.float32)}
+
+
+def temporal_weights(seed: int, d: int, bias_range: float = 0.1) -> dict:
+    """Temporal-module weights, float32: Q, Wi, Wh U(+-1/sqrt(d)) (a GRU
+    cell's default range), r U(+-1), biases U(+-bias_range) (zeros if 0)."""
+    rng = _rng(seed, 400)
+    a = 1.0 / np.sqrt(d)
+    out = {"Q": rng.uniform(-a, a, size=(d, d)).astype(np.float32),
+           "r": rng.uniform(-1.0, 1.0, size=d).astype(np.float32),
+           "Wi": rng.uniform(-a, a, size=(3, d, d)).astype(np.float32),
+           "Wh": rng.uniform(-a, a, size=(3, d, d)).astype(np.float32)}
+    for name in ("bi", "bh"):
+        if bias_range > 0:
+            out[name] = rng.uniform(-bias_range, bias_range, size=(3, d)).astype(np.float32)
+        else:
+            out[name] = np.zeros((3, d), dtype=np.float32)
+    return out
 
 
 def round_bf16(x: np.ndarray) -> np.ndarray:

@@ -172,6 +172,41 @@ def test_align_validation(L, args, code):
     assert L.hg_align_workspace_size(5, 64) > 0
 
 
+def test_temporal_validation(L):
+    fake, out = C.c_void_p(0x1000), C.c_void_p(0x2000)
+    ctx = (C.c_void_p * 4)(0x3000, 0x4000, 0x5000, 0x6000)
+    cp = C.cast(ctx, C.c_void_p)
+    W = api.TemporalWeights(fake, fake, fake, None, fake, None)
+
+    def fwd(n=10, d=64, w=2, dtype=0, h=fake, ctxp=cp, Wp=W, H=out):
+        return L.hg_temporal_fwd(n, d, w, dtype, h, ctxp, C.byref(Wp), H, None)
+
+    assert fwd(d=128) == api.HG_ERR_UNSUPPORTED
+    assert fwd(w=5) == api.HG_ERR_UNSUPPORTED
+    assert fwd(dtype=7) == api.HG_ERR_UNSUPPORTED
+    assert fwd(n=-1) == api.HG_ERR_ARG
+    assert fwd(w=-1) == api.HG_ERR_ARG
+    assert fwd(H=C.c_void_p(0x4000)) == api.HG_ERR_ARG          # aliases context state 1
+    assert fwd(H=fake) == api.HG_ERR_ARG                         # aliases h
+    assert fwd(ctxp=None) == api.HG_ERR_ARG
+    assert fwd(Wp=api.TemporalWeights(None, fake, fake, None, fake, None)) == api.HG_ERR_ARG
+    assert fwd(n=0) == api.HG_OK                                 # nothing to do, no device work
+    G = api.TemporalWeights(fake, fake, fake, None, fake, None)
+    dctx = (C.c_void_p * 4)(0x7000, 0x2000, 0, 0)
+
+    def bwd(accumulate=0, Gp=G, dh=C.c_void_p(0x8000), dcp=None, dH=C.c_void_p(0x9000)):
+        return L.hg_temporal_bwd(10, 64, 2, 0, fake, cp, C.byref(W), dH, dh, dcp, accumulate, C.byref(Gp),
+                                 fake, 1 << 30, None)
+
+    assert bwd(accumulate=2) == api.HG_ERR_ARG
+    assert bwd(Gp=api.TemporalWeights(fake, None, fake, None, fake, None)) == api.HG_ERR_ARG
+    assert bwd(dh=C.c_void_p(0x9000)) == api.HG_ERR_ARG          # dh aliases dH
+    assert bwd(dcp=C.cast(dctx, C.c_void_p), dh=C.c_void_p(0x2000)) == api.HG_ERR_ARG
+    assert L.hg_temporal_bwd_workspace_size(10, 128, 1) == 0
+    assert L.hg_temporal_bwd_workspace_size(10, 64, 5) == 0
+    assert L.hg_temporal_bwd_workspace_size(1000, 64, 3) > L.hg_temporal_bwd_workspace_size(1000, 64, 1) > 0
+
+
 def test_product_path_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(api, "_lib", None)
     monkeypatch.setattr(api, "LIB_PATH", str(tmp_path / "missing.so"))
