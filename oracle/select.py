@@ -16,7 +16,10 @@ construction loop of Algorithm 1:
    subgraph G[V~_k], relabelled in (node type, global id) order;
 5. per-relation CSR (destination-major) and CSC (source-major) of the induced
    subgraph, entries of a row in ascending original edge index, and the CSC
-   scale 1/deg_r(destination) as a float32 quotient.
+   scale 1/deg_r(destination) as a float32 quotient;
+6. optionally one snapshot of it: only the induced edges whose timestamp is at
+   most the cut (the node set, fixed by steps 1-4 on every edge, is shared by
+   all snapshots).
 
 Readings where the paper is silent are the ones listed in the design notes:
 either edge direction for adjacency, out-neighbour h-index with degrees over
@@ -128,7 +131,12 @@ class Subgraph:
 
 def build(src, dst, rel, ntype, part, k: int, n_rel: int, n_ntype: int,
           budget: int, key: int = KEY_OUTDEG, theta: int = THETA_NONE,
-          seed: int = 0) -> Subgraph:
+          seed: int = 0, edge_ts=None, t_cut=None) -> Subgraph:
+    """The overlapping subgraph of partition k.  With edge_ts, one snapshot
+    of it: the node set (and everything that decides it) uses every edge, and
+    only the induced edges with edge_ts <= t_cut are kept (snapshots are
+    taken of the augmented subgraph by filtering its edges on their
+    timestamps, end of "Risk-Aware Subgraph Construction")."""
     src = np.asarray(src, dtype=np.int64)
     dst = np.asarray(dst, dtype=np.int64)
     rel = np.asarray(rel, dtype=np.int64)
@@ -153,6 +161,8 @@ def build(src, dst, rel, ntype, part, k: int, n_rel: int, n_ntype: int,
     type_off = np.concatenate([[0], np.cumsum(np.bincount(ntype_l, minlength=n_ntype))])
 
     keep = member[src] & member[dst]
+    if edge_ts is not None:
+        keep &= np.asarray(edge_ts, dtype=np.int64) <= int(t_cut)
     eid = np.nonzero(keep)[0]
     src_l = global2local[src[eid]]
     dst_l = global2local[dst[eid]]

@@ -62,7 +62,7 @@ def _brute_hindex(n, src, dst):
     return np.array(h)
 
 
-def _brute_build(src, dst, rel, ntype, part, k, R, T, budget, key, theta, seed):
+def _brute_build(src, dst, rel, ntype, part, k, R, T, budget, key, theta, seed, ts=None, cut=None):
     n, e = len(ntype), len(src)
     base = {v for v in range(n) if part[v] == k}
     cand = {v for v in range(n) if v not in base and any(
@@ -78,7 +78,7 @@ def _brute_build(src, dst, rel, ntype, part, k, R, T, budget, key, theta, seed):
     local = sorted(nodes, key=lambda v: (ntype[v], v))
     g2l = {v: i for i, v in enumerate(local)}
     edges = [(i, g2l[src[i]], g2l[dst[i]], rel[i]) for i in range(e)
-             if src[i] in nodes and dst[i] in nodes]
+             if src[i] in nodes and dst[i] in nodes and (ts is None or ts[i] <= cut)]
     ns = len(local)
     csr_rows = [[] for _ in range(ns * R)]
     csc_rows = [[] for _ in range(ns * R)]
@@ -129,6 +129,55 @@ def test_build_matches_brute_force(seed, key):
             d = sub.csc_row[p]
             deg = len(bf["csr_rows"][d * R + r])
             assert sub.csc_scale[p] == np.float32(1.0) / np.float32(deg)
+
+
+@pytest.mark.parametrize("seed", range(4))
+@pytest.mark.parametrize("cut", [-1, 3, 6, 9])
+def test_snapshot_matches_brute_force(seed, cut):
+    rng = np.random.default_rng(100 + seed)
+    n, e, R = 50 + seed * 5, 220 + seed * 20, 1 + seed % 3
+    src, dst, rel, ntype, part = _random_graph(rng, n, e, R)
+    ts = rng.integers(0, 10, e)
+    key = seed % 2
+    sub = select.build(src, dst, rel, ntype, part, 1, R, 2, 6, key, select.THETA_NONE, seed=seed,
+                       edge_ts=ts, t_cut=cut)
+    bf = _brute_build(list(src), list(dst), list(rel), list(ntype), list(part), 1, R, 2, 6, key,
+                      select.THETA_NONE, seed, ts=list(ts), cut=cut)
+    assert list(sub.local2global) == bf["local"]
+    assert list(sub.overlap) == bf["overlap"]
+    assert list(sub.eid) == [x[0] for x in bf["edges"]]
+    for row in range(sub.n_sub * R):
+        got = list(zip(sub.csr_col[sub.csr_ptr[row]:sub.csr_ptr[row + 1]],
+                       sub.csr_eid[sub.csr_ptr[row]:sub.csr_ptr[row + 1]]))
+        assert got == bf["csr_rows"][row]
+        got = list(sub.csc_row[sub.csc_ptr[row]:sub.csc_ptr[row + 1]])
+        assert got == [d for d, _ in bf["csc_rows"][row]]
+        r = row % R
+        for p in range(sub.csc_ptr[row], sub.csc_ptr[row + 1]):
+            deg = len(bf["csr_rows"][sub.csc_row[p] * R + r])
+            assert sub.csc_scale[p] == np.float32(1.0) / np.float32(deg)
+
+
+def test_snapshots_share_nodes_and_nest():
+    g = synth.make_graph(synth.WORKLOADS["tiny"].graph)
+    ts = synth.edge_times(0, g.n_edges)
+    cfg = synth.WORKLOADS["tiny"].graph
+    args = (g.src, g.dst, g.rel, g.ntype, g.part, g.k, cfg.n_rel, 2, cfg.budget, cfg.key, cfg.theta, 7)
+    full = select.build(*args)
+    cuts = synth.snapshot_cuts(4)
+    snaps = [select.build(*args, edge_ts=ts, t_cut=c) for c in cuts]
+    for a, b in zip(snaps, snaps[1:]):
+        assert a.e_sub < b.e_sub
+        assert set(a.eid) <= set(b.eid)
+    last = snaps[-1]
+    assert int(ts.max()) <= cuts[-1]
+    for name in ("local2global", "overlap", "overlap_rel", "csr_ptr", "csr_col", "csr_eid", "csc_ptr",
+                 "csc_row", "csc_scale"):
+        assert np.array_equal(getattr(last, name), getattr(full, name)), name
+    for s in snaps:
+        assert np.array_equal(s.local2global, full.local2global)
+        assert np.array_equal(s.overlap, full.overlap)
+        assert np.array_equal(s.eid, full.eid[ts[full.eid] <= cuts[snaps.index(s)]])
 
 
 def test_hindex_brute_force_and_bounds():
