@@ -334,3 +334,19 @@ def align_weights(overlap_rel: np.ndarray, graph_rel: np.ndarray, n_rel: int) ->
     if w.size:
         w = w / w.mean()
     return w.astype(np.float32)
+
+
+# Snapshot calendar: T monthly snapshots of 30 days (the paper's temporal
+# window of w = 3 covers the past three months).
+DAYS_PER_SNAPSHOT = 30
+
+
+def edge_times(seed: int, n_edges: int, n_snapshots: int = 4, days: int = DAYS_PER_SNAPSHOT) -> np.ndarray:
+    """Day index of every edge, uniform over [0, n_snapshots * days), int32."""
+    rng = _rng(seed, 500)
+    return rng.integers(0, n_snapshots * days, size=n_edges, dtype=np.int32)
+
+
+def snapshot_cuts(n_snapshots: int = 4, days: int = DAYS_PER_SNAPSHOT) -> list:
+    """Last day of each snapshot: snapshot t holds the edges with day <= cut[t]."""
+    return [(t + 1) * days - 1 for t in range(n_snapshots)]
