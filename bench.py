@@ -5,6 +5,12 @@ forward, the CCA alignment loss + gradient on the overlap rows, L layers
 backward -- every step of it in libhg.so's HIP kernels, inputs resident in
 HBM before the timed region.
 
+With a multi-snapshot workload (large_dyn, tiny_dyn) a step covers every
+snapshot: T snapshot builds, per snapshot L attention layers and the
+temporal module, the head with masked BCE and the alignment on the last
+state, the backward through every snapshot and one Adam update; the edge
+count is then the sum of the snapshots' edges.
+
 Prints one JSON line: value = L * E_sub / t_step in GTEPS (edges x layers
 per second, forward + backward of every layer, build and alignment included),
 plus the roofline of the dominant kernel (algorithmic bytes per launch /
@@ -98,11 +104,13 @@ def main():
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--config", default="large",
-                    help="tiny | medium | large | large_bf16 | skew | large_hgt | tiny_hgt | large_full | tiny_full")
+                    help="tiny | medium | large | large_bf16 | skew | large_hgt | tiny_hgt | large_full | tiny_full | "
+                         "large_dyn | tiny_dyn")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=float, default=None,
                     help="fraction of the workload's node/edge counts the oracle runs on "
-                         "(default 0.01, or 0.001 for attention layers, about 10-30 s of CPU work)")
+                         "(default 0.01, 0.001 for attention layers, 0.0005 for snapshot sequences: "
+                         "about 10-30 s of CPU work)")
     ap.add_argument("--no-ceiling", action="store_true",
                     help="skip the random-row gather ceiling measurement")
     args = ap.parse_args()
@@ -121,34 +129,51 @@ def main():
     g = synth.make_graph(wl.graph)
     print(f"[bench] graph {wl.graph.name}: N={g.n_nodes} E={g.n_edges} generated in {time.time() - t0:.1f}s",
           file=sys.stderr, flush=True)
-    inp = runner.make_inputs(wl, g, device="cuda")
-    sub = inp.sub
-    print(f"[bench] subgraph N_s={sub.n_sub} E_s={sub.e_sub} M_sel={sub.m_sel}", file=sys.stderr, flush=True)
+    seq = wl.model.snapshots > 1
+    if seq:
+        inp = runner.make_seq_inputs(wl, g, device="cuda")
+        subs = inp.subs
+        step = lambda: runner.run_seq_step(inp)
+    else:
+        inp = runner.make_inputs(wl, g, device="cuda")
+        subs = [inp.sub]
+        step = lambda: runner.run_step(inp)
+    sub = subs[-1]
+    print(f"[bench] subgraph N_s={sub.n_sub} E_s={[s.e_sub for s in subs]} M_sel={sub.m_sel}", file=sys.stderr,
+          flush=True)
     L = wl.model.n_layers
     for _ in range(args.warmup):
-        runner.run_step(inp)
+        step()
     torch.cuda.synchronize()
     api.hg_timing_collect()
     api.hg_timing_enable(True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        runner.run_step(inp)
+        step()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     api.hg_timing_enable(False)
     kern = api.hg_timing_collect()
     ms = (t1 - t0) * 1e3 / args.steps
-    edges = L * sub.e_sub
+    e_pass = sum(s.e_sub for s in subs)
+    edges = L * e_pass
     value = edges / (ms * 1e-3) / 1e9
 
-    info = dict(E=sub.e_sub, N=sub.n_sub, A=sum(sub.n_active()), d=wl.model.d,
-                s=2 if wl.model.dtype == "bf16" else 4, R=sub.n_rel, T=sub.n_ntype, S=wl.model.heads)
+    infos = [dict(E=s.e_sub, N=s.n_sub, A=sum(s.n_active()), d=wl.model.d, s=2 if wl.model.dtype == "bf16" else 4,
+                  R=s.n_rel, T=s.n_ntype, S=wl.model.heads) for s in subs]
+    info = infos[-1]
     spmm = {k: v for k, v in kern.items() if k in SPARSE_KERNELS[wl.model.kind]}
     dom = max(spmm, key=lambda k: spmm[k][1])
     launches, total_ms = spmm[dom]
     avg_ms = total_ms / launches
-    nbytes, _ = algorithmic_cost(dom, info)
+    # launches of the dominant kernel per step and layer, per snapshot: the
+    # forward runs twice for every snapshot but the last (its activations are
+    # computed again before its backward), each backward pass once
+    per_snap = [2 if (seq and dom.endswith("fwd") and i < len(subs) - 1) else 1 for i in range(len(subs))]
+    step_bytes = L * sum(n * algorithmic_cost(dom, inf)[0] for n, inf in zip(per_snap, infos))
+    assert launches == args.steps * L * sum(per_snap), (dom, launches)
+    nbytes = step_bytes / (L * sum(per_snap))
     achieved = nbytes / (avg_ms * 1e-3) / 1e9
     traffic = counted_traffic(dom, args.config)
     roofline = {"kernel": dom, "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
@@ -164,8 +189,9 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        frac = args.cpu_sample if args.cpu_sample is not None else (0.001 if wl.model.kind == "hgt" else 0.01)
-        cpu = cpu_baseline(wl, frac)
+        frac = args.cpu_sample if args.cpu_sample is not None else (
+            0.0005 if seq else 0.001 if wl.model.kind == "hgt" else 0.01)
+        cpu = cpu_baseline_sequence(wl, frac) if seq else cpu_baseline(wl, frac)
 
     out = {
         "metric": "GNN layer fwd+bwd edges/sec (GTEPS) + achieved HBM GB/s fraction, 1 GPU",
@@ -177,6 +203,8 @@ def main():
                    "n_edges": g.n_edges, "n_sub": sub.n_sub, "e_sub": sub.e_sub, "m_sel": sub.m_sel,
                    "n_rel": sub.n_rel, "d": wl.model.d, "layers": L,
                    **({"heads": wl.model.heads} if wl.model.kind == "hgt" else {}),
+                   **({"snapshots": len(subs), "window": wl.model.window, "e_sub_per_snapshot":
+                       [s.e_sub for s in subs]} if seq else {}),
                    "parallelism": "none (1 GPU)"},
         "roofline": roofline,
         "cpu_baseline": cpu,
@@ -221,6 +249,42 @@ def gather_ceiling(n_rows, n_idx, row_bytes, group, achieved):
                        f"groups of {g}, one row written per group",
             "gather_only": res["gather_only"], "with_writes": res["with_writes"], "unit": "GB/s",
             "frac": round(achieved / res["with_writes"], 4)}
+
+
+def cpu_baseline_sequence(wl, frac):
+    """The oracle's sequence step (oracle/step.py run_sequence, unchanged) on
+    the same recipe at a fraction of the node and edge counts."""
+    from threadpoolctl import threadpool_info
+
+    from oracle import step as oracle_step
+    from paper_2608_02168_amd import synth
+
+    cfg = synth.scaled(wl.graph, frac)
+    g = synth.make_graph(cfg)
+    mc = wl.model
+    ts = synth.edge_times(cfg.seed, g.n_edges, mc.snapshots)
+    cuts = synth.snapshot_cuts(mc.snapshots)
+    feats = synth.features(mc.seed, g.n_nodes, mc.d)
+    weights = [synth.hgt_weights(mc.seed, li, cfg.n_rel, 2, mc.d, mc.heads, mc.bias_range)
+               for li in range(mc.n_layers)]
+    t0 = time.perf_counter()
+    out = oracle_step.run_sequence(dict(src=g.src, dst=g.dst, rel=g.rel, ntype=g.ntype, part=g.part),
+                                   dict(k=g.k, n_rel=cfg.n_rel, n_ntype=2, budget=cfg.budget, key=cfg.key,
+                                        theta=cfg.theta, seed=cfg.seed),
+                                   ts, cuts, feats, weights, mc.heads, synth.temporal_weights(mc.seed, mc.d),
+                                   mc.window, synth.reference_embeddings(mc.seed, max(cfg.budget, 1), mc.d),
+                                   synth.head_weights(mc.seed, mc.d), synth.labels(mc.seed, g.ntype),
+                                   lambda_n=mc.lambda_n, scale=mc.lambda_cca, eps=mc.eps, ddof=mc.ddof)
+    dt = time.perf_counter() - t0
+    e_pass = sum(s.e_sub for s in out["subs"])
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    return {"value": round(mc.n_layers * e_pass / dt / 1e9, 6), "unit": "GTEPS", "cores": threads,
+            "kind": "oracle",
+            "sample": f"same recipe at {frac:g} of the node/edge counts: N={g.n_nodes}, E={g.n_edges}, "
+                      f"E_sub per snapshot {[s.e_sub for s in out['subs']]}; one full sequence step ("
+                      f"{mc.snapshots} snapshot builds, {mc.n_layers} attention layers and the temporal module "
+                      f"per snapshot, head, BCE and alignment, backward through every snapshot) in {dt:.1f}s; "
+                      f"float64; BLAS {threads} threads"}
 
 
 def cpu_baseline(wl, frac):

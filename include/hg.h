@@ -89,6 +89,15 @@ typedef struct hg_graph_desc {
   const int32_t* part;    /* [n_nodes] partition id of every node */
   int32_t k;              /* this worker's partition */
   const float* edge_w;    /* must be NULL: weighted edges are not implemented */
+  /* Snapshots (end of "Risk-Aware Subgraph Construction": the snapshot
+   * sequence is taken from the augmented subgraph by filtering on edge
+   * timestamps).  With edge_ts != NULL the node set, the keys, the candidates
+   * and the selection still use EVERY edge, and the induced subgraph keeps
+   * only the edges with edge_ts[e] <= t_cut, so the snapshots of one
+   * subgraph share local ids, overlap and type ranges.  NULL = no filter. */
+  const int32_t* edge_ts; /* [n_edges] or NULL */
+  int32_t t_cut;
+  int32_t reserved;
 } hg_graph_desc;
 
 /* Budgeted long-tail overlap selection (h-index filter and TopM steps of
@@ -250,11 +259,13 @@ int hg_hgt_fwd(const hg_subgraph* s, const hg_hgt_desc* L, const void* H_in, con
 
 /* Backward of hg_hgt_fwd for dH_out = dL/dH_out, from the mask and `saved`
  * of the forward call with the same inputs (dZ = dH_out * mask).  dH_in
- * [n_sub, d] and every gradient are OVERWRITTEN.  Deterministic: no
- * floating-point atomics. */
+ * [n_sub, d] is OVERWRITTEN.  The weight gradients are OVERWRITTEN when
+ * accumulate = 0 and added into when accumulate = 1 (a layer shared by the
+ * snapshots of a sequence sums its per-snapshot gradients).  Deterministic:
+ * no floating-point atomics. */
 int hg_hgt_bwd(const hg_subgraph* s, const hg_hgt_desc* L, const void* H_in, const hg_hgt_weights* W,
                const void* mask, const void* saved, const void* dH_out, void* dH_in, const hg_hgt_grads* dW,
-               void* ws, size_t ws_bytes, void* stream);
+               int32_t accumulate, void* ws, size_t ws_bytes, void* stream);
 
 /* CCA alignment on the overlap batch B (|B| = M):
  *   X = H[overlap] (local view), Y = H_ref (the other subgraph's view, row b

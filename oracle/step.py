@@ -56,7 +56,7 @@ def run(graph_arrays: dict, build_args: dict, feats_global: np.ndarray, weights:
 
 def run_sequence(graph_arrays: dict, build_args: dict, edge_ts, cuts, feats_global: np.ndarray, weights: list,
                  heads: int, tparams: dict, window: int, h_ref: np.ndarray, head: dict, labels_global,
-                 omega=None, lambda_n=2e-4, scale=0.1, eps=1e-5, ddof=0):
+                 omega=None, lambda_n=2e-4, scale=0.1, eps=1e-5, ddof=0, masks=None):
     """T snapshots of one overlapping subgraph (snapshot t keeps the edges
     with timestamp <= cuts[t]; all share the node set).  Per snapshot the
     attention layers map the features to the spatial embedding h^t and the
@@ -65,7 +65,10 @@ def run_sequence(graph_arrays: dict, build_args: dict, edge_ts, cuts, feats_glob
     alignment act on the last S.  The backward runs through every snapshot
     (the gradient of S^j collects the contributions of every later snapshot
     whose context holds it); weights shared over the snapshots get the sum of
-    their per-snapshot gradients.  Returns a dict."""
+    their per-snapshot gradients.  `masks[t][l]` (optional) gives the ReLU
+    decisions of layer l at snapshot t for the backward (a caller whose
+    pre-activations were decided in another precision passes its own);
+    otherwise they are Z > 0.  Returns a dict."""
     subs = [select.build(**graph_arrays, **build_args, edge_ts=edge_ts, t_cut=c) for c in cuts]
     T = len(subs)
     sub0 = subs[0]
@@ -101,7 +104,8 @@ def run_sequence(graph_arrays: dict, build_args: dict, edge_ts, cuts, feats_glob
             tgrads[k] = tgrads[k] + gt[k]
         gg = dh
         for li in reversed(range(len(weights))):
-            gg, gp = hgt.backward(*edges[t], hs[t][li], params[li], heads, gg)
+            mk = None if masks is None else masks[t][li]
+            gg, gp = hgt.backward(*edges[t], hs[t][li], params[li], heads, gg, mask=mk)
             for n in hgt.PARAM_NAMES:
                 lgrads[li][n] = lgrads[li][n] + getattr(gp, n)
         dx += gg

@@ -53,7 +53,8 @@ class GraphDesc(C.Structure):
     _fields_ = [("n_nodes", C.c_int64), ("n_edges", C.c_int64), ("n_rel", C.c_int32),
                 ("n_ntype", C.c_int32), ("src", C.c_void_p), ("dst", C.c_void_p),
                 ("rel", C.c_void_p), ("ntype", C.c_void_p), ("part", C.c_void_p),
-                ("k", C.c_int32), ("edge_w", C.c_void_p)]
+                ("k", C.c_int32), ("edge_w", C.c_void_p), ("edge_ts", C.c_void_p), ("t_cut", C.c_int32),
+                ("reserved", C.c_int32)]
 
 
 class OverlapDesc(C.Structure):
@@ -124,7 +125,7 @@ def lib() -> C.CDLL:
         "hg_hgt_fwd_workspace_size": (sz, [vp, vp]),
         "hg_hgt_bwd_workspace_size": (sz, [vp, vp]),
         "hg_hgt_fwd": (C.c_int, [vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
-        "hg_hgt_bwd": (C.c_int, [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "hg_hgt_bwd": (C.c_int, [vp, vp, vp, vp, vp, vp, vp, vp, vp, i32, vp, sz, vp]),
         "hg_align_workspace_size": (sz, [i64, i32]),
         "hg_align_loss_fwd_bwd": (C.c_int, [i64, i32, i32, i64, vp, vp, vp, vp, f32, f32, f32,
                                             i32, vp, vp, vp, vp, sz, vp]),
@@ -225,14 +226,16 @@ def hg_plan_size(n_nodes: int, n_edges: int, n_rel: int) -> int:
 def hg_build_csr(src, dst, rel, ntype, part, k: int, n_rel: int, n_ntype: int, budget_M: int,
                  key: int = HG_KEY_OUTDEG, theta: int = HG_THETA_NONE, seed: int = 0,
                  want_eid: bool = True, stream=None, ws: Optional[torch.Tensor] = None,
-                 out: Optional[Subgraph] = None) -> Subgraph:
+                 out: Optional[Subgraph] = None, edge_ts=None, t_cut: int = 0) -> Subgraph:
     """Overlapping-subgraph construction; inputs are device tensors
-    (src/dst/part int32, rel/ntype uint8).  Synchronous.  ``out`` reuses the
-    arrays of an earlier build of the same input sizes."""
+    (src/dst/part int32, rel/ntype uint8, edge_ts int32 or None).
+    Synchronous.  ``out`` reuses the arrays of an earlier build of the same
+    input sizes.  With edge_ts, the snapshot that keeps the induced edges with
+    edge_ts <= t_cut."""
     dev = ntype.device
     n, e = int(ntype.shape[0]), int(src.shape[0])
     g = GraphDesc(n, e, n_rel, n_ntype, _ptr(src), _ptr(dst), _ptr(rel), _ptr(ntype), _ptr(part),
-                  k, None)
+                  k, None, _ptr(edge_ts), int(t_cut), 0)
     o = OverlapDesc(budget_M, key, HG_KEYDIR_OUT, theta, 0, seed)
     L = lib()
     if out is not None:
@@ -386,9 +389,10 @@ def hg_hgt_fwd(sub: Subgraph, H_in, weights: dict, heads: int, relu=True, residu
 
 
 def hg_hgt_bwd(sub: Subgraph, H_in, weights: dict, heads: int, mask, saved, dH_out, relu=True, residual=True,
-               dH_in=None, grads: Optional[dict] = None, ws=None, stream=None):
+               dH_in=None, grads: Optional[dict] = None, accumulate: bool = False, ws=None, stream=None):
     """Attention layer backward; returns (dH_in, grads) with grads a dict of
-    the same names as the weights (bias gradients for the biases given)."""
+    the same names as the weights (bias gradients for the biases given),
+    overwritten, or added into when accumulate."""
     d = int(H_in.shape[1])
     desc = _hgt_desc(d, heads, relu, residual)
     L = lib()
@@ -401,7 +405,8 @@ def hg_hgt_bwd(sub: Subgraph, H_in, weights: dict, heads: int, mask, saved, dH_o
     G = _hgt_struct(grads)
     W = _hgt_struct(weights)
     _check(L.hg_hgt_bwd(C.byref(sub.c), C.byref(desc), _ptr(H_in), C.byref(W), _ptr(mask), _ptr(saved),
-                        _ptr(dH_out), _ptr(dH_in), C.byref(G), _ptr(ws), ws.numel(), _stream(stream)), "hg_hgt_bwd")
+                        _ptr(dH_out), _ptr(dH_in), C.byref(G), int(accumulate), _ptr(ws), ws.numel(),
+                        _stream(stream)), "hg_hgt_bwd")
     return dH_in, grads
 
 

@@ -341,11 +341,16 @@ __global__ void k_member_bits(const int32_t* __restrict__ g2l, int64_t n, uint32
 }
 
 // Local ids of both endpoints (one random gather each) and the keep flag.
+// With timestamps, an edge after the cut is dropped like an edge that leaves
+// the node set (its source id is written as -1).
 __global__ void k_edge_keep(const int32_t* __restrict__ src, const int32_t* __restrict__ dst,
-                            const int32_t* __restrict__ g2l, int64_t n_edges, int32_t* __restrict__ keep,
-                            int32_t* __restrict__ sl, int32_t* __restrict__ dl) {
+                            const int32_t* __restrict__ g2l, const int32_t* __restrict__ ts, int32_t t_cut,
+                            int64_t n_edges, int32_t* __restrict__ keep, int32_t* __restrict__ sl,
+                            int32_t* __restrict__ dl) {
   GRID_STRIDE(e, n_edges) {
-    const int32_t s = g2l[src[e]], d = g2l[dst[e]];
+    int32_t s = g2l[src[e]];
+    const int32_t d = g2l[dst[e]];
+    if (ts && ts[e] > t_cut) s = -1;
     sl[e] = s;
     dl[e] = d;
     keep[e] = (s >= 0 && d >= 0) ? 1 : 0;
@@ -666,7 +671,7 @@ extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg
   if (E > 0) {
     // local ids land in the sort's ping-pong buffers (free until the sorts)
     HG_LAUNCH("build_edge_keep", k_edge_keep, dim3(gE), dim3(kBT), 0, s, g->src, g->dst,
-              (const int32_t*)out->global2local, E, w.keep, w.alt1, w.alt2);
+              (const int32_t*)out->global2local, g->edge_ts, g->t_cut, E, w.keep, w.alt1, w.alt2);
     HG_TRY(scan_exclusive_i32(w.keep, w.keep, E, w.cnt + C_ESUB, w.scratch, s));
     HG_LAUNCH("build_edge_compact", k_edge_compact, dim3(gE), dim3(kBT), 0, s, (const int32_t*)w.alt1,
               (const int32_t*)w.alt2, g->rel, (const int32_t*)w.keep, E, (int32_t)R, w.kcsr, w.kcsc, w.vsrc,

@@ -572,15 +572,17 @@ __global__ void k_hgt_heavy_reduce(int64_t n_heavy, const int4* __restrict__ hea
   }
 }
 
-// [R, d, d] -> its diagonal blocks [R, S, dk, dk].
-__global__ void k_diagblocks(const float* __restrict__ full, int64_t R, int d, int S, float* __restrict__ out) {
+// [R, d, d] -> its diagonal blocks [R, S, dk, dk] (added into out when accumulate).
+__global__ void k_diagblocks(const float* __restrict__ full, int64_t R, int d, int S, float* __restrict__ out,
+                             int accumulate) {
   const int dk = d / S;
   const int64_t total = R * S * dk * dk;
   for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
     const int64_t r = e / ((int64_t)S * dk * dk);
     const int s = (int)((e / ((int64_t)dk * dk)) % S);
     const int a = (int)((e / dk) % dk), b = (int)(e % dk);
-    out[e] = full[(r * d + s * dk + a) * d + s * dk + b];
+    const float v = full[(r * d + s * dk + a) * d + s * dk + b];
+    out[e] = accumulate ? out[e] + v : v;
   }
 }
 
@@ -605,18 +607,18 @@ __global__ void __launch_bounds__(256) k_dmu_partial(const float* __restrict__ r
   if (threadIdx.x == 0) mupart[(int64_t)m * kMuChunks + blockIdx.x] = red[0];
 }
 
-__global__ void k_dmu_final(const float* __restrict__ mupart, int M, float* __restrict__ dmu) {
+__global__ void k_dmu_final(const float* __restrict__ mupart, int M, float* __restrict__ dmu, int accumulate) {
   const int m = blockIdx.x * blockDim.x + threadIdx.x;
   if (m >= M) return;
   float s = 0.f;
   for (int c = 0; c < kMuChunks; ++c) s += mupart[(int64_t)m * kMuChunks + c];
-  dmu[m] = s;
+  dmu[m] = accumulate ? dmu[m] + s : s;
 }
 
 template <int D>
 int hgt_bwd_impl(const hg_subgraph* s, const hg_hgt_desc* L, const float* Hin, const hg_hgt_weights* W,
                  const uint32_t* mask, const void* saved, const float* G, float* dHin, const hg_hgt_grads* dW,
-                 void* ws, size_t ws_bytes, hipStream_t st) {
+                 int acc, void* ws, size_t ws_bytes, hipStream_t st) {
   const int S = L->heads;
   const int32_t R = s->n_rel, T = s->n_ntype;
   Arena as(const_cast<void*>(saved), (size_t)-1);
@@ -642,7 +644,7 @@ int hgt_bwd_impl(const hg_subgraph* s, const hg_hgt_desc* L, const float* Hin, c
                                          StoreRows<D, float>{w.dht, rows_contig(lo), nullptr, nullptr}, st)));
     HG_TRY((launch_gemm_tn<D>("hgt_bwd_dw", hi - lo, LoadRows<D, float>{sv.ht, rows_contig(lo)},
                               LoadRows<D, float>{w.dZ, rows_contig(lo)}, w.splitk, w.colsum,
-                              dW->W_agg + (int64_t)t * D * D, dW->b_agg ? dW->b_agg + (int64_t)t * D : nullptr, 0, st)));
+                              dW->W_agg + (int64_t)t * D * D, dW->b_agg ? dW->b_agg + (int64_t)t * D : nullptr, acc, st)));
   }
   // (2) destination pass, (3) source pass
   if (s->n_sub > 0) {
@@ -697,8 +699,10 @@ int hgt_bwd_impl(const hg_subgraph* s, const hg_hgt_desc* L, const float* Hin, c
   {
     const int64_t n = (int64_t)R * D * D / S;
     const unsigned g = (unsigned)(cdiv(n, 256) < 4096 ? cdiv(n, 256) : 4096);
-    HG_LAUNCH("hgt_diagblocks", k_diagblocks, dim3(g), dim3(256), 0, st, (const float*)w.gatt, (int64_t)R, D, S, dW->W_att);
-    HG_LAUNCH("hgt_diagblocks", k_diagblocks, dim3(g), dim3(256), 0, st, (const float*)w.gmsg, (int64_t)R, D, S, dW->W_msg);
+    HG_LAUNCH("hgt_diagblocks", k_diagblocks, dim3(g), dim3(256), 0, st, (const float*)w.gatt, (int64_t)R, D, S, dW->W_att,
+              acc);
+    HG_LAUNCH("hgt_diagblocks", k_diagblocks, dim3(g), dim3(256), 0, st, (const float*)w.gmsg, (int64_t)R, D, S, dW->W_msg,
+              acc);
   }
   // (5) dH = G (residual) + dK W_K^T + dQ W_Q^T + dV W_V^T per type; projection gradients
   for (int t = 0; t < T; ++t) {
@@ -714,7 +718,7 @@ int hgt_bwd_impl(const hg_subgraph* s, const hg_hgt_desc* L, const float* Hin, c
                                            StoreRows<D, float>{dHin, rows_contig(lo), nullptr, addend}, st)));
       HG_TRY((launch_gemm_tn<D>("hgt_bwd_dw", hi - lo, LoadRows<D, float>{Hin, rows_contig(lo)},
                                 LoadRows<D, float>{srcs[k], rows_contig(lo)}, w.splitk, w.colsum, dWs[k] + wo,
-                                dbs[k] ? dbs[k] + bo : nullptr, 0, st)));
+                                dbs[k] ? dbs[k] + bo : nullptr, acc, st)));
     }
   }
   // (6) dmu: per CSR row by source type, then per meta relation over each type range
@@ -728,7 +732,7 @@ int hgt_bwd_impl(const hg_subgraph* s, const hg_hgt_desc* L, const float* Hin, c
     HG_LAUNCH("hgt_bwd_dmu", k_dmu_partial, dim3(kMuChunks, M), dim3(256), 0, st, (const float*)w.rowpart,
               (const int32_t*)s->type_off, R, T, w.mupart);
     HG_LAUNCH("hgt_bwd_dmu", k_dmu_final, dim3((unsigned)cdiv(M, 256)), dim3(256), 0, st, (const float*)w.mupart, M,
-              dW->mu);
+              dW->mu, acc);
   }
   return HG_OK;
 }
@@ -785,9 +789,10 @@ int hg_hgt_fwd(const hg_subgraph* s, const hg_hgt_desc* L, const void* H_in, con
 }
 
 int hg_hgt_bwd(const hg_subgraph* s, const hg_hgt_desc* L, const void* H_in, const hg_hgt_weights* W,
-               const void* mask, const void* saved, const void* dH_out, void* dH_in, const hg_hgt_grads* dW, void* ws,
-               size_t ws_bytes, void* stream) {
+               const void* mask, const void* saved, const void* dH_out, void* dH_in, const hg_hgt_grads* dW,
+               int32_t accumulate, void* ws, size_t ws_bytes, void* stream) {
   HG_TRY(validate_hgt(s, L));
+  if (accumulate != 0 && accumulate != 1) return fail(HG_ERR_ARG, "accumulate must be 0 or 1");
   if (s->n_ntype > kMaxTypesBwd)
     return fail(HG_ERR_UNSUPPORTED, "attention-layer backward: at most %d node types (got %d)", kMaxTypesBwd,
                 s->n_ntype);
@@ -803,8 +808,8 @@ int hg_hgt_bwd(const hg_subgraph* s, const hg_hgt_desc* L, const void* H_in, con
   const uint32_t* m = static_cast<const uint32_t*>(mask);
   const float* G = static_cast<const float*>(dH_out);
   float* dH = static_cast<float*>(dH_in);
-  if (L->d == 64) return hgt_bwd_impl<64>(s, L, Hin, W, m, saved, G, dH, dW, ws, ws_bytes, st);
-  return hgt_bwd_impl<128>(s, L, Hin, W, m, saved, G, dH, dW, ws, ws_bytes, st);
+  if (L->d == 64) return hgt_bwd_impl<64>(s, L, Hin, W, m, saved, G, dH, dW, accumulate, ws, ws_bytes, st);
+  return hgt_bwd_impl<128>(s, L, Hin, W, m, saved, G, dH, dW, accumulate, ws, ws_bytes, st);
 }
 
 }  // extern "C"

@@ -182,3 +182,170 @@ def run_step(inp: StepInputs, rebuild: bool = True) -> StepResult:
         for p, gr, m1, m2 in inp.adam:
             api.hg_adam_step(p, gr, m1, m2, inp.t, lr=mc.lr, weight_decay=mc.weight_decay)
     return StepResult(inp.loss, inp.dH[cur], inp.grads)
+
+
+# ---- multi-snapshot step (attention layers + temporal module) ---------------
+
+@dataclass
+class SeqInputs:
+    wl: synth.Workload
+    graph: dict                 # device tensors src, dst, rel, ntype, part, ts
+    k: int
+    cuts: List[int]
+    subs: List[api.Subgraph]    # one per snapshot; all share local ids and overlap
+    build_ws: torch.Tensor
+    h0: torch.Tensor            # [n_sub, d] features in local order (shared by the snapshots)
+    weights: List[dict]
+    weights_np: List[dict]
+    tparams: dict
+    tparams_np: dict
+    head: dict
+    head_np: dict
+    labels: torch.Tensor
+    labels_np: np.ndarray
+    href: torch.Tensor
+    href_np: np.ndarray
+    feats_np: np.ndarray
+    ts_np: np.ndarray
+    H: List[torch.Tensor] = field(default_factory=list)       # layer activations of the current snapshot
+    masks: List[torch.Tensor] = field(default_factory=list)
+    saved: List[torch.Tensor] = field(default_factory=list)
+    S: List[torch.Tensor] = field(default_factory=list)       # temporal states, one per snapshot
+    dS: List[torch.Tensor] = field(default_factory=list)
+    dH: List[torch.Tensor] = field(default_factory=list)      # ping-pong gradient buffers
+    grads: List[dict] = field(default_factory=list)
+    tgrads: Optional[dict] = None
+    head_grads: Optional[dict] = None
+    fwd_ws: Optional[torch.Tensor] = None
+    bwd_ws: Optional[torch.Tensor] = None
+    t_ws: Optional[torch.Tensor] = None
+    align_ws: Optional[torch.Tensor] = None
+    head_ws: Optional[torch.Tensor] = None
+    loss: Optional[torch.Tensor] = None
+    loss_bce: Optional[torch.Tensor] = None
+    adam: list = field(default_factory=list)
+    t: int = 0
+
+    @property
+    def edges_per_pass(self) -> int:
+        """Edges of all snapshots (one pass of a layer over every snapshot)."""
+        return sum(s.e_sub for s in self.subs)
+
+
+def _build_snapshots(inp_graph, g_k, cfg, cuts, ws=None, subs=None):
+    out = []
+    for i, c in enumerate(cuts):
+        sub = api.hg_build_csr(inp_graph["src"], inp_graph["dst"], inp_graph["rel"], inp_graph["ntype"],
+                               inp_graph["part"], g_k, cfg.n_rel, 2, cfg.budget, key=cfg.key, theta=cfg.theta,
+                               seed=cfg.seed, want_eid=False, ws=ws, out=None if subs is None else subs[i],
+                               edge_ts=inp_graph["ts"], t_cut=c)
+        if ws is None:
+            ws = sub.arrays["ws"]
+        out.append(sub)
+    return out, ws
+
+
+def make_seq_inputs(wl: synth.Workload, g: synth.Graph, device="cuda") -> SeqInputs:
+    cfg, mc = wl.graph, wl.model
+    d, T = mc.d, mc.snapshots
+    ts_np = synth.edge_times(cfg.seed, g.n_edges, T)
+    cuts = synth.snapshot_cuts(T)
+    gd = {k: _dev(getattr(g, k), device) for k in ("src", "dst", "rel", "ntype", "part")}
+    gd["ts"] = _dev(ts_np, device)
+    subs, build_ws = _build_snapshots(gd, g.k, cfg, cuts)
+    sub0 = subs[0]
+    feats = synth.features(mc.seed, g.n_nodes, d)
+    l2g = sub0.view("local2global").long()
+    h0 = _dev(feats, device).index_select(0, l2g).contiguous()
+    weights_np = [synth.hgt_weights(mc.seed, li, cfg.n_rel, g.n_ntype, d, mc.heads, mc.bias_range)
+                  for li in range(mc.n_layers)]
+    weights = [{n: _dev(v, device) for n, v in w.items()} for w in weights_np]
+    tparams_np = synth.temporal_weights(mc.seed, d)
+    tparams = {k: _dev(v, device) for k, v in tparams_np.items()}
+    head_np = synth.head_weights(mc.seed, d)
+    head = {k: _dev(v, device) for k, v in head_np.items()}
+    labels_np = synth.labels(mc.seed, g.ntype)
+    labels = _dev(labels_np, device).index_select(0, l2g).contiguous()
+    m = sub0.m_sel
+    href_np = synth.reference_embeddings(mc.seed, max(m, 1), d)
+    inp = SeqInputs(wl, gd, g.k, cuts, subs, build_ws, h0, weights, weights_np, tparams, tparams_np, head, head_np,
+                    labels, labels_np, _dev(href_np[:m], device), href_np, feats, ts_np)
+    ns = sub0.n_sub
+    f32 = dict(dtype=torch.float32, device=device)
+    inp.H = [h0] + [torch.empty((ns, d), **f32) for _ in range(mc.n_layers)]
+    inp.masks = [torch.empty((max(ns, 1), d // 32), dtype=torch.int32, device=device) for _ in range(mc.n_layers)]
+    inp.saved = [api._ws(api.hg_hgt_saved_size(sub0, d, mc.heads), device) for _ in range(mc.n_layers)]
+    inp.S = [torch.empty((ns, d), **f32) for _ in range(T)]
+    inp.dS = [torch.empty((ns, d), **f32) for _ in range(T)]
+    inp.dH = [torch.empty((ns, d), **f32) for _ in range(2)]
+    inp.grads = [{n: torch.empty_like(v) for n, v in w.items()} for w in weights]
+    inp.tgrads = {k: torch.empty_like(v) for k, v in tparams.items()}
+    inp.head_grads = {k: torch.empty_like(v) for k, v in head.items()}
+    inp.fwd_ws = api._ws(max(api.hg_hgt_fwd_workspace_size(s, d, mc.heads) for s in subs), device)
+    inp.bwd_ws = api._ws(max(api.hg_hgt_bwd_workspace_size(s, d, mc.heads) for s in subs), device)
+    inp.t_ws = api._ws(api.hg_temporal_bwd_workspace_size(ns, d, min(mc.window, T - 1)), device)
+    inp.align_ws = api._ws(api.hg_align_workspace_size(m, d), device)
+    inp.head_ws = api._ws(api.hg_mlp_bce_workspace_size(ns, d), device)
+    inp.loss = torch.empty(3, **f32)
+    inp.loss_bce = torch.empty(1, **f32)
+    pairs = []
+    for w, gw in zip(inp.weights, inp.grads):
+        pairs += [(w[k], gw[k]) for k in w]
+    pairs += [(inp.tparams[k], inp.tgrads[k]) for k in inp.tparams]
+    pairs += [(inp.head[k], inp.head_grads[k]) for k in inp.head]
+    inp.adam = [(p, gr, torch.zeros_like(p), torch.zeros_like(p)) for p, gr in pairs]
+    return inp
+
+
+def _seq_layers_fwd(inp: SeqInputs, t: int):
+    mc = inp.wl.model
+    for li in range(mc.n_layers):
+        api.hg_hgt_fwd(inp.subs[t], inp.H[li], inp.weights[li], mc.heads, H_out=inp.H[li + 1], mask=inp.masks[li],
+                       saved=inp.saved[li], ws=inp.fwd_ws)
+
+
+def run_seq_step(inp: SeqInputs, rebuild: bool = True, update: bool = True, on_snapshot=None):
+    """One step over the snapshots of the subgraph: per snapshot t the
+    attention layers give h^t and the temporal module S^t = GRU(h^t,
+    attention over the previous min(t, w) states); the head's masked BCE and
+    the alignment act on the last state.  The backward runs through every
+    snapshot, latest first: the layer activations of snapshot t are computed
+    again from the shared input features before its backward (only the last
+    snapshot's are still held), the temporal backward adds each context
+    state's gradient into that state's buffer, and the shared weights sum
+    their per-snapshot gradients.  Then Adam updates every parameter.
+    `on_snapshot(t)`, if given, is called after the forward of snapshot t
+    (its layer activations and masks are then in inp.H and inp.masks)."""
+    cfg, mc = inp.wl.graph, inp.wl.model
+    T, w = len(inp.subs), mc.window
+    if rebuild:
+        _build_snapshots(inp.graph, inp.k, cfg, inp.cuts, ws=inp.build_ws, subs=inp.subs)
+    for t in range(T):
+        _seq_layers_fwd(inp, t)
+        api.hg_temporal_fwd(inp.H[-1], inp.S[max(0, t - w):t], inp.tparams, H=inp.S[t])
+        if on_snapshot is not None:
+            on_snapshot(t)
+    g = inp.dS[T - 1]
+    api.hg_mlp_bce_fwd_bwd(inp.S[T - 1], inp.head["W1"], inp.head["b1"], inp.head["W2"], inp.head["b2"], inp.labels,
+                           dH=g, grads=inp.head_grads, loss=inp.loss_bce, ws=inp.head_ws)
+    api.hg_align_loss_fwd_bwd(inp.S[T - 1], inp.subs[0].view("overlap"), inp.href, g, lambda_n=mc.lambda_n,
+                              scale=mc.lambda_cca, eps=mc.eps, ddof=mc.ddof, loss3=inp.loss, ws=inp.align_ws)
+    for j in range(T - 1):
+        inp.dS[j].zero_()
+    for t in reversed(range(T)):
+        if t < T - 1:
+            _seq_layers_fwd(inp, t)
+        lo = max(0, t - w)
+        acc = t < T - 1
+        cur, nxt = 0, 1
+        api.hg_temporal_bwd(inp.H[-1], inp.S[lo:t], inp.tparams, inp.dS[t], dh=inp.dH[cur], dstates=inp.dS[lo:t],
+                            grads=inp.tgrads, accumulate=acc, ws=inp.t_ws)
+        for li in reversed(range(mc.n_layers)):
+            api.hg_hgt_bwd(inp.subs[t], inp.H[li], inp.weights[li], mc.heads, inp.masks[li], inp.saved[li],
+                           inp.dH[cur], dH_in=inp.dH[nxt], grads=inp.grads[li], accumulate=acc, ws=inp.bwd_ws)
+            cur, nxt = nxt, cur
+    if update:
+        inp.t += 1
+        for p, gr, m1, m2 in inp.adam:
+            api.hg_adam_step(p, gr, m1, m2, inp.t, lr=mc.lr, weight_decay=mc.weight_decay)
+    return inp

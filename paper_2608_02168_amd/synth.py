@@ -68,6 +68,8 @@ class ModelConfig:
     objective: str = "synthetic"  # "synthetic" (seeded upstream gradient) or "bce" (head, BCE, Adam)
     lr: float = 1e-3
     weight_decay: float = 1e-5
+    snapshots: int = 1      # T monthly snapshots of the subgraph (> 1: the temporal module runs between them)
+    window: int = 3         # temporal window w: previous states each snapshot attends over
 
 
 @dataclass(frozen=True)
@@ -110,6 +112,15 @@ WORKLOADS = {
         GraphConfig("tiny", 10_000, 100_000, 3, 1.1, 0.0, 9_500, 500, seed=0),
         ModelConfig(64, 2, seed=0, kind="hgt", heads=4),
         "10k nodes, 100k edges, 3 relations, attention layers (4 heads), d=64 fp32, L=2"),
+    "large_dyn": Workload(
+        GraphConfig("large", 10_000_000, 200_000_000, 5, 1.3, 634.0, 9_200_000, 800_000, seed=3),
+        ModelConfig(64, 2, seed=3, kind="hgt", heads=4, objective="bce", snapshots=4, window=3),
+        "the 10M/200M graph over 4 monthly snapshots: attention layers (4 heads) at d=64 fp32, L=2, the temporal "
+        "module with w=3, the prediction head, masked BCE and Adam"),
+    "tiny_dyn": Workload(
+        GraphConfig("tiny", 10_000, 100_000, 3, 1.1, 0.0, 9_500, 500, seed=0),
+        ModelConfig(64, 2, seed=0, kind="hgt", heads=4, objective="bce", snapshots=4, window=3),
+        "10k nodes, 100k edges over 4 monthly snapshots, attention layers, temporal module w=3, head, BCE, Adam"),
     "skew": Workload(
         GraphConfig("skew", 5_000_000, 150_000_000, 8, 1.6, 6339.0, 4_250_000, 750_000,
                     theta=3, rel_split=SKEW_SPLIT, seed=5),

@@ -109,3 +109,34 @@ def test_build_range_error_is_reported():
     with pytest.raises(api.HgError) as ei:
         api.hg_build_csr(src, dst, rel, ntype, part, 0, 1, 1, 5)
     assert ei.value.status == api.HG_ERR_RANGE
+
+
+SNAPSHOT_CASES = {
+    "tiny": (synth.WORKLOADS["tiny"].graph, 0, select.THETA_NONE, None),
+    "tiny_hindex_budget_cut": (synth.WORKLOADS["tiny"].graph, 1, select.THETA_NONE, 211),
+    "skew_small_theta3": (synth.scaled(synth.WORKLOADS["skew"].graph, 0.002), 0, 3, None),
+}
+
+
+@pytest.mark.parametrize("case", sorted(SNAPSHOT_CASES))
+def test_snapshot_build_bit_exact(case):
+    """Each snapshot (edges with timestamp <= cut, node set from every edge)
+    matches the oracle's snapshot bit for bit, for every monthly cut plus a
+    cut before the first day (no edges) and one inside a month."""
+    cfg, key, theta, budget = SNAPSHOT_CASES[case]
+    budget = cfg.budget if budget is None else budget
+    g = synth.make_graph(cfg)
+    ts = synth.edge_times(cfg.seed, g.n_edges)
+    d = graph_to_dev(g)
+    ts_d = torch.from_numpy(ts).cuda()
+    cuts = [-1, 13] + synth.snapshot_cuts(4)
+    sub = None
+    for cut in cuts:
+        ref = select.build(g.src, g.dst, g.rel, g.ntype, g.part, g.k, cfg.n_rel, 2, budget, key, theta, 99,
+                           edge_ts=ts, t_cut=cut)
+        sub = api.hg_build_csr(d["src"], d["dst"], d["rel"], d["ntype"], d["part"], g.k, cfg.n_rel, 2, budget,
+                               key=key, theta=theta, seed=99, edge_ts=ts_d, t_cut=cut, out=sub)
+        print(f"snapshot {case} cut={cut}: e_sub={ref.e_sub}", flush=True)
+        assert_same(ref, sub)
+    assert sub.e_sub == select.build(g.src, g.dst, g.rel, g.ntype, g.part, g.k, cfg.n_rel, 2, budget, key, theta,
+                                     99).e_sub

@@ -127,3 +127,24 @@ def test_hgt_backward_deterministic_and_null_bias_grads():
     for n in runs[0][1]:
         assert np.array_equal(runs[0][1][n], runs[1][1][n]), n
         assert np.all(np.isfinite(runs[0][1][n])), n
+
+
+def test_hgt_backward_accumulate_sums_two_calls():
+    """accumulate = 1 adds the weight gradients of a second upstream gradient
+    into the first call's: the sum matches the oracle's gradients of G1 + G2
+    (the backward is linear in the upstream gradient for a fixed mask)."""
+    cfg, d, heads = CFGS["tiny_d64_h4"]
+    ref, sub, X, w = setup(cfg, d, heads)
+    G1, G2 = synth.upstream_grad(5, ref.n_sub, d), synth.upstream_grad(6, ref.n_sub, d)
+    p = oracle_params(w)
+    _, Z, _, _ = hgt.forward(ref.n_sub, ref.src_l, ref.dst_l, ref.rel_l, ref.ntype_l, X, p, heads)
+    _, g = hgt.backward(ref.n_sub, ref.src_l, ref.dst_l, ref.rel_l, ref.ntype_l, X, p, heads,
+                        G1.astype(np.float64) + G2, mask=Z > 0)
+    Xd, wd = to_dev(X), dev_weights(w)
+    _, _, saved = api.hg_hgt_fwd(sub, Xd, wd, heads)
+    mask = to_dev(pack_mask(Z > 0))
+    _, grads = api.hg_hgt_bwd(sub, Xd, wd, heads, mask, saved, to_dev(G1))
+    _, grads = api.hg_hgt_bwd(sub, Xd, wd, heads, mask, saved, to_dev(G2), grads=grads, accumulate=True)
+    torch.cuda.synchronize()
+    errs = {n: parity_err(grads[n].cpu().numpy(), getattr(g, n)) for n in hgt.PARAM_NAMES}
+    assert max(errs.values()) <= TOL, errs
