@@ -330,3 +330,34 @@ def test_fullsize_attention_layer_sampled_rows(full):
     exp = dHl[np.searchsorted(nodes, srcs)]
     assert parity_err(got[ok], exp[ok]) <= TOL
     del Hd, out, mask, saved, dH
+
+
+def test_fullsize_temporal_sampled_rows():
+    """The temporal module at the sequence workload's full shape (10M rows,
+    d = 64, w = 3, the launch configuration the sequence step uses): the
+    outputs of a row depend on that row only, so H, dh and every dC_k are
+    checked on sampled rows (plus the first and last rows) against the oracle
+    computed for those rows alone."""
+    from oracle import temporal
+    n, d, w = synth.WORKLOADS["large_dyn"].graph.n_nodes, 64, 3
+    p = synth.temporal_weights(3, d)
+    h = synth.features(71, n, d)
+    C = synth.context_states(72, w, n, d)
+    dH = synth.upstream_grad(73, n, d)
+    hd, dHd = to_dev(h), to_dev(dH)
+    Cd = [to_dev(c) for c in C]
+    W = {k: to_dev(v) for k, v in p.items()}
+    H = api.hg_temporal_fwd(hd, Cd, W)
+    dCd = [torch.zeros_like(hd) for _ in range(w)]
+    dh, _ = api.hg_temporal_bwd(hd, Cd, W, dHd, dstates=dCd)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(74)
+    rows = np.unique(np.concatenate([rng.integers(0, n, 8192), [0, 1, n - 2, n - 1]]))
+    ri = torch.from_numpy(rows).cuda()
+    Cs = np.stack([c[rows] for c in C])
+    Hr, _ = temporal.forward(h[rows], Cs, p)
+    dhr, dCr, _ = temporal.backward(h[rows], Cs, p, dH[rows])
+    errs = {"H": parity_err(H[ri].cpu().numpy(), Hr), "dh": parity_err(dh[ri].cpu().numpy(), dhr)}
+    for k in range(w):
+        errs[f"dC{k}"] = parity_err(dCd[k][ri].cpu().numpy(), dCr[k])
+    assert max(errs.values()) <= TOL, errs
