@@ -403,8 +403,11 @@ int layer_bwd_impl(const hg_subgraph* s, const hg_layer_desc* L, const T* Hin, c
   for (int t = 0; t < s->n_ntype; ++t) {
     const int64_t lo = s->type_off_host[t], hi = s->type_off_host[t + 1];
     LoadMasked<D, T> la{G, mask, rows_contig(lo), w.dZ};
-    // the residual addend G is A's own rows before masking
-    StoreRows<D, float, T, true> ep{dacc, rows_contig(lo), nullptr, L->residual ? G : nullptr};
+    // the residual addend G is A's own rows before masking; float32 rows of
+    // d = 128 are read again instead (held through the tile they would not
+    // fit the registers beside the next tile's rows and the split operand)
+    constexpr bool kFromA = !(D == 128 && sizeof(T) == 4);
+    StoreRows<D, float, T, kFromA> ep{dacc, rows_contig(lo), nullptr, L->residual ? G : nullptr};
     HG_TRY((rows_f32<D, true>("gemm_bwd_dx_self", hi - lo, W_self + (int64_t)t * D * D, la, ep, st)));
   }
   // (b) transposed SpMM into float32 dY

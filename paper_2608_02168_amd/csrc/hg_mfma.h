@@ -116,6 +116,61 @@ __device__ __forceinline__ f32x4 mfma4(float a, float b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
 }
 
+// ---- split-fp16 products ------------------------------------------------------
+// A float32 product x w is formed on the fp16 MFMA from two fp16 parts of each
+// factor: with 2^ex the power of two that brings the largest |x| of a scaled
+// group into [2^14, 2^15),  xh = fp16(x 2^ex)  and  xl = fp16(x 2^ex - xh),
+// likewise for w, and
+//   x w ~= 2^-(ex+ew) (xh wh + xh wl + xl wh).
+// The three fp16 MFMAs accumulate into one float32 accumulator (fp16 products
+// are exact in float32) and do the work of one K=32 block at 3/16 of the cost
+// of the float32 MFMA.  The omitted xl wl term and the two conversions leave
+// a relative error of about 2^-21 of the group's largest magnitude, near
+// float32 rounding.  Scaling by powers of two is exact; the range [2^14, 2^15)
+// keeps every part below the fp16 maximum, and a low part falls into the fp16
+// subnormal range only below 2^-28 of the group's largest magnitude.
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+
+__device__ __forceinline__ f32x4 mfma_f16(uint4 a, uint4 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c,
+                                                0, 0, 0);
+}
+
+// Biased float32 exponent of the largest magnitude m of a group, clamped so
+// that both 2^(14 - e) and 2^(e - 14) (e the unbiased exponent) are normal.
+__device__ __forceinline__ uint32_t split_exp(float m) {
+  uint32_t eb = (__float_as_uint(m) >> 23) & 0xFFu;
+  return eb < 15u ? 15u : (eb > 254u ? 254u : eb);
+}
+// 2^(14 - e): multiplies the group into [2^14, 2^15)
+__device__ __forceinline__ float split_scale(uint32_t eb) { return __uint_as_float((268u - eb) << 23); }
+// 2^(e - 14): undoes split_scale
+__device__ __forceinline__ float split_unscale(uint32_t eb) { return __uint_as_float((eb - 14u) << 23); }
+
+// Eight scaled values -> fp16 high parts and fp16 remainders.
+__device__ __forceinline__ void split8(const float (&v)[8], uint4& hi, uint4& lo) {
+  uint32_t h[4], l[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const auto hp = __builtin_amdgcn_cvt_pkrtz(v[2 * q], v[2 * q + 1]);
+    const float r0 = v[2 * q] - (float)hp[0];
+    const float r1 = v[2 * q + 1] - (float)hp[1];
+    h[q] = __builtin_bit_cast(uint32_t, hp);
+    l[q] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(r0, r1));
+  }
+  hi = uint4{h[0], h[1], h[2], h[3]};
+  lo = uint4{l[0], l[1], l[2], l[3]};
+}
+
+// acc unscaled by the two factors' scales one after the other (their product
+// alone could leave the normal range)
+__device__ __forceinline__ f32x4 split_unscale4(f32x4 acc, float ux, float uw) {
+  f32x4 r;
+#pragma unroll
+  for (int v = 0; v < 4; ++v) r[v] = (acc[v] * ux) * uw;
+  return r;
+}
+
 __device__ __forceinline__ int lane64() { return threadIdx.x & 63; }
 
 // Row map: row(i) = (list ? list[i] : first + i) * mul + add.
@@ -197,6 +252,7 @@ struct LoadRows {
   __device__ __forceinline__ f32x4 stored4(const RowRaw& r, int kb) const { return Elt<T>::cook4(r.x[kb]); }
   __device__ __forceinline__ f32x4 operand4(const RowRaw& r, int kb, int) const { return Elt<T>::cook4(r.x[kb]); }
   static constexpr bool kTee = false;
+  static constexpr bool kBoundByStored = false;
   __device__ __forceinline__ void tee4(int64_t, int, int, f32x4) const {}
 };
 
@@ -341,6 +397,8 @@ struct LoadMasked {
     return x;
   }
   static constexpr bool kTee = true;
+  // |operand| <= |stored| element by element (the mask only zeroes)
+  static constexpr bool kBoundByStored = true;
   __device__ __forceinline__ void tee4(int64_t b, int kb, int g, f32x4 x) const {
     if (!tee) return;
     T* o = tee + b * D + 16 * kb + 4 * g;
@@ -534,45 +592,82 @@ int launch_gemm_rows(const char* name, int64_t n_rows, const float* W, ALoad alo
 }
 
 // ---- gemm_rows, software-pipelined (d <= 128) ---------------------------------------
-// Same tiles, LDS layout and transposed MFMA as k_gemm_rows, with the memory
-// traffic spread over the tile instead of bunched at its ends:
-//  - the next tile's A rows are loaded while the current tile is multiplied,
-//    into the other of two register sets (the tile loop is unrolled by two,
-//    so no prefetched value is copied: a copy would wait for the load);
-//  - row-list entries of A are read two tiles ahead, the output rows' one
-//    tile ahead, so no address waits on a load issued just before;
-//  - output columns go in groups of NG blocks: a group's epilogue operands
-//    are loaded before its MFMAs and its results stored right after them.
-// The loader's fetch_row issues the loads; cook_row turns them into MFMA
+// Row GEMM on the split-fp16 MFMA (v_mfma_f32_16x16x32_f16, three products
+// per K block, see split8): tiles of 16 rows per wave, 8 waves per block,
+// persistent over tiles, op(W) staged once per block in LDS.
+//  - Layout.  The MFMA computes the transpose (W fragments as its A operand,
+//    the rows as its B operand), so lane (c, g) ends with 4 consecutive
+//    columns 16 nb + 4 g of row c and the epilogue moves 16 bytes per lane.
+//    Lane (c, g) holds columns 16 kb + 4 g .. + 3 of its row (kb = 0..D/16-1,
+//    one float4 each); the K block kb2 of 32 takes the lane's columns from
+//    kb = 2 kb2 (slots 0-3) and 2 kb2 + 1 (slots 4-7), and LDS holds op(W)
+//    with the same K permutation: uint4 element (kb2 NB + nb) 64 + lane is
+//    op(W)[k][16 nb + c] for the lane's 8 K slots, fp16 high parts, then the
+//    same array of remainders.
+//  - Scaling.  Each row is scaled by the power of two of its largest |x| (the
+//    4 lanes of a row agree by two xor shuffles), op(W) by that of its
+//    largest |w| (a block reduction while it is staged).
+//  - Pipelining.  The next tile's A rows are loaded while the current tile is
+//    multiplied, into the other of two register sets (the tile loop is
+//    unrolled by two, so no prefetched value is copied: a copy would wait for
+//    the load); row-list entries of A are read two tiles ahead, the output
+//    rows' one tile ahead; output columns go in groups of NG blocks whose
+//    epilogue operands are loaded before their MFMAs and stored right after.
+// The loader's fetch_row issues the loads; operand4 turns them into MFMA
 // operands (mask, conversion) when they are used.
 template <int D, bool kTransW, class ALoad, class Epi, bool kListA, bool kListO, int NG>
 __global__ void __launch_bounds__(kGemmThreads, 4) k_gemm_rows_pp(int64_t n_rows, const float* __restrict__ W,
                                                                ALoad aload, Epi epi) {
   static_assert(D == 64 || D == 128, "pipelined gemm_rows: d = 64 or 128");
-  constexpr int KB = D / 16, NB = D / 16;
+  constexpr int KB = D / 16, KB2 = D / 32, NB = D / 16;
   static_assert(NB % NG == 0, "column groups must divide the column blocks");
   static_assert(!Epi::kAddA || !kListO, "an addend taken from A needs the output rows to be the A rows");
   constexpr int kRowsPerTile = 16 * (kGemmThreads / 64);
-  extern __shared__ f32x4 wl[];
+  constexpr int kFrag = KB2 * NB * 64;
+  extern __shared__ uint4 wfr[];  // [kFrag] high parts, then [kFrag] low parts
+  constexpr int kWaves = kGemmThreads / 64;
+  __shared__ float wmax[kWaves + 1];  // per-wave maxima, then the unscale factor of op(W)
   const int tid = threadIdx.x;
-  for (int e = tid; e < KB * NB * 64; e += kGemmThreads) {
-    const int l = e & 63;
-    const int nb = (e >> 6) % NB;
-    const int kb = (e >> 6) / NB;
-    const int j = 16 * nb + (l & 15);
-    const int k0 = 16 * kb + 4 * (l >> 4);
-    f32x4 v;
-    if (kTransW) {
-      v = *reinterpret_cast<const f32x4*>(W + (int64_t)j * D + k0);
-    } else {
-      v[0] = W[(int64_t)(k0 + 0) * D + j];
-      v[1] = W[(int64_t)(k0 + 1) * D + j];
-      v[2] = W[(int64_t)(k0 + 2) * D + j];
-      v[3] = W[(int64_t)(k0 + 3) * D + j];
+  // largest |w| of op(W) (= of W)
+  {
+    float m = 0.f;
+    for (int e = tid; e < D * D / 4; e += kGemmThreads) {
+      const f32x4 v = *reinterpret_cast<const f32x4*>(W + 4 * e);
+      m = fmaxf(m, fmaxf(fmaxf(fabsf(v[0]), fabsf(v[1])), fmaxf(fabsf(v[2]), fabsf(v[3]))));
     }
-    wl[e] = v;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
+    if ((tid & 63) == 0) wmax[tid >> 6] = m;
+    __syncthreads();
+    m = wmax[0];
+#pragma unroll
+    for (int q = 1; q < kWaves; ++q) m = fmaxf(m, wmax[q]);
+    const uint32_t ew = split_exp(m);
+    const float sw = split_scale(ew);
+    for (int e = tid; e < kFrag; e += kGemmThreads) {
+      const int l = e & 63;
+      const int nb = (e >> 6) % NB;
+      const int kb2 = (e >> 6) / NB;
+      const int j = 16 * nb + (l & 15);
+      float v[8];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int k0 = 16 * (2 * kb2 + h) + 4 * (l >> 4);
+        if (kTransW) {
+          const f32x4 x = *reinterpret_cast<const f32x4*>(W + (int64_t)j * D + k0);
+#pragma unroll
+          for (int q = 0; q < 4; ++q) v[4 * h + q] = x[q] * sw;
+        } else {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) v[4 * h + q] = W[(int64_t)(k0 + q) * D + j] * sw;
+        }
+      }
+      split8(v, wfr[e], wfr[kFrag + e]);
+    }
+    if (tid == 0) wmax[kWaves] = split_unscale(ew);
+    __syncthreads();
   }
-  __syncthreads();
+  const float uw = wmax[kWaves];
   const int w = tid >> 6;
   const int l = lane64();
   const int g = l >> 4, c = l & 15;
@@ -592,6 +687,38 @@ __global__ void __launch_bounds__(kGemmThreads, 4) k_gemm_rows_pp(int64_t n_rows
     const bool live = i < n_rows;
     const int64_t ro = epi.map.template row_of<kListO>(ko);
     const int64_t ra = aload.map.template row_of<kListA>(ka);
+    // the row as MFMA operand: scaled by a power of two of its largest
+    // magnitude (or of a bound of it: the stored row, for loaders whose
+    // operand only zeroes elements of it), split in two
+    uint4 xh[KB2], xlo[KB2];
+    float ux;
+    {
+      auto absmax4 = [](f32x4 v) { return fmaxf(fmaxf(fabsf(v[0]), fabsf(v[1])), fmaxf(fabsf(v[2]), fabsf(v[3]))); };
+      float m = 0.f;
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb)
+        m = fmaxf(m, absmax4(ALoad::kBoundByStored ? aload.stored4(x, kb) : aload.operand4(x, kb, g)));
+      m = fmaxf(m, __shfl_xor(m, 16, 64));
+      m = fmaxf(m, __shfl_xor(m, 32, 64));
+      const uint32_t ex = split_exp(m);
+      const float sx = split_scale(ex);
+      ux = split_unscale(ex);
+#pragma unroll
+      for (int kb2 = 0; kb2 < KB2; ++kb2) {
+        const f32x4 a0 = aload.operand4(x, 2 * kb2, g), a1 = aload.operand4(x, 2 * kb2 + 1, g);
+        if (ALoad::kTee && live) {
+          aload.tee4(ra, 2 * kb2, g, a0);
+          aload.tee4(ra, 2 * kb2 + 1, g, a1);
+        }
+        float v[8];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          v[q] = a0[q] * sx;
+          v[4 + q] = a1[q] * sx;
+        }
+        split8(v, xh[kb2], xlo[kb2]);
+      }
+    }
 #pragma unroll
     for (int p = 0; p < NB / NG; ++p) {
       f32x4 pre[NG];
@@ -609,17 +736,18 @@ __global__ void __launch_bounds__(kGemmThreads, 4) k_gemm_rows_pp(int64_t n_rows
 #pragma unroll
       for (int q = 0; q < NG; ++q) acc[q] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int kb = 0; kb < KB; ++kb) {
-        const f32x4 a = aload.operand4(x, kb, g);
-        if (ALoad::kTee && p == 0 && live) aload.tee4(ra, kb, g, a);
-        f32x4 b[NG];
+      for (int kb2 = 0; kb2 < KB2; ++kb2) {
 #pragma unroll
-        for (int q = 0; q < NG; ++q) b[q] = wl[(kb * NB + p * NG + q) * 64 + l];
-#pragma unroll
-        for (int s = 0; s < 4; ++s)
-#pragma unroll
-          for (int q = 0; q < NG; ++q) acc[q] = mfma4(b[q][s], a[s], acc[q]);
+        for (int q = 0; q < NG; ++q) {
+          const int e = (kb2 * NB + p * NG + q) * 64 + l;
+          const uint4 bh = wfr[e], bl = wfr[kFrag + e];
+          acc[q] = mfma_f16(bh, xh[kb2], acc[q]);
+          acc[q] = mfma_f16(bh, xlo[kb2], acc[q]);
+          acc[q] = mfma_f16(bl, xh[kb2], acc[q]);
+        }
       }
+#pragma unroll
+      for (int q = 0; q < NG; ++q) acc[q] = split_unscale4(acc[q], ux, uw);
       if constexpr (Epi::kMask) {
         // store4 returns the 4 output-decision bits of its columns; the lanes
         // (c, 0..3) of a 32-column group hold one 32-bit mask word together
@@ -675,9 +803,10 @@ constexpr int kGemmPPBlocksPerCu = 2;
 template <int D, bool kTransW, class ALoad, class Epi>
 int launch_gemm_rows_pp(const char* name, int64_t n_rows, const float* W, ALoad aload, Epi epi, hipStream_t s) {
   if (n_rows <= 0) return HG_OK;
-  // the masked fp32 loader keeps its raw rows live through the tile (they are
-  // the residual addend): one column block per group keeps it in 128 VGPRs
-  constexpr int NG = (Epi::kAddA && ALoad::kTee && sizeof(typename ALoad::Raw) == 16) ? 1 : 2;
+  // the masked loader's rows (with their mask words) are the largest prefetch
+  // and, as the residual addend, may stay live through the tile: one column
+  // block per group keeps it within 128 VGPRs
+  constexpr int NG = (ALoad::kTee && (D == 128 || (Epi::kAddA && sizeof(typename ALoad::Raw) == 16))) ? 1 : 2;
   const int64_t tiles = cdiv(n_rows, 16 * (kGemmThreads / 64));
   const int64_t cap = (int64_t)num_cus() * kGemmPPBlocksPerCu;
   const int64_t grid = tiles < cap ? tiles : cap;

@@ -64,6 +64,7 @@ struct LoadRank1Masked {
   }
   __device__ __forceinline__ f32x4 stored4(const RowRaw& r, int kb) const { return operand4(r, kb, 0); }
   static constexpr bool kTee = false;
+  static constexpr bool kBoundByStored = false;
   __device__ __forceinline__ void tee4(int64_t, int, int, f32x4) const {}
 };
 
