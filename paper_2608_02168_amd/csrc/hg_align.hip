@@ -231,7 +231,7 @@ int colsum(const char* name, int64_t m, F f, float* part, float* out, hipStream_
 
 template <int D, class T, class ALoad, class Epi>
 int grad_gemm(int64_t m, const float* W, ALoad la, Epi ep, hipStream_t s) {
-  return launch_gemm_rows<D, false, false>("align_grad_gemm", m, W, la, ep, s);
+  return launch_gemm_rows<D, false>("align_grad_gemm", m, W, la, ep, s);
 }
 
 template <int D, class T>

@@ -332,15 +332,10 @@ struct BwdWs {
   }
 };
 
-// fp32 MFMA row transform: the software-pipelined kernel up to d = 128,
-// the column-sliced one at d = 256.
+// Row transform with float32 operands and results (split-fp16 MFMA products).
 template <int D, bool kTransW, class ALoad, class Epi>
 int rows_f32(const char* name, int64_t n, const float* W, ALoad la, Epi ep, hipStream_t st) {
-  if constexpr (D <= 128) {
-    return launch_gemm_rows_pp<D, kTransW>(name, n, W, la, ep, st);
-  } else {
-    return launch_gemm_rows<D, kTransW, false>(name, n, W, la, ep, st);
-  }
+  return launch_gemm_rows_pp<D, kTransW>(name, n, W, la, ep, st);
 }
 
 // fp32 features use the fp32 MFMA transform, bf16 features the bf16 one.

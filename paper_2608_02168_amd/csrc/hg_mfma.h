@@ -460,125 +460,154 @@ struct StoreRows {
 
 // ---- gemm_rows --------------------------------------------------------------
 // Block = 8 waves sharing one LDS copy of a column slice of op(W); a wave owns
-// 16 rows, a block 128 rows; persistent over tiles.  About 100-150 registers
-// per lane keep two to four waves per SIMD resident, which hides the A-row
-// loads behind other waves' MFMAs.  W is D x D; blockIdx.y picks the column
-// slice [DN*y, DN*y + DN) (DN = D for D <= 128, 128 for D = 256).  LDS holds
-// the slice in fragment order: f32x4 element (kb*NB + nb)*64 + lane is
-// op(W)[16 kb + 4 (lane/16) + s][col0 + 16 nb + lane%16], s = 0..3.
+// 16 rows, a block 128 rows; persistent over tiles.  W is D x D; blockIdx.y
+// picks the column slice [DN*y, DN*y + DN) (DN = D for D <= 128, 128 for
+// D = 256).  Products on the split-fp16 MFMA (split8): each row is scaled by
+// the power of two of its largest magnitude, op(W) by that of its own; LDS
+// holds the slice in fragment order, uint4 element (kb2*NB + nb)*64 + lane
+// being op(W)[k][col0 + 16 nb + lane%16] for the lane's 8 K slots of K block
+// kb2 (columns 16 (2 kb2) + 4 (lane/16) .. + 3 and the same 16 further on),
+// high parts first, then the remainders.
 constexpr int kGemmThreads = 512;
 template <int D>
 struct F32Slice {
   static constexpr int DN = D > 128 ? 128 : D;
 };
 
-template <int D, bool kTransW, class ALoad, class Epi, bool kPrefetchArg>
+template <int D, bool kTransW, class ALoad, class Epi>
 __global__ void __launch_bounds__(kGemmThreads) k_gemm_rows(int64_t n_rows, const float* __restrict__ W,
                                                             ALoad aload, Epi epi) {
   constexpr int DN = F32Slice<D>::DN;
-  constexpr int KB = D / 16, NB = DN / 16;
-  constexpr int kWavesPerBlock = kGemmThreads / 64;
-  constexpr int kRowsPerTile = 16 * kWavesPerBlock;
-  extern __shared__ f32x4 wl[];
+  constexpr int KB = D / 16, KB2 = D / 32, NB = DN / 16;
+  constexpr int kWaves = kGemmThreads / 64;
+  constexpr int kRowsPerTile = 16 * kWaves;
+  constexpr int kFrag = KB2 * NB * 64;
+  extern __shared__ uint4 wsl[];  // [kFrag] high parts, then [kFrag] remainders
+  __shared__ float wmax[kWaves + 1];
   const int tid = threadIdx.x;
   const int col0 = DN * blockIdx.y;
-  for (int e = tid; e < KB * NB * 64; e += kGemmThreads) {
-    const int l = e & 63;
-    const int nb = (e >> 6) % NB;
-    const int kb = (e >> 6) / NB;
-    const int j = col0 + 16 * nb + (l & 15);
-    const int k0 = 16 * kb + 4 * (l >> 4);
-    f32x4 v;
-    if (kTransW) {
-      v = *reinterpret_cast<const f32x4*>(W + (int64_t)j * D + k0);
-    } else {
-      v[0] = W[(int64_t)(k0 + 0) * D + j];
-      v[1] = W[(int64_t)(k0 + 1) * D + j];
-      v[2] = W[(int64_t)(k0 + 2) * D + j];
-      v[3] = W[(int64_t)(k0 + 3) * D + j];
+  {
+    float m = 0.f;
+    for (int e = tid; e < D * D / 4; e += kGemmThreads) {
+      const f32x4 v = *reinterpret_cast<const f32x4*>(W + 4 * e);
+      m = fmaxf(m, fmaxf(fmaxf(fabsf(v[0]), fabsf(v[1])), fmaxf(fabsf(v[2]), fabsf(v[3]))));
     }
-    wl[e] = v;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
+    if ((tid & 63) == 0) wmax[tid >> 6] = m;
+    __syncthreads();
+    m = wmax[0];
+#pragma unroll
+    for (int q = 1; q < kWaves; ++q) m = fmaxf(m, wmax[q]);
+    const uint32_t ew = split_exp(m);
+    const float sw = split_scale(ew);
+    for (int e = tid; e < kFrag; e += kGemmThreads) {
+      const int l = e & 63;
+      const int nb = (e >> 6) % NB;
+      const int kb2 = (e >> 6) / NB;
+      const int j = col0 + 16 * nb + (l & 15);
+      float v[8];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int k0 = 16 * (2 * kb2 + h) + 4 * (l >> 4);
+        if (kTransW) {
+          const f32x4 x = *reinterpret_cast<const f32x4*>(W + (int64_t)j * D + k0);
+#pragma unroll
+          for (int q = 0; q < 4; ++q) v[4 * h + q] = x[q] * sw;
+        } else {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) v[4 * h + q] = W[(int64_t)(k0 + q) * D + j] * sw;
+        }
+      }
+      split8(v, wsl[e], wsl[kFrag + e]);
+    }
+    if (tid == 0) wmax[kWaves] = split_unscale(ew);
+    __syncthreads();
   }
-  __syncthreads();
+  const float uw = wmax[kWaves];
   const int w = tid >> 6;
   const int l = lane64();
   const int g = l >> 4, c = l & 15;
   const int64_t ntiles = (n_rows + kRowsPerTile - 1) / kRowsPerTile;
-  // A rows of the next tile are loaded into registers before the current
-  // tile's MFMAs (software pipelining; two waves per SIMD at D = 128).
-  auto load_a = [&](int64_t tt, f32x4 (&dst)[KB]) {
-    const int64_t ia = tt * kRowsPerTile + 16 * w + c;
-    if (tt < ntiles && ia < n_rows) {
-      const auto p = aload.rowp(ia);
-#pragma unroll
-      for (int kb = 0; kb < KB; ++kb) dst[kb] = aload.load4(p, 16 * kb + 4 * g);
-    } else {
-#pragma unroll
-      for (int kb = 0; kb < KB; ++kb) dst[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
-    }
-  };
-  // at D = 256 the next tile's registers do not fit: no prefetch there
-  constexpr bool kPrefetch = kPrefetchArg && D <= 128;
-  f32x4 a[KB];
-  if (kPrefetch) load_a(blockIdx.x, a);
   for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
-    const int64_t r0 = t * kRowsPerTile + 16 * w;
-    if (!kPrefetch) load_a(t, a);
+    // lane (c, g) owns row r0 + c; rows past the end are zero and never stored
+    const int64_t i = t * kRowsPerTile + 16 * w + c;
+    const bool live = i < n_rows;
+    uint4 xh[KB2], xlo[KB2];
+    float ux;
+    {
+      f32x4 a[KB];
+      if (live) {
+        const auto p = aload.rowp(i);
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb) a[kb] = aload.load4(p, 16 * kb + 4 * g);
+      } else {
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb) a[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+      float m = 0.f;
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb)
+        m = fmaxf(m, fmaxf(fmaxf(fabsf(a[kb][0]), fabsf(a[kb][1])), fmaxf(fabsf(a[kb][2]), fabsf(a[kb][3]))));
+      m = fmaxf(m, __shfl_xor(m, 16, 64));
+      m = fmaxf(m, __shfl_xor(m, 32, 64));
+      const uint32_t ex = split_exp(m);
+      const float sx = split_scale(ex);
+      ux = split_unscale(ex);
+#pragma unroll
+      for (int kb2 = 0; kb2 < KB2; ++kb2) {
+        float v[8];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          v[q] = a[2 * kb2][q] * sx;
+          v[4 + q] = a[2 * kb2 + 1][q] * sx;
+        }
+        split8(v, xh[kb2], xlo[kb2]);
+      }
+    }
     // The MFMA computes the transpose, out^T = op(W)^T A^T (W fragments as the
     // A operand, A rows as the B operand), so lane (c, g) ends up holding
-    // row r0 + c, columns col0 + 16 nb + 4 g .. + 3 of the output: the
-    // epilogue reads and writes 16 bytes per lane per column block.
-    const int64_t i = r0 + c;
-    const bool live = i < n_rows;
-    int64_t ro = 0;
-    f32x4 pre[NB];
-    auto load_pre = [&]() {
-      ro = live ? epi.row(i) : 0;
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb)
-        pre[nb] = live ? epi.pre4(i, ro, col0 + 16 * nb + 4 * g) : f32x4{0.f, 0.f, 0.f, 0.f};
-    };
-    if constexpr (kPrefetch) load_pre();
-    f32x4 an[kPrefetch ? KB : 1];
-    if constexpr (kPrefetch) load_a(t + gridDim.x, an);
+    // row i, columns col0 + 16 nb + 4 g .. + 3 of the output: the epilogue
+    // reads and writes 16 bytes per lane per column block.
     f32x4 acc[NB];
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int kb = 0; kb < KB; ++kb) {
+    for (int kb2 = 0; kb2 < KB2; ++kb2) {
       // keep each K block's W fragments local (no hoisting of all LDS reads)
       __builtin_amdgcn_sched_barrier(0);
-      f32x4 b[NB];
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) b[nb] = wl[(kb * NB + nb) * 64 + l];
-#pragma unroll
-      for (int s = 0; s < 4; ++s)
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb) acc[nb] = mfma4(b[nb][s], a[kb][s], acc[nb]);
+      for (int nb = 0; nb < NB; ++nb) {
+        const int e = (kb2 * NB + nb) * 64 + l;
+        const uint4 bh = wsl[e], bl = wsl[kFrag + e];
+        acc[nb] = mfma_f16(bh, xh[kb2], acc[nb]);
+        acc[nb] = mfma_f16(bh, xlo[kb2], acc[nb]);
+        acc[nb] = mfma_f16(bl, xh[kb2], acc[nb]);
+      }
     }
     __builtin_amdgcn_sched_barrier(0);
-    if constexpr (!kPrefetch) load_pre();
     if (live) {
+      const int64_t ro = epi.row(i);
+      f32x4 pre[NB];
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) epi.store4(i, ro, col0 + 16 * nb + 4 * g, acc[nb], pre[nb]);
-    }
-    if constexpr (kPrefetch) {
+      for (int nb = 0; nb < NB; ++nb) pre[nb] = epi.pre4(i, ro, col0 + 16 * nb + 4 * g);
 #pragma unroll
-      for (int kb = 0; kb < KB; ++kb) a[kb] = an[kb];
+      for (int nb = 0; nb < NB; ++nb)
+        epi.store4(i, ro, col0 + 16 * nb + 4 * g, split_unscale4(acc[nb], ux, uw), pre[nb]);
     }
   }
 }
 
-template <int D, bool kTransW, bool kPrefetch = true, class ALoad, class Epi>
+template <int D, bool kTransW, class ALoad, class Epi>
 int launch_gemm_rows(const char* name, int64_t n_rows, const float* W, ALoad aload, Epi epi,
                      hipStream_t s) {
   if (n_rows <= 0) return HG_OK;
   constexpr int DN = F32Slice<D>::DN;
   const int64_t tiles = cdiv(n_rows, 16 * (kGemmThreads / 64));
-  const int64_t cap = (int64_t)num_cus() * ((kPrefetch || D > 128) ? 1 : 2);
+  const int64_t cap = (int64_t)num_cus() * (D > 128 ? 1 : 2);
   const int64_t grid = tiles < cap ? tiles : cap;
   const size_t lds = sizeof(float) * D * DN;
-  auto kern = k_gemm_rows<D, kTransW, ALoad, Epi, kPrefetch>;
+  auto kern = k_gemm_rows<D, kTransW, ALoad, Epi>;
   if (lds > 65536) {
     static bool attr_set = false;
     if (!attr_set) {
@@ -616,10 +645,13 @@ int launch_gemm_rows(const char* name, int64_t n_rows, const float* W, ALoad alo
 // The loader's fetch_row issues the loads; operand4 turns them into MFMA
 // operands (mask, conversion) when they are used.
 template <int D, bool kTransW, class ALoad, class Epi, bool kListA, bool kListO, int NG>
-__global__ void __launch_bounds__(kGemmThreads, 4) k_gemm_rows_pp(int64_t n_rows, const float* __restrict__ W,
-                                                               ALoad aload, Epi epi) {
-  static_assert(D == 64 || D == 128, "pipelined gemm_rows: d = 64 or 128");
-  constexpr int KB = D / 16, KB2 = D / 32, NB = D / 16;
+__global__ void __launch_bounds__(kGemmThreads, D > 128 ? 2 : 4) k_gemm_rows_pp(int64_t n_rows,
+                                                                            const float* __restrict__ W,
+                                                                            ALoad aload, Epi epi) {
+  static_assert(D == 64 || D == 128 || D == 256, "pipelined gemm_rows: d = 64, 128 or 256");
+  constexpr int DN = F32Slice<D>::DN;
+  constexpr int KB = D / 16, KB2 = D / 32, NB = DN / 16;
+  static_assert(!Epi::kMask || D == DN, "mask words need the whole row in one block");
   static_assert(NB % NG == 0, "column groups must divide the column blocks");
   static_assert(!Epi::kAddA || !kListO, "an addend taken from A needs the output rows to be the A rows");
   constexpr int kRowsPerTile = 16 * (kGemmThreads / 64);
@@ -628,6 +660,13 @@ __global__ void __launch_bounds__(kGemmThreads, 4) k_gemm_rows_pp(int64_t n_rows
   constexpr int kWaves = kGemmThreads / 64;
   __shared__ float wmax[kWaves + 1];  // per-wave maxima, then the unscale factor of op(W)
   const int tid = threadIdx.x;
+  // Block -> (column slice, tile group).  With two slices the blocks that
+  // share a tile group differ by 8 in block index, so they run on the same
+  // XCD (blocks go round-robin over the 8) at about the same time and the
+  // second read of each A row hits its L2.
+  const int slice = (D == DN) ? 0 : (int)((blockIdx.x >> 3) & 1);
+  const int64_t bgroup = (D == DN) ? (int64_t)blockIdx.x : (int64_t)(((blockIdx.x >> 4) << 3) | (blockIdx.x & 7));
+  const int col0 = DN * slice;
   // largest |w| of op(W) (= of W)
   {
     float m = 0.f;
@@ -648,7 +687,7 @@ __global__ void __launch_bounds__(kGemmThreads, 4) k_gemm_rows_pp(int64_t n_rows
       const int l = e & 63;
       const int nb = (e >> 6) % NB;
       const int kb2 = (e >> 6) / NB;
-      const int j = 16 * nb + (l & 15);
+      const int j = col0 + 16 * nb + (l & 15);
       float v[8];
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
@@ -672,7 +711,7 @@ __global__ void __launch_bounds__(kGemmThreads, 4) k_gemm_rows_pp(int64_t n_rows
   const int l = lane64();
   const int g = l >> 4, c = l & 15;
   const int64_t ntiles = (n_rows + kRowsPerTile - 1) / kRowsPerTile;
-  const int64_t G = gridDim.x;
+  const int64_t G = (D == DN) ? (int64_t)gridDim.x : (int64_t)(gridDim.x >> 1);
   typedef RowMap::Key<kListA> KA;
   typedef RowMap::Key<kListO> KO;
   typedef typename ALoad::RowRaw RR;
@@ -724,10 +763,19 @@ __global__ void __launch_bounds__(kGemmThreads, 4) k_gemm_rows_pp(int64_t n_rows
       f32x4 pre[NG];
 #pragma unroll
       for (int q = 0; q < NG; ++q) {
-        const int col = 16 * (p * NG + q) + 4 * g;
+        const int col = col0 + 16 * (p * NG + q) + 4 * g;
         if constexpr (Epi::kAddA) {
-          // output column block p NG + q covers the lane's A columns of K block p NG + q
-          pre[q] = epi.addend ? epi.bias4(col) + aload.stored4(x, p * NG + q) : epi.bias4(col);
+          // output column block col0/16 + p NG + q covers the lane's A columns of that K block
+          // (both candidate blocks are named at compile time: a run-time index
+          // would send the row's registers to memory)
+          f32x4 st;
+          if constexpr (D == DN) {
+            st = aload.stored4(x, p * NG + q);
+          } else {
+            static_assert(D == 2 * DN, "two column slices");
+            st = slice == 0 ? aload.stored4(x, p * NG + q) : aload.stored4(x, NB + p * NG + q);
+          }
+          pre[q] = epi.addend ? epi.bias4(col) + st : epi.bias4(col);
         } else {
           pre[q] = epi.pre4(i, ro, col);
         }
@@ -755,7 +803,7 @@ __global__ void __launch_bounds__(kGemmThreads, 4) k_gemm_rows_pp(int64_t n_rows
         uint32_t word = 0;
 #pragma unroll
         for (int q = 0; q < NG; ++q) {
-          const uint32_t nib = live ? epi.store4(i, ro, 16 * (p * NG + q) + 4 * g, acc[q], pre[q]) : 0u;
+          const uint32_t nib = live ? epi.store4(i, ro, col0 + 16 * (p * NG + q) + 4 * g, acc[q], pre[q]) : 0u;
           word |= nib << (16 * q + 4 * g);
         }
         word |= __shfl_xor(word, 16, 64);
@@ -763,11 +811,11 @@ __global__ void __launch_bounds__(kGemmThreads, 4) k_gemm_rows_pp(int64_t n_rows
         if (live && g == 0) epi.mask_word(ro, p, word);
       } else if (live) {
 #pragma unroll
-        for (int q = 0; q < NG; ++q) epi.store4(i, ro, 16 * (p * NG + q) + 4 * g, acc[q], pre[q]);
+        for (int q = 0; q < NG; ++q) epi.store4(i, ro, col0 + 16 * (p * NG + q) + 4 * g, acc[q], pre[q]);
       }
     }
   };
-  int64_t t = blockIdx.x;
+  int64_t t = bgroup;
   if (t >= ntiles) return;
   KA ka0 = aload.map.template key<kListA>(row_in(t));
   KA ka1 = aload.map.template key<kListA>(row_in(t + G));
@@ -807,14 +855,30 @@ int launch_gemm_rows_pp(const char* name, int64_t n_rows, const float* W, ALoad 
   // and, as the residual addend, may stay live through the tile: one column
   // block per group keeps it within 128 VGPRs
   constexpr int NG = (ALoad::kTee && (D == 128 || (Epi::kAddA && sizeof(typename ALoad::Raw) == 16))) ? 1 : 2;
+  constexpr int DN = F32Slice<D>::DN;
   const int64_t tiles = cdiv(n_rows, 16 * (kGemmThreads / 64));
-  const int64_t cap = (int64_t)num_cus() * kGemmPPBlocksPerCu;
-  const int64_t grid = tiles < cap ? tiles : cap;
-  const size_t lds = sizeof(float) * D * D;
+  // LDS holds a D x DN slice of op(W): 64 KB up to d = 128 (two blocks per
+  // compute unit), 128 KB at d = 256 (one)
+  const int64_t cap = (int64_t)num_cus() * (D > 128 ? 1 : kGemmPPBlocksPerCu);
+  int64_t grid = tiles < cap ? tiles : cap;
+  // two column slices: 2 blocks per tile group, groups in multiples of 8 (the
+  // kernel's block -> (slice, group) map pairs blocks 16 q + x and 16 q + 8 + x)
+  if (D > DN) grid = 2 * (cdiv(tiles < cap / 2 ? tiles : cap / 2, 8) * 8);
+  const size_t lds = sizeof(float) * D * DN;
   const bool la = aload.map.list != nullptr, lo = epi.map.list != nullptr;
-#define HG_PP_LAUNCH(LA_, LO_) \
-  HG_LAUNCH(name, (k_gemm_rows_pp<D, kTransW, ALoad, Epi, LA_, LO_, NG>), dim3((unsigned)grid), \
-            dim3(kGemmThreads), lds, s, n_rows, W, aload, epi)
+#define HG_PP_LAUNCH(LA_, LO_)                                                                          \
+  do {                                                                                                  \
+    auto kern = k_gemm_rows_pp<D, kTransW, ALoad, Epi, LA_, LO_, NG>;                                   \
+    if (lds > 65536) {                                                                                  \
+      static bool attr_set = false;                                                                     \
+      if (!attr_set) {                                                                                  \
+        HG_HIP_TRY(hipFuncSetAttribute(reinterpret_cast<const void*>(kern),                             \
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));          \
+        attr_set = true;                                                                                \
+      }                                                                                                 \
+    }                                                                                                   \
+    HG_LAUNCH(name, kern, dim3((unsigned)grid), dim3(kGemmThreads), lds, s, n_rows, W, aload, epi);          \
+  } while (0)
   if constexpr (Epi::kAddA) {
     // the addend is read from the A registers: output row i must be A row i
     if (la || lo || aload.map.first != epi.map.first || aload.map.mul != epi.map.mul ||
@@ -1089,6 +1153,194 @@ __global__ void __launch_bounds__(256) k_gemm_tn(int64_t n_rows, int64_t kc, LA 
   }
 }
 
+// gemm_tn for a bfloat16 A (feature rows stored in bf16, exact as MFMA
+// operands) on v_mfma_f32_16x16x32_bf16, K = 32 rows per step: lane (c, g)
+// reads rows 8 g .. 8 g + 7 of the step (one 8-byte A load and one B load of
+// 4 features each), and block b of the A operand is feature ca + 4 c + b of
+// those 8 rows, as in k_gemm_tn.  A bf16 B is exact too (one MFMA per block
+// pair); a float32 B is split into a bf16 high part and a bf16 remainder (two
+// MFMAs; about 2^-16 of each element is lost), which keeps the weight
+// gradients of the bfloat16 layers far inside their tolerance at a fraction
+// of the float32 MFMA's cost.  Same outputs, chunking, wave tiling and
+// epilogue as k_gemm_tn.
+template <int D, class TB, bool kListA, bool kListB>
+__global__ void __launch_bounds__(256, 2) k_gemm_tn_bf(int64_t n_rows, int64_t kc, LoadRows<D, bf16_t> la,
+                                                       LoadRows<D, TB> lb, float* __restrict__ partial,
+                                                       float* __restrict__ colsum) {
+  static_assert(D == 64 || D == 128 || D == 256, "gemm_tn_bf: d must be 64, 128 or 256");
+  constexpr bool kQuad = (D >= 128);
+  constexpr bool kSplitB = sizeof(TB) == 4;
+  constexpr int E = 8;  // rows per lane and step
+  const int w = threadIdx.x >> 6;
+  const int l = lane64();
+  const int g = l >> 4, c = l & 15;
+  const int64_t chunk = blockIdx.x;
+  const int64_t k_beg = chunk * kc;
+  const int64_t k_end = (k_beg + kc < n_rows) ? k_beg + kc : n_rows;
+  const int qi = kQuad ? (w >> 1) : 0;
+  const int qj = kQuad ? (w & 1) : 0;
+  const int64_t step0 = kQuad ? 0 : 32 * w;
+  const int64_t S = kQuad ? 32 : 128;
+  const int ti = (D == 256) ? (int)(blockIdx.y >> 1) : 0;
+  const int tj = (D == 256) ? (int)(blockIdx.y & 1) : 0;
+  const int ca = 128 * ti + 64 * qi + 4 * c, cb = 128 * tj + 64 * qj + 4 * c;
+  f32x4 acc[4][4];
+  f32x4 bs = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int bi = 0; bi < 4; ++bi)
+#pragma unroll
+    for (int bj = 0; bj < 4; ++bj) acc[bi][bj] = f32x4{0.f, 0.f, 0.f, 0.f};
+  typedef typename Elt<bf16_t>::raw4_t RA;
+  typedef typename Elt<TB>::raw4_t RB;
+  typedef RowMap::Key<kListA> KA;
+  typedef RowMap::Key<kListB> KB;
+  auto keys = [&](int64_t k0, KA (&ka)[E], KB (&kb)[E]) {
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      int64_t r = k0 + 8 * g + e;
+      r = r < k_end ? r : k_end - 1;
+      ka[e] = la.map.template key<kListA>(r);
+      kb[e] = lb.map.template key<kListB>(r);
+    }
+  };
+  auto fetch = [&](const KA (&ka)[E], const KB (&kb)[E], RA (&xa)[E], RB (&xb)[E]) {
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      xa[e] = la.raw4b(la.map.template row_of<kListA>(ka[e]), ca);
+      xb[e] = lb.raw4b(lb.map.template row_of<kListB>(kb[e]), cb);
+    }
+  };
+  // rows 2p, 2p + 1 of bf16 feature f (of 4 per raw uint2) as one bf16 pair
+  auto pair_bf = [](uint2 x0, uint2 x1, int f) -> uint32_t {
+    const uint32_t a = (f < 2) ? x0.x : x0.y, b = (f < 2) ? x1.x : x1.y;
+    return (f & 1) ? ((a >> 16) | (b & 0xFFFF0000u)) : ((a & 0xFFFFu) | (b << 16));
+  };
+  auto compute = [&](int64_t k0, const RA (&xa0)[E], const RB (&xb0)[E]) {
+    RA xa[E];
+    RB xb[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      const bool ok = k0 + 8 * g + e < k_end;
+      xa[e] = ok ? xa0[e] : RA{0u, 0u};
+      if constexpr (kSplitB) {
+        xb[e] = ok ? xb0[e] : RB{0.f, 0.f, 0.f, 0.f};
+      } else {
+        xb[e] = ok ? xb0[e] : RB{0u, 0u};
+      }
+    }
+    uint4 bh[4], bl[4];
+#pragma unroll
+    for (int bj = 0; bj < 4; ++bj) {
+      uint32_t hw[4], lw[4];
+#pragma unroll
+      for (int p = 0; p < 4; ++p) {
+        if constexpr (kSplitB) {
+          const float v0 = xb[2 * p][bj], v1 = xb[2 * p + 1][bj];
+          bs[bj] += v0 + v1;
+          typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+          const bf16x2_t h = {(__bf16)v0, (__bf16)v1};
+          const uint32_t hb = __builtin_bit_cast(uint32_t, h);
+          const bf16x2_t r = {(__bf16)(v0 - __uint_as_float(hb << 16)),
+                              (__bf16)(v1 - __uint_as_float(hb & 0xFFFF0000u))};
+          hw[p] = hb;
+          lw[p] = __builtin_bit_cast(uint32_t, r);
+        } else {
+          hw[p] = pair_bf(xb[2 * p], xb[2 * p + 1], bj);
+          bs[bj] += __uint_as_float(hw[p] << 16) + __uint_as_float(hw[p] & 0xFFFF0000u);
+        }
+      }
+      bh[bj] = uint4{hw[0], hw[1], hw[2], hw[3]};
+      if constexpr (kSplitB) bl[bj] = uint4{lw[0], lw[1], lw[2], lw[3]};
+    }
+#pragma unroll
+    for (int bi = 0; bi < 4; ++bi) {
+      const uint4 a = uint4{pair_bf(xa[0], xa[1], bi), pair_bf(xa[2], xa[3], bi), pair_bf(xa[4], xa[5], bi),
+                            pair_bf(xa[6], xa[7], bi)};
+#pragma unroll
+      for (int bj = 0; bj < 4; ++bj) {
+        acc[bi][bj] = mfma_bf16(a, bh[bj], acc[bi][bj]);
+        if constexpr (kSplitB) acc[bi][bj] = mfma_bf16(a, bl[bj], acc[bi][bj]);
+      }
+    }
+  };
+  int64_t k0 = k_beg + step0;
+  if (k0 < k_end) {
+    KA k0a[E], k1a[E];
+    KB k0b[E], k1b[E];
+    RA x0a[E], x1a[E];
+    RB x0b[E], x1b[E];
+    keys(k0, k0a, k0b);
+    fetch(k0a, k0b, x0a, x0b);
+    keys(k0 + S, k1a, k1b);
+    // one basic block per pair of steps (a second step past the chunk end
+    // multiplies zeroed rows); the barriers keep each phase where it is
+    for (; k0 < k_end; k0 += 2 * S) {
+      fetch(k1a, k1b, x1a, x1b);
+      keys(k0 + 2 * S, k0a, k0b);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(k0, x0a, x0b);
+      __builtin_amdgcn_sched_barrier(0);
+      fetch(k0a, k0b, x0a, x0b);
+      keys(k0 + 3 * S, k1a, k1b);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(k0 + S, x1a, x1b);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+  // column sums: reduce the 4 row groups of the wave
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    bs[q] += __shfl_xor(bs[q], 16, 64);
+    bs[q] += __shfl_xor(bs[q], 32, 64);
+  }
+  float* out = partial + chunk * (int64_t)D * D;
+  if (kQuad) {
+#pragma unroll
+    for (int bi = 0; bi < 4; ++bi)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int64_t i = 128 * ti + 64 * qi + 4 * (4 * g + v) + bi;
+        f32x4 row4;
+#pragma unroll
+        for (int bj = 0; bj < 4; ++bj) row4[bj] = acc[bi][bj][v];
+        *reinterpret_cast<f32x4*>(out + i * D + cb) = row4;
+      }
+    if (colsum && ti == 0 && qi == 0 && g == 0) *reinterpret_cast<f32x4*>(colsum + chunk * D + cb) = bs;
+  } else {
+    __shared__ float red[64 * 64];
+    __shared__ float cred[64];
+    for (int ww = 0; ww < 4; ++ww) {
+      if (w == ww) {
+#pragma unroll
+        for (int bi = 0; bi < 4; ++bi)
+#pragma unroll
+          for (int v = 0; v < 4; ++v)
+#pragma unroll
+            for (int bj = 0; bj < 4; ++bj) {
+              const int idx = (4 * (4 * g + v) + bi) * 64 + 4 * c + bj;
+              red[idx] = (ww == 0 ? 0.f : red[idx]) + acc[bi][bj][v];
+            }
+        if (g == 0) {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) cred[4 * c + q] = (ww == 0 ? 0.f : cred[4 * c + q]) + bs[q];
+        }
+      }
+      __syncthreads();
+    }
+    for (int e = threadIdx.x; e < 64 * 64; e += 256) out[e] = red[e];
+    if (colsum && threadIdx.x < 64) colsum[chunk * D + threadIdx.x] = cred[threadIdx.x];
+  }
+}
+
+template <class L>
+struct IsBf16Rows : std::false_type {};
+template <int D>
+struct IsBf16Rows<LoadRows<D, bf16_t>> : std::true_type {};
+template <class L>
+struct IsPlainRows : std::false_type {};
+template <int D, class T>
+struct IsPlainRows<LoadRows<D, T>> : std::true_type {};
+
 // Fixed-order reduction of nchunks partial arrays of n floats, in two stages:
 // group g sums chunks [g*per, (g+1)*per) in order into tmp[g], then the groups
 // are summed in order: out[i] (+)= sum_g tmp[g][i].
@@ -1164,7 +1416,22 @@ int launch_gemm_tn(const char* name, int64_t n_rows, LA la, LB lb, float* partia
   const bool list_a = la.map.list != nullptr, list_b = lb.map.list != nullptr;
   float* cs = out_colsum ? colsum : nullptr;
   const dim3 grid((unsigned)chunks, tiles);
-  if (list_a && list_b) {
+  if constexpr (IsBf16Rows<LA>::value && IsPlainRows<LB>::value) {
+    // bfloat16 A rows: the bf16 MFMA kernel
+#define HG_TN_BF(LA_, LB_) \
+  HG_LAUNCH(name, (k_gemm_tn_bf<D, typename std::remove_cv<typename std::remove_pointer<decltype(lb.base)>::type>::type, LA_, LB_>), \
+            grid, dim3(256), 0, s, n_rows, kc, la, lb, partial, cs)
+    if (list_a && list_b) {
+      HG_TN_BF(true, true);
+    } else if (!list_a && !list_b) {
+      HG_TN_BF(false, false);
+    } else if (list_a) {
+      HG_TN_BF(true, false);
+    } else {
+      HG_TN_BF(false, true);
+    }
+#undef HG_TN_BF
+  } else if (list_a && list_b) {
     HG_LAUNCH(name, (k_gemm_tn<D, LA, LB, true, true>), grid, dim3(256), 0, s, n_rows, kc, la, lb, partial, cs);
   } else if (!list_a && !list_b) {
     HG_LAUNCH(name, (k_gemm_tn<D, LA, LB, false, false>), grid, dim3(256), 0, s, n_rows, kc, la, lb, partial, cs);
