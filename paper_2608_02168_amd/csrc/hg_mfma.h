@@ -1153,22 +1153,39 @@ __global__ void __launch_bounds__(256) k_gemm_tn(int64_t n_rows, int64_t kc, LA 
   }
 }
 
-// gemm_tn for a bfloat16 A (feature rows stored in bf16, exact as MFMA
-// operands) on v_mfma_f32_16x16x32_bf16, K = 32 rows per step: lane (c, g)
-// reads rows 8 g .. 8 g + 7 of the step (one 8-byte A load and one B load of
-// 4 features each), and block b of the A operand is feature ca + 4 c + b of
-// those 8 rows, as in k_gemm_tn.  A bf16 B is exact too (one MFMA per block
-// pair); a float32 B is split into a bf16 high part and a bf16 remainder (two
-// MFMAs; about 2^-16 of each element is lost), which keeps the weight
-// gradients of the bfloat16 layers far inside their tolerance at a fraction
-// of the float32 MFMA's cost.  Same outputs, chunking, wave tiling and
-// epilogue as k_gemm_tn.
-template <int D, class TB, bool kListA, bool kListB>
-__global__ void __launch_bounds__(256, 2) k_gemm_tn_bf(int64_t n_rows, int64_t kc, LoadRows<D, bf16_t> la,
+// Two float32 values -> three bf16 parts each (packed pairs, round to nearest
+// even): v = p0 + p1 + p2 + r with |r| <= 2^-24 |v| (each part carries the
+// next 8 significant bits of what the previous ones left).
+__device__ __forceinline__ void split_bf3(float v0, float v1, uint32_t (&part)[3]) {
+  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+#pragma unroll
+  for (int k = 0; k < 3; ++k) {
+    const bf16x2_t h = {(__bf16)v0, (__bf16)v1};
+    part[k] = __builtin_bit_cast(uint32_t, h);
+    v0 -= __uint_as_float(part[k] << 16);
+    v1 -= __uint_as_float(part[k] & 0xFFFF0000u);
+  }
+}
+
+// gemm_tn on v_mfma_f32_16x16x32_bf16 for plain feature rows, K = 32 rows
+// per step: lane (c, g) reads rows 8 g .. 8 g + 7 of the step (one A load and
+// one B load of 4 features each per row), and block b of an operand is
+// feature ca + 4 c + b (cb + 4 c + b) of those 8 rows, as in k_gemm_tn.
+// Rows stored in bfloat16 are exact MFMA operands; float32 rows are split
+// into three bf16 parts (split_bf3, 2^-24 of each element left over).  Per
+// block pair: one MFMA (bf16 x bf16), three (one side split: the bf16 side
+// times each part) or six (both split: every part product of order <= 2,
+// p0 q0, p0 q1, p1 q0, p0 q2, p2 q0, p1 q1; the dropped ones are below
+// 2^-24 of the product), at a fraction of the float32 MFMA's cost with
+// float32-like products.  Same outputs, chunking, wave tiling and epilogue
+// as k_gemm_tn.
+template <int D, class TA, class TB, bool kListA, bool kListB>
+__global__ void __launch_bounds__(256, 2) k_gemm_tn_bf(int64_t n_rows, int64_t kc, LoadRows<D, TA> la,
                                                        LoadRows<D, TB> lb, float* __restrict__ partial,
                                                        float* __restrict__ colsum) {
   static_assert(D == 64 || D == 128 || D == 256, "gemm_tn_bf: d must be 64, 128 or 256");
   constexpr bool kQuad = (D >= 128);
+  constexpr bool kSplitA = sizeof(TA) == 4;
   constexpr bool kSplitB = sizeof(TB) == 4;
   constexpr int E = 8;  // rows per lane and step
   const int w = threadIdx.x >> 6;
@@ -1190,7 +1207,7 @@ __global__ void __launch_bounds__(256, 2) k_gemm_tn_bf(int64_t n_rows, int64_t k
   for (int bi = 0; bi < 4; ++bi)
 #pragma unroll
     for (int bj = 0; bj < 4; ++bj) acc[bi][bj] = f32x4{0.f, 0.f, 0.f, 0.f};
-  typedef typename Elt<bf16_t>::raw4_t RA;
+  typedef typename Elt<TA>::raw4_t RA;
   typedef typename Elt<TB>::raw4_t RB;
   typedef RowMap::Key<kListA> KA;
   typedef RowMap::Key<kListB> KB;
@@ -1221,45 +1238,67 @@ __global__ void __launch_bounds__(256, 2) k_gemm_tn_bf(int64_t n_rows, int64_t k
 #pragma unroll
     for (int e = 0; e < E; ++e) {
       const bool ok = k0 + 8 * g + e < k_end;
-      xa[e] = ok ? xa0[e] : RA{0u, 0u};
+      if constexpr (kSplitA) {
+        xa[e] = ok ? xa0[e] : RA{0.f, 0.f, 0.f, 0.f};
+      } else {
+        xa[e] = ok ? xa0[e] : RA{0u, 0u};
+      }
       if constexpr (kSplitB) {
         xb[e] = ok ? xb0[e] : RB{0.f, 0.f, 0.f, 0.f};
       } else {
         xb[e] = ok ? xb0[e] : RB{0u, 0u};
       }
     }
-    uint4 bh[4], bl[4];
+    constexpr int PA = kSplitA ? 3 : 1, PB = kSplitB ? 3 : 1;
+    uint4 bq[4][PB];
 #pragma unroll
     for (int bj = 0; bj < 4; ++bj) {
-      uint32_t hw[4], lw[4];
+      uint32_t w[PB][4];
 #pragma unroll
       for (int p = 0; p < 4; ++p) {
         if constexpr (kSplitB) {
           const float v0 = xb[2 * p][bj], v1 = xb[2 * p + 1][bj];
           bs[bj] += v0 + v1;
-          typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-          const bf16x2_t h = {(__bf16)v0, (__bf16)v1};
-          const uint32_t hb = __builtin_bit_cast(uint32_t, h);
-          const bf16x2_t r = {(__bf16)(v0 - __uint_as_float(hb << 16)),
-                              (__bf16)(v1 - __uint_as_float(hb & 0xFFFF0000u))};
-          hw[p] = hb;
-          lw[p] = __builtin_bit_cast(uint32_t, r);
+          uint32_t part[3];
+          split_bf3(v0, v1, part);
+#pragma unroll
+          for (int k = 0; k < 3; ++k) w[k][p] = part[k];
         } else {
-          hw[p] = pair_bf(xb[2 * p], xb[2 * p + 1], bj);
-          bs[bj] += __uint_as_float(hw[p] << 16) + __uint_as_float(hw[p] & 0xFFFF0000u);
+          w[0][p] = pair_bf(xb[2 * p], xb[2 * p + 1], bj);
+          bs[bj] += __uint_as_float(w[0][p] << 16) + __uint_as_float(w[0][p] & 0xFFFF0000u);
         }
       }
-      bh[bj] = uint4{hw[0], hw[1], hw[2], hw[3]};
-      if constexpr (kSplitB) bl[bj] = uint4{lw[0], lw[1], lw[2], lw[3]};
+#pragma unroll
+      for (int k = 0; k < PB; ++k) bq[bj][k] = uint4{w[k][0], w[k][1], w[k][2], w[k][3]};
     }
 #pragma unroll
     for (int bi = 0; bi < 4; ++bi) {
-      const uint4 a = uint4{pair_bf(xa[0], xa[1], bi), pair_bf(xa[2], xa[3], bi), pair_bf(xa[4], xa[5], bi),
-                            pair_bf(xa[6], xa[7], bi)};
+      uint4 aq[PA];
+      if constexpr (kSplitA) {
+        uint32_t w[3][4];
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+          uint32_t part[3];
+          split_bf3(xa[2 * p][bi], xa[2 * p + 1][bi], part);
+#pragma unroll
+          for (int k = 0; k < 3; ++k) w[k][p] = part[k];
+        }
+#pragma unroll
+        for (int k = 0; k < 3; ++k) aq[k] = uint4{w[k][0], w[k][1], w[k][2], w[k][3]};
+      } else {
+        aq[0] = uint4{pair_bf(xa[0], xa[1], bi), pair_bf(xa[2], xa[3], bi), pair_bf(xa[4], xa[5], bi),
+                      pair_bf(xa[6], xa[7], bi)};
+      }
 #pragma unroll
       for (int bj = 0; bj < 4; ++bj) {
-        acc[bi][bj] = mfma_bf16(a, bh[bj], acc[bi][bj]);
-        if constexpr (kSplitB) acc[bi][bj] = mfma_bf16(a, bl[bj], acc[bi][bj]);
+        // part products of order pa + pb <= 2, smallest first
+#pragma unroll
+        for (int ord = 2; ord >= 0; --ord)
+#pragma unroll
+          for (int pa = 0; pa < PA; ++pa) {
+            const int pb = ord - pa;
+            if (pb >= 0 && pb < PB) acc[bi][bj] = mfma_bf16(aq[pa], bq[bj][pb], acc[bi][bj]);
+          }
       }
     }
   };
@@ -1267,24 +1306,44 @@ __global__ void __launch_bounds__(256, 2) k_gemm_tn_bf(int64_t n_rows, int64_t k
   if (k0 < k_end) {
     KA k0a[E], k1a[E];
     KB k0b[E], k1b[E];
-    RA x0a[E], x1a[E];
-    RB x0b[E], x1b[E];
     keys(k0, k0a, k0b);
-    fetch(k0a, k0b, x0a, x0b);
-    keys(k0 + S, k1a, k1b);
-    // one basic block per pair of steps (a second step past the chunk end
-    // multiplies zeroed rows); the barriers keep each phase where it is
-    for (; k0 < k_end; k0 += 2 * S) {
-      fetch(k1a, k1b, x1a, x1b);
-      keys(k0 + 2 * S, k0a, k0b);
-      __builtin_amdgcn_sched_barrier(0);
-      compute(k0, x0a, x0b);
-      __builtin_amdgcn_sched_barrier(0);
+    if constexpr (kSplitA && kSplitB) {
+      // float32 rows on both sides: their split parts take the registers of
+      // a second row set, so rows are not prefetched (the other waves of the
+      // compute unit cover the load latency); row-list entries still are
+      RA xa[E];
+      RB xb[E];
+      for (; k0 < k_end; k0 += S) {
+        fetch(k0a, k0b, xa, xb);
+        keys(k0 + S, k1a, k1b);
+        __builtin_amdgcn_sched_barrier(0);
+        compute(k0, xa, xb);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          k0a[e] = k1a[e];
+          k0b[e] = k1b[e];
+        }
+      }
+    } else {
+      RA x0a[E], x1a[E];
+      RB x0b[E], x1b[E];
       fetch(k0a, k0b, x0a, x0b);
-      keys(k0 + 3 * S, k1a, k1b);
-      __builtin_amdgcn_sched_barrier(0);
-      compute(k0 + S, x1a, x1b);
-      __builtin_amdgcn_sched_barrier(0);
+      keys(k0 + S, k1a, k1b);
+      // one basic block per pair of steps (a second step past the chunk end
+      // multiplies zeroed rows); the barriers keep each phase where it is
+      for (; k0 < k_end; k0 += 2 * S) {
+        fetch(k1a, k1b, x1a, x1b);
+        keys(k0 + 2 * S, k0a, k0b);
+        __builtin_amdgcn_sched_barrier(0);
+        compute(k0, x0a, x0b);
+        __builtin_amdgcn_sched_barrier(0);
+        fetch(k0a, k0b, x0a, x0b);
+        keys(k0 + 3 * S, k1a, k1b);
+        __builtin_amdgcn_sched_barrier(0);
+        compute(k0 + S, x1a, x1b);
+        __builtin_amdgcn_sched_barrier(0);
+      }
     }
   }
   // column sums: reduce the 4 row groups of the wave
@@ -1332,10 +1391,6 @@ __global__ void __launch_bounds__(256, 2) k_gemm_tn_bf(int64_t n_rows, int64_t k
   }
 }
 
-template <class L>
-struct IsBf16Rows : std::false_type {};
-template <int D>
-struct IsBf16Rows<LoadRows<D, bf16_t>> : std::true_type {};
 template <class L>
 struct IsPlainRows : std::false_type {};
 template <int D, class T>
@@ -1416,11 +1471,12 @@ int launch_gemm_tn(const char* name, int64_t n_rows, LA la, LB lb, float* partia
   const bool list_a = la.map.list != nullptr, list_b = lb.map.list != nullptr;
   float* cs = out_colsum ? colsum : nullptr;
   const dim3 grid((unsigned)chunks, tiles);
-  if constexpr (IsBf16Rows<LA>::value && IsPlainRows<LB>::value) {
-    // bfloat16 A rows: the bf16 MFMA kernel
+  if constexpr (IsPlainRows<LA>::value && IsPlainRows<LB>::value) {
+    // plain feature rows: the bf16 MFMA kernel
+    typedef typename std::remove_cv<typename std::remove_pointer<decltype(la.base)>::type>::type TA_;
+    typedef typename std::remove_cv<typename std::remove_pointer<decltype(lb.base)>::type>::type TB_;
 #define HG_TN_BF(LA_, LB_) \
-  HG_LAUNCH(name, (k_gemm_tn_bf<D, typename std::remove_cv<typename std::remove_pointer<decltype(lb.base)>::type>::type, LA_, LB_>), \
-            grid, dim3(256), 0, s, n_rows, kc, la, lb, partial, cs)
+  HG_LAUNCH(name, (k_gemm_tn_bf<D, TA_, TB_, LA_, LB_>), grid, dim3(256), 0, s, n_rows, kc, la, lb, partial, cs)
     if (list_a && list_b) {
       HG_TN_BF(true, true);
     } else if (!list_a && !list_b) {

@@ -73,4 +73,5 @@ def test_sequence_step_matches_oracle(factor, window):
     for li in range(L):
         for n in hgt.PARAM_NAMES:
             errs[f"layer{li} {n}"] = parity_err(inp.grads[li][n].cpu().numpy(), ref["layer_grads"][li][n])
-    assert max(errs.values()) <= TOL, errs
+    worst = sorted(errs.items(), key=lambda kv: -kv[1])[:4]
+    assert worst[0][1] <= TOL, worst
