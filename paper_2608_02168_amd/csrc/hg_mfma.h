@@ -857,8 +857,8 @@ int launch_gemm_rows_pp(const char* name, int64_t n_rows, const float* W, ALoad 
   constexpr int NG = (ALoad::kTee && (D == 128 || (Epi::kAddA && sizeof(typename ALoad::Raw) == 16))) ? 1 : 2;
   constexpr int DN = F32Slice<D>::DN;
   const int64_t tiles = cdiv(n_rows, 16 * (kGemmThreads / 64));
-  // LDS holds a D x DN slice of op(W): 64 KB up to d = 128 (two blocks per
-  // compute unit), 128 KB at d = 256 (one)
+  // LDS holds a D x DN slice of op(W): 64 KB up to d = 128 (two resident
+  // blocks per compute unit), 128 KB at d = 256 (one)
   const int64_t cap = (int64_t)num_cus() * (D > 128 ? 1 : kGemmPPBlocksPerCu);
   int64_t grid = tiles < cap ? tiles : cap;
   // two column slices: 2 blocks per tile group, groups in multiples of 8 (the
