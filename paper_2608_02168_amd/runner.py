@@ -35,6 +35,8 @@ class StepInputs:
     H: List[torch.Tensor] = field(default_factory=list)
     saved: List[torch.Tensor] = field(default_factory=list)
     dH: List[torch.Tensor] = field(default_factory=list)
+    g: Optional[torch.Tensor] = None        # upstream gradient of the last layer (the alignment adds into it)
+    gext_ovl: Optional[torch.Tensor] = None  # G_ext rows of the overlap nodes
     grads: List[tuple] = field(default_factory=list)
     fwd_ws: Optional[torch.Tensor] = None
     bwd_ws: Optional[torch.Tensor] = None
@@ -106,6 +108,10 @@ def make_inputs(wl: synth.Workload, g: synth.Graph, device="cuda", feats: Option
     inp.saved = [torch.empty((max(ns, 1), d // 32), dtype=torch.int32, device=device)
                  for _ in range(mc.n_layers)]
     inp.dH = [torch.empty((ns, d), **act) for _ in range(2)]
+    # g holds G_ext outside the overlap rows for good; a step only has to
+    # restore the overlap rows the previous step's alignment added into
+    inp.g = inp.gext.clone() if mc.objective != "bce" else torch.empty((ns, d), **act)
+    inp.gext_ovl = inp.gext.index_select(0, sub.view("overlap").long()).contiguous()
     if mc.kind == "hgt":
         inp.grads = [{n: torch.empty_like(v) for n, v in w.items()} for w in weights]
         inp.hgt_saved = [api._ws(api.hg_hgt_saved_size(sub, d, mc.heads), device) for _ in range(mc.n_layers)]
@@ -154,34 +160,33 @@ def run_step(inp: StepInputs, rebuild: bool = True) -> StepResult:
         w_rel, w_self, bias = inp.weights[li]
         api.hg_layer_fwd(sub, inp.H[li], w_rel, w_self, bias, H_out=inp.H[li + 1], saved=inp.saved[li],
                          ws=inp.fwd_ws)
-    g = inp.dH[0]
+    g = inp.g
+    overlap = sub.view("overlap")
     if mc.objective == "bce":
         # dL_BCE/dH of the prediction head on the labelled rows (overwrites g)
         api.hg_mlp_bce_fwd_bwd(inp.H[-1], inp.head["W1"], inp.head["b1"], inp.head["W2"], inp.head["b2"],
                                inp.labels, dH=g, grads=inp.head_grads, loss=inp.loss_bce, ws=inp.head_ws)
     else:
-        g.copy_(inp.gext)
-    overlap = sub.view("overlap")
+        g.index_copy_(0, overlap.long(), inp.gext_ovl)
     api.hg_align_loss_fwd_bwd(inp.H[-1], overlap, inp.href, g, w=inp.omega, lambda_n=mc.lambda_n,
                               scale=mc.lambda_cca, eps=mc.eps, ddof=mc.ddof, loss3=inp.loss,
                               ws=inp.align_ws)
-    cur, nxt = 0, 1
+    gin, nxt = g, 0
     for li in reversed(range(mc.n_layers)):
         if hgt:
-            api.hg_hgt_bwd(sub, inp.H[li], inp.weights[li], mc.heads, inp.saved[li], inp.hgt_saved[li], inp.dH[cur],
+            api.hg_hgt_bwd(sub, inp.H[li], inp.weights[li], mc.heads, inp.saved[li], inp.hgt_saved[li], gin,
                            dH_in=inp.dH[nxt], grads=inp.grads[li], ws=inp.bwd_ws)
-            cur, nxt = nxt, cur
-            continue
-        w_rel, w_self, _ = inp.weights[li]
-        gw = inp.grads[li]
-        api.hg_layer_bwd(sub, inp.H[li], w_rel, w_self, inp.saved[li], inp.dH[cur], dH_in=inp.dH[nxt],
-                         dW_rel=gw[0], dW_self=gw[1], dbias=gw[2], ws=inp.bwd_ws)
-        cur, nxt = nxt, cur
+        else:
+            w_rel, w_self, _ = inp.weights[li]
+            gw = inp.grads[li]
+            api.hg_layer_bwd(sub, inp.H[li], w_rel, w_self, inp.saved[li], gin, dH_in=inp.dH[nxt],
+                             dW_rel=gw[0], dW_self=gw[1], dbias=gw[2], ws=inp.bwd_ws)
+        gin, nxt = inp.dH[nxt], 1 - nxt
     if mc.objective == "bce":
         inp.t += 1
         for p, gr, m1, m2 in inp.adam:
             api.hg_adam_step(p, gr, m1, m2, inp.t, lr=mc.lr, weight_decay=mc.weight_decay)
-    return StepResult(inp.loss, inp.dH[cur], inp.grads)
+    return StepResult(inp.loss, gin, inp.grads)
 
 
 # ---- multi-snapshot step (attention layers + temporal module) ---------------
