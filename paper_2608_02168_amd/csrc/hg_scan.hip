@@ -94,6 +94,10 @@ __global__ void k_scan_tiles(const int32_t* __restrict__ in, int32_t* __restrict
 }
 
 // ---- radix sort -------------------------------------------------------------
+// Tiles of 8192 items (32 per thread): a digit's run inside a tile then
+// averages 32 items, so the scatter writes whole 128-byte lines.
+constexpr int kRItems = 32;
+constexpr int kRTile = kThreads * kRItems;
 
 // Digit histogram of one tile: hist[d * ntiles + tile].
 template <bool kDigitArray>
@@ -103,9 +107,9 @@ __global__ void k_radix_upsweep(const uint32_t* __restrict__ keys, const uint8_t
   __shared__ int cnt[256];
   cnt[threadIdx.x] = 0;
   __syncthreads();
-  const int64_t base = (int64_t)blockIdx.x * kTile;
+  const int64_t base = (int64_t)blockIdx.x * kRTile;
 #pragma unroll 4
-  for (int j = 0; j < kItems; ++j) {
+  for (int j = 0; j < kRItems; ++j) {
     int64_t i = base + (int64_t)j * kThreads + threadIdx.x;
     if (i < n) {
       uint32_t d = kDigitArray ? (uint32_t)digits[i] : ((keys[i] >> shift) & dmask);
@@ -116,8 +120,8 @@ __global__ void k_radix_upsweep(const uint32_t* __restrict__ keys, const uint8_t
   hist[(int64_t)threadIdx.x * ntiles + blockIdx.x] = cnt[threadIdx.x];
 }
 
-// Stable scatter of one tile, staged through LDS.  Wave w owns the 1024
-// consecutive items [1024 w, 1024 w + 1024) of the tile and visits them in 16
+// Stable scatter of one tile, staged through LDS.  Wave w owns the 2048
+// consecutive items [2048 w, 2048 w + 2048) of the tile and visits them in 32
 // rounds of 64 (lane order), so the tile order is (wave, round, lane).  An
 // item's rank among equal digits inside its wave comes from wave-private LDS
 // counters (no block barrier per round); one barrier later the per-digit
@@ -135,10 +139,10 @@ __global__ void __launch_bounds__(256) k_radix_downsweep(
   __shared__ int gbase[256];
   __shared__ int loff[256];
   __shared__ int wcnt[kWaves][256];
-  __shared__ uint32_t sk[kDigitArray ? 1 : kTile];
-  __shared__ int32_t sv1[kTile];
-  __shared__ int32_t sv2[kHasV2 ? kTile : 1];
-  __shared__ uint8_t sd[kTile];
+  __shared__ uint32_t sk[kDigitArray ? 1 : kRTile];
+  __shared__ int32_t sv1[kRTile];
+  __shared__ int32_t sv2[kHasV2 ? kRTile : 1];
+  __shared__ uint8_t sd[kRTile];
   const int t = threadIdx.x;
   const int w = t / kWave;
   const int l = lane_id();
@@ -149,12 +153,12 @@ __global__ void __launch_bounds__(256) k_radix_downsweep(
 #pragma unroll
   for (int i = 0; i < kWaves; ++i) wcnt[i][t] = 0;
   const uint64_t lt_mask = (l == 0) ? 0ull : (~0ull >> (kWave - l));
-  const int64_t wbase = (int64_t)blockIdx.x * kTile + (int64_t)w * (kItems * kWave);
+  const int64_t wbase = (int64_t)blockIdx.x * kRTile + (int64_t)w * (kRItems * kWave);
   // all loads of the wave's slice first
-  uint32_t kd[kItems];  // key, or digit
-  int32_t a1[kItems], a2[kHasV2 ? kItems : 1];
+  uint32_t kd[kRItems];  // key, or digit
+  int32_t a1[kRItems], a2[kHasV2 ? kRItems : 1];
 #pragma unroll
-  for (int j = 0; j < kItems; ++j) {
+  for (int j = 0; j < kRItems; ++j) {
     const int64_t i = wbase + (int64_t)j * kWave + l;
     if (i < n) {
       kd[j] = kDigitArray ? (uint32_t)digits[i] : keys[i];
@@ -170,9 +174,9 @@ __global__ void __launch_bounds__(256) k_radix_downsweep(
   lo = block_excl_scan(cnt, &kept);  // includes a barrier: wcnt zeroing is visible after it
   loff[t] = lo;
   // ranks inside the wave
-  uint16_t rk[kItems];
+  uint16_t rk[kRItems];
 #pragma unroll
-  for (int j = 0; j < kItems; ++j) {
+  for (int j = 0; j < kRItems; ++j) {
     const int64_t i = wbase + (int64_t)j * kWave + l;
     const uint32_t d = kDigitArray ? kd[j] : ((kd[j] >> shift) & dmask);
     const bool valid = i < n && (!kDigitArray || d != 255u);
@@ -204,7 +208,7 @@ __global__ void __launch_bounds__(256) k_radix_downsweep(
   }
   __syncthreads();
 #pragma unroll
-  for (int j = 0; j < kItems; ++j) {
+  for (int j = 0; j < kRItems; ++j) {
     if (rk[j] != 0xFFFFu) {
       const uint32_t d = kDigitArray ? kd[j] : ((kd[j] >> shift) & dmask);
       const int lpos = wcnt[w][d] + rk[j];
@@ -266,7 +270,7 @@ int scan_exclusive_i32(const int32_t* in, int32_t* out, int64_t n, int32_t* tota
 }
 
 int64_t radix_scratch_elems(int64_t n) {
-  const int64_t tiles = cdiv(n > 0 ? n : 1, kTile);
+  const int64_t tiles = cdiv(n > 0 ? n : 1, kRTile);
   const int64_t h = 256 * tiles;
   return h + 1 + scan_scratch_elems(h) + 64;
 }
@@ -278,7 +282,7 @@ int radix_sort_pairs(uint32_t* keys, uint32_t* keys_alt, int32_t* v1, int32_t* v
   *v1_out = v1;
   if (v2_out) *v2_out = v2;
   if (n <= 0 || bits <= 0) return HG_OK;
-  const int64_t tiles = cdiv(n, kTile);
+  const int64_t tiles = cdiv(n, kRTile);
   int32_t* hist = scratch;
   int32_t* sscr = scratch + 256 * tiles + 1;
   uint32_t *ka = keys, *kb = keys_alt;
@@ -314,7 +318,7 @@ int bucket_partition(const uint8_t* digit, const int32_t* val, int64_t n, int nb
                      int32_t* bin_off, int32_t* scratch, hipStream_t s) {
   if (nbins < 1 || nbins > 255) return fail(HG_ERR_ARG, "bucket_partition: nbins %d", nbins);
   if (n <= 0) return fill_i32(bin_off, 0, nbins + 1, s);
-  const int64_t tiles = cdiv(n, kTile);
+  const int64_t tiles = cdiv(n, kRTile);
   int32_t* hist = scratch;
   int32_t* sscr = scratch + 256 * tiles + 1;
   int32_t* total = hist + 256 * tiles;
