@@ -472,7 +472,7 @@ __global__ void __launch_bounds__(kAttnThreads) k_hgt_attn_bwd_src(
     const float* __restrict__ Vt, const float* __restrict__ dht, const float* __restrict__ ld,
     const float* __restrict__ mu, float inv_sqrt_dk, float* __restrict__ dKt,
     float* __restrict__ dVt, double* __restrict__ pk, double* __restrict__ pv) {
-  constexpr int LPR = D / 4, EPW = 64 / LPR, DK = D / S, LPH = DK / 4, U = 2;
+  constexpr int LPR = D / 4, EPW = 64 / LPR, DK = D / S, LPH = DK / 4, U = 4;
   const int l = threadIdx.x & 63;
   const int slot = l / LPR, lr = l % LPR, c0 = lr * 4, head = lr / LPH;
   const int64_t wave0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
