@@ -29,10 +29,13 @@ reordering beyond what the definition states:
   Adam update ("Prediction and Optimization").
 * ``temporal`` -- attention over the w previous states and the GRU update,
   forward and backward ("Temporal Graph Learning").
+* ``kway``    -- K overlapping subgraphs of one graph, MeanAgg of their
+  embeddings, and their joint step with the alignment to the home copies
+  (Algorithm 1 on K workers).
 * ``splitmix`` -- the SplitMix64 mixer used as the seeded tie-break of the
   budgeted sampling.
 
 Every function is pinned by tests under ``tests/`` against brute force,
 closed forms, finite differences or published test vectors.
 """
-from . import splitmix, select, layer, align, step, hgt, objective, temporal  # noqa: F401
+from . import splitmix, select, layer, align, step, hgt, objective, temporal, kway  # noqa: F401

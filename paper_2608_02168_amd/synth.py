@@ -129,6 +129,12 @@ WORKLOADS = {
 }
 
 
+def random_partition(n: int, k_parts: int, seed: int) -> np.ndarray:
+    """Partition block of every node, uniform over [0, k_parts) and
+    independent per node (a random hash partition), int32 [n]."""
+    return _rng(seed, 7).integers(0, k_parts, size=n, dtype=np.int32)
+
+
 def scaled(graph: GraphConfig, factor: float, name: str | None = None) -> GraphConfig:
     """The same recipe at a fraction of the node and edge counts."""
     n = max(16, int(round(graph.n_nodes * factor)))
