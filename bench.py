@@ -5,6 +5,13 @@ forward, the CCA alignment loss + gradient on the overlap rows, L layers
 backward -- every step of it in libhg.so's HIP kernels, inputs resident in
 HBM before the timed region.
 
+With a K-subgraph workload (large_kway, tiny_kway) a step covers the K
+workers one after another: K subgraph builds, L layers forward per
+subgraph, MeanAgg, the head with masked BCE on the average, each
+subgraph's alignment with its overlap nodes' home copies, L layers backward
+per subgraph (weight gradients summed) and one Adam update; the edge count
+is the sum of the K subgraphs' edges.
+
 With a multi-snapshot workload (large_dyn, tiny_dyn) a step covers every
 snapshot: T snapshot builds, per snapshot L attention layers and the
 temporal module, the head with masked BCE and the alignment on the last
@@ -105,7 +112,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--config", default="large",
                     help="tiny | medium | large | large_bf16 | skew | large_hgt | tiny_hgt | large_full | tiny_full | "
-                         "large_dyn | tiny_dyn")
+                         "large_dyn | tiny_dyn | large_kway | tiny_kway")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=float, default=None,
                     help="fraction of the workload's node/edge counts the oracle runs on "
@@ -130,10 +137,15 @@ def main():
     print(f"[bench] graph {wl.graph.name}: N={g.n_nodes} E={g.n_edges} generated in {time.time() - t0:.1f}s",
           file=sys.stderr, flush=True)
     seq = wl.model.snapshots > 1
+    kway = wl.model.parts > 1
     if seq:
         inp = runner.make_seq_inputs(wl, g, device="cuda")
         subs = inp.subs
         step = lambda: runner.run_seq_step(inp)
+    elif kway:
+        inp = runner.make_kway_inputs(wl, g, device="cuda")
+        subs = inp.subs
+        step = lambda: runner.run_kway_step(inp)
     else:
         inp = runner.make_inputs(wl, g, device="cuda")
         subs = [inp.sub]
@@ -191,7 +203,8 @@ def main():
     if not args.no_cpu_baseline:
         frac = args.cpu_sample if args.cpu_sample is not None else (
             0.0005 if seq else 0.001 if wl.model.kind == "hgt" else 0.01)
-        cpu = cpu_baseline_sequence(wl, frac) if seq else cpu_baseline(wl, frac)
+        cpu = (cpu_baseline_sequence(wl, frac) if seq else cpu_baseline_kway(wl, frac) if kway
+               else cpu_baseline(wl, frac))
 
     out = {
         "metric": "GNN layer fwd+bwd edges/sec (GTEPS) + achieved HBM GB/s fraction, 1 GPU",
@@ -205,6 +218,9 @@ def main():
                    **({"heads": wl.model.heads} if wl.model.kind == "hgt" else {}),
                    **({"snapshots": len(subs), "window": wl.model.window, "e_sub_per_snapshot":
                        [s.e_sub for s in subs]} if seq else {}),
+                   **({"parts": len(subs), "n_sub_per_part": [s.n_sub for s in subs],
+                       "e_sub_per_part": [s.e_sub for s in subs], "m_sel_per_part": [s.m_sel for s in subs]}
+                      if kway else {}),
                    "parallelism": "none (1 GPU)"},
         "roofline": roofline,
         "cpu_baseline": cpu,
@@ -285,6 +301,37 @@ def cpu_baseline_sequence(wl, frac):
                       f"{mc.snapshots} snapshot builds, {mc.n_layers} attention layers and the temporal module "
                       f"per snapshot, head, BCE and alignment, backward through every snapshot) in {dt:.1f}s; "
                       f"float64; BLAS {threads} threads"}
+
+
+def cpu_baseline_kway(wl, frac):
+    """The oracle's K-worker step (oracle/kway.py run_kway, unchanged) on the
+    same recipe at a fraction of the node and edge counts."""
+    from threadpoolctl import threadpool_info
+
+    from oracle import kway as oracle_kway
+    from paper_2608_02168_amd import synth
+
+    cfg = synth.scaled(wl.graph, frac)
+    g = synth.make_graph(cfg)
+    mc = wl.model
+    part = synth.random_partition(g.n_nodes, mc.parts, mc.seed)
+    feats = synth.features(mc.seed, g.n_nodes, mc.d)
+    weights = [synth.layer_weights(mc.seed, li, cfg.n_rel, 2, mc.d, mc.bias_range) for li in range(mc.n_layers)]
+    t0 = time.perf_counter()
+    out = oracle_kway.run_kway(dict(src=g.src, dst=g.dst, rel=g.rel, ntype=g.ntype, part=part), mc.parts,
+                               dict(n_rel=cfg.n_rel, n_ntype=2, budget=cfg.budget, key=cfg.key, theta=cfg.theta,
+                                    seed=cfg.seed),
+                               feats, weights, synth.head_weights(mc.seed, mc.d), synth.labels(mc.seed, g.ntype),
+                               lambda_n=mc.lambda_n, scale=mc.lambda_cca, eps=mc.eps, ddof=mc.ddof)
+    dt = time.perf_counter() - t0
+    e_pass = sum(s.e_sub for s in out["subs"])
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    return {"value": round(mc.n_layers * e_pass / dt / 1e9, 6), "unit": "GTEPS", "cores": threads,
+            "kind": "oracle",
+            "sample": f"same recipe at {frac:g} of the node/edge counts: N={g.n_nodes}, E={g.n_edges}, "
+                      f"E_sub per subgraph {[s.e_sub for s in out['subs']]}; one full K-worker step ("
+                      f"{mc.parts} subgraph builds, {mc.n_layers} mean layers fwd+bwd per subgraph, MeanAgg, "
+                      f"head, BCE and home-copy alignment) in {dt:.1f}s; float64; BLAS {threads} threads"}
 
 
 def cpu_baseline(wl, frac):

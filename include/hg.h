@@ -200,12 +200,15 @@ int hg_layer_fwd(const hg_subgraph* s, const hg_layer_desc* L, const void* H_in,
 /* Backward of hg_layer_fwd for upstream gradient dH_out = dL/dH_out:
  *   dZ = dH_out * mask,  dH_in = dH_out (residual) + dZ W_self^T + sum_r A_r^T dZ W_r^T,
  *   dW_r = (A_r H_in)^T dZ,  dW_self[t] = H_t^T dZ_t,  dbias[t] = sum_t dZ_t.
- * Every output is OVERWRITTEN.  dbias may be NULL.  Deterministic: no
- * floating-point atomics, fixed reduction orders. */
+ * dH_in is OVERWRITTEN.  The weight gradients are OVERWRITTEN when
+ * accumulate = 0 and added into when accumulate = 1 (weights shared by
+ * several subgraphs: the sum over workers that the data-parallel gradient
+ * all-reduce forms).  dbias may be NULL.  Deterministic: no floating-point
+ * atomics, fixed reduction orders. */
 int hg_layer_bwd(const hg_subgraph* s, const hg_layer_desc* L, const void* H_in,
                  const float* W_rel, const float* W_self, const void* saved,
                  const void* dH_out, void* dH_in, float* dW_rel, float* dW_self,
-                 float* dbias, void* ws, size_t ws_bytes, void* stream);
+                 float* dbias, int32_t accumulate, void* ws, size_t ws_bytes, void* stream);
 
 /* ---- heterogeneous graph transformer layer (E6-E11) ------------------------
  * S heads of width dk = d / S.  For an edge e = (i -> j) of relation r:
@@ -361,6 +364,52 @@ size_t hg_temporal_bwd_workspace_size(int64_t n, int32_t d, int32_t w);
 int hg_temporal_bwd(int64_t n, int32_t d, int32_t w, int32_t dtype, const void* h, const void* const* C,
                     const hg_temporal_weights* W, const void* dH, void* dh, void* const* dC, int32_t accumulate,
                     const hg_temporal_grads* G, void* ws, size_t ws_bytes, void* stream);
+
+/* ---- several subgraphs of one graph on one device (Algorithm 1 over K
+ * workers) ---------------------------------------------------------------
+ * The K overlapping subgraphs built by hg_build_csr from one graph with one
+ * part[] (values in [0, K)) and k = 0 .. K-1 hold every node once as a base
+ * node (in the subgraph of its own partition block) and once more in every
+ * subgraph that selected it into its overlap.  These calls combine the
+ * subgraphs' per-node rows.  g2l and h_parts are HOST arrays of K DEVICE
+ * pointers: g2l[k] is subgraph k's global2local [n_nodes] (-1 = absent) and
+ * h_parts[k] its rows [n_sub_k, d] in dtype (HG_DTYPE_F32 or HG_DTYPE_BF16,
+ * float32 arithmetic); d in {64, 128, 256}; 1 <= K <= HG_MAX_PARTS.  All
+ * three are asynchronous and deterministic (no atomics). */
+#define HG_MAX_PARTS 64
+
+/* MeanAgg (the inference step of Algorithm 1, and the averaging of an
+ * overlap node's representations across workers in "Prediction and
+ * Optimization"):
+ *   H[v] = (1/cnt[v]) sum_{k : g2l[k][v] >= 0} h_parts[k][g2l[k][v]]
+ * summed in k order, cnt[v] = number of those k.  A node in no subgraph gets
+ * a zero row and cnt 0.  H [n_nodes, d] in dtype is OVERWRITTEN, as is cnt
+ * int32 [n_nodes] (may be NULL).  H must not alias a subgraph's rows. */
+int hg_mean_agg_fwd(int64_t n_nodes, int32_t d, int32_t dtype, int32_t K, const int32_t* const* g2l,
+                    const void* const* h_parts, void* H, int32_t* cnt, void* stream);
+
+/* Backward of hg_mean_agg_fwd into one subgraph with n_sub rows and
+ * local2global l2g [n_sub]:  dh_part[i] = dH[l2g[i]] / cnt[l2g[i]],
+ * OVERWRITTEN when accumulate = 0, added into when accumulate = 1.  cnt is
+ * the forward's; a row whose node has cnt 0 (not possible for cnt from a
+ * forward that included this subgraph) is written as NaN.  dH [n_nodes, d]
+ * and dh_part [n_sub, d] in dtype; they must not alias. */
+int hg_mean_agg_bwd(int64_t n_sub, int32_t d, int32_t dtype, const int32_t* l2g, const int32_t* cnt,
+                    const void* dH, void* dh_part, int32_t accumulate, void* stream);
+
+/* Home copies of one subgraph's overlap rows: the alignment target of an
+ * overlap node is its representation in the subgraph of its own partition
+ * block (Algorithm 1, the CCA term between a worker's overlap nodes and
+ * their home copies):
+ *   v = l2g[overlap[i]],  h = home[i],  Y[i] = h_parts[h][g2l[h][v]]
+ * with overlap, home the subgraph's overlap [m] and overlap_home [m] and l2g
+ * its local2global.  Y [m, d] in dtype is OVERWRITTEN; a row whose home is
+ * outside [0, K) or whose node is absent from the home subgraph is written
+ * as NaN.  On several devices this gather is the all-to-all exchange of the
+ * overlap rows between the workers. */
+int hg_home_gather(int64_t m, int32_t d, int32_t dtype, int32_t K, const int32_t* overlap, const int32_t* l2g,
+                   const int32_t* home, const int32_t* const* g2l, const void* const* h_parts, void* Y,
+                   void* stream);
 
 /* ---- diagnostics ------------------------------------------------------- */
 const char* hg_status_string(int status);

@@ -31,6 +31,7 @@ HG_DTYPE_F32 = 0
 HG_DTYPE_BF16 = 1
 HG_MAX_REL = 255
 HG_MAX_NTYPE = 255
+HG_MAX_PARTS = 64
 
 EXPORTS = [
     "hg_plan_size", "hg_build_csr_workspace_size", "hg_build_csr",
@@ -39,6 +40,7 @@ EXPORTS = [
     "hg_hgt_bwd_workspace_size", "hg_hgt_fwd", "hg_hgt_bwd", "hg_align_workspace_size", "hg_align_loss_fwd_bwd",
     "hg_mlp_bce_workspace_size", "hg_mlp_bce_fwd_bwd", "hg_adam_step",
     "hg_temporal_fwd", "hg_temporal_bwd_workspace_size", "hg_temporal_bwd",
+    "hg_mean_agg_fwd", "hg_mean_agg_bwd", "hg_home_gather",
     "hg_status_string", "hg_last_error_detail", "hg_timing_enable", "hg_timing_collect",
 ]
 
@@ -120,7 +122,7 @@ def lib() -> C.CDLL:
         "hg_layer_fwd_workspace_size": (sz, [vp, vp]),
         "hg_layer_bwd_workspace_size": (sz, [vp, vp]),
         "hg_layer_fwd": (C.c_int, [vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
-        "hg_layer_bwd": (C.c_int, [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "hg_layer_bwd": (C.c_int, [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, i32, vp, sz, vp]),
         "hg_hgt_saved_size": (sz, [vp, vp]),
         "hg_hgt_fwd_workspace_size": (sz, [vp, vp]),
         "hg_hgt_bwd_workspace_size": (sz, [vp, vp]),
@@ -135,6 +137,9 @@ def lib() -> C.CDLL:
         "hg_temporal_fwd": (C.c_int, [i64, i32, i32, i32, vp, vp, vp, vp, vp]),
         "hg_temporal_bwd_workspace_size": (sz, [i64, i32, i32]),
         "hg_temporal_bwd": (C.c_int, [i64, i32, i32, i32, vp, vp, vp, vp, vp, vp, i32, vp, vp, sz, vp]),
+        "hg_mean_agg_fwd": (C.c_int, [i64, i32, i32, i32, vp, vp, vp, vp, vp]),
+        "hg_mean_agg_bwd": (C.c_int, [i64, i32, i32, vp, vp, vp, vp, i32, vp]),
+        "hg_home_gather": (C.c_int, [i64, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp]),
         "hg_status_string": (C.c_char_p, [C.c_int]),
         "hg_last_error_detail": (C.c_char_p, []),
         "hg_timing_enable": (C.c_int, [C.c_int]),
@@ -319,9 +324,10 @@ def hg_layer_fwd(sub: Subgraph, H_in, W_rel, W_self, bias=None, relu=True, resid
 
 
 def hg_layer_bwd(sub: Subgraph, H_in, W_rel, W_self, saved, dH_out, relu=True, residual=True,
-                 dH_in=None, dW_rel=None, dW_self=None, dbias=None, want_dbias=True, ws=None,
-                 stream=None):
-    """Returns (dH_in, dW_rel, dW_self, dbias)."""
+                 dH_in=None, dW_rel=None, dW_self=None, dbias=None, want_dbias=True, accumulate=False,
+                 ws=None, stream=None):
+    """Returns (dH_in, dW_rel, dW_self, dbias); with accumulate the weight
+    gradients are added into the given buffers."""
     d = int(H_in.shape[1])
     desc = _layer_desc(d, H_in.dtype, relu, residual)
     L = lib()
@@ -339,7 +345,8 @@ def hg_layer_bwd(sub: Subgraph, H_in, W_rel, W_self, saved, dH_out, relu=True, r
         ws = _ws(need, dev)
     _check(L.hg_layer_bwd(C.byref(sub.c), C.byref(desc), _ptr(H_in), _ptr(W_rel), _ptr(W_self),
                           _ptr(saved), _ptr(dH_out), _ptr(dH_in), _ptr(dW_rel), _ptr(dW_self),
-                          _ptr(dbias), _ptr(ws), ws.numel(), _stream(stream)), "hg_layer_bwd")
+                          _ptr(dbias), int(bool(accumulate)), _ptr(ws), ws.numel(), _stream(stream)),
+           "hg_layer_bwd")
     return dH_in, dW_rel, dW_self, dbias
 
 
@@ -492,6 +499,42 @@ def hg_temporal_bwd(h, states, weights: dict, dH, dh=None, dstates=None, grads: 
                              _ptr(dh), dctx, int(accumulate), C.byref(G), _ptr(ws), ws.numel(), _stream(stream)),
            "hg_temporal_bwd")
     return dh, grads
+
+
+def hg_mean_agg_fwd(g2l: list, h_parts: list, H=None, cnt=None, stream=None):
+    """MeanAgg over K subgraphs: g2l[k] (int32 [n_nodes]) and h_parts[k]
+    ([n_sub_k, d]) of subgraph k; returns (H [n_nodes, d], cnt int32 [n_nodes])."""
+    n, d = int(g2l[0].shape[0]), int(h_parts[0].shape[1])
+    if H is None:
+        H = torch.empty((n, d), dtype=h_parts[0].dtype, device=h_parts[0].device)
+    if cnt is None:
+        cnt = torch.empty(n, dtype=torch.int32, device=h_parts[0].device)
+    ga, ha = _host_ptrs(g2l), _host_ptrs(h_parts)
+    _check(lib().hg_mean_agg_fwd(n, d, _dtype_code(h_parts[0]), len(h_parts), C.cast(ga, C.c_void_p),
+                                 C.cast(ha, C.c_void_p), _ptr(H), _ptr(cnt), _stream(stream)), "hg_mean_agg_fwd")
+    return H, cnt
+
+
+def hg_mean_agg_bwd(l2g, cnt, dH, dh_part=None, accumulate=False, stream=None):
+    """dh_part[i] = dH[l2g[i]] / cnt[l2g[i]] (added into dh_part when accumulate)."""
+    n_sub, d = int(l2g.shape[0]), int(dH.shape[1])
+    if dh_part is None:
+        dh_part = torch.empty((n_sub, d), dtype=dH.dtype, device=dH.device)
+    _check(lib().hg_mean_agg_bwd(n_sub, d, _dtype_code(dH), _ptr(l2g), _ptr(cnt), _ptr(dH), _ptr(dh_part),
+                                 int(bool(accumulate)), _stream(stream)), "hg_mean_agg_bwd")
+    return dh_part
+
+
+def hg_home_gather(overlap, l2g, home, g2l: list, h_parts: list, Y=None, stream=None):
+    """Home copies of one subgraph's overlap rows: Y [m, d]."""
+    m, d = int(overlap.shape[0]), int(h_parts[0].shape[1])
+    if Y is None:
+        Y = torch.empty((m, d), dtype=h_parts[0].dtype, device=h_parts[0].device)
+    ga, ha = _host_ptrs(g2l), _host_ptrs(h_parts)
+    _check(lib().hg_home_gather(m, d, _dtype_code(h_parts[0]), len(h_parts), _ptr(overlap), _ptr(l2g), _ptr(home),
+                                C.cast(ga, C.c_void_p), C.cast(ha, C.c_void_p), _ptr(Y), _stream(stream)),
+           "hg_home_gather")
+    return Y
 
 
 def hg_align_workspace_size(M: int, d: int) -> int:

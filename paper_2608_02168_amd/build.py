@@ -19,7 +19,7 @@ CEILING_LIB = os.path.join(HERE, "libhg_ceiling.so")
 ARCH = os.environ.get("HG_OFFLOAD_ARCH", "gfx950")
 
 SOURCES = ["hg_api.hip", "hg_scan.hip", "hg_build.hip", "hg_layer.hip", "hg_hgt.hip", "hg_align.hip", "hg_objective.hip",
-           "hg_temporal.hip"]
+           "hg_temporal.hip", "hg_kway.hip"]
 CEILING_SOURCES = ["hg_ceiling.hip"]
 
 FLAGS = [

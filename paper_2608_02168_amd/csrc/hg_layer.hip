@@ -385,7 +385,7 @@ int layer_fwd_impl(const hg_subgraph* s, const hg_layer_desc* L, const T* Hin, c
 template <int D, class T>
 int layer_bwd_impl(const hg_subgraph* s, const hg_layer_desc* L, const T* Hin, const float* W_rel,
                    const float* W_self, const uint32_t* mask, const T* G, T* dHin, float* dW_rel,
-                   float* dW_self, float* dbias, void* ws, size_t ws_bytes, hipStream_t st) {
+                   float* dW_self, float* dbias, int acc, void* ws, size_t ws_bytes, hipStream_t st) {
   Arena a(ws, ws_bytes);
   BwdWs<D, T> w;
   w.layout(a, s);
@@ -434,7 +434,7 @@ int layer_bwd_impl(const hg_subgraph* s, const hg_layer_desc* L, const T* Hin, c
     LoadRows<D, T> la{Hin, rows_contig(lo)};
     LoadRows<D, T> lb{w.dZ, rows_contig(lo)};
     HG_TRY((launch_gemm_tn<D>("gemm_bwd_dw_self", hi - lo, la, lb, w.splitk, w.colsum,
-                              dW_self + (int64_t)t * D * D, dbias ? dbias + (int64_t)t * D : nullptr, 0, st)));
+                              dW_self + (int64_t)t * D * D, dbias ? dbias + (int64_t)t * D : nullptr, acc, st)));
   }
   off = 0;
   for (int r = 0; r < R; ++r) {
@@ -442,7 +442,7 @@ int layer_bwd_impl(const hg_subgraph* s, const hg_layer_desc* L, const T* Hin, c
     LoadRows<D, T> la{Hin, rows_list(pv.active + off)};
     LoadRows<D, float> lb{w.dY, rows_list(pv.active + off, R, r)};
     HG_TRY((launch_gemm_tn<D>("gemm_bwd_dw_rel", n, la, lb, w.splitk, w.colsum, dW_rel + (int64_t)r * D * D,
-                              nullptr, 0, st)));
+                              nullptr, acc, st)));
     off += n;
   }
   return HG_OK;
@@ -507,8 +507,9 @@ extern "C" int hg_layer_fwd(const hg_subgraph* s, const hg_layer_desc* L, const 
 extern "C" int hg_layer_bwd(const hg_subgraph* s, const hg_layer_desc* L, const void* H_in,
                             const float* W_rel, const float* W_self, const void* saved,
                             const void* dH_out, void* dH_in, float* dW_rel, float* dW_self,
-                            float* dbias, void* ws, size_t ws_bytes, void* stream) {
+                            float* dbias, int32_t accumulate, void* ws, size_t ws_bytes, void* stream) {
   HG_TRY(validate_layer(s, L));
+  if (accumulate != 0 && accumulate != 1) return fail(HG_ERR_ARG, "accumulate must be 0 or 1");
   if (!W_rel || !W_self || !dW_rel || !dW_self) return fail(HG_ERR_ARG, "null weight argument");
   if (s->n_sub > 0 && (!H_in || !saved || !dH_out || !dH_in)) return fail(HG_ERR_ARG, "null layer argument");
   if (dH_in == dH_out && s->n_sub > 0) return fail(HG_ERR_ARG, "dH_in must not alias dH_out");
@@ -519,17 +520,17 @@ extern "C" int hg_layer_bwd(const hg_subgraph* s, const hg_layer_desc* L, const 
     const bf16_t* g = (const bf16_t*)dH_out;
     bf16_t* dh = (bf16_t*)dH_in;
     if (L->d_in == 64)
-      return layer_bwd_impl<64, bf16_t>(s, L, hi, W_rel, W_self, m, g, dh, dW_rel, dW_self, dbias, ws, ws_bytes, st);
+      return layer_bwd_impl<64, bf16_t>(s, L, hi, W_rel, W_self, m, g, dh, dW_rel, dW_self, dbias, accumulate, ws, ws_bytes, st);
     if (L->d_in == 128)
-      return layer_bwd_impl<128, bf16_t>(s, L, hi, W_rel, W_self, m, g, dh, dW_rel, dW_self, dbias, ws, ws_bytes, st);
-    return layer_bwd_impl<256, bf16_t>(s, L, hi, W_rel, W_self, m, g, dh, dW_rel, dW_self, dbias, ws, ws_bytes, st);
+      return layer_bwd_impl<128, bf16_t>(s, L, hi, W_rel, W_self, m, g, dh, dW_rel, dW_self, dbias, accumulate, ws, ws_bytes, st);
+    return layer_bwd_impl<256, bf16_t>(s, L, hi, W_rel, W_self, m, g, dh, dW_rel, dW_self, dbias, accumulate, ws, ws_bytes, st);
   }
   const float* hi = (const float*)H_in;
   const float* g = (const float*)dH_out;
   float* dh = (float*)dH_in;
   if (L->d_in == 64)
-    return layer_bwd_impl<64, float>(s, L, hi, W_rel, W_self, m, g, dh, dW_rel, dW_self, dbias, ws, ws_bytes, st);
+    return layer_bwd_impl<64, float>(s, L, hi, W_rel, W_self, m, g, dh, dW_rel, dW_self, dbias, accumulate, ws, ws_bytes, st);
   if (L->d_in == 128)
-    return layer_bwd_impl<128, float>(s, L, hi, W_rel, W_self, m, g, dh, dW_rel, dW_self, dbias, ws, ws_bytes, st);
-  return layer_bwd_impl<256, float>(s, L, hi, W_rel, W_self, m, g, dh, dW_rel, dW_self, dbias, ws, ws_bytes, st);
+    return layer_bwd_impl<128, float>(s, L, hi, W_rel, W_self, m, g, dh, dW_rel, dW_self, dbias, accumulate, ws, ws_bytes, st);
+  return layer_bwd_impl<256, float>(s, L, hi, W_rel, W_self, m, g, dh, dW_rel, dW_self, dbias, accumulate, ws, ws_bytes, st);
 }

@@ -354,3 +354,154 @@ def run_seq_step(inp: SeqInputs, rebuild: bool = True, update: bool = True, on_s
         for p, gr, m1, m2 in inp.adam:
             api.hg_adam_step(p, gr, m1, m2, inp.t, lr=mc.lr, weight_decay=mc.weight_decay)
     return inp
+
+
+# ---- K subgraphs of one graph on one device (Algorithm 1 over K workers) ----
+
+@dataclass
+class KwayInputs:
+    wl: synth.Workload
+    graph: dict                 # device tensors src, dst, rel, ntype, part (the K-way partition)
+    part_np: np.ndarray
+    subs: List[api.Subgraph]    # subgraph k of partition block k
+    build_ws: torch.Tensor      # shared by the K builds (each keeps its own outputs)
+    weights: List[tuple]        # per layer (w_rel, w_self, bias), shared by the K workers
+    weights_np: list
+    head: dict
+    head_np: dict
+    labels: torch.Tensor        # int8 [n_nodes], global order
+    labels_np: np.ndarray
+    feats_np: np.ndarray
+    H: List[List[torch.Tensor]] = field(default_factory=list)      # H[k][l]: layer l rows of subgraph k
+    saved: List[List[torch.Tensor]] = field(default_factory=list)
+    H_agg: Optional[torch.Tensor] = None     # MeanAgg of the K last-layer outputs [n_nodes, d]
+    cnt: Optional[torch.Tensor] = None       # copies of every node
+    dH_agg: Optional[torch.Tensor] = None
+    g: Optional[torch.Tensor] = None         # upstream gradient of one subgraph's last layer
+    dH: List[torch.Tensor] = field(default_factory=list)
+    Y: Optional[torch.Tensor] = None         # home copies of one subgraph's overlap rows
+    grads: List[tuple] = field(default_factory=list)
+    head_grads: Optional[dict] = None
+    fwd_ws: Optional[torch.Tensor] = None
+    bwd_ws: Optional[torch.Tensor] = None
+    align_ws: Optional[torch.Tensor] = None
+    head_ws: Optional[torch.Tensor] = None
+    loss: Optional[torch.Tensor] = None      # [K, 3] alignment losses
+    loss_bce: Optional[torch.Tensor] = None
+    adam: list = field(default_factory=list)
+    t: int = 0
+
+    @property
+    def edges_per_pass(self) -> int:
+        """Edges of all K subgraphs (one pass of a layer over every worker)."""
+        return sum(s.e_sub for s in self.subs)
+
+
+def _build_parts(gd, cfg, K, ws=None, subs=None):
+    out = []
+    for k in range(K):
+        sub = api.hg_build_csr(gd["src"], gd["dst"], gd["rel"], gd["ntype"], gd["part"], k, cfg.n_rel, 2,
+                               cfg.budget, key=cfg.key, theta=cfg.theta, seed=cfg.seed, want_eid=False, ws=ws,
+                               out=None if subs is None else subs[k])
+        if ws is None:
+            ws = sub.arrays["ws"]
+        out.append(sub)
+    return out, ws
+
+
+def make_kway_inputs(wl: synth.Workload, g: synth.Graph, device="cuda") -> KwayInputs:
+    cfg, mc = wl.graph, wl.model
+    d, K = mc.d, mc.parts
+    if mc.kind != "mean" or mc.dtype != "f32" or mc.objective != "bce":
+        raise ValueError("the K-subgraph step runs mean layers on float32 rows with the head objective")
+    part_np = synth.random_partition(g.n_nodes, K, mc.seed)
+    gd = {k: _dev(getattr(g, k), device) for k in ("src", "dst", "rel", "ntype")}
+    gd["part"] = _dev(part_np, device)
+    subs, build_ws = _build_parts(gd, cfg, K)
+    feats = synth.features(mc.seed, g.n_nodes, d)
+    feats_d = _dev(feats, device)
+    weights_np = [synth.layer_weights(mc.seed, li, cfg.n_rel, g.n_ntype, d, mc.bias_range)
+                  for li in range(mc.n_layers)]
+    weights = [(_dev(w.w_rel, device), _dev(w.w_self, device), _dev(w.bias, device)) for w in weights_np]
+    head_np = synth.head_weights(mc.seed, d)
+    head = {k: _dev(v, device) for k, v in head_np.items()}
+    labels_np = synth.labels(mc.seed, g.ntype)
+    inp = KwayInputs(wl, gd, part_np, subs, build_ws, weights, weights_np, head, head_np,
+                     _dev(labels_np, device), labels_np, feats)
+    f32 = dict(dtype=torch.float32, device=device)
+    for sb in subs:
+        h0 = feats_d.index_select(0, sb.view("local2global").long()).contiguous()
+        inp.H.append([h0] + [torch.empty((sb.n_sub, d), **f32) for _ in range(mc.n_layers)])
+        inp.saved.append([torch.empty((max(sb.n_sub, 1), d // 32), dtype=torch.int32, device=device)
+                          for _ in range(mc.n_layers)])
+    del feats_d
+    n = g.n_nodes
+    ns = max(sb.n_sub for sb in subs)
+    m = max(sb.m_sel for sb in subs)
+    inp.H_agg = torch.empty((n, d), **f32)
+    inp.cnt = torch.empty(n, dtype=torch.int32, device=device)
+    inp.dH_agg = torch.empty((n, d), **f32)
+    inp.g = torch.empty((ns, d), **f32)
+    inp.dH = [torch.empty((ns, d), **f32) for _ in range(2)]
+    inp.Y = torch.empty((max(m, 1), d), **f32)
+    inp.grads = [(torch.empty_like(w[0]), torch.empty_like(w[1]), torch.empty_like(w[2])) for w in weights]
+    inp.head_grads = {k: torch.empty_like(v) for k, v in head.items()}
+    inp.fwd_ws = api._ws(max(api.hg_layer_fwd_workspace_size(s, d, torch.float32) for s in subs), device)
+    inp.bwd_ws = api._ws(max(api.hg_layer_bwd_workspace_size(s, d, torch.float32) for s in subs), device)
+    inp.align_ws = api._ws(api.hg_align_workspace_size(m, d), device)
+    inp.head_ws = api._ws(api.hg_mlp_bce_workspace_size(n, d), device)
+    inp.loss = torch.empty((K, 3), **f32)
+    inp.loss_bce = torch.empty(1, **f32)
+    pairs = []
+    for w, gw in zip(inp.weights, inp.grads):
+        pairs += list(zip(w, gw))
+    pairs += [(inp.head[k], inp.head_grads[k]) for k in inp.head]
+    inp.adam = [(p, gr, torch.zeros_like(p), torch.zeros_like(p)) for p, gr in pairs]
+    return inp
+
+
+def run_kway_step(inp: KwayInputs, rebuild: bool = True, update: bool = True):
+    """One step of Algorithm 1 over the K workers' subgraphs, the workers run
+    one after another on this device: each worker's layers map its features
+    to H_k; MeanAgg averages every node's copies into H; the head with the
+    masked BCE acts on H; every worker aligns its overlap rows with their
+    home copies (held constant) through the CCA loss; each worker's backward
+    starts from the MeanAgg backward of dL_BCE/dH plus its alignment
+    gradient; the shared weights collect the sum of the K workers' gradients
+    (what the gradient all-reduce forms); then Adam updates every parameter."""
+    cfg, mc = inp.wl.graph, inp.wl.model
+    K = len(inp.subs)
+    if rebuild:
+        _build_parts(inp.graph, cfg, K, ws=inp.build_ws, subs=inp.subs)
+    for k, sb in enumerate(inp.subs):
+        for li in range(mc.n_layers):
+            w_rel, w_self, bias = inp.weights[li]
+            api.hg_layer_fwd(sb, inp.H[k][li], w_rel, w_self, bias, H_out=inp.H[k][li + 1], saved=inp.saved[k][li],
+                             ws=inp.fwd_ws)
+    g2l = [sb.view("global2local") for sb in inp.subs]
+    last = [h[-1] for h in inp.H]
+    api.hg_mean_agg_fwd(g2l, last, H=inp.H_agg, cnt=inp.cnt)
+    api.hg_mlp_bce_fwd_bwd(inp.H_agg, inp.head["W1"], inp.head["b1"], inp.head["W2"], inp.head["b2"], inp.labels,
+                           dH=inp.dH_agg, grads=inp.head_grads, loss=inp.loss_bce, ws=inp.head_ws)
+    for k, sb in enumerate(inp.subs):
+        ns, m = sb.n_sub, sb.m_sel
+        l2g = sb.view("local2global")
+        overlap = sb.view("overlap")
+        g = inp.g[:ns]
+        api.hg_mean_agg_bwd(l2g, inp.cnt, inp.dH_agg, dh_part=g)
+        Y = inp.Y[:m]
+        api.hg_home_gather(overlap, l2g, sb.view("overlap_home"), g2l, last, Y=Y)
+        api.hg_align_loss_fwd_bwd(last[k], overlap, Y, g, lambda_n=mc.lambda_n, scale=mc.lambda_cca, eps=mc.eps,
+                                  ddof=mc.ddof, loss3=inp.loss[k], ws=inp.align_ws)
+        gin, nxt = g, 0
+        for li in reversed(range(mc.n_layers)):
+            w_rel, w_self, _ = inp.weights[li]
+            gw = inp.grads[li]
+            api.hg_layer_bwd(sb, inp.H[k][li], w_rel, w_self, inp.saved[k][li], gin, dH_in=inp.dH[nxt][:ns],
+                             dW_rel=gw[0], dW_self=gw[1], dbias=gw[2], accumulate=k > 0, ws=inp.bwd_ws)
+            gin, nxt = inp.dH[nxt][:ns], 1 - nxt
+    if update:
+        inp.t += 1
+        for p, gr, m1, m2 in inp.adam:
+            api.hg_adam_step(p, gr, m1, m2, inp.t, lr=mc.lr, weight_decay=mc.weight_decay)
+    return inp

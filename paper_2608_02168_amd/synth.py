@@ -70,6 +70,7 @@ class ModelConfig:
     weight_decay: float = 1e-5
     snapshots: int = 1      # T monthly snapshots of the subgraph (> 1: the temporal module runs between them)
     window: int = 3         # temporal window w: previous states each snapshot attends over
+    parts: int = 1          # K > 1: K subgraphs of a random K-way partition, MeanAgg and home-copy alignment
 
 
 @dataclass(frozen=True)
@@ -121,6 +122,17 @@ WORKLOADS = {
         GraphConfig("tiny", 10_000, 100_000, 3, 1.1, 0.0, 9_500, 500, seed=0),
         ModelConfig(64, 2, seed=0, kind="hgt", heads=4, objective="bce", snapshots=4, window=3),
         "10k nodes, 100k edges over 4 monthly snapshots, attention layers, temporal module w=3, head, BCE, Adam"),
+    "large_kway": Workload(
+        GraphConfig("large", 10_000_000, 200_000_000, 5, 1.3, 634.0, 9_200_000, 800_000, seed=3),
+        ModelConfig(128, 2, seed=3, objective="bce", parts=4),
+        "the 10M/200M graph split by a random 4-way partition: 4 overlapping subgraphs (overlap budget 800k each), "
+        "mean layers d=128 fp32, L=2, MeanAgg, head and masked BCE on the average, alignment of each subgraph's "
+        "overlap rows to their home copies, summed weight gradients and Adam"),
+    "tiny_kway": Workload(
+        GraphConfig("tiny", 10_000, 100_000, 3, 1.1, 0.0, 9_500, 500, seed=0),
+        ModelConfig(64, 2, seed=0, objective="bce", parts=4),
+        "10k nodes, 100k edges split 4 ways: 4 overlapping subgraphs, mean layers d=64, MeanAgg, head, BCE, "
+        "home-copy alignment, Adam"),
     "skew": Workload(
         GraphConfig("skew", 5_000_000, 150_000_000, 8, 1.6, 6339.0, 4_250_000, 750_000,
                     theta=3, rel_split=SKEW_SPLIT, seed=5),

@@ -136,7 +136,9 @@ def test_layer_alias_and_null_checks(L):
     assert L.hg_layer_fwd(C.byref(s), C.byref(ld), None, fake, fake, None, C.c_void_p(8), fake, fake,
                           1, None) == api.HG_ERR_ARG
     assert L.hg_layer_bwd(C.byref(s), C.byref(ld), fake, None, fake, fake, fake, fake, fake, fake,
-                          None, fake, 1, None) == api.HG_ERR_ARG
+                          None, 0, fake, 1, None) == api.HG_ERR_ARG
+    assert L.hg_layer_bwd(C.byref(s), C.byref(ld), fake, fake, fake, fake, fake, fake, fake, fake,
+                          None, 2, fake, 1, None) == api.HG_ERR_ARG
     assert L.hg_layer_fwd(None, C.byref(ld), fake, fake, fake, None, fake, fake, fake, 1,
                           None) == api.HG_ERR_ARG
 
@@ -240,3 +242,25 @@ def test_binding_structs_match_the_header(tmp_path):
         assert got[(cname, "size")] == C.sizeof(py), cname
         for fname, _ in py._fields_:
             assert got[(cname, fname)] == getattr(py, fname).offset, (cname, fname)
+
+
+def test_kway_calls_reject_bad_arguments(L):
+    fake = C.c_void_p(0x1000)
+    arr = (C.c_void_p * 1)(0x1000)
+    # K out of range, bad width, bad dtype, null tables: rejected before any device work
+    assert L.hg_mean_agg_fwd(10, 64, 0, 0, arr, arr, fake, None, None) == api.HG_ERR_ARG
+    assert L.hg_mean_agg_fwd(10, 64, 0, api.HG_MAX_PARTS + 1, arr, arr, fake, None, None) == api.HG_ERR_ARG
+    assert L.hg_mean_agg_fwd(10, 96, 0, 1, arr, arr, fake, None, None) == api.HG_ERR_UNSUPPORTED
+    assert L.hg_mean_agg_fwd(10, 64, 5, 1, arr, arr, fake, None, None) == api.HG_ERR_ARG
+    assert L.hg_mean_agg_fwd(10, 64, 0, 1, None, arr, fake, None, None) == api.HG_ERR_ARG
+    nul = (C.c_void_p * 2)(0x1000, None)
+    assert L.hg_mean_agg_fwd(10, 64, 0, 2, nul, arr, fake, None, None) == api.HG_ERR_ARG
+    assert L.hg_mean_agg_bwd(10, 64, 0, fake, fake, fake, fake, 2, None) == api.HG_ERR_ARG
+    assert L.hg_mean_agg_bwd(10, 64, 0, fake, fake, fake, fake, 0, None) == api.HG_ERR_ARG  # dh aliases dH
+    assert L.hg_mean_agg_bwd(-1, 64, 0, fake, fake, fake, None, 0, None) == api.HG_ERR_ARG
+    assert L.hg_home_gather(4, 64, 0, 0, fake, fake, fake, arr, arr, fake, None) == api.HG_ERR_ARG
+    assert L.hg_home_gather(4, 64, 0, 1, None, fake, fake, arr, arr, fake, None) == api.HG_ERR_ARG
+    # empty inputs are no-ops
+    assert L.hg_mean_agg_fwd(0, 64, 0, 1, arr, arr, None, None, None) == api.HG_OK
+    assert L.hg_mean_agg_bwd(0, 64, 0, None, None, None, None, 0, None) == api.HG_OK
+    assert L.hg_home_gather(0, 64, 0, 1, None, None, None, arr, arr, None, None) == api.HG_OK
