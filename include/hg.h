@@ -113,7 +113,24 @@ typedef struct hg_overlap_desc {
   int32_t theta;          /* >= 0; HG_THETA_NONE = no filter */
   int32_t reserved;
   uint64_t seed;
+  /* NULL, or the key of every node [n_nodes] as hg_node_keys computes it
+   * for this graph and key (device memory, read only).  Keys do not depend
+   * on the partition block, so the builds of several blocks can share one
+   * computation; the build then skips its own. */
+  const int32_t* node_key;
 } hg_overlap_desc;
+
+/* Keys of every node of the graph (the selection key of the h-index filter
+ * and TopM steps of Algorithm 1): keys[v] = out-degree of v over all
+ * relations (HG_KEY_OUTDEG) or the h-index of the multiset of its
+ * out-neighbours' out-degrees, one entry per edge (HG_KEY_HINDEX).  Uses
+ * n_nodes, n_edges, n_rel, src, dst and rel of g; requires n_edges + n_nodes
+ * < 2^31.  SYNCHRONOUS (like hg_build_csr); returns HG_ERR_RANGE when an
+ * edge endpoint or relation is out of range (keys then unspecified).
+ * keys int32 [n_nodes] is OVERWRITTEN.  ws: ws_bytes >=
+ * hg_node_keys_workspace_size(g, key). */
+size_t hg_node_keys_workspace_size(const hg_graph_desc* g, int32_t key);
+int hg_node_keys(const hg_graph_desc* g, int32_t key, int32_t* keys, void* ws, size_t ws_bytes, void* stream);
 
 /* Overlapping subgraph G[V_k u C_{k,M}] (union equation; induced subgraph of
  * Algorithm 1).  Local ids order the nodes by (node type, global id), so each

@@ -34,7 +34,7 @@ HG_MAX_NTYPE = 255
 HG_MAX_PARTS = 64
 
 EXPORTS = [
-    "hg_plan_size", "hg_build_csr_workspace_size", "hg_build_csr",
+    "hg_plan_size", "hg_build_csr_workspace_size", "hg_build_csr", "hg_node_keys_workspace_size", "hg_node_keys",
     "hg_layer_saved_size", "hg_layer_fwd_workspace_size", "hg_layer_bwd_workspace_size",
     "hg_layer_fwd", "hg_layer_bwd", "hg_hgt_saved_size", "hg_hgt_fwd_workspace_size",
     "hg_hgt_bwd_workspace_size", "hg_hgt_fwd", "hg_hgt_bwd", "hg_align_workspace_size", "hg_align_loss_fwd_bwd",
@@ -61,7 +61,7 @@ class GraphDesc(C.Structure):
 
 class OverlapDesc(C.Structure):
     _fields_ = [("budget_M", C.c_int64), ("key", C.c_int32), ("key_dir", C.c_int32),
-                ("theta", C.c_int32), ("reserved", C.c_int32), ("seed", C.c_uint64)]
+                ("theta", C.c_int32), ("reserved", C.c_int32), ("seed", C.c_uint64), ("node_key", C.c_void_p)]
 
 
 class SubgraphStruct(C.Structure):
@@ -116,6 +116,8 @@ def lib() -> C.CDLL:
     vp, sz, i64, i32, f32 = C.c_void_p, C.c_size_t, C.c_int64, C.c_int32, C.c_float
     sig = {
         "hg_plan_size": (sz, [i64, i64, i32]),
+        "hg_node_keys_workspace_size": (sz, [vp, i32]),
+        "hg_node_keys": (C.c_int, [vp, i32, vp, vp, sz, vp]),
         "hg_build_csr_workspace_size": (sz, [vp, vp]),
         "hg_build_csr": (C.c_int, [vp, vp, vp, vp, sz, vp]),
         "hg_layer_saved_size": (sz, [vp, vp]),
@@ -231,17 +233,18 @@ def hg_plan_size(n_nodes: int, n_edges: int, n_rel: int) -> int:
 def hg_build_csr(src, dst, rel, ntype, part, k: int, n_rel: int, n_ntype: int, budget_M: int,
                  key: int = HG_KEY_OUTDEG, theta: int = HG_THETA_NONE, seed: int = 0,
                  want_eid: bool = True, stream=None, ws: Optional[torch.Tensor] = None,
-                 out: Optional[Subgraph] = None, edge_ts=None, t_cut: int = 0) -> Subgraph:
+                 out: Optional[Subgraph] = None, edge_ts=None, t_cut: int = 0, node_key=None) -> Subgraph:
     """Overlapping-subgraph construction; inputs are device tensors
     (src/dst/part int32, rel/ntype uint8, edge_ts int32 or None).
     Synchronous.  ``out`` reuses the arrays of an earlier build of the same
     input sizes.  With edge_ts, the snapshot that keeps the induced edges with
-    edge_ts <= t_cut."""
+    edge_ts <= t_cut.  node_key: the graph's keys from hg_node_keys (same
+    key kind), or None to compute them inside the build."""
     dev = ntype.device
     n, e = int(ntype.shape[0]), int(src.shape[0])
     g = GraphDesc(n, e, n_rel, n_ntype, _ptr(src), _ptr(dst), _ptr(rel), _ptr(ntype), _ptr(part),
                   k, None, _ptr(edge_ts), int(t_cut), 0)
-    o = OverlapDesc(budget_M, key, HG_KEYDIR_OUT, theta, 0, seed)
+    o = OverlapDesc(budget_M, key, HG_KEYDIR_OUT, theta, 0, seed, _ptr(node_key))
     L = lib()
     if out is not None:
         if ws is None:
@@ -499,6 +502,28 @@ def hg_temporal_bwd(h, states, weights: dict, dH, dh=None, dstates=None, grads: 
                              _ptr(dh), dctx, int(accumulate), C.byref(G), _ptr(ws), ws.numel(), _stream(stream)),
            "hg_temporal_bwd")
     return dh, grads
+
+
+def hg_node_keys(src, dst, rel, n_nodes: int, n_rel: int, key: int = HG_KEY_OUTDEG, keys=None, ws=None,
+                 stream=None):
+    """Key of every node (out-degree or out-neighbour h-index), int32
+    [n_nodes] on the device.  Synchronous."""
+    dev = src.device
+    g = GraphDesc(n_nodes, int(src.shape[0]), n_rel, 1, _ptr(src), _ptr(dst), _ptr(rel), None, None, 0, None, None,
+                  0, 0)
+    L = lib()
+    if keys is None:
+        keys = torch.empty(n_nodes, dtype=torch.int32, device=dev)
+    if ws is None:
+        ws = _ws(int(L.hg_node_keys_workspace_size(C.byref(g), key)), dev)
+    _check(L.hg_node_keys(C.byref(g), key, _ptr(keys), _ptr(ws), ws.numel(), _stream(stream)), "hg_node_keys")
+    return keys
+
+
+def hg_node_keys_workspace_size(n_nodes: int, n_edges: int, n_rel: int, key: int = HG_KEY_OUTDEG) -> int:
+    g = GraphDesc(n_nodes, n_edges, n_rel, 1, None, C.c_void_p(8), C.c_void_p(8), None, None, 0, None, None, 0, 0)
+    g.src = C.c_void_p(8)
+    return int(lib().hg_node_keys_workspace_size(C.byref(g), key))
 
 
 def hg_mean_agg_fwd(g2l: list, h_parts: list, H=None, cnt=None, stream=None):

@@ -98,6 +98,20 @@ __global__ void k_cand_bits(const int32_t* __restrict__ first, int32_t n_edges, 
   }
 }
 
+// Membership of the subgraph's node set: base nodes and selected overlap nodes.
+__global__ void k_member_bits(const int32_t* __restrict__ part, int32_t k, const uint8_t* __restrict__ sel,
+                              int64_t n, uint32_t* __restrict__ bits) {
+  GRID_STRIDE(v0, cdiv_dev(n, 64) * 64) {
+    const bool in = v0 < n && (part[v0] == k || sel[v0]);
+    const uint64_t m = __ballot(in);
+    if ((threadIdx.x & 63) == 0) {
+      const int64_t wd = v0 >> 5;
+      bits[wd] = (uint32_t)m;
+      if ((v0 + 32) < n) bits[wd + 1] = (uint32_t)(m >> 32);
+    }
+  }
+}
+
 __device__ __forceinline__ bool bit_of(const uint32_t* __restrict__ bits, int32_t v) {
   return (bits[v >> 5] >> (v & 31)) & 1u;
 }
@@ -218,6 +232,29 @@ __global__ void __launch_bounds__(kAggBT) k_cand_outdeg(const int32_t* __restric
   GRID_STRIDE(e, n_edges) {
     const int32_t s = src[e];
     if (bit_of(cand_bits, s)) deg.put((uint32_t)s, 1, outdeg);
+  }
+  __syncthreads();
+  deg.flush(outdeg);
+}
+
+// Out-degrees of every node, with the range checks of the edge arrays.
+__global__ void __launch_bounds__(kAggBT) k_all_outdeg(const int32_t* __restrict__ src,
+                                                   const int32_t* __restrict__ dst,
+                                                   const uint8_t* __restrict__ rel, int64_t n_nodes,
+                                                   int64_t n_edges, int32_t n_rel, int32_t* __restrict__ outdeg,
+                                                   int32_t* __restrict__ cnt) {
+  __shared__ uint32_t lk[kAggSlots];
+  __shared__ int32_t lv[kAggSlots];
+  LdsAgg<false> deg{lk, lv};
+  deg.init();
+  __syncthreads();
+  GRID_STRIDE(e, n_edges) {
+    const int32_t s = src[e], d = dst[e];
+    if (s < 0 || s >= n_nodes || d < 0 || d >= n_nodes || rel[e] >= n_rel) {
+      atomicOr(&cnt[C_ERR], 1);
+      continue;
+    }
+    deg.put((uint32_t)s, 1, outdeg);
   }
   __syncthreads();
   deg.flush(outdeg);
@@ -438,13 +475,20 @@ __global__ void k_member_bits(const int32_t* __restrict__ g2l, int64_t n, uint32
   }
 }
 
+// Two ways to find the induced edges, with equal results.  Where most nodes
+// of the graph are in the subgraph, most edges stay and every edge needs its
+// endpoints' local ids: they are gathered in the first pass and the keep flag
+// follows from them.  Where the subgraph holds a smaller share of the nodes
+// (one block of a K-way partition), the first pass only tests membership in
+// a bitmap and the compaction gathers the local ids of the kept edges alone.
+
 // Local ids of both endpoints (one random gather each) and the keep flag.
 // With timestamps, an edge after the cut is dropped like an edge that leaves
 // the node set (its source id is written as -1).
-__global__ void k_edge_keep(const int32_t* __restrict__ src, const int32_t* __restrict__ dst,
-                            const int32_t* __restrict__ g2l, const int32_t* __restrict__ ts, int32_t t_cut,
-                            int64_t n_edges, int32_t* __restrict__ keep, int32_t* __restrict__ sl,
-                            int32_t* __restrict__ dl) {
+__global__ void k_edge_keep_ids(const int32_t* __restrict__ src, const int32_t* __restrict__ dst,
+                                const int32_t* __restrict__ g2l, const int32_t* __restrict__ ts, int32_t t_cut,
+                                int64_t n_edges, int32_t* __restrict__ keep, int32_t* __restrict__ sl,
+                                int32_t* __restrict__ dl) {
   GRID_STRIDE(e, n_edges) {
     int32_t s = g2l[src[e]];
     const int32_t d = g2l[dst[e]];
@@ -455,16 +499,52 @@ __global__ void k_edge_keep(const int32_t* __restrict__ src, const int32_t* __re
   }
 }
 
-// Stable compaction of the kept edges (pos = exclusive scan of keep).
-__global__ void k_edge_compact(const int32_t* __restrict__ sl, const int32_t* __restrict__ dl,
-                               const uint8_t* __restrict__ rel, const int32_t* __restrict__ pos,
-                               int64_t n_edges, int32_t n_rel, uint32_t* __restrict__ kcsr,
-                               uint32_t* __restrict__ kcsc, int32_t* __restrict__ vsrc,
-                               int32_t* __restrict__ vdst, int32_t* __restrict__ veid) {
+// Stable compaction of the kept edges from their local ids (pos = exclusive
+// scan of keep).
+__global__ void k_edge_compact_ids(const int32_t* __restrict__ sl, const int32_t* __restrict__ dl,
+                                   const uint8_t* __restrict__ rel, const int32_t* __restrict__ pos,
+                                   int64_t n_edges, int32_t n_rel, uint32_t* __restrict__ kcsr,
+                                   uint32_t* __restrict__ kcsc, int32_t* __restrict__ vsrc,
+                                   int32_t* __restrict__ vdst, int32_t* __restrict__ veid) {
   GRID_STRIDE(e, n_edges) {
     const int32_t s = sl[e], d = dl[e];
     if (s >= 0 && d >= 0) {
       const int32_t p = pos[e];
+      const uint32_t r = rel[e];
+      kcsr[p] = (uint32_t)d * (uint32_t)n_rel + r;
+      kcsc[p] = (uint32_t)s * (uint32_t)n_rel + r;
+      vsrc[p] = s;
+      vdst[p] = d;
+      veid[p] = (int32_t)e;
+    }
+  }
+}
+
+// Keep flag of every edge: both endpoints in the node set (two lookups in the
+// membership bitmap, N/8 bytes, which stays in the L2 cache).  With
+// timestamps, an edge after the cut is dropped like an edge that leaves the
+// node set.
+__global__ void k_edge_keep(const int32_t* __restrict__ src, const int32_t* __restrict__ dst,
+                            const uint32_t* __restrict__ member, const int32_t* __restrict__ ts, int32_t t_cut,
+                            int64_t n_edges, int32_t* __restrict__ keep) {
+  GRID_STRIDE(e, n_edges) {
+    const bool in = bit_of(member, src[e]) && bit_of(member, dst[e]) && !(ts && ts[e] > t_cut);
+    keep[e] = in ? 1 : 0;
+  }
+}
+
+// Stable compaction of the kept edges (pos = exclusive scan of keep,
+// pos[n_edges] = their count); the local ids of a kept edge's endpoints are
+// gathered here, so an edge that leaves the node set costs no lookup.
+__global__ void k_edge_compact(const int32_t* __restrict__ src, const int32_t* __restrict__ dst,
+                               const int32_t* __restrict__ g2l, const uint8_t* __restrict__ rel,
+                               const int32_t* __restrict__ pos, int64_t n_edges, int32_t n_rel,
+                               uint32_t* __restrict__ kcsr, uint32_t* __restrict__ kcsc, int32_t* __restrict__ vsrc,
+                               int32_t* __restrict__ vdst, int32_t* __restrict__ veid) {
+  GRID_STRIDE(e, n_edges) {
+    const int32_t p = pos[e];
+    if (pos[e + 1] != p) {
+      const int32_t s = g2l[src[e]], d = g2l[dst[e]];
       const uint32_t r = rel[e];
       kcsr[p] = (uint32_t)d * (uint32_t)n_rel + r;
       kcsc[p] = (uint32_t)s * (uint32_t)n_rel + r;
@@ -657,6 +737,88 @@ static int validate_build(const hg_graph_desc* g, const hg_overlap_desc* o) {
   return HG_OK;
 }
 
+// ---- node keys of the whole graph (the same for every partition block) ----
+
+namespace {
+
+struct KeyWs {
+  int32_t *cnt, *outdeg, *first, *hoff, *hist, *flag, *scratch;
+  template <class A>
+  void layout(A& a, int64_t N, int64_t E, bool hindex) {
+    cnt = a.template take<int32_t>(C_COUNT + 8);
+    outdeg = a.template take<int32_t>(hindex ? N : 0);
+    first = a.template take<int32_t>(hindex ? N : 0);
+    hoff = a.template take<int32_t>(hindex ? N + 1 : 0);
+    hist = a.template take<int32_t>(hindex ? E + N : 0);
+    flag = a.template take<int32_t>(hindex ? N + 1 : 0);
+    scratch = a.template take<int32_t>(hindex ? scan_scratch_elems(N + 1) : 0);
+  }
+};
+
+int validate_keys(const hg_graph_desc* g, int32_t key) {
+  if (!g) return fail(HG_ERR_ARG, "null descriptor");
+  if (g->n_nodes < 1 || g->n_nodes >= ((int64_t)1 << 31))
+    return fail(HG_ERR_ARG, "n_nodes %lld outside [1, 2^31)", (long long)g->n_nodes);
+  if (g->n_edges < 0) return fail(HG_ERR_ARG, "n_edges %lld < 0", (long long)g->n_edges);
+  if (g->n_edges + g->n_nodes >= ((int64_t)1 << 31))
+    return fail(HG_ERR_UNSUPPORTED, "n_edges + n_nodes >= 2^31");
+  if (g->n_rel < 1 || g->n_rel > HG_MAX_REL) return fail(HG_ERR_UNSUPPORTED, "n_rel %d", g->n_rel);
+  if (g->n_edges > 0 && (!g->src || !g->dst || !g->rel)) return fail(HG_ERR_ARG, "null edge array");
+  if (key != HG_KEY_OUTDEG && key != HG_KEY_HINDEX) return fail(HG_ERR_ARG, "key %d", key);
+  return HG_OK;
+}
+
+}  // namespace
+
+extern "C" size_t hg_node_keys_workspace_size(const hg_graph_desc* g, int32_t key) {
+  if (validate_keys(g, key) != HG_OK) return 0;
+  Sizer sz;
+  KeyWs w;
+  w.layout(sz, g->n_nodes, g->n_edges, key == HG_KEY_HINDEX);
+  return sz.used + 256;
+}
+
+extern "C" int hg_node_keys(const hg_graph_desc* g, int32_t key, int32_t* keys, void* ws, size_t ws_bytes,
+                            void* stream) {
+  HG_TRY(validate_keys(g, key));
+  if (!keys) return fail(HG_ERR_ARG, "null keys");
+  const size_t need = hg_node_keys_workspace_size(g, key);
+  if (!ws || ws_bytes < need) return fail(HG_ERR_CAPACITY, "workspace needs %zu bytes, got %zu", need, ws_bytes);
+  const int64_t N = g->n_nodes, E = g->n_edges;
+  const bool hindex = key == HG_KEY_HINDEX;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  Arena arena(ws, ws_bytes);
+  KeyWs w;
+  w.layout(arena, N, E, hindex);
+  if (!arena.ok()) return fail(HG_ERR_CAPACITY, "workspace layout overflow");
+  const unsigned gN = grid_for(N);
+  int32_t* deg = hindex ? w.outdeg : keys;
+  HG_TRY(fill_i32(w.cnt, 0, C_COUNT + 8, s));
+  HG_TRY(fill_i32(keys, 0, N, s));
+  if (hindex) HG_TRY(fill_i32(deg, 0, N, s));
+  if (E > 0)
+    HG_LAUNCH("keys_outdeg", k_all_outdeg, dim3(agg_grid(E)), dim3(kAggBT), 0, s, g->src, g->dst, g->rel, N, E,
+              g->n_rel, deg, w.cnt);
+  int32_t herr = 0;
+  HG_HIP_TRY(hipMemcpyAsync(&herr, w.cnt + C_ERR, sizeof(int32_t), hipMemcpyDeviceToHost, s));
+  HG_HIP_TRY(hipStreamSynchronize(s));
+  if (herr) return fail(HG_ERR_RANGE, "input ids out of range (flags 0x%x)", herr);
+  if (hindex && E > 0) {
+    // every node is treated as a candidate: first[v] = 0 < E
+    HG_TRY(fill_i32(w.first, 0, N, s));
+    HG_LAUNCH("keys_hindex_sizes", k_hindex_sizes, dim3(gN), dim3(kBT), 0, s, (const int32_t*)deg,
+              (const int32_t*)w.first, N, (int32_t)E, w.flag);
+    HG_TRY(fill_i32(w.flag + N, 0, 1, s));
+    HG_TRY(scan_exclusive_i32(w.flag, w.hoff, N + 1, nullptr, w.scratch, s));
+    HG_TRY(fill_i32(w.hist, 0, E + N, s));
+    HG_LAUNCH("keys_hindex_hist", k_hindex_hist, dim3(agg_grid(E)), dim3(kAggBT), 0, s, g->src, g->dst, E,
+              (const int32_t*)deg, (const int32_t*)w.first, (const int32_t*)w.hoff, w.hist);
+    HG_LAUNCH("keys_hindex_final", k_hindex_final, dim3(gN), dim3(kBT), 0, s, (const int32_t*)deg,
+              (const int32_t*)w.first, (const int32_t*)w.hoff, (const int32_t*)w.hist, N, (int32_t)E, keys);
+  }
+  return HG_OK;
+}
+
 extern "C" size_t hg_build_csr_workspace_size(const hg_graph_desc* g, const hg_overlap_desc* o) {
   if (validate_build(g, o) != HG_OK) return 0;
   Sizer sz;
@@ -706,8 +868,9 @@ extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg
     HG_HIP_TRY(hipStreamSynchronize(s));
     if (herr) return fail(HG_ERR_RANGE, "input ids out of range (flags 0x%x)", herr);
   }
-  // 2. keys
-  if (hindex) {
+  // 2. keys (the caller's, when given: they do not depend on k)
+  const int32_t* key = o->node_key ? o->node_key : w.key;
+  if (hindex && !o->node_key) {
     HG_LAUNCH("build_hindex_sizes", k_hindex_sizes, dim3(gN), dim3(kBT), 0, s,
               (const int32_t*)w.outdeg, (const int32_t*)w.first, N, (int32_t)E, w.flag);
     HG_TRY(fill_i32(w.flag + N, 0, 1, s));
@@ -719,7 +882,7 @@ extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg
     HG_LAUNCH("build_hindex_final", k_hindex_final, dim3(gN), dim3(kBT), 0, s,
               (const int32_t*)w.outdeg, (const int32_t*)w.first, (const int32_t*)w.hoff,
               (const int32_t*)w.hist, N, (int32_t)E, w.key);
-  } else {
+  } else if (!o->node_key) {
     HG_LAUNCH("build_cand_bits", k_cand_bits, dim3(gB), dim3(kBT), 0, s, (const int32_t*)w.first, (int32_t)E, N,
               w.cbits);
     if (E > 0)
@@ -729,10 +892,10 @@ extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg
   }
   // 3. filtered candidates, compacted in gid order
   HG_LAUNCH("build_filter_flags", k_filter_flags, dim3(gN), dim3(kBT), 0, s, (const int32_t*)w.first,
-            (const int32_t*)w.key, N, (int32_t)E, o->theta, w.flag);
+            key, N, (int32_t)E, o->theta, w.flag);
   HG_TRY(scan_exclusive_i32(w.flag, w.pos, N, w.cnt + C_CPRIME, w.scratch, s));
   HG_LAUNCH("build_compact_nodes", k_compact_nodes, dim3(gN), dim3(kBT), 0, s, (const int32_t*)w.first,
-            (const int32_t*)w.key, (const int32_t*)w.pos, N, (int32_t)E, o->theta, w.list);
+            key, (const int32_t*)w.pos, N, (int32_t)E, o->theta, w.list);
   // 4. TopM by exact radix select over the 128-bit composite
   {
     const int64_t budget = o->budget_M;
@@ -740,13 +903,13 @@ extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg
               (const int32_t*)(w.cnt + C_CPRIME), budget);
     for (int p = 0; p < 16; ++p) {
       HG_LAUNCH("build_select_hist", k_select_hist, dim3(grid_for(N, 2048)), dim3(256), 0, s, w.st,
-                (const int32_t*)w.list, (const int32_t*)(w.cnt + C_CPRIME), (const int32_t*)w.key,
+                (const int32_t*)w.list, (const int32_t*)(w.cnt + C_CPRIME), key,
                 o->seed);
       HG_LAUNCH("build_select_pick", k_select_pick, dim3(1), dim3(256), 0, s, w.st);
     }
     HG_LAUNCH("build_select_mark", k_select_mark, dim3(grid_for(N, 2048)), dim3(256), 0, s,
               (const SelectState*)w.st, (const int32_t*)w.list, (const int32_t*)(w.cnt + C_CPRIME),
-              (const int32_t*)w.key, o->seed, w.sel);
+              key, o->seed, w.sel);
   }
   // 5. local ids in (ntype, gid) order
   HG_LAUNCH("build_member_digit", k_member_digit, dim3(gN), dim3(kBT), 0, s, g->part, g->k,
@@ -767,13 +930,29 @@ extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg
               out->overlap_home, out->overlap_rel);
   // 6. induced-subgraph edges in original order
   if (E > 0) {
-    // local ids land in the sort's ping-pong buffers (free until the sorts)
-    HG_LAUNCH("build_edge_keep", k_edge_keep, dim3(gE), dim3(kBT), 0, s, g->src, g->dst,
-              (const int32_t*)out->global2local, g->edge_ts, g->t_cut, E, w.keep, w.alt1, w.alt2);
-    HG_TRY(scan_exclusive_i32(w.keep, w.keep, E, w.cnt + C_ESUB, w.scratch, s));
-    HG_LAUNCH("build_edge_compact", k_edge_compact, dim3(gE), dim3(kBT), 0, s, (const int32_t*)w.alt1,
-              (const int32_t*)w.alt2, g->rel, (const int32_t*)w.keep, E, (int32_t)R, w.kcsr, w.kcsc, w.vsrc,
-              w.vdst, w.veid);
+    int32_t ns_host = 0;
+    HG_HIP_TRY(hipMemcpyAsync(&ns_host, w.cnt + C_NSUB, sizeof(int32_t), hipMemcpyDeviceToHost, s));
+    HG_HIP_TRY(hipStreamSynchronize(s));
+    if (4 * (int64_t)ns_host >= 3 * N) {
+      // local ids land in the sort's ping-pong buffers (free until the sorts)
+      HG_LAUNCH("build_edge_keep", k_edge_keep_ids, dim3(gE), dim3(kBT), 0, s, g->src, g->dst,
+                (const int32_t*)out->global2local, g->edge_ts, g->t_cut, E, w.keep, w.alt1, w.alt2);
+      HG_TRY(scan_exclusive_i32(w.keep, w.keep, E, w.cnt + C_ESUB, w.scratch, s));
+      HG_LAUNCH("build_edge_compact", k_edge_compact_ids, dim3(gE), dim3(kBT), 0, s, (const int32_t*)w.alt1,
+                (const int32_t*)w.alt2, g->rel, (const int32_t*)w.keep, E, (int32_t)R, w.kcsr, w.kcsc, w.vsrc,
+                w.vdst, w.veid);
+    } else {
+      HG_LAUNCH("build_member_bits", k_member_bits, dim3(gB), dim3(kBT), 0, s, g->part, g->k,
+                (const uint8_t*)w.sel, N, w.mbits);
+      HG_LAUNCH("build_edge_keep", k_edge_keep, dim3(gE), dim3(kBT), 0, s, g->src, g->dst,
+                (const uint32_t*)w.mbits, g->edge_ts, g->t_cut, E, w.keep);
+      // keep[E] = 0, so the scan's entry E is the number of kept edges
+      HG_TRY(fill_i32(w.keep + E, 0, 1, s));
+      HG_TRY(scan_exclusive_i32(w.keep, w.keep, E + 1, w.cnt + C_ESUB, w.scratch, s));
+      HG_LAUNCH("build_edge_compact", k_edge_compact, dim3(gE), dim3(kBT), 0, s, g->src, g->dst,
+                (const int32_t*)out->global2local, g->rel, (const int32_t*)w.keep, E, (int32_t)R, w.kcsr, w.kcsc,
+                w.vsrc, w.vdst, w.veid);
+    }
   } else {
     HG_TRY(fill_i32(w.cnt + C_ESUB, 0, 1, s));
   }

@@ -365,6 +365,8 @@ class KwayInputs:
     part_np: np.ndarray
     subs: List[api.Subgraph]    # subgraph k of partition block k
     build_ws: torch.Tensor      # shared by the K builds (each keeps its own outputs)
+    keys: torch.Tensor          # selection key of every node, computed once for the K builds
+    keys_ws: torch.Tensor
     weights: List[tuple]        # per layer (w_rel, w_self, bias), shared by the K workers
     weights_np: list
     head: dict
@@ -397,12 +399,12 @@ class KwayInputs:
         return sum(s.e_sub for s in self.subs)
 
 
-def _build_parts(gd, cfg, K, ws=None, subs=None):
+def _build_parts(gd, cfg, K, keys, ws=None, subs=None):
     out = []
     for k in range(K):
         sub = api.hg_build_csr(gd["src"], gd["dst"], gd["rel"], gd["ntype"], gd["part"], k, cfg.n_rel, 2,
                                cfg.budget, key=cfg.key, theta=cfg.theta, seed=cfg.seed, want_eid=False, ws=ws,
-                               out=None if subs is None else subs[k])
+                               out=None if subs is None else subs[k], node_key=keys)
         if ws is None:
             ws = sub.arrays["ws"]
         out.append(sub)
@@ -417,7 +419,9 @@ def make_kway_inputs(wl: synth.Workload, g: synth.Graph, device="cuda") -> KwayI
     part_np = synth.random_partition(g.n_nodes, K, mc.seed)
     gd = {k: _dev(getattr(g, k), device) for k in ("src", "dst", "rel", "ntype")}
     gd["part"] = _dev(part_np, device)
-    subs, build_ws = _build_parts(gd, cfg, K)
+    keys_ws = api._ws(api.hg_node_keys_workspace_size(g.n_nodes, g.n_edges, cfg.n_rel, cfg.key), device)
+    keys = api.hg_node_keys(gd["src"], gd["dst"], gd["rel"], g.n_nodes, cfg.n_rel, cfg.key, ws=keys_ws)
+    subs, build_ws = _build_parts(gd, cfg, K, keys)
     feats = synth.features(mc.seed, g.n_nodes, d)
     feats_d = _dev(feats, device)
     weights_np = [synth.layer_weights(mc.seed, li, cfg.n_rel, g.n_ntype, d, mc.bias_range)
@@ -426,7 +430,7 @@ def make_kway_inputs(wl: synth.Workload, g: synth.Graph, device="cuda") -> KwayI
     head_np = synth.head_weights(mc.seed, d)
     head = {k: _dev(v, device) for k, v in head_np.items()}
     labels_np = synth.labels(mc.seed, g.ntype)
-    inp = KwayInputs(wl, gd, part_np, subs, build_ws, weights, weights_np, head, head_np,
+    inp = KwayInputs(wl, gd, part_np, subs, build_ws, keys, keys_ws, weights, weights_np, head, head_np,
                      _dev(labels_np, device), labels_np, feats)
     f32 = dict(dtype=torch.float32, device=device)
     for sb in subs:
@@ -468,11 +472,16 @@ def run_kway_step(inp: KwayInputs, rebuild: bool = True, update: bool = True):
     home copies (held constant) through the CCA loss; each worker's backward
     starts from the MeanAgg backward of dL_BCE/dH plus its alignment
     gradient; the shared weights collect the sum of the K workers' gradients
-    (what the gradient all-reduce forms); then Adam updates every parameter."""
+    (what the gradient all-reduce forms); then Adam updates every parameter.
+    The node keys of the selection do not depend on the partition block: they
+    are computed once and shared by the K builds."""
     cfg, mc = inp.wl.graph, inp.wl.model
     K = len(inp.subs)
     if rebuild:
-        _build_parts(inp.graph, cfg, K, ws=inp.build_ws, subs=inp.subs)
+        gd = inp.graph
+        api.hg_node_keys(gd["src"], gd["dst"], gd["rel"], int(gd["ntype"].shape[0]), cfg.n_rel, cfg.key,
+                         keys=inp.keys, ws=inp.keys_ws)
+        _build_parts(gd, cfg, K, inp.keys, ws=inp.build_ws, subs=inp.subs)
     for k, sb in enumerate(inp.subs):
         for li in range(mc.n_layers):
             w_rel, w_self, bias = inp.weights[li]

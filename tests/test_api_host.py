@@ -264,3 +264,15 @@ def test_kway_calls_reject_bad_arguments(L):
     assert L.hg_mean_agg_fwd(0, 64, 0, 1, arr, arr, None, None, None) == api.HG_OK
     assert L.hg_mean_agg_bwd(0, 64, 0, None, None, None, None, 0, None) == api.HG_OK
     assert L.hg_home_gather(0, 64, 0, 1, None, None, None, arr, arr, None, None) == api.HG_OK
+
+
+def test_node_keys_reject_bad_arguments(L):
+    fake = C.c_void_p(0x1000)
+    g = api.GraphDesc(10, 5, 2, 1, fake, fake, fake, None, None, 0, None, None, 0, 0)
+    assert L.hg_node_keys(C.byref(g), 2, fake, fake, 1 << 20, None) == api.HG_ERR_ARG      # key kind
+    assert L.hg_node_keys(C.byref(g), 0, None, fake, 1 << 20, None) == api.HG_ERR_ARG      # no output
+    assert L.hg_node_keys(C.byref(g), 0, fake, fake, 1, None) == api.HG_ERR_CAPACITY       # workspace
+    assert L.hg_node_keys(None, 0, fake, fake, 1 << 20, None) == api.HG_ERR_ARG
+    big = api.GraphDesc(1 << 30, (1 << 31) - 1, 2, 1, fake, fake, fake, None, None, 0, None, None, 0, 0)
+    assert L.hg_node_keys_workspace_size(C.byref(big), 0) == 0
+    assert L.hg_node_keys_workspace_size(C.byref(g), 1) > L.hg_node_keys_workspace_size(C.byref(g), 0)

@@ -119,13 +119,18 @@ SNAPSHOT_CASES = {
 
 
 @pytest.mark.parametrize("case", sorted(SNAPSHOT_CASES))
-def test_snapshot_build_bit_exact(case):
+@pytest.mark.parametrize("parts", [0, 3])
+def test_snapshot_build_bit_exact(case, parts):
     """Each snapshot (edges with timestamp <= cut, node set from every edge)
     matches the oracle's snapshot bit for bit, for every monthly cut plus a
-    cut before the first day (no edges) and one inside a month."""
+    cut before the first day (no edges) and one inside a month; with the
+    configuration's base set (most nodes in the subgraph) and with block 0 of
+    a random 3-way partition (a third of them: the membership-bitmap path)."""
     cfg, key, theta, budget = SNAPSHOT_CASES[case]
     budget = cfg.budget if budget is None else budget
     g = synth.make_graph(cfg)
+    if parts:
+        g.part = synth.random_partition(g.n_nodes, parts, 11)
     ts = synth.edge_times(cfg.seed, g.n_edges)
     d = graph_to_dev(g)
     ts_d = torch.from_numpy(ts).cuda()
@@ -140,3 +145,45 @@ def test_snapshot_build_bit_exact(case):
         assert_same(ref, sub)
     assert sub.e_sub == select.build(g.src, g.dst, g.rel, g.ntype, g.part, g.k, cfg.n_rel, 2, budget, key, theta,
                                      99).e_sub
+
+
+@pytest.mark.parametrize("case", ["tiny", "tiny_hindex_theta2", "skew_small_theta3", "medium_small"])
+def test_node_keys_bit_exact(case):
+    cfg, key, _, _ = CASES[case]
+    g = synth.make_graph(cfg)
+    d = graph_to_dev(g)
+    got = api.hg_node_keys(d["src"], d["dst"], d["rel"], g.n_nodes, cfg.n_rel, key).cpu().numpy()
+    assert np.array_equal(got, select.node_keys(g.n_nodes, g.src, g.dst, key))
+
+
+@pytest.mark.parametrize("case", sorted(CASES))
+def test_build_with_given_keys_bit_exact(case):
+    # the keys of the whole graph given to the build (shared by the builds
+    # of several blocks) change none of its outputs; a random 3-way
+    # partition, block 1
+    cfg, key, theta, budget = CASES[case]
+    g = synth.make_graph(cfg)
+    budget = cfg.budget if budget is None else budget
+    part = synth.random_partition(g.n_nodes, 3, 5)
+    ref = select.build(g.src, g.dst, g.rel, g.ntype, part, 1, cfg.n_rel, 2, budget, key, theta, 77)
+    d = graph_to_dev(g)
+    d["part"] = torch.from_numpy(part).cuda()
+    keys = api.hg_node_keys(d["src"], d["dst"], d["rel"], g.n_nodes, cfg.n_rel, key)
+    sub = api.hg_build_csr(d["src"], d["dst"], d["rel"], d["ntype"], d["part"], 1, cfg.n_rel, 2, budget, key=key,
+                           theta=theta, seed=77, node_key=keys)
+    assert_same(ref, sub)
+
+
+def test_node_keys_range_error_and_empty():
+    n = 50
+    src = torch.tensor([0, 3, n], dtype=torch.int32, device="cuda")
+    dst = torch.tensor([1, 2, 4], dtype=torch.int32, device="cuda")
+    rel = torch.zeros(3, dtype=torch.uint8, device="cuda")
+    for key in (0, 1):
+        with pytest.raises(api.HgError) as e:
+            api.hg_node_keys(src, dst, rel, n, 1, key)
+        assert e.value.status == api.HG_ERR_RANGE
+    empty = torch.zeros(0, dtype=torch.int32, device="cuda")
+    for key in (0, 1):
+        got = api.hg_node_keys(empty, empty, empty.to(torch.uint8), n, 1, key).cpu().numpy()
+        assert np.all(got == 0)
