@@ -293,17 +293,20 @@ int hg_hgt_bwd(const hg_subgraph* s, const hg_hgt_desc* L, const void* H_in, con
  *   divisor M - ddof; Xh = (X - mu) / (sigma sqrt(M)), same for Y;
  *   L_inv = sum_b w_b ||Xh_b - Yh_b||^2 (w = 1 if NULL),
  *   L_dec = ||Xh^T Xh - I||_F^2 + ||Yh^T Yh - I||_F^2,  L = L_inv + lambda_n L_dec.
- * Writes loss3[0..2] = (L_inv, L_dec, L) (device float32) and ADDS
- * scale * dL/dX into rows overlap[b] of dH (scale = lambda_CCA).  If dH_ref is
- * not NULL it is OVERWRITTEN with scale * dL/dY.  H, dH: [n_rows, d];
- * H_ref, dH_ref: [M, d]; overlap entries distinct and in [0, n_rows).
+ * Writes loss3[0..2] = (L_inv, L_dec, L) (device float32) and writes
+ * rows overlap[b] of dH as base[overlap[b]] + scale * dL/dX (scale =
+ * lambda_CCA), base = dH_base when it is not NULL (then the other rows of
+ * dH are untouched and dH_base is only read), else dH itself (the gradient
+ * is ADDED into dH).  If dH_ref is not NULL it is OVERWRITTEN with
+ * scale * dL/dY.  H, dH, dH_base: [n_rows, d]; H_ref, dH_ref: [M, d];
+ * overlap entries distinct and in [0, n_rows).
  * M = 0 writes zeros.  Requires M > ddof, d in {64, 128, 256}.  dtype is
  * the storage type of H, H_ref, dH and dH_ref (float32 or bfloat16). */
 size_t hg_align_workspace_size(int64_t M, int32_t d);
 int hg_align_loss_fwd_bwd(int64_t M, int32_t d, int32_t dtype, int64_t n_rows,
                           const void* H, const int32_t* overlap, const void* H_ref,
                           const float* w, float lambda_n, float scale, float eps,
-                          int32_t ddof, float* loss3, void* dH, void* dH_ref,
+                          int32_t ddof, float* loss3, void* dH, const void* dH_base, void* dH_ref,
                           void* ws, size_t ws_bytes, void* stream);
 
 /* ---- prediction head, masked BCE and Adam ("Prediction and Optimization":

@@ -132,7 +132,7 @@ def lib() -> C.CDLL:
         "hg_hgt_bwd": (C.c_int, [vp, vp, vp, vp, vp, vp, vp, vp, vp, i32, vp, sz, vp]),
         "hg_align_workspace_size": (sz, [i64, i32]),
         "hg_align_loss_fwd_bwd": (C.c_int, [i64, i32, i32, i64, vp, vp, vp, vp, f32, f32, f32,
-                                            i32, vp, vp, vp, vp, sz, vp]),
+                                            i32, vp, vp, vp, vp, vp, sz, vp]),
         "hg_mlp_bce_workspace_size": (sz, [i64, i32, i32]),
         "hg_mlp_bce_fwd_bwd": (C.c_int, [i64, i32, i32] + [vp] * 14 + [sz, vp]),
         "hg_adam_step": (C.c_int, [i64, vp, vp, vp, vp, i64, f32, f32, f32, f32, f32, vp]),
@@ -567,9 +567,10 @@ def hg_align_workspace_size(M: int, d: int) -> int:
 
 
 def hg_align_loss_fwd_bwd(H, overlap, H_ref, dH, w=None, lambda_n=2e-4, scale=0.1, eps=1e-5,
-                          ddof=0, dH_ref=None, loss3=None, ws=None, stream=None):
+                          ddof=0, dH_ref=None, loss3=None, ws=None, stream=None, dH_base=None):
     """CCA alignment: returns loss3 (device float32 [3] = L_inv, L_dec, L);
-    adds scale * dL/dX into dH[overlap] and overwrites dH_ref if given."""
+    dH[overlap] = dH_base[overlap] + scale * dL/dX (dH_base = dH when None:
+    the gradient is added into dH) and overwrites dH_ref if given."""
     M = int(overlap.shape[0])
     d = int(H.shape[1])
     L = lib()
@@ -579,7 +580,7 @@ def hg_align_loss_fwd_bwd(H, overlap, H_ref, dH, w=None, lambda_n=2e-4, scale=0.
     if ws is None:
         ws = _ws(int(L.hg_align_workspace_size(M, d)), H.device)
     _check(L.hg_align_loss_fwd_bwd(M, d, code, int(H.shape[0]), _ptr(H), _ptr(overlap), _ptr(H_ref),
-                                   _ptr(w), lambda_n, scale, eps, ddof, _ptr(loss3), _ptr(dH),
+                                   _ptr(w), lambda_n, scale, eps, ddof, _ptr(loss3), _ptr(dH), _ptr(dH_base),
                                    _ptr(dH_ref), _ptr(ws), ws.numel(), _stream(stream)),
            "hg_align_loss_fwd_bwd")
     return loss3

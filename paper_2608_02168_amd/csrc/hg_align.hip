@@ -167,12 +167,13 @@ struct GradEpi {
   }
 };
 
-// dX = (1/sigma)(g' - S1/M - xt * S2/(M - ddof)); dst[row] (+)= scale * dX.
+// dX = (1/sigma)(g' - S1/M - xt * S2/(M - ddof)); dst[row] = scale * dX,
+// plus base[row] when accumulate (base may be dst itself).
 template <int D, class T>
 __global__ void k_std_backward(int64_t m, const float* __restrict__ G, float inv_sqrt_m, LoadStd<D, T> xt,
                                const float* __restrict__ inv_sig, const float* __restrict__ S1,
-                               const float* __restrict__ S2, int32_t ddof, float scale,
-                               T* __restrict__ dst, RowMap dmap, int accumulate) {
+                               const float* __restrict__ S2, int32_t ddof, float scale, const T* base,
+                               T* dst, RowMap dmap, int accumulate) {
   const int64_t total = m * D;
   const float inv_m = 1.0f / (float)m;
   const float inv_md = 1.0f / (float)(m - ddof);
@@ -183,7 +184,7 @@ __global__ void k_std_backward(int64_t m, const float* __restrict__ G, float inv
     const float g = G[e] * inv_sqrt_m;
     const float dx = inv_sig[c] * (g - S1[c] * inv_m - xt.at(b, c) * S2[c] * inv_md);
     const int64_t o = dmap(b) * D + c;
-    const float v = (accumulate ? Elt<T>::get(dst + o) : 0.f) + scale * dx;
+    const float v = (accumulate ? Elt<T>::get(base + o) : 0.f) + scale * dx;
     if constexpr (sizeof(T) == 4) {
       dst[o] = v;
     } else {
@@ -236,8 +237,8 @@ int grad_gemm(int64_t m, const float* W, ALoad la, Epi ep, hipStream_t s) {
 
 template <int D, class T>
 int align_impl(int64_t m, const T* H, const int32_t* overlap, const T* Href, const float* w, float lambda_n,
-               float scale, float eps, int32_t ddof, float* loss3, T* dH, T* dHref, void* ws, size_t ws_bytes,
-               hipStream_t s) {
+               float scale, float eps, int32_t ddof, float* loss3, T* dH, const T* dHbase, T* dHref, void* ws,
+               size_t ws_bytes, hipStream_t s) {
   Arena a(ws, ws_bytes);
   AlignWs<D> q;
   q.layout(a, m, align_chunks(m));
@@ -271,8 +272,8 @@ int align_impl(int64_t m, const T* H, const int32_t* overlap, const T* Href, con
     HG_TRY((colsum<D>("align_grad_stats", m, FGrad<D>{q.gx, inv_sqrt_m}, q.cpart, q.s1, s)));
     HG_TRY((colsum<D>("align_grad_stats", m, FGradX<D, T>{q.gx, inv_sqrt_m, xt}, q.cpart, q.s2, s)));
     HG_LAUNCH("align_std_backward", (k_std_backward<D, T>), dim3(ge), dim3(256), 0, s, m, (const float*)q.gx,
-              inv_sqrt_m, xt, (const float*)q.isx, (const float*)q.s1, (const float*)q.s2, ddof, scale, dH,
-              mx, 1);
+              inv_sqrt_m, xt, (const float*)q.isx, (const float*)q.s1, (const float*)q.s2, ddof, scale,
+              dHbase ? dHbase : (const T*)dH, dH, mx, 1);
   }
   if (dHref) {
     GradEpi<D, T> ep{q.gx, yh, xh, w, 4.0f * lambda_n, 2.0f};
@@ -282,7 +283,7 @@ int align_impl(int64_t m, const T* H, const int32_t* overlap, const T* Href, con
     HG_TRY((colsum<D>("align_grad_stats", m, FGradX<D, T>{q.gx, inv_sqrt_m, yt}, q.cpart, q.s2, s)));
     HG_LAUNCH("align_std_backward", (k_std_backward<D, T>), dim3(ge), dim3(256), 0, s, m, (const float*)q.gx,
               inv_sqrt_m, yt, (const float*)q.isy, (const float*)q.s1, (const float*)q.s2, ddof, scale,
-              dHref, my, 0);
+              (const T*)dHref, dHref, my, 0);
   }
   return HG_OK;
 }
@@ -314,7 +315,8 @@ extern "C" size_t hg_align_workspace_size(int64_t M, int32_t d) {
 extern "C" int hg_align_loss_fwd_bwd(int64_t M, int32_t d, int32_t dtype, int64_t n_rows, const void* H,
                                      const int32_t* overlap, const void* H_ref, const float* w,
                                      float lambda_n, float scale, float eps, int32_t ddof, float* loss3,
-                                     void* dH, void* dH_ref, void* ws, size_t ws_bytes, void* stream) {
+                                     void* dH, const void* dH_base, void* dH_ref, void* ws, size_t ws_bytes,
+                                     void* stream) {
   if (M < 0 || n_rows < 0) return fail(HG_ERR_ARG, "negative size");
   if (!loss3) return fail(HG_ERR_ARG, "null loss3");
   if (dtype != HG_DTYPE_F32 && dtype != HG_DTYPE_BF16) return fail(HG_ERR_ARG, "dtype %d", dtype);
@@ -330,13 +332,15 @@ extern "C" int hg_align_loss_fwd_bwd(int64_t M, int32_t d, int32_t dtype, int64_
   if (dtype == HG_DTYPE_BF16) {
     const bf16_t *h = (const bf16_t*)H, *r = (const bf16_t*)H_ref;
     bf16_t *dh = (bf16_t*)dH, *dr = (bf16_t*)dH_ref;
-    if (d == 64) return align_impl<64, bf16_t>(M, h, overlap, r, w, lambda_n, scale, eps, ddof, loss3, dh, dr, ws, ws_bytes, s);
-    if (d == 128) return align_impl<128, bf16_t>(M, h, overlap, r, w, lambda_n, scale, eps, ddof, loss3, dh, dr, ws, ws_bytes, s);
-    return align_impl<256, bf16_t>(M, h, overlap, r, w, lambda_n, scale, eps, ddof, loss3, dh, dr, ws, ws_bytes, s);
+    const bf16_t* db = (const bf16_t*)dH_base;
+    if (d == 64) return align_impl<64, bf16_t>(M, h, overlap, r, w, lambda_n, scale, eps, ddof, loss3, dh, db, dr, ws, ws_bytes, s);
+    if (d == 128) return align_impl<128, bf16_t>(M, h, overlap, r, w, lambda_n, scale, eps, ddof, loss3, dh, db, dr, ws, ws_bytes, s);
+    return align_impl<256, bf16_t>(M, h, overlap, r, w, lambda_n, scale, eps, ddof, loss3, dh, db, dr, ws, ws_bytes, s);
   }
   const float *h = (const float*)H, *r = (const float*)H_ref;
   float *dh = (float*)dH, *dr = (float*)dH_ref;
-  if (d == 64) return align_impl<64, float>(M, h, overlap, r, w, lambda_n, scale, eps, ddof, loss3, dh, dr, ws, ws_bytes, s);
-  if (d == 128) return align_impl<128, float>(M, h, overlap, r, w, lambda_n, scale, eps, ddof, loss3, dh, dr, ws, ws_bytes, s);
-  return align_impl<256, float>(M, h, overlap, r, w, lambda_n, scale, eps, ddof, loss3, dh, dr, ws, ws_bytes, s);
+  const float* db = (const float*)dH_base;
+  if (d == 64) return align_impl<64, float>(M, h, overlap, r, w, lambda_n, scale, eps, ddof, loss3, dh, db, dr, ws, ws_bytes, s);
+  if (d == 128) return align_impl<128, float>(M, h, overlap, r, w, lambda_n, scale, eps, ddof, loss3, dh, db, dr, ws, ws_bytes, s);
+  return align_impl<256, float>(M, h, overlap, r, w, lambda_n, scale, eps, ddof, loss3, dh, db, dr, ws, ws_bytes, s);
 }

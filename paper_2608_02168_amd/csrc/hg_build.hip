@@ -860,7 +860,8 @@ extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg
   HG_LAUNCH("build_base_bits", k_base_bits, dim3(gB), dim3(kBT), 0, s, g->part, g->k, N, w.bbits);
   if (E > 0)
     HG_LAUNCH("build_edges_pass", k_edges_pass, dim3(agg_grid(E)), dim3(kAggBT), 0, s, g->src, g->dst, g->rel,
-              (const uint32_t*)w.bbits, N, E, (int32_t)R, hindex ? 1 : 0, w.outdeg, w.first, w.cnt);
+              (const uint32_t*)w.bbits, N, E, (int32_t)R, (hindex && !o->node_key) ? 1 : 0, w.outdeg, w.first,
+              w.cnt);
   HG_LAUNCH("build_check_ntype", k_check_ntype, dim3(gN), dim3(kBT), 0, s, g->ntype, N, (int32_t)T, w.cnt);
   {
     int32_t herr = 0;
@@ -969,8 +970,9 @@ extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg
     int32_t *v1o, *v2o;
     const bool want_eid = out->csr_eid != nullptr;
     HG_TRY(radix_sort_pairs(w.kcsr, w.kalt, w.vsrc, w.alt1, want_eid ? w.veid : nullptr,
-                            want_eid ? w.alt2 : nullptr, ES, bits, w.scratch, s, &ko, &v1o, &v2o));
-    if (ES > 0) {
+                            want_eid ? w.alt2 : nullptr, ES, bits, w.scratch, s, &ko, &v1o, &v2o, out->csr_col,
+                            want_eid ? out->csr_eid : nullptr));
+    if (ES > 0 && v1o != out->csr_col) {  // no pass ran (a single key value)
       HG_HIP_TRY(hipMemcpyAsync(out->csr_col, v1o, sizeof(int32_t) * ES, hipMemcpyDeviceToDevice, s));
       if (want_eid)
         HG_HIP_TRY(hipMemcpyAsync(out->csr_eid, v2o, sizeof(int32_t) * ES, hipMemcpyDeviceToDevice, s));
@@ -985,8 +987,8 @@ extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg
     uint32_t* ko;
     int32_t *v1o, *v2o;
     HG_TRY(radix_sort_pairs(w.kcsc, w.kalt, w.vdst, w.alt3, nullptr, nullptr, ES, bits, w.scratch, s,
-                            &ko, &v1o, &v2o));
-    if (ES > 0)
+                            &ko, &v1o, &v2o, out->csc_row, nullptr));
+    if (ES > 0 && v1o != out->csc_row)
       HG_HIP_TRY(hipMemcpyAsync(out->csc_row, v1o, sizeof(int32_t) * ES, hipMemcpyDeviceToDevice, s));
     HG_TRY(fill_i32(w.rowcnt, 0, NQ + 1, s));
     if (ES > 0)

@@ -277,7 +277,8 @@ int64_t radix_scratch_elems(int64_t n) {
 
 int radix_sort_pairs(uint32_t* keys, uint32_t* keys_alt, int32_t* v1, int32_t* v1_alt,
                      int32_t* v2, int32_t* v2_alt, int64_t n, int bits, int32_t* scratch,
-                     hipStream_t s, uint32_t** keys_out, int32_t** v1_out, int32_t** v2_out) {
+                     hipStream_t s, uint32_t** keys_out, int32_t** v1_out, int32_t** v2_out,
+                     int32_t* v1_final, int32_t* v2_final) {
   *keys_out = keys;
   *v1_out = v1;
   if (v2_out) *v2_out = v2;
@@ -290,6 +291,11 @@ int radix_sort_pairs(uint32_t* keys, uint32_t* keys_alt, int32_t* v1, int32_t* v
   for (int shift = 0; shift < bits; shift += 8) {
     const int nb = (bits - shift) < 8 ? (bits - shift) : 8;
     const uint32_t dmask = (1u << nb) - 1u;
+    // the last pass writes the values straight into their final arrays
+    if (shift + 8 >= bits) {
+      if (v1_final) b1 = v1_final;
+      if (v2_final && v2) b2 = v2_final;
+    }
     HG_LAUNCH("radix_upsweep", (k_radix_upsweep<false>), dim3((unsigned)tiles), dim3(kThreads), 0, s,
               (const uint32_t*)ka, (const uint8_t*)nullptr, n, shift, dmask, hist, tiles);
     HG_TRY(scan_exclusive_i32(hist, hist, 256 * tiles, hist + 256 * tiles, sscr, s));

@@ -35,8 +35,7 @@ class StepInputs:
     H: List[torch.Tensor] = field(default_factory=list)
     saved: List[torch.Tensor] = field(default_factory=list)
     dH: List[torch.Tensor] = field(default_factory=list)
-    g: Optional[torch.Tensor] = None        # upstream gradient of the last layer (the alignment adds into it)
-    gext_ovl: Optional[torch.Tensor] = None  # G_ext rows of the overlap nodes
+    g: Optional[torch.Tensor] = None        # upstream gradient of the last layer (G_ext + the alignment's)
     grads: List[tuple] = field(default_factory=list)
     fwd_ws: Optional[torch.Tensor] = None
     bwd_ws: Optional[torch.Tensor] = None
@@ -108,10 +107,9 @@ def make_inputs(wl: synth.Workload, g: synth.Graph, device="cuda", feats: Option
     inp.saved = [torch.empty((max(ns, 1), d // 32), dtype=torch.int32, device=device)
                  for _ in range(mc.n_layers)]
     inp.dH = [torch.empty((ns, d), **act) for _ in range(2)]
-    # g holds G_ext outside the overlap rows for good; a step only has to
-    # restore the overlap rows the previous step's alignment added into
+    # g holds G_ext outside the overlap rows for good; every step's alignment
+    # writes its overlap rows as G_ext + its gradient
     inp.g = inp.gext.clone() if mc.objective != "bce" else torch.empty((ns, d), **act)
-    inp.gext_ovl = inp.gext.index_select(0, sub.view("overlap").long()).contiguous()
     if mc.kind == "hgt":
         inp.grads = [{n: torch.empty_like(v) for n, v in w.items()} for w in weights]
         inp.hgt_saved = [api._ws(api.hg_hgt_saved_size(sub, d, mc.heads), device) for _ in range(mc.n_layers)]
@@ -162,15 +160,16 @@ def run_step(inp: StepInputs, rebuild: bool = True) -> StepResult:
                          ws=inp.fwd_ws)
     g = inp.g
     overlap = sub.view("overlap")
+    base = None
     if mc.objective == "bce":
         # dL_BCE/dH of the prediction head on the labelled rows (overwrites g)
         api.hg_mlp_bce_fwd_bwd(inp.H[-1], inp.head["W1"], inp.head["b1"], inp.head["W2"], inp.head["b2"],
                                inp.labels, dH=g, grads=inp.head_grads, loss=inp.loss_bce, ws=inp.head_ws)
     else:
-        g.index_copy_(0, overlap.long(), inp.gext_ovl)
+        base = inp.gext
     api.hg_align_loss_fwd_bwd(inp.H[-1], overlap, inp.href, g, w=inp.omega, lambda_n=mc.lambda_n,
                               scale=mc.lambda_cca, eps=mc.eps, ddof=mc.ddof, loss3=inp.loss,
-                              ws=inp.align_ws)
+                              ws=inp.align_ws, dH_base=base)
     gin, nxt = g, 0
     for li in reversed(range(mc.n_layers)):
         if hgt:

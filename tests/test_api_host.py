@@ -166,7 +166,7 @@ def test_layer_workspace_sizes_scale_with_graph(L):
 def test_align_validation(L, args, code):
     fake = C.c_void_p(0x1000)
     a = dict(M=5, d=64, dtype=0, n_rows=10, H=fake, overlap=fake, H_ref=fake, w=None, lambda_n=2e-4,
-             scale=0.1, eps=1e-5, ddof=0, loss3=fake, dH=fake, dH_ref=None, ws=fake, ws_bytes=1 << 20,
+             scale=0.1, eps=1e-5, ddof=0, loss3=fake, dH=fake, dH_base=None, dH_ref=None, ws=fake, ws_bytes=1 << 20,
              stream=None)
     a.update(args)
     assert L.hg_align_loss_fwd_bwd(*a.values()) == code

@@ -70,3 +70,22 @@ def test_align_deterministic():
         loss = api.hg_align_loss_fwd_bwd(to_dev(H), to_dev(ov), to_dev(Href), dH)
         outs.append((loss.cpu(), dH.cpu()))
     assert torch.equal(outs[0][0], outs[1][0]) and torch.equal(outs[0][1], outs[1][1])
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_align_with_base_rows(dtype):
+    # dH[overlap] = base[overlap] + scale dX; every other row of dH untouched
+    # and base only read -- equal, bit for bit, to adding into a copy of base
+    H, ov, Href = make(6000, 1500, 128, seed=21)
+    G0 = synth.upstream_grad(4, H.shape[0], 128)
+    junk = np.full_like(G0, 7.0)
+    base = to_dev(G0).to(dtype)
+    dH = to_dev(junk).to(dtype)
+    api.hg_align_loss_fwd_bwd(to_dev(H).to(dtype), to_dev(ov), to_dev(Href).to(dtype), dH, dH_base=base)
+    ref = to_dev(G0).to(dtype)
+    api.hg_align_loss_fwd_bwd(to_dev(H).to(dtype), to_dev(ov), to_dev(Href).to(dtype), ref)
+    got, want = dH.float().cpu().numpy(), ref.float().cpu().numpy()
+    assert np.array_equal(got[ov], want[ov])
+    rest = np.setdiff1d(np.arange(H.shape[0]), ov)
+    assert np.all(got[rest] == 7.0)
+    assert torch.equal(base, to_dev(G0).to(dtype))
