@@ -321,12 +321,18 @@ int hg_align_loss_fwd_bwd(int64_t M, int32_t d, int32_t dtype, int64_t n_rows,
  * the weight gradients (db1, db2 may be NULL).  The joint objective adds
  * lambda_CCA * dL_CCA/dH with hg_align_loss_fwd_bwd into the same dH.
  * Requires d_hidden == d in {64, 128}; H, labels, dH may be NULL when
- * n_rows = 0.  Deterministic (fixed reduction order). */
+ * n_rows = 0.  Deterministic (fixed reduction order).
+ * rows (may be NULL): int32 [n_list] distinct row indices in [0, n_rows)
+ * that include every row with labels >= 0 (the labelled users, computed
+ * once by the caller).  Only the listed rows go through the head -- the
+ * loss and the gradients are those of the whole call, since an unlabelled
+ * row contributes nothing -- and the other rows of dH are written as zero;
+ * prob must then be NULL. */
 size_t hg_mlp_bce_workspace_size(int64_t n_rows, int32_t d, int32_t d_hidden);
 int hg_mlp_bce_fwd_bwd(int64_t n_rows, int32_t d, int32_t d_hidden, const float* H, const float* W1,
-                       const float* b1, const float* W2, const float* b2, const int8_t* labels, float* loss,
-                       float* prob, float* dH, float* dW1, float* db1, float* dW2, float* db2, void* ws,
-                       size_t ws_bytes, void* stream);
+                       const float* b1, const float* W2, const float* b2, const int8_t* labels,
+                       const int32_t* rows, int64_t n_list, float* loss, float* prob, float* dH, float* dW1,
+                       float* db1, float* dW2, float* db2, void* ws, size_t ws_bytes, void* stream);
 
 /* One Adam update (the optimiser paragraph; weight decay added to the
  * gradient, bias-corrected moments), in place on n float32 values:

@@ -134,7 +134,7 @@ def lib() -> C.CDLL:
         "hg_align_loss_fwd_bwd": (C.c_int, [i64, i32, i32, i64, vp, vp, vp, vp, f32, f32, f32,
                                             i32, vp, vp, vp, vp, vp, sz, vp]),
         "hg_mlp_bce_workspace_size": (sz, [i64, i32, i32]),
-        "hg_mlp_bce_fwd_bwd": (C.c_int, [i64, i32, i32] + [vp] * 14 + [sz, vp]),
+        "hg_mlp_bce_fwd_bwd": (C.c_int, [i64, i32, i32] + [vp] * 7 + [i64] + [vp] * 8 + [sz, vp]),
         "hg_adam_step": (C.c_int, [i64, vp, vp, vp, vp, i64, f32, f32, f32, f32, f32, vp]),
         "hg_temporal_fwd": (C.c_int, [i64, i32, i32, i32, vp, vp, vp, vp, vp]),
         "hg_temporal_bwd_workspace_size": (sz, [i64, i32, i32]),
@@ -425,9 +425,10 @@ def hg_mlp_bce_workspace_size(n_rows: int, d: int) -> int:
 
 
 def hg_mlp_bce_fwd_bwd(H, W1, b1, W2, b2, labels, dH=None, grads: Optional[dict] = None, loss=None, prob=None,
-                       ws=None, stream=None):
+                       ws=None, stream=None, rows=None):
     """Prediction head + masked BCE: returns (loss [1], dH, grads) with grads
-    {W1, b1, W2, b2}; dH is overwritten with dL_BCE/dH."""
+    {W1, b1, W2, b2}; dH is overwritten with dL_BCE/dH.  rows: int32 list
+    of rows holding every labelled one (only those go through the head)."""
     n, d = int(H.shape[0]), int(H.shape[1])
     L = lib()
     if dH is None:
@@ -439,7 +440,9 @@ def hg_mlp_bce_fwd_bwd(H, W1, b1, W2, b2, labels, dH=None, grads: Optional[dict]
         loss = torch.empty(1, dtype=torch.float32, device=H.device)
     if ws is None:
         ws = _ws(int(L.hg_mlp_bce_workspace_size(n, d, d)), H.device)
-    _check(L.hg_mlp_bce_fwd_bwd(n, d, d, _ptr(H), _ptr(W1), _ptr(b1), _ptr(W2), _ptr(b2), _ptr(labels), _ptr(loss),
+    n_list = 0 if rows is None else int(rows.shape[0])
+    _check(L.hg_mlp_bce_fwd_bwd(n, d, d, _ptr(H), _ptr(W1), _ptr(b1), _ptr(W2), _ptr(b2), _ptr(labels), _ptr(rows),
+                                n_list, _ptr(loss),
                                 _ptr(prob), _ptr(dH), _ptr(grads["W1"]), _ptr(grads.get("b1")), _ptr(grads["W2"]),
                                 _ptr(grads.get("b2")), _ptr(ws), ws.numel(), _stream(stream)), "hg_mlp_bce_fwd_bwd")
     return loss, dH, grads

@@ -105,13 +105,15 @@ __device__ __forceinline__ float block_sum_256(float v, float* red) {
   return r;
 }
 
-// Number of labelled rows, as per-block partial counts.
-__global__ void __launch_bounds__(kHeadThreads) k_count_labels(const int8_t* __restrict__ labels, int64_t n,
+// Number of labelled rows, as per-block partial counts (row i of the head is
+// row rows[i] of the labels when a row list is given).
+__global__ void __launch_bounds__(kHeadThreads) k_count_labels(const int8_t* __restrict__ labels,
+                                                               const int32_t* __restrict__ rows, int64_t n,
                                                                int32_t* __restrict__ part) {
   __shared__ float red[kHeadThreads];
   float c = 0.f;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
-    c += labels[i] >= 0 ? 1.f : 0.f;
+    c += labels[rows ? (int64_t)rows[i] : i] >= 0 ? 1.f : 0.f;
   const float s = block_sum_256(c, red);
   if (threadIdx.x == 0) part[blockIdx.x] = (int32_t)s;
 }
@@ -122,6 +124,7 @@ template <int D>
 __global__ void __launch_bounds__(kHeadThreads) k_mlp_head(int64_t n, const float* __restrict__ hid,
                                                            const float* __restrict__ W2, const float* __restrict__ b2,
                                                            const int8_t* __restrict__ labels,
+                                                           const int32_t* __restrict__ rows,
                                                            const int32_t* __restrict__ cnt_part,
                                                            float* __restrict__ dout, float* __restrict__ prob,
                                                            float* __restrict__ part) {
@@ -152,7 +155,7 @@ __global__ void __launch_bounds__(kHeadThreads) k_mlp_head(int64_t n, const floa
 #pragma unroll
     for (int q = 1; q < LPR; q <<= 1) o += __shfl_xor(o, q, 64);
     o += bb;
-    const int lab = live ? (int)labels[i] : -1;
+    const int lab = live ? (int)labels[rows ? (int64_t)rows[i] : i] : -1;
     float d_o = 0.f, term = 0.f;
     const float p = 1.0f / (1.0f + __expf(-o));
     if (lab >= 0) {
@@ -237,27 +240,32 @@ struct HeadWs {
   }
 };
 
+// With a row list only the listed rows (a superset of the labelled ones) go
+// through the head: the hidden rows, logits and dL/do are kept compactly in
+// list order, H is read and dH written through the list, and the other rows
+// of dH are zero.
 template <int D>
 int head_impl(int64_t n, const float* H, const float* W1, const float* b1, const float* W2, const float* b2,
-              const int8_t* labels, float* loss, float* prob, float* dH, float* dW1, float* db1, float* dW2,
-              float* db2, void* ws, size_t ws_bytes, hipStream_t st) {
+              const int8_t* labels, const int32_t* rows, int64_t n_list, float* loss, float* prob, float* dH,
+              float* dW1, float* db1, float* dW2, float* db2, void* ws, size_t ws_bytes, hipStream_t st) {
   Arena a(ws, ws_bytes);
   HeadWs w;
   w.layout(a, n, D);
   if (!a.ok()) return fail(HG_ERR_CAPACITY, "prediction-head workspace needs %zu bytes, got %zu", a.used, ws_bytes);
+  const int64_t m = rows ? n_list : n;
+  const RowMap hm = rows ? rows_list(rows) : rows_contig(0);
   // hidden layer and its ReLU mask
-  HG_TRY((launch_gemm_rows_pp<D, false>("head_hidden", n, W1, LoadRows<D, float>{H, rows_contig(0)},
+  HG_TRY((launch_gemm_rows_pp<D, false>("head_hidden", m, W1, LoadRows<D, float>{H, hm},
                                         StoreHidden<D>{w.hid, rows_contig(0), b1, w.mask}, st)));
-  HG_LAUNCH("head_count", k_count_labels, dim3(kHeadBlocks), dim3(kHeadThreads), 0, st, labels, n, w.cnt);
-  HG_LAUNCH("head_logit", k_mlp_head<D>, dim3(kHeadBlocks), dim3(kHeadThreads), 0, st, n, (const float*)w.hid, W2, b2,
-            labels, (const int32_t*)w.cnt, w.dout, prob, w.part);
+  HG_LAUNCH("head_count", k_count_labels, dim3(kHeadBlocks), dim3(kHeadThreads), 0, st, labels, rows, m, w.cnt);
+  HG_LAUNCH("head_logit", k_mlp_head<D>, dim3(kHeadBlocks), dim3(kHeadThreads), 0, st, m, (const float*)w.hid, W2, b2,
+            labels, rows, (const int32_t*)w.cnt, w.dout, prob, w.part);
   HG_LAUNCH("head_final", k_head_final<D>, dim3(1), dim3(256), 0, st, (const float*)w.part, dW2, db2, loss);
   // dH = da W1^T and dW1 = H^T da with da = mask * (dL/do W2^T) formed in the loaders
+  if (rows && n > 0) HG_TRY(fill_f32(dH, 0.f, n * D, st));
   const LoadRank1Masked<D> da{w.dout, W2, w.mask, rows_contig(0)};
-  HG_TRY((launch_gemm_rows_pp<D, true>("head_dx", n, W1, da, StoreRows<D, float>{dH, rows_contig(0), nullptr, nullptr},
-                                       st)));
-  HG_TRY((launch_gemm_tn<D>("head_dw", n, LoadRows<D, float>{H, rows_contig(0)}, da, w.splitk, w.colsum, dW1, db1, 0,
-                            st)));
+  HG_TRY((launch_gemm_rows_pp<D, true>("head_dx", m, W1, da, StoreRows<D, float>{dH, hm, nullptr, nullptr}, st)));
+  HG_TRY((launch_gemm_tn<D>("head_dw", m, LoadRows<D, float>{H, hm}, da, w.splitk, w.colsum, dW1, db1, 0, st)));
   return HG_OK;
 }
 
@@ -277,17 +285,23 @@ size_t hg_mlp_bce_workspace_size(int64_t n_rows, int32_t d, int32_t d_hidden) {
 }
 
 int hg_mlp_bce_fwd_bwd(int64_t n_rows, int32_t d, int32_t d_hidden, const float* H, const float* W1, const float* b1,
-                       const float* W2, const float* b2, const int8_t* labels, float* loss, float* prob, float* dH,
-                       float* dW1, float* db1, float* dW2, float* db2, void* ws, size_t ws_bytes, void* stream) {
+                       const float* W2, const float* b2, const int8_t* labels, const int32_t* rows, int64_t n_list,
+                       float* loss, float* prob, float* dH, float* dW1, float* db1, float* dW2, float* db2, void* ws,
+                       size_t ws_bytes, void* stream) {
   if (n_rows < 0) return fail(HG_ERR_ARG, "n_rows < 0");
+  if (rows && (n_list < 0 || n_list > n_rows)) return fail(HG_ERR_ARG, "n_list outside [0, n_rows]");
+  if (rows && prob) return fail(HG_ERR_ARG, "prob needs every row: it must be NULL with a row list");
   if (d != d_hidden || (d != 64 && d != 128))
     return fail(HG_ERR_UNSUPPORTED, "prediction head: d_hidden == d in {64, 128} (d=%d, d_hidden=%d)", d, d_hidden);
   if (!W1 || !W2 || !loss || !dW1 || !dW2 || (n_rows > 0 && (!H || !labels || !dH)))
     return fail(HG_ERR_ARG, "null pointer (only b1, b2, prob, db1, db2 may be NULL; H, labels, dH when n_rows = 0)");
   if (n_rows > 0 && dH == H) return fail(HG_ERR_ARG, "dH must not alias H");
   const hipStream_t st = static_cast<hipStream_t>(stream);
-  if (d == 64) return head_impl<64>(n_rows, H, W1, b1, W2, b2, labels, loss, prob, dH, dW1, db1, dW2, db2, ws, ws_bytes, st);
-  return head_impl<128>(n_rows, H, W1, b1, W2, b2, labels, loss, prob, dH, dW1, db1, dW2, db2, ws, ws_bytes, st);
+  if (d == 64)
+    return head_impl<64>(n_rows, H, W1, b1, W2, b2, labels, rows, n_list, loss, prob, dH, dW1, db1, dW2, db2, ws,
+                         ws_bytes, st);
+  return head_impl<128>(n_rows, H, W1, b1, W2, b2, labels, rows, n_list, loss, prob, dH, dW1, db1, dW2, db2, ws,
+                        ws_bytes, st);
 }
 
 int hg_adam_step(int64_t n, float* param, const float* grad, float* m, float* v, int64_t step, float lr, float beta1,

@@ -45,6 +45,7 @@ class StepInputs:
     # full objective (prediction head, masked BCE, Adam)
     labels: Optional[torch.Tensor] = None
     labels_np: Optional[np.ndarray] = None
+    label_rows: Optional[torch.Tensor] = None  # rows with a label, ascending (only they go through the head)
     head: Optional[dict] = None
     head_np: Optional[dict] = None
     head_grads: Optional[dict] = None
@@ -63,6 +64,12 @@ class StepResult:
 
 def _dev(x, device):
     return torch.from_numpy(np.ascontiguousarray(x)).to(device)
+
+
+def _label_rows(labels: torch.Tensor) -> torch.Tensor:
+    """Rows with a label (>= 0), ascending int32: fixed by the input labels,
+    computed once at set-up."""
+    return torch.nonzero(labels >= 0).flatten().to(torch.int32).contiguous()
 
 
 def make_inputs(wl: synth.Workload, g: synth.Graph, device="cuda", feats: Optional[np.ndarray] = None
@@ -124,6 +131,7 @@ def make_inputs(wl: synth.Workload, g: synth.Graph, device="cuda", feats: Option
     if mc.objective == "bce":
         inp.labels_np = synth.labels(mc.seed, g.ntype)
         inp.labels = _dev(inp.labels_np, device).index_select(0, l2g).contiguous()
+        inp.label_rows = _label_rows(inp.labels)
         inp.head_np = synth.head_weights(mc.seed, d)
         inp.head = {k: _dev(v, device) for k, v in inp.head_np.items()}
         inp.head_grads = {k: torch.empty_like(v) for k, v in inp.head.items()}
@@ -164,7 +172,8 @@ def run_step(inp: StepInputs, rebuild: bool = True) -> StepResult:
     if mc.objective == "bce":
         # dL_BCE/dH of the prediction head on the labelled rows (overwrites g)
         api.hg_mlp_bce_fwd_bwd(inp.H[-1], inp.head["W1"], inp.head["b1"], inp.head["W2"], inp.head["b2"],
-                               inp.labels, dH=g, grads=inp.head_grads, loss=inp.loss_bce, ws=inp.head_ws)
+                               inp.labels, dH=g, grads=inp.head_grads, loss=inp.loss_bce, ws=inp.head_ws,
+                               rows=inp.label_rows)
     else:
         base = inp.gext
     api.hg_align_loss_fwd_bwd(inp.H[-1], overlap, inp.href, g, w=inp.omega, lambda_n=mc.lambda_n,
@@ -207,6 +216,7 @@ class SeqInputs:
     head_np: dict
     labels: torch.Tensor
     labels_np: np.ndarray
+    label_rows: torch.Tensor
     href: torch.Tensor
     href_np: np.ndarray
     feats_np: np.ndarray
@@ -273,7 +283,7 @@ def make_seq_inputs(wl: synth.Workload, g: synth.Graph, device="cuda") -> SeqInp
     m = sub0.m_sel
     href_np = synth.reference_embeddings(mc.seed, max(m, 1), d)
     inp = SeqInputs(wl, gd, g.k, cuts, subs, build_ws, h0, weights, weights_np, tparams, tparams_np, head, head_np,
-                    labels, labels_np, _dev(href_np[:m], device), href_np, feats, ts_np)
+                    labels, labels_np, _label_rows(labels), _dev(href_np[:m], device), href_np, feats, ts_np)
     ns = sub0.n_sub
     f32 = dict(dtype=torch.float32, device=device)
     inp.H = [h0] + [torch.empty((ns, d), **f32) for _ in range(mc.n_layers)]
@@ -331,7 +341,7 @@ def run_seq_step(inp: SeqInputs, rebuild: bool = True, update: bool = True, on_s
             on_snapshot(t)
     g = inp.dS[T - 1]
     api.hg_mlp_bce_fwd_bwd(inp.S[T - 1], inp.head["W1"], inp.head["b1"], inp.head["W2"], inp.head["b2"], inp.labels,
-                           dH=g, grads=inp.head_grads, loss=inp.loss_bce, ws=inp.head_ws)
+                           dH=g, grads=inp.head_grads, loss=inp.loss_bce, ws=inp.head_ws, rows=inp.label_rows)
     api.hg_align_loss_fwd_bwd(inp.S[T - 1], inp.subs[0].view("overlap"), inp.href, g, lambda_n=mc.lambda_n,
                               scale=mc.lambda_cca, eps=mc.eps, ddof=mc.ddof, loss3=inp.loss, ws=inp.align_ws)
     for j in range(T - 1):
@@ -372,6 +382,7 @@ class KwayInputs:
     head_np: dict
     labels: torch.Tensor        # int8 [n_nodes], global order
     labels_np: np.ndarray
+    label_rows: torch.Tensor
     feats_np: np.ndarray
     H: List[List[torch.Tensor]] = field(default_factory=list)      # H[k][l]: layer l rows of subgraph k
     saved: List[List[torch.Tensor]] = field(default_factory=list)
@@ -429,8 +440,9 @@ def make_kway_inputs(wl: synth.Workload, g: synth.Graph, device="cuda") -> KwayI
     head_np = synth.head_weights(mc.seed, d)
     head = {k: _dev(v, device) for k, v in head_np.items()}
     labels_np = synth.labels(mc.seed, g.ntype)
+    labels = _dev(labels_np, device)
     inp = KwayInputs(wl, gd, part_np, subs, build_ws, keys, keys_ws, weights, weights_np, head, head_np,
-                     _dev(labels_np, device), labels_np, feats)
+                     labels, labels_np, _label_rows(labels), feats)
     f32 = dict(dtype=torch.float32, device=device)
     for sb in subs:
         h0 = feats_d.index_select(0, sb.view("local2global").long()).contiguous()
@@ -490,7 +502,8 @@ def run_kway_step(inp: KwayInputs, rebuild: bool = True, update: bool = True):
     last = [h[-1] for h in inp.H]
     api.hg_mean_agg_fwd(g2l, last, H=inp.H_agg, cnt=inp.cnt)
     api.hg_mlp_bce_fwd_bwd(inp.H_agg, inp.head["W1"], inp.head["b1"], inp.head["W2"], inp.head["b2"], inp.labels,
-                           dH=inp.dH_agg, grads=inp.head_grads, loss=inp.loss_bce, ws=inp.head_ws)
+                           dH=inp.dH_agg, grads=inp.head_grads, loss=inp.loss_bce, ws=inp.head_ws,
+                           rows=inp.label_rows)
     for k, sb in enumerate(inp.subs):
         ns, m = sb.n_sub, sb.m_sel
         l2g = sb.view("local2global")

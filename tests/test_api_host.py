@@ -276,3 +276,12 @@ def test_node_keys_reject_bad_arguments(L):
     big = api.GraphDesc(1 << 30, (1 << 31) - 1, 2, 1, fake, fake, fake, None, None, 0, None, None, 0, 0)
     assert L.hg_node_keys_workspace_size(C.byref(big), 0) == 0
     assert L.hg_node_keys_workspace_size(C.byref(g), 1) > L.hg_node_keys_workspace_size(C.byref(g), 0)
+
+
+def test_head_rejects_bad_row_lists(L):
+    fake = C.c_void_p(0x1000)
+    args = lambda rows, n_list, prob: (10, 64, 64, fake, fake, None, fake, None, fake, rows, n_list, fake, prob, fake,
+                                       fake, None, fake, None, fake, 1 << 30, None)
+    assert L.hg_mlp_bce_fwd_bwd(*args(fake, 11, None)) == api.HG_ERR_ARG   # longer than the rows
+    assert L.hg_mlp_bce_fwd_bwd(*args(fake, -1, None)) == api.HG_ERR_ARG
+    assert L.hg_mlp_bce_fwd_bwd(*args(fake, 4, fake)) == api.HG_ERR_ARG    # prob needs every row

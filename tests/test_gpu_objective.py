@@ -49,6 +49,44 @@ def test_head_matches_oracle(seed, n, d):
     assert parity_err(prob.cpu().numpy(), 1 / (1 + np.exp(-o[:, 0]))) <= TOL
 
 
+@pytest.mark.parametrize("seed,n,d", CASES)
+@pytest.mark.parametrize("superset", [False, True])
+def test_head_on_listed_rows_matches_oracle(seed, n, d, superset):
+    """Only the listed rows (the labelled ones, or a shuffled superset with
+    unlabelled rows among them) go through the head: same loss and
+    gradients as the oracle on every row, and dH zero off the list."""
+    H, W1, b1, W2, b2, lab = head_case(seed, n, d)
+    loss, dH, dW1, db1, dW2, db2, _ = objective.mlp_bce(H, W1, b1, W2, b2, lab)
+    rows = np.nonzero(lab >= 0)[0]
+    if superset:
+        extra = np.random.default_rng(seed).choice(np.nonzero(lab < 0)[0], size=min(37, int((lab < 0).sum())),
+                                                   replace=False)
+        rows = np.random.default_rng(seed + 1).permutation(np.concatenate([rows, extra]))
+    junk = torch.full((n, d), 3.0, dtype=torch.float32, device="cuda")
+    got_loss, got_dH, g = api.hg_mlp_bce_fwd_bwd(to_dev(H), to_dev(W1), to_dev(b1), to_dev(W2), to_dev(b2),
+                                                 torch.from_numpy(lab).cuda(), dH=junk,
+                                                 rows=to_dev(rows.astype(np.int32)))
+    torch.cuda.synchronize()
+    assert abs(float(got_loss.cpu()[0]) - loss) <= 1e-5 * abs(loss)
+    errs = {"dH": parity_err(got_dH.cpu().numpy(), dH), "W1": parity_err(g["W1"].cpu().numpy(), dW1),
+            "b1": parity_err(g["b1"].cpu().numpy(), db1), "W2": parity_err(g["W2"].cpu().numpy(), dW2),
+            "b2": parity_err(g["b2"].cpu().numpy(), db2)}
+    assert max(errs.values()) <= TOL, errs
+    off = np.setdiff1d(np.arange(n), rows)
+    assert not got_dH.cpu().numpy()[off].any()
+
+
+def test_head_on_an_empty_list():
+    H, W1, b1, W2, b2, lab = head_case(3, 500, 64)
+    lab[:] = -1
+    rows = torch.zeros(0, dtype=torch.int32, device="cuda")
+    loss, dH, g = api.hg_mlp_bce_fwd_bwd(to_dev(H), to_dev(W1), to_dev(b1), to_dev(W2), to_dev(b2),
+                                         torch.from_numpy(lab).cuda(), rows=rows)
+    torch.cuda.synchronize()
+    assert float(loss.cpu()[0]) == 0.0
+    assert not dH.cpu().numpy().any() and not g["W1"].cpu().numpy().any() and not g["b2"].cpu().numpy().any()
+
+
 def test_head_without_labels_and_empty():
     H, W1, b1, W2, b2, lab = head_case(3, 500, 64)
     lab[:] = -1
