@@ -39,7 +39,18 @@ __device__ __forceinline__ int64_t cdiv_dev(int64_t a, int64_t b) { return (a + 
        i += (int64_t)gridDim.x * blockDim.x)
 
 // Device counters written by the build.
-enum : int { C_ERR = 0, C_NSUB, C_ESUB, C_MSEL, C_ITEMS, C_HEAVY, C_PARTS, C_CPRIME, C_COUNT };
+enum : int { C_ERR = 0, C_NSUB, C_ESUB, C_MSEL, C_ITEMS, C_HEAVY, C_PARTS, C_CPRIME, C_BASE, C_COUNT };
+
+// A subgraph that can hold three quarters of the graph's nodes (|V_k| plus
+// the budget) is built the "dense" way: the base edge of every candidate is
+// found in the first edge pass and the induced edges from gathered local ids.
+// Otherwise the first pass only marks candidates, the base edges of the
+// selected nodes are found with the induced edges, and those come from a
+// membership bitmap.  Both give the same outputs.
+__host__ __device__ inline bool dense_build(int64_t n_base, int64_t budget, int64_t n_nodes) {
+  const int64_t b = budget < n_nodes ? budget : n_nodes;
+  return 4 * (n_base + b) >= 3 * n_nodes;
+}
 
 struct SelectState {
   uint32_t k_rem;   // how many more to take from the current prefix bucket
@@ -72,17 +83,43 @@ __device__ __forceinline__ uint32_t composite_digit(uint32_t key, uint64_t h, ui
 }
 
 // bits[v / 32] bit v % 32 = pred(v); one wave covers 64 nodes (two words).
-__global__ void k_base_bits(const int32_t* __restrict__ part, int32_t k, int64_t n,
-                            uint32_t* __restrict__ bits) {
+// Also |V_k|, as one partial count per block (summed by k_sum_counts).
+__global__ void __launch_bounds__(kBT) k_base_bits(const int32_t* __restrict__ part, int32_t k, int64_t n,
+                                                   uint32_t* __restrict__ bits, int32_t* __restrict__ block_cnt) {
+  __shared__ int32_t wc[kBT / 64];
+  int32_t c = 0;  // the same in every lane of a wave
   GRID_STRIDE(v0, cdiv_dev(n, 64) * 64) {
     const bool in = v0 < n && part[v0] == k;
     const uint64_t m = __ballot(in);
+    c += (int32_t)__popcll(m);
     if ((threadIdx.x & 63) == 0) {
       const int64_t wd = v0 >> 5;
       bits[wd] = (uint32_t)m;
       if ((v0 + 32) < n) bits[wd + 1] = (uint32_t)(m >> 32);
     }
   }
+  if ((threadIdx.x & 63) == 0) wc[threadIdx.x >> 6] = c;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int32_t t = 0;
+    for (int q = 0; q < kBT / 64; ++q) t += wc[q];
+    block_cnt[blockIdx.x] = t;
+  }
+}
+
+// out[0] = sum of the nb block counts (one block, fixed order).
+__global__ void __launch_bounds__(256) k_sum_counts(const int32_t* __restrict__ block_cnt, int nb,
+                                                    int32_t* __restrict__ out) {
+  __shared__ int32_t red[256];
+  int32_t t = 0;
+  for (int i = threadIdx.x; i < nb; i += 256) t += block_cnt[i];
+  red[threadIdx.x] = t;
+  __syncthreads();
+  for (int o = 128; o > 0; o >>= 1) {
+    if ((int)threadIdx.x < o) red[threadIdx.x] += red[threadIdx.x + o];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) out[0] = red[0];
 }
 
 __global__ void k_cand_bits(const int32_t* __restrict__ first, int32_t n_edges, int64_t n,
@@ -186,21 +223,27 @@ inline unsigned agg_grid(int64_t n) {
   return (unsigned)(b < cap ? b : cap);
 }
 
-// Range checks and, for every node outside V_k, the smallest index of an edge
-// joining it to V_k; all out-degrees when count_all (needed by the h-index).
+// Range checks and the candidates C_k: every node outside V_k joined to V_k
+// by an edge gets first[v] < n_edges -- in a dense build the smallest index of
+// such an edge (block-aggregated atomic minimum), otherwise 0 (a plain store:
+// every writer stores the same value, and a node already marked is only
+// read).  All out-degrees when count_all (needed by the h-index).
 __global__ void __launch_bounds__(kAggBT) k_edges_pass(const int32_t* __restrict__ src, const int32_t* __restrict__ dst,
                                                    const uint8_t* __restrict__ rel,
                                                    const uint32_t* __restrict__ base_bits, int64_t n_nodes,
-                                                   int64_t n_edges, int32_t n_rel, int count_all,
+                                                   int64_t n_edges, int32_t n_rel, int count_all, int64_t budget,
                                                    int32_t* __restrict__ outdeg, int32_t* __restrict__ first,
                                                    int32_t* __restrict__ cnt) {
   __shared__ uint32_t lk[3][kAggSlots];
   __shared__ int32_t lv[3][kAggSlots];
   LdsAgg<false> deg{lk[0], lv[0]};
   LdsAgg<true> fs{lk[1], lv[1]}, fd{lk[2], lv[2]};
+  const bool exact = dense_build(cnt[C_BASE], budget, n_nodes);
   if (count_all) deg.init();
-  fs.init();
-  fd.init();
+  if (exact) {
+    fs.init();
+    fd.init();
+  }
   __syncthreads();
   GRID_STRIDE(e, n_edges) {
     const int32_t s = src[e], d = dst[e];
@@ -211,13 +254,20 @@ __global__ void __launch_bounds__(kAggBT) k_edges_pass(const int32_t* __restrict
     }
     if (count_all) deg.put((uint32_t)s, 1, outdeg);
     const bool ps = bit_of(base_bits, s), pd = bit_of(base_bits, d);
-    if (pd && !ps) fs.put((uint32_t)s, (int32_t)e, first);
-    if (ps && !pd) fd.put((uint32_t)d, (int32_t)e, first);
+    if (exact) {
+      if (pd && !ps) fs.put((uint32_t)s, (int32_t)e, first);
+      if (ps && !pd) fd.put((uint32_t)d, (int32_t)e, first);
+    } else {
+      if (pd && !ps && first[s] != 0) first[s] = 0;
+      if (ps && !pd && first[d] != 0) first[d] = 0;
+    }
   }
   __syncthreads();
   if (count_all) deg.flush(outdeg);
-  fs.flush(first);
-  fd.flush(first);
+  if (exact) {
+    fs.flush(first);
+    fd.flush(first);
+  }
 }
 
 // Out-degrees of the candidate nodes only (the out-degree key needs no other).
@@ -424,12 +474,17 @@ __global__ void k_select_mark(const SelectState* st, const int32_t* __restrict__
   }
 }
 
+// Node-set digits for the relabel; in a sparse build the selected nodes'
+// first[] goes back to n_edges for the base-edge minimum of the edge pass.
 __global__ void k_member_digit(const int32_t* __restrict__ part, int32_t k,
                                const uint8_t* __restrict__ sel, const uint8_t* __restrict__ ntype,
-                               int64_t n, uint8_t* __restrict__ digit, int32_t* __restrict__ iota) {
+                               int64_t n, int64_t n_edges, int64_t budget, const int32_t* __restrict__ cnt,
+                               uint8_t* __restrict__ digit, int32_t* __restrict__ iota, int32_t* __restrict__ first) {
+  const bool exact = dense_build(cnt[C_BASE], budget, n);
   GRID_STRIDE(v, n) {
     digit[v] = (part[v] == k || sel[v]) ? ntype[v] : (uint8_t)255;
     iota[v] = (int32_t)v;
+    if (!exact && sel[v]) first[v] = (int32_t)n_edges;
   }
 }
 
@@ -459,18 +514,6 @@ __global__ void k_overlap_fill(const int32_t* __restrict__ l2g, const int32_t* _
       overlap[p] = (int32_t)i;
       home[p] = part[g];
       orel[p] = rel[first[g]];
-    }
-  }
-}
-
-__global__ void k_member_bits(const int32_t* __restrict__ g2l, int64_t n, uint32_t* __restrict__ bits) {
-  GRID_STRIDE(v0, cdiv_dev(n, 64) * 64) {
-    const bool in = v0 < n && g2l[v0] >= 0;
-    const uint64_t m = __ballot(in);
-    if ((threadIdx.x & 63) == 0) {
-      const int64_t wd = v0 >> 5;
-      bits[wd] = (uint32_t)m;
-      if ((v0 + 32) < n) bits[wd + 1] = (uint32_t)(m >> 32);
     }
   }
 }
@@ -524,12 +567,22 @@ __global__ void k_edge_compact_ids(const int32_t* __restrict__ sl, const int32_t
 // membership bitmap, N/8 bytes, which stays in the L2 cache).  With
 // timestamps, an edge after the cut is dropped like an edge that leaves the
 // node set.
+// An edge of the node set (timestamps aside) between a selected node and a
+// base node is a candidate edge of the selected node: the smallest such index
+// is its base edge (atomic minimum; selected nodes are few and of small key).
 __global__ void k_edge_keep(const int32_t* __restrict__ src, const int32_t* __restrict__ dst,
-                            const uint32_t* __restrict__ member, const int32_t* __restrict__ ts, int32_t t_cut,
-                            int64_t n_edges, int32_t* __restrict__ keep) {
+                            const uint32_t* __restrict__ member, const uint32_t* __restrict__ base_bits,
+                            const int32_t* __restrict__ ts, int32_t t_cut, int64_t n_edges,
+                            int32_t* __restrict__ keep, int32_t* __restrict__ first) {
   GRID_STRIDE(e, n_edges) {
-    const bool in = bit_of(member, src[e]) && bit_of(member, dst[e]) && !(ts && ts[e] > t_cut);
-    keep[e] = in ? 1 : 0;
+    const int32_t s = src[e], d = dst[e];
+    const bool in = bit_of(member, s) && bit_of(member, d);
+    if (in) {
+      const bool ps = bit_of(base_bits, s), pd = bit_of(base_bits, d);
+      if (pd && !ps) atomicMin(&first[s], (int32_t)e);
+      if (ps && !pd) atomicMin(&first[d], (int32_t)e);
+    }
+    keep[e] = (in && !(ts && ts[e] > t_cut)) ? 1 : 0;
   }
 }
 
@@ -635,11 +688,12 @@ struct BuildWs {
   uint8_t *sel, *digit;
   SelectState* st;
   int32_t *keep, *vsrc, *vdst, *veid, *alt1, *alt2, *alt3, *rowcnt, *q_items, *q_heavy, *q_parts,
-      *q_src, *scratch;
+      *q_src, *scratch, *bcnt;
   uint32_t *kcsr, *kcsc, *kalt, *bbits, *cbits, *mbits;
   void layout(A& a, int64_t N, int64_t E, int64_t R, bool hindex) {
     const int64_t NQ = N * R + 1;
     cnt = a.template take<int32_t>(C_COUNT + 8);
+    bcnt = a.template take<int32_t>(16384);  // block counts of k_base_bits (grid_for caps it there)
     outdeg = a.template take<int32_t>(N);
     first = a.template take<int32_t>(N);
     key = a.template take<int32_t>(N);
@@ -857,11 +911,13 @@ extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg
   HG_TRY(fill_i32(w.first, (int32_t)E, N, s));
   HG_TRY(fill_u8(w.sel, 0, N, s));
   const unsigned gB = grid_for(cdiv(N, 64) * 64);
-  HG_LAUNCH("build_base_bits", k_base_bits, dim3(gB), dim3(kBT), 0, s, g->part, g->k, N, w.bbits);
+  HG_LAUNCH("build_base_bits", k_base_bits, dim3(gB), dim3(kBT), 0, s, g->part, g->k, N, w.bbits, w.bcnt);
+  HG_LAUNCH("build_base_count", k_sum_counts, dim3(1), dim3(256), 0, s, (const int32_t*)w.bcnt, (int)gB,
+            w.cnt + C_BASE);
   if (E > 0)
     HG_LAUNCH("build_edges_pass", k_edges_pass, dim3(agg_grid(E)), dim3(kAggBT), 0, s, g->src, g->dst, g->rel,
-              (const uint32_t*)w.bbits, N, E, (int32_t)R, (hindex && !o->node_key) ? 1 : 0, w.outdeg, w.first,
-              w.cnt);
+              (const uint32_t*)w.bbits, N, E, (int32_t)R, (hindex && !o->node_key) ? 1 : 0, o->budget_M, w.outdeg,
+              w.first, w.cnt);
   HG_LAUNCH("build_check_ntype", k_check_ntype, dim3(gN), dim3(kBT), 0, s, g->ntype, N, (int32_t)T, w.cnt);
   {
     int32_t herr = 0;
@@ -914,27 +970,19 @@ extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg
   }
   // 5. local ids in (ntype, gid) order
   HG_LAUNCH("build_member_digit", k_member_digit, dim3(gN), dim3(kBT), 0, s, g->part, g->k,
-            (const uint8_t*)w.sel, g->ntype, N, w.digit, w.iota);
+            (const uint8_t*)w.sel, g->ntype, N, E, o->budget_M, (const int32_t*)w.cnt, w.digit, w.iota, w.first);
   HG_TRY(bucket_partition(w.digit, w.iota, N, (int)T, out->local2global, out->type_off, w.scratch, s));
   HG_TRY(fill_i32(out->global2local, -1, N, s));
   HG_LAUNCH("build_global2local", k_global2local, dim3(gN), dim3(kBT), 0, s,
             (const int32_t*)out->local2global, (const int32_t*)out->type_off, (int32_t)T,
             out->global2local, w.cnt);
-  // overlap list (local ids ascending)
-  HG_LAUNCH("build_overlap_flags", k_overlap_flags, dim3(gN), dim3(kBT), 0, s,
-            (const int32_t*)out->local2global, (const uint8_t*)w.sel, (const int32_t*)w.cnt, N, w.flag);
-  HG_TRY(scan_exclusive_i32(w.flag, w.pos, N, w.cnt + C_MSEL, w.scratch, s));
-  if (o->budget_M > 0)
-    HG_LAUNCH("build_overlap_fill", k_overlap_fill, dim3(gN), dim3(kBT), 0, s,
-              (const int32_t*)out->local2global, (const int32_t*)w.flag, (const int32_t*)w.pos,
-              (const int32_t*)w.cnt, g->part, (const int32_t*)w.first, g->rel, out->overlap,
-              out->overlap_home, out->overlap_rel);
-  // 6. induced-subgraph edges in original order
+  // 6. induced-subgraph edges in original order (and, in a sparse build, the
+  // base edges of the selected nodes)
   if (E > 0) {
-    int32_t ns_host = 0;
-    HG_HIP_TRY(hipMemcpyAsync(&ns_host, w.cnt + C_NSUB, sizeof(int32_t), hipMemcpyDeviceToHost, s));
+    int32_t nb_host = 0;
+    HG_HIP_TRY(hipMemcpyAsync(&nb_host, w.cnt + C_BASE, sizeof(int32_t), hipMemcpyDeviceToHost, s));
     HG_HIP_TRY(hipStreamSynchronize(s));
-    if (4 * (int64_t)ns_host >= 3 * N) {
+    if (dense_build(nb_host, o->budget_M, N)) {
       // local ids land in the sort's ping-pong buffers (free until the sorts)
       HG_LAUNCH("build_edge_keep", k_edge_keep_ids, dim3(gE), dim3(kBT), 0, s, g->src, g->dst,
                 (const int32_t*)out->global2local, g->edge_ts, g->t_cut, E, w.keep, w.alt1, w.alt2);
@@ -946,7 +994,7 @@ extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg
       HG_LAUNCH("build_member_bits", k_member_bits, dim3(gB), dim3(kBT), 0, s, g->part, g->k,
                 (const uint8_t*)w.sel, N, w.mbits);
       HG_LAUNCH("build_edge_keep", k_edge_keep, dim3(gE), dim3(kBT), 0, s, g->src, g->dst,
-                (const uint32_t*)w.mbits, g->edge_ts, g->t_cut, E, w.keep);
+                (const uint32_t*)w.mbits, (const uint32_t*)w.bbits, g->edge_ts, g->t_cut, E, w.keep, w.first);
       // keep[E] = 0, so the scan's entry E is the number of kept edges
       HG_TRY(fill_i32(w.keep + E, 0, 1, s));
       HG_TRY(scan_exclusive_i32(w.keep, w.keep, E + 1, w.cnt + C_ESUB, w.scratch, s));
@@ -957,6 +1005,16 @@ extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg
   } else {
     HG_TRY(fill_i32(w.cnt + C_ESUB, 0, 1, s));
   }
+  // overlap list (local ids ascending) with each node's home block and the
+  // relation of its base edge
+  HG_LAUNCH("build_overlap_flags", k_overlap_flags, dim3(gN), dim3(kBT), 0, s,
+            (const int32_t*)out->local2global, (const uint8_t*)w.sel, (const int32_t*)w.cnt, N, w.flag);
+  HG_TRY(scan_exclusive_i32(w.flag, w.pos, N, w.cnt + C_MSEL, w.scratch, s));
+  if (o->budget_M > 0)
+    HG_LAUNCH("build_overlap_fill", k_overlap_fill, dim3(gN), dim3(kBT), 0, s,
+              (const int32_t*)out->local2global, (const int32_t*)w.flag, (const int32_t*)w.pos,
+              (const int32_t*)w.cnt, g->part, (const int32_t*)w.first, g->rel, out->overlap,
+              out->overlap_home, out->overlap_rel);
   // counts needed to size the sorts
   int32_t hc[C_COUNT];
   HG_HIP_TRY(hipMemcpyAsync(hc, w.cnt, sizeof(hc), hipMemcpyDeviceToHost, s));
