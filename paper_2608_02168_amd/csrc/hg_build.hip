@@ -626,12 +626,23 @@ __global__ void k_row_count(const uint32_t* __restrict__ keys, int64_t n, int32_
   }
 }
 
+// In-degree of every CSR row (dst, r) as one byte, 255 standing for "255 or
+// more": the CSC scales look their rows up at random, in a table a quarter
+// the size of csr_ptr (and a quarter of the lines).
+__global__ void k_deg_bytes(const int32_t* __restrict__ rowcnt, int64_t nq, uint8_t* __restrict__ deg8) {
+  GRID_STRIDE(q, nq) {
+    const int32_t c = rowcnt[q];
+    deg8[q] = (uint8_t)(c < 255 ? c : 255);
+  }
+}
+
 __global__ void k_csc_scale(const uint32_t* __restrict__ kcsc, const int32_t* __restrict__ csc_row,
-                            const int32_t* __restrict__ csr_ptr, int64_t n, int32_t n_rel,
-                            float* __restrict__ scale) {
+                            const uint8_t* __restrict__ deg8, const int32_t* __restrict__ csr_ptr, int64_t n,
+                            int32_t n_rel, float* __restrict__ scale) {
   GRID_STRIDE(p, n) {
     const int64_t row = (int64_t)csc_row[p] * n_rel + (int64_t)(kcsc[p] % (uint32_t)n_rel);
-    const int32_t deg = csr_ptr[row + 1] - csr_ptr[row];
+    int32_t deg = deg8[row];
+    if (deg == 255) deg = csr_ptr[row + 1] - csr_ptr[row];
     scale[p] = 1.0f / (float)deg;
   }
 }
@@ -1040,6 +1051,10 @@ extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg
       HG_LAUNCH("build_row_count", k_row_count, dim3((unsigned)cdiv(ES, kBT)), dim3(kBT), 0, s,
                 (const uint32_t*)ko, ES, w.rowcnt);
     HG_TRY(scan_exclusive_i32(w.rowcnt, out->csr_ptr, NQ + 1, nullptr, w.scratch, s));
+    // row degrees as bytes for the CSC scales (w.digit is free until the plan)
+    if (ES > 0)
+      HG_LAUNCH("build_deg_bytes", k_deg_bytes, dim3(grid_for(NQ)), dim3(kBT), 0, s, (const int32_t*)w.rowcnt, NQ,
+                w.digit);
   }
   {
     uint32_t* ko;
@@ -1055,8 +1070,8 @@ extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg
     HG_TRY(scan_exclusive_i32(w.rowcnt, out->csc_ptr, NQ + 1, nullptr, w.scratch, s));
     if (ES > 0)
       HG_LAUNCH("build_csc_scale", k_csc_scale, dim3(grid_for(ES)), dim3(kBT), 0, s,
-                (const uint32_t*)ko, (const int32_t*)out->csc_row, (const int32_t*)out->csr_ptr, ES,
-                (int32_t)R, out->csc_scale);
+                (const uint32_t*)ko, (const int32_t*)out->csc_row, (const uint8_t*)w.digit,
+                (const int32_t*)out->csr_ptr, ES, (int32_t)R, out->csc_scale);
   }
   // 8. plan: active-source lists and backward work items
   PlanLayout pl(N, E, R);

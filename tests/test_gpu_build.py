@@ -87,6 +87,34 @@ def test_build_single_type_single_relation_and_ragged():
     assert_same(ref, sub)
 
 
+@pytest.mark.parametrize("parts", [0, 3])
+def test_build_hub_destinations(parts):
+    """Rows (dst, r) with 254, 255, 256 and 1000 in-edges: the mean weight of
+    a row past the byte table's range comes from the row pointers."""
+    rng = np.random.default_rng(8)
+    n, R = 700, 2
+    hubs = {3: 254, 10: 255, 11: 256, 20: 1000, 30: 3000}
+    src = [rng.integers(0, n, 4000)]
+    dst = [rng.integers(0, n, 4000)]
+    rel = [rng.integers(0, R, 4000)]
+    for h, k in hubs.items():
+        src.append(rng.integers(0, n, k))
+        dst.append(np.full(k, h))
+        rel.append(np.full(k, 1))
+    perm = rng.permutation(sum(len(x) for x in src))
+    src = np.concatenate(src)[perm].astype(np.int32)
+    dst = np.concatenate(dst)[perm].astype(np.int32)
+    rel = np.concatenate(rel)[perm].astype(np.uint8)
+    ntype = (rng.random(n) < 0.2).astype(np.uint8)
+    part = (synth.random_partition(n, 3, 2) if parts else (np.arange(n) >= 600).astype(np.int32))
+    part[list(hubs)] = 0
+    ref = select.build(src, dst, rel, ntype, part, 0, R, 2, 150, 0, select.THETA_NONE, 5)
+    t = lambda x: torch.from_numpy(np.ascontiguousarray(x)).cuda()
+    sub = api.hg_build_csr(t(src), t(dst), t(rel), t(ntype), t(part), 0, R, 2, 150, seed=5)
+    assert_same(ref, sub)
+    assert ref.csc_scale.min() < 1.0 / 255
+
+
 def test_build_no_edges_and_zero_budget():
     n = 100
     z32 = torch.zeros(0, dtype=torch.int32, device="cuda")
