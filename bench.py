@@ -179,10 +179,9 @@ def main():
     dom = max(spmm, key=lambda k: spmm[k][1])
     launches, total_ms = spmm[dom]
     avg_ms = total_ms / launches
-    # launches of the dominant kernel per step and layer, per snapshot: the
-    # forward runs twice for every snapshot but the last (its activations are
-    # computed again before its backward), each backward pass once
-    per_snap = [2 if (seq and dom.endswith("fwd") and i < len(subs) - 1) else 1 for i in range(len(subs))]
+    # launches of the dominant kernel per step and layer: one per snapshot
+    # (every snapshot keeps its activations for the backward)
+    per_snap = [1 for _ in subs]
     step_bytes = L * sum(n * algorithmic_cost(dom, inf)[0] for n, inf in zip(per_snap, infos))
     assert launches == args.steps * L * sum(per_snap), (dom, launches)
     nbytes = step_bytes / (L * sum(per_snap))

@@ -247,6 +247,11 @@ typedef struct hg_hgt_desc {
   int32_t dtype;     /* HG_DTYPE_F32 */
   int32_t relu;      /* 0 or 1 */
   int32_t residual;  /* 0 or 1 */
+  int32_t lean;      /* 0 or 1: `saved` leaves out the relation transforms of K
+                        and V (about 5/7 of it at R = 5); the forward keeps them
+                        in its workspace and the backward computes them again.
+                        Sizes and results follow the flag; forward and backward
+                        must be called with the same value. */
 } hg_hgt_desc;
 
 typedef struct hg_hgt_weights {

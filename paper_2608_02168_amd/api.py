@@ -87,7 +87,7 @@ HGT_PARAMS = ("W_K", "b_K", "W_Q", "b_Q", "W_V", "b_V", "W_att", "W_msg", "mu", 
 
 class HgtDesc(C.Structure):
     _fields_ = [("d", C.c_int32), ("heads", C.c_int32), ("dtype", C.c_int32), ("relu", C.c_int32),
-                ("residual", C.c_int32)]
+                ("residual", C.c_int32), ("lean", C.c_int32)]
 
 
 class HgtWeights(C.Structure):
@@ -353,8 +353,8 @@ def hg_layer_bwd(sub: Subgraph, H_in, W_rel, W_self, saved, dH_out, relu=True, r
     return dH_in, dW_rel, dW_self, dbias
 
 
-def _hgt_desc(d: int, heads: int, relu: bool, residual: bool) -> HgtDesc:
-    return HgtDesc(d, heads, HG_DTYPE_F32, int(relu), int(residual))
+def _hgt_desc(d: int, heads: int, relu: bool, residual: bool, lean: bool = False) -> HgtDesc:
+    return HgtDesc(d, heads, HG_DTYPE_F32, int(relu), int(residual), int(lean))
 
 
 def _hgt_struct(weights: dict) -> HgtWeights:
@@ -362,27 +362,28 @@ def _hgt_struct(weights: dict) -> HgtWeights:
     return HgtWeights(*[_ptr(weights.get(n)) for n in HGT_PARAMS])
 
 
-def hg_hgt_saved_size(sub: Subgraph, d: int, heads: int) -> int:
-    desc = _hgt_desc(d, heads, True, True)
+def hg_hgt_saved_size(sub: Subgraph, d: int, heads: int, lean: bool = False) -> int:
+    desc = _hgt_desc(d, heads, True, True, lean)
     return int(lib().hg_hgt_saved_size(C.byref(sub.c), C.byref(desc)))
 
 
-def hg_hgt_fwd_workspace_size(sub: Subgraph, d: int, heads: int) -> int:
-    desc = _hgt_desc(d, heads, True, True)
+def hg_hgt_fwd_workspace_size(sub: Subgraph, d: int, heads: int, lean: bool = False) -> int:
+    desc = _hgt_desc(d, heads, True, True, lean)
     return int(lib().hg_hgt_fwd_workspace_size(C.byref(sub.c), C.byref(desc)))
 
 
-def hg_hgt_bwd_workspace_size(sub: Subgraph, d: int, heads: int) -> int:
-    desc = _hgt_desc(d, heads, True, True)
+def hg_hgt_bwd_workspace_size(sub: Subgraph, d: int, heads: int, lean: bool = False) -> int:
+    desc = _hgt_desc(d, heads, True, True, lean)
     return int(lib().hg_hgt_bwd_workspace_size(C.byref(sub.c), C.byref(desc)))
 
 
 def hg_hgt_fwd(sub: Subgraph, H_in, weights: dict, heads: int, relu=True, residual=True, H_out=None,
-               mask=None, saved=None, ws=None, stream=None):
+               mask=None, saved=None, ws=None, stream=None, lean=False):
     """Attention layer forward; returns (H_out, mask, saved): mask is the ReLU
-    bitmask [n_sub, d/32] int32, saved a uint8 buffer for the backward."""
+    bitmask [n_sub, d/32] int32, saved a uint8 buffer for the backward (lean:
+    without the relation transforms, which the backward computes again)."""
     d = int(H_in.shape[1])
-    desc = _hgt_desc(d, heads, relu, residual)
+    desc = _hgt_desc(d, heads, relu, residual, lean)
     L = lib()
     if H_out is None:
         H_out = torch.empty_like(H_in)
@@ -399,12 +400,12 @@ def hg_hgt_fwd(sub: Subgraph, H_in, weights: dict, heads: int, relu=True, residu
 
 
 def hg_hgt_bwd(sub: Subgraph, H_in, weights: dict, heads: int, mask, saved, dH_out, relu=True, residual=True,
-               dH_in=None, grads: Optional[dict] = None, accumulate: bool = False, ws=None, stream=None):
+               dH_in=None, grads: Optional[dict] = None, accumulate: bool = False, ws=None, stream=None, lean=False):
     """Attention layer backward; returns (dH_in, grads) with grads a dict of
     the same names as the weights (bias gradients for the biases given),
-    overwritten, or added into when accumulate."""
+    overwritten, or added into when accumulate.  lean as in the forward."""
     d = int(H_in.shape[1])
-    desc = _hgt_desc(d, heads, relu, residual)
+    desc = _hgt_desc(d, heads, relu, residual, lean)
     L = lib()
     if dH_in is None:
         dH_in = torch.empty_like(H_in)

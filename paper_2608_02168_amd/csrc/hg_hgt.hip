@@ -36,22 +36,27 @@ int validate_hgt(const hg_subgraph* s, const hg_hgt_desc* L) {
   if (!hgt_shape_ok(L->d, L->heads))
     return fail(HG_ERR_UNSUPPORTED, "attention layer: d in {64, 128} and d / heads a power of two >= 4 (d=%d, heads=%d)",
                 L->d, L->heads);
-  if ((L->relu != 0 && L->relu != 1) || (L->residual != 0 && L->residual != 1))
-    return fail(HG_ERR_ARG, "relu and residual must be 0 or 1");
+  if ((L->relu != 0 && L->relu != 1) || (L->residual != 0 && L->residual != 1) || (L->lean != 0 && L->lean != 1))
+    return fail(HG_ERR_ARG, "relu, residual and lean must be 0 or 1");
   if (s->n_rel < 1 || s->n_ntype < 1) return fail(HG_ERR_ARG, "subgraph has no relations or node types");
   if (s->n_sub < 0 || s->e_sub < 0) return fail(HG_ERR_ARG, "subgraph sizes are negative");
   return HG_OK;
 }
 
 // Layout of `saved` (float32 unless noted).
+// The forward's intermediates for the backward.  A lean layer keeps Kt and
+// Vt out of them (they are 5/7 of the bytes at R = 5): the forward writes them
+// to its workspace and the backward computes them again from K and V, two row
+// transforms instead of a whole forward, so that a caller holding the layers
+// of several snapshots at once keeps 2/7 of the bytes per layer.
 struct HgtSaved {
   float *K, *Q, *V;   // [n_sub, d]
-  float *Kt, *Vt;     // [n_sub * R, d], rows src * R + r of active (src, r)
+  float *Kt, *Vt;     // [n_sub * R, d], rows src * R + r of active (src, r); absent when lean
   float* ht;          // [n_sub, d]
   float* lse;         // [n_sub, S]
   template <class A>
-  void layout(A& a, const hg_subgraph* s, int d, int S) {
-    const int64_t n = s->n_sub, nr = s->n_sub * (int64_t)s->n_rel;
+  void layout(A& a, const hg_subgraph* s, int d, int S, bool lean) {
+    const int64_t n = s->n_sub, nr = lean ? 0 : s->n_sub * (int64_t)s->n_rel;
     K = a.template take<float>(n * d);
     Q = a.template take<float>(n * d);
     V = a.template take<float>(n * d);
@@ -64,10 +69,14 @@ struct HgtSaved {
 
 struct HgtFwdWs {
   float *Watt, *Wmsg;  // [R, d, d] block-diagonal expansions
+  float *Kt, *Vt;      // lean layers: [n_sub * R, d]
   template <class A>
-  void layout(A& a, const hg_subgraph* s, int d) {
+  void layout(A& a, const hg_subgraph* s, int d, bool lean) {
+    const int64_t nr = lean ? s->n_sub * (int64_t)s->n_rel : 0;
     Watt = a.template take<float>((int64_t)s->n_rel * d * d);
     Wmsg = a.template take<float>((int64_t)s->n_rel * d * d);
+    Kt = a.template take<float>(nr * d);
+    Vt = a.template take<float>(nr * d);
   }
 };
 
@@ -218,17 +227,42 @@ inline unsigned attn_grid(int64_t rows) {
   return (unsigned)(blocks > 0 ? blocks : 1);
 }
 
+// Kt = K W_att[r] and Vt = V W_msg[r] for the active sources of each
+// relation, at rows src * R + r (Watt, Wmsg: the block-diagonal expansions).
+template <int D>
+int rel_transforms(const hg_subgraph* s, const PlanView& pv, const float* Watt, const float* Wmsg, const float* K,
+                   const float* V, float* Kt, float* Vt, hipStream_t st) {
+  const int32_t R = s->n_rel;
+  int64_t off = 0;
+  for (int r = 0; r < R; ++r) {
+    const int64_t n = s->n_active[r];
+    const float* wa = Watt + (int64_t)r * D * D;
+    const float* wm = Wmsg + (int64_t)r * D * D;
+    HG_TRY((launch_gemm_rows_pp<D, false>("hgt_rel", n, wa, LoadRows<D, float>{K, rows_list(pv.active + off)},
+                                          StoreRows<D, float>{Kt, rows_list(pv.active + off, R, r), nullptr, nullptr},
+                                          st)));
+    HG_TRY((launch_gemm_rows_pp<D, false>("hgt_rel", n, wm, LoadRows<D, float>{V, rows_list(pv.active + off)},
+                                          StoreRows<D, float>{Vt, rows_list(pv.active + off, R, r), nullptr, nullptr},
+                                          st)));
+    off += n;
+  }
+  return HG_OK;
+}
+
 template <int D>
 int hgt_fwd_impl(const hg_subgraph* s, const hg_hgt_desc* L, const float* Hin, const hg_hgt_weights* W,
                  float* Hout, uint32_t* mask, void* saved, void* ws, size_t ws_bytes, hipStream_t st) {
   const int S = L->heads;
   const int32_t R = s->n_rel, T = s->n_ntype;
+  const bool lean = L->lean != 0;
   Arena as(saved, (size_t)-1);
   HgtSaved sv;
-  sv.layout(as, s, D, S);
+  sv.layout(as, s, D, S, lean);
   Arena a(ws, ws_bytes);
   HgtFwdWs w;
-  w.layout(a, s, D);
+  w.layout(a, s, D, lean);
+  float* Kt = lean ? w.Kt : sv.Kt;
+  float* Vt = lean ? w.Vt : sv.Vt;
   if (!a.ok()) return fail(HG_ERR_CAPACITY, "attention forward workspace needs %zu bytes, got %zu", a.used, ws_bytes);
   const PlanView pv = plan_view(s);
   // block-diagonal relation matrices
@@ -254,26 +288,14 @@ int hgt_fwd_impl(const hg_subgraph* s, const hg_hgt_desc* L, const float* Hin, c
                                           st)));
   }
   // (2) relation transforms of the keys and values of each relation's active sources
-  int64_t off = 0;
-  for (int r = 0; r < R; ++r) {
-    const int64_t n = s->n_active[r];
-    const float* wa = w.Watt + (int64_t)r * D * D;
-    const float* wm = w.Wmsg + (int64_t)r * D * D;
-    HG_TRY((launch_gemm_rows_pp<D, false>("hgt_rel", n, wa, LoadRows<D, float>{sv.K, rows_list(pv.active + off)},
-                                          StoreRows<D, float>{sv.Kt, rows_list(pv.active + off, R, r), nullptr, nullptr},
-                                          st)));
-    HG_TRY((launch_gemm_rows_pp<D, false>("hgt_rel", n, wm, LoadRows<D, float>{sv.V, rows_list(pv.active + off)},
-                                          StoreRows<D, float>{sv.Vt, rows_list(pv.active + off, R, r), nullptr, nullptr},
-                                          st)));
-    off += n;
-  }
+  HG_TRY(rel_transforms<D>(s, pv, w.Watt, w.Wmsg, sv.K, sv.V, Kt, Vt, st));
   // (3) attention-weighted aggregation
   const float inv_sqrt_dk = 1.0f / std::sqrt((float)(D / S));
   if (s->n_sub > 0) {
 #define HG_ATTN_FWD(S_)                                                                                         \
   HG_LAUNCH("hgt_attn_fwd", (k_hgt_attn_fwd<D, S_>), dim3(attn_grid(s->n_sub)), dim3(kAttnThreads), 0, st,     \
             s->n_sub, R, T, (const int32_t*)s->type_off, (const int32_t*)s->csr_ptr, (const int32_t*)s->csr_col, \
-            (const float*)sv.Q, (const float*)sv.Kt, (const float*)sv.Vt, W->mu, inv_sqrt_dk, sv.ht, sv.lse)
+            (const float*)sv.Q, (const float*)Kt, (const float*)Vt, W->mu, inv_sqrt_dk, sv.ht, sv.lse)
     switch (D / S) {
       case 4: HG_ATTN_FWD(D / 4); break;
       case 8: HG_ATTN_FWD(D / 8); break;
@@ -318,13 +340,14 @@ struct HgtBwdWs {
   float *Watt, *Wmsg;              // [R, d, d] block-diagonal expansions
   float *gatt, *gmsg;              // [R, d, d] full gradients before the block extraction
   float *splitk, *colsum;          // split-K partials
+  float *Kt, *Vt;                  // lean layers: Kt and Vt computed again, [n_sub * R, d]
   template <class A>
-  void layout(A& a, const hg_subgraph* s, int d, int S);
+  void layout(A& a, const hg_subgraph* s, int d, int S, bool lean);
 };
 constexpr int kMuChunks = 64;
 
 template <class A>
-void HgtBwdWs::layout(A& a, const hg_subgraph* s, int d, int S) {
+void HgtBwdWs::layout(A& a, const hg_subgraph* s, int d, int S, bool lean) {
   const int64_t n = s->n_sub, R = s->n_rel, T = s->n_ntype;
   dZ = a.template take<float>(n * d);
   dht = a.template take<float>(n * d);
@@ -345,6 +368,9 @@ void HgtBwdWs::layout(A& a, const hg_subgraph* s, int d, int S) {
   gmsg = a.template take<float>(R * d * d);
   splitk = a.template take<float>(splitk_max_chunks() * (int64_t)d * d);
   colsum = a.template take<float>(splitk_max_chunks() * (int64_t)d);
+  const int64_t nr = lean ? n * R : 0;
+  Kt = a.template take<float>(nr * d);
+  Vt = a.template take<float>(nr * d);
 }
 
 template <int LPH>
@@ -621,12 +647,13 @@ int hgt_bwd_impl(const hg_subgraph* s, const hg_hgt_desc* L, const float* Hin, c
                  int acc, void* ws, size_t ws_bytes, hipStream_t st) {
   const int S = L->heads;
   const int32_t R = s->n_rel, T = s->n_ntype;
+  const bool lean = L->lean != 0;
   Arena as(const_cast<void*>(saved), (size_t)-1);
   HgtSaved sv;
-  sv.layout(as, s, D, S);
+  sv.layout(as, s, D, S, lean);
   Arena a(ws, ws_bytes);
   HgtBwdWs w;
-  w.layout(a, s, D, S);
+  w.layout(a, s, D, S, lean);
   if (!a.ok()) return fail(HG_ERR_CAPACITY, "attention backward workspace needs %zu bytes, got %zu", a.used, ws_bytes);
   const PlanView pv = plan_view(s);
   const float inv_sqrt_dk = 1.0f / std::sqrt((float)(D / S));
@@ -636,6 +663,10 @@ int hgt_bwd_impl(const hg_subgraph* s, const hg_hgt_desc* L, const float* Hin, c
     HG_LAUNCH("hgt_blockdiag", k_blockdiag, dim3(g), dim3(256), 0, st, W->W_att, (int64_t)R, D, S, w.Watt);
     HG_LAUNCH("hgt_blockdiag", k_blockdiag, dim3(g), dim3(256), 0, st, W->W_msg, (int64_t)R, D, S, w.Wmsg);
   }
+  // a lean layer's Kt and Vt, from the saved K and V
+  if (lean) HG_TRY(rel_transforms<D>(s, pv, w.Watt, w.Wmsg, sv.K, sv.V, w.Kt, w.Vt, st));
+  const float* Kt = lean ? w.Kt : sv.Kt;
+  const float* Vt = lean ? w.Vt : sv.Vt;
   // (1) dZ = G * mask (written by the A load), dh~ = dZ W_agg^T; dW_agg, db_agg
   for (int t = 0; t < T; ++t) {
     const int64_t lo = s->type_off_host[t], hi = s->type_off_host[t + 1];
@@ -652,12 +683,12 @@ int hgt_bwd_impl(const hg_subgraph* s, const hg_hgt_desc* L, const float* Hin, c
   do {                                                                                                                \
     HG_LAUNCH("hgt_attn_bwd_dst", (k_hgt_attn_bwd_dst<D, S_>), dim3(attn_grid(s->n_sub)), dim3(kAttnThreads), 0, st, \
               s->n_sub, R, T, (const int32_t*)s->type_off, (const int32_t*)s->csr_ptr, (const int32_t*)s->csr_col,   \
-              (const float*)sv.Q, (const float*)sv.Kt, (const float*)sv.Vt, (const float*)sv.ht,                     \
+              (const float*)sv.Q, Kt, Vt, (const float*)sv.ht,                                                        \
               (const float*)w.dht, (const float*)sv.lse, W->mu, inv_sqrt_dk, w.dQ, w.ld, w.contrib);                 \
     if (s->plan_items > 0)                                                                                            \
       HG_LAUNCH("hgt_attn_bwd_src", (k_hgt_attn_bwd_src<D, S_>), dim3(attn_grid(s->plan_items)), dim3(kAttnThreads),  \
                 0, st, (int64_t)s->plan_items, pv.items, R, T, (const int32_t*)s->type_off,                           \
-                (const int32_t*)s->csc_row, (const float*)sv.Q, (const float*)sv.Kt, (const float*)sv.Vt,             \
+                (const int32_t*)s->csc_row, (const float*)sv.Q, Kt, Vt,                                               \
                 (const float*)w.dht, (const float*)w.ld, W->mu, inv_sqrt_dk, w.dKt, w.dVt,                            \
                 w.pk, w.pv);                                                                                          \
   } while (0)
@@ -737,10 +768,10 @@ int hgt_bwd_impl(const hg_subgraph* s, const hg_hgt_desc* L, const float* Hin, c
   return HG_OK;
 }
 
-size_t saved_size(const hg_subgraph* s, int d, int S) {
+size_t saved_size(const hg_subgraph* s, int d, int S, bool lean) {
   Sizer z;
   HgtSaved sv;
-  sv.layout(z, s, d, S);
+  sv.layout(z, s, d, S, lean);
   return z.used;
 }
 
@@ -753,14 +784,14 @@ extern "C" {
 
 size_t hg_hgt_saved_size(const hg_subgraph* s, const hg_hgt_desc* L) {
   if (!s || !L || !hgt_shape_ok(L->d, L->heads)) return 0;
-  return saved_size(s, L->d, L->heads);
+  return saved_size(s, L->d, L->heads, L->lean != 0);
 }
 
 size_t hg_hgt_fwd_workspace_size(const hg_subgraph* s, const hg_hgt_desc* L) {
   if (!s || !L || !hgt_shape_ok(L->d, L->heads)) return 0;
   Sizer z;
   HgtFwdWs w;
-  w.layout(z, s, L->d);
+  w.layout(z, s, L->d, L->lean != 0);
   return z.used;
 }
 
@@ -768,7 +799,7 @@ size_t hg_hgt_bwd_workspace_size(const hg_subgraph* s, const hg_hgt_desc* L) {
   if (!s || !L || !hgt_shape_ok(L->d, L->heads)) return 0;
   Sizer z;
   HgtBwdWs w;
-  w.layout(z, s, L->d, L->heads);
+  w.layout(z, s, L->d, L->heads, L->lean != 0);
   return z.used;
 }
 

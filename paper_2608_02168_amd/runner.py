@@ -221,9 +221,11 @@ class SeqInputs:
     href_np: np.ndarray
     feats_np: np.ndarray
     ts_np: np.ndarray
-    H: List[torch.Tensor] = field(default_factory=list)       # layer activations of the current snapshot
-    masks: List[torch.Tensor] = field(default_factory=list)
-    saved: List[torch.Tensor] = field(default_factory=list)
+    H: List[torch.Tensor] = field(default_factory=list)       # layer activations of the latest snapshot run
+    masks: List[torch.Tensor] = field(default_factory=list)   # its ReLU masks
+    Hs: List[List[torch.Tensor]] = field(default_factory=list)     # Hs[t][l]: every snapshot's activations
+    ms: List[List[torch.Tensor]] = field(default_factory=list)     # ms[t][l]: their masks
+    saved: List[List[torch.Tensor]] = field(default_factory=list)  # saved[t][l]: lean attention intermediates
     S: List[torch.Tensor] = field(default_factory=list)       # temporal states, one per snapshot
     dS: List[torch.Tensor] = field(default_factory=list)
     dH: List[torch.Tensor] = field(default_factory=list)      # ping-pong gradient buffers
@@ -286,17 +288,25 @@ def make_seq_inputs(wl: synth.Workload, g: synth.Graph, device="cuda") -> SeqInp
                     labels, labels_np, _label_rows(labels), _dev(href_np[:m], device), href_np, feats, ts_np)
     ns = sub0.n_sub
     f32 = dict(dtype=torch.float32, device=device)
-    inp.H = [h0] + [torch.empty((ns, d), **f32) for _ in range(mc.n_layers)]
-    inp.masks = [torch.empty((max(ns, 1), d // 32), dtype=torch.int32, device=device) for _ in range(mc.n_layers)]
-    inp.saved = [api._ws(api.hg_hgt_saved_size(sub0, d, mc.heads), device) for _ in range(mc.n_layers)]
+    # every snapshot keeps its activations, masks and lean intermediates (the
+    # relation transforms are left out of them and computed again in the
+    # backward), so the backward never runs an earlier snapshot's forward again
+    inp.Hs = [[h0] + [torch.empty((ns, d), **f32) for _ in range(mc.n_layers)] for _ in range(T)]
+    inp.ms = [[torch.empty((max(ns, 1), d // 32), dtype=torch.int32, device=device) for _ in range(mc.n_layers)]
+              for _ in range(T)]
+    inp.saved = [[api._ws(api.hg_hgt_saved_size(sb, d, mc.heads, lean=True), device) for _ in range(mc.n_layers)]
+                 for sb in subs]
+    inp.H, inp.masks = inp.Hs[0], inp.ms[0]
     inp.S = [torch.empty((ns, d), **f32) for _ in range(T)]
     inp.dS = [torch.empty((ns, d), **f32) for _ in range(T)]
     inp.dH = [torch.empty((ns, d), **f32) for _ in range(2)]
     inp.grads = [{n: torch.empty_like(v) for n, v in w.items()} for w in weights]
     inp.tgrads = {k: torch.empty_like(v) for k, v in tparams.items()}
     inp.head_grads = {k: torch.empty_like(v) for k, v in head.items()}
-    inp.fwd_ws = api._ws(max(api.hg_hgt_fwd_workspace_size(s, d, mc.heads) for s in subs), device)
-    inp.bwd_ws = api._ws(max(api.hg_hgt_bwd_workspace_size(s, d, mc.heads) for s in subs), device)
+    # forward and backward never overlap: one workspace serves both
+    inp.fwd_ws = api._ws(max(max(api.hg_hgt_fwd_workspace_size(s, d, mc.heads, lean=True),
+                                 api.hg_hgt_bwd_workspace_size(s, d, mc.heads, lean=True)) for s in subs), device)
+    inp.bwd_ws = inp.fwd_ws
     inp.t_ws = api._ws(api.hg_temporal_bwd_workspace_size(ns, d, min(mc.window, T - 1)), device)
     inp.align_ws = api._ws(api.hg_align_workspace_size(m, d), device)
     inp.head_ws = api._ws(api.hg_mlp_bce_workspace_size(ns, d), device)
@@ -313,9 +323,11 @@ def make_seq_inputs(wl: synth.Workload, g: synth.Graph, device="cuda") -> SeqInp
 
 def _seq_layers_fwd(inp: SeqInputs, t: int):
     mc = inp.wl.model
+    H, m = inp.Hs[t], inp.ms[t]
     for li in range(mc.n_layers):
-        api.hg_hgt_fwd(inp.subs[t], inp.H[li], inp.weights[li], mc.heads, H_out=inp.H[li + 1], mask=inp.masks[li],
-                       saved=inp.saved[li], ws=inp.fwd_ws)
+        api.hg_hgt_fwd(inp.subs[t], H[li], inp.weights[li], mc.heads, H_out=H[li + 1], mask=m[li],
+                       saved=inp.saved[t][li], ws=inp.fwd_ws, lean=True)
+    inp.H, inp.masks = H, m
 
 
 def run_seq_step(inp: SeqInputs, rebuild: bool = True, update: bool = True, on_snapshot=None):
@@ -323,11 +335,11 @@ def run_seq_step(inp: SeqInputs, rebuild: bool = True, update: bool = True, on_s
     attention layers give h^t and the temporal module S^t = GRU(h^t,
     attention over the previous min(t, w) states); the head's masked BCE and
     the alignment act on the last state.  The backward runs through every
-    snapshot, latest first: the layer activations of snapshot t are computed
-    again from the shared input features before its backward (only the last
-    snapshot's are still held), the temporal backward adds each context
-    state's gradient into that state's buffer, and the shared weights sum
-    their per-snapshot gradients.  Then Adam updates every parameter.
+    snapshot, latest first, from the activations every snapshot kept (the
+    attention layers' relation transforms are computed again from their
+    kept keys and values), the temporal backward adds each context state's
+    gradient into that state's buffer, and the shared weights sum their
+    per-snapshot gradients.  Then Adam updates every parameter.
     `on_snapshot(t)`, if given, is called after the forward of snapshot t
     (its layer activations and masks are then in inp.H and inp.masks)."""
     cfg, mc = inp.wl.graph, inp.wl.model
@@ -336,7 +348,7 @@ def run_seq_step(inp: SeqInputs, rebuild: bool = True, update: bool = True, on_s
         _build_snapshots(inp.graph, inp.k, cfg, inp.cuts, ws=inp.build_ws, subs=inp.subs)
     for t in range(T):
         _seq_layers_fwd(inp, t)
-        api.hg_temporal_fwd(inp.H[-1], inp.S[max(0, t - w):t], inp.tparams, H=inp.S[t])
+        api.hg_temporal_fwd(inp.Hs[t][-1], inp.S[max(0, t - w):t], inp.tparams, H=inp.S[t])
         if on_snapshot is not None:
             on_snapshot(t)
     g = inp.dS[T - 1]
@@ -347,16 +359,16 @@ def run_seq_step(inp: SeqInputs, rebuild: bool = True, update: bool = True, on_s
     for j in range(T - 1):
         inp.dS[j].zero_()
     for t in reversed(range(T)):
-        if t < T - 1:
-            _seq_layers_fwd(inp, t)
+        H, m = inp.Hs[t], inp.ms[t]
         lo = max(0, t - w)
         acc = t < T - 1
         cur, nxt = 0, 1
-        api.hg_temporal_bwd(inp.H[-1], inp.S[lo:t], inp.tparams, inp.dS[t], dh=inp.dH[cur], dstates=inp.dS[lo:t],
+        api.hg_temporal_bwd(H[-1], inp.S[lo:t], inp.tparams, inp.dS[t], dh=inp.dH[cur], dstates=inp.dS[lo:t],
                             grads=inp.tgrads, accumulate=acc, ws=inp.t_ws)
         for li in reversed(range(mc.n_layers)):
-            api.hg_hgt_bwd(inp.subs[t], inp.H[li], inp.weights[li], mc.heads, inp.masks[li], inp.saved[li],
-                           inp.dH[cur], dH_in=inp.dH[nxt], grads=inp.grads[li], accumulate=acc, ws=inp.bwd_ws)
+            api.hg_hgt_bwd(inp.subs[t], H[li], inp.weights[li], mc.heads, m[li], inp.saved[t][li],
+                           inp.dH[cur], dH_in=inp.dH[nxt], grads=inp.grads[li], accumulate=acc, ws=inp.bwd_ws,
+                           lean=True)
             cur, nxt = nxt, cur
     if update:
         inp.t += 1

@@ -148,3 +148,25 @@ def test_hgt_backward_accumulate_sums_two_calls():
     torch.cuda.synchronize()
     errs = {n: parity_err(grads[n].cpu().numpy(), getattr(g, n)) for n in hgt.PARAM_NAMES}
     assert max(errs.values()) <= TOL, errs
+
+
+@pytest.mark.parametrize("name", sorted(CFGS))
+def test_hgt_lean_saved_gives_identical_results(name):
+    """A lean layer (relation transforms left out of `saved`, computed again
+    in the backward) returns bit for bit what the full layer returns, from a
+    smaller `saved`."""
+    cfg, d, heads = CFGS[name]
+    ref, sub, X, w = setup(cfg, d, heads)
+    G = to_dev(synth.upstream_grad(7, ref.n_sub, d))
+    Xd, wd = to_dev(X), dev_weights(w)
+    out = {}
+    for lean in (False, True):
+        H, mask, saved = api.hg_hgt_fwd(sub, Xd, wd, heads, lean=lean)
+        dH, grads = api.hg_hgt_bwd(sub, Xd, wd, heads, mask, saved, G, lean=lean)
+        torch.cuda.synchronize()
+        out[lean] = (H.cpu(), mask.cpu(), dH.cpu(), {n: v.cpu() for n, v in grads.items()}, saved.numel())
+    a, b = out[False], out[True]
+    assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1]) and torch.equal(a[2], b[2])
+    for n in a[3]:
+        assert torch.equal(a[3][n], b[3][n]), n
+    assert b[4] < a[4]
