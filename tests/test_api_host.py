@@ -285,3 +285,21 @@ def test_head_rejects_bad_row_lists(L):
     assert L.hg_mlp_bce_fwd_bwd(*args(fake, 11, None)) == api.HG_ERR_ARG   # longer than the rows
     assert L.hg_mlp_bce_fwd_bwd(*args(fake, -1, None)) == api.HG_ERR_ARG
     assert L.hg_mlp_bce_fwd_bwd(*args(fake, 4, fake)) == api.HG_ERR_ARG    # prob needs every row
+
+
+def test_hgt_descriptor_flags_and_lean_sizes(L):
+    s = _sub(n_sub=1000, R=5, T=2)
+    full = api.HgtDesc(64, 4, 0, 1, 1, 0)
+    lean = api.HgtDesc(64, 4, 0, 1, 1, 1)
+    bad = api.HgtDesc(64, 4, 0, 1, 1, 2)
+    fake = C.c_void_p(0x1000)
+    w = api.HgtWeights(*([fake] * 11))
+    # the relation transforms (2 x n_sub x R x d floats) leave `saved` and go to the workspaces
+    kt = 2 * 1000 * 5 * 64 * 4
+    assert L.hg_hgt_saved_size(C.byref(s), C.byref(full)) - L.hg_hgt_saved_size(C.byref(s), C.byref(lean)) == kt
+    assert L.hg_hgt_fwd_workspace_size(C.byref(s), C.byref(lean)) - \
+        L.hg_hgt_fwd_workspace_size(C.byref(s), C.byref(full)) >= kt
+    assert L.hg_hgt_bwd_workspace_size(C.byref(s), C.byref(lean)) - \
+        L.hg_hgt_bwd_workspace_size(C.byref(s), C.byref(full)) >= kt
+    assert L.hg_hgt_fwd(C.byref(s), C.byref(bad), fake, C.byref(w), fake, fake, fake, fake, 1 << 30,
+                        None) == api.HG_ERR_ARG

@@ -127,6 +127,18 @@ def test_build_no_edges_and_zero_budget():
     assert int(sub.view("csr_ptr").abs().sum()) == 0
 
 
+def test_build_single_row_needs_no_sort_pass():
+    # one node, one relation: every CSR/CSC key is 0 (no radix pass runs)
+    src = torch.zeros(7, dtype=torch.int32, device="cuda")
+    rel = torch.zeros(7, dtype=torch.uint8, device="cuda")
+    ntype = torch.zeros(1, dtype=torch.uint8, device="cuda")
+    part = torch.zeros(1, dtype=torch.int32, device="cuda")
+    ref = select.build(np.zeros(7, np.int32), np.zeros(7, np.int32), np.zeros(7, np.uint8), np.zeros(1, np.uint8),
+                       np.zeros(1, np.int32), 0, 1, 1, 0, 0, select.THETA_NONE, 0)
+    sub = api.hg_build_csr(src, src, rel, ntype, part, 0, 1, 1, 0)
+    assert_same(ref, sub)
+
+
 def test_build_range_error_is_reported():
     n = 50
     src = torch.tensor([1, 2, 70], dtype=torch.int32, device="cuda")  # 70 >= n
