@@ -608,21 +608,64 @@ __global__ void k_edge_compact(const int32_t* __restrict__ src, const int32_t* _
   }
 }
 
-// Row lengths of sorted keys: one atomic per run of equal keys inside a wave.
-__global__ void k_row_count(const uint32_t* __restrict__ keys, int64_t n, int32_t* __restrict__ cnt) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int lane = threadIdx.x & (kWave - 1);
-  const bool valid = i < n;
-  const uint32_t k = valid ? keys[i] : 0xFFFFFFFFu;
-  const uint32_t kp = __shfl_up(k, 1, kWave);
-  const bool start = valid && (lane == 0 || k != kp);
-  const uint64_t starts = __ballot(start);
-  const int nvalid = __popcll(__ballot(valid));
-  if (start) {
-    const uint64_t above = (lane == kWave - 1) ? 0ull : (starts & ~((2ull << lane) - 1ull));
-    int next = above ? __ffsll((long long)above) - 1 : kWave;
-    if (next > nvalid) next = nvalid;
-    atomicAdd(&cnt[k], next - lane);
+// Row lengths of sorted keys.  A block takes kRCChunk consecutive keys (16
+// contiguous ones per thread); a run of equal keys that lies inside the chunk
+// is counted by a plain store (no other block sees that key), the chunk's
+// first and last runs, which may continue into a neighbour, by an atomic
+// add.  A row of any length then costs at most one atomic per chunk it
+// touches (a hub's row of millions of entries no longer serialises one
+// atomic per wave on one counter).  cnt must be zero on entry.
+constexpr int kRCItems = 16;
+constexpr int kRCChunk = kBT * kRCItems;
+__global__ void __launch_bounds__(kBT) k_row_count(const uint32_t* __restrict__ keys, int64_t n,
+                                                   int32_t* __restrict__ cnt) {
+  __shared__ int32_t starts[kRCChunk + 1];
+  __shared__ int32_t wsum[kBT / 64];
+  const int t = threadIdx.x;
+  const int64_t base = (int64_t)blockIdx.x * kRCChunk;
+  const int m = (int)((n - base) < kRCChunk ? (n - base) : kRCChunk);
+  const int p0 = t * kRCItems;
+  uint32_t k[kRCItems];
+#pragma unroll
+  for (int j = 0; j < kRCItems; ++j) k[j] = (p0 + j < m) ? keys[base + p0 + j] : 0u;
+  uint32_t prev = (p0 > 0 && p0 - 1 < m) ? keys[base + p0 - 1] : ~k[0];
+  int nf = 0;
+#pragma unroll
+  for (int j = 0; j < kRCItems; ++j) {
+    nf += (p0 + j < m && (j == 0 ? k[0] != prev : k[j] != k[j - 1])) ? 1 : 0;
+  }
+  // exclusive scan of the run-start counts over the block
+  int inc = nf;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int v = __shfl_up(inc, o, 64);
+    if ((t & 63) >= o) inc += v;
+  }
+  if ((t & 63) == 63) wsum[t >> 6] = inc;
+  __syncthreads();
+  int off = 0, total = 0;
+#pragma unroll
+  for (int q = 0; q < kBT / 64; ++q) {
+    off += (q < (t >> 6)) ? wsum[q] : 0;
+    total += wsum[q];
+  }
+  int idx = off + inc - nf;
+#pragma unroll
+  for (int j = 0; j < kRCItems; ++j) {
+    if (p0 + j < m && (j == 0 ? k[0] != prev : k[j] != k[j - 1])) starts[idx++] = p0 + j;
+  }
+  if (t == 0) starts[total] = m;
+  __syncthreads();
+  const bool cont_in = base > 0 && m > 0 && keys[base - 1] == keys[base];
+  const bool cont_out = m > 0 && base + m < n && keys[base + m] == keys[base + m - 1];
+  for (int r = t; r < total; r += kBT) {
+    const int s0 = starts[r], len = starts[r + 1] - s0;
+    const uint32_t key = keys[base + s0];
+    if ((r == 0 && cont_in) || (r == total - 1 && cont_out)) {
+      atomicAdd(&cnt[key], len);
+    } else {
+      cnt[key] = len;
+    }
   }
 }
 
@@ -1048,7 +1091,7 @@ extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg
     }
     HG_TRY(fill_i32(w.rowcnt, 0, NQ + 1, s));
     if (ES > 0)
-      HG_LAUNCH("build_row_count", k_row_count, dim3((unsigned)cdiv(ES, kBT)), dim3(kBT), 0, s,
+      HG_LAUNCH("build_row_count", k_row_count, dim3((unsigned)cdiv(ES, kRCChunk)), dim3(kBT), 0, s,
                 (const uint32_t*)ko, ES, w.rowcnt);
     HG_TRY(scan_exclusive_i32(w.rowcnt, out->csr_ptr, NQ + 1, nullptr, w.scratch, s));
     // row degrees as bytes for the CSC scales (w.digit is free until the plan)
@@ -1065,7 +1108,7 @@ extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg
       HG_HIP_TRY(hipMemcpyAsync(out->csc_row, v1o, sizeof(int32_t) * ES, hipMemcpyDeviceToDevice, s));
     HG_TRY(fill_i32(w.rowcnt, 0, NQ + 1, s));
     if (ES > 0)
-      HG_LAUNCH("build_row_count", k_row_count, dim3((unsigned)cdiv(ES, kBT)), dim3(kBT), 0, s,
+      HG_LAUNCH("build_row_count", k_row_count, dim3((unsigned)cdiv(ES, kRCChunk)), dim3(kBT), 0, s,
                 (const uint32_t*)ko, ES, w.rowcnt);
     HG_TRY(scan_exclusive_i32(w.rowcnt, out->csc_ptr, NQ + 1, nullptr, w.scratch, s));
     if (ES > 0)

@@ -248,29 +248,58 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 4 && D <= 128) ? 8 : 4) k_s
   }
 }
 
-// Split rows: dY[q] = sum of its partial rows, in chunk order (float64).
+// Split rows: dY[q] = sum of its partial rows (float64), in a fixed order:
+// the 64 / (D/4) lane groups of the wave take interleaved partials, each
+// group with four accumulators for partials i, i + G, i + 2G, i + 3G (G the
+// group count) so that eight or more rows are in flight per wave, then the
+// accumulators and the groups are added in a fixed tree.  A hub's row of
+// millions of entries (thousands of partials) no longer waits on one load
+// at a time.
 template <int D, class T>
 __global__ void k_heavy_reduce(int64_t n_heavy, const int4* __restrict__ heavy,
                                const double* __restrict__ partial, T* __restrict__ dY) {
   constexpr int EL = 4;
   constexpr int LPR = D / EL;
+  constexpr int NG = 64 / LPR;  // lane groups per wave
+  constexpr int U = 4;
   const int l = threadIdx.x & 63;
+  const int grp = l / LPR, lr = l % LPR;
   const int64_t wave0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
   const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
   for (int64_t h = wave0; h < n_heavy; h += nwaves) {
     const int4 hv = heavy[h];
-    if (l < LPR) {
-      double s[EL];
+    double s[U][EL];
 #pragma unroll
-      for (int k = 0; k < EL; ++k) s[k] = 0.0;
-      for (int32_t i = 0; i < hv.z; ++i) {
-        const double* p = partial + (int64_t)(hv.y + i) * D + l * EL;
+    for (int u = 0; u < U; ++u)
 #pragma unroll
-        for (int k = 0; k < EL; ++k) s[k] += p[k];
-      }
-      *reinterpret_cast<f32x4*>(dY + (int64_t)hv.x * D + l * EL) =
-          f32x4{(float)s[0], (float)s[1], (float)s[2], (float)s[3]};
+      for (int k = 0; k < EL; ++k) s[u][k] = 0.0;
+    const double* base = partial + (int64_t)hv.y * D + lr * EL;
+    int32_t i = grp;
+    for (; i + (U - 1) * NG < hv.z; i += U * NG) {
+      double x[U][EL];
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int k = 0; k < EL; ++k) x[u][k] = base[(int64_t)(i + u * NG) * D + k];
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int k = 0; k < EL; ++k) s[u][k] += x[u][k];
     }
+    for (; i < hv.z; i += NG) {
+#pragma unroll
+      for (int k = 0; k < EL; ++k) s[0][k] += base[(int64_t)i * D + k];
+    }
+    double t[EL];
+#pragma unroll
+    for (int k = 0; k < EL; ++k) t[k] = (s[0][k] + s[1][k]) + (s[2][k] + s[3][k]);
+#pragma unroll
+    for (int o = LPR; o < 64; o <<= 1)
+#pragma unroll
+      for (int k = 0; k < EL; ++k) t[k] += __shfl_xor(t[k], o, 64);
+    if (grp == 0)
+      *reinterpret_cast<f32x4*>(dY + (int64_t)hv.x * D + lr * EL) =
+          f32x4{(float)t[0], (float)t[1], (float)t[2], (float)t[3]};
   }
 }
 
