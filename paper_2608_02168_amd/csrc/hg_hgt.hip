@@ -580,20 +580,43 @@ __global__ void __launch_bounds__(kAttnThreads) k_hgt_attn_bwd_src(
 template <int D>
 __global__ void k_hgt_heavy_reduce(int64_t n_heavy, const int4* __restrict__ heavy, const double* __restrict__ pk,
                                    const double* __restrict__ pv, float* __restrict__ dKt, float* __restrict__ dVt) {
-  constexpr int LPR = D / 4;
+  // as the mean layer's split-row reduction: the lane groups of the wave take
+  // interleaved partials, two per group in flight, fixed-order combination
+  constexpr int LPR = D / 4, NG = 64 / LPR;
   const int l = threadIdx.x & 63;
+  const int grp = l / LPR, lr = l % LPR;
   const int64_t wave0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
   const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
   for (int64_t h = wave0; h < n_heavy; h += nwaves) {
     const int4 hv = heavy[h];
-    if (l < LPR) {
-      f64x4 a = {0.0, 0.0, 0.0, 0.0}, b = {0.0, 0.0, 0.0, 0.0};
-      for (int32_t c = 0; c < hv.z; ++c) {
-        a += *reinterpret_cast<const f64x4*>(pk + (int64_t)(hv.y + c) * D + 4 * l);
-        b += *reinterpret_cast<const f64x4*>(pv + (int64_t)(hv.y + c) * D + 4 * l);
+    f64x4 a0 = {0.0, 0.0, 0.0, 0.0}, b0 = a0, a1 = a0, b1 = a0;
+    const int64_t o = (int64_t)hv.y * D + 4 * lr;
+    int32_t c = grp;
+    for (; c + NG < hv.z; c += 2 * NG) {
+      const f64x4 x0 = *reinterpret_cast<const f64x4*>(pk + o + (int64_t)c * D);
+      const f64x4 y0 = *reinterpret_cast<const f64x4*>(pv + o + (int64_t)c * D);
+      const f64x4 x1 = *reinterpret_cast<const f64x4*>(pk + o + (int64_t)(c + NG) * D);
+      const f64x4 y1 = *reinterpret_cast<const f64x4*>(pv + o + (int64_t)(c + NG) * D);
+      a0 += x0;
+      b0 += y0;
+      a1 += x1;
+      b1 += y1;
+    }
+    if (c < hv.z) {
+      a0 += *reinterpret_cast<const f64x4*>(pk + o + (int64_t)c * D);
+      b0 += *reinterpret_cast<const f64x4*>(pv + o + (int64_t)c * D);
+    }
+    f64x4 a = a0 + a1, b = b0 + b1;
+#pragma unroll
+    for (int m = LPR; m < 64; m <<= 1)
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        a[k] += __shfl_xor(a[k], m, 64);
+        b[k] += __shfl_xor(b[k], m, 64);
       }
-      *reinterpret_cast<f32x4*>(dKt + (int64_t)hv.x * D + 4 * l) = f32x4{(float)a[0], (float)a[1], (float)a[2], (float)a[3]};
-      *reinterpret_cast<f32x4*>(dVt + (int64_t)hv.x * D + 4 * l) = f32x4{(float)b[0], (float)b[1], (float)b[2], (float)b[3]};
+    if (grp == 0) {
+      *reinterpret_cast<f32x4*>(dKt + (int64_t)hv.x * D + 4 * lr) = f32x4{(float)a[0], (float)a[1], (float)a[2], (float)a[3]};
+      *reinterpret_cast<f32x4*>(dVt + (int64_t)hv.x * D + 4 * lr) = f32x4{(float)b[0], (float)b[1], (float)b[2], (float)b[3]};
     }
   }
 }
