@@ -69,8 +69,9 @@ def algorithmic_cost(kind: str, info: dict):
         return E * (d * s + 4) + N * (4 * (R + 1) + 3 * d * s + d / 8), 2.0 * E * d
     if kind == "spmm_bwd":
         # per edge: one gathered dZ row, destination id and scale; per work
-        # item 16 bytes; per active row one dY row written
-        return E * (d * s + 8) + A * (d * s + 16), 2.0 * E * d
+        # item 16 bytes; per active row one dY row written (float32 for every
+        # feature type: dY feeds the float32 GEMMs)
+        return E * (d * s + 8) + A * (d * 4 + 16), 2.0 * E * d
     raise KeyError(kind)
 
 
