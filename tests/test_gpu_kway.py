@@ -74,13 +74,14 @@ def test_mean_agg_node_in_no_subgraph_is_zero():
     assert np.array_equal(H[::2], h)
 
 
-def small_kway(factor=0.3, budget=None):
+def small_kway(factor=0.3, budget=None, parts=None):
+    from dataclasses import replace
     base = synth.WORKLOADS["tiny_kway"]
     gc = synth.scaled(base.graph, factor)
     if budget is not None:
-        from dataclasses import replace
         gc = replace(gc, budget=budget)
-    return synth.Workload(gc, base.model, "tiny_kway")
+    mc = base.model if parts is None else replace(base.model, parts=parts)
+    return synth.Workload(gc, mc, "tiny_kway")
 
 
 def test_home_gather_bit_exact_on_real_subgraphs():
@@ -121,9 +122,13 @@ def test_home_gather_poisons_inconsistent_rows():
     assert np.all(Y[0] == 1) and np.all(np.isnan(Y[1:]))
 
 
-@pytest.mark.parametrize("factor", [0.3, 0.1])
-def test_kway_step_matches_oracle(factor):
-    wl = small_kway(factor)
+@pytest.mark.parametrize("factor,parts,budget", [(0.3, None, None), (0.1, None, None), (0.2, 2, None),
+                                                (0.3, 7, 60), (0.2, 3, 0)])
+def test_kway_step_matches_oracle(factor, parts, budget):
+    """Every size of a 4-way split, a 2-way and a 7-way split (ragged blocks,
+    small budget) and a split with no overlap at all (copy counts all 1, no
+    alignment term)."""
+    wl = small_kway(factor, budget=budget, parts=parts)
     mc, cfg = wl.model, wl.graph
     g = synth.make_graph(cfg)
     inp = runner.make_kway_inputs(wl, g)
@@ -138,7 +143,7 @@ def test_kway_step_matches_oracle(factor):
         assert np.array_equal(sb.view("local2global").cpu().numpy(), osb.local2global)
         assert np.array_equal(sb.view("overlap").cpu().numpy(), osb.overlap)
         assert sb.e_sub == osb.e_sub
-        assert osb.overlap.shape[0] > 1
+        assert osb.overlap.shape[0] > 1 or wl.graph.budget == 0
     assert np.array_equal(inp.cnt.cpu().numpy(), out["cnt"])
     masks_agree = True
     d = mc.d
