@@ -215,6 +215,46 @@ def test_fullsize_layer_sampled_rows(full):
     del Hd, out, saved, dH
 
 
+def test_fullsize_bf16_layer_sampled_rows(full):
+    """The bfloat16 workload's layer (d = 256, bf16 rows, float32 weights) at
+    full size: forward on sampled and the heaviest destination rows, the
+    backward's dH on sampled source rows under the GPU's own mask, against
+    float64 on the same bf16-rounded inputs (bar 2e-2, as the bf16 tests);
+    on both full-size graphs."""
+    sub, R, d = full.sub, full.R, 256
+    H = synth.round_bf16(synth.features(4, full.g.n_nodes, d)[full.ref["l2g"]])
+    w = synth.layer_weights(4, 0, R, 2, d, 0.1)
+    Hd = to_dev(H).to(torch.bfloat16)
+    wr, wsf, b = to_dev(w.w_rel), to_dev(w.w_self), to_dev(w.bias)
+    out, saved = api.hg_layer_fwd(sub, Hd, wr, wsf, b)
+    rng = np.random.default_rng(3)
+    indeg = np.bincount(full.dst_l, minlength=full.ns)
+    rows = np.unique(np.concatenate([rng.choice(full.ns, 2000, replace=False), np.argsort(indeg)[-8:]]))
+    z = _z_rows(full, rows, H, w)
+    got = out[torch.from_numpy(rows).cuda()].float().cpu().numpy()
+    assert parity_err(got, np.maximum(z, 0) + H[rows]) <= 2e-2
+    G = synth.round_bf16(synth.upstream_grad(4, full.ns, d))
+    dH, _, _, _ = api.hg_layer_bwd(sub, Hd, wr, wsf, saved, to_dev(G).to(torch.bfloat16))
+    srcs = np.unique(rng.choice(full.ns, 200, replace=False))
+    mo = np.isin(full.src_l, srcs)
+    es, er, ed = full.src_l[mo], full.rel_l[mo], full.dst_l[mo]
+    need = np.unique(np.concatenate([ed, srcs]))
+    mask = unpack_mask(saved[torch.from_numpy(need).cuda().long()].cpu().numpy(), d)
+    pos = {v: i for i, v in enumerate(need)}
+    dz = G[need].astype(np.float64) * mask
+    deg = np.bincount(full.dst_l * R + full.rel_l, minlength=full.ns * R)
+    typ = full.g.ntype[full.ref["l2g"][srcs]].astype(np.int64)
+    exp = G[srcs].astype(np.float64).copy()
+    for k, i in enumerate(srcs):
+        exp[k] += dz[pos[i]] @ w.w_self[typ[k]].astype(np.float64).T
+        sel = es == i
+        for j, r in zip(ed[sel], er[sel]):
+            exp[k] += dz[pos[j]] / deg[j * R + r] @ w.w_rel[r].astype(np.float64).T
+    got = dH[torch.from_numpy(srcs).cuda()].float().cpu().numpy()
+    assert parity_err(got, exp) <= 2e-2
+    del Hd, out, saved, dH
+
+
 def test_fullsize_alignment(full):
     sub, wl = full.sub, full.wl
     d = wl.model.d
