@@ -664,6 +664,148 @@ __global__ void k_dmu_final(const float* __restrict__ mupart, int M, float* __re
   dmu[m] = accumulate ? dmu[m] + s : s;
 }
 
+// out[row0 + i] = addend[row0 + i] + sum_m A_m[row0 + i] W_m^T over three
+// row sets of the same rows (dH = G + dK W_K^T + dQ W_Q^T + dV W_V^T): the
+// three d x d matrices stay in LDS together (48 KB at d = 64, split-fp16
+// fragments as in k_gemm_rows), and each output row is written once instead
+// of being read and written again for every product.  Each product is
+// unscaled on its own (the rows of A_m have their own scales) and the three
+// are added in the order m = 0, 1, 2.
+constexpr int kSum3 = 3;
+template <int D>
+__global__ void __launch_bounds__(kGemmThreads) k_gemm_rows_sum3(int64_t n_rows, int64_t row0,
+                                                                 const float* __restrict__ W0,
+                                                                 const float* __restrict__ W1,
+                                                                 const float* __restrict__ W2,
+                                                                 const float* __restrict__ A0,
+                                                                 const float* __restrict__ A1,
+                                                                 const float* __restrict__ A2,
+                                                                 const float* __restrict__ addend,
+                                                                 float* __restrict__ out) {
+  static_assert(D == 64, "three 64 x 64 matrices in LDS");
+  constexpr int KB = D / 16, KB2 = D / 32, NB = D / 16;
+  constexpr int kWaves = kGemmThreads / 64;
+  constexpr int kRowsPerTile = 16 * kWaves;
+  constexpr int kFrag = KB2 * NB * 64;
+  __shared__ uint4 wsl[kSum3][2 * kFrag];  // per matrix: high parts, then remainders
+  __shared__ float wmax[kWaves];
+  __shared__ float uws[kSum3];
+  const int tid = threadIdx.x;
+  const float* Ws[kSum3] = {W0, W1, W2};
+  const float* As[kSum3] = {A0, A1, A2};
+#pragma unroll
+  for (int mi = 0; mi < kSum3; ++mi) {
+    const float* W = Ws[mi];
+    float m = 0.f;
+    for (int e = tid; e < D * D / 4; e += kGemmThreads) {
+      const f32x4 v = *reinterpret_cast<const f32x4*>(W + 4 * e);
+      m = fmaxf(m, fmaxf(fmaxf(fabsf(v[0]), fabsf(v[1])), fmaxf(fabsf(v[2]), fabsf(v[3]))));
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
+    if ((tid & 63) == 0) wmax[tid >> 6] = m;
+    __syncthreads();
+    m = wmax[0];
+#pragma unroll
+    for (int q = 1; q < kWaves; ++q) m = fmaxf(m, wmax[q]);
+    const uint32_t ew = split_exp(m);
+    const float sw = split_scale(ew);
+    for (int e = tid; e < kFrag; e += kGemmThreads) {
+      const int l = e & 63;
+      const int nb = (e >> 6) % NB;
+      const int kb2 = (e >> 6) / NB;
+      const int j = 16 * nb + (l & 15);
+      float v[8];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        // op(W) = W^T: element (k, j) is W[j][k]
+        const f32x4 x = *reinterpret_cast<const f32x4*>(W + (int64_t)j * D + 16 * (2 * kb2 + h) + 4 * (l >> 4));
+#pragma unroll
+        for (int q = 0; q < 4; ++q) v[4 * h + q] = x[q] * sw;
+      }
+      split8(v, wsl[mi][e], wsl[mi][kFrag + e]);
+    }
+    if (tid == 0) uws[mi] = split_unscale(ew);
+    __syncthreads();
+  }
+  const int w = tid >> 6;
+  const int l = lane64();
+  const int g = l >> 4, c = l & 15;
+  const int64_t ntiles = (n_rows + kRowsPerTile - 1) / kRowsPerTile;
+  for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
+    const int64_t i = t * kRowsPerTile + 16 * w + c;
+    const bool live = i < n_rows;
+    const int64_t row = row0 + (live ? i : 0);
+    f32x4 tot[NB];
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) tot[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // the next operand's row is loaded while the current one is multiplied
+    f32x4 nxt[KB];
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb)
+      nxt[kb] = live ? *reinterpret_cast<const f32x4*>(As[0] + row * D + 16 * kb + 4 * g) : f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int mi = 0; mi < kSum3; ++mi) {
+      __builtin_amdgcn_sched_barrier(0);
+      f32x4 a[KB];
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) a[kb] = nxt[kb];
+      if (mi + 1 < kSum3) {
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb)
+          nxt[kb] = live ? *reinterpret_cast<const f32x4*>(As[mi + 1] + row * D + 16 * kb + 4 * g)
+                         : f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+      float m = 0.f;
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb)
+        m = fmaxf(m, fmaxf(fmaxf(fabsf(a[kb][0]), fabsf(a[kb][1])), fmaxf(fabsf(a[kb][2]), fabsf(a[kb][3]))));
+      m = fmaxf(m, __shfl_xor(m, 16, 64));
+      m = fmaxf(m, __shfl_xor(m, 32, 64));
+      const uint32_t ex = split_exp(m);
+      const float sx = split_scale(ex), ux = split_unscale(ex);
+      uint4 xh[KB2], xlo[KB2];
+#pragma unroll
+      for (int kb2 = 0; kb2 < KB2; ++kb2) {
+        float v[8];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          v[q] = a[2 * kb2][q] * sx;
+          v[4 + q] = a[2 * kb2 + 1][q] * sx;
+        }
+        split8(v, xh[kb2], xlo[kb2]);
+      }
+      f32x4 acc[NB];
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kb2 = 0; kb2 < KB2; ++kb2) {
+        // each K block's fragments are read right before its MFMAs
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+          const int e = (kb2 * NB + nb) * 64 + l;
+          const uint4 bh = wsl[mi][e], bl = wsl[mi][kFrag + e];
+          acc[nb] = mfma_f16(bh, xh[kb2], acc[nb]);
+          acc[nb] = mfma_f16(bh, xlo[kb2], acc[nb]);
+          acc[nb] = mfma_f16(bl, xh[kb2], acc[nb]);
+        }
+      }
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) tot[nb] += split_unscale4(acc[nb], ux, uws[mi]);
+    }
+    if (live) {
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        const int col = 16 * nb + 4 * g;
+        const f32x4 pre = addend ? *reinterpret_cast<const f32x4*>(addend + row * D + col)
+                                 : f32x4{0.f, 0.f, 0.f, 0.f};
+        *reinterpret_cast<f32x4*>(out + row * D + col) = pre + tot[nb];
+      }
+    }
+  }
+}
+
 template <int D>
 int hgt_bwd_impl(const hg_subgraph* s, const hg_hgt_desc* L, const float* Hin, const hg_hgt_weights* W,
                  const uint32_t* mask, const void* saved, const float* G, float* dHin, const hg_hgt_grads* dW,
@@ -766,14 +908,28 @@ int hgt_bwd_impl(const hg_subgraph* s, const hg_hgt_desc* L, const float* Hin, c
     const float* Ws[3] = {W->W_K, W->W_Q, W->W_V};
     float* dWs[3] = {dW->W_K, dW->W_Q, dW->W_V};
     float* dbs[3] = {dW->b_K, dW->b_Q, dW->b_V};
-    for (int k = 0; k < 3; ++k) {
-      const float* addend = (k == 0) ? (L->residual ? G : nullptr) : dHin;
-      HG_TRY((launch_gemm_rows_pp<D, true>("hgt_bwd_dx", hi - lo, Ws[k] + wo, LoadRows<D, float>{srcs[k], rows_contig(lo)},
-                                           StoreRows<D, float>{dHin, rows_contig(lo), nullptr, addend}, st)));
+    if constexpr (D == 64) {
+      // the three products in one pass (their matrices fit LDS together)
+      const int64_t n = hi - lo;
+      if (n > 0) {
+        const int64_t tiles = cdiv(n, 16 * (kGemmThreads / 64));
+        const int64_t cap = (int64_t)num_cus() * 3;
+        HG_LAUNCH("hgt_bwd_dx", k_gemm_rows_sum3<D>, dim3((unsigned)(tiles < cap ? tiles : cap)), dim3(kGemmThreads),
+                  0, st, n, lo, W->W_K + wo, W->W_Q + wo, W->W_V + wo, (const float*)w.dK, (const float*)w.dQ,
+                  (const float*)w.dV, L->residual ? G : nullptr, dHin);
+      }
+    } else {
+      for (int k = 0; k < 3; ++k) {
+        const float* addend = (k == 0) ? (L->residual ? G : nullptr) : dHin;
+        HG_TRY((launch_gemm_rows_pp<D, true>("hgt_bwd_dx", hi - lo, Ws[k] + wo,
+                                             LoadRows<D, float>{srcs[k], rows_contig(lo)},
+                                             StoreRows<D, float>{dHin, rows_contig(lo), nullptr, addend}, st)));
+      }
+    }
+    for (int k = 0; k < 3; ++k)
       HG_TRY((launch_gemm_tn<D>("hgt_bwd_dw", hi - lo, LoadRows<D, float>{Hin, rows_contig(lo)},
                                 LoadRows<D, float>{srcs[k], rows_contig(lo)}, w.splitk, w.colsum, dWs[k] + wo,
                                 dbs[k] ? dbs[k] + bo : nullptr, acc, st)));
-    }
   }
   // (6) dmu: per CSR row by source type, then per meta relation over each type range
   {
