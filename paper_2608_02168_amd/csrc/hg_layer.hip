@@ -28,7 +28,7 @@ namespace {
 // ds_bpermute.  Accumulation is float32.
 // fp32 rows: 8 waves per SIMD (<= 64 VGPRs) keep the most gathers in flight.
 template <int D, class T>
-__global__ void __launch_bounds__(256, (sizeof(T) == 4 && D <= 128) ? 8 : 4) k_spmm_fwd(int64_t n_sub, int32_t R, const int32_t* __restrict__ csr_ptr,
+__global__ void __launch_bounds__(256, (sizeof(T) == 2 || D <= 128) ? 8 : 4) k_spmm_fwd(int64_t n_sub, int32_t R, const int32_t* __restrict__ csr_ptr,
                                                   const int32_t* __restrict__ csr_col,
                                                   const T* __restrict__ Y, const T* __restrict__ Yself,
                                                   const T* __restrict__ Hin, T* __restrict__ Hout,
@@ -71,7 +71,7 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 4 && D <= 128) ? 8 : 4) k_s
       }
       const int cnt = (pe - base) < 64 ? (pe - base) : 64;
       for (int e = 0; e < cnt; e += EPW * U) {
-        float v[U][EL];
+        typename Elt<T>::rawv_t v[U];
         float ww[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
@@ -79,17 +79,12 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 4 && D <= 128) ? 8 : 4) k_s
           const int32_t q = __shfl(rowi, my & 63, 64);
           const float wq = __shfl(wgt, my & 63, 64);
           ww[u] = (my < cnt) ? wq : 0.f;
-          if (my < cnt) {
-            Elt<T>::load(Y + (int64_t)q * D + c0, v[u]);
-          } else {
-#pragma unroll
-            for (int k = 0; k < EL; ++k) v[u][k] = 0.f;
-          }
+          v[u] = (my < cnt) ? Elt<T>::rawv(Y + (int64_t)q * D + c0) : Elt<T>::rawv_zero();
         }
 #pragma unroll
         for (int u = 0; u < U; ++u)
 #pragma unroll
-          for (int k = 0; k < EL; ++k) acc[k] += ww[u] * v[u][k];
+          for (int k = 0; k < EL; ++k) acc[k] += ww[u] * Elt<T>::rawv_get(v[u], k);
       }
     }
 #pragma unroll
@@ -126,7 +121,7 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 4 && D <= 128) ? 8 : 4) k_s
 // accumulates in float64 (the kernel is bound by the gathers, not the adds);
 // split rows keep float64 partial rows.
 template <int D, class T, class TO>
-__global__ void __launch_bounds__(256, (sizeof(T) == 4 && D <= 128) ? 8 : 4) k_spmm_bwd(int64_t n_items, const int4* __restrict__ items,
+__global__ void __launch_bounds__(256, (sizeof(T) == 2 || D <= 128) ? 8 : 4) k_spmm_bwd(int64_t n_items, const int4* __restrict__ items,
                                                   const int32_t* __restrict__ csc_row,
                                                   const float* __restrict__ csc_scale,
                                                   const T* __restrict__ dZ,
@@ -195,12 +190,14 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 4 && D <= 128) ? 8 : 4) k_s
       }
     }
   } else {
-    typedef typename Elt<T>::vf vf;
-    typedef typename Elt<T>::vd vd;
+    // bf16 rows: the gathered chunks stay packed until the float64 adds
+    // (<= 64 VGPRs, 8 waves per SIMD as for float32 rows)
     for (int64_t it = wave0; it < n_items; it += nwaves) {
       const int4 item = items[it];
       const int32_t beg = item.y, end = item.z;
-      vd acc = (vd)0.0;
+      double acc[EL];
+#pragma unroll
+      for (int k = 0; k < EL; ++k) acc[k] = 0.0;
       for (int32_t base = beg; base < end; base += 64) {
         const int32_t pos = base + l;
         int32_t dst = 0;
@@ -211,7 +208,7 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 4 && D <= 128) ? 8 : 4) k_s
         }
         const int cnt = (end - base) < 64 ? (end - base) : 64;
         for (int e = 0; e < cnt; e += EPW * U) {
-          vf v[U];
+          typename Elt<T>::rawv_t v[U];
           float ww[U];
   #pragma unroll
           for (int u = 0; u < U; ++u) {
@@ -219,10 +216,14 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 4 && D <= 128) ? 8 : 4) k_s
             const int32_t q = __shfl(dst, my & 63, 64);
             const float wq = __shfl(sc, my & 63, 64);
             ww[u] = (my < cnt) ? wq : 0.f;
-            v[u] = (my < cnt) ? Elt<T>::loadv(dZ + (int64_t)q * D + c0) : (vf)0.f;
+            v[u] = (my < cnt) ? Elt<T>::rawv(dZ + (int64_t)q * D + c0) : Elt<T>::rawv_zero();
           }
   #pragma unroll
-          for (int u = 0; u < U; ++u) acc += __builtin_convertvector(v[u], vd) * (double)ww[u];
+          for (int u = 0; u < U; ++u) {
+            const double w = (double)ww[u];
+  #pragma unroll
+            for (int k = 0; k < EL; ++k) acc[k] += (double)Elt<T>::rawv_get(v[u], k) * w;
+          }
         }
       }
   #pragma unroll

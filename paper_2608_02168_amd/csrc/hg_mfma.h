@@ -22,6 +22,7 @@ namespace hg {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef double f64x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef uint16_t bf16_t;  // bfloat16 storage
 
@@ -61,6 +62,12 @@ struct Elt<float> {
   typedef f32x4 raw4_t;
   __device__ static __forceinline__ raw4_t raw4(const float* p) { return *reinterpret_cast<const f32x4*>(p); }
   __device__ static __forceinline__ f32x4 cook4(raw4_t r) { return r; }
+  // one 16-byte chunk (EL elements) as loaded; element k is unpacked where it
+  // is used, so a gather keeps 4 registers per row in flight
+  typedef f32x4 rawv_t;
+  __device__ static __forceinline__ rawv_t rawv(const float* p) { return *reinterpret_cast<const f32x4*>(p); }
+  __device__ static __forceinline__ rawv_t rawv_zero() { return f32x4{0.f, 0.f, 0.f, 0.f}; }
+  __device__ static __forceinline__ float rawv_get(const rawv_t& x, int k) { return x[k]; }
 };
 template <>
 struct Elt<bf16_t> {
@@ -104,6 +111,13 @@ struct Elt<bf16_t> {
   __device__ static __forceinline__ f32x4 cook4(raw4_t x) {
     return f32x4{__uint_as_float(x.x << 16), __uint_as_float(x.x & 0xFFFF0000u),
                  __uint_as_float(x.y << 16), __uint_as_float(x.y & 0xFFFF0000u)};
+  }
+  typedef u32x4 rawv_t;
+  __device__ static __forceinline__ rawv_t rawv(const bf16_t* p) { return *reinterpret_cast<const u32x4*>(p); }
+  __device__ static __forceinline__ rawv_t rawv_zero() { return u32x4{0u, 0u, 0u, 0u}; }
+  // element 2q is the low half of word q, element 2q + 1 the high half
+  __device__ static __forceinline__ float rawv_get(const rawv_t& x, int k) {
+    return (k & 1) ? __uint_as_float(x[k >> 1] & 0xFFFF0000u) : __uint_as_float(x[k >> 1] << 16);
   }
 };
 
