@@ -267,6 +267,19 @@ def gather_ceiling(n_rows, n_idx, row_bytes, group, achieved):
             "frac": round(achieved / res["with_writes"], 4)}
 
 
+def _timed_runs(fn, min_s=10.0):
+    """Run fn() until at least min_s seconds of work have been timed (at least
+    once); returns (its last result, seconds per run, runs)."""
+    runs, total = 0, 0.0
+    while True:
+        t0 = time.perf_counter()
+        out = fn()
+        total += time.perf_counter() - t0
+        runs += 1
+        if total >= min_s:
+            return out, total / runs, runs
+
+
 def cpu_baseline_sequence(wl, frac):
     """The oracle's sequence step (oracle/step.py run_sequence, unchanged) on
     the same recipe at a fraction of the node and edge counts."""
@@ -283,15 +296,13 @@ def cpu_baseline_sequence(wl, frac):
     feats = synth.features(mc.seed, g.n_nodes, mc.d)
     weights = [synth.hgt_weights(mc.seed, li, cfg.n_rel, 2, mc.d, mc.heads, mc.bias_range)
                for li in range(mc.n_layers)]
-    t0 = time.perf_counter()
-    out = oracle_step.run_sequence(dict(src=g.src, dst=g.dst, rel=g.rel, ntype=g.ntype, part=g.part),
+    out, dt, runs = _timed_runs(lambda: oracle_step.run_sequence(dict(src=g.src, dst=g.dst, rel=g.rel, ntype=g.ntype, part=g.part),
                                    dict(k=g.k, n_rel=cfg.n_rel, n_ntype=2, budget=cfg.budget, key=cfg.key,
                                         theta=cfg.theta, seed=cfg.seed),
                                    ts, cuts, feats, weights, mc.heads, synth.temporal_weights(mc.seed, mc.d),
                                    mc.window, synth.reference_embeddings(mc.seed, max(cfg.budget, 1), mc.d),
                                    synth.head_weights(mc.seed, mc.d), synth.labels(mc.seed, g.ntype),
-                                   lambda_n=mc.lambda_n, scale=mc.lambda_cca, eps=mc.eps, ddof=mc.ddof)
-    dt = time.perf_counter() - t0
+                                   lambda_n=mc.lambda_n, scale=mc.lambda_cca, eps=mc.eps, ddof=mc.ddof))
     e_pass = sum(s.e_sub for s in out["subs"])
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
     return {"value": round(mc.n_layers * e_pass / dt / 1e9, 6), "unit": "GTEPS", "cores": threads,
@@ -299,7 +310,7 @@ def cpu_baseline_sequence(wl, frac):
             "sample": f"same recipe at {frac:g} of the node/edge counts: N={g.n_nodes}, E={g.n_edges}, "
                       f"E_sub per snapshot {[s.e_sub for s in out['subs']]}; one full sequence step ("
                       f"{mc.snapshots} snapshot builds, {mc.n_layers} attention layers and the temporal module "
-                      f"per snapshot, head, BCE and alignment, backward through every snapshot) in {dt:.1f}s; "
+                      f"per snapshot, head, BCE and alignment, backward through every snapshot) in {dt:.1f}s, mean of {runs} runs; "
                       f"float64; BLAS {threads} threads"}
 
 
@@ -317,13 +328,11 @@ def cpu_baseline_kway(wl, frac):
     part = synth.random_partition(g.n_nodes, mc.parts, mc.seed)
     feats = synth.features(mc.seed, g.n_nodes, mc.d)
     weights = [synth.layer_weights(mc.seed, li, cfg.n_rel, 2, mc.d, mc.bias_range) for li in range(mc.n_layers)]
-    t0 = time.perf_counter()
-    out = oracle_kway.run_kway(dict(src=g.src, dst=g.dst, rel=g.rel, ntype=g.ntype, part=part), mc.parts,
+    out, dt, runs = _timed_runs(lambda: oracle_kway.run_kway(dict(src=g.src, dst=g.dst, rel=g.rel, ntype=g.ntype, part=part), mc.parts,
                                dict(n_rel=cfg.n_rel, n_ntype=2, budget=cfg.budget, key=cfg.key, theta=cfg.theta,
                                     seed=cfg.seed),
                                feats, weights, synth.head_weights(mc.seed, mc.d), synth.labels(mc.seed, g.ntype),
-                               lambda_n=mc.lambda_n, scale=mc.lambda_cca, eps=mc.eps, ddof=mc.ddof)
-    dt = time.perf_counter() - t0
+                               lambda_n=mc.lambda_n, scale=mc.lambda_cca, eps=mc.eps, ddof=mc.ddof))
     e_pass = sum(s.e_sub for s in out["subs"])
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
     return {"value": round(mc.n_layers * e_pass / dt / 1e9, 6), "unit": "GTEPS", "cores": threads,
@@ -331,7 +340,7 @@ def cpu_baseline_kway(wl, frac):
             "sample": f"same recipe at {frac:g} of the node/edge counts: N={g.n_nodes}, E={g.n_edges}, "
                       f"E_sub per subgraph {[s.e_sub for s in out['subs']]}; one full K-worker step ("
                       f"{mc.parts} subgraph builds, {mc.n_layers} mean layers fwd+bwd per subgraph, MeanAgg, "
-                      f"head, BCE and home-copy alignment) in {dt:.1f}s; float64; BLAS {threads} threads"}
+                      f"head, BCE and home-copy alignment) in {dt:.1f}s, mean of {runs} runs; float64; BLAS {threads} threads"}
 
 
 def cpu_baseline(wl, frac):
@@ -359,20 +368,18 @@ def cpu_baseline(wl, frac):
     extra = {}
     if mc.objective == "bce":
         extra = dict(head=synth.head_weights(mc.seed, mc.d), labels_global=synth.labels(mc.seed, g.ntype))
-    t0 = time.perf_counter()
-    sub, *_ = oracle_step.run(dict(src=g.src, dst=g.dst, rel=g.rel, ntype=g.ntype, part=g.part),
+    (sub, *_), dt, runs = _timed_runs(lambda: oracle_step.run(dict(src=g.src, dst=g.dst, rel=g.rel, ntype=g.ntype, part=g.part),
                               dict(k=g.k, n_rel=cfg.n_rel, n_ntype=2, budget=cfg.budget, key=cfg.key,
                                    theta=cfg.theta, seed=cfg.seed),
                               feats, weights, href, gext, lambda_n=mc.lambda_n, scale=mc.lambda_cca,
-                              eps=mc.eps, ddof=mc.ddof, heads=mc.heads, **extra)
-    dt = time.perf_counter() - t0
+                              eps=mc.eps, ddof=mc.ddof, heads=mc.heads, **extra))
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
     return {"value": round(mc.n_layers * sub.e_sub / dt / 1e9, 6), "unit": "GTEPS", "cores": threads,
             "kind": "oracle",
             "sample": f"same recipe at {frac:g} of the node/edge counts: N={g.n_nodes}, E={g.n_edges}, "
                       f"E_sub={sub.e_sub}; one full step (build, {mc.n_layers} layers fwd+bwd, alignment"
                       f"{', prediction head and BCE' if mc.objective == 'bce' else ''}) "
-                      f"in {dt:.1f}s; float64; scipy sparse products single-threaded, BLAS {threads} threads"}
+                      f"in {dt:.1f}s, mean of {runs} runs; float64; scipy sparse products single-threaded, BLAS {threads} threads"}
 
 
 if __name__ == "__main__":
