@@ -162,21 +162,22 @@ __device__ __forceinline__ bool bit_of(const uint32_t* __restrict__ bits, int32_
 // min, whose result does not depend on the order) and sends one global
 // atomic per table entry when it is done; a key that finds no free slot goes
 // straight to the global atomic.  Hot keys arrive early and keep their slots.
-constexpr int kAggSlots = 2048;
+constexpr int kAggBits = 11, kAggSlots = 1 << kAggBits;
 constexpr uint32_t kAggEmpty = 0xFFFFFFFFu;
 
-template <bool kMin>
+template <bool kMin, int kBits = kAggBits>
 struct LdsAgg {
-  uint32_t* key;  // [kAggSlots] in LDS
+  static constexpr int kSlots = 1 << kBits;
+  uint32_t* key;  // [kSlots] in LDS
   int32_t* val;
   __device__ __forceinline__ void init() {
-    for (int q = threadIdx.x; q < kAggSlots; q += blockDim.x) {
+    for (int q = threadIdx.x; q < kSlots; q += blockDim.x) {
       key[q] = kAggEmpty;
       val[q] = kMin ? INT32_MAX : 0;
     }
   }
   __device__ __forceinline__ void put(uint32_t k, int32_t v, int32_t* __restrict__ tgt) {
-    uint32_t h = (k * 0x9E3779B1u) >> (32 - 11);  // kAggSlots = 2^11
+    uint32_t h = (k * 0x9E3779B1u) >> (32 - kBits);
 #pragma unroll
     for (int probe = 0; probe < 4; ++probe) {
       // a plain read first: a full table costs loads, not compare-and-swaps
@@ -190,7 +191,7 @@ struct LdsAgg {
         }
         return;
       }
-      h = (h + 1) & (kAggSlots - 1);
+      h = (h + 1) & (kSlots - 1);
     }
     if (kMin) {
       atomicMin(&tgt[k], v);
@@ -200,7 +201,7 @@ struct LdsAgg {
   }
   // after a __syncthreads: one global atomic per filled slot
   __device__ __forceinline__ void flush(int32_t* __restrict__ tgt) {
-    for (int q = threadIdx.x; q < kAggSlots; q += blockDim.x) {
+    for (int q = threadIdx.x; q < kSlots; q += blockDim.x) {
       const uint32_t k = key[q];
       if (k != kAggEmpty) {
         if (kMin) {
@@ -212,16 +213,21 @@ struct LdsAgg {
     }
   }
 };
-static_assert(kAggSlots == 2048, "the hash keeps 11 bits");
 
 // Launch shape of the aggregation passes: blocks of 512 threads, three per
 // compute unit (the edge pass's three tables take 48 KB of LDS), each working
 // through a long stretch of edges before it flushes its table.
 constexpr int kAggBT = 512;
-inline unsigned agg_grid(int64_t n) {
-  const int64_t b = cdiv(n > 0 ? n : 1, kAggBT), cap = (int64_t)num_cus() * 3;
+inline unsigned agg_grid(int64_t n, int per_cu = 3) {
+  const int64_t b = cdiv(n > 0 ? n : 1, kAggBT), cap = (int64_t)num_cus() * per_cu;
   return (unsigned)(b < cap ? b : cap);
 }
+
+// The out-degree counts: every edge adds 1 to its source, and with Zipf
+// sources a few thousand hubs take most of the edges.  A table of 2^13 slots
+// (64 KB, two blocks per compute unit) keeps far more of them than the
+// 2^11-slot tables of the passes that hold several tables at once.
+constexpr int kDegBits = 13, kDegSlots = 1 << kDegBits, kDegPerCu = 2;
 
 // Range checks and the candidates C_k: every node outside V_k joined to V_k
 // by an edge gets first[v] < n_edges -- in a dense build the smallest index of
@@ -274,9 +280,9 @@ __global__ void __launch_bounds__(kAggBT) k_edges_pass(const int32_t* __restrict
 __global__ void __launch_bounds__(kAggBT) k_cand_outdeg(const int32_t* __restrict__ src, int64_t n_edges,
                                                     const uint32_t* __restrict__ cand_bits,
                                                     int32_t* __restrict__ outdeg) {
-  __shared__ uint32_t lk[kAggSlots];
-  __shared__ int32_t lv[kAggSlots];
-  LdsAgg<false> deg{lk, lv};
+  __shared__ uint32_t lk[kDegSlots];
+  __shared__ int32_t lv[kDegSlots];
+  LdsAgg<false, kDegBits> deg{lk, lv};
   deg.init();
   __syncthreads();
   GRID_STRIDE(e, n_edges) {
@@ -293,9 +299,9 @@ __global__ void __launch_bounds__(kAggBT) k_all_outdeg(const int32_t* __restrict
                                                    const uint8_t* __restrict__ rel, int64_t n_nodes,
                                                    int64_t n_edges, int32_t n_rel, int32_t* __restrict__ outdeg,
                                                    int32_t* __restrict__ cnt) {
-  __shared__ uint32_t lk[kAggSlots];
-  __shared__ int32_t lv[kAggSlots];
-  LdsAgg<false> deg{lk, lv};
+  __shared__ uint32_t lk[kDegSlots];
+  __shared__ int32_t lv[kDegSlots];
+  LdsAgg<false, kDegBits> deg{lk, lv};
   deg.init();
   __syncthreads();
   GRID_STRIDE(e, n_edges) {
@@ -905,7 +911,7 @@ extern "C" int hg_node_keys(const hg_graph_desc* g, int32_t key, int32_t* keys, 
   HG_TRY(fill_i32(keys, 0, N, s));
   if (hindex) HG_TRY(fill_i32(deg, 0, N, s));
   if (E > 0)
-    HG_LAUNCH("keys_outdeg", k_all_outdeg, dim3(agg_grid(E)), dim3(kAggBT), 0, s, g->src, g->dst, g->rel, N, E,
+    HG_LAUNCH("keys_outdeg", k_all_outdeg, dim3(agg_grid(E, kDegPerCu)), dim3(kAggBT), 0, s, g->src, g->dst, g->rel, N, E,
               g->n_rel, deg, w.cnt);
   int32_t herr = 0;
   HG_HIP_TRY(hipMemcpyAsync(&herr, w.cnt + C_ERR, sizeof(int32_t), hipMemcpyDeviceToHost, s));
@@ -997,7 +1003,7 @@ extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg
     HG_LAUNCH("build_cand_bits", k_cand_bits, dim3(gB), dim3(kBT), 0, s, (const int32_t*)w.first, (int32_t)E, N,
               w.cbits);
     if (E > 0)
-      HG_LAUNCH("build_cand_outdeg", k_cand_outdeg, dim3(agg_grid(E)), dim3(kAggBT), 0, s, g->src, E,
+      HG_LAUNCH("build_cand_outdeg", k_cand_outdeg, dim3(agg_grid(E, kDegPerCu)), dim3(kAggBT), 0, s, g->src, E,
                 (const uint32_t*)w.cbits, w.outdeg);
     HG_LAUNCH("build_copy_key", k_copy_key, dim3(gN), dim3(kBT), 0, s, (const int32_t*)w.outdeg, N, w.key);
   }
