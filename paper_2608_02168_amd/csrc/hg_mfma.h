@@ -759,7 +759,9 @@ __global__ void __launch_bounds__(kGemmThreads, D > 128 ? 2 : 4) k_gemm_rows_pp(
 #pragma unroll
       for (int kb2 = 0; kb2 < KB2; ++kb2) {
         const f32x4 a0 = aload.operand4(x, 2 * kb2, g), a1 = aload.operand4(x, 2 * kb2 + 1, g);
-        if (ALoad::kTee && live) {
+        // with two column slices, the two blocks of a tile group load the
+        // same A rows: each writes the half of the row in its own columns
+        if (ALoad::kTee && live && (D == DN || (2 * kb2 < KB2) == (slice == 0))) {
           aload.tee4(ra, 2 * kb2, g, a0);
           aload.tee4(ra, 2 * kb2 + 1, g, a1);
         }
