@@ -1019,6 +1019,29 @@ int launch_gemm_rows_bf16(const char* name, int64_t n_rows, const float* W, ALoa
 }
 
 // ---- gemm_tn split-K ----------------------------------------------------------
+// Split-K block -> (chunk, output tile).  At d = 256 the output is four
+// 128 x 128 tiles (ti, tj) that read the same rows of a chunk: the four blocks
+// of a chunk are 8 apart in groups of 32 consecutive blocks, so they go to the
+// same XCD (blocks are dealt round-robin over the 8) at about the same time
+// and the rows come from HBM once, then from that XCD's L2.  The grid covers
+// the chunk count rounded up to 8; a block past the last chunk has no rows.
+template <int D>
+__device__ __forceinline__ void tn_block(int64_t& chunk, int& ti, int& tj) {
+  if constexpr (D == 256) {
+    const unsigned b = blockIdx.x;
+    const int t = (int)((b >> 3) & 3u);
+    chunk = (int64_t)(((b >> 5) << 3) | (b & 7u));
+    ti = t >> 1;
+    tj = t & 1;
+  } else {
+    chunk = blockIdx.x;
+    ti = tj = 0;
+  }
+}
+inline unsigned tn_grid(int D, int64_t chunks) {
+  return (unsigned)(D == 256 ? 4 * cdiv(chunks, 8) * 8 : chunks);
+}
+
 // partial[chunk][i][j] = sum_{rows k of the chunk} A[k][i] * B[k][j]
 // colsum[chunk][j]    = sum_{rows k of the chunk} B[k][j]        (if colsum)
 // A wave owns a 64 x 64 block of the output (D = 128: wave w takes quadrant
@@ -1037,16 +1060,16 @@ __global__ void __launch_bounds__(256) k_gemm_tn(int64_t n_rows, int64_t kc, LA 
   const int w = threadIdx.x >> 6;
   const int l = lane64();
   const int g = l >> 4, c = l & 15;
-  const int64_t chunk = blockIdx.x;
+  int64_t chunk;
+  int ti, tj;
+  tn_block<D>(chunk, ti, tj);
   const int64_t k_beg = chunk * kc;
+  if (k_beg >= n_rows) return;  // a padding block (the whole block)
   const int64_t k_end = (k_beg + kc < n_rows) ? k_beg + kc : n_rows;
   const int qi = kQuad ? (w >> 1) : 0;
   const int qj = kQuad ? (w & 1) : 0;
   const int64_t step0 = kQuad ? 0 : 4 * w;
   const int64_t stride = kQuad ? 4 : 16;
-  // D = 256: blockIdx.y picks the 128 x 128 output tile (ti, tj)
-  const int ti = (D == 256) ? (int)(blockIdx.y >> 1) : 0;
-  const int tj = (D == 256) ? (int)(blockIdx.y & 1) : 0;
   const int ca = 128 * ti + 64 * qi + 4 * c, cb = 128 * tj + 64 * qj + 4 * c;
   f32x4 acc[4][4];
   f32x4 bs = {0.f, 0.f, 0.f, 0.f};
@@ -1207,15 +1230,16 @@ __global__ void __launch_bounds__(256, 2) k_gemm_tn_bf(int64_t n_rows, int64_t k
   const int w = threadIdx.x >> 6;
   const int l = lane64();
   const int g = l >> 4, c = l & 15;
-  const int64_t chunk = blockIdx.x;
+  int64_t chunk;
+  int ti, tj;
+  tn_block<D>(chunk, ti, tj);
   const int64_t k_beg = chunk * kc;
+  if (k_beg >= n_rows) return;  // a padding block (the whole block)
   const int64_t k_end = (k_beg + kc < n_rows) ? k_beg + kc : n_rows;
   const int qi = kQuad ? (w >> 1) : 0;
   const int qj = kQuad ? (w & 1) : 0;
   const int64_t step0 = kQuad ? 0 : 32 * w;
   const int64_t S = kQuad ? 32 : 128;
-  const int ti = (D == 256) ? (int)(blockIdx.y >> 1) : 0;
-  const int tj = (D == 256) ? (int)(blockIdx.y & 1) : 0;
   const int ca = 128 * ti + 64 * qi + 4 * c, cb = 128 * tj + 64 * qj + 4 * c;
   f32x4 acc[4][4];
   f32x4 bs = {0.f, 0.f, 0.f, 0.f};
@@ -1483,10 +1507,9 @@ int launch_gemm_tn(const char* name, int64_t n_rows, LA la, LB lb, float* partia
   }
   const int64_t kc = splitk_chunk(n_rows);
   const int64_t chunks = cdiv(n_rows, kc);
-  const unsigned tiles = D == 256 ? 4u : 1u;
   const bool list_a = la.map.list != nullptr, list_b = lb.map.list != nullptr;
   float* cs = out_colsum ? colsum : nullptr;
-  const dim3 grid((unsigned)chunks, tiles);
+  const dim3 grid(tn_grid(D, chunks));
   if constexpr (IsPlainRows<LA>::value && IsPlainRows<LB>::value) {
     // plain feature rows: the bf16 MFMA kernel
     typedef typename std::remove_cv<typename std::remove_pointer<decltype(la.base)>::type>::type TA_;
