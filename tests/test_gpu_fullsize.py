@@ -220,7 +220,9 @@ def test_fullsize_bf16_layer_sampled_rows(full):
     full size: forward on sampled and the heaviest destination rows, the
     backward's dH on sampled source rows under the GPU's own mask, against
     float64 on the same bf16-rounded inputs (bar 2e-2, as the bf16 tests);
-    on both full-size graphs."""
+    and four whole columns of dW_self, dW_rel and db, reduced over every row
+    and edge (split-K over all chunks), where the inputs are exact bf16 values
+    and the bar is float32's 1e-4; on both full-size graphs."""
     sub, R, d = full.sub, full.R, 256
     H = synth.round_bf16(synth.features(4, full.g.n_nodes, d)[full.ref["l2g"]])
     w = synth.layer_weights(4, 0, R, 2, d, 0.1)
@@ -234,7 +236,7 @@ def test_fullsize_bf16_layer_sampled_rows(full):
     got = out[torch.from_numpy(rows).cuda()].float().cpu().numpy()
     assert parity_err(got, np.maximum(z, 0) + H[rows]) <= 2e-2
     G = synth.round_bf16(synth.upstream_grad(4, full.ns, d))
-    dH, _, _, _ = api.hg_layer_bwd(sub, Hd, wr, wsf, saved, to_dev(G).to(torch.bfloat16))
+    dH, dWr, dWs, db = api.hg_layer_bwd(sub, Hd, wr, wsf, saved, to_dev(G).to(torch.bfloat16))
     srcs = np.unique(rng.choice(full.ns, 200, replace=False))
     mo = np.isin(full.src_l, srcs)
     es, er, ed = full.src_l[mo], full.rel_l[mo], full.dst_l[mo]
@@ -252,7 +254,44 @@ def test_fullsize_bf16_layer_sampled_rows(full):
             exp[k] += dz[pos[j]] / deg[j * R + r] @ w.w_rel[r].astype(np.float64).T
     got = dH[torch.from_numpy(srcs).cuda()].float().cpu().numpy()
     assert parity_err(got, exp) <= 2e-2
-    del Hd, out, saved, dH
+    # weight gradients on columns J: dZ[:, J] = G[:, J] * mask[:, J] (the GPU's
+    # mask bits), dW_self[t][:, J] = H_t^T dZ_t[:, J], db[t][J] = sum dZ_t[:, J],
+    # dW_r[:, J] = H^T w_r with w_r[i] = sum over edges i -> k of relation r of
+    # dZ[k, J] / deg_r(k)
+    J = np.array([0, 77, 130, 255])
+    words = saved[: full.ns].cpu().numpy()
+    mJ = np.stack([(words[:, j // 32] >> np.uint32(j % 32)) & np.uint32(1) for j in J], axis=1)
+    dzJ = G[:, J].astype(np.float64) * mJ
+    del words, mJ
+    ntype = full.g.ntype[full.ref["l2g"]]
+    toff = np.searchsorted(ntype, np.arange(3))
+    exp_ws, exp_db = [], []
+    for t in range(2):
+        lo, hi = toff[t], toff[t + 1]
+        acc = np.zeros((d, len(J)))
+        for c0 in range(lo, hi, 1 << 20):
+            c1 = min(hi, c0 + (1 << 20))
+            acc += H[c0:c1].astype(np.float64).T @ dzJ[c0:c1]
+        exp_ws.append(acc)
+        exp_db.append(dzJ[lo:hi].sum(axis=0))
+    scale = 1.0 / deg[full.dst_l * R + full.rel_l]
+    exp_wr = []
+    for r in range(R):
+        er_ = full.rel_l == r
+        wsum = np.stack([np.bincount(full.src_l[er_], weights=dzJ[full.dst_l[er_], q] * scale[er_],
+                                     minlength=full.ns) for q in range(len(J))], axis=1)
+        acc = np.zeros((d, len(J)))
+        for c0 in range(0, full.ns, 1 << 20):
+            c1 = min(full.ns, c0 + (1 << 20))
+            acc += H[c0:c1].astype(np.float64).T @ wsum[c0:c1]
+        exp_wr.append(acc)
+    Jt = torch.from_numpy(J).cuda()
+    for t in range(2):
+        assert parity_err(dWs[t][:, Jt].cpu().numpy(), exp_ws[t]) <= TOL, ("dW_self", t)
+        assert parity_err(db[t][Jt].cpu().numpy(), exp_db[t]) <= TOL, ("db", t)
+    for r in range(R):
+        assert parity_err(dWr[r][:, Jt].cpu().numpy(), exp_wr[r]) <= TOL, ("dW_rel", r)
+    del Hd, out, saved, dH, dWr, dWs, db
 
 
 def test_fullsize_alignment(full):
