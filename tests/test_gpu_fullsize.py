@@ -164,6 +164,50 @@ def _z_rows(full, rows, H, w):
     return z
 
 
+def _check_dw_columns(full, H, G, saved, dWr, dWs, db, deg):
+    """Four whole columns J of dW_self, db and every dW_r, each a reduction
+    over all rows and edges (every split-K chunk and output tile), against
+    float64 under the GPU's own mask, within float32's 1e-4."""
+    R, d = full.R, H.shape[1]
+    # weight gradients on columns J: dZ[:, J] = G[:, J] * mask[:, J] (the GPU's
+    # mask bits), dW_self[t][:, J] = H_t^T dZ_t[:, J], db[t][J] = sum dZ_t[:, J],
+    # dW_r[:, J] = H^T w_r with w_r[i] = sum over edges i -> k of relation r of
+    # dZ[k, J] / deg_r(k)
+    J = np.array(sorted({0, 77 % d, 130 % d, d - 1}))
+    words = saved[: full.ns].cpu().numpy()
+    mJ = np.stack([(words[:, j // 32] >> np.uint32(j % 32)) & np.uint32(1) for j in J], axis=1)
+    dzJ = G[:, J].astype(np.float64) * mJ
+    del words, mJ
+    ntype = full.g.ntype[full.ref["l2g"]]
+    toff = np.searchsorted(ntype, np.arange(3))
+    exp_ws, exp_db = [], []
+    for t in range(2):
+        lo, hi = toff[t], toff[t + 1]
+        acc = np.zeros((d, len(J)))
+        for c0 in range(lo, hi, 1 << 20):
+            c1 = min(hi, c0 + (1 << 20))
+            acc += H[c0:c1].astype(np.float64).T @ dzJ[c0:c1]
+        exp_ws.append(acc)
+        exp_db.append(dzJ[lo:hi].sum(axis=0))
+    scale = 1.0 / deg[full.dst_l * R + full.rel_l]
+    exp_wr = []
+    for r in range(R):
+        er_ = full.rel_l == r
+        wsum = np.stack([np.bincount(full.src_l[er_], weights=dzJ[full.dst_l[er_], q] * scale[er_],
+                                     minlength=full.ns) for q in range(len(J))], axis=1)
+        acc = np.zeros((d, len(J)))
+        for c0 in range(0, full.ns, 1 << 20):
+            c1 = min(full.ns, c0 + (1 << 20))
+            acc += H[c0:c1].astype(np.float64).T @ wsum[c0:c1]
+        exp_wr.append(acc)
+    Jt = torch.from_numpy(J).cuda()
+    for t in range(2):
+        assert parity_err(dWs[t][:, Jt].cpu().numpy(), exp_ws[t]) <= TOL, ("dW_self", t)
+        assert parity_err(db[t][Jt].cpu().numpy(), exp_db[t]) <= TOL, ("db", t)
+    for r in range(R):
+        assert parity_err(dWr[r][:, Jt].cpu().numpy(), exp_wr[r]) <= TOL, ("dW_rel", r)
+
+
 def test_fullsize_layer_sampled_rows(full):
     sub, wl = full.sub, full.wl
     d, R = wl.model.d, full.R
@@ -212,7 +256,8 @@ def test_fullsize_layer_sampled_rows(full):
     assert ok.sum() > 0.8 * ok.shape[0]
     got = dH[torch.from_numpy(srcs).cuda()].cpu().numpy()
     assert parity_err(got[ok], exp[ok]) <= TOL
-    del Hd, out, saved, dH
+    _check_dw_columns(full, H, G, saved, dWr, dWs, db, deg)
+    del Hd, out, saved, dH, dWr, dWs, db
 
 
 def test_fullsize_bf16_layer_sampled_rows(full):
@@ -254,43 +299,7 @@ def test_fullsize_bf16_layer_sampled_rows(full):
             exp[k] += dz[pos[j]] / deg[j * R + r] @ w.w_rel[r].astype(np.float64).T
     got = dH[torch.from_numpy(srcs).cuda()].float().cpu().numpy()
     assert parity_err(got, exp) <= 2e-2
-    # weight gradients on columns J: dZ[:, J] = G[:, J] * mask[:, J] (the GPU's
-    # mask bits), dW_self[t][:, J] = H_t^T dZ_t[:, J], db[t][J] = sum dZ_t[:, J],
-    # dW_r[:, J] = H^T w_r with w_r[i] = sum over edges i -> k of relation r of
-    # dZ[k, J] / deg_r(k)
-    J = np.array([0, 77, 130, 255])
-    words = saved[: full.ns].cpu().numpy()
-    mJ = np.stack([(words[:, j // 32] >> np.uint32(j % 32)) & np.uint32(1) for j in J], axis=1)
-    dzJ = G[:, J].astype(np.float64) * mJ
-    del words, mJ
-    ntype = full.g.ntype[full.ref["l2g"]]
-    toff = np.searchsorted(ntype, np.arange(3))
-    exp_ws, exp_db = [], []
-    for t in range(2):
-        lo, hi = toff[t], toff[t + 1]
-        acc = np.zeros((d, len(J)))
-        for c0 in range(lo, hi, 1 << 20):
-            c1 = min(hi, c0 + (1 << 20))
-            acc += H[c0:c1].astype(np.float64).T @ dzJ[c0:c1]
-        exp_ws.append(acc)
-        exp_db.append(dzJ[lo:hi].sum(axis=0))
-    scale = 1.0 / deg[full.dst_l * R + full.rel_l]
-    exp_wr = []
-    for r in range(R):
-        er_ = full.rel_l == r
-        wsum = np.stack([np.bincount(full.src_l[er_], weights=dzJ[full.dst_l[er_], q] * scale[er_],
-                                     minlength=full.ns) for q in range(len(J))], axis=1)
-        acc = np.zeros((d, len(J)))
-        for c0 in range(0, full.ns, 1 << 20):
-            c1 = min(full.ns, c0 + (1 << 20))
-            acc += H[c0:c1].astype(np.float64).T @ wsum[c0:c1]
-        exp_wr.append(acc)
-    Jt = torch.from_numpy(J).cuda()
-    for t in range(2):
-        assert parity_err(dWs[t][:, Jt].cpu().numpy(), exp_ws[t]) <= TOL, ("dW_self", t)
-        assert parity_err(db[t][Jt].cpu().numpy(), exp_db[t]) <= TOL, ("db", t)
-    for r in range(R):
-        assert parity_err(dWr[r][:, Jt].cpu().numpy(), exp_wr[r]) <= TOL, ("dW_rel", r)
+    _check_dw_columns(full, H, G, saved, dWr, dWs, db, deg)
     del Hd, out, saved, dH, dWr, dWs, db
 
 
