@@ -180,26 +180,30 @@ def _check_dw_columns(full, H, G, saved, dWr, dWs, db, deg):
     del words, mJ
     ntype = full.g.ntype[full.ref["l2g"]]
     toff = np.searchsorted(ntype, np.arange(3))
-    exp_ws, exp_db = [], []
+    nj = len(J)
+    # right-hand sides side by side, so H is read once: block t < 2 is dZ[:, J]
+    # on the rows of type t (zero elsewhere), block 2 + r is w_r
+    rhs = np.zeros((full.ns, (2 + R) * nj))
+    exp_db = []
     for t in range(2):
         lo, hi = toff[t], toff[t + 1]
-        acc = np.zeros((d, len(J)))
-        for c0 in range(lo, hi, 1 << 20):
-            c1 = min(hi, c0 + (1 << 20))
-            acc += H[c0:c1].astype(np.float64).T @ dzJ[c0:c1]
-        exp_ws.append(acc)
+        rhs[lo:hi, t * nj:(t + 1) * nj] = dzJ[lo:hi]
         exp_db.append(dzJ[lo:hi].sum(axis=0))
     scale = 1.0 / deg[full.dst_l * R + full.rel_l]
-    exp_wr = []
     for r in range(R):
-        er_ = full.rel_l == r
-        wsum = np.stack([np.bincount(full.src_l[er_], weights=dzJ[full.dst_l[er_], q] * scale[er_],
-                                     minlength=full.ns) for q in range(len(J))], axis=1)
-        acc = np.zeros((d, len(J)))
-        for c0 in range(0, full.ns, 1 << 20):
-            c1 = min(full.ns, c0 + (1 << 20))
-            acc += H[c0:c1].astype(np.float64).T @ wsum[c0:c1]
-        exp_wr.append(acc)
+        er_ = np.nonzero(full.rel_l == r)[0]
+        vals = dzJ[full.dst_l[er_]] * scale[er_, None]
+        src_r = full.src_l[er_]
+        for q in range(nj):
+            rhs[:, (2 + r) * nj + q] = np.bincount(src_r, weights=vals[:, q], minlength=full.ns)
+        del er_, vals, src_r
+    acc = np.zeros((d, (2 + R) * nj))
+    for c0 in range(0, full.ns, 1 << 20):
+        c1 = min(full.ns, c0 + (1 << 20))
+        acc += H[c0:c1].astype(np.float64).T @ rhs[c0:c1]
+    del rhs
+    exp_ws = [acc[:, t * nj:(t + 1) * nj] for t in range(2)]
+    exp_wr = [acc[:, (2 + r) * nj:(3 + r) * nj] for r in range(R)]
     Jt = torch.from_numpy(J).cuda()
     for t in range(2):
         assert parity_err(dWs[t][:, Jt].cpu().numpy(), exp_ws[t]) <= TOL, ("dW_self", t)
