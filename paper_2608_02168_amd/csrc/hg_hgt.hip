@@ -806,6 +806,172 @@ __global__ void __launch_bounds__(kGemmThreads) k_gemm_rows_sum3(int64_t n_rows,
   }
 }
 
+// out[i] = sum over the relations r with (i, r) active (CSC row i R + r not
+// empty, i.e. i in S_r) of A[i R + r] op(W_r), op(W_r) = W_r^T, for every row
+// i < n_rows: dK = sum_r dKt_r W_att[r]^T and dV likewise, each row written
+// once (no zero fill, no read-modify-write per relation).  The R split-fp16
+// matrices sit in LDS together (16 KB each at d = 64, R <= kSumRMax); each
+// product is unscaled on its own and added in relation order; a relation no
+// row of a wave's 16 is active in costs no MFMA; the next relation's rows are
+// loaded while the current ones are multiplied.
+constexpr int kSumRMax = 8;
+// one block of 16 waves per compute unit: R = 5 matrices take 80 KB, so two
+// blocks would need a few bytes more than the 160 KB of LDS
+constexpr int kSumRThreads = 1024;
+template <int D>
+__global__ void __launch_bounds__(kSumRThreads) k_gemm_rows_sumr(int64_t n_rows, int32_t R,
+                                                                 const float* __restrict__ W,
+                                                                 const float* __restrict__ A,
+                                                                 const int32_t* __restrict__ csc_ptr,
+                                                                 float* __restrict__ out) {
+  static_assert(D == 64, "R matrices of 64 x 64 in LDS");
+  constexpr int KB = D / 16, KB2 = D / 32, NB = D / 16;
+  constexpr int kWaves = kSumRThreads / 64;
+  constexpr int kRowsPerTile = 16 * kWaves;
+  constexpr int kFrag = KB2 * NB * 64;
+  extern __shared__ uint4 wsr[];  // per relation: [kFrag] high parts, then [kFrag] remainders
+  __shared__ float wmax[kWaves];
+  __shared__ float uws[kSumRMax];
+  const int tid = threadIdx.x;
+  for (int r = 0; r < R; ++r) {
+    const float* Wr = W + (int64_t)r * D * D;
+    float m = 0.f;
+    for (int e = tid; e < D * D / 4; e += kSumRThreads) {
+      const f32x4 v = *reinterpret_cast<const f32x4*>(Wr + 4 * e);
+      m = fmaxf(m, fmaxf(fmaxf(fabsf(v[0]), fabsf(v[1])), fmaxf(fabsf(v[2]), fabsf(v[3]))));
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
+    if ((tid & 63) == 0) wmax[tid >> 6] = m;
+    __syncthreads();
+    m = wmax[0];
+#pragma unroll
+    for (int q = 1; q < kWaves; ++q) m = fmaxf(m, wmax[q]);
+    const uint32_t ew = split_exp(m);
+    const float sw = split_scale(ew);
+    uint4* wl = wsr + (int64_t)r * 2 * kFrag;
+    for (int e = tid; e < kFrag; e += kSumRThreads) {
+      const int l = e & 63;
+      const int nb = (e >> 6) % NB;
+      const int kb2 = (e >> 6) / NB;
+      const int j = 16 * nb + (l & 15);
+      float v[8];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        // op(W) = W^T: element (k, j) is W[j][k]
+        const f32x4 x = *reinterpret_cast<const f32x4*>(Wr + (int64_t)j * D + 16 * (2 * kb2 + h) + 4 * (l >> 4));
+#pragma unroll
+        for (int q = 0; q < 4; ++q) v[4 * h + q] = x[q] * sw;
+      }
+      split8(v, wl[e], wl[kFrag + e]);
+    }
+    if (tid == 0) uws[r] = split_unscale(ew);
+    __syncthreads();
+  }
+  const int w = tid >> 6;
+  const int l = lane64();
+  const int g = l >> 4, c = l & 15;
+  const int64_t ntiles = (n_rows + kRowsPerTile - 1) / kRowsPerTile;
+  for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
+    const int64_t i = t * kRowsPerTile + 16 * w + c;
+    const bool live = i < n_rows;
+    // the row's CSC pointers i R .. i R + R: relation r is active iff its row is not empty
+    int32_t p[kSumRMax + 1];
+#pragma unroll
+    for (int q = 0; q <= kSumRMax; ++q) p[q] = (live && q <= R) ? csc_ptr[i * R + q] : 0;
+    f32x4 tot[NB];
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) tot[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    f32x4 nxt[KB];
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb)
+      nxt[kb] = (live && R > 0 && p[1] > p[0])
+                    ? *reinterpret_cast<const f32x4*>(A + (i * R) * D + 16 * kb + 4 * g)
+                    : f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int r = 0; r < kSumRMax; ++r) {
+      if (r >= R) break;
+      __builtin_amdgcn_sched_barrier(0);
+      const bool act = live && p[r + 1] > p[r];
+      f32x4 a[KB];
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) a[kb] = nxt[kb];
+      if (r + 1 < R && r + 1 < kSumRMax) {
+        const bool act1 = live && p[r + 2] > p[r + 1];
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb)
+          nxt[kb] = act1 ? *reinterpret_cast<const f32x4*>(A + (i * R + r + 1) * D + 16 * kb + 4 * g)
+                         : f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+      if (__ballot(act) == 0) continue;  // wave-uniform: no row of the 16 is in S_r
+      float m = 0.f;
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb)
+        m = fmaxf(m, fmaxf(fmaxf(fabsf(a[kb][0]), fabsf(a[kb][1])), fmaxf(fabsf(a[kb][2]), fabsf(a[kb][3]))));
+      m = fmaxf(m, __shfl_xor(m, 16, 64));
+      m = fmaxf(m, __shfl_xor(m, 32, 64));
+      const uint32_t ex = split_exp(m);
+      const float sx = split_scale(ex), ux = split_unscale(ex);
+      uint4 xh[KB2], xlo[KB2];
+#pragma unroll
+      for (int kb2 = 0; kb2 < KB2; ++kb2) {
+        float v[8];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          v[q] = a[2 * kb2][q] * sx;
+          v[4 + q] = a[2 * kb2 + 1][q] * sx;
+        }
+        split8(v, xh[kb2], xlo[kb2]);
+      }
+      const uint4* wl = wsr + (int64_t)r * 2 * kFrag;
+      f32x4 acc[NB];
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kb2 = 0; kb2 < KB2; ++kb2) {
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+          const int e = (kb2 * NB + nb) * 64 + l;
+          const uint4 bh = wl[e], bl = wl[kFrag + e];
+          acc[nb] = mfma_f16(bh, xh[kb2], acc[nb]);
+          acc[nb] = mfma_f16(bh, xlo[kb2], acc[nb]);
+          acc[nb] = mfma_f16(bl, xh[kb2], acc[nb]);
+        }
+      }
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) tot[nb] += split_unscale4(acc[nb], ux, uws[r]);
+    }
+    if (live) {
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+        *reinterpret_cast<f32x4*>(out + i * D + 16 * nb + 4 * g) = tot[nb];
+    }
+  }
+}
+
+template <int D>
+int launch_gemm_rows_sumr(const char* name, int64_t n_rows, int32_t R, const float* W, const float* A,
+                          const int32_t* csc_ptr, float* out, hipStream_t st) {
+  if (n_rows <= 0) return HG_OK;
+  if (R < 1 || R > kSumRMax) return fail(HG_ERR_ARG, "%s: R = %d outside [1, %d]", name, R, kSumRMax);
+  const size_t lds = sizeof(uint4) * 2 * ((D / 32) * (D / 16) * 64) * (size_t)R;
+  auto kern = k_gemm_rows_sumr<D>;
+  if (lds > 65536) {
+    static bool attr_set = false;
+    if (!attr_set) {
+      HG_HIP_TRY(hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
+                                     (int)(sizeof(uint4) * 2 * ((D / 32) * (D / 16) * 64) * kSumRMax)));
+      attr_set = true;
+    }
+  }
+  const int64_t tiles = cdiv(n_rows, 16 * (kSumRThreads / 64));
+  const int64_t cap = (int64_t)num_cus();
+  HG_LAUNCH(name, kern, dim3((unsigned)(tiles < cap ? tiles : cap)), dim3(kSumRThreads), lds, st, n_rows, R, W, A,
+            csc_ptr, out);
+  return HG_OK;
+}
+
 template <int D>
 int hgt_bwd_impl(const hg_subgraph* s, const hg_hgt_desc* L, const float* Hin, const hg_hgt_weights* W,
                  const uint32_t* mask, const void* saved, const float* G, float* dHin, const hg_hgt_grads* dW,
@@ -871,19 +1037,32 @@ int hgt_bwd_impl(const hg_subgraph* s, const hg_hgt_desc* L, const float* Hin, c
       HG_LAUNCH("hgt_bwd_heavy", k_hgt_heavy_reduce<D>, dim3(attn_grid(s->plan_heavy)), dim3(kAttnThreads), 0, st,
                 (int64_t)s->plan_heavy, pv.heavy, (const double*)w.pk, (const double*)w.pv, w.dKt, w.dVt);
   }
-  // (4) dK += dKt_r W_att[r]^T, dV += dVt_r W_msg[r]^T; full dW_att, dW_msg
-  HG_TRY(fill_f32(w.dK, 0.f, s->n_sub * (int64_t)D, st));
-  HG_TRY(fill_f32(w.dV, 0.f, s->n_sub * (int64_t)D, st));
+  // (4) dK = sum_r dKt_r W_att[r]^T, dV = sum_r dVt_r W_msg[r]^T over the rows
+  // of S_r; full dW_att, dW_msg
+  const bool fused_rel = D == 64 && R <= kSumRMax;
+  if (fused_rel) {
+    if constexpr (D == 64) {
+      HG_TRY(launch_gemm_rows_sumr<D>("hgt_bwd_dx_rel", s->n_sub, R, w.Watt, w.dKt, (const int32_t*)s->csc_ptr,
+                                      w.dK, st));
+      HG_TRY(launch_gemm_rows_sumr<D>("hgt_bwd_dx_rel", s->n_sub, R, w.Wmsg, w.dVt, (const int32_t*)s->csc_ptr,
+                                      w.dV, st));
+    }
+  } else {
+    HG_TRY(fill_f32(w.dK, 0.f, s->n_sub * (int64_t)D, st));
+    HG_TRY(fill_f32(w.dV, 0.f, s->n_sub * (int64_t)D, st));
+  }
   int64_t off = 0;
   for (int r = 0; r < R; ++r) {
     const int64_t n = s->n_active[r];
     const int64_t wo = (int64_t)r * D * D;
-    HG_TRY((launch_gemm_rows_pp<D, true>("hgt_bwd_dx_rel", n, w.Watt + wo,
-                                         LoadRows<D, float>{w.dKt, rows_list(pv.active + off, R, r)},
-                                         StoreRows<D, float>{w.dK, rows_list(pv.active + off), nullptr, w.dK}, st)));
-    HG_TRY((launch_gemm_rows_pp<D, true>("hgt_bwd_dx_rel", n, w.Wmsg + wo,
-                                         LoadRows<D, float>{w.dVt, rows_list(pv.active + off, R, r)},
-                                         StoreRows<D, float>{w.dV, rows_list(pv.active + off), nullptr, w.dV}, st)));
+    if (!fused_rel) {
+      HG_TRY((launch_gemm_rows_pp<D, true>("hgt_bwd_dx_rel", n, w.Watt + wo,
+                                           LoadRows<D, float>{w.dKt, rows_list(pv.active + off, R, r)},
+                                           StoreRows<D, float>{w.dK, rows_list(pv.active + off), nullptr, w.dK}, st)));
+      HG_TRY((launch_gemm_rows_pp<D, true>("hgt_bwd_dx_rel", n, w.Wmsg + wo,
+                                           LoadRows<D, float>{w.dVt, rows_list(pv.active + off, R, r)},
+                                           StoreRows<D, float>{w.dV, rows_list(pv.active + off), nullptr, w.dV}, st)));
+    }
     HG_TRY((launch_gemm_tn<D>("hgt_bwd_dw", n, LoadRows<D, float>{sv.K, rows_list(pv.active + off)},
                               LoadRows<D, float>{w.dKt, rows_list(pv.active + off, R, r)}, w.splitk, w.colsum,
                               w.gatt + wo, nullptr, 0, st)));
