@@ -99,6 +99,14 @@ def _softmax_by_dst(n, dst, score):
     return ex / den[dst]
 
 
+def _softmax_backward(n, dst, alpha, dalpha):
+    """dscore[e, s] = alpha (dalpha - sum over the edges e' into dst[e] of
+    alpha(e') dalpha(e')): the softmax's Jacobian applied per destination."""
+    sdot = np.zeros((n, alpha.shape[1]))
+    np.add.at(sdot, dst, alpha * dalpha)
+    return alpha * (dalpha - sdot[dst])
+
+
 def forward(n: int, src_l, dst_l, rel_l, ntype_l, H, params: Params, S: int):
     """Returns (H_out, Z, h_tilde, alpha) in float64."""
     src = np.asarray(src_l, dtype=np.int64)
@@ -155,9 +163,7 @@ def backward(n: int, src_l, dst_l, rel_l, ntype_l, H, params: Params, S: int, G,
     dht_j = _heads(dht, S)[dst]                                   # [E, S, dk]
     dalpha = (dht_j * msg).sum(-1)                                # [E, S]
     dmsg = alpha[:, :, None] * dht_j
-    sdot = np.zeros((n, S))
-    np.add.at(sdot, dst, alpha * dalpha)
-    dscore = alpha * (dalpha - sdot[dst])
+    dscore = _softmax_backward(n, dst, alpha, dalpha)
     dkt = (dscore * c[:, None])[:, :, None] * Qj
     dQ = np.zeros((n, S, dk))
     np.add.at(dQ, dst, (dscore * c[:, None])[:, :, None] * kt)

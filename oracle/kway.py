@@ -56,10 +56,11 @@ def home_rows(subs, part, sub_k):
 
 
 def run_kway(graph_arrays: dict, K: int, build_args: dict, feats_global, weights: list, head: dict,
-             labels_global, lambda_n=2e-4, scale=0.1, eps=1e-5, ddof=0, frozen_home=None):
+             labels_global, lambda_n=2e-4, scale=0.1, eps=1e-5, ddof=0, frozen_home=None, masks=None):
     """One step over the K subgraphs.  `frozen_home` (list of K arrays) replaces
     the home copies (finite-difference checks hold them fixed, as the
-    gradient does).  Returns a dict."""
+    gradient does).  `masks[k][l]` (optional) gives the ReLU decisions of
+    layer l in subgraph k for the backward (otherwise Z > 0).  Returns a dict."""
     part = graph_arrays["part"]
     subs = [select.build(**graph_arrays, k=k, **build_args) for k in range(K)]
     x = np.asarray(feats_global, dtype=np.float64)
@@ -90,8 +91,9 @@ def run_kway(graph_arrays: dict, K: int, build_args: dict, feats_global, weights
         g = dHk[k]
         for li in reversed(range(len(weights))):
             w = weights[li]
+            mk = None if masks is None else masks[k][li]
             g, dwr, dws, db = layer.backward(sb.n_sub, sb.src_l, sb.dst_l, sb.rel_l, sb.ntype_l, hs[k][li], w.w_rel,
-                                             w.w_self, w.bias, g)
+                                             w.w_self, w.bias, g, mask=mk)
             if grads is None:
                 grads = [None] * len(weights)
             gk = (dwr, dws, db)

@@ -49,12 +49,15 @@ def out_hindex(n: int, src: np.ndarray, dst: np.ndarray) -> np.ndarray:
     out-degree >= h (the out-neighbour multiset, duplicates counted)."""
     src = np.asarray(src, dtype=np.int64)
     vals = out_degree(n, src)[np.asarray(dst, dtype=np.int64)]
-    order = np.lexsort((-vals, src))           # group by source, values descending
-    s, a = src[order], vals[order]
-    first = np.searchsorted(s, s, side="left")
-    rank = np.arange(s.shape[0]) - first + 1   # 1-based position inside the group
-    # a is descending inside a group, so "a_i >= i" holds on a prefix whose
-    # length is the h-index.
+    # group by source, values descending inside a group: one sort of the key
+    # (source, vmax - value), both parts below 2^32
+    vmax = np.int64(src.shape[0])
+    key = np.sort((src << 32) | (vmax - vals))
+    s, a = key >> 32, vmax - (key & np.int64(0xFFFFFFFF))
+    start = np.flatnonzero(np.r_[True, s[1:] != s[:-1]]) if s.size else np.zeros(0, np.int64)
+    rank = np.arange(s.shape[0]) - np.repeat(start, np.diff(np.r_[start, s.shape[0]])) + 1
+    # a is descending inside a group, so "a_i >= i" (1-based i) holds on a
+    # prefix whose length is the h-index.
     return np.bincount(s, weights=(a >= rank), minlength=n).astype(np.int64)
 
 

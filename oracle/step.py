@@ -17,10 +17,13 @@ from . import align, hgt, layer, objective, select, temporal
 
 def run(graph_arrays: dict, build_args: dict, feats_global: np.ndarray, weights: list,
         h_ref: np.ndarray, g_ext: np.ndarray, omega=None, lambda_n=2e-4, scale=0.1,
-        eps=1e-5, ddof=0, heads=None, head=None, labels_global=None):
+        eps=1e-5, ddof=0, heads=None, head=None, labels_global=None, masks=None):
     """With `head` (dict W1, b1, W2, b2) and labels (global order), the
     upstream gradient is the prediction head's dL_BCE/dH instead of g_ext, and
-    the result also holds the BCE loss and the head's gradients."""
+    the result also holds the BCE loss and the head's gradients.  `masks[l]`
+    (optional) gives the ReLU decisions of layer l for the backward (a caller
+    whose pre-activations were decided in another precision passes its own);
+    otherwise they are Z > 0."""
     sub = select.build(**graph_arrays, **build_args)
     edges = (sub.n_sub, sub.src_l, sub.dst_l, sub.rel_l, sub.ntype_l)
     h = [np.asarray(feats_global, dtype=np.float64)[sub.local2global]]
@@ -43,11 +46,12 @@ def run(graph_arrays: dict, build_args: dict, feats_global: np.ndarray, weights:
     grads = []
     for li in reversed(range(len(weights))):
         w = weights[li]
+        mk = None if masks is None else masks[li]
         if isinstance(w, dict):
-            g, gp = hgt.backward(*edges, h[li], hgt.Params(*[w[n] for n in hgt.PARAM_NAMES]), heads, g)
+            g, gp = hgt.backward(*edges, h[li], hgt.Params(*[w[n] for n in hgt.PARAM_NAMES]), heads, g, mask=mk)
             grads.append({n: getattr(gp, n) for n in hgt.PARAM_NAMES})
             continue
-        g, dwr, dws, db = layer.backward(*edges, h[li], w.w_rel, w.w_self, w.bias, g)
+        g, dwr, dws, db = layer.backward(*edges, h[li], w.w_rel, w.w_self, w.bias, g, mask=mk)
         grads.append((dwr, dws, db))
     if head is not None:
         return sub, h, losses, g, grads[::-1], head_out

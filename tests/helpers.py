@@ -42,3 +42,26 @@ def graph_to_dev(g, device="cuda"):
     import torch
     return dict(src=to_dev(g.src, device), dst=to_dev(g.dst, device), rel=to_dev(g.rel, device),
                 ntype=to_dev(g.ntype, device), part=to_dev(g.part, device))
+
+
+def clear_relu_kinks(a, rows, margin_rel=1e-4):
+    """Per-column shift of a bias that keeps every pre-activation a[rows, j]
+    at least margin_rel * rms(a[rows]) away from the ReLU kink, so that a
+    float32 and a float64 evaluation take the same decision there.  Returns
+    the shift [d] (zero for a column that needs none); tests add it to the
+    bias before either side runs."""
+    a = np.asarray(a, dtype=np.float64)[rows]
+    d = a.shape[1]
+    if a.size == 0:
+        return np.zeros(d)
+    margin = margin_rel * np.sqrt(np.mean(a * a))
+    delta = np.zeros(d)
+    for j in range(d):
+        for k in range(256):
+            cand = ((k + 1) // 2) * (1 if k % 2 else -1) * 2.0 * margin   # 0, +2m, -2m, +4m, ...
+            if np.min(np.abs(a[:, j] + cand)) > margin:
+                delta[j] = cand
+                break
+        else:
+            raise AssertionError(f"no bias shift clears column {j}")
+    return delta

@@ -72,22 +72,55 @@ def test_bf16_alignment(d):
     assert parity_err(dHref.float().cpu().numpy(), dY) <= TOL
 
 
-def test_bf16_step_runs_and_matches_layerwise():
-    """The d=256, 3-layer bf16 workload's recipe at reduced size through the
-    runner: first-layer output against the oracle on the same bf16 input."""
+def test_bf16_step_every_layer_and_gradient():
+    """The d = 256, 3-layer bf16 workload's recipe at reduced size through the
+    runner (the step the benchmark times), checked layer by layer against the
+    oracle fed the GPU's own bf16 values: every layer's output and ReLU mask
+    (checked outside the rounding band, kept inside it), the loss, the
+    alignment's upstream gradient, and every layer's dH_in, dW_rel, dW_self
+    and db under the checked masks."""
     base = synth.WORKLOADS["large_bf16"]
     wl = synth.Workload(synth.scaled(base.graph, 0.0005), base.model, "bf16-small")
+    mc = wl.model
     g = synth.make_graph(wl.graph)
     inp = runner.make_inputs(wl, g)
     res = runner.run_step(inp)
     torch.cuda.synchronize()
-    assert np.all(np.isfinite(res.loss.cpu().numpy()))
-    sub = inp.sub
+    sub, d, L = inp.sub, mc.d, mc.n_layers
+    assert d == 256 and L == 3
     ref = select.build(g.src, g.dst, g.rel, g.ntype, g.part, g.k, wl.graph.n_rel, 2, wl.graph.budget)
-    X = inp.h0.float().cpu().numpy()
-    w = inp.weights_np[0]
-    out, _ = layer.forward(ref.n_sub, ref.src_l, ref.dst_l, ref.rel_l, ref.ntype_l, X, w.w_rel, w.w_self, w.bias)
-    assert parity_err(inp.H[1].float().cpu().numpy(), out) <= TOL
-    for gw in res.grads:
-        for t in gw:
-            assert torch.isfinite(t).all()
+    args = (ref.n_sub, ref.src_l, ref.dst_l, ref.rel_l, ref.ntype_l)
+    f = lambda t: t.float().cpu().numpy()
+    masks = []
+    for li in range(L):
+        w = inp.weights_np[li]
+        out, Z = layer.forward(*args, f(inp.H[li]), w.w_rel, w.w_self, w.bias)
+        assert parity_err(f(inp.H[li + 1]), out) <= TOL, ("H", li + 1)
+        gm = unpack_mask(inp.saved[li][: ref.n_sub].cpu().numpy(), d)
+        near = np.abs(Z) <= TOL * np.sqrt(np.mean(Z * Z))
+        assert np.array_equal(gm[~near], Z[~near] > 0), ("mask", li)
+        masks.append(gm)
+    # loss and the last layer's upstream gradient G_ext + lambda_CCA dL/dX
+    ov = ref.overlap
+    Hl = f(inp.H[L])
+    (li_, ld_, L_), dX, _ = align.loss_and_grad(Hl[ov], f(inp.href), None, mc.lambda_n, mc.lambda_cca, mc.eps,
+                                               mc.ddof)
+    for a, b in zip(res.loss.cpu().numpy(), (li_, ld_, L_)):
+        assert abs(a - b) <= TOL * abs(b)
+    G = f(inp.gext).astype(np.float64)
+    G[ov] += dX
+    assert parity_err(f(inp.g), G) <= TOL
+    # backward layer by layer, each from the GPU's bf16 upstream gradient;
+    # the step's ping-pong buffers hold the input gradients of layers 0 and 1,
+    # and the last layer's is formed again (the backward is deterministic)
+    w2 = inp.weights[L - 1]
+    d2 = api.hg_layer_bwd(sub, inp.H[L - 1], w2[0], w2[1], inp.saved[L - 1], inp.g)[0]
+    dh_in = {L - 1: d2, 1: inp.dH[1], 0: inp.dH[0]}
+    upstream = {L - 1: inp.g, 1: d2, 0: inp.dH[1]}
+    for li in reversed(range(L)):
+        w = inp.weights_np[li]
+        exp = layer.backward(*args, f(inp.H[li]), w.w_rel, w.w_self, w.bias, f(upstream[li]), mask=masks[li])
+        got = (dh_in[li],) + tuple(res.grads[li])
+        for a, b, nm in zip(got, exp, ("dH", "dW_rel", "dW_self", "dbias")):
+            err = parity_err(f(a), b)
+            assert err <= TOL, (li, nm, err)

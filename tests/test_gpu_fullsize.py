@@ -7,8 +7,8 @@ The oracle cannot redo a 200M-edge step in float64 within a test, so:
   * the CSR is pinned by properties that fix it uniquely: every entry's
     original edge id maps to its row (dst, r) and to its column, rows are in
     ascending edge id, and every kept edge appears exactly once; the CSC by
-    exact row counts, per-row destination fingerprints and bit-exact
-    csc_scale;
+    exact row counts, the destination of every entry in the oracle's order
+    and bit-exact csc_scale;
   * the layer forward on sampled destination rows (plus the heaviest rows),
     the layer backward on sampled dH rows, computed one by one from the
     edge list in float64; the alignment on the full overlap batch;
@@ -22,7 +22,7 @@ import pytest
 
 torch = pytest.importorskip("torch")
 
-from oracle import align, layer, select, splitmix
+from oracle import align, layer, select
 from paper_2608_02168_amd import api, runner, synth
 from tests.helpers import pack_mask, parity_err, to_dev, unpack_mask
 
@@ -68,9 +68,19 @@ class Full:
         self.rel_l = g.rel[self.eid].astype(np.int64)
         self.R = cfg.n_rel
         self.ns = self.ref["l2g"].shape[0]
+        self.ntype_l = g.ntype[self.ref["l2g"]].astype(np.int64)
+        self._adj = None
+
+    def adjacency(self):
+        """oracle.layer's mean adjacency of every relation (kept for the module)."""
+        if self._adj is None:
+            self._adj = [layer.mean_adjacency(self.ns, self.src_l, self.dst_l, self.rel_l, r)
+                         for r in range(self.R)]
+        return self._adj
 
     def free(self):
         del self.sub
+        self._adj = None
         gc.collect()
         torch.cuda.empty_cache()
 
@@ -120,190 +130,175 @@ def test_fullsize_csr_csc_properties(full):
     expect[full.eid] = 1
     assert np.array_equal(seen, expect)
     del eid, col, row, seen, expect
-    # CSC: counts, destination fingerprints per row, exact scale
+    # CSC: counts, every entry in order, exact scale
     cptr = sub.view("csc_ptr").cpu().numpy().astype(np.int64)
     assert np.array_equal(np.diff(cptr), cnt_csc)
     crow = sub.view("csc_row").cpu().numpy().astype(np.int64)
-    # per-row sums of two 24-bit hashes of the destination ids (exact in float64)
-    h = splitmix.mix(crow.astype(np.uint64))
+    # exact order: the oracle's CSC lists the kept edges by (source row, edge
+    # index), i.e. its stable sort on the row key; one sort of the unique
+    # int64 key (row << 28 | position among the kept edges) gives that order
+    e_s = full.eid.shape[0]
+    assert e_s < (1 << 28) and nq < (1 << 35)
+    order = np.sort((key_csc << 28) | np.arange(e_s, dtype=np.int64)) & ((1 << 28) - 1)
+    assert np.array_equal(crow, full.dst_l[order])
     rows = np.repeat(np.arange(nq), cnt_csc)
-    hs = splitmix.mix(full.dst_l.astype(np.uint64))
-    for shift in (40, 16):
-        a = ((h >> np.uint64(shift)) & np.uint64(0xFFFFFF)).astype(np.float64)
-        b = ((hs >> np.uint64(shift)) & np.uint64(0xFFFFFF)).astype(np.float64)
-        got = np.bincount(rows, weights=a, minlength=nq)
-        exp = np.bincount(key_csc, weights=b, minlength=nq)
-        assert np.array_equal(got, exp)
+    del order
     scale = sub.view("csc_scale").cpu().numpy()
     deg = cnt_csr[crow * R + (rows % R)].astype(np.float32)
     assert np.array_equal(scale.view(np.uint32), (np.float32(1.0) / deg).view(np.uint32))
 
 
-def _in_edges(full, rows):
-    """Edges (src, rel, dst) of the subgraph whose destination is in rows."""
-    m = np.isin(full.dst_l, rows)
-    return full.src_l[m], full.rel_l[m], full.dst_l[m]
+def _closure(full, dsts):
+    """The sub-graph of all in-edges of `dsts`, relabelled: (nodes, src, dst, rel)
+    with nodes the sorted local ids involved.  A layer's pre-activation of a
+    node of `dsts` on this sub-graph equals its value on the whole graph."""
+    m = np.isin(full.dst_l, dsts)
+    s, r, t = full.src_l[m], full.rel_l[m], full.dst_l[m]
+    nodes = np.unique(np.concatenate([s, t, dsts]))
+    return nodes, np.searchsorted(nodes, s), np.searchsorted(nodes, t), r
 
 
-def _z_rows(full, rows, H, w):
-    """float64 pre-activations z for the given destination rows."""
-    R = full.R
-    s, r, t = _in_edges(full, rows)
-    pos = {v: i for i, v in enumerate(rows)}
-    idx = np.array([pos[x] for x in t], dtype=np.int64) if t.size else np.zeros(0, np.int64)
-    n, d = rows.shape[0], H.shape[1]
-    agg = np.zeros((n, R, d))
-    cnt = np.zeros((n, R))
-    np.add.at(agg, (idx, r), H[s].astype(np.float64))
-    np.add.at(cnt, (idx, r), 1.0)
-    mean = np.divide(agg, cnt[:, :, None], out=np.zeros_like(agg), where=cnt[:, :, None] > 0)
-    z = np.einsum("nrd,rde->ne", mean, w.w_rel.astype(np.float64))
-    typ = full.g.ntype[full.ref["l2g"][rows]].astype(np.int64)
-    z += np.einsum("nd,nde->ne", H[rows].astype(np.float64), w.w_self.astype(np.float64)[typ])
-    z += w.bias.astype(np.float64)[typ]
-    return z
+def _mask_checked(gpu_bits, z, band):
+    """The GPU's ReLU decisions agree with z > 0 wherever |z| exceeds the
+    rounding band; inside the band either decision is correct and the GPU's
+    is kept.  Returns the mask the oracle's backward takes."""
+    near = np.abs(z) <= band
+    assert np.array_equal(gpu_bits[~near], z[~near] > 0)
+    return np.where(near, gpu_bits, z > 0)
 
 
-def _check_dw_columns(full, H, G, saved, dWr, dWs, db, deg):
+def _check_layer_rows(full, H, w, out, saved, dH, G, rows, srcs, bar):
+    """Forward rows and dH source rows of the mean layer against oracle.layer
+    on the closed sub-graphs that determine them (float64), the backward
+    under the GPU's mask after checking it outside the rounding band."""
+    d, nt = H.shape[1], full.ntype_l
+    H64 = H.astype(np.float64)
+    nodes, s, t, r = _closure(full, rows)
+    Ho, Z = layer.forward(nodes.shape[0], s, t, r, nt[nodes], H64[nodes], w.w_rel, w.w_self, w.bias)
+    at = np.searchsorted(nodes, rows)
+    ri = torch.from_numpy(rows).cuda()
+    assert parity_err(out[ri].float().cpu().numpy(), Ho[at]) <= bar
+    band = bar * np.sqrt(np.mean(Z[at] ** 2))
+    _mask_checked(unpack_mask(saved[ri].cpu().numpy(), d), Z[at], band)
+    del Ho, Z
+    # dH_i needs dZ of i and of every destination of its out-edges, each from
+    # its full in-edge set
+    dsts = np.unique(np.concatenate([full.dst_l[np.isin(full.src_l, srcs)], srcs]))
+    nodes, s, t, r = _closure(full, dsts)
+    _, Z = layer.forward(nodes.shape[0], s, t, r, nt[nodes], H64[nodes], w.w_rel, w.w_self, w.bias)
+    inside = np.searchsorted(nodes, dsts)
+    gm = unpack_mask(saved[torch.from_numpy(dsts).cuda()].cpu().numpy(), d)
+    band = bar * np.sqrt(np.mean(Z[inside] ** 2))
+    mask = np.zeros(Z.shape, bool)
+    mask[inside] = _mask_checked(gm, Z[inside], band)
+    Gl = np.zeros(Z.shape)
+    Gl[inside] = G[dsts]
+    dHl = layer.backward(nodes.shape[0], s, t, r, nt[nodes], H64[nodes], w.w_rel, w.w_self, w.bias, Gl,
+                         mask=mask)[0]
+    got = dH[torch.from_numpy(srcs).cuda()].float().cpu().numpy()
+    assert parity_err(got, dHl[np.searchsorted(nodes, srcs)]) <= bar
+
+
+def _check_dw_columns(full, H, w, G, saved, dWr, dWs, db, band_rel):
     """Four whole columns J of dW_self, db and every dW_r, each a reduction
     over all rows and edges (every split-K chunk and output tile), against
-    float64 under the GPU's own mask, within float32's 1e-4."""
-    R, d = full.R, H.shape[1]
-    # weight gradients on columns J: dZ[:, J] = G[:, J] * mask[:, J] (the GPU's
-    # mask bits), dW_self[t][:, J] = H_t^T dZ_t[:, J], db[t][J] = sum dZ_t[:, J],
-    # dW_r[:, J] = H^T w_r with w_r[i] = sum over edges i -> k of relation r of
-    # dZ[k, J] / deg_r(k)
+    float64 within float32's 1e-4.  The ReLU decisions on J come from z[:, J]
+    computed in float64 for every row (the oracle's mean adjacency of each
+    relation applied to H W_r[:, J]); the GPU's bit is taken only where |z| is
+    within band_rel * rms(z) of the kink, and must agree everywhere else."""
+    R, d, ns = full.R, H.shape[1], full.ns
     J = np.array(sorted({0, 77 % d, 130 % d, d - 1}))
-    words = saved[: full.ns].cpu().numpy()
-    mJ = np.stack([(words[:, j // 32] >> np.uint32(j % 32)) & np.uint32(1) for j in J], axis=1)
-    dzJ = G[:, J].astype(np.float64) * mJ
-    del words, mJ
-    ntype = full.g.ntype[full.ref["l2g"]]
-    toff = np.searchsorted(ntype, np.arange(3))
     nj = len(J)
+    adj = full.adjacency()
+    zJ = np.zeros((ns, nj))
+    step = 1 << 20
+
+    def rows_times(Wc):
+        out = np.empty((ns, Wc.shape[1]))
+        for c0 in range(0, ns, step):
+            out[c0:c0 + step] = H[c0:c0 + step].astype(np.float64) @ Wc
+        return out
+
+    for r in range(R):
+        zJ += adj[r] @ rows_times(w.w_rel[r][:, J].astype(np.float64))
+    toff = full.sub.type_off_host()
+    for t in range(2):
+        lo, hi = toff[t], toff[t + 1]
+        zJ[lo:hi] += (H[lo:hi].astype(np.float64) @ w.w_self[t][:, J].astype(np.float64)
+                      + w.bias[t][J].astype(np.float64))
+    words = saved[:ns].cpu().numpy()
+    gm = np.stack([((words[:, j // 32] >> np.uint32(j % 32)) & np.uint32(1)).astype(bool) for j in J], axis=1)
+    del words
+    mask = _mask_checked(gm, zJ, band_rel * np.sqrt(np.mean(zJ * zJ)))
+    del gm, zJ
+    dzJ = G[:, J].astype(np.float64) * mask
     # right-hand sides side by side, so H is read once: block t < 2 is dZ[:, J]
-    # on the rows of type t (zero elsewhere), block 2 + r is w_r
-    rhs = np.zeros((full.ns, (2 + R) * nj))
+    # on the rows of type t (zero elsewhere), block 2 + r is A_r^T dZ[:, J]
+    rhs = np.zeros((ns, (2 + R) * nj))
     exp_db = []
     for t in range(2):
         lo, hi = toff[t], toff[t + 1]
         rhs[lo:hi, t * nj:(t + 1) * nj] = dzJ[lo:hi]
         exp_db.append(dzJ[lo:hi].sum(axis=0))
-    scale = 1.0 / deg[full.dst_l * R + full.rel_l]
     for r in range(R):
-        er_ = np.nonzero(full.rel_l == r)[0]
-        vals = dzJ[full.dst_l[er_]] * scale[er_, None]
-        src_r = full.src_l[er_]
-        for q in range(nj):
-            rhs[:, (2 + r) * nj + q] = np.bincount(src_r, weights=vals[:, q], minlength=full.ns)
-        del er_, vals, src_r
+        rhs[:, (2 + r) * nj:(3 + r) * nj] = adj[r].T @ dzJ
     acc = np.zeros((d, (2 + R) * nj))
-    for c0 in range(0, full.ns, 1 << 20):
-        c1 = min(full.ns, c0 + (1 << 20))
-        acc += H[c0:c1].astype(np.float64).T @ rhs[c0:c1]
+    for c0 in range(0, ns, step):
+        acc += H[c0:c0 + step].astype(np.float64).T @ rhs[c0:c0 + step]
     del rhs
-    exp_ws = [acc[:, t * nj:(t + 1) * nj] for t in range(2)]
-    exp_wr = [acc[:, (2 + r) * nj:(3 + r) * nj] for r in range(R)]
     Jt = torch.from_numpy(J).cuda()
     for t in range(2):
-        assert parity_err(dWs[t][:, Jt].cpu().numpy(), exp_ws[t]) <= TOL, ("dW_self", t)
+        assert parity_err(dWs[t][:, Jt].cpu().numpy(), acc[:, t * nj:(t + 1) * nj]) <= TOL, ("dW_self", t)
         assert parity_err(db[t][Jt].cpu().numpy(), exp_db[t]) <= TOL, ("db", t)
     for r in range(R):
-        assert parity_err(dWr[r][:, Jt].cpu().numpy(), exp_wr[r]) <= TOL, ("dW_rel", r)
+        assert parity_err(dWr[r][:, Jt].cpu().numpy(), acc[:, (2 + r) * nj:(3 + r) * nj]) <= TOL, ("dW_rel", r)
+
+
+def _sample_rows(full, rng, n_rows, n_hubs, n_srcs):
+    indeg = np.bincount(full.dst_l, minlength=full.ns)
+    rows = np.unique(np.concatenate([rng.choice(full.ns, n_rows, replace=False), np.argsort(indeg)[-n_hubs:]]))
+    srcs = np.unique(rng.choice(full.ns, n_srcs, replace=False))
+    return rows, srcs
 
 
 def test_fullsize_layer_sampled_rows(full):
+    """fp32 layer at the workload's width: forward rows (sampled and the
+    heaviest destinations), dH on sampled source rows, and whole columns of
+    every weight gradient, against the oracle."""
     sub, wl = full.sub, full.wl
-    d, R = wl.model.d, full.R
+    d = wl.model.d
     H = synth.features(wl.model.seed, full.g.n_nodes, d)[full.ref["l2g"]]
-    w = synth.layer_weights(wl.model.seed, 0, R, 2, d, 0.1)
+    w = synth.layer_weights(wl.model.seed, 0, full.R, 2, d, 0.1)
     Hd = to_dev(H)
     wr, wsf, b = to_dev(w.w_rel), to_dev(w.w_self), to_dev(w.bias)
     out, saved = api.hg_layer_fwd(sub, Hd, wr, wsf, b)
-    rng = np.random.default_rng(0)
-    indeg = np.bincount(full.dst_l, minlength=full.ns)
-    rows = np.unique(np.concatenate([rng.choice(full.ns, 3000, replace=False),
-                                     np.argsort(indeg)[-16:]]))
-    z = _z_rows(full, rows, H, w)
-    got = out[torch.from_numpy(rows).cuda()].cpu().numpy()
-    assert parity_err(got, np.maximum(z, 0) + H[rows]) <= TOL
-    band = 1e-4 * np.sqrt(np.mean(z * z))
-    gm = unpack_mask(saved.cpu().numpy()[rows], d)
-    diff = gm != (z > 0)
-    assert np.all(np.abs(z[diff]) <= band)
-
-    # backward, sampled dH rows: dH_i = G_i + dZ_i W_self^T + sum_{i->j, r} dZ_j / deg_r(j) W_r^T
     G = synth.upstream_grad(wl.model.seed, full.ns, d)
     dH, dWr, dWs, db = api.hg_layer_bwd(sub, Hd, wr, wsf, saved, to_dev(G))
-    srcs = np.unique(rng.choice(full.ns, 300, replace=False))
-    mo = np.isin(full.src_l, srcs)
-    es, er, ed = full.src_l[mo], full.rel_l[mo], full.dst_l[mo]
-    need = np.unique(np.concatenate([ed, srcs]))
-    zn = _z_rows(full, need, H, w)
-    pos = {v: i for i, v in enumerate(need)}
-    dz = G[need] * (zn > 0)
-    near = np.abs(zn) <= band
-    key_csr = full.dst_l * R + full.rel_l
-    deg = np.bincount(key_csr, minlength=full.ns * R)
-    typ = full.g.ntype[full.ref["l2g"][srcs]].astype(np.int64)
-    exp = G[srcs].astype(np.float64).copy()
-    ok = np.ones(srcs.shape[0], bool)
-    for k, i in enumerate(srcs):
-        p = pos[i]
-        exp[k] += dz[p] @ w.w_self[typ[k]].astype(np.float64).T
-        ok[k] &= not near[p].any()
-        sel = es == i
-        for j, r in zip(ed[sel], er[sel]):
-            q = pos[j]
-            exp[k] += dz[q] / deg[j * R + r] @ w.w_rel[r].astype(np.float64).T
-            ok[k] &= not near[q].any()
-    assert ok.sum() > 0.8 * ok.shape[0]
-    got = dH[torch.from_numpy(srcs).cuda()].cpu().numpy()
-    assert parity_err(got[ok], exp[ok]) <= TOL
-    _check_dw_columns(full, H, G, saved, dWr, dWs, db, deg)
+    rows, srcs = _sample_rows(full, np.random.default_rng(0), 3000, 16, 300)
+    _check_layer_rows(full, H, w, out, saved, dH, G, rows, srcs, TOL)
+    _check_dw_columns(full, H, w, G, saved, dWr, dWs, db, TOL)
     del Hd, out, saved, dH, dWr, dWs, db
 
 
 def test_fullsize_bf16_layer_sampled_rows(full):
     """The bfloat16 workload's layer (d = 256, bf16 rows, float32 weights) at
-    full size: forward on sampled and the heaviest destination rows, the
-    backward's dH on sampled source rows under the GPU's own mask, against
-    float64 on the same bf16-rounded inputs (bar 2e-2, as the bf16 tests);
-    and four whole columns of dW_self, dW_rel and db, reduced over every row
-    and edge (split-K over all chunks), where the inputs are exact bf16 values
-    and the bar is float32's 1e-4; on both full-size graphs."""
+    full size: forward on sampled and the heaviest destination rows and dH on
+    sampled source rows against oracle.layer on the same bf16-rounded inputs
+    (bar 2e-2, as the bf16 tests); four whole columns of dW_self, dW_rel and
+    db, reduced over every row and edge (split-K over all chunks), where the
+    inputs are exact bf16 values and the bar is float32's 1e-4; on both
+    full-size graphs."""
     sub, R, d = full.sub, full.R, 256
     H = synth.round_bf16(synth.features(4, full.g.n_nodes, d)[full.ref["l2g"]])
     w = synth.layer_weights(4, 0, R, 2, d, 0.1)
     Hd = to_dev(H).to(torch.bfloat16)
     wr, wsf, b = to_dev(w.w_rel), to_dev(w.w_self), to_dev(w.bias)
     out, saved = api.hg_layer_fwd(sub, Hd, wr, wsf, b)
-    rng = np.random.default_rng(3)
-    indeg = np.bincount(full.dst_l, minlength=full.ns)
-    rows = np.unique(np.concatenate([rng.choice(full.ns, 2000, replace=False), np.argsort(indeg)[-8:]]))
-    z = _z_rows(full, rows, H, w)
-    got = out[torch.from_numpy(rows).cuda()].float().cpu().numpy()
-    assert parity_err(got, np.maximum(z, 0) + H[rows]) <= 2e-2
     G = synth.round_bf16(synth.upstream_grad(4, full.ns, d))
     dH, dWr, dWs, db = api.hg_layer_bwd(sub, Hd, wr, wsf, saved, to_dev(G).to(torch.bfloat16))
-    srcs = np.unique(rng.choice(full.ns, 200, replace=False))
-    mo = np.isin(full.src_l, srcs)
-    es, er, ed = full.src_l[mo], full.rel_l[mo], full.dst_l[mo]
-    need = np.unique(np.concatenate([ed, srcs]))
-    mask = unpack_mask(saved[torch.from_numpy(need).cuda().long()].cpu().numpy(), d)
-    pos = {v: i for i, v in enumerate(need)}
-    dz = G[need].astype(np.float64) * mask
-    deg = np.bincount(full.dst_l * R + full.rel_l, minlength=full.ns * R)
-    typ = full.g.ntype[full.ref["l2g"][srcs]].astype(np.int64)
-    exp = G[srcs].astype(np.float64).copy()
-    for k, i in enumerate(srcs):
-        exp[k] += dz[pos[i]] @ w.w_self[typ[k]].astype(np.float64).T
-        sel = es == i
-        for j, r in zip(ed[sel], er[sel]):
-            exp[k] += dz[pos[j]] / deg[j * R + r] @ w.w_rel[r].astype(np.float64).T
-    got = dH[torch.from_numpy(srcs).cuda()].float().cpu().numpy()
-    assert parity_err(got, exp) <= 2e-2
-    _check_dw_columns(full, H, G, saved, dWr, dWs, db, deg)
+    rows, srcs = _sample_rows(full, np.random.default_rng(3), 2000, 8, 200)
+    _check_layer_rows(full, H, w, out, saved, dH, G, rows, srcs, 2e-2)
+    _check_dw_columns(full, H, w, G, saved, dWr, dWs, db, 2e-2)
     del Hd, out, saved, dH, dWr, dWs, db
 
 
@@ -355,15 +350,6 @@ def test_medium_full_layer_and_weight_gradients():
     for a, b, nm in zip(got, exp, ("dH", "dW_rel", "dW_self", "dbias")):
         err = parity_err(a.cpu().numpy(), b)
         assert err <= TOL, (nm, err)
-
-
-def _closure(full, dsts):
-    """The sub-graph of all in-edges of `dsts`, relabelled: (nodes, src, dst, rel)
-    with nodes the sorted global-local ids involved."""
-    m = np.isin(full.dst_l, dsts)
-    s, r, t = full.src_l[m], full.rel_l[m], full.dst_l[m]
-    nodes = np.unique(np.concatenate([s, t, dsts]))
-    return nodes, np.searchsorted(nodes, s), np.searchsorted(nodes, t), r
 
 
 def test_fullsize_attention_layer_sampled_rows(full):

@@ -2,6 +2,8 @@
 oracle (oracle/hgt.py, float64): element-wise relative error <= 1e-4 for
 float32 features, on seeded synthetic graphs of several tiles with ragged
 tails, d = 64 and 128, one to sixteen heads, and nodes without in-edges."""
+from dataclasses import replace
+
 import numpy as np
 import pytest
 
@@ -21,6 +23,8 @@ CFGS = {
     "tiny_d128_h1": (synth.scaled(synth.WORKLOADS["tiny"].graph, 0.3), 128, 1),
     "tiny_d64_h16": (synth.scaled(synth.WORKLOADS["tiny"].graph, 0.3), 64, 16),
     "skew_small_d64_h2": (synth.scaled(synth.WORKLOADS["skew"].graph, 0.002), 64, 2),
+    # more than 8 relations: the d = 64 backward forms dK and dV one relation at a time
+    "rel12_d64_h4": (replace(synth.scaled(synth.WORKLOADS["tiny"].graph, 0.3), n_rel=12, name="rel12"), 64, 4),
 }
 
 

@@ -2,7 +2,10 @@
 does not go through it: central finite differences of every gradient, the
 reduction to the (separately pinned) mean-aggregation layer when the
 attention is uniform, invariance to the attention parameters when every node
-has one in-edge, and invariance to the order of the edges."""
+has one in-edge, invariance to the order of the edges, and a two-edge closed
+form.  Planted mistakes (scale dropped, mu indexed the wrong way round,
+W_att transposed, softmax grouped by source, the softmax-gradient term
+dropped) are each caught by one of these pins."""
 import numpy as np
 import pytest
 
@@ -33,7 +36,8 @@ def rand_graph(rng, n, E, R, T):
     return (rng.integers(0, n, E), rng.integers(0, n, E), rng.integers(0, R, E), rng.integers(0, T, n))
 
 
-def test_gradients_match_finite_differences():
+def pin_finite_differences():
+    """Every gradient of the backward against central differences of the forward."""
     rng = np.random.default_rng(1)
     n, E, R, T, d, S = 9, 34, 2, 2, 8, 2
     src, dst, rel, nt = rand_graph(rng, n, E, R, T)
@@ -69,6 +73,10 @@ def test_gradients_match_finite_differences():
             P[idx] = old
             num[idx] = (fp - fm) / (2 * eps)
         np.testing.assert_allclose(getattr(g, name), num, rtol=1e-6, atol=1e-7, err_msg=name)
+
+
+def test_gradients_match_finite_differences():
+    pin_finite_differences()
 
 
 @pytest.mark.parametrize("zero", ["W_att", "mu"])
@@ -156,7 +164,7 @@ def test_nodes_without_in_edges_pass_the_residual_and_bias():
         np.testing.assert_allclose(Ho[j], np.maximum(p.b_agg[0], 0) + H[j], rtol=1e-15)
 
 
-def test_two_in_edges_closed_form():
+def pin_two_in_edges_closed_form():
     # node 0 (type 0) receives from node 1 (type 1, relation 0) and node 2
     # (type 0, relation 1); with identity projections the weights of the two
     # edges are per head a logistic function of the score difference, the
@@ -183,3 +191,43 @@ def test_two_in_edges_closed_form():
         np.testing.assert_allclose(alpha[:, s], [a1, 1 - a1], rtol=1e-13)
         np.testing.assert_allclose(ht[0, sl], a1 * H[1, sl] + (1 - a1) * H[2, sl], rtol=1e-12, atol=1e-14)
     np.testing.assert_allclose(Z[0], ht[0], rtol=1e-14)
+
+
+def test_two_in_edges_closed_form():
+    pin_two_in_edges_closed_form()
+
+
+def _mutant_tables(kind):
+    """_edge_tables with one plausible mistake planted."""
+    orig = hgt._edge_tables
+
+    def tables(src, dst, rel, ntype, p, K, Q, V, S):
+        if kind == "W_att transposed":
+            p = hgt.Params(*[np.swapaxes(getattr(p, k), -1, -2) if k == "W_att" else getattr(p, k)
+                             for k in hgt.PARAM_NAMES])
+        Ki, Vi, Qj, kt, msg, dot, c = orig(src, dst, rel, ntype, p, K, Q, V, S)
+        dk = K.shape[1] // S
+        if kind == "scale dropped":
+            c = c * np.sqrt(dk)
+        if kind == "mu transposed":
+            c = p.mu[ntype[dst], rel, ntype[src]] / np.sqrt(dk)
+        return Ki, Vi, Qj, kt, msg, dot, c
+    return tables
+
+
+@pytest.mark.parametrize("kind", ["scale dropped", "mu transposed", "W_att transposed", "softmax by source",
+                                  "softmax gradient term dropped"])
+def test_planted_mistakes_are_caught(monkeypatch, kind):
+    if kind == "softmax by source":
+        # the closed form's two edges come from two different sources
+        orig = hgt._softmax_by_dst
+        monkeypatch.setattr(hgt, "_softmax_by_dst", lambda n, dst, score: orig(n, np.array([1, 2]), score))
+        pin = pin_two_in_edges_closed_form
+    elif kind == "softmax gradient term dropped":
+        monkeypatch.setattr(hgt, "_softmax_backward", lambda n, dst, alpha, dalpha: alpha * dalpha)
+        pin = pin_finite_differences
+    else:
+        monkeypatch.setattr(hgt, "_edge_tables", _mutant_tables(kind))
+        pin = pin_two_in_edges_closed_form
+    with pytest.raises(AssertionError):
+        pin()
