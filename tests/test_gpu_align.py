@@ -21,7 +21,7 @@ def make(n_rows, m, d, seed):
     return H.astype(np.float32), ov, Href
 
 
-@pytest.mark.parametrize("d", [64, 128])
+@pytest.mark.parametrize("d", [64, 128, 256])
 @pytest.mark.parametrize("m", [500, 4099])
 @pytest.mark.parametrize("weighted,ddof,eps", [(False, 0, 1e-5), (True, 1, 1e-3), (False, 1, 0.0)])
 def test_align_parity(d, m, weighted, ddof, eps):
@@ -42,6 +42,28 @@ def test_align_parity(d, m, weighted, ddof, eps):
     assert parity_err(dH.cpu().numpy()[ov], expect[ov]) <= TOL
     rest = np.setdiff1d(np.arange(H.shape[0]), ov)
     assert np.array_equal(dH.cpu().numpy()[rest], G0[rest])
+    assert parity_err(dHref.cpu().numpy(), dY) <= TOL
+
+
+@pytest.mark.parametrize("d", [64, 128, 256])
+@pytest.mark.parametrize("m", [5, 33, 70000])
+def test_align_parity_sizes(d, m):
+    """Batches of one 32-row step or less (5, 33 rows) and one of many chunks
+    and reduction groups (70000 rows: every level of the Gram pass's
+    fixed-order reduction, padding blocks at d = 256).  (At M = ddof + 1 the
+    standardisation backward removes every direction but the one eps leaves:
+    dX is float32 rounding of a cancellation, so tiny batches start at 5.)"""
+    H, ov, Href = make(max(9000, 2 * m), m, d, seed=m + 3 * d)
+    w = np.random.default_rng(2).uniform(0.2, 3.0, m).astype(np.float32)
+    lam, scale, eps, ddof = 2e-4, 0.1, 1e-5, 1
+    (li, ld, L), dX, dY = align.loss_and_grad(H[ov], Href, w, lam, scale, eps, ddof)
+    dH = torch.zeros(H.shape, dtype=torch.float32, device="cuda")
+    dHref = torch.empty((m, d), dtype=torch.float32, device="cuda")
+    loss = api.hg_align_loss_fwd_bwd(to_dev(H), to_dev(ov), to_dev(Href), dH, w=to_dev(w), lambda_n=lam,
+                                     scale=scale, eps=eps, ddof=ddof, dH_ref=dHref).cpu().numpy()
+    for got, exp in zip(loss, (li, ld, L)):
+        assert abs(got - exp) <= TOL * abs(exp)
+    assert parity_err(dH.cpu().numpy()[ov], dX) <= TOL
     assert parity_err(dHref.cpu().numpy(), dY) <= TOL
 
 
