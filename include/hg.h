@@ -31,8 +31,9 @@
  *    the comment says "host".  Matrices are row-major and contiguous.
  *  - The caller owns every buffer.  The library never allocates or frees
  *    device memory, keeps no pointer past a call and holds no mutable global
- *    state apart from a per-device property cache and the optional timing
- *    log (hg_timing_*).  Calls on disjoint buffers are re-entrant.
+ *    state apart from a per-device property cache, the optional timing log
+ *    (hg_timing_*) and the static device scratch of
+ *    hg_align_loss_fwd_bwd_noalloc.  Calls on disjoint buffers are re-entrant.
  *  - `stream` is a hipStream_t passed as void* (NULL = the default stream).
  *    Everything except hg_build_csr is asynchronous on that stream.
  *  - Return value: HG_OK (0) or a negative HG_ERR_* code.  Arguments are
@@ -313,6 +314,25 @@ int hg_align_loss_fwd_bwd(int64_t M, int32_t d, int32_t dtype, int64_t n_rows,
                           const float* w, float lambda_n, float scale, float eps,
                           int32_t ddof, float* loss3, void* dH, const void* dH_base, void* dH_ref,
                           void* ws, size_t ws_bytes, void* stream);
+
+/* The same alignment without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  The scratch lives in a static device
+ * array of hg_align_noalloc_scratch_size() bytes (48 MiB) that every device
+ * the library runs on holds until the process ends; it covers every batch
+ * size at d <= 256 (the workspace of hg_align_loss_fwd_bwd is at most about
+ * 43 MiB), and a call that would need more returns HG_ERR_CAPACITY.  The
+ * call allocates nothing.  Arguments, results and errors are those of
+ * hg_align_loss_fwd_bwd, bit for bit.  All calls on one device share its
+ * scratch, which keeps the last call's contents (nothing in it has to start
+ * at zero): calls that overlap on one device (other streams, other host
+ * threads) race and must be serialised by the caller. */
+size_t hg_align_noalloc_scratch_size(void);
+int hg_align_loss_fwd_bwd_noalloc(int64_t M, int32_t d, int32_t dtype, int64_t n_rows,
+                                  const void* H, const int32_t* overlap, const void* H_ref,
+                                  const float* w, float lambda_n, float scale, float eps,
+                                  int32_t ddof, float* loss3, void* dH, const void* dH_base, void* dH_ref,
+                                  void* stream);
 
 /* ---- prediction head, masked BCE and Adam ("Prediction and Optimization":
  * the two-layer MLP E18, the BCE loss E19, the joint objective E20) ---------

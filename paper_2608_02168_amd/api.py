@@ -37,7 +37,8 @@ EXPORTS = [
     "hg_plan_size", "hg_build_csr_workspace_size", "hg_build_csr", "hg_node_keys_workspace_size", "hg_node_keys",
     "hg_layer_saved_size", "hg_layer_fwd_workspace_size", "hg_layer_bwd_workspace_size",
     "hg_layer_fwd", "hg_layer_bwd", "hg_hgt_saved_size", "hg_hgt_fwd_workspace_size",
-    "hg_hgt_bwd_workspace_size", "hg_hgt_fwd", "hg_hgt_bwd", "hg_align_workspace_size", "hg_align_loss_fwd_bwd",
+    "hg_hgt_bwd_workspace_size", "hg_hgt_fwd", "hg_hgt_bwd", "hg_align_workspace_size", "hg_align_loss_fwd_bwd", "hg_align_noalloc_scratch_size",
+    "hg_align_loss_fwd_bwd_noalloc",
     "hg_mlp_bce_workspace_size", "hg_mlp_bce_fwd_bwd", "hg_adam_step",
     "hg_temporal_fwd", "hg_temporal_bwd_workspace_size", "hg_temporal_bwd",
     "hg_mean_agg_fwd", "hg_mean_agg_bwd", "hg_home_gather",
@@ -133,6 +134,9 @@ def lib() -> C.CDLL:
         "hg_align_workspace_size": (sz, [i64, i32]),
         "hg_align_loss_fwd_bwd": (C.c_int, [i64, i32, i32, i64, vp, vp, vp, vp, f32, f32, f32,
                                             i32, vp, vp, vp, vp, vp, sz, vp]),
+        "hg_align_noalloc_scratch_size": (sz, []),
+        "hg_align_loss_fwd_bwd_noalloc": (C.c_int, [i64, i32, i32, i64, vp, vp, vp, vp, f32, f32, f32,
+                                                    i32, vp, vp, vp, vp, vp]),
         "hg_mlp_bce_workspace_size": (sz, [i64, i32, i32]),
         "hg_mlp_bce_fwd_bwd": (C.c_int, [i64, i32, i32] + [vp] * 7 + [i64] + [vp] * 8 + [sz, vp]),
         "hg_adam_step": (C.c_int, [i64, vp, vp, vp, vp, i64, f32, f32, f32, f32, f32, vp]),
@@ -587,6 +591,23 @@ def hg_align_loss_fwd_bwd(H, overlap, H_ref, dH, w=None, lambda_n=2e-4, scale=0.
                                    _ptr(w), lambda_n, scale, eps, ddof, _ptr(loss3), _ptr(dH), _ptr(dH_base),
                                    _ptr(dH_ref), _ptr(ws), ws.numel(), _stream(stream)),
            "hg_align_loss_fwd_bwd")
+    return loss3
+
+
+def hg_align_noalloc_scratch_size() -> int:
+    return int(lib().hg_align_noalloc_scratch_size())
+
+
+def hg_align_loss_fwd_bwd_noalloc(H, overlap, H_ref, dH, loss3, w=None, lambda_n=2e-4, scale=0.1, eps=1e-5,
+                                  ddof=0, dH_ref=None, stream=None, dH_base=None):
+    """hg_align_loss_fwd_bwd with the library's static scratch instead of a
+    workspace: allocates nothing (loss3 is the caller's device float32 [3])."""
+    code = HG_DTYPE_BF16 if H.dtype == torch.bfloat16 else HG_DTYPE_F32
+    _check(lib().hg_align_loss_fwd_bwd_noalloc(int(overlap.shape[0]), int(H.shape[1]), code, int(H.shape[0]),
+                                               _ptr(H), _ptr(overlap), _ptr(H_ref), _ptr(w), lambda_n, scale, eps,
+                                               ddof, _ptr(loss3), _ptr(dH), _ptr(dH_base), _ptr(dH_ref),
+                                               _stream(stream)),
+           "hg_align_loss_fwd_bwd_noalloc")
     return loss3
 
 

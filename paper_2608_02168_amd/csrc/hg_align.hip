@@ -29,6 +29,8 @@
 //
 // The counters of (d2) are zeroed by (d1), which runs first on the stream.
 // Every reduction has a fixed order: results are bitwise reproducible.
+#include <mutex>
+
 #include "hg_internal.h"
 #include "hg_mfma.h"
 
@@ -883,4 +885,55 @@ extern "C" int hg_align_loss_fwd_bwd(int64_t M, int32_t d, int32_t dtype, int64_
   if (d == 64) return align_impl<64, float>(M, h, overlap, r, w, lambda_n, scale, eps, ddof, loss3, dh, db, dr, ws, ws_bytes, s);
   if (d == 128) return align_impl<128, float>(M, h, overlap, r, w, lambda_n, scale, eps, ddof, loss3, dh, db, dr, ws, ws_bytes, s);
   return align_impl<256, float>(M, h, overlap, r, w, lambda_n, scale, eps, ddof, loss3, dh, db, dr, ws, ws_bytes, s);
+}
+
+// ---- no-allocation variant -------------------------------------------------------
+// The same passes with the workspace in a file-scope device array.  In host
+// code `scratch` names a host-side stand-in, not device memory: its device
+// address is taken with hipGetSymbolAddress once per device (each device
+// holds its own copy) and only that address is passed to the kernels.  The
+// counters of the Gram pass are zeroed by the statistics pass of the same
+// call, so nothing has to be cleared between calls.
+namespace hg {
+namespace {
+constexpr size_t kAlignScratchBytes = size_t(48) << 20;
+constexpr int kMaxDevices = 64;
+__device__ __align__(256) unsigned char scratch[kAlignScratchBytes];
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+int scratch_address(void** out) {
+  int dev = 0;
+  HG_HIP_TRY(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices) return fail(HG_ERR_UNSUPPORTED, "device %d beyond %d", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(HG_ERR_HIP, "hipGetSymbolAddress(scratch) on device %d failed: %s", dev, hipGetErrorString(e));
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return HG_OK;
+}
+}  // namespace
+}  // namespace hg
+
+extern "C" size_t hg_align_noalloc_scratch_size(void) { return kAlignScratchBytes; }
+
+extern "C" int hg_align_loss_fwd_bwd_noalloc(int64_t M, int32_t d, int32_t dtype, int64_t n_rows, const void* H,
+                                             const int32_t* overlap, const void* H_ref, const float* w,
+                                             float lambda_n, float scale, float eps, int32_t ddof, float* loss3,
+                                             void* dH, const void* dH_base, void* dH_ref, void* stream) {
+  if (d != 64 && d != 128 && d != 256)
+    return fail(HG_ERR_UNSUPPORTED, "alignment supports d in {64, 128, 256}, got %d", d);
+  const size_t need = hg_align_workspace_size(M, d);
+  if (need > kAlignScratchBytes)
+    return fail(HG_ERR_CAPACITY, "alignment needs %zu bytes of scratch, the static scratch holds %zu", need,
+                kAlignScratchBytes);
+  void* ws = nullptr;
+  HG_TRY(scratch_address(&ws));
+  return hg_align_loss_fwd_bwd(M, d, dtype, n_rows, H, overlap, H_ref, w, lambda_n, scale, eps, ddof, loss3, dH,
+                               dH_base, dH_ref, ws, kAlignScratchBytes, stream);
 }
