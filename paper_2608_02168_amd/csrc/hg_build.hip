@@ -11,7 +11,8 @@
 //      composites (key, splitmix64(seed ^ gid), gid) -- unique by gid, so the
 //      selected set is unique;
 //   5. local ids in (node type, gid) order by a stable bucket partition;
-//   6. induced-subgraph edge compaction in original edge order;
+//   6. induced-subgraph edge compaction in original edge order (local ids
+//      from a 32-byte-per-64-nodes rank table, per-tile counts, ballots);
 //   7. stable LSD radix sorts by (dst, r) and (src, r) give the CSR and CSC;
 //      row pointers from run-length counts; csc_scale = 1/deg_r(dst);
 //   8. the execution plan: per-relation active-source lists and the chunked
@@ -41,12 +42,12 @@ __device__ __forceinline__ int64_t cdiv_dev(int64_t a, int64_t b) { return (a + 
 // Device counters written by the build.
 enum : int { C_ERR = 0, C_NSUB, C_ESUB, C_MSEL, C_ITEMS, C_HEAVY, C_PARTS, C_CPRIME, C_BASE, C_COUNT };
 
-// A subgraph that can hold three quarters of the graph's nodes (|V_k| plus
-// the budget) is built the "dense" way: the base edge of every candidate is
-// found in the first edge pass and the induced edges from gathered local ids.
-// Otherwise the first pass only marks candidates, the base edges of the
-// selected nodes are found with the induced edges, and those come from a
-// membership bitmap.  Both give the same outputs.
+// A subgraph that holds three quarters of the graph's nodes or more (|V_k|
+// plus the budget) is built the "dense" way: the base edge of every candidate
+// is found in the first edge pass, whose LDS tables absorb the hub nodes'
+// many edges.  Otherwise the first pass only marks candidates and the base
+// edges of the few selected nodes are found with the induced edges.  Both
+// give the same outputs.
 __host__ __device__ inline bool dense_build(int64_t n_base, int64_t budget, int64_t n_nodes) {
   const int64_t b = budget < n_nodes ? budget : n_nodes;
   return 4 * (n_base + b) >= 3 * n_nodes;
@@ -120,19 +121,6 @@ __global__ void __launch_bounds__(256) k_sum_counts(const int32_t* __restrict__ 
     __syncthreads();
   }
   if (threadIdx.x == 0) out[0] = red[0];
-}
-
-__global__ void k_cand_bits(const int32_t* __restrict__ first, int32_t n_edges, int64_t n,
-                            uint32_t* __restrict__ bits) {
-  GRID_STRIDE(v0, cdiv_dev(n, 64) * 64) {
-    const bool in = v0 < n && first[v0] < n_edges;
-    const uint64_t m = __ballot(in);
-    if ((threadIdx.x & 63) == 0) {
-      const int64_t wd = v0 >> 5;
-      bits[wd] = (uint32_t)m;
-      if ((v0 + 32) < n) bits[wd + 1] = (uint32_t)(m >> 32);
-    }
-  }
 }
 
 // Membership of the subgraph's node set: base nodes and selected overlap nodes.
@@ -233,19 +221,23 @@ constexpr int kDegBits = 13, kDegSlots = 1 << kDegBits, kDegPerCu = 2;
 // by an edge gets first[v] < n_edges -- in a dense build the smallest index of
 // such an edge (block-aggregated atomic minimum), otherwise 0 (a plain store:
 // every writer stores the same value, and a node already marked is only
-// read).  All out-degrees when count_all (needed by the h-index).
+// read).  Out-degrees: of every node when count_all (the h-index needs them),
+// else of the nodes outside V_k when count_out (the out-degree key of the
+// candidates, all of which lie outside V_k), else none (keys given by the
+// caller).
 __global__ void __launch_bounds__(kAggBT) k_edges_pass(const int32_t* __restrict__ src, const int32_t* __restrict__ dst,
                                                    const uint8_t* __restrict__ rel,
                                                    const uint32_t* __restrict__ base_bits, int64_t n_nodes,
-                                                   int64_t n_edges, int32_t n_rel, int count_all, int64_t budget,
-                                                   int32_t* __restrict__ outdeg, int32_t* __restrict__ first,
-                                                   int32_t* __restrict__ cnt) {
+                                                   int64_t n_edges, int32_t n_rel, int count_all, int count_out,
+                                                   int64_t budget, int32_t* __restrict__ outdeg,
+                                                   int32_t* __restrict__ first, int32_t* __restrict__ cnt) {
   __shared__ uint32_t lk[3][kAggSlots];
   __shared__ int32_t lv[3][kAggSlots];
   LdsAgg<false> deg{lk[0], lv[0]};
   LdsAgg<true> fs{lk[1], lv[1]}, fd{lk[2], lv[2]};
   const bool exact = dense_build(cnt[C_BASE], budget, n_nodes);
-  if (count_all) deg.init();
+  const bool counting = count_all || count_out;
+  if (counting) deg.init();
   if (exact) {
     fs.init();
     fd.init();
@@ -258,8 +250,8 @@ __global__ void __launch_bounds__(kAggBT) k_edges_pass(const int32_t* __restrict
       atomicOr(&cnt[C_ERR], 1);
       continue;
     }
-    if (count_all) deg.put((uint32_t)s, 1, outdeg);
     const bool ps = bit_of(base_bits, s), pd = bit_of(base_bits, d);
+    if (count_all || (count_out && !ps)) deg.put((uint32_t)s, 1, outdeg);
     if (exact) {
       if (pd && !ps) fs.put((uint32_t)s, (int32_t)e, first);
       if (ps && !pd) fd.put((uint32_t)d, (int32_t)e, first);
@@ -269,28 +261,11 @@ __global__ void __launch_bounds__(kAggBT) k_edges_pass(const int32_t* __restrict
     }
   }
   __syncthreads();
-  if (count_all) deg.flush(outdeg);
+  if (counting) deg.flush(outdeg);
   if (exact) {
     fs.flush(first);
     fd.flush(first);
   }
-}
-
-// Out-degrees of the candidate nodes only (the out-degree key needs no other).
-__global__ void __launch_bounds__(kAggBT) k_cand_outdeg(const int32_t* __restrict__ src, int64_t n_edges,
-                                                    const uint32_t* __restrict__ cand_bits,
-                                                    int32_t* __restrict__ outdeg) {
-  __shared__ uint32_t lk[kDegSlots];
-  __shared__ int32_t lv[kDegSlots];
-  LdsAgg<false, kDegBits> deg{lk, lv};
-  deg.init();
-  __syncthreads();
-  GRID_STRIDE(e, n_edges) {
-    const int32_t s = src[e];
-    if (bit_of(cand_bits, s)) deg.put((uint32_t)s, 1, outdeg);
-  }
-  __syncthreads();
-  deg.flush(outdeg);
 }
 
 // Out-degrees of every node, with the range checks of the edge arrays.
@@ -481,7 +456,8 @@ __global__ void k_select_mark(const SelectState* st, const int32_t* __restrict__
 }
 
 // Node-set digits for the relabel; in a sparse build the selected nodes'
-// first[] goes back to n_edges for the base-edge minimum of the edge pass.
+// first[] goes back to n_edges for the base-edge minimum of the induced-edge
+// pass.
 __global__ void k_member_digit(const int32_t* __restrict__ part, int32_t k,
                                const uint8_t* __restrict__ sel, const uint8_t* __restrict__ ntype,
                                int64_t n, int64_t n_edges, int64_t budget, const int32_t* __restrict__ cnt,
@@ -524,46 +500,153 @@ __global__ void k_overlap_fill(const int32_t* __restrict__ l2g, const int32_t* _
   }
 }
 
-// Two ways to find the induced edges, with equal results.  Where most nodes
-// of the graph are in the subgraph, most edges stay and every edge needs its
-// endpoints' local ids: they are gathered in the first pass and the keep flag
-// follows from them.  Where the subgraph holds a smaller share of the nodes
-// (one block of a K-way partition), the first pass only tests membership in
-// a bitmap and the compaction gathers the local ids of the kept edges alone.
+// ---- induced edges from a rank table (node types 0 and 1) ------------------
+// Local ids order the node set by (type, gid).  For 64 consecutive gids an
+// entry holds the masks of their type-0 and type-1 members and the number of
+// type-0 and type-1 members before them (32 bytes per 64 nodes, 5 MB for 10M
+// nodes, where global2local takes 40 MB), so
+//   local(v) = pre0 + popc(mem0 below v)                          (type 0)
+//   local(v) = type_off[1] + pre1 + popc(mem1 below v)            (type 1)
+// and -1 outside the node set: one 32-byte lookup per endpoint.
+struct __align__(16) RankEnt {
+  uint64_t mem0, mem1;
+  uint32_t pre0, pre1, pad0, pad1;
+};
 
-// Local ids of both endpoints (one random gather each) and the keep flag.
-// With timestamps, an edge after the cut is dropped like an edge that leaves
-// the node set (its source id is written as -1).
-__global__ void k_edge_keep_ids(const int32_t* __restrict__ src, const int32_t* __restrict__ dst,
-                                const int32_t* __restrict__ g2l, const int32_t* __restrict__ ts, int32_t t_cut,
-                                int64_t n_edges, int32_t* __restrict__ keep, int32_t* __restrict__ sl,
-                                int32_t* __restrict__ dl) {
-  GRID_STRIDE(e, n_edges) {
-    int32_t s = g2l[src[e]];
-    const int32_t d = g2l[dst[e]];
-    if (ts && ts[e] > t_cut) s = -1;
-    sl[e] = s;
-    dl[e] = d;
-    keep[e] = (s >= 0 && d >= 0) ? 1 : 0;
+// Masks and member counts of every 64-node group (one wave per group).
+__global__ void __launch_bounds__(kBT) k_rank_bits(const int32_t* __restrict__ part, int32_t k,
+                                                   const uint8_t* __restrict__ sel, const uint8_t* __restrict__ ntype,
+                                                   int64_t n, RankEnt* __restrict__ rt, int32_t* __restrict__ c0,
+                                                   int32_t* __restrict__ c1) {
+  GRID_STRIDE(v, cdiv_dev(n, 64) * 64) {
+    const bool in = v < n && (part[v] == k || sel[v]);
+    const bool t1 = in && ntype[v] == 1;
+    const uint64_t m = __ballot(in), m1 = __ballot(t1);
+    if ((threadIdx.x & 63) == 0) {
+      const int64_t b = v >> 6;
+      rt[b].mem0 = m & ~m1;
+      rt[b].mem1 = m1;
+      c0[b] = (int32_t)__popcll(m & ~m1);
+      c1[b] = (int32_t)__popcll(m1);
+    }
   }
 }
 
-// Stable compaction of the kept edges from their local ids (pos = exclusive
-// scan of keep).
-__global__ void k_edge_compact_ids(const int32_t* __restrict__ sl, const int32_t* __restrict__ dl,
-                                   const uint8_t* __restrict__ rel, const int32_t* __restrict__ pos,
-                                   int64_t n_edges, int32_t n_rel, uint32_t* __restrict__ kcsr,
-                                   uint32_t* __restrict__ kcsc, int32_t* __restrict__ vsrc,
-                                   int32_t* __restrict__ vdst, int32_t* __restrict__ veid) {
-  GRID_STRIDE(e, n_edges) {
-    const int32_t s = sl[e], d = dl[e];
-    if (s >= 0 && d >= 0) {
-      const int32_t p = pos[e];
+__global__ void k_rank_pack(const int32_t* __restrict__ pre0, const int32_t* __restrict__ pre1, int64_t nb,
+                            RankEnt* __restrict__ rt) {
+  GRID_STRIDE(b, nb) {
+    rt[b].pre0 = (uint32_t)pre0[b];
+    rt[b].pre1 = (uint32_t)pre1[b];
+  }
+}
+
+__device__ __forceinline__ int32_t rank_local(const RankEnt* __restrict__ rt, int32_t off1, int32_t v) {
+  const uint4* p = reinterpret_cast<const uint4*>(rt + (v >> 6));
+  const uint4 a = p[0], b = p[1];
+  const uint64_t mem0 = (uint64_t)a.x | ((uint64_t)a.y << 32), mem1 = (uint64_t)a.z | ((uint64_t)a.w << 32);
+  const uint64_t bit = 1ull << (v & 63), below = bit - 1ull;
+  if (mem0 & bit) return (int32_t)b.x + __popcll(mem0 & below);
+  if (mem1 & bit) return off1 + (int32_t)b.y + __popcll(mem1 & below);
+  return -1;
+}
+
+// Edges in tiles of kETile = 16 rounds of kBT consecutive edges (round j of a
+// tile: edges base + kBT j .. + kBT - 1, one per thread, coalesced).
+constexpr int kERounds = 16;
+constexpr int kETile = kBT * kERounds;
+
+// Local ids of both endpoints of every edge (-1 outside the node set; an edge
+// after the snapshot cut gets source -1) and the number of kept edges per
+// tile.  In a sparse build also the base edge of every selected node: the
+// smallest index of an edge of the node set joining it to V_k (atomic
+// minimum; the selected nodes are few and of small key).
+__global__ void __launch_bounds__(kBT) k_edge_ids(const int32_t* __restrict__ src, const int32_t* __restrict__ dst,
+                                                  const RankEnt* __restrict__ rt, const int32_t* __restrict__ type_off,
+                                                  const uint32_t* __restrict__ base_bits, const int32_t* __restrict__ ts,
+                                                  int32_t t_cut, int64_t n_edges, int sparse, int32_t* __restrict__ sl,
+                                                  int32_t* __restrict__ dl, int32_t* __restrict__ tile_cnt,
+                                                  int32_t* __restrict__ first) {
+  __shared__ int32_t wsum[kBT / 64];
+  const int64_t base = (int64_t)blockIdx.x * kETile;
+  const int32_t off1 = type_off[1];
+  int32_t c = 0;
+#pragma unroll 4
+  for (int j = 0; j < kERounds; ++j) {
+    const int64_t e = base + (int64_t)j * kBT + threadIdx.x;
+    bool keep = false;
+    if (e < n_edges) {
+      const int32_t s = src[e], d = dst[e];
+      int32_t a = rank_local(rt, off1, s);
+      const int32_t b = rank_local(rt, off1, d);
+      if (sparse && a >= 0 && b >= 0) {
+        const bool ps = bit_of(base_bits, s), pd = bit_of(base_bits, d);
+        if (pd && !ps) atomicMin(&first[s], (int32_t)e);
+        if (ps && !pd) atomicMin(&first[d], (int32_t)e);
+      }
+      if (ts && ts[e] > t_cut) a = -1;
+      keep = a >= 0 && b >= 0;
+      sl[e] = a;
+      dl[e] = b;
+    }
+    c += __popcll(__ballot(keep));
+  }
+  if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = c;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int32_t t = 0;
+#pragma unroll
+    for (int q = 0; q < kBT / 64; ++q) t += wsum[q];
+    tile_cnt[blockIdx.x] = t;
+  }
+}
+
+// Stable compaction of the kept edges of a tile at tile_off[tile] (exclusive
+// scan of the tile counts): the rank of a kept edge is the number of kept
+// edges before it in (round, wave, lane) order, i.e. in edge order.
+__global__ void __launch_bounds__(kBT) k_edge_emit(const int32_t* __restrict__ sl, const int32_t* __restrict__ dl,
+                                                   const uint8_t* __restrict__ rel, int64_t n_edges, int32_t n_rel,
+                                                   const int32_t* __restrict__ tile_off, uint32_t* __restrict__ kcsr,
+                                                   uint32_t* __restrict__ kcsc, int32_t* __restrict__ vsrc,
+                                                   int32_t* __restrict__ vdst, int32_t* __restrict__ veid) {
+  constexpr int NW = kBT / 64;
+  __shared__ int32_t cnt[kERounds * NW];
+  const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+  const uint64_t lt = (l == 0) ? 0ull : (~0ull >> (64 - l));
+  const int64_t base = (int64_t)blockIdx.x * kETile;
+  int32_t a[kERounds], b[kERounds];
+  uint64_t bal[kERounds];
+#pragma unroll
+  for (int j = 0; j < kERounds; ++j) {
+    const int64_t e = base + (int64_t)j * kBT + threadIdx.x;
+    a[j] = b[j] = -1;
+    if (e < n_edges) {
+      a[j] = sl[e];
+      b[j] = dl[e];
+    }
+    bal[j] = __ballot(a[j] >= 0 && b[j] >= 0);
+    if (l == 0) cnt[j * NW + w] = (int32_t)__popcll(bal[j]);
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {  // exclusive prefix in (round, wave) order
+    int32_t run = 0;
+    for (int q = 0; q < kERounds * NW; ++q) {
+      const int32_t c = cnt[q];
+      cnt[q] = run;
+      run += c;
+    }
+  }
+  __syncthreads();
+  const int32_t t0 = tile_off[blockIdx.x];
+#pragma unroll
+  for (int j = 0; j < kERounds; ++j) {
+    if ((bal[j] >> l) & 1ull) {
+      const int64_t e = base + (int64_t)j * kBT + threadIdx.x;
+      const int32_t p = t0 + cnt[j * NW + w] + (int32_t)__popcll(bal[j] & lt);
       const uint32_t r = rel[e];
-      kcsr[p] = (uint32_t)d * (uint32_t)n_rel + r;
-      kcsc[p] = (uint32_t)s * (uint32_t)n_rel + r;
-      vsrc[p] = s;
-      vdst[p] = d;
+      kcsr[p] = (uint32_t)b[j] * (uint32_t)n_rel + r;
+      kcsc[p] = (uint32_t)a[j] * (uint32_t)n_rel + r;
+      vsrc[p] = a[j];
+      vdst[p] = b[j];
       veid[p] = (int32_t)e;
     }
   }
@@ -749,7 +832,9 @@ struct BuildWs {
   SelectState* st;
   int32_t *keep, *vsrc, *vdst, *veid, *alt1, *alt2, *alt3, *rowcnt, *q_items, *q_heavy, *q_parts,
       *q_src, *scratch, *bcnt;
-  uint32_t *kcsr, *kcsc, *kalt, *bbits, *cbits, *mbits;
+  uint32_t *kcsr, *kcsc, *kalt, *bbits, *mbits;
+  RankEnt* rt;
+  int32_t *rc0, *rc1, *tile_cnt;
   void layout(A& a, int64_t N, int64_t E, int64_t R, bool hindex) {
     const int64_t NQ = N * R + 1;
     cnt = a.template take<int32_t>(C_COUNT + 8);
@@ -765,8 +850,11 @@ struct BuildWs {
     hist = a.template take<int32_t>(hindex ? E + N : 0);
     sel = a.template take<uint8_t>(N);
     bbits = a.template take<uint32_t>(N / 32 + 2);
-    cbits = a.template take<uint32_t>(N / 32 + 2);
-    mbits = a.template take<uint32_t>(N / 32 + 2);
+    mbits = a.template take<uint32_t>(2 * (N / 64 + 1));
+    rt = a.template take<RankEnt>(N / 64 + 1);
+    rc0 = a.template take<int32_t>(N / 64 + 1);
+    rc1 = a.template take<int32_t>(N / 64 + 1);
+    tile_cnt = a.template take<int32_t>(E / kETile + 2);
     digit = a.template take<uint8_t>(NQ > N ? NQ : N);
     st = a.template take<SelectState>(1);
     keep = a.template take<int32_t>(E + 1);
@@ -975,9 +1063,9 @@ extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg
   HG_LAUNCH("build_base_count", k_sum_counts, dim3(1), dim3(256), 0, s, (const int32_t*)w.bcnt, (int)gB,
             w.cnt + C_BASE);
   if (E > 0)
-    HG_LAUNCH("build_edges_pass", k_edges_pass, dim3(agg_grid(E)), dim3(kAggBT), 0, s, g->src, g->dst, g->rel,
-              (const uint32_t*)w.bbits, N, E, (int32_t)R, (hindex && !o->node_key) ? 1 : 0, o->budget_M, w.outdeg,
-              w.first, w.cnt);
+    HG_LAUNCH("build_edges_pass", k_edges_pass, dim3(agg_grid(E, kDegPerCu)), dim3(kAggBT), 0, s, g->src, g->dst,
+              g->rel, (const uint32_t*)w.bbits, N, E, (int32_t)R, (hindex && !o->node_key) ? 1 : 0,
+              (!hindex && !o->node_key) ? 1 : 0, o->budget_M, w.outdeg, w.first, w.cnt);
   HG_LAUNCH("build_check_ntype", k_check_ntype, dim3(gN), dim3(kBT), 0, s, g->ntype, N, (int32_t)T, w.cnt);
   {
     int32_t herr = 0;
@@ -1000,11 +1088,7 @@ extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg
               (const int32_t*)w.outdeg, (const int32_t*)w.first, (const int32_t*)w.hoff,
               (const int32_t*)w.hist, N, (int32_t)E, w.key);
   } else if (!o->node_key) {
-    HG_LAUNCH("build_cand_bits", k_cand_bits, dim3(gB), dim3(kBT), 0, s, (const int32_t*)w.first, (int32_t)E, N,
-              w.cbits);
-    if (E > 0)
-      HG_LAUNCH("build_cand_outdeg", k_cand_outdeg, dim3(agg_grid(E, kDegPerCu)), dim3(kAggBT), 0, s, g->src, E,
-                (const uint32_t*)w.cbits, w.outdeg);
+    // the out-degrees of the nodes outside V_k (every candidate among them)
     HG_LAUNCH("build_copy_key", k_copy_key, dim3(gN), dim3(kBT), 0, s, (const int32_t*)w.outdeg, N, w.key);
   }
   // 3. filtered candidates, compacted in gid order
@@ -1036,21 +1120,31 @@ extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg
   HG_LAUNCH("build_global2local", k_global2local, dim3(gN), dim3(kBT), 0, s,
             (const int32_t*)out->local2global, (const int32_t*)out->type_off, (int32_t)T,
             out->global2local, w.cnt);
-  // 6. induced-subgraph edges in original order (and, in a sparse build, the
-  // base edges of the selected nodes)
+  // 6. induced-subgraph edges in original order, and the base edges of the
+  // selected nodes
   if (E > 0) {
     int32_t nb_host = 0;
     HG_HIP_TRY(hipMemcpyAsync(&nb_host, w.cnt + C_BASE, sizeof(int32_t), hipMemcpyDeviceToHost, s));
     HG_HIP_TRY(hipStreamSynchronize(s));
-    if (dense_build(nb_host, o->budget_M, N)) {
+    const bool dense = dense_build(nb_host, o->budget_M, N);
+    if (T <= 2) {
+      const int64_t nb = N / 64 + 1, ntiles = cdiv(E, kETile);
+      HG_LAUNCH("build_rank_bits", k_rank_bits, dim3(grid_for(nb * 64)), dim3(kBT), 0, s, g->part, g->k,
+                (const uint8_t*)w.sel, g->ntype, N, w.rt, w.rc0, w.rc1);
+      HG_TRY(scan_exclusive_i32(w.rc0, w.rc0, nb, nullptr, w.scratch, s));
+      HG_TRY(scan_exclusive_i32(w.rc1, w.rc1, nb, nullptr, w.scratch, s));
+      HG_LAUNCH("build_rank_pack", k_rank_pack, dim3(grid_for(nb)), dim3(kBT), 0, s, (const int32_t*)w.rc0,
+                (const int32_t*)w.rc1, nb, w.rt);
       // local ids land in the sort's ping-pong buffers (free until the sorts)
-      HG_LAUNCH("build_edge_keep", k_edge_keep_ids, dim3(gE), dim3(kBT), 0, s, g->src, g->dst,
-                (const int32_t*)out->global2local, g->edge_ts, g->t_cut, E, w.keep, w.alt1, w.alt2);
-      HG_TRY(scan_exclusive_i32(w.keep, w.keep, E, w.cnt + C_ESUB, w.scratch, s));
-      HG_LAUNCH("build_edge_compact", k_edge_compact_ids, dim3(gE), dim3(kBT), 0, s, (const int32_t*)w.alt1,
-                (const int32_t*)w.alt2, g->rel, (const int32_t*)w.keep, E, (int32_t)R, w.kcsr, w.kcsc, w.vsrc,
+      HG_LAUNCH("build_edge_ids", k_edge_ids, dim3((unsigned)ntiles), dim3(kBT), 0, s, g->src, g->dst,
+                (const RankEnt*)w.rt, (const int32_t*)out->type_off, (const uint32_t*)w.bbits, g->edge_ts,
+                g->t_cut, E, dense ? 0 : 1, w.alt1, w.alt2, w.tile_cnt, w.first);
+      HG_TRY(scan_exclusive_i32(w.tile_cnt, w.tile_cnt, ntiles, w.cnt + C_ESUB, w.scratch, s));
+      HG_LAUNCH("build_edge_compact", k_edge_emit, dim3((unsigned)ntiles), dim3(kBT), 0, s, (const int32_t*)w.alt1,
+                (const int32_t*)w.alt2, g->rel, E, (int32_t)R, (const int32_t*)w.tile_cnt, w.kcsr, w.kcsc, w.vsrc,
                 w.vdst, w.veid);
     } else {
+      // more than two node types: local ids from global2local, membership from a bitmap
       HG_LAUNCH("build_member_bits", k_member_bits, dim3(gB), dim3(kBT), 0, s, g->part, g->k,
                 (const uint8_t*)w.sel, N, w.mbits);
       HG_LAUNCH("build_edge_keep", k_edge_keep, dim3(gE), dim3(kBT), 0, s, g->src, g->dst,
