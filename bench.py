@@ -23,6 +23,11 @@ per second, forward + backward of every layer, build and alignment included),
 plus the roofline of the dominant kernel (algorithmic bytes per launch /
 average launch time from HIP events recorded around each launch on its own
 stream) and the oracle timed on the host cores on a bounded sample.
+
+Beside the value: the same steps timed again on the subgraphs already built
+(construction done once, before training; `ms_per_step_no_rebuild`), and for
+the build and alignment kernel families their time per step and algorithmic
+rate (`families`).
 """
 from __future__ import annotations
 
@@ -38,6 +43,14 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0
 FP32_MFMA_PEAK_TFLOPS = 157.3
 
+
+# kernel families by timing-log name: the subgraph build (keys, selection,
+# relabel, CSR/CSC, plan) and the alignment loss + gradient
+FAMILIES = {"build": ("build_", "keys_", "radix_", "scan_", "partition_", "fill"),
+            "align": ("align_",)}
+# algorithmic bytes of the build per input edge: edge compaction plus two
+# stable sorts (lower end of the 80-130 B range of the design estimate)
+BUILD_BYTES_PER_EDGE = 80
 
 SPARSE_KERNELS = {"mean": ("spmm_fwd", "spmm_bwd"),
                   "hgt": ("hgt_attn_fwd", "hgt_attn_bwd_dst", "hgt_attn_bwd_src")}
@@ -73,6 +86,32 @@ def algorithmic_cost(kind: str, info: dict):
         # feature type: dY feeds the float32 GEMMs)
         return E * (d * s + 8) + A * (d * 4 + 16), 2.0 * E * d
     raise KeyError(kind)
+
+
+def family_rates(kern: dict, steps: int, n_edges: int, builds: int, align_rows: int, d: int, s: int):
+    """Per-step time and algorithmic rate of the build and alignment families.
+    Build: BUILD_BYTES_PER_EDGE per input edge per build.  Alignment: about
+    6*M*d*s bytes (gather both views, write dX, read them again for the
+    gradient) and 6*M*d*d flop (two Grams and the gradient product)."""
+    out = {}
+    for fam, prefixes in FAMILIES.items():
+        ms = sum(v[1] for k, v in kern.items() if k.startswith(prefixes)) / steps
+        if fam == "build":
+            nbytes, flops = BUILD_BYTES_PER_EDGE * n_edges * builds, 0.0
+        else:
+            nbytes, flops = 6.0 * align_rows * d * s, 6.0 * align_rows * d * d
+        ent = {"ms_per_step": round(ms, 3), "algorithmic_bytes_per_step": int(nbytes)}
+        if ms > 0:
+            gbs = nbytes / (ms * 1e-3) / 1e9
+            ent.update({"achieved_GBs": round(gbs, 1), "hbm_frac": round(gbs / HBM_PEAK_GBS, 4)})
+            if flops:
+                tf = flops / (ms * 1e-3) / 1e12
+                ent.update({"algorithmic_flop_per_step": int(flops), "achieved_TFLOPs": round(tf, 2),
+                            "fp32_mfma_frac": round(tf / FP32_MFMA_PEAK_TFLOPS, 4)})
+            t_bound = max(nbytes / (HBM_PEAK_GBS * 1e9), flops / (FP32_MFMA_PEAK_TFLOPS * 1e12)) * 1e3
+            ent.update({"bound_ms": round(t_bound, 3), "frac_of_bound": round(t_bound / ms, 4)})
+        out[fam] = ent
+    return out
 
 
 def kernel_source_sha(path: str, kernel: str) -> str:
@@ -142,15 +181,15 @@ def main():
     if seq:
         inp = runner.make_seq_inputs(wl, g, device="cuda")
         subs = inp.subs
-        step = lambda: runner.run_seq_step(inp)
+        step = lambda rebuild=True: runner.run_seq_step(inp, rebuild=rebuild)
     elif kway:
         inp = runner.make_kway_inputs(wl, g, device="cuda")
         subs = inp.subs
-        step = lambda: runner.run_kway_step(inp)
+        step = lambda rebuild=True: runner.run_kway_step(inp, rebuild=rebuild)
     else:
         inp = runner.make_inputs(wl, g, device="cuda")
         subs = [inp.sub]
-        step = lambda: runner.run_step(inp)
+        step = lambda rebuild=True: runner.run_step(inp, rebuild=rebuild)
     sub = subs[-1]
     print(f"[bench] subgraph N_s={sub.n_sub} E_s={[s.e_sub for s in subs]} M_sel={sub.m_sel}", file=sys.stderr,
           flush=True)
@@ -169,6 +208,14 @@ def main():
     api.hg_timing_enable(False)
     kern = api.hg_timing_collect()
     ms = (t1 - t0) * 1e3 / args.steps
+    # the same steps on the subgraphs already built (construction done once,
+    # before training): reported beside the step, never as its value
+    torch.cuda.synchronize()
+    t2 = time.perf_counter()
+    for _ in range(args.steps):
+        step(rebuild=False)
+    torch.cuda.synchronize()
+    ms_nb = (time.perf_counter() - t2) * 1e3 / args.steps
     e_pass = sum(s.e_sub for s in subs)
     edges = L * e_pass
     value = edges / (ms * 1e-3) / 1e9
@@ -190,7 +237,8 @@ def main():
     traffic = counted_traffic(dom, args.config)
     roofline = {"kernel": dom, "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
-                "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE x2 + WRITE_SIZE, copy-calibrated)",
+                "traffic_unit": "L2-miss bytes per launch (rocprofv3 TCC_EA0 read requests x 128 B + write requests by size; "
+                                "includes Infinity Cache hits)",
                 "avg_launch_ms": round(avg_ms, 4), "algorithmic_bytes_per_launch": int(nbytes)}
     if not args.no_ceiling:
         groups = info["E"] / max(info["A"] if dom in ("spmm_bwd", "hgt_attn_bwd_src") else info["N"], 1)
@@ -198,6 +246,8 @@ def main():
     layer_ms = sum(v[1] for k, v in kern.items()
                    if k.startswith(("spmm", "gemm_fwd", "gemm_bwd", "relu_grad", "splitk", "hgt_"))) / args.steps
     breakdown = {k: round(v[1] / args.steps, 3) for k, v in sorted(kern.items(), key=lambda kv: -kv[1][1])}
+    align_rows = sum(x.m_sel for x in subs) if kway else subs[0].m_sel
+    families = family_rates(kern, args.steps, g.n_edges, len(subs), align_rows, info["d"], info["s"])
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -225,6 +275,9 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
         "layer_gteps": round(edges / (layer_ms * 1e-3) / 1e9, 4) if layer_ms > 0 else None,
+        "ms_per_step_no_rebuild": round(ms_nb, 3),
+        "gteps_no_rebuild": round(edges / (ms_nb * 1e-3) / 1e9, 4),
+        "families": families,
         "kernel_ms_per_step": breakdown,
     }
     print(json.dumps(out), flush=True)
@@ -264,7 +317,8 @@ def gather_ceiling(n_rows, n_idx, row_bytes, group, achieved):
     return {"pattern": f"uniform random {row_bytes}-byte rows, {n_idx} ids over {n_rows} rows, "
                        f"groups of {g}, one row written per group",
             "gather_only": res["gather_only"], "with_writes": res["with_writes"], "unit": "GB/s",
-            "frac": round(achieved / res["with_writes"], 4)}
+            "frac": round(achieved / res["gather_only"], 4),
+            "frac_with_writes": round(achieved / res["with_writes"], 4)}
 
 
 def _timed_runs(fn, min_s=10.0):
