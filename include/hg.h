@@ -174,6 +174,9 @@ typedef struct hg_subgraph {
   int64_t plan_items;     /* backward work items (internal) */
   int64_t plan_heavy;     /* split CSC rows (internal) */
   int64_t plan_partials;  /* partial rows of split CSC rows (internal) */
+  int64_t plan_fwd_heavy; /* destination rows split into chunks (internal) */
+  int64_t plan_fwd_parts; /* chunks of those rows (internal) */
+  int64_t plan_slot_rows; /* rows of the relation transforms in the layer workspaces (internal) */
 } hg_subgraph;
 
 /* Bytes of `plan` for a graph with these input sizes. */

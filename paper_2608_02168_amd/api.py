@@ -75,7 +75,8 @@ class SubgraphStruct(C.Structure):
                 ("e_sub", C.c_int64), ("m_sel", C.c_int64), ("n_rel", C.c_int32),
                 ("n_ntype", C.c_int32), ("type_off_host", C.c_int64 * (HG_MAX_NTYPE + 1)),
                 ("n_active", C.c_int64 * HG_MAX_REL), ("plan_items", C.c_int64),
-                ("plan_heavy", C.c_int64), ("plan_partials", C.c_int64)]
+                ("plan_heavy", C.c_int64), ("plan_partials", C.c_int64),
+                ("plan_fwd_heavy", C.c_int64), ("plan_fwd_parts", C.c_int64), ("plan_slot_rows", C.c_int64)]
 
 
 class LayerDesc(C.Structure):

@@ -40,7 +40,12 @@ __device__ __forceinline__ int64_t cdiv_dev(int64_t a, int64_t b) { return (a + 
        i += (int64_t)gridDim.x * blockDim.x)
 
 // Device counters written by the build.
-enum : int { C_ERR = 0, C_NSUB, C_ESUB, C_MSEL, C_ITEMS, C_HEAVY, C_PARTS, C_CPRIME, C_BASE, C_COUNT };
+enum : int { C_ERR = 0, C_NSUB, C_ESUB, C_MSEL, C_ITEMS, C_HEAVY, C_PARTS, C_CPRIME, C_BASE, C_FHEAVY, C_FPARTS,
+             C_ASLOTS, C_COUNT };
+
+// The row-indexed layout of the relation transforms is kept when nq rows cost
+// at most kRowLayoutMaxSpread times the a active ones.
+__host__ __device__ inline bool row_layout(int64_t nq, int64_t a) { return nq <= kRowLayoutMaxSpread * a; }
 
 // A subgraph that holds three quarters of the graph's nodes or more (|V_k|
 // plus the budget) is built the "dense" way: the base edge of every candidate
@@ -779,42 +784,132 @@ __global__ void k_csc_scale(const uint32_t* __restrict__ kcsc, const int32_t* __
   }
 }
 
-__global__ void k_active_digit(const int32_t* __restrict__ csc_ptr, int64_t nq, int32_t n_rel,
-                               uint8_t* __restrict__ digit, int32_t* __restrict__ srcid,
-                               int32_t* __restrict__ n_items, int32_t* __restrict__ n_heavy,
-                               int32_t* __restrict__ n_parts) {
-  GRID_STRIDE(q, nq) {
-    const int32_t len = csc_ptr[q + 1] - csc_ptr[q];
-    digit[q] = len > 0 ? (uint8_t)(q % n_rel) : (uint8_t)255;
-    srcid[q] = (int32_t)(q / n_rel);
-    const int32_t nch = (len + kChunk - 1) / kChunk;
-    n_items[q] = nch;
-    n_heavy[q] = nch > 1 ? 1 : 0;
-    n_parts[q] = nch > 1 ? nch : 0;
+// Per CSC row q: relation digit for the active-source partition, work-item
+// counts, and the slot table's active mask and count of each 64 rows (one
+// wave covers 64 consecutive rows: the grid stride is a multiple of 64).
+__global__ void __launch_bounds__(kBT) k_active_digit(const int32_t* __restrict__ csc_ptr, int64_t nq, int32_t n_rel,
+                                                      uint8_t* __restrict__ digit, int32_t* __restrict__ srcid,
+                                                      int32_t* __restrict__ n_items, int32_t* __restrict__ n_heavy,
+                                                      int32_t* __restrict__ n_parts, SlotEnt* __restrict__ tab,
+                                                      int32_t* __restrict__ tab_cnt) {
+  const int lane = threadIdx.x & 63;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q - lane < nq; q += stride) {
+    const bool live = q < nq;
+    const int32_t len = live ? csc_ptr[q + 1] - csc_ptr[q] : 0;
+    if (live) {
+      digit[q] = len > 0 ? (uint8_t)(q % n_rel) : (uint8_t)255;
+      srcid[q] = (int32_t)(q / n_rel);
+      const int32_t nch = (len + kChunk - 1) / kChunk;
+      n_items[q] = nch;
+      n_heavy[q] = nch > 1 ? 1 : 0;
+      n_parts[q] = nch > 1 ? nch : 0;
+    }
+    const uint64_t m = __ballot(len > 0);
+    if (lane == 0) {
+      tab[q >> 6].mask = m;
+      tab_cnt[q >> 6] = (int32_t)__popcll(m);
+    }
   }
 }
 
+// The count before each 64 rows; for the row-indexed layout the identity
+// (all rows marked, 64 b before block b), so that slot(q) = q.
+__global__ void k_slot_pack(const int32_t* __restrict__ pre, int64_t nb, int64_t nq,
+                            const int32_t* __restrict__ a_total, SlotEnt* __restrict__ tab) {
+  const bool by_row = row_layout(nq, *a_total);
+  GRID_STRIDE(b, nb) {
+    if (by_row) tab[b].mask = ~0ull;
+    tab[b].pre = by_row ? (int32_t)(64 * b) : pre[b];
+    tab[b].pad = 0;
+  }
+}
+
+// Work items of the CSC rows (first field: the row's slot) and the slot ->
+// row map.
 __global__ void k_plan_items(const int32_t* __restrict__ csc_ptr, int64_t nq,
                              const int32_t* __restrict__ item_off, const int32_t* __restrict__ heavy_off,
-                             const int32_t* __restrict__ part_off, int4* __restrict__ items,
-                             int4* __restrict__ heavy) {
+                             const int32_t* __restrict__ part_off, const SlotEnt* __restrict__ tab,
+                             const int32_t* __restrict__ a_total, int4* __restrict__ items, int4* __restrict__ heavy,
+                             int32_t* __restrict__ slot_q) {
+  const bool by_row = row_layout(nq, *a_total);
   GRID_STRIDE(q, nq) {
     const int32_t beg = csc_ptr[q], end = csc_ptr[q + 1];
     const int32_t len = end - beg;
     if (len <= 0) continue;
+    const int32_t sl = slot_of(tab, q);
+    if (!by_row) slot_q[sl] = (int32_t)q;
     const int32_t nch = (len + kChunk - 1) / kChunk;
     const int32_t io = item_off[q];
     if (nch == 1) {
-      items[io] = make_int4((int32_t)q, beg, end, -1);
+      items[io] = make_int4(sl, beg, end, -1);
     } else {
       const int32_t so = part_off[q];
       for (int32_t c = 0; c < nch; ++c) {
         const int32_t b = beg + c * kChunk;
         const int32_t e2 = min(end, b + kChunk);
-        items[io + c] = make_int4((int32_t)q, b, e2, so + c);
+        items[io + c] = make_int4(sl, b, e2, so + c);
       }
-      heavy[heavy_off[q]] = make_int4((int32_t)q, so, nch, 0);
+      heavy[heavy_off[q]] = make_int4(sl, so, nch, 0);
     }
+  }
+}
+
+// Destination rows longer than kFwdChunk entries: per node j a 0/1 flag
+// and its number of chunks (0 for the rows one wave walks).
+__global__ void k_fwd_counts(const int32_t* __restrict__ csr_ptr, int64_t ns, int32_t n_rel,
+                             int32_t* __restrict__ heavy_flag, int32_t* __restrict__ n_parts) {
+  GRID_STRIDE(j, ns) {
+    const int32_t len = csr_ptr[(j + 1) * n_rel] - csr_ptr[j * n_rel];
+    const int32_t nch = len > kFwdChunk ? (len + kFwdChunk - 1) / kFwdChunk : 0;
+    heavy_flag[j] = nch > 0 ? 1 : 0;
+    n_parts[j] = nch;
+  }
+}
+
+// The chunks of the long destination rows (each chunk is one partial slot)
+// and one entry per long row.
+__global__ void k_fwd_items(const int32_t* __restrict__ csr_ptr, int64_t ns, int32_t n_rel,
+                            const int32_t* __restrict__ heavy_off, const int32_t* __restrict__ part_off,
+                            int4* __restrict__ items, int4* __restrict__ heavy) {
+  GRID_STRIDE(j, ns) {
+    const int32_t beg = csr_ptr[j * n_rel], end = csr_ptr[(j + 1) * n_rel];
+    const int32_t len = end - beg;
+    if (len <= kFwdChunk) continue;
+    const int32_t nch = (len + kFwdChunk - 1) / kFwdChunk;
+    const int32_t so = part_off[j];
+    for (int32_t c = 0; c < nch; ++c) {
+      const int32_t b = beg + c * kFwdChunk;
+      items[so + c] = make_int4((int32_t)j, b, min(end, b + kFwdChunk), so + c);
+    }
+    heavy[heavy_off[j]] = make_int4((int32_t)j, so, nch, 0);
+  }
+}
+
+// Slot of each entry of the per-relation active-source lists.
+__global__ void k_act_slot(const int32_t* __restrict__ act, const int32_t* __restrict__ act_off, int32_t n_rel,
+                           int64_t cap, const SlotEnt* __restrict__ tab, int32_t* __restrict__ act_slot) {
+  const int64_t n = act_off[n_rel];
+  GRID_STRIDE(k, cap) {
+    if (k >= n) break;
+    int32_t lo = 0, hi = n_rel;  // act_off[lo] <= k < act_off[hi]
+    while (hi - lo > 1) {
+      const int32_t mid = (lo + hi) >> 1;
+      if (act_off[mid] <= k) lo = mid; else hi = mid;
+    }
+    act_slot[k] = slot_of(tab, (int64_t)act[k] * n_rel + lo);
+  }
+}
+
+// Slot of the (source, relation) row of each CSR entry; the relation is the
+// low part of the entry's sorted CSR key dst * R + r.
+__global__ void k_csr_slot(const int32_t* __restrict__ csr_col, const uint32_t* __restrict__ kcsr, int64_t n,
+                           int32_t n_rel, int64_t nq, const int32_t* __restrict__ a_total,
+                           const SlotEnt* __restrict__ tab, int32_t* __restrict__ csr_slot) {
+  if (row_layout(nq, *a_total)) return;  // the kernels index by q
+  GRID_STRIDE(p, n) {
+    const int64_t q = (int64_t)csr_col[p] * n_rel + (int64_t)(kcsr[p] % (uint32_t)n_rel);
+    csr_slot[p] = slot_of(tab, q);
   }
 }
 
@@ -879,18 +974,30 @@ struct BuildWs {
 };
 
 struct PlanLayout {
-  size_t s_off, soff_off, items_off, heavy_off, total;
-  int64_t cap_s, cap_items, cap_heavy;
+  size_t s_off, soff_off, aslot_off, slotq_off, cslot_off, tab_off, items_off, heavy_off, fitems_off, fheavy_off,
+      total;
+  int64_t cap_s, cap_items, cap_heavy, cap_tab, cap_fitems, cap_fheavy;
   PlanLayout(int64_t N, int64_t E, int64_t R) {
     const int64_t nq = N * R;
     cap_s = nq < E ? nq : E;
     cap_heavy = E / kChunk + 1;
     cap_items = cap_s + cap_heavy;
+    cap_tab = nq / 64 + 1;
+    // a row of L > kFwdChunk entries has ceil(L / kFwdChunk) < 2 L / kFwdChunk chunks
+    cap_fheavy = E / kFwdChunk + 1;
+    cap_fitems = 2 * (E / kFwdChunk) + 2;
+    const size_t ns = (size_t)(cap_s > 0 ? cap_s : 1);
     size_t o = 0;
-    s_off = o; o = align_up(o + sizeof(int32_t) * (size_t)(cap_s > 0 ? cap_s : 1));
+    s_off = o; o = align_up(o + sizeof(int32_t) * ns);
     soff_off = o; o = align_up(o + sizeof(int32_t) * (size_t)(R + 1));
+    aslot_off = o; o = align_up(o + sizeof(int32_t) * ns);
+    slotq_off = o; o = align_up(o + sizeof(int32_t) * ns);
+    cslot_off = o; o = align_up(o + sizeof(int32_t) * (size_t)(E > 0 ? E : 1));
+    tab_off = o; o = align_up(o + sizeof(SlotEnt) * (size_t)cap_tab);
     items_off = o; o = align_up(o + sizeof(int4) * (size_t)cap_items);
     heavy_off = o; o = align_up(o + sizeof(int4) * (size_t)cap_heavy);
+    fitems_off = o; o = align_up(o + sizeof(int4) * (size_t)cap_fitems);
+    fheavy_off = o; o = align_up(o + sizeof(int4) * (size_t)cap_fheavy);
     total = o;
   }
 };
@@ -902,8 +1009,15 @@ PlanView plan_view(const hg_subgraph* s) {
   const char* b = static_cast<const char*>(s->plan);
   PlanView v;
   v.active = reinterpret_cast<const int32_t*>(b + pl.s_off);
+  v.act_slot = reinterpret_cast<const int32_t*>(b + pl.aslot_off);
+  const bool by_row = s->plan_slot_rows == s->n_sub * (int64_t)s->n_rel;
+  v.slot_q = by_row ? nullptr : reinterpret_cast<const int32_t*>(b + pl.slotq_off);
+  v.csr_slot = by_row ? nullptr : reinterpret_cast<const int32_t*>(b + pl.cslot_off);
+  v.slot_tab = by_row ? nullptr : reinterpret_cast<const SlotEnt*>(b + pl.tab_off);
   v.items = reinterpret_cast<const int4*>(b + pl.items_off);
   v.heavy = reinterpret_cast<const int4*>(b + pl.heavy_off);
+  v.fwd_items = reinterpret_cast<const int4*>(b + pl.fitems_off);
+  v.fwd_heavy = reinterpret_cast<const int4*>(b + pl.fheavy_off);
   return v;
 }
 
@@ -1177,6 +1291,7 @@ extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg
   const int64_t NQ = NS * R;
   // 7. CSR: stable sort by dst*R + r; CSC: stable sort by src*R + r
   const int bits = bits_for(NQ);
+  uint32_t* csr_keys = w.kcsr;  // the CSR's sorted keys, kept for the slots of its entries
   {
     uint32_t* ko;
     int32_t *v1o, *v2o;
@@ -1184,6 +1299,7 @@ extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg
     HG_TRY(radix_sort_pairs(w.kcsr, w.kalt, w.vsrc, w.alt1, want_eid ? w.veid : nullptr,
                             want_eid ? w.alt2 : nullptr, ES, bits, w.scratch, s, &ko, &v1o, &v2o, out->csr_col,
                             want_eid ? out->csr_eid : nullptr));
+    csr_keys = ko;
     if (ES > 0 && v1o != out->csr_col) {  // no pass ran (a single key value)
       HG_HIP_TRY(hipMemcpyAsync(out->csr_col, v1o, sizeof(int32_t) * ES, hipMemcpyDeviceToDevice, s));
       if (want_eid)
@@ -1202,8 +1318,9 @@ extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg
   {
     uint32_t* ko;
     int32_t *v1o, *v2o;
-    HG_TRY(radix_sort_pairs(w.kcsc, w.kalt, w.vdst, w.alt3, nullptr, nullptr, ES, bits, w.scratch, s,
-                            &ko, &v1o, &v2o, out->csc_row, nullptr));
+    // the CSR keys stay where the CSR sort left them
+    HG_TRY(radix_sort_pairs(w.kcsc, csr_keys == w.kalt ? w.kcsr : w.kalt, w.vdst, w.alt3, nullptr, nullptr, ES,
+                            bits, w.scratch, s, &ko, &v1o, &v2o, out->csc_row, nullptr));
     if (ES > 0 && v1o != out->csc_row)
       HG_HIP_TRY(hipMemcpyAsync(out->csc_row, v1o, sizeof(int32_t) * ES, hipMemcpyDeviceToDevice, s));
     HG_TRY(fill_i32(w.rowcnt, 0, NQ + 1, s));
@@ -1223,20 +1340,48 @@ extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg
   int32_t* act_off = reinterpret_cast<int32_t*>(pb + pl.soff_off);
   int4* items = reinterpret_cast<int4*>(pb + pl.items_off);
   int4* heavy = reinterpret_cast<int4*>(pb + pl.heavy_off);
+  int32_t* act_slot = reinterpret_cast<int32_t*>(pb + pl.aslot_off);
+  int32_t* slot_q = reinterpret_cast<int32_t*>(pb + pl.slotq_off);
+  int32_t* csr_slot = reinterpret_cast<int32_t*>(pb + pl.cslot_off);
+  SlotEnt* tab = reinterpret_cast<SlotEnt*>(pb + pl.tab_off);
   if (NQ > 0) {
+    const int64_t nb = NQ / 64 + 1;  // w.rowcnt (NQ + 1 entries) is free: it holds the slot counts
+    HG_TRY(fill_i32(w.rowcnt, 0, nb, s));
     HG_LAUNCH("build_active_digit", k_active_digit, dim3(grid_for(NQ)), dim3(kBT), 0, s,
               (const int32_t*)out->csc_ptr, NQ, (int32_t)R, w.digit, w.q_src, w.q_items, w.q_heavy,
-              w.q_parts);
+              w.q_parts, tab, w.rowcnt);
+    HG_TRY(scan_exclusive_i32(w.rowcnt, w.rowcnt, nb, w.cnt + C_ASLOTS, w.scratch, s));
+    HG_LAUNCH("build_slot_pack", k_slot_pack, dim3(grid_for(nb)), dim3(kBT), 0, s, (const int32_t*)w.rowcnt, nb,
+              NQ, (const int32_t*)(w.cnt + C_ASLOTS), tab);
     HG_TRY(bucket_partition(w.digit, w.q_src, NQ, (int)R, act, act_off, w.scratch, s));
     HG_TRY(scan_exclusive_i32(w.q_items, w.q_items, NQ, w.cnt + C_ITEMS, w.scratch, s));
     HG_TRY(scan_exclusive_i32(w.q_heavy, w.q_heavy, NQ, w.cnt + C_HEAVY, w.scratch, s));
     HG_TRY(scan_exclusive_i32(w.q_parts, w.q_parts, NQ, w.cnt + C_PARTS, w.scratch, s));
     HG_LAUNCH("build_plan_items", k_plan_items, dim3(grid_for(NQ)), dim3(kBT), 0, s,
               (const int32_t*)out->csc_ptr, NQ, (const int32_t*)w.q_items, (const int32_t*)w.q_heavy,
-              (const int32_t*)w.q_parts, items, heavy);
+              (const int32_t*)w.q_parts, (const SlotEnt*)tab, (const int32_t*)(w.cnt + C_ASLOTS), items, heavy,
+              slot_q);
+    const int64_t cap_a = NQ < ES ? NQ : ES;
+    if (cap_a > 0)
+      HG_LAUNCH("build_act_slot", k_act_slot, dim3(grid_for(cap_a)), dim3(kBT), 0, s, (const int32_t*)act,
+                (const int32_t*)act_off, (int32_t)R, cap_a, (const SlotEnt*)tab, act_slot);
+    if (ES > 0)
+      HG_LAUNCH("build_csr_slot", k_csr_slot, dim3(grid_for(ES)), dim3(kBT), 0, s, (const int32_t*)out->csr_col,
+                (const uint32_t*)csr_keys, ES, (int32_t)R, NQ, (const int32_t*)(w.cnt + C_ASLOTS),
+                (const SlotEnt*)tab, csr_slot);
+    // long destination rows and their chunks (w.q_items, w.q_heavy are free again)
+    int4* fitems = reinterpret_cast<int4*>(pb + pl.fitems_off);
+    int4* fheavy = reinterpret_cast<int4*>(pb + pl.fheavy_off);
+    HG_LAUNCH("build_fwd_counts", k_fwd_counts, dim3(grid_for(NS)), dim3(kBT), 0, s, (const int32_t*)out->csr_ptr,
+              NS, (int32_t)R, w.q_heavy, w.q_items);
+    HG_TRY(scan_exclusive_i32(w.q_heavy, w.q_heavy, NS, w.cnt + C_FHEAVY, w.scratch, s));
+    HG_TRY(scan_exclusive_i32(w.q_items, w.q_items, NS, w.cnt + C_FPARTS, w.scratch, s));
+    HG_LAUNCH("build_fwd_items", k_fwd_items, dim3(grid_for(NS)), dim3(kBT), 0, s, (const int32_t*)out->csr_ptr, NS,
+              (int32_t)R, (const int32_t*)w.q_heavy, (const int32_t*)w.q_items, fitems, fheavy);
   } else {
     HG_TRY(fill_i32(act_off, 0, R + 1, s));
     HG_TRY(fill_i32(w.cnt + C_ITEMS, 0, 3, s));
+    HG_TRY(fill_i32(w.cnt + C_FHEAVY, 0, 3, s));
   }
   // final sync: host counts
   std::vector<int32_t> tof(T + 1), aof(R + 1);
@@ -1256,5 +1401,8 @@ extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg
   out->plan_items = hc[C_ITEMS];
   out->plan_heavy = hc[C_HEAVY];
   out->plan_partials = hc[C_PARTS];
+  out->plan_fwd_heavy = hc[C_FHEAVY];
+  out->plan_fwd_parts = hc[C_FPARTS];
+  out->plan_slot_rows = row_layout(NQ, hc[C_ASLOTS]) ? NQ : hc[C_ASLOTS];
   return HG_OK;
 }

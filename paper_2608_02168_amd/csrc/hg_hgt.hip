@@ -6,8 +6,8 @@
 //   1. K, Q, V: per-type projections with bias (pipelined fp32 MFMA GEMM);
 //   2. Kt = K W_att[r], Vt = V W_msg[r] for the active sources of each
 //      relation (the per-head dk x dk blocks expanded to one block-diagonal
-//      d x d matrix per relation), stored at row src * R + r like the mean
-//      layer's relation transforms;
+//      d x d matrix per relation), one row per active (source, relation)
+//      slot like the mean layer's relation transforms;
 //   3. k_hgt_attn_fwd: one wave per destination j streams its CSR row,
 //      gathers Kt and Vt of every in-edge, and keeps an online softmax per
 //      head (running max, running sum, running weighted sum), so the scores
@@ -51,12 +51,12 @@ int validate_hgt(const hg_subgraph* s, const hg_hgt_desc* L) {
 // of several snapshots at once keeps 2/7 of the bytes per layer.
 struct HgtSaved {
   float *K, *Q, *V;   // [n_sub, d]
-  float *Kt, *Vt;     // [n_sub * R, d], rows src * R + r of active (src, r); absent when lean
+  float *Kt, *Vt;     // [A, d], one row per active (source, relation) slot; absent when lean
   float* ht;          // [n_sub, d]
   float* lse;         // [n_sub, S]
   template <class A>
   void layout(A& a, const hg_subgraph* s, int d, int S, bool lean) {
-    const int64_t n = s->n_sub, nr = lean ? 0 : s->n_sub * (int64_t)s->n_rel;
+    const int64_t n = s->n_sub, nr = lean ? 0 : n_slots(s);
     K = a.template take<float>(n * d);
     Q = a.template take<float>(n * d);
     V = a.template take<float>(n * d);
@@ -69,14 +69,17 @@ struct HgtSaved {
 
 struct HgtFwdWs {
   float *Watt, *Wmsg;  // [R, d, d] block-diagonal expansions
-  float *Kt, *Vt;      // lean layers: [n_sub * R, d]
+  float *Kt, *Vt;      // lean layers: [A, d]
+  float *pacc, *pml;   // chunks of long destination rows: [parts, d], [parts, 2 S] (2 S <= d / 2)
   template <class A>
   void layout(A& a, const hg_subgraph* s, int d, bool lean) {
-    const int64_t nr = lean ? s->n_sub * (int64_t)s->n_rel : 0;
+    const int64_t nr = lean ? n_slots(s) : 0;
     Watt = a.template take<float>((int64_t)s->n_rel * d * d);
     Wmsg = a.template take<float>((int64_t)s->n_rel * d * d);
     Kt = a.template take<float>(nr * d);
     Vt = a.template take<float>(nr * d);
+    pacc = a.template take<float>(s->plan_fwd_parts * d);
+    pml = a.template take<float>(s->plan_fwd_parts * (d / 2));
   }
 };
 
@@ -98,92 +101,187 @@ __device__ __forceinline__ int type_of(int64_t v, int T, const int32_t* __restri
   return t;
 }
 
+// Online softmax over the CSR entries [beg, end) of destination row j
+// (entries [p0, pe) over all relations): per lane the running max m, sum ls
+// and weighted value sum acc of its slot and head, merged over the slots at
+// the end (every lane then holds its head's state of the whole range).
+template <int D, int S>
+__device__ __forceinline__ void attn_fwd_range(int64_t j, int tj, int32_t R, int32_t T,
+                                               const int32_t* __restrict__ type_off,
+                                               const int32_t* __restrict__ csr_ptr,
+                                               const int32_t* __restrict__ csr_col,
+                                               const int32_t* __restrict__ csr_slot, const float* __restrict__ Kt,
+                                               const float* __restrict__ Vt, const float* __restrict__ mu,
+                                               float inv_sqrt_dk, int32_t beg, int32_t end, f32x4 q, int l,
+                                               float& m, float& ls, f32x4& acc) {
+  constexpr int LPR = D / 4, EPW = 64 / LPR, DK = D / S, LPH = DK / 4, U = 2;
+  const int slot = l / LPR, c0 = (l % LPR) * 4;
+  const int64_t rb = j * R;
+  m = -INFINITY;
+  ls = 0.f;
+  acc = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int32_t base = beg; base < end; base += 64) {
+    const int32_t pos = base + l;
+    int32_t rowi = 0;
+    float cf = 0.f;
+    if (pos < end) {
+      const int32_t src = csr_col[pos];
+      int r = 0;
+      for (int t = 1; t < R; ++t) r += (csr_ptr[rb + t] <= pos) ? 1 : 0;
+      rowi = csr_slot ? csr_slot[pos] : src * R + r;
+      cf = mu[((int64_t)type_of(src, T, type_off) * R + r) * T + tj] * inv_sqrt_dk;
+    }
+    const int cnt = (end - base) < 64 ? (end - base) : 64;
+    for (int e = 0; e < cnt; e += EPW * U) {
+      f32x4 kv[U], vv[U];
+      float cc[U];
+      bool ok[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int my = e + u * EPW + slot;
+        const int32_t qi = __shfl(rowi, my & 63, 64);
+        cc[u] = __shfl(cf, my & 63, 64);
+        ok[u] = my < cnt;
+        if (ok[u]) {
+          kv[u] = *reinterpret_cast<const f32x4*>(Kt + (int64_t)qi * D + c0);
+          vv[u] = *reinterpret_cast<const f32x4*>(Vt + (int64_t)qi * D + c0);
+        } else {
+          kv[u] = vv[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        float dot = kv[u][0] * q[0] + kv[u][1] * q[1] + kv[u][2] * q[2] + kv[u][3] * q[3];
+#pragma unroll
+        for (int o = 1; o < LPH; o <<= 1) dot += __shfl_xor(dot, o, 64);
+        if (ok[u]) {
+          const float sc = dot * cc[u];
+          const float mn = fmaxf(m, sc);
+          const float a = __expf(m - mn), p = __expf(sc - mn);
+          ls = ls * a + p;
+          acc = acc * a + p * vv[u];
+          m = mn;
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int o = LPR; o < 64; o <<= 1) {
+    const float m2 = __shfl_xor(m, o, 64), l2 = __shfl_xor(ls, o, 64);
+    f32x4 a2;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) a2[k] = __shfl_xor(acc[k], o, 64);
+    const float mn = fmaxf(m, m2);
+    const float s1 = (m == -INFINITY) ? 0.f : __expf(m - mn);
+    const float s2 = (m2 == -INFINITY) ? 0.f : __expf(m2 - mn);
+    ls = ls * s1 + l2 * s2;
+    acc = acc * s1 + a2 * s2;
+    m = mn;
+  }
+}
+
 // One wave per destination row; the row's lanes form 64 / (D/4) slots that
 // take alternate in-edges, each slot with its own online-softmax state per
 // head (lanes of one head hold its dk columns); the slot states are merged at
-// the end.  U in-edges per slot are in flight (two row gathers each).
+// the end.  U in-edges per slot are in flight (two row gathers each).  Rows
+// of more than kFwdChunk entries are left to the plan's chunks
+// (k_hgt_attn_fwd_part, k_hgt_attn_fwd_merge).
 template <int D, int S>
 __global__ void __launch_bounds__(kAttnThreads) k_hgt_attn_fwd(
     int64_t n_sub, int32_t R, int32_t T, const int32_t* __restrict__ type_off, const int32_t* __restrict__ csr_ptr,
-    const int32_t* __restrict__ csr_col, const float* __restrict__ Q, const float* __restrict__ Kt,
-    const float* __restrict__ Vt, const float* __restrict__ mu, float inv_sqrt_dk, float* __restrict__ ht,
-    float* __restrict__ lse) {
-  constexpr int LPR = D / 4, EPW = 64 / LPR, DK = D / S, LPH = DK / 4, U = 2;
+    const int32_t* __restrict__ csr_col, const int32_t* __restrict__ csr_slot, const float* __restrict__ Q,
+    const float* __restrict__ Kt, const float* __restrict__ Vt, const float* __restrict__ mu, float inv_sqrt_dk,
+    float* __restrict__ ht, float* __restrict__ lse) {
+  constexpr int LPR = D / 4, DK = D / S, LPH = DK / 4;
   static_assert(LPH >= 1 && (LPH & (LPH - 1)) == 0, "head width must be a power of two >= 4");
   const int l = threadIdx.x & 63;
   const int slot = l / LPR, lr = l % LPR, c0 = lr * 4, head = lr / LPH;
   const int64_t wave0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
   const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
   for (int64_t j = wave0; j < n_sub; j += nwaves) {
-    const int tj = type_of(j, T, type_off);
-    const f32x4 q = *reinterpret_cast<const f32x4*>(Q + j * D + c0);
     const int64_t rb = j * R;
     const int32_t p0 = csr_ptr[rb], pe = csr_ptr[rb + R];
-    float m = -INFINITY, ls = 0.f;
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    for (int32_t base = p0; base < pe; base += 64) {
-      const int32_t pos = base + l;
-      int32_t rowi = 0;
-      float cf = 0.f;
-      if (pos < pe) {
-        const int32_t src = csr_col[pos];
-        int r = 0;
-        for (int t = 1; t < R; ++t) r += (csr_ptr[rb + t] <= pos) ? 1 : 0;
-        rowi = src * R + r;
-        cf = mu[((int64_t)type_of(src, T, type_off) * R + r) * T + tj] * inv_sqrt_dk;
-      }
-      const int cnt = (pe - base) < 64 ? (pe - base) : 64;
-      for (int e = 0; e < cnt; e += EPW * U) {
-        f32x4 kv[U], vv[U];
-        float cc[U];
-        bool ok[U];
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-          const int my = e + u * EPW + slot;
-          const int32_t qi = __shfl(rowi, my & 63, 64);
-          cc[u] = __shfl(cf, my & 63, 64);
-          ok[u] = my < cnt;
-          if (ok[u]) {
-            kv[u] = *reinterpret_cast<const f32x4*>(Kt + (int64_t)qi * D + c0);
-            vv[u] = *reinterpret_cast<const f32x4*>(Vt + (int64_t)qi * D + c0);
-          } else {
-            kv[u] = vv[u] = f32x4{0.f, 0.f, 0.f, 0.f};
-          }
-        }
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-          float dot = kv[u][0] * q[0] + kv[u][1] * q[1] + kv[u][2] * q[2] + kv[u][3] * q[3];
-#pragma unroll
-          for (int o = 1; o < LPH; o <<= 1) dot += __shfl_xor(dot, o, 64);
-          if (ok[u]) {
-            const float sc = dot * cc[u];
-            const float mn = fmaxf(m, sc);
-            const float a = __expf(m - mn), p = __expf(sc - mn);
-            ls = ls * a + p;
-            acc = acc * a + p * vv[u];
-            m = mn;
-          }
-        }
-      }
-    }
-#pragma unroll
-    for (int o = LPR; o < 64; o <<= 1) {
-      const float m2 = __shfl_xor(m, o, 64), l2 = __shfl_xor(ls, o, 64);
-      f32x4 a2;
-#pragma unroll
-      for (int k = 0; k < 4; ++k) a2[k] = __shfl_xor(acc[k], o, 64);
-      const float mn = fmaxf(m, m2);
-      const float s1 = (m == -INFINITY) ? 0.f : __expf(m - mn);
-      const float s2 = (m2 == -INFINITY) ? 0.f : __expf(m2 - mn);
-      ls = ls * s1 + l2 * s2;
-      acc = acc * s1 + a2 * s2;
-      m = mn;
-    }
+    if (pe - p0 > kFwdChunk) continue;  // a chunked row
+    const int tj = type_of(j, T, type_off);
+    const f32x4 q = *reinterpret_cast<const f32x4*>(Q + j * D + c0);
+    float m, ls;
+    f32x4 acc;
+    attn_fwd_range<D, S>(j, tj, R, T, type_off, csr_ptr, csr_col, csr_slot, Kt, Vt, mu, inv_sqrt_dk, p0, pe, q, l,
+                         m, ls, acc);
     if (slot == 0) {
       const float inv = ls > 0.f ? 1.0f / ls : 0.f;
       *reinterpret_cast<f32x4*>(ht + j * D + c0) = acc * inv;
       if (lr % LPH == 0) lse[j * S + head] = ls > 0.f ? m + logf(ls) : -INFINITY;
     }
+  }
+}
+
+// One wave per chunk (j, begin, end, partial slot) of a long destination row:
+// the chunk's softmax state, acc into pacc [part, D] and (m, ls) per head
+// into pml [part, 2 S].
+template <int D, int S>
+__global__ void __launch_bounds__(kAttnThreads) k_hgt_attn_fwd_part(
+    int64_t n_items, const int4* __restrict__ items, int32_t R, int32_t T, const int32_t* __restrict__ type_off,
+    const int32_t* __restrict__ csr_ptr, const int32_t* __restrict__ csr_col, const int32_t* __restrict__ csr_slot,
+    const float* __restrict__ Q, const float* __restrict__ Kt, const float* __restrict__ Vt,
+    const float* __restrict__ mu, float inv_sqrt_dk, float* __restrict__ pacc, float* __restrict__ pml) {
+  constexpr int LPR = D / 4, DK = D / S, LPH = DK / 4;
+  const int l = threadIdx.x & 63;
+  const int slot = l / LPR, lr = l % LPR, c0 = lr * 4, head = lr / LPH;
+  const int64_t wave0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+  const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
+  for (int64_t it = wave0; it < n_items; it += nwaves) {
+    const int4 item = items[it];
+    const int64_t j = item.x;
+    const int tj = type_of(j, T, type_off);
+    const f32x4 q = *reinterpret_cast<const f32x4*>(Q + j * D + c0);
+    float m, ls;
+    f32x4 acc;
+    attn_fwd_range<D, S>(j, tj, R, T, type_off, csr_ptr, csr_col, csr_slot, Kt, Vt, mu, inv_sqrt_dk, item.y,
+                         item.z, q, l, m, ls, acc);
+    if (slot == 0) {
+      *reinterpret_cast<f32x4*>(pacc + (int64_t)item.w * D + c0) = acc;
+      if (lr % LPH == 0) {
+        pml[(int64_t)item.w * 2 * S + head] = m;
+        pml[(int64_t)item.w * 2 * S + S + head] = ls;
+      }
+    }
+  }
+}
+
+// One wave per long row (j, first partial, count): the chunks' softmax states
+// combined in chunk order, then h~_j and the log-sum-exps.  Every chunk holds
+// at least one entry, so every m is finite.
+template <int D, int S>
+__global__ void __launch_bounds__(kAttnThreads) k_hgt_attn_fwd_merge(int64_t n_heavy, const int4* __restrict__ heavy,
+                                                                     const float* __restrict__ pacc,
+                                                                     const float* __restrict__ pml,
+                                                                     float* __restrict__ ht, float* __restrict__ lse) {
+  constexpr int LPR = D / 4, DK = D / S, LPH = DK / 4;
+  const int l = threadIdx.x & 63;
+  const int slot = l / LPR, lr = l % LPR, c0 = lr * 4, head = lr / LPH;
+  const int64_t wave0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+  const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
+  for (int64_t h = wave0; h < n_heavy; h += nwaves) {
+    const int4 hv = heavy[h];
+    if (slot != 0) continue;
+    float m = -INFINITY, ls = 0.f;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int32_t c = 0; c < hv.z; ++c) {
+      const int64_t pi = hv.y + c;
+      const float m2 = pml[pi * 2 * S + head], l2 = pml[pi * 2 * S + S + head];
+      const f32x4 a2 = *reinterpret_cast<const f32x4*>(pacc + pi * D + c0);
+      const float mn = fmaxf(m, m2);
+      const float s1 = (m == -INFINITY) ? 0.f : __expf(m - mn);
+      const float s2 = __expf(m2 - mn);
+      ls = ls * s1 + l2 * s2;
+      acc = acc * s1 + a2 * s2;
+      m = mn;
+    }
+    const int64_t j = hv.x;
+    const float inv = ls > 0.f ? 1.0f / ls : 0.f;
+    *reinterpret_cast<f32x4*>(ht + j * D + c0) = acc * inv;
+    if (lr % LPH == 0) lse[j * S + head] = ls > 0.f ? m + logf(ls) : -INFINITY;
   }
 }
 
@@ -228,7 +326,8 @@ inline unsigned attn_grid(int64_t rows) {
 }
 
 // Kt = K W_att[r] and Vt = V W_msg[r] for the active sources of each
-// relation, at rows src * R + r (Watt, Wmsg: the block-diagonal expansions).
+// relation, at the rows of their slots (Watt, Wmsg: the block-diagonal
+// expansions).
 template <int D>
 int rel_transforms(const hg_subgraph* s, const PlanView& pv, const float* Watt, const float* Wmsg, const float* K,
                    const float* V, float* Kt, float* Vt, hipStream_t st) {
@@ -239,10 +338,10 @@ int rel_transforms(const hg_subgraph* s, const PlanView& pv, const float* Watt, 
     const float* wa = Watt + (int64_t)r * D * D;
     const float* wm = Wmsg + (int64_t)r * D * D;
     HG_TRY((launch_gemm_rows_pp<D, false>("hgt_rel", n, wa, LoadRows<D, float>{K, rows_list(pv.active + off)},
-                                          StoreRows<D, float>{Kt, rows_list(pv.active + off, R, r), nullptr, nullptr},
+                                          StoreRows<D, float>{Kt, rows_list(pv.act_slot + off), nullptr, nullptr},
                                           st)));
     HG_TRY((launch_gemm_rows_pp<D, false>("hgt_rel", n, wm, LoadRows<D, float>{V, rows_list(pv.active + off)},
-                                          StoreRows<D, float>{Vt, rows_list(pv.active + off, R, r), nullptr, nullptr},
+                                          StoreRows<D, float>{Vt, rows_list(pv.act_slot + off), nullptr, nullptr},
                                           st)));
     off += n;
   }
@@ -293,9 +392,22 @@ int hgt_fwd_impl(const hg_subgraph* s, const hg_hgt_desc* L, const float* Hin, c
   const float inv_sqrt_dk = 1.0f / std::sqrt((float)(D / S));
   if (s->n_sub > 0) {
 #define HG_ATTN_FWD(S_)                                                                                         \
-  HG_LAUNCH("hgt_attn_fwd", (k_hgt_attn_fwd<D, S_>), dim3(attn_grid(s->n_sub)), dim3(kAttnThreads), 0, st,     \
-            s->n_sub, R, T, (const int32_t*)s->type_off, (const int32_t*)s->csr_ptr, (const int32_t*)s->csr_col, \
-            (const float*)sv.Q, (const float*)Kt, (const float*)Vt, W->mu, inv_sqrt_dk, sv.ht, sv.lse)
+  do {                                                                                                          \
+    HG_LAUNCH("hgt_attn_fwd", (k_hgt_attn_fwd<D, S_>), dim3(attn_grid(s->n_sub)), dim3(kAttnThreads), 0, st,   \
+              s->n_sub, R, T, (const int32_t*)s->type_off, (const int32_t*)s->csr_ptr,                          \
+              (const int32_t*)s->csr_col, pv.csr_slot, (const float*)sv.Q, (const float*)Kt, (const float*)Vt,  \
+              W->mu, inv_sqrt_dk, sv.ht, sv.lse);                                                               \
+    if (s->plan_fwd_heavy > 0) {                                                                                \
+      HG_LAUNCH("hgt_attn_fwd_part", (k_hgt_attn_fwd_part<D, S_>), dim3(attn_grid(s->plan_fwd_parts)),          \
+                dim3(kAttnThreads), 0, st, (int64_t)s->plan_fwd_parts, pv.fwd_items, R, T,                      \
+                (const int32_t*)s->type_off, (const int32_t*)s->csr_ptr, (const int32_t*)s->csr_col,            \
+                pv.csr_slot, (const float*)sv.Q, (const float*)Kt, (const float*)Vt, W->mu, inv_sqrt_dk,        \
+                w.pacc, w.pml);                                                                                 \
+      HG_LAUNCH("hgt_attn_fwd_merge", (k_hgt_attn_fwd_merge<D, S_>), dim3(attn_grid(s->plan_fwd_heavy)),        \
+                dim3(kAttnThreads), 0, st, (int64_t)s->plan_fwd_heavy, pv.fwd_heavy, (const float*)w.pacc,      \
+                (const float*)w.pml, sv.ht, sv.lse);                                                            \
+    }                                                                                                           \
+  } while (0)
     switch (D / S) {
       case 4: HG_ATTN_FWD(D / 4); break;
       case 8: HG_ATTN_FWD(D / 8); break;
@@ -333,14 +445,15 @@ struct HgtBwdWs {
   float *dZ, *dht, *dQ, *dK, *dV;  // [n_sub, d]
   float* ld;                       // [n_sub, 2S]: per head the log-sum-exp, then per head D_j
   float* contrib;                  // [e_sub]: each CSR entry's term of the mu gradient (summed over heads)
-  float *dKt, *dVt;                // [n_sub * R, d]
+  float *dKt, *dVt;                // [A, d]
   double *pk, *pv;                 // [plan_partials, d]
   float* rowpart;                  // [n_sub * R * T]: dmu sums of each CSR row, by source type
   float* mupart;                   // [T * R * T, kMuChunks]
   float *Watt, *Wmsg;              // [R, d, d] block-diagonal expansions
   float *gatt, *gmsg;              // [R, d, d] full gradients before the block extraction
   float *splitk, *colsum;          // split-K partials
-  float *Kt, *Vt;                  // lean layers: Kt and Vt computed again, [n_sub * R, d]
+  float *Kt, *Vt;                  // lean layers: Kt and Vt computed again, [A, d]
+  float* pdq;                      // [fwd parts, d]: dQ shares of the chunks of long destination rows
   template <class A>
   void layout(A& a, const hg_subgraph* s, int d, int S, bool lean);
 };
@@ -356,8 +469,8 @@ void HgtBwdWs::layout(A& a, const hg_subgraph* s, int d, int S, bool lean) {
   dV = a.template take<float>(n * d);
   ld = a.template take<float>(n * 2 * S);
   contrib = a.template take<float>(s->e_sub);
-  dKt = a.template take<float>(n * R * d);
-  dVt = a.template take<float>(n * R * d);
+  dKt = a.template take<float>(n_slots(s) * d);
+  dVt = a.template take<float>(n_slots(s) * d);
   pk = a.template take<double>(s->plan_partials * d);
   pv = a.template take<double>(s->plan_partials * d);
   rowpart = a.template take<float>(n * R * T);
@@ -368,9 +481,10 @@ void HgtBwdWs::layout(A& a, const hg_subgraph* s, int d, int S, bool lean) {
   gmsg = a.template take<float>(R * d * d);
   splitk = a.template take<float>(splitk_max_chunks() * (int64_t)d * d);
   colsum = a.template take<float>(splitk_max_chunks() * (int64_t)d);
-  const int64_t nr = lean ? n * R : 0;
+  const int64_t nr = lean ? n_slots(s) : 0;
   Kt = a.template take<float>(nr * d);
   Vt = a.template take<float>(nr * d);
+  pdq = a.template take<float>(s->plan_fwd_parts * d);
 }
 
 template <int LPH>
@@ -386,26 +500,97 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
+// dq (lane's slot share) += the destination-side terms of the CSR entries
+// [beg, end) of row j, and each entry's mu-gradient term (summed over the
+// heads) into contrib.  q, g: Q_j and dh~_j columns of the lane; lj, dsum:
+// its head's log-sum-exp and D_j.
+template <int D, int S>
+__device__ __forceinline__ void attn_bwd_dst_range(int64_t j, int tj, int32_t R, int32_t T,
+                                                   const int32_t* __restrict__ type_off,
+                                                   const int32_t* __restrict__ csr_ptr,
+                                                   const int32_t* __restrict__ csr_col,
+                                                   const int32_t* __restrict__ csr_slot,
+                                                   const float* __restrict__ Kt, const float* __restrict__ Vt,
+                                                   const float* __restrict__ mu, float inv_sqrt_dk, int32_t beg,
+                                                   int32_t end, f32x4 q, f32x4 g, float lj, float dsum, int l,
+                                                   f32x4& dq, float* __restrict__ contrib) {
+  constexpr int LPR = D / 4, EPW = 64 / LPR, DK = D / S, LPH = DK / 4, U = 2;
+  const int slot = l / LPR, lr = l % LPR, c0 = lr * 4;
+  const bool head_lead = (lr % LPH) == 0;
+  const int64_t rb = j * R;
+  for (int32_t base = beg; base < end; base += 64) {
+    const int32_t pos = base + l;
+    int32_t rowi = 0;
+    float cf = 0.f;
+    if (pos < end) {
+      const int32_t src = csr_col[pos];
+      int r = 0;
+      for (int t = 1; t < R; ++t) r += (csr_ptr[rb + t] <= pos) ? 1 : 0;
+      rowi = csr_slot ? csr_slot[pos] : src * R + r;
+      cf = mu[((int64_t)type_of(src, T, type_off) * R + r) * T + tj] * inv_sqrt_dk;
+    }
+    const int cnt = (end - base) < 64 ? (end - base) : 64;
+    for (int e = 0; e < cnt; e += EPW * U) {
+      f32x4 kv[U], vv[U];
+      float cc[U];
+      bool ok[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int my = e + u * EPW + slot;
+        const int32_t qi = __shfl(rowi, my & 63, 64);
+        cc[u] = __shfl(cf, my & 63, 64);
+        ok[u] = my < cnt;
+        if (ok[u]) {
+          kv[u] = *reinterpret_cast<const f32x4*>(Kt + (int64_t)qi * D + c0);
+          vv[u] = *reinterpret_cast<const f32x4*>(Vt + (int64_t)qi * D + c0);
+        } else {
+          kv[u] = vv[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const float dot = head_sum<LPH>(kv[u][0] * q[0] + kv[u][1] * q[1] + kv[u][2] * q[2] + kv[u][3] * q[3]);
+        const float dal = head_sum<LPH>(vv[u][0] * g[0] + vv[u][1] * g[1] + vv[u][2] * g[2] + vv[u][3] * g[3]);
+        float cm = 0.f;
+        if (ok[u]) {
+          const float a = __expf(dot * cc[u] - lj);
+          const float ds = a * (dal - dsum);
+          dq += (ds * cc[u]) * kv[u];
+          cm = head_lead ? ds * dot * inv_sqrt_dk : 0.f;
+        }
+        // the mu term of this entry: sum over the heads of the slot
+#pragma unroll
+        for (int o = LPH; o < LPR; o <<= 1) cm += __shfl_xor(cm, o, 64);
+        if (ok[u] && lr == 0) contrib[base + e + u * EPW + slot] = cm;
+      }
+    }
+  }
+#pragma unroll
+  for (int o = LPR; o < 64; o <<= 1)
+#pragma unroll
+    for (int k = 0; k < 4; ++k) dq[k] += __shfl_xor(dq[k], o, 64);
+}
+
 // Destination pass: one wave per node j over all its in-edges (the relation
 // of each entry is found from the row pointers, as in the forward).  Writes
 // dQ_j, the packed per-head (log-sum-exp, D_j) record of j, and each CSR
-// entry's mu-gradient term (summed over the heads) for k_dmu_rows.
+// entry's mu-gradient term (summed over the heads) for k_dmu_rows.  The
+// in-edges of rows longer than kFwdChunk are left to the plan's chunks
+// (k_hgt_attn_bwd_dst_part, k_hgt_dq_merge); their record is written here.
 template <int D, int S>
 __global__ void __launch_bounds__(kAttnThreads) k_hgt_attn_bwd_dst(
     int64_t n_sub, int32_t R, int32_t T, const int32_t* __restrict__ type_off, const int32_t* __restrict__ csr_ptr,
-    const int32_t* __restrict__ csr_col, const float* __restrict__ Q, const float* __restrict__ Kt,
-    const float* __restrict__ Vt, const float* __restrict__ ht, const float* __restrict__ dht,
+    const int32_t* __restrict__ csr_col, const int32_t* __restrict__ csr_slot, const float* __restrict__ Q,
+    const float* __restrict__ Kt, const float* __restrict__ Vt, const float* __restrict__ ht, const float* __restrict__ dht,
     const float* __restrict__ lse, const float* __restrict__ mu, float inv_sqrt_dk, float* __restrict__ dQ,
     float* __restrict__ ld, float* __restrict__ contrib) {
-  constexpr int LPR = D / 4, EPW = 64 / LPR, DK = D / S, LPH = DK / 4, U = 2;
+  constexpr int LPR = D / 4, DK = D / S, LPH = DK / 4;
   const int l = threadIdx.x & 63;
   const int slot = l / LPR, lr = l % LPR, c0 = lr * 4, head = lr / LPH;
   const bool head_lead = (lr % LPH) == 0;
   const int64_t wave0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
   const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
   for (int64_t j = wave0; j < n_sub; j += nwaves) {
-    const int tj = type_of(j, T, type_off);
-    const f32x4 q = *reinterpret_cast<const f32x4*>(Q + j * D + c0);
     const f32x4 g = *reinterpret_cast<const f32x4*>(dht + j * D + c0);
     const f32x4 h = *reinterpret_cast<const f32x4*>(ht + j * D + c0);
     const float dsum = head_sum<LPH>(g[0] * h[0] + g[1] * h[1] + g[2] * h[2] + g[3] * h[3]);
@@ -414,70 +599,87 @@ __global__ void __launch_bounds__(kAttnThreads) k_hgt_attn_bwd_dst(
       ld[j * 2 * S + head] = lj;
       ld[j * 2 * S + S + head] = dsum;
     }
-    f32x4 dq = {0.f, 0.f, 0.f, 0.f};
     const int64_t rb = j * R;
     const int32_t p0 = csr_ptr[rb], pe = csr_ptr[rb + R];
-    for (int32_t base = p0; base < pe; base += 64) {
-      const int32_t pos = base + l;
-      int32_t rowi = 0;
-      float cf = 0.f;
-      if (pos < pe) {
-        const int32_t src = csr_col[pos];
-        int r = 0;
-        for (int t = 1; t < R; ++t) r += (csr_ptr[rb + t] <= pos) ? 1 : 0;
-        rowi = src * R + r;
-        cf = mu[((int64_t)type_of(src, T, type_off) * R + r) * T + tj] * inv_sqrt_dk;
-      }
-      const int cnt = (pe - base) < 64 ? (pe - base) : 64;
-      for (int e = 0; e < cnt; e += EPW * U) {
-        f32x4 kv[U], vv[U];
-        float cc[U];
-        bool ok[U];
+    if (pe - p0 > kFwdChunk) continue;  // a chunked row
+    const int tj = type_of(j, T, type_off);
+    const f32x4 q = *reinterpret_cast<const f32x4*>(Q + j * D + c0);
+    f32x4 dq = {0.f, 0.f, 0.f, 0.f};
+    attn_bwd_dst_range<D, S>(j, tj, R, T, type_off, csr_ptr, csr_col, csr_slot, Kt, Vt, mu, inv_sqrt_dk, p0, pe, q,
+                             g, lj, dsum, l, dq, contrib);
+    if (slot == 0) *reinterpret_cast<f32x4*>(dQ + j * D + c0) = dq;
+  }
+}
+
+// One wave per chunk (j, begin, end, partial slot) of a long destination row:
+// the chunk's share of dQ_j into pdq [part, D], and its entries' mu terms.
+template <int D, int S>
+__global__ void __launch_bounds__(kAttnThreads) k_hgt_attn_bwd_dst_part(
+    int64_t n_items, const int4* __restrict__ items, int32_t R, int32_t T, const int32_t* __restrict__ type_off,
+    const int32_t* __restrict__ csr_ptr, const int32_t* __restrict__ csr_col, const int32_t* __restrict__ csr_slot,
+    const float* __restrict__ Q, const float* __restrict__ Kt, const float* __restrict__ Vt,
+    const float* __restrict__ ht, const float* __restrict__ dht, const float* __restrict__ lse,
+    const float* __restrict__ mu, float inv_sqrt_dk, float* __restrict__ pdq, float* __restrict__ contrib) {
+  constexpr int LPR = D / 4, DK = D / S, LPH = DK / 4;
+  const int l = threadIdx.x & 63;
+  const int slot = l / LPR, lr = l % LPR, c0 = lr * 4, head = lr / LPH;
+  const int64_t wave0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+  const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
+  for (int64_t it = wave0; it < n_items; it += nwaves) {
+    const int4 item = items[it];
+    const int64_t j = item.x;
+    const f32x4 g = *reinterpret_cast<const f32x4*>(dht + j * D + c0);
+    const f32x4 h = *reinterpret_cast<const f32x4*>(ht + j * D + c0);
+    const float dsum = head_sum<LPH>(g[0] * h[0] + g[1] * h[1] + g[2] * h[2] + g[3] * h[3]);
+    const float lj = lse[j * S + head];
+    const int tj = type_of(j, T, type_off);
+    const f32x4 q = *reinterpret_cast<const f32x4*>(Q + j * D + c0);
+    f32x4 dq = {0.f, 0.f, 0.f, 0.f};
+    attn_bwd_dst_range<D, S>(j, tj, R, T, type_off, csr_ptr, csr_col, csr_slot, Kt, Vt, mu, inv_sqrt_dk, item.y,
+                             item.z, q, g, lj, dsum, l, dq, contrib);
+    if (slot == 0) *reinterpret_cast<f32x4*>(pdq + (int64_t)item.w * D + c0) = dq;
+  }
+}
+
+// One wave per long row (j, first partial, count): dQ_j = the chunks' shares
+// added in float64 (lane group s takes chunks s, s + G, ...; the groups then
+// add in a fixed tree).
+template <int D>
+__global__ void __launch_bounds__(kAttnThreads) k_hgt_dq_merge(int64_t n_heavy, const int4* __restrict__ heavy,
+                                                               const float* __restrict__ pdq, float* __restrict__ dQ) {
+  constexpr int LPR = D / 4, EPW = 64 / LPR;
+  const int l = threadIdx.x & 63;
+  const int slot = l / LPR, c0 = (l % LPR) * 4;
+  const int64_t wave0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+  const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
+  for (int64_t h = wave0; h < n_heavy; h += nwaves) {
+    const int4 hv = heavy[h];
+    f64x4 sd = {0.0, 0.0, 0.0, 0.0};
+    for (int32_t c = slot; c < hv.z; c += EPW) {
+      const f32x4 x = *reinterpret_cast<const f32x4*>(pdq + (int64_t)(hv.y + c) * D + c0);
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-          const int my = e + u * EPW + slot;
-          const int32_t qi = __shfl(rowi, my & 63, 64);
-          cc[u] = __shfl(cf, my & 63, 64);
-          ok[u] = my < cnt;
-          if (ok[u]) {
-            kv[u] = *reinterpret_cast<const f32x4*>(Kt + (int64_t)qi * D + c0);
-            vv[u] = *reinterpret_cast<const f32x4*>(Vt + (int64_t)qi * D + c0);
-          } else {
-            kv[u] = vv[u] = f32x4{0.f, 0.f, 0.f, 0.f};
-          }
-        }
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-          const float dot = head_sum<LPH>(kv[u][0] * q[0] + kv[u][1] * q[1] + kv[u][2] * q[2] + kv[u][3] * q[3]);
-          const float dal = head_sum<LPH>(vv[u][0] * g[0] + vv[u][1] * g[1] + vv[u][2] * g[2] + vv[u][3] * g[3]);
-          float cm = 0.f;
-          if (ok[u]) {
-            const float a = __expf(dot * cc[u] - lj);
-            const float ds = a * (dal - dsum);
-            dq += (ds * cc[u]) * kv[u];
-            cm = head_lead ? ds * dot * inv_sqrt_dk : 0.f;
-          }
-          // the mu term of this entry: sum over the heads of the slot
-#pragma unroll
-          for (int o = LPH; o < LPR; o <<= 1) cm += __shfl_xor(cm, o, 64);
-          if (ok[u] && lr == 0) contrib[base + e + u * EPW + slot] = cm;
-        }
-      }
+      for (int k = 0; k < 4; ++k) sd[k] += (double)x[k];
     }
 #pragma unroll
     for (int o = LPR; o < 64; o <<= 1)
 #pragma unroll
-      for (int k = 0; k < 4; ++k) dq[k] += __shfl_xor(dq[k], o, 64);
-    if (slot == 0) *reinterpret_cast<f32x4*>(dQ + j * D + c0) = dq;
+      for (int k = 0; k < 4; ++k) sd[k] += __shfl_xor(sd[k], o, 64);
+    if (slot == 0)
+      *reinterpret_cast<f32x4*>(dQ + (int64_t)hv.x * D + c0) =
+          f32x4{(float)sd[0], (float)sd[1], (float)sd[2], (float)sd[3]};
   }
 }
 
 // rowpart[(j R + r) T + ti] = sum of the mu terms of CSR row (j, r) whose
 // source has type ti (one thread per row, entries in order).
-__global__ void k_dmu_rows(int64_t n_rows, int32_t T, const int32_t* __restrict__ type_off,
+// Rows of destinations whose in-edges are chunked (more than kFwdChunk over
+// all relations) are left to k_dmu_heavy.
+__global__ void k_dmu_rows(int64_t n_rows, int32_t R, int32_t T, const int32_t* __restrict__ type_off,
                            const int32_t* __restrict__ csr_ptr, const int32_t* __restrict__ csr_col,
                            const float* __restrict__ contrib, float* __restrict__ rowpart) {
   for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < n_rows; q += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t rb = q - q % R;
+    if (csr_ptr[rb + R] - csr_ptr[rb] > kFwdChunk) continue;
     float acc[kMaxTypesBwd] = {0.f, 0.f, 0.f, 0.f};
     for (int32_t p = csr_ptr[q]; p < csr_ptr[q + 1]; ++p) {
       const int ti = type_of(csr_col[p], T, type_off);
@@ -490,10 +692,12 @@ __global__ void k_dmu_rows(int64_t n_rows, int32_t T, const int32_t* __restrict_
 }
 
 // Source pass: one wave per work item (CSC row q = i * R + r or a chunk of
-// it); Kt and Vt of the row are read once, Q and dh~ gathered per out-edge.
+// it, at slot item.x); Kt and Vt of the row are read once, Q and dh~
+// gathered per out-edge.
 template <int D, int S>
 __global__ void __launch_bounds__(kAttnThreads) k_hgt_attn_bwd_src(
-    int64_t n_items, const int4* __restrict__ items, int32_t R, int32_t T, const int32_t* __restrict__ type_off,
+    int64_t n_items, const int4* __restrict__ items, const int32_t* __restrict__ slot_q, int32_t R, int32_t T,
+    const int32_t* __restrict__ type_off,
     const int32_t* __restrict__ csc_row, const float* __restrict__ Q, const float* __restrict__ Kt,
     const float* __restrict__ Vt, const float* __restrict__ dht, const float* __restrict__ ld,
     const float* __restrict__ mu, float inv_sqrt_dk, float* __restrict__ dKt,
@@ -505,11 +709,12 @@ __global__ void __launch_bounds__(kAttnThreads) k_hgt_attn_bwd_src(
   const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
   for (int64_t it = wave0; it < n_items; it += nwaves) {
     const int4 item = items[it];
-    const int64_t qrow = item.x;
-    const int32_t i = (int32_t)(qrow / R), r = (int32_t)(qrow % R);
+    const int64_t srow = item.x;
+    const int32_t qrow = slot_q ? slot_q[srow] : (int32_t)srow;
+    const int32_t i = qrow / R, r = qrow % R;
     const int ti = type_of(i, T, type_off);
-    const f32x4 kt = *reinterpret_cast<const f32x4*>(Kt + qrow * D + c0);
-    const f32x4 vt = *reinterpret_cast<const f32x4*>(Vt + qrow * D + c0);
+    const f32x4 kt = *reinterpret_cast<const f32x4*>(Kt + srow * D + c0);
+    const f32x4 vt = *reinterpret_cast<const f32x4*>(Vt + srow * D + c0);
     f64x4 dk = {0.0, 0.0, 0.0, 0.0}, dv = {0.0, 0.0, 0.0, 0.0};
     for (int32_t base = item.y; base < item.z; base += 64) {
       const int32_t pos = base + l;
@@ -566,8 +771,8 @@ __global__ void __launch_bounds__(kAttnThreads) k_hgt_attn_bwd_src(
       }
     if (slot == 0) {
       if (item.w < 0) {
-        *reinterpret_cast<f32x4*>(dKt + qrow * D + c0) = f32x4{(float)dk[0], (float)dk[1], (float)dk[2], (float)dk[3]};
-        *reinterpret_cast<f32x4*>(dVt + qrow * D + c0) = f32x4{(float)dv[0], (float)dv[1], (float)dv[2], (float)dv[3]};
+        *reinterpret_cast<f32x4*>(dKt + srow * D + c0) = f32x4{(float)dk[0], (float)dk[1], (float)dk[2], (float)dk[3]};
+        *reinterpret_cast<f32x4*>(dVt + srow * D + c0) = f32x4{(float)dv[0], (float)dv[1], (float)dv[2], (float)dv[3]};
       } else {
         *reinterpret_cast<f64x4*>(pk + (int64_t)item.w * D + c0) = dk;
         *reinterpret_cast<f64x4*>(pv + (int64_t)item.w * D + c0) = dv;
@@ -632,6 +837,44 @@ __global__ void k_diagblocks(const float* __restrict__ full, int64_t R, int d, i
     const int a = (int)((e / dk) % dk), b = (int)(e % dk);
     const float v = full[(r * d + s * dk + a) * d + s * dk + b];
     out[e] = accumulate ? out[e] + v : v;
+  }
+}
+
+// The rows (j, r) of one long destination row j per block: each thread sums
+// the entries t, t + 256, ... by source type, then a fixed tree over the
+// threads.
+constexpr int kDmuThreads = 256;
+__global__ void __launch_bounds__(kDmuThreads) k_dmu_heavy(int64_t n_heavy, const int4* __restrict__ heavy, int32_t R,
+                                                          int32_t T, const int32_t* __restrict__ type_off,
+                                                          const int32_t* __restrict__ csr_ptr,
+                                                          const int32_t* __restrict__ csr_col,
+                                                          const float* __restrict__ contrib,
+                                                          float* __restrict__ rowpart) {
+  __shared__ float red[kMaxTypesBwd][kDmuThreads];
+  const int tid = threadIdx.x;
+  for (int64_t h = blockIdx.x; h < n_heavy; h += gridDim.x) {
+    const int64_t j = heavy[h].x;
+    for (int32_t r = 0; r < R; ++r) {
+      const int64_t q = j * R + r;
+      float acc[kMaxTypesBwd] = {0.f, 0.f, 0.f, 0.f};
+      for (int32_t p = csr_ptr[q] + tid; p < csr_ptr[q + 1]; p += kDmuThreads) {
+        const int ti = type_of(csr_col[p], T, type_off);
+        const float v = contrib[p];
+#pragma unroll
+        for (int t = 0; t < kMaxTypesBwd; ++t) acc[t] += (ti == t) ? v : 0.f;
+      }
+#pragma unroll
+      for (int t = 0; t < kMaxTypesBwd; ++t) red[t][tid] = acc[t];
+      __syncthreads();
+      for (int o = kDmuThreads / 2; o > 0; o >>= 1) {
+        if (tid < o)
+#pragma unroll
+          for (int t = 0; t < kMaxTypesBwd; ++t) red[t][tid] += red[t][tid + o];
+        __syncthreads();
+      }
+      if (tid < T) rowpart[q * T + tid] = red[tid][0];
+      __syncthreads();
+    }
   }
 }
 
@@ -823,6 +1066,7 @@ __global__ void __launch_bounds__(kSumRThreads) k_gemm_rows_sumr(int64_t n_rows,
                                                                  const float* __restrict__ W,
                                                                  const float* __restrict__ A,
                                                                  const int32_t* __restrict__ csc_ptr,
+                                                                 const SlotEnt* __restrict__ slot_tab,
                                                                  float* __restrict__ out) {
   static_assert(D == 64, "R matrices of 64 x 64 in LDS");
   constexpr int KB = D / 16, KB2 = D / 32, NB = D / 16;
@@ -875,10 +1119,13 @@ __global__ void __launch_bounds__(kSumRThreads) k_gemm_rows_sumr(int64_t n_rows,
   for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
     const int64_t i = t * kRowsPerTile + 16 * w + c;
     const bool live = i < n_rows;
-    // the row's CSC pointers i R .. i R + R: relation r is active iff its row is not empty
+    // the row's CSC pointers i R .. i R + R: relation r is active iff its row
+    // is not empty; the active relations of row i hold consecutive slots
+    // from slot(i R) (row-indexed layout, slot_tab null: rows i R + r)
     int32_t p[kSumRMax + 1];
 #pragma unroll
     for (int q = 0; q <= kSumRMax; ++q) p[q] = (live && q <= R) ? csc_ptr[i * R + q] : 0;
+    int64_t sl = (live && slot_tab) ? slot_of(slot_tab, i * R) : 0;
     f32x4 tot[NB];
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) tot[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -886,13 +1133,14 @@ __global__ void __launch_bounds__(kSumRThreads) k_gemm_rows_sumr(int64_t n_rows,
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb)
       nxt[kb] = (live && R > 0 && p[1] > p[0])
-                    ? *reinterpret_cast<const f32x4*>(A + (i * R) * D + 16 * kb + 4 * g)
+                    ? *reinterpret_cast<const f32x4*>(A + (slot_tab ? sl : i * R) * D + 16 * kb + 4 * g)
                     : f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int r = 0; r < kSumRMax; ++r) {
       if (r >= R) break;
       __builtin_amdgcn_sched_barrier(0);
       const bool act = live && p[r + 1] > p[r];
+      if (act) ++sl;  // sl: slot of the next active relation of row i
       f32x4 a[KB];
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb) a[kb] = nxt[kb];
@@ -900,7 +1148,7 @@ __global__ void __launch_bounds__(kSumRThreads) k_gemm_rows_sumr(int64_t n_rows,
         const bool act1 = live && p[r + 2] > p[r + 1];
 #pragma unroll
         for (int kb = 0; kb < KB; ++kb)
-          nxt[kb] = act1 ? *reinterpret_cast<const f32x4*>(A + (i * R + r + 1) * D + 16 * kb + 4 * g)
+          nxt[kb] = act1 ? *reinterpret_cast<const f32x4*>(A + (slot_tab ? sl : i * R + r + 1) * D + 16 * kb + 4 * g)
                          : f32x4{0.f, 0.f, 0.f, 0.f};
       }
       if (__ballot(act) == 0) continue;  // wave-uniform: no row of the 16 is in S_r
@@ -952,7 +1200,7 @@ __global__ void __launch_bounds__(kSumRThreads) k_gemm_rows_sumr(int64_t n_rows,
 
 template <int D>
 int launch_gemm_rows_sumr(const char* name, int64_t n_rows, int32_t R, const float* W, const float* A,
-                          const int32_t* csc_ptr, float* out, hipStream_t st) {
+                          const int32_t* csc_ptr, const SlotEnt* slot_tab, float* out, hipStream_t st) {
   if (n_rows <= 0) return HG_OK;
   if (R < 1 || R > kSumRMax) return fail(HG_ERR_ARG, "%s: R = %d outside [1, %d]", name, R, kSumRMax);
   const size_t lds = sizeof(uint4) * 2 * ((D / 32) * (D / 16) * 64) * (size_t)R;
@@ -968,7 +1216,7 @@ int launch_gemm_rows_sumr(const char* name, int64_t n_rows, int32_t R, const flo
   const int64_t tiles = cdiv(n_rows, 16 * (kSumRThreads / 64));
   const int64_t cap = (int64_t)num_cus();
   HG_LAUNCH(name, kern, dim3((unsigned)(tiles < cap ? tiles : cap)), dim3(kSumRThreads), lds, st, n_rows, R, W, A,
-            csc_ptr, out);
+            csc_ptr, slot_tab, out);
   return HG_OK;
 }
 
@@ -1014,11 +1262,20 @@ int hgt_bwd_impl(const hg_subgraph* s, const hg_hgt_desc* L, const float* Hin, c
   do {                                                                                                                \
     HG_LAUNCH("hgt_attn_bwd_dst", (k_hgt_attn_bwd_dst<D, S_>), dim3(attn_grid(s->n_sub)), dim3(kAttnThreads), 0, st, \
               s->n_sub, R, T, (const int32_t*)s->type_off, (const int32_t*)s->csr_ptr, (const int32_t*)s->csr_col,   \
-              (const float*)sv.Q, Kt, Vt, (const float*)sv.ht,                                                        \
+              pv.csr_slot, (const float*)sv.Q, Kt, Vt, (const float*)sv.ht,                                           \
               (const float*)w.dht, (const float*)sv.lse, W->mu, inv_sqrt_dk, w.dQ, w.ld, w.contrib);                 \
+    if (s->plan_fwd_heavy > 0) {                                                                                      \
+      HG_LAUNCH("hgt_attn_bwd_dst_part", (k_hgt_attn_bwd_dst_part<D, S_>), dim3(attn_grid(s->plan_fwd_parts)),        \
+                dim3(kAttnThreads), 0, st, (int64_t)s->plan_fwd_parts, pv.fwd_items, R, T,                            \
+                (const int32_t*)s->type_off, (const int32_t*)s->csr_ptr, (const int32_t*)s->csr_col, pv.csr_slot,    \
+                (const float*)sv.Q, Kt, Vt, (const float*)sv.ht, (const float*)w.dht, (const float*)sv.lse, W->mu,   \
+                inv_sqrt_dk, w.pdq, w.contrib);                                                                       \
+      HG_LAUNCH("hgt_dq_merge", k_hgt_dq_merge<D>, dim3(attn_grid(s->plan_fwd_heavy)), dim3(kAttnThreads), 0, st,     \
+                (int64_t)s->plan_fwd_heavy, pv.fwd_heavy, (const float*)w.pdq, w.dQ);                                 \
+    }                                                                                                                 \
     if (s->plan_items > 0)                                                                                            \
       HG_LAUNCH("hgt_attn_bwd_src", (k_hgt_attn_bwd_src<D, S_>), dim3(attn_grid(s->plan_items)), dim3(kAttnThreads),  \
-                0, st, (int64_t)s->plan_items, pv.items, R, T, (const int32_t*)s->type_off,                           \
+                0, st, (int64_t)s->plan_items, pv.items, pv.slot_q, R, T, (const int32_t*)s->type_off,                \
                 (const int32_t*)s->csc_row, (const float*)sv.Q, Kt, Vt,                                               \
                 (const float*)w.dht, (const float*)w.ld, W->mu, inv_sqrt_dk, w.dKt, w.dVt,                            \
                 w.pk, w.pv);                                                                                          \
@@ -1042,9 +1299,9 @@ int hgt_bwd_impl(const hg_subgraph* s, const hg_hgt_desc* L, const float* Hin, c
   const bool fused_rel = D == 64 && R <= kSumRMax;
   if (fused_rel) {
     if constexpr (D == 64) {
-      HG_TRY(launch_gemm_rows_sumr<D>("hgt_bwd_dx_rel", s->n_sub, R, w.Watt, w.dKt, (const int32_t*)s->csc_ptr,
+      HG_TRY(launch_gemm_rows_sumr<D>("hgt_bwd_dx_rel", s->n_sub, R, w.Watt, w.dKt, (const int32_t*)s->csc_ptr, pv.slot_tab,
                                       w.dK, st));
-      HG_TRY(launch_gemm_rows_sumr<D>("hgt_bwd_dx_rel", s->n_sub, R, w.Wmsg, w.dVt, (const int32_t*)s->csc_ptr,
+      HG_TRY(launch_gemm_rows_sumr<D>("hgt_bwd_dx_rel", s->n_sub, R, w.Wmsg, w.dVt, (const int32_t*)s->csc_ptr, pv.slot_tab,
                                       w.dV, st));
     }
   } else {
@@ -1057,17 +1314,17 @@ int hgt_bwd_impl(const hg_subgraph* s, const hg_hgt_desc* L, const float* Hin, c
     const int64_t wo = (int64_t)r * D * D;
     if (!fused_rel) {
       HG_TRY((launch_gemm_rows_pp<D, true>("hgt_bwd_dx_rel", n, w.Watt + wo,
-                                           LoadRows<D, float>{w.dKt, rows_list(pv.active + off, R, r)},
+                                           LoadRows<D, float>{w.dKt, rows_list(pv.act_slot + off)},
                                            StoreRows<D, float>{w.dK, rows_list(pv.active + off), nullptr, w.dK}, st)));
       HG_TRY((launch_gemm_rows_pp<D, true>("hgt_bwd_dx_rel", n, w.Wmsg + wo,
-                                           LoadRows<D, float>{w.dVt, rows_list(pv.active + off, R, r)},
+                                           LoadRows<D, float>{w.dVt, rows_list(pv.act_slot + off)},
                                            StoreRows<D, float>{w.dV, rows_list(pv.active + off), nullptr, w.dV}, st)));
     }
     HG_TRY((launch_gemm_tn<D>("hgt_bwd_dw", n, LoadRows<D, float>{sv.K, rows_list(pv.active + off)},
-                              LoadRows<D, float>{w.dKt, rows_list(pv.active + off, R, r)}, w.splitk, w.colsum,
+                              LoadRows<D, float>{w.dKt, rows_list(pv.act_slot + off)}, w.splitk, w.colsum,
                               w.gatt + wo, nullptr, 0, st)));
     HG_TRY((launch_gemm_tn<D>("hgt_bwd_dw", n, LoadRows<D, float>{sv.V, rows_list(pv.active + off)},
-                              LoadRows<D, float>{w.dVt, rows_list(pv.active + off, R, r)}, w.splitk, w.colsum,
+                              LoadRows<D, float>{w.dVt, rows_list(pv.act_slot + off)}, w.splitk, w.colsum,
                               w.gmsg + wo, nullptr, 0, st)));
     off += n;
   }
@@ -1115,8 +1372,12 @@ int hgt_bwd_impl(const hg_subgraph* s, const hg_hgt_desc* L, const float* Hin, c
     const int64_t nq = s->n_sub * (int64_t)R;
     if (nq > 0)
       HG_LAUNCH("hgt_bwd_dmu", k_dmu_rows, dim3((unsigned)(cdiv(nq, 256) < 65536 ? cdiv(nq, 256) : 65536)), dim3(256), 0,
-                st, nq, T, (const int32_t*)s->type_off, (const int32_t*)s->csr_ptr, (const int32_t*)s->csr_col,
+                st, nq, R, T, (const int32_t*)s->type_off, (const int32_t*)s->csr_ptr, (const int32_t*)s->csr_col,
                 (const float*)w.contrib, w.rowpart);
+    if (s->plan_fwd_heavy > 0)
+      HG_LAUNCH("hgt_bwd_dmu", k_dmu_heavy, dim3((unsigned)(s->plan_fwd_heavy < 65536 ? s->plan_fwd_heavy : 65536)),
+                dim3(kDmuThreads), 0, st, (int64_t)s->plan_fwd_heavy, pv.fwd_heavy, R, T, (const int32_t*)s->type_off,
+                (const int32_t*)s->csr_ptr, (const int32_t*)s->csr_col, (const float*)w.contrib, w.rowpart);
     const int M = T * R * T;
     HG_LAUNCH("hgt_bwd_dmu", k_dmu_partial, dim3(kMuChunks, M), dim3(256), 0, st, (const float*)w.rowpart,
               (const int32_t*)s->type_off, R, T, w.mupart);

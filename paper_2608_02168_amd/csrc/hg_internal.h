@@ -79,13 +79,54 @@ struct Sizer {
 
 int num_cus();
 
+// Slots of the relation transforms.  The active (source, relation) pairs --
+// the CSC rows q = i * R + r that hold at least one entry -- are numbered
+// 0 .. A-1 in q order, so the transforms Y_r[slot] take A rows instead of
+// n_sub * R, and the active relations of one source have consecutive slots.
+// slot(q) = the number of active rows before q, from one 16-byte entry per
+// 64 rows: the active-row mask of the 64 and the count before them.
+//
+// When the row-indexed layout (slot = q, n_sub * R rows) costs at most
+// kRowLayoutMaxSpread times the compact one, the build keeps it instead: the
+// gathers and row writes of the SpMMs run 5-7% faster over rows spread at
+// the pitch of R rows per node than over packed rows (measured at R = 5,
+// 3.6x spread), and the memory is there.  The plan then has no slot arrays
+// (PlanView's csr_slot, slot_q and slot_tab are null) and the kernels index
+// the transforms by q.
+constexpr int64_t kRowLayoutMaxSpread = 4;
+struct alignas(16) SlotEnt {
+  uint64_t mask;
+  int32_t pre;
+  int32_t pad;
+};
+
+__device__ __forceinline__ int32_t slot_of(const SlotEnt* __restrict__ tab, int64_t q) {
+  const int4 e = *reinterpret_cast<const int4*>(tab + (q >> 6));
+  const uint64_t m = ((uint64_t)(uint32_t)e.y << 32) | (uint32_t)e.x;
+  return e.z + (int32_t)__popcll(m & ((1ull << (q & 63)) - 1ull));
+}
+
 // Execution plan written by hg_build_csr (laid out for the input capacities).
 struct PlanView {
-  const int32_t* active;  // concatenated S_r lists: sources with >= 1 out-edge of relation r, ascending
-  const int4* items;      // backward work items (csc row q, begin, end, partial slot or -1)
-  const int4* heavy;      // split rows (q, first partial slot, number of slots, 0)
+  const int32_t* active;    // concatenated S_r lists: sources with >= 1 out-edge of relation r, ascending
+  const int32_t* act_slot;  // slot of each entry of `active` (same order)
+  const int32_t* slot_q;    // [A]: the CSC row q = i * R + r of each slot (null: row-indexed, slot = q)
+  const int32_t* csr_slot;  // [e_sub]: slot of the (source, relation) of each CSR entry (null: row-indexed)
+  const SlotEnt* slot_tab;  // [n_sub * R / 64 + 1] (null: row-indexed)
+  const int4* items;        // backward work items (slot, begin, end, partial slot or -1)
+  const int4* heavy;        // split rows (slot, first partial slot, number of slots, 0)
+  const int4* fwd_items;    // chunks of long destination rows (j, begin, end, partial slot)
+  const int4* fwd_heavy;    // long destination rows (j, first partial slot, number of slots, 0)
 };
+
+// Destination rows (all relations of one node j in the CSR) longer than
+// this are not walked by one wave: the plan cuts them into chunks of this
+// many entries whose partial results are merged in chunk order.
+constexpr int32_t kFwdChunk = 2048;
 PlanView plan_view(const hg_subgraph* s);
+
+// Rows of the relation transforms: A (compact) or n_sub * R (row-indexed).
+inline int64_t n_slots(const hg_subgraph* s) { return s->plan_slot_rows; }
 
 // ---- primitives (hg_scan.hip) -------------------------------------------
 // Exclusive prefix sum of n int32 values into out (out may equal in).

@@ -3,12 +3,16 @@
 // Forward (message, aggregation and update equations of the "Heterogeneous
 // Graph Transformer" paragraph in relation-typed mean form):
 //   (c) MFMA transforms  Y_self = H W_self[t] + b[t]   per contiguous type range
-//                        Y[i*R + r] = H_i W_r           for i in S_r (active sources)
-//   (b) SpMM             z_j = Y_self[j] + sum_{edges i->j of relation r} Y[i*R+r] / deg_r(j)
+//                        Y[slot(i,r)] = H_i W_r         for i in S_r (active sources)
+//   (b) SpMM             z_j = Y_self[j] + sum_{edges i->j of relation r} Y[slot(i,r)] / deg_r(j)
 //                        h'_j = ReLU(z_j) + h_j, ReLU mask saved as bits
+// Y holds one row per active (source, relation) pair, A rows in all (slots
+// numbered in CSC row order; the plan gives the slot of every CSR entry), or
+// is indexed by the CSC row q = i R + r when that costs at most a few times
+// more (the plan's row-indexed layout).
 // Backward:
 //   dZ = G * mask, formed while the dX self-transform loads G (and written out)
-//   (b) transposed SpMM  dY[i*R + r] = sum_{edges i->j of r} csc_scale * dZ_j  (no atomics;
+//   (b) transposed SpMM  dY[slot(i,r)] = sum_{edges i->j of r} csc_scale * dZ_j  (no atomics;
 //                        rows longer than the chunk size are split, then summed in order)
 //   (c) MFMA             dH = G + dZ W_self^T, then dH[S_r] += dY_r W_r^T for r = 0..R-1
 //                        dW_self[t] = H_t^T dZ_t, db[t] = colsum dZ_t, dW_r = H[S_r]^T dY_r
@@ -27,16 +31,103 @@ namespace {
 // and weights of up to 64 entries sit one per lane and are broadcast with
 // ds_bpermute.  Accumulation is float32.
 // fp32 rows: 8 waves per SIMD (<= 64 VGPRs) keep the most gathers in flight.
+// Rows of more than kFwdChunk entries (destination hubs) are left to the
+// plan's chunks: k_spmm_fwd_part sums one chunk each, k_spmm_fwd_merge adds
+// a row's chunks in order and applies the epilogue.
+
+// acc (lane's slot share, columns c0..c0+EL) += weighted Y rows of the CSR
+// entries [beg, end) of destination row rb / R, whose entries over all
+// relations are [p0, pe).  Y row of an entry: its slot, or src * R + r in
+// the row-indexed layout (csr_slot null).
+template <int D, class T>
+__device__ __forceinline__ void fwd_gather(int64_t rb, int32_t R, int32_t p0, int32_t pe, int32_t beg, int32_t end,
+                                           const int32_t* __restrict__ csr_ptr, const int32_t* __restrict__ csr_col,
+                                           const int32_t* __restrict__ csr_slot, const T* __restrict__ Y, int l,
+                                           int slot, int c0, float (&acc)[Elt<T>::EL]) {
+  constexpr int EL = Elt<T>::EL;
+  constexpr int EPW = 64 / (D / EL);
+  constexpr int U = 4;
+  for (int32_t base = beg; base < end; base += 64) {
+    const int32_t pos = base + l;
+    int32_t rowi = 0;
+    float wgt = 0.f;
+    if (pos < end) {
+      int32_t lo = p0, hi = pe, r = 0;
+      for (int t = 1; t < R; ++t) {
+        const int32_t pt = csr_ptr[rb + t];
+        if (pt <= pos) {
+          lo = pt;
+          r = t;
+        } else if (pt < hi) {
+          hi = pt;
+        }
+      }
+      rowi = csr_slot ? csr_slot[pos] : csr_col[pos] * R + r;
+      wgt = 1.0f / (float)(hi - lo);
+    }
+    const int cnt = (end - base) < 64 ? (end - base) : 64;
+    for (int e = 0; e < cnt; e += EPW * U) {
+      typename Elt<T>::rawv_t v[U];
+      float ww[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int my = e + u * EPW + slot;
+        const int32_t q = __shfl(rowi, my & 63, 64);
+        const float wq = __shfl(wgt, my & 63, 64);
+        ww[u] = (my < cnt) ? wq : 0.f;
+        v[u] = (my < cnt) ? Elt<T>::rawv(Y + (int64_t)q * D + c0) : Elt<T>::rawv_zero();
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int k = 0; k < EL; ++k) acc[k] += ww[u] * Elt<T>::rawv_get(v[u], k);
+    }
+  }
+}
+
+// z = acc + Y_self[j]; h' = ReLU(z) + h; the mask bits.  acc is reduced over
+// the slots; every lane of the wave calls it (the mask word is gathered with
+// shuffles), slot 0 stores.
+template <int D, class T>
+__device__ __forceinline__ void fwd_epilogue(int64_t j, const float (&acc)[Elt<T>::EL], int slot, int c0,
+                                             const T* __restrict__ Yself, const T* __restrict__ Hin,
+                                             T* __restrict__ Hout, uint32_t* __restrict__ mask, int relu,
+                                             int residual) {
+  constexpr int EL = Elt<T>::EL;
+  const int64_t off = j * D + c0;
+  uint32_t word = 0;
+  if (slot == 0) {
+    float ys[EL], h[EL], z[EL];
+    Elt<T>::load(Yself + off, ys);
+    float hin[EL];
+    if (residual) Elt<T>::load(Hin + off, hin);
+    uint32_t bits = 0;
+#pragma unroll
+    for (int k = 0; k < EL; ++k) {
+      z[k] = acc[k] + ys[k];
+      h[k] = (relu && !(z[k] > 0.f)) ? 0.f : z[k];
+      if (residual) h[k] += hin[k];
+      bits |= ((!relu || z[k] > 0.f) ? 1u : 0u) << k;
+    }
+    Elt<T>::store(Hout + off, h);
+    word = bits << (c0 & 31);
+  }
+  // OR the EL-bit groups of the 32/EL lanes that share a mask word
+#pragma unroll
+  for (int o = 1; o < 32 / EL; o <<= 1) word |= __shfl_xor(word, o, 64);
+  if (slot == 0 && (c0 & 31) == 0) mask[j * (D / 32) + (c0 >> 5)] = word;
+}
+
 template <int D, class T>
 __global__ void __launch_bounds__(256, (sizeof(T) == 2 || D <= 128) ? 8 : 4) k_spmm_fwd(int64_t n_sub, int32_t R, const int32_t* __restrict__ csr_ptr,
                                                   const int32_t* __restrict__ csr_col,
+                                                  const int32_t* __restrict__ csr_slot,
                                                   const T* __restrict__ Y, const T* __restrict__ Yself,
                                                   const T* __restrict__ Hin, T* __restrict__ Hout,
                                                   uint32_t* __restrict__ mask, int relu, int residual) {
   constexpr int EL = Elt<T>::EL;
   constexpr int LPR = D / EL;
   constexpr int EPW = 64 / LPR;
-  constexpr int U = 4;
   static_assert(LPR <= 64 && EPW * LPR == 64, "row must span a power-of-two number of lanes");
   const int l = threadIdx.x & 63;
   const int slot = l / LPR;
@@ -47,72 +138,91 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 2 || D <= 128) ? 8 : 4) k_s
     const int64_t rb = j * R;
     const int32_t p0 = csr_ptr[rb];
     const int32_t pe = csr_ptr[rb + R];
+    if (pe - p0 > kFwdChunk) continue;  // a chunked row
     float acc[EL];
 #pragma unroll
     for (int q = 0; q < EL; ++q) acc[q] = 0.f;
-    for (int32_t base = p0; base < pe; base += 64) {
-      const int32_t pos = base + l;
-      int32_t rowi = 0;
-      float wgt = 0.f;
-      if (pos < pe) {
-        const int32_t src = csr_col[pos];
-        int32_t r = 0, lo = p0, hi = pe;
-        for (int t = 1; t < R; ++t) {
-          const int32_t pt = csr_ptr[rb + t];
-          if (pt <= pos) {
-            r = t;
-            lo = pt;
-          } else if (pt < hi) {
-            hi = pt;
-          }
-        }
-        rowi = src * R + r;
-        wgt = 1.0f / (float)(hi - lo);
-      }
-      const int cnt = (pe - base) < 64 ? (pe - base) : 64;
-      for (int e = 0; e < cnt; e += EPW * U) {
-        typename Elt<T>::rawv_t v[U];
-        float ww[U];
+    fwd_gather<D, T>(rb, R, p0, pe, p0, pe, csr_ptr, csr_col, csr_slot, Y, l, slot, c0, acc);
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-          const int my = e + u * EPW + slot;
-          const int32_t q = __shfl(rowi, my & 63, 64);
-          const float wq = __shfl(wgt, my & 63, 64);
-          ww[u] = (my < cnt) ? wq : 0.f;
-          v[u] = (my < cnt) ? Elt<T>::rawv(Y + (int64_t)q * D + c0) : Elt<T>::rawv_zero();
-        }
+    for (int o = LPR; o < 64; o <<= 1)
 #pragma unroll
-        for (int u = 0; u < U; ++u)
+      for (int k = 0; k < EL; ++k) acc[k] += __shfl_xor(acc[k], o, 64);
+    fwd_epilogue<D, T>(j, acc, slot, c0, Yself, Hin, Hout, mask, relu, residual);
+  }
+}
+
+// One wave per chunk (j, begin, end, partial slot) of a long destination
+// row: the chunk's weighted sum, float32, into its partial row.
+template <int D, class T>
+__global__ void __launch_bounds__(256) k_spmm_fwd_part(int64_t n_items, const int4* __restrict__ items, int32_t R,
+                                                       const int32_t* __restrict__ csr_ptr,
+                                                       const int32_t* __restrict__ csr_col,
+                                                       const int32_t* __restrict__ csr_slot, const T* __restrict__ Y,
+                                                       float* __restrict__ part) {
+  constexpr int EL = Elt<T>::EL;
+  constexpr int LPR = D / EL;
+  const int l = threadIdx.x & 63;
+  const int slot = l / LPR;
+  const int c0 = (l % LPR) * EL;
+  const int64_t wave0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+  const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
+  for (int64_t it = wave0; it < n_items; it += nwaves) {
+    const int4 item = items[it];
+    const int64_t rb = (int64_t)item.x * R;
+    float acc[EL];
 #pragma unroll
-          for (int k = 0; k < EL; ++k) acc[k] += ww[u] * Elt<T>::rawv_get(v[u], k);
+    for (int q = 0; q < EL; ++q) acc[q] = 0.f;
+    fwd_gather<D, T>(rb, R, csr_ptr[rb], csr_ptr[rb + R], item.y, item.z, csr_ptr, csr_col, csr_slot, Y, l, slot, c0,
+                     acc);
+#pragma unroll
+    for (int o = LPR; o < 64; o <<= 1)
+#pragma unroll
+      for (int k = 0; k < EL; ++k) acc[k] += __shfl_xor(acc[k], o, 64);
+    if (slot == 0) {
+      float* p = part + (int64_t)item.w * D + c0;
+#pragma unroll
+      for (int k = 0; k < EL; k += 4) *reinterpret_cast<f32x4*>(p + k) = f32x4{acc[k], acc[k + 1], acc[k + 2], acc[k + 3]};
+    }
+  }
+}
+
+// One wave per long row (j, first partial, count): the partial rows added in
+// float64 (slot s takes partials s, s + EPW, ...; the slots then add in a
+// fixed tree), then the epilogue.
+template <int D, class T>
+__global__ void __launch_bounds__(256) k_spmm_fwd_merge(int64_t n_heavy, const int4* __restrict__ heavy,
+                                                        const float* __restrict__ part, const T* __restrict__ Yself,
+                                                        const T* __restrict__ Hin, T* __restrict__ Hout,
+                                                        uint32_t* __restrict__ mask, int relu, int residual) {
+  constexpr int EL = Elt<T>::EL;
+  constexpr int LPR = D / EL;
+  constexpr int EPW = 64 / LPR;
+  const int l = threadIdx.x & 63;
+  const int slot = l / LPR;
+  const int c0 = (l % LPR) * EL;
+  const int64_t wave0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+  const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
+  for (int64_t h = wave0; h < n_heavy; h += nwaves) {
+    const int4 hv = heavy[h];
+    double sd[EL];
+#pragma unroll
+    for (int k = 0; k < EL; ++k) sd[k] = 0.0;
+    for (int32_t c = slot; c < hv.z; c += EPW) {
+      const float* p = part + (int64_t)(hv.y + c) * D + c0;
+#pragma unroll
+      for (int k = 0; k < EL; k += 4) {
+        const f32x4 x = *reinterpret_cast<const f32x4*>(p + k);
+        sd[k] += x[0]; sd[k + 1] += x[1]; sd[k + 2] += x[2]; sd[k + 3] += x[3];
       }
     }
 #pragma unroll
     for (int o = LPR; o < 64; o <<= 1)
 #pragma unroll
-      for (int k = 0; k < EL; ++k) acc[k] += __shfl_xor(acc[k], o, 64);
-    const int64_t off = j * D + c0;
-    uint32_t word = 0;
-    if (slot == 0) {
-      float ys[EL], h[EL], z[EL];
-      Elt<T>::load(Yself + off, ys);
-      float hin[EL];
-      if (residual) Elt<T>::load(Hin + off, hin);
-      uint32_t bits = 0;
+      for (int k = 0; k < EL; ++k) sd[k] += __shfl_xor(sd[k], o, 64);
+    float acc[EL];
 #pragma unroll
-      for (int k = 0; k < EL; ++k) {
-        z[k] = acc[k] + ys[k];
-        h[k] = (relu && !(z[k] > 0.f)) ? 0.f : z[k];
-        if (residual) h[k] += hin[k];
-        bits |= ((!relu || z[k] > 0.f) ? 1u : 0u) << k;
-      }
-      Elt<T>::store(Hout + off, h);
-      word = bits << (c0 & 31);
-    }
-    // OR the EL-bit groups of the 32/EL lanes that share a mask word
-#pragma unroll
-    for (int o = 1; o < 32 / EL; o <<= 1) word |= __shfl_xor(word, o, 64);
-    if (slot == 0 && (c0 & 31) == 0) mask[j * (D / 32) + (c0 >> 5)] = word;
+    for (int k = 0; k < EL; ++k) acc[k] = (float)sd[k];
+    fwd_epilogue<D, T>(hv.x, acc, slot, c0, Yself, Hin, Hout, mask, relu, residual);
   }
 }
 
@@ -336,10 +446,12 @@ int validate_layer(const hg_subgraph* s, const hg_layer_desc* L) {
 template <int D, class T>
 struct FwdWs {
   T *Y, *Yself;
+  float* part;  // partial rows of the chunks of long destination rows
   template <class A>
   void layout(A& a, const hg_subgraph* s) {
-    Y = a.template take<T>(s->n_sub * s->n_rel * (int64_t)D);
+    Y = a.template take<T>(n_slots(s) * (int64_t)D);
     Yself = a.template take<T>(s->n_sub * (int64_t)D);
+    part = a.template take<float>(s->plan_fwd_parts * (int64_t)D);
   }
 };
 
@@ -354,7 +466,7 @@ struct BwdWs {
   template <class A>
   void layout(A& a, const hg_subgraph* s) {
     dZ = a.template take<T>(s->n_sub * (int64_t)D);
-    dY = a.template take<float>(s->n_sub * s->n_rel * (int64_t)D);
+    dY = a.template take<float>(n_slots(s) * (int64_t)D);
     dhacc = a.template take<float>(sizeof(T) == 2 ? s->n_sub * (int64_t)D : 0);
     part = a.template take<double>(s->plan_partials * (int64_t)D);
     splitk = a.template take<float>(splitk_max_chunks() * (int64_t)D * D);
@@ -400,15 +512,23 @@ int layer_fwd_impl(const hg_subgraph* s, const hg_layer_desc* L, const T* Hin, c
   for (int r = 0; r < R; ++r) {
     const int64_t n = s->n_active[r];
     LoadRows<D, T> la{Hin, rows_list(pv.active + off)};
-    StoreRows<D, T> ep{w.Y, rows_list(pv.active + off, R, r), nullptr, nullptr};
+    StoreRows<D, T> ep{w.Y, rows_list(pv.act_slot + off), nullptr, nullptr};
     HG_TRY((transform<D, T, false>("gemm_fwd_rel", n, W_rel + (int64_t)r * D * D, la, ep, st)));
     off += n;
   }
-  // (b) aggregation + epilogue
+  // (b) aggregation + epilogue; long destination rows by chunks
   if (s->n_sub > 0)
     HG_LAUNCH("spmm_fwd", (k_spmm_fwd<D, T>), dim3(wave_grid(s->n_sub)), dim3(256), 0, st, s->n_sub, R,
-              (const int32_t*)s->csr_ptr, (const int32_t*)s->csr_col, (const T*)w.Y, (const T*)w.Yself, Hin,
+              (const int32_t*)s->csr_ptr, (const int32_t*)s->csr_col, pv.csr_slot, (const T*)w.Y, (const T*)w.Yself, Hin,
               Hout, mask, L->relu, L->residual);
+  if (s->plan_fwd_heavy > 0) {
+    HG_LAUNCH("spmm_fwd_part", (k_spmm_fwd_part<D, T>), dim3(wave_grid(s->plan_fwd_parts)), dim3(256), 0, st,
+              (int64_t)s->plan_fwd_parts, pv.fwd_items, R, (const int32_t*)s->csr_ptr, (const int32_t*)s->csr_col,
+              pv.csr_slot, (const T*)w.Y, w.part);
+    HG_LAUNCH("spmm_fwd_merge", (k_spmm_fwd_merge<D, T>), dim3(wave_grid(s->plan_fwd_heavy)), dim3(256), 0, st,
+              (int64_t)s->plan_fwd_heavy, pv.fwd_heavy, (const float*)w.part, (const T*)w.Yself, Hin, Hout, mask,
+              L->relu, L->residual);
+  }
   return HG_OK;
 }
 
@@ -447,7 +567,7 @@ int layer_bwd_impl(const hg_subgraph* s, const hg_layer_desc* L, const T* Hin, c
   int64_t off = 0;
   for (int r = 0; r < R; ++r) {
     const int64_t n = s->n_active[r];
-    LoadRows<D, float> la{w.dY, rows_list(pv.active + off, R, r)};
+    LoadRows<D, float> la{w.dY, rows_list(pv.act_slot + off)};
     StoreRows<D, float, float> ep{dacc, rows_list(pv.active + off), nullptr, dacc};
     HG_TRY((rows_f32<D, true>("gemm_bwd_dx_rel", n, W_rel + (int64_t)r * D * D, la, ep, st)));
     off += n;
@@ -470,7 +590,7 @@ int layer_bwd_impl(const hg_subgraph* s, const hg_layer_desc* L, const T* Hin, c
   for (int r = 0; r < R; ++r) {
     const int64_t n = s->n_active[r];
     LoadRows<D, T> la{Hin, rows_list(pv.active + off)};
-    LoadRows<D, float> lb{w.dY, rows_list(pv.active + off, R, r)};
+    LoadRows<D, float> lb{w.dY, rows_list(pv.act_slot + off)};
     HG_TRY((launch_gemm_tn<D>("gemm_bwd_dw_rel", n, la, lb, w.splitk, w.colsum, dW_rel + (int64_t)r * D * D,
                               nullptr, acc, st)));
     off += n;

@@ -106,6 +106,7 @@ def _sub(n_sub=10, R=2, T=2):
     fake = C.c_void_p(0x1000)
     s.csr_ptr = s.csc_ptr = s.plan = fake
     s.n_sub, s.n_rel, s.n_ntype = n_sub, R, T
+    s.plan_slot_rows = n_sub * R  # the row-indexed layout of the relation transforms
     return s
 
 
@@ -294,7 +295,8 @@ def test_hgt_descriptor_flags_and_lean_sizes(L):
     bad = api.HgtDesc(64, 4, 0, 1, 1, 2)
     fake = C.c_void_p(0x1000)
     w = api.HgtWeights(*([fake] * 11))
-    # the relation transforms (2 x n_sub x R x d floats) leave `saved` and go to the workspaces
+    # the relation transforms (2 x rows x d floats, rows = n_sub x R in the row-indexed
+    # layout) leave `saved` and go to the workspaces
     kt = 2 * 1000 * 5 * 64 * 4
     assert L.hg_hgt_saved_size(C.byref(s), C.byref(full)) - L.hg_hgt_saved_size(C.byref(s), C.byref(lean)) == kt
     assert L.hg_hgt_fwd_workspace_size(C.byref(s), C.byref(lean)) - \

@@ -227,3 +227,20 @@ def test_node_keys_range_error_and_empty():
     for key in (0, 1):
         got = api.hg_node_keys(empty, empty, empty.to(torch.uint8), n, 1, key).cpu().numpy()
         assert np.all(got == 0)
+
+
+@pytest.mark.parametrize("n_rel", [3, 64])
+def test_transform_layout_choice(n_rel):
+    """The relation transforms take one row per active (source, relation)
+    pair (A rows) unless the row-indexed layout (n_sub * R rows) costs at
+    most four times that: tiny at R = 3 (A / (n_sub R) = 0.45) keeps the
+    row-indexed layout, R = 64 (0.06) the compact one."""
+    from dataclasses import replace
+    cfg = replace(synth.WORKLOADS["tiny"].graph, n_rel=n_rel)
+    g = synth.make_graph(cfg)
+    d = graph_to_dev(g)
+    sub = api.hg_build_csr(d["src"], d["dst"], d["rel"], d["ntype"], d["part"], g.k, n_rel, 2, cfg.budget)
+    A, nq = sum(sub.n_active()), sub.n_sub * n_rel
+    assert int(sub.c.plan_slot_rows) == (nq if nq <= 4 * A else A)
+    assert (nq <= 4 * A) == (n_rel == 3)
+

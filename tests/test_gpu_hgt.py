@@ -25,6 +25,8 @@ CFGS = {
     "skew_small_d64_h2": (synth.scaled(synth.WORKLOADS["skew"].graph, 0.002), 64, 2),
     # more than 8 relations: the d = 64 backward forms dK and dV one relation at a time
     "rel12_d64_h4": (replace(synth.scaled(synth.WORKLOADS["tiny"].graph, 0.3), n_rel=12, name="rel12"), 64, 4),
+    # 64 relations (the risk graph's 60+ event types): most (node, relation) pairs are empty
+    "rel64_d64_h4": (replace(synth.scaled(synth.WORKLOADS["tiny"].graph, 0.5), n_rel=64, name="rel64"), 64, 4),
 }
 
 
