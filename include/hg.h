@@ -43,6 +43,28 @@
  *    the ABI.
  *  - Ids are int32, counts int64, features float32 or bfloat16 (dtype),
  *    weights and weight gradients always float32.
+ *  - Precision of the float32 dense products.  They run on the 16-bit MFMA
+ *    with each float32 operand split into parts, a published way to recover
+ *    float32 accuracy from 16-bit matrix units:
+ *      row transforms (forward transforms, dX, the alignment's Grams and
+ *      gradient): the fp16 high part plus the fp16 remainder of each value,
+ *      after scaling the row (and W) by a power of two so that its largest
+ *      magnitude lies in [2^14, 2^15), with three of the four part
+ *      products formed (Ootomo and Yokota, "Recovering single precision
+ *      accuracy from Tensor Cores while surpassing the FP32 theoretical
+ *      peak performance", IJHPCA 2022).  Each product term is exact to
+ *      about 2^-21 of max|a row| x max|W| (the dropped remainder product
+ *      and the rounded remainders), so a K-term dot product is within
+ *      about K x 2^-21 x max|a| x max|w| of the exact value: float32
+ *      rounding relative to the row's largest terms, not to each term, so
+ *      a value much smaller than the largest of its row keeps fewer bits.
+ *      weight gradients (split-K over rows): three bfloat16 parts per
+ *      float32 value with the six part products of order at most two
+ *      (Henry, Tang and Heinecke, "Leveraging the bfloat16 artificial
+ *      intelligence datatype for higher-precision computations", ARITH
+ *      2019): each product term relative to itself within about 2^-22;
+ *      bfloat16 rows enter exactly.
+ *    Sums are float32 (float64 where the kernel says so).
  */
 #ifndef HG_H_
 #define HG_H_

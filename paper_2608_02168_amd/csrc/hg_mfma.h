@@ -472,7 +472,7 @@ struct StoreRows {
   }
 };
 
-// ---- gemm_rows --------------------------------------------------------------
+// ---- row GEMMs on the split-fp16 MFMA: shared shape ------------------------------
 // Block = 8 waves sharing one LDS copy of a column slice of op(W); a wave owns
 // 16 rows, a block 128 rows; persistent over tiles.  W is D x D; blockIdx.y
 // picks the column slice [DN*y, DN*y + DN) (DN = D for D <= 128, 128 for
@@ -487,152 +487,6 @@ template <int D>
 struct F32Slice {
   static constexpr int DN = D > 128 ? 128 : D;
 };
-
-template <int D, bool kTransW, class ALoad, class Epi>
-__global__ void __launch_bounds__(kGemmThreads) k_gemm_rows(int64_t n_rows, const float* __restrict__ W,
-                                                            ALoad aload, Epi epi) {
-  constexpr int DN = F32Slice<D>::DN;
-  constexpr int KB = D / 16, KB2 = D / 32, NB = DN / 16;
-  constexpr int kWaves = kGemmThreads / 64;
-  constexpr int kRowsPerTile = 16 * kWaves;
-  constexpr int kFrag = KB2 * NB * 64;
-  extern __shared__ uint4 wsl[];  // [kFrag] high parts, then [kFrag] remainders
-  __shared__ float wmax[kWaves + 1];
-  const int tid = threadIdx.x;
-  const int col0 = DN * blockIdx.y;
-  {
-    float m = 0.f;
-    for (int e = tid; e < D * D / 4; e += kGemmThreads) {
-      const f32x4 v = *reinterpret_cast<const f32x4*>(W + 4 * e);
-      m = fmaxf(m, fmaxf(fmaxf(fabsf(v[0]), fabsf(v[1])), fmaxf(fabsf(v[2]), fabsf(v[3]))));
-    }
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
-    if ((tid & 63) == 0) wmax[tid >> 6] = m;
-    __syncthreads();
-    m = wmax[0];
-#pragma unroll
-    for (int q = 1; q < kWaves; ++q) m = fmaxf(m, wmax[q]);
-    const uint32_t ew = split_exp(m);
-    const float sw = split_scale(ew);
-    for (int e = tid; e < kFrag; e += kGemmThreads) {
-      const int l = e & 63;
-      const int nb = (e >> 6) % NB;
-      const int kb2 = (e >> 6) / NB;
-      const int j = col0 + 16 * nb + (l & 15);
-      float v[8];
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const int k0 = 16 * (2 * kb2 + h) + 4 * (l >> 4);
-        if (kTransW) {
-          const f32x4 x = *reinterpret_cast<const f32x4*>(W + (int64_t)j * D + k0);
-#pragma unroll
-          for (int q = 0; q < 4; ++q) v[4 * h + q] = x[q] * sw;
-        } else {
-#pragma unroll
-          for (int q = 0; q < 4; ++q) v[4 * h + q] = W[(int64_t)(k0 + q) * D + j] * sw;
-        }
-      }
-      split8(v, wsl[e], wsl[kFrag + e]);
-    }
-    if (tid == 0) wmax[kWaves] = split_unscale(ew);
-    __syncthreads();
-  }
-  const float uw = wmax[kWaves];
-  const int w = tid >> 6;
-  const int l = lane64();
-  const int g = l >> 4, c = l & 15;
-  const int64_t ntiles = (n_rows + kRowsPerTile - 1) / kRowsPerTile;
-  for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
-    // lane (c, g) owns row r0 + c; rows past the end are zero and never stored
-    const int64_t i = t * kRowsPerTile + 16 * w + c;
-    const bool live = i < n_rows;
-    uint4 xh[KB2], xlo[KB2];
-    float ux;
-    {
-      f32x4 a[KB];
-      if (live) {
-        const auto p = aload.rowp(i);
-#pragma unroll
-        for (int kb = 0; kb < KB; ++kb) a[kb] = aload.load4(p, 16 * kb + 4 * g);
-      } else {
-#pragma unroll
-        for (int kb = 0; kb < KB; ++kb) a[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
-      }
-      float m = 0.f;
-#pragma unroll
-      for (int kb = 0; kb < KB; ++kb)
-        m = fmaxf(m, fmaxf(fmaxf(fabsf(a[kb][0]), fabsf(a[kb][1])), fmaxf(fabsf(a[kb][2]), fabsf(a[kb][3]))));
-      m = fmaxf(m, __shfl_xor(m, 16, 64));
-      m = fmaxf(m, __shfl_xor(m, 32, 64));
-      const uint32_t ex = split_exp(m);
-      const float sx = split_scale(ex);
-      ux = split_unscale(ex);
-#pragma unroll
-      for (int kb2 = 0; kb2 < KB2; ++kb2) {
-        float v[8];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          v[q] = a[2 * kb2][q] * sx;
-          v[4 + q] = a[2 * kb2 + 1][q] * sx;
-        }
-        split8(v, xh[kb2], xlo[kb2]);
-      }
-    }
-    // The MFMA computes the transpose, out^T = op(W)^T A^T (W fragments as the
-    // A operand, A rows as the B operand), so lane (c, g) ends up holding
-    // row i, columns col0 + 16 nb + 4 g .. + 3 of the output: the epilogue
-    // reads and writes 16 bytes per lane per column block.
-    f32x4 acc[NB];
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int kb2 = 0; kb2 < KB2; ++kb2) {
-      // keep each K block's W fragments local (no hoisting of all LDS reads)
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
-        const int e = (kb2 * NB + nb) * 64 + l;
-        const uint4 bh = wsl[e], bl = wsl[kFrag + e];
-        acc[nb] = mfma_f16(bh, xh[kb2], acc[nb]);
-        acc[nb] = mfma_f16(bh, xlo[kb2], acc[nb]);
-        acc[nb] = mfma_f16(bl, xh[kb2], acc[nb]);
-      }
-    }
-    __builtin_amdgcn_sched_barrier(0);
-    if (live) {
-      const int64_t ro = epi.row(i);
-      f32x4 pre[NB];
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) pre[nb] = epi.pre4(i, ro, col0 + 16 * nb + 4 * g);
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb)
-        epi.store4(i, ro, col0 + 16 * nb + 4 * g, split_unscale4(acc[nb], ux, uw), pre[nb]);
-    }
-  }
-}
-
-template <int D, bool kTransW, class ALoad, class Epi>
-int launch_gemm_rows(const char* name, int64_t n_rows, const float* W, ALoad aload, Epi epi,
-                     hipStream_t s) {
-  if (n_rows <= 0) return HG_OK;
-  constexpr int DN = F32Slice<D>::DN;
-  const int64_t tiles = cdiv(n_rows, 16 * (kGemmThreads / 64));
-  const int64_t cap = (int64_t)num_cus() * (D > 128 ? 1 : 2);
-  const int64_t grid = tiles < cap ? tiles : cap;
-  const size_t lds = sizeof(float) * D * DN;
-  auto kern = k_gemm_rows<D, kTransW, ALoad, Epi>;
-  if (lds > 65536) {
-    static bool attr_set = false;
-    if (!attr_set) {
-      HG_HIP_TRY(hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
-      attr_set = true;
-    }
-  }
-  HG_LAUNCH(name, kern, dim3((unsigned)grid, D / DN), dim3(kGemmThreads), lds, s, n_rows, W, aload, epi);
-  return HG_OK;
-}
 
 // ---- gemm_rows, software-pipelined (d <= 128) ---------------------------------------
 // Row GEMM on the split-fp16 MFMA (v_mfma_f32_16x16x32_f16, three products
