@@ -17,6 +17,8 @@
 //   (c) MFMA             dH = G + dZ W_self^T, then dH[S_r] += dY_r W_r^T for r = 0..R-1
 //                        dW_self[t] = H_t^T dZ_t, db[t] = colsum dZ_t, dW_r = H[S_r]^T dY_r
 //                        (split-K with a fixed-order reduction)
+#include <vector>
+
 #include "hg_internal.h"
 #include "hg_mfma.h"
 
@@ -414,9 +416,17 @@ __global__ void k_heavy_reduce(int64_t n_heavy, const int4* __restrict__ heavy,
   }
 }
 
-__global__ void k_to_bf16(const float* __restrict__ x, bf16_t* __restrict__ y, int64_t n) {
-  for (int64_t i = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4; i < n;
-       i += (int64_t)gridDim.x * blockDim.x * 4) {
+// y = bf16(x) on the rows whose CSC row of relation r is empty (the others
+// were written by that relation's dX pass): one thread per 4 columns.
+template <int D>
+__global__ void k_to_bf16_rest(const float* __restrict__ x, bf16_t* __restrict__ y, int64_t n_rows,
+                               const int32_t* __restrict__ csc_ptr, int32_t R, int32_t r) {
+  const int64_t total = n_rows * (D / 4);
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t row = e / (D / 4);
+    const int64_t q = row * R + r;
+    if (csc_ptr[q + 1] > csc_ptr[q]) continue;
+    const int64_t i = row * D + (e % (D / 4)) * 4;
     const f32x4 v = *reinterpret_cast<const f32x4*>(x + i);
     *reinterpret_cast<uint2*>(y + i) = uint2{pack2bf(v[0], v[1]), pack2bf(v[2], v[3])};
   }
@@ -563,20 +573,36 @@ int layer_bwd_impl(const hg_subgraph* s, const hg_layer_desc* L, const T* Hin, c
   if (s->plan_heavy > 0)
     HG_LAUNCH("spmm_bwd_reduce", (k_heavy_reduce<D, float>), dim3(wave_grid(s->plan_heavy)), dim3(256), 0, st,
               (int64_t)s->plan_heavy, pv.heavy, (const double*)w.part, w.dY);
-  // (c) dH += dY_r W_r^T per relation, in relation order
-  int64_t off = 0;
-  for (int r = 0; r < R; ++r) {
-    const int64_t n = s->n_active[r];
+  // (c) dH += dY_r W_r^T per relation, in relation order; for bfloat16 rows
+  // the relation with the most active sources goes last and writes its rows
+  // of dH in bf16 straight from the float32 accumulator, and only the other
+  // rows are converted afterwards
+  int32_t rlast = -1;
+  if constexpr (sizeof(T) == 2) {
+    rlast = 0;
+    for (int r = 1; r < R; ++r)
+      if (s->n_active[r] > s->n_active[rlast]) rlast = r;
+  }
+  std::vector<int64_t> act_off(R + 1, 0);
+  for (int r = 0; r < R; ++r) act_off[r + 1] = act_off[r] + s->n_active[r];
+  for (int k = 0; k < R; ++k) {
+    const int r = (rlast < 0) ? k : (k < rlast ? k : (k < R - 1 ? k + 1 : rlast));
+    const int64_t n = s->n_active[r], off = act_off[r];
     LoadRows<D, float> la{w.dY, rows_list(pv.act_slot + off)};
-    StoreRows<D, float, float> ep{dacc, rows_list(pv.active + off), nullptr, dacc};
-    HG_TRY((rows_f32<D, true>("gemm_bwd_dx_rel", n, W_rel + (int64_t)r * D * D, la, ep, st)));
-    off += n;
+    if (r == rlast) {
+      StoreRows<D, T, float> ep{dHin, rows_list(pv.active + off), nullptr, dacc};
+      HG_TRY((rows_f32<D, true>("gemm_bwd_dx_rel", n, W_rel + (int64_t)r * D * D, la, ep, st)));
+    } else {
+      StoreRows<D, float, float> ep{dacc, rows_list(pv.active + off), nullptr, dacc};
+      HG_TRY((rows_f32<D, true>("gemm_bwd_dx_rel", n, W_rel + (int64_t)r * D * D, la, ep, st)));
+    }
   }
   if constexpr (sizeof(T) == 2) {
-    const int64_t n = s->n_sub * (int64_t)D;
+    const int64_t n = s->n_sub * (int64_t)(D / 4);
     if (n > 0)
-      HG_LAUNCH("dh_to_bf16", k_to_bf16, dim3((unsigned)(cdiv(n / 4, 256) < 65536 ? cdiv(n / 4, 256) : 65536)),
-                dim3(256), 0, st, (const float*)w.dhacc, reinterpret_cast<bf16_t*>(dHin), n);
+      HG_LAUNCH("dh_to_bf16", k_to_bf16_rest<D>, dim3((unsigned)(cdiv(n, 256) < 65536 ? cdiv(n, 256) : 65536)),
+                dim3(256), 0, st, (const float*)w.dhacc, reinterpret_cast<bf16_t*>(dHin), s->n_sub,
+                (const int32_t*)s->csc_ptr, R, rlast);
   }
   // (c) weight gradients, split-K
   for (int t = 0; t < s->n_ntype; ++t) {
@@ -586,14 +612,12 @@ int layer_bwd_impl(const hg_subgraph* s, const hg_layer_desc* L, const T* Hin, c
     HG_TRY((launch_gemm_tn<D>("gemm_bwd_dw_self", hi - lo, la, lb, w.splitk, w.colsum,
                               dW_self + (int64_t)t * D * D, dbias ? dbias + (int64_t)t * D : nullptr, acc, st)));
   }
-  off = 0;
   for (int r = 0; r < R; ++r) {
-    const int64_t n = s->n_active[r];
+    const int64_t n = s->n_active[r], off = act_off[r];
     LoadRows<D, T> la{Hin, rows_list(pv.active + off)};
     LoadRows<D, float> lb{w.dY, rows_list(pv.act_slot + off)};
     HG_TRY((launch_gemm_tn<D>("gemm_bwd_dw_rel", n, la, lb, w.splitk, w.colsum, dW_rel + (int64_t)r * D * D,
                               nullptr, acc, st)));
-    off += n;
   }
   return HG_OK;
 }

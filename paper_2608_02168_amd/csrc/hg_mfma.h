@@ -779,8 +779,11 @@ int launch_gemm_rows_pp(const char* name, int64_t n_rows, const float* W, ALoad 
 // columns.  Accumulation is float32.
 template <int D>
 struct BfShape {
-  static constexpr int CG = D >= 256 ? 4 : 1;
-  static constexpr int RG = D >= 256 ? 4 : 8;
+  // one wave per 16 rows and all D columns: each A row is read by one wave
+  // only (column groups of waves sharing rows fetched them from memory up to
+  // 2.4 times at d = 256)
+  static constexpr int CG = 1;
+  static constexpr int RG = 8;
   static constexpr int kThreads = 64 * CG * RG;
 };
 
@@ -830,12 +833,15 @@ __global__ void __launch_bounds__(BfShape<D>::kThreads) k_gemm_rows_bf16(int64_t
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb) {
       __builtin_amdgcn_sched_barrier(0);
-      uint4 b[NBW];
 #pragma unroll
-      for (int nb = 0; nb < NBW; ++nb) b[nb] = wlb[(kb * NB + cg * NBW + nb) * 64 + l];
-      // transposed product: W fragments as the A operand, A rows as the B operand
+      for (int nb0 = 0; nb0 < NBW; nb0 += 4) {
+        uint4 b[4];
 #pragma unroll
-      for (int nb = 0; nb < NBW; ++nb) acc[nb] = mfma_bf16(b[nb], a[kb], acc[nb]);
+        for (int u = 0; u < 4; ++u) b[u] = wlb[(kb * NB + cg * NBW + nb0 + u) * 64 + l];
+        // transposed product: W fragments as the A operand, A rows as the B operand
+#pragma unroll
+        for (int u = 0; u < 4; ++u) acc[nb0 + u] = mfma_bf16(b[u], a[kb], acc[nb0 + u]);
+      }
     }
     __builtin_amdgcn_sched_barrier(0);
     // lane (c, g) holds row r0 + c, columns 16 (cg*NBW + nb) + 4 g .. + 3
