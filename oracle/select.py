@@ -16,7 +16,9 @@ construction loop of Algorithm 1:
    subgraph G[V~_k], relabelled in (node type, global id) order;
 5. per-relation CSR (destination-major) and CSC (source-major) of the induced
    subgraph, entries of a row in ascending original edge index, and the CSC
-   scale 1/deg_r(destination) as a float32 quotient;
+   scale 1/deg_r(destination) as a float32 quotient (w_ij/deg_r(destination)
+   for weighted edges, the message weight over the in-edge count, with the
+   weight of every CSR entry);
 6. optionally one snapshot of it: only the induced edges whose timestamp is at
    most the cut (the node set, fixed by steps 1-4 on every edge, is shared by
    all snapshots).
@@ -130,11 +132,13 @@ class Subgraph:
     csc_scale: np.ndarray      # float32 [E_s] 1 / deg_r(destination)
     n_active: np.ndarray       # int64 [R] sources with at least one out-edge of relation r
     ntype_l: np.ndarray        # uint8 [N_s] node type by local id
+    w_l: np.ndarray = None     # float32 [E_s] edge weights in original order (weighted graphs)
+    csr_w: np.ndarray = None   # float32 [E_s] weight of each CSR entry (weighted graphs)
 
 
 def build(src, dst, rel, ntype, part, k: int, n_rel: int, n_ntype: int,
           budget: int, key: int = KEY_OUTDEG, theta: int = THETA_NONE,
-          seed: int = 0, edge_ts=None, t_cut=None) -> Subgraph:
+          seed: int = 0, edge_ts=None, t_cut=None, edge_w=None) -> Subgraph:
     """The overlapping subgraph of partition k.  With edge_ts, one snapshot
     of it: the node set (and everything that decides it) uses every edge, and
     only the induced edges with edge_ts <= t_cut are kept (snapshots are
@@ -185,7 +189,13 @@ def build(src, dst, rel, ntype, part, k: int, n_rel: int, n_ntype: int,
     csc_row = dst_l[q]
     dst_row = csc_row * r_count + rel_l[q]
     deg = (csr_ptr[dst_row + 1] - csr_ptr[dst_row]).astype(np.float32)
-    csc_scale = (np.float32(1.0) / deg).astype(np.float32)
+    w_l = csr_w = None
+    if edge_w is None:
+        csc_scale = (np.float32(1.0) / deg).astype(np.float32)
+    else:
+        w_l = np.asarray(edge_w, dtype=np.float32)[eid]
+        csr_w = w_l[p]
+        csc_scale = (w_l[q] / deg).astype(np.float32)   # float32 quotient
     n_active = (csc_counts.reshape(n_sub, r_count) > 0).sum(axis=0).astype(np.int64) \
         if n_sub else np.zeros(r_count, dtype=np.int64)
 
@@ -204,4 +214,4 @@ def build(src, dst, rel, ntype, part, k: int, n_rel: int, n_ntype: int,
         csr_ptr=csr_ptr.astype(np.int32), csr_col=csr_col.astype(np.int32),
         csr_eid=csr_eid.astype(np.int32),
         csc_ptr=csc_ptr.astype(np.int32), csc_row=csc_row.astype(np.int32),
-        csc_scale=csc_scale, n_active=n_active, ntype_l=ntype_l.astype(np.uint8))
+        csc_scale=csc_scale, n_active=n_active, ntype_l=ntype_l.astype(np.uint8), w_l=w_l, csr_w=csr_w)

@@ -184,6 +184,11 @@ def _rng(seed: int, stream: int) -> np.random.Generator:
     return np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, stream])))
 
 
+def edge_weights(seed: int, n_edges: int) -> np.ndarray:
+    """Positive per-edge message weights w_ij, float32, uniform in [0.1, 2)."""
+    return _rng(seed, 31).uniform(0.1, 2.0, n_edges).astype(np.float32)
+
+
 def make_graph(cfg: GraphConfig) -> Graph:
     """Draw the typed edge list of one configuration (deterministic in cfg)."""
     n, e = cfg.n_nodes, cfg.n_edges

@@ -22,18 +22,22 @@ def _case(seed, n=30, e=120, R=3, T=2, d=6, bias=0.1):
     return n, src, dst, rel, ntype, H, w_rel, w_self, b
 
 
-def _dense_forward(n, src, dst, rel, ntype, H, w_rel, w_self, b):
+def _dense_forward(n, src, dst, rel, ntype, H, w_rel, w_self, b, ew=None):
+    """Dense brute force: per relation the weighted adjacency A[t, s] += w and
+    the in-edge count, loops over the destinations."""
     R, d = w_rel.shape[0], H.shape[1]
     Z = np.zeros((n, d))
+    ew = np.ones(len(src)) if ew is None else ew
     for r in range(R):
         A = np.zeros((n, n))
-        for s, t, rr in zip(src, dst, rel):
+        cnt = np.zeros(n)
+        for s, t, rr, we in zip(src, dst, rel, ew):
             if rr == r:
-                A[t, s] += 1.0
-        deg = A.sum(axis=1)
+                A[t, s] += we
+                cnt[t] += 1
         for j in range(n):
-            if deg[j] > 0:
-                Z[j] += (A[j] @ H) / deg[j] @ w_rel[r]
+            if cnt[j] > 0:
+                Z[j] += (A[j] @ H) / cnt[j] @ w_rel[r]
     for j in range(n):
         Z[j] += H[j] @ w_self[ntype[j]] + b[ntype[j]]
     return np.maximum(Z, 0) + H, Z
@@ -135,3 +139,64 @@ def test_adjoint_identity():
     for r in range(3):
         A = layer.mean_adjacency(n, src, dst, rel, r)
         assert abs(np.sum((A @ X) * Y) - np.sum(X * (A.T @ Y))) < 1e-12
+
+
+def _weights(seed, e):
+    return np.random.default_rng(seed + 50).uniform(0.1, 2.0, e)
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_weighted_forward_matches_dense_brute_force(seed):
+    """Edge weights multiply the messages; the normaliser stays the in-edge
+    count."""
+    c = _case(seed)
+    ew = _weights(seed, len(c[1]))
+    out, Z = layer.forward(*c, edge_w=ew)
+    out2, Z2 = _dense_forward(*c, ew=ew)
+    np.testing.assert_allclose(Z, Z2, rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(out, out2, rtol=1e-12, atol=1e-12)
+
+
+def test_unit_weights_equal_the_unweighted_layer():
+    c = _case(3)
+    ones = np.ones(len(c[1]))
+    np.testing.assert_array_equal(layer.forward(*c)[1], layer.forward(*c, edge_w=ones)[1])
+    G = np.random.default_rng(2).standard_normal(c[5].shape)
+    for a, b in zip(layer.backward(*c, G), layer.backward(*c, G, edge_w=ones)):
+        np.testing.assert_array_equal(a, b)
+
+
+def test_weights_scale_the_relation_part_linearly():
+    """w = c everywhere multiplies z - (self term) by c (closed form)."""
+    n, src, dst, rel, ntype, H, w_rel, w_self, b = _case(8)
+    zero_self = np.zeros_like(w_self)
+    zb = np.zeros_like(b)
+    _, Z1 = layer.forward(n, src, dst, rel, ntype, H, w_rel, zero_self, zb)
+    _, Zc = layer.forward(n, src, dst, rel, ntype, H, w_rel, zero_self, zb, edge_w=np.full(len(src), 2.5))
+    np.testing.assert_allclose(Zc, 2.5 * Z1, rtol=1e-13, atol=1e-13)
+
+
+def test_weighted_backward_matches_finite_differences():
+    n, src, dst, rel, ntype, H, w_rel, w_self, b = _case(21, n=14, e=50, R=2, d=4, bias=0.3)
+    ew = _weights(21, len(src))
+    G = np.random.default_rng(121).standard_normal(H.shape)
+    _, Z = layer.forward(n, src, dst, rel, ntype, H, w_rel, w_self, b, edge_w=ew)
+    assert np.min(np.abs(Z)) > 1e-3, "pick a case away from ReLU kinks"
+    grads = layer.backward(n, src, dst, rel, ntype, H, w_rel, w_self, b, G, edge_w=ew)
+
+    def loss(H_, wr_, ws_, b_):
+        out, _ = layer.forward(n, src, dst, rel, ntype, H_, wr_, ws_, b_, edge_w=ew)
+        return float((out * G).sum())
+
+    h = 1e-6
+    args = [H, w_rel, w_self, b]
+    for which, grad in enumerate(grads):
+        num = np.zeros_like(grad)
+        it = np.nditer(args[which], flags=["multi_index"])
+        for _ in it:
+            idx = it.multi_index
+            plus = [a.copy() for a in args]; minus = [a.copy() for a in args]
+            plus[which][idx] += h; minus[which][idx] -= h
+            num[idx] = (loss(*plus) - loss(*minus)) / (2 * h)
+        np.testing.assert_allclose(grad, num, rtol=1e-6, atol=1e-6)
+

@@ -132,6 +132,32 @@ def test_build_matches_brute_force(seed, key):
 
 
 @pytest.mark.parametrize("seed", range(4))
+def test_weighted_build_matches_brute_force(seed):
+    """Edge weights: every CSR entry carries its edge's weight and every CSC
+    entry's scale is w / deg_r(destination), a float32 quotient; the rest of
+    the build is the unweighted one."""
+    rng = np.random.default_rng(300 + seed)
+    n, e, R = 45 + seed * 5, 200 + seed * 25, 1 + seed % 3
+    src, dst, rel, ntype, part = _random_graph(rng, n, e, R)
+    w = rng.uniform(0.1, 2.0, e).astype(np.float32)
+    sub = select.build(src, dst, rel, ntype, part, 1, R, 2, 7, seed=seed, edge_w=w)
+    plain = select.build(src, dst, rel, ntype, part, 1, R, 2, 7, seed=seed)
+    for name in ("local2global", "csr_ptr", "csr_col", "csr_eid", "csc_ptr", "csc_row"):
+        assert np.array_equal(getattr(sub, name), getattr(plain, name)), name
+    bf = _brute_build(list(src), list(dst), list(rel), list(ntype), list(part), 1, R, 2, 7,
+                      select.KEY_OUTDEG, select.THETA_NONE, seed)
+    for row in range(sub.n_sub * R):
+        entries = bf["csr_rows"][row]
+        got = sub.csr_w[sub.csr_ptr[row]:sub.csr_ptr[row + 1]]
+        assert [float(x) for x in got] == [float(w[eid]) for _, eid in entries]
+    for row in range(sub.n_sub * R):
+        r = row % R
+        for p, (d, eid) in zip(range(sub.csc_ptr[row], sub.csc_ptr[row + 1]), bf["csc_rows"][row]):
+            deg = len(bf["csr_rows"][d * R + r])
+            assert sub.csc_scale[p] == np.float32(w[eid]) / np.float32(deg)
+
+
+@pytest.mark.parametrize("seed", range(4))
 @pytest.mark.parametrize("cut", [-1, 3, 6, 9])
 def test_snapshot_matches_brute_force(seed, cut):
     rng = np.random.default_rng(100 + seed)
