@@ -111,7 +111,10 @@ typedef struct hg_graph_desc {
   const uint8_t* ntype;   /* [n_nodes] */
   const int32_t* part;    /* [n_nodes] partition id of every node */
   int32_t k;              /* this worker's partition */
-  const float* edge_w;    /* must be NULL: weighted edges are not implemented */
+  const float* edge_w;    /* [n_edges] message weight w_ij of each edge (the weighted
+                           * edges of the problem formulation), or NULL = 1.  A
+                           * message is multiplied by its weight; the mean's
+                           * normaliser stays the in-edge count (reading A10). */
   /* Snapshots (end of "Risk-Aware Subgraph Construction": the snapshot
    * sequence is taken from the augmented subgraph by filtering on edge
    * timestamps).  With edge_ts != NULL the node set, the keys, the candidates
@@ -160,13 +163,15 @@ int hg_node_keys(const hg_graph_desc* g, int32_t key, int32_t* keys, void* ws, s
  * type is a contiguous range [type_off[t], type_off[t+1]).  Row (v, r) of the
  * CSR holds the in-edges of relation r of local node v (index v*n_rel + r),
  * entries in ascending original edge index; the CSC likewise holds
- * out-edges.  csc_scale[p] = 1 / deg_r(csc_row[p]), the mean-aggregation
- * weight, as a correctly rounded float32 quotient.
+ * out-edges.  csc_scale[p] = w / deg_r(csc_row[p]), the mean-aggregation
+ * weight (w = the entry's edge weight, 1 without weights), as a correctly
+ * rounded float32 quotient.
  *
  * The caller allocates every device array to CAPACITY: node arrays n_nodes,
  * overlap arrays min(budget_M, n_nodes), type_off n_ntype + 1, pointer arrays
  * n_nodes * n_rel + 1, edge arrays n_edges, plan hg_plan_size() bytes.
- * csr_eid may be NULL.  hg_build_csr fills the host fields. */
+ * csr_eid may be NULL; csr_w may be NULL for a graph without weights.
+ * hg_build_csr fills the host fields. */
 typedef struct hg_subgraph {
   /* device outputs */
   int32_t* local2global;  /* [n_sub]  */
@@ -181,6 +186,8 @@ typedef struct hg_subgraph {
   int32_t* csc_ptr;       /* [n_sub * n_rel + 1] */
   int32_t* csc_row;       /* [e_sub] destination local id */
   float*   csc_scale;     /* [e_sub] */
+  float*   csr_w;         /* [e_sub] weight of each CSR entry; written for a weighted
+                           * graph (required then), else unused and may be NULL */
   void*    plan;          /* opaque execution plan used by the layer kernels */
   size_t   plan_bytes;    /* capacity of plan */
   /* host outputs */
@@ -199,6 +206,7 @@ typedef struct hg_subgraph {
   int64_t plan_fwd_heavy; /* destination rows split into chunks (internal) */
   int64_t plan_fwd_parts; /* chunks of those rows (internal) */
   int64_t plan_slot_rows; /* rows of the relation transforms in the layer workspaces (internal) */
+  int64_t weighted;       /* 1 if built from a weighted graph (csr_w and csc_scale carry w) */
 } hg_subgraph;
 
 /* Bytes of `plan` for a graph with these input sizes. */

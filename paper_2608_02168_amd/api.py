@@ -70,13 +70,15 @@ class SubgraphStruct(C.Structure):
                 ("type_off", C.c_void_p), ("overlap", C.c_void_p), ("overlap_home", C.c_void_p),
                 ("overlap_rel", C.c_void_p), ("csr_ptr", C.c_void_p), ("csr_col", C.c_void_p),
                 ("csr_eid", C.c_void_p), ("csc_ptr", C.c_void_p), ("csc_row", C.c_void_p),
-                ("csc_scale", C.c_void_p), ("plan", C.c_void_p), ("plan_bytes", C.c_size_t),
+                ("csc_scale", C.c_void_p), ("csr_w", C.c_void_p), ("plan", C.c_void_p),
+                ("plan_bytes", C.c_size_t),
                 ("n_nodes", C.c_int64), ("n_edges", C.c_int64), ("n_sub", C.c_int64),
                 ("e_sub", C.c_int64), ("m_sel", C.c_int64), ("n_rel", C.c_int32),
                 ("n_ntype", C.c_int32), ("type_off_host", C.c_int64 * (HG_MAX_NTYPE + 1)),
                 ("n_active", C.c_int64 * HG_MAX_REL), ("plan_items", C.c_int64),
                 ("plan_heavy", C.c_int64), ("plan_partials", C.c_int64),
-                ("plan_fwd_heavy", C.c_int64), ("plan_fwd_parts", C.c_int64), ("plan_slot_rows", C.c_int64)]
+                ("plan_fwd_heavy", C.c_int64), ("plan_fwd_parts", C.c_int64), ("plan_slot_rows", C.c_int64),
+                ("weighted", C.c_int64)]
 
 
 class LayerDesc(C.Structure):
@@ -221,7 +223,7 @@ class Subgraph:
                   "type_off": self.n_ntype + 1, "overlap": self.m_sel,
                   "overlap_home": self.m_sel, "overlap_rel": self.m_sel, "csr_ptr": n_ptr,
                   "csc_ptr": n_ptr, "csr_col": self.e_sub, "csr_eid": self.e_sub,
-                  "csc_row": self.e_sub, "csc_scale": self.e_sub}[name]
+                  "csc_row": self.e_sub, "csc_scale": self.e_sub, "csr_w": self.e_sub}[name]
         return self.arrays[name][:length]
 
     def n_active(self):
@@ -238,17 +240,19 @@ def hg_plan_size(n_nodes: int, n_edges: int, n_rel: int) -> int:
 def hg_build_csr(src, dst, rel, ntype, part, k: int, n_rel: int, n_ntype: int, budget_M: int,
                  key: int = HG_KEY_OUTDEG, theta: int = HG_THETA_NONE, seed: int = 0,
                  want_eid: bool = True, stream=None, ws: Optional[torch.Tensor] = None,
-                 out: Optional[Subgraph] = None, edge_ts=None, t_cut: int = 0, node_key=None) -> Subgraph:
+                 out: Optional[Subgraph] = None, edge_ts=None, t_cut: int = 0, node_key=None,
+                 edge_w=None) -> Subgraph:
     """Overlapping-subgraph construction; inputs are device tensors
-    (src/dst/part int32, rel/ntype uint8, edge_ts int32 or None).
-    Synchronous.  ``out`` reuses the arrays of an earlier build of the same
-    input sizes.  With edge_ts, the snapshot that keeps the induced edges with
-    edge_ts <= t_cut.  node_key: the graph's keys from hg_node_keys (same
-    key kind), or None to compute them inside the build."""
+    (src/dst/part int32, rel/ntype uint8, edge_ts int32 or None, edge_w
+    float32 or None).  Synchronous.  ``out`` reuses the arrays of an earlier
+    build of the same input sizes.  With edge_ts, the snapshot that keeps the
+    induced edges with edge_ts <= t_cut.  node_key: the graph's keys from
+    hg_node_keys (same key kind), or None to compute them inside the build.
+    edge_w: message weights of the edges (csr_w is then allocated)."""
     dev = ntype.device
     n, e = int(ntype.shape[0]), int(src.shape[0])
     g = GraphDesc(n, e, n_rel, n_ntype, _ptr(src), _ptr(dst), _ptr(rel), _ptr(ntype), _ptr(part),
-                  k, None, _ptr(edge_ts), int(t_cut), 0)
+                  k, _ptr(edge_w), _ptr(edge_ts), int(t_cut), 0)
     o = OverlapDesc(budget_M, key, HG_KEYDIR_OUT, theta, 0, seed, _ptr(node_key))
     L = lib()
     if out is not None:
@@ -271,13 +275,14 @@ def hg_build_csr(src, dst, rel, ntype, part, k: int, n_rel: int, n_ntype: int, b
         "csr_eid": torch.empty(max(1, e), **i32) if want_eid else None,
         "csc_ptr": torch.empty(nq, **i32), "csc_row": torch.empty(max(1, e), **i32),
         "csc_scale": torch.empty(max(1, e), dtype=torch.float32, device=dev),
+        "csr_w": torch.empty(max(1, e), dtype=torch.float32, device=dev) if edge_w is not None else None,
     }
     plan_bytes = hg_plan_size(n, e, n_rel)
     arrays["plan"] = _ws(plan_bytes, dev)
     s = SubgraphStruct()
     for name in ("local2global", "global2local", "type_off", "overlap", "overlap_home",
                  "overlap_rel", "csr_ptr", "csr_col", "csr_eid", "csc_ptr", "csc_row",
-                 "csc_scale", "plan"):
+                 "csc_scale", "csr_w", "plan"):
         setattr(s, name, _ptr(arrays[name]))
     s.plan_bytes = plan_bytes
     need = int(L.hg_build_csr_workspace_size(C.byref(g), C.byref(o)))

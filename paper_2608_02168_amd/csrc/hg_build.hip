@@ -612,7 +612,9 @@ __global__ void __launch_bounds__(kBT) k_edge_emit(const int32_t* __restrict__ s
                                                    const uint8_t* __restrict__ rel, int64_t n_edges, int32_t n_rel,
                                                    const int32_t* __restrict__ tile_off, uint32_t* __restrict__ kcsr,
                                                    uint32_t* __restrict__ kcsc, int32_t* __restrict__ vsrc,
-                                                   int32_t* __restrict__ vdst, int32_t* __restrict__ veid) {
+                                                   int32_t* __restrict__ vdst, int32_t* __restrict__ veid,
+                                                   const float* __restrict__ edge_w, int32_t* __restrict__ vw1,
+                                                   int32_t* __restrict__ vw2) {
   constexpr int NW = kBT / 64;
   __shared__ int32_t cnt[kERounds * NW];
   const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
@@ -653,6 +655,7 @@ __global__ void __launch_bounds__(kBT) k_edge_emit(const int32_t* __restrict__ s
       vsrc[p] = a[j];
       vdst[p] = b[j];
       veid[p] = (int32_t)e;
+      if (edge_w) vw1[p] = vw2[p] = __float_as_int(edge_w[e]);
     }
   }
 }
@@ -687,7 +690,9 @@ __global__ void k_edge_compact(const int32_t* __restrict__ src, const int32_t* _
                                const int32_t* __restrict__ g2l, const uint8_t* __restrict__ rel,
                                const int32_t* __restrict__ pos, int64_t n_edges, int32_t n_rel,
                                uint32_t* __restrict__ kcsr, uint32_t* __restrict__ kcsc, int32_t* __restrict__ vsrc,
-                               int32_t* __restrict__ vdst, int32_t* __restrict__ veid) {
+                               int32_t* __restrict__ vdst, int32_t* __restrict__ veid,
+                               const float* __restrict__ edge_w, int32_t* __restrict__ vw1,
+                               int32_t* __restrict__ vw2) {
   GRID_STRIDE(e, n_edges) {
     const int32_t p = pos[e];
     if (pos[e + 1] != p) {
@@ -698,6 +703,7 @@ __global__ void k_edge_compact(const int32_t* __restrict__ src, const int32_t* _
       vsrc[p] = s;
       vdst[p] = d;
       veid[p] = (int32_t)e;
+      if (edge_w) vw1[p] = vw2[p] = __float_as_int(edge_w[e]);
     }
   }
 }
@@ -773,15 +779,23 @@ __global__ void k_deg_bytes(const int32_t* __restrict__ rowcnt, int64_t nq, uint
   }
 }
 
+// csc_scale = w / deg_r(destination), an IEEE float32 quotient; w = 1, or the
+// entry's edge weight already sorted into scale (weighted graphs).
 __global__ void k_csc_scale(const uint32_t* __restrict__ kcsc, const int32_t* __restrict__ csc_row,
                             const uint8_t* __restrict__ deg8, const int32_t* __restrict__ csr_ptr, int64_t n,
-                            int32_t n_rel, float* __restrict__ scale) {
+                            int32_t n_rel, int weighted, float* __restrict__ scale) {
   GRID_STRIDE(p, n) {
     const int64_t row = (int64_t)csc_row[p] * n_rel + (int64_t)(kcsc[p] % (uint32_t)n_rel);
     int32_t deg = deg8[row];
     if (deg == 255) deg = csr_ptr[row + 1] - csr_ptr[row];
-    scale[p] = 1.0f / (float)deg;
+    const float w = weighted ? scale[p] : 1.0f;
+    scale[p] = w / (float)deg;
   }
+}
+
+__global__ void k_gather_w(const int32_t* __restrict__ eid, const float* __restrict__ edge_w, int64_t n,
+                           float* __restrict__ out) {
+  GRID_STRIDE(p, n) out[p] = edge_w[eid[p]];
 }
 
 // Per CSC row q: relation digit for the active-source partition, work-item
@@ -927,10 +941,11 @@ struct BuildWs {
   SelectState* st;
   int32_t *keep, *vsrc, *vdst, *veid, *alt1, *alt2, *alt3, *rowcnt, *q_items, *q_heavy, *q_parts,
       *q_src, *scratch, *bcnt;
+  int32_t *vw1, *vw2, *walt;  // weighted graphs: edge weights (float bits) in edge order for each sort
   uint32_t *kcsr, *kcsc, *kalt, *bbits, *mbits;
   RankEnt* rt;
   int32_t *rc0, *rc1, *tile_cnt;
-  void layout(A& a, int64_t N, int64_t E, int64_t R, bool hindex) {
+  void layout(A& a, int64_t N, int64_t E, int64_t R, bool hindex, bool weighted) {
     const int64_t NQ = N * R + 1;
     cnt = a.template take<int32_t>(C_COUNT + 8);
     bcnt = a.template take<int32_t>(16384);  // block counts of k_base_bits (grid_for caps it there)
@@ -967,6 +982,9 @@ struct BuildWs {
     q_heavy = a.template take<int32_t>(NQ);
     q_parts = a.template take<int32_t>(NQ);
     q_src = a.template take<int32_t>(NQ);
+    vw1 = a.template take<int32_t>(weighted ? E : 0);
+    vw2 = a.template take<int32_t>(weighted ? E : 0);
+    walt = a.template take<int32_t>(weighted ? E : 0);
     int64_t sc = scan_scratch_elems(E + N + NQ + 1);
     int64_t rs = radix_scratch_elems(E > NQ ? E : NQ);
     scratch = a.template take<int32_t>(sc > rs ? sc : rs);
@@ -1045,7 +1063,6 @@ static int validate_build(const hg_graph_desc* g, const hg_overlap_desc* o) {
   if (g->n_edges > 0 && (!g->src || !g->dst || !g->rel))
     return fail(HG_ERR_ARG, "null edge array");
   if (!g->ntype || !g->part) return fail(HG_ERR_ARG, "null node array");
-  if (g->edge_w) return fail(HG_ERR_UNSUPPORTED, "edge weights are not implemented");
   if (o->budget_M < 0) return fail(HG_ERR_ARG, "budget_M < 0");
   if (o->key != HG_KEY_OUTDEG && o->key != HG_KEY_HINDEX) return fail(HG_ERR_ARG, "key %d", o->key);
   if (o->key_dir != HG_KEYDIR_OUT) return fail(HG_ERR_UNSUPPORTED, "key_dir %d", o->key_dir);
@@ -1139,7 +1156,7 @@ extern "C" size_t hg_build_csr_workspace_size(const hg_graph_desc* g, const hg_o
   if (validate_build(g, o) != HG_OK) return 0;
   Sizer sz;
   BuildWs<Sizer> w;
-  w.layout(sz, g->n_nodes, g->n_edges, g->n_rel, o->key == HG_KEY_HINDEX);
+  w.layout(sz, g->n_nodes, g->n_edges, g->n_rel, o->key == HG_KEY_HINDEX, g->edge_w != nullptr);
   return sz.used + 256;
 }
 
@@ -1152,6 +1169,8 @@ extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg
       (!out->overlap_home && o->budget_M > 0) || (!out->overlap_rel && o->budget_M > 0) ||
       (g->n_edges > 0 && (!out->csr_col || !out->csc_row || !out->csc_scale)))
     return fail(HG_ERR_ARG, "null output array");
+  const bool weighted = g->edge_w != nullptr;
+  if (weighted && g->n_edges > 0 && !out->csr_w) return fail(HG_ERR_ARG, "a weighted graph needs the csr_w output");
   const int64_t N = g->n_nodes, E = g->n_edges, R = g->n_rel, T = g->n_ntype;
   const size_t need_plan = hg_plan_size(N, E, (int32_t)R);
   if (out->plan_bytes < need_plan)
@@ -1163,7 +1182,7 @@ extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg
 
   Arena arena(ws, ws_bytes);
   BuildWs<Arena> w;
-  w.layout(arena, N, E, R, hindex);
+  w.layout(arena, N, E, R, hindex, g->edge_w != nullptr);
   if (!arena.ok()) return fail(HG_ERR_CAPACITY, "workspace layout overflow");
 
   const unsigned gN = grid_for(N), gE = grid_for(E);
@@ -1256,7 +1275,7 @@ extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg
       HG_TRY(scan_exclusive_i32(w.tile_cnt, w.tile_cnt, ntiles, w.cnt + C_ESUB, w.scratch, s));
       HG_LAUNCH("build_edge_compact", k_edge_emit, dim3((unsigned)ntiles), dim3(kBT), 0, s, (const int32_t*)w.alt1,
                 (const int32_t*)w.alt2, g->rel, E, (int32_t)R, (const int32_t*)w.tile_cnt, w.kcsr, w.kcsc, w.vsrc,
-                w.vdst, w.veid);
+                w.vdst, w.veid, g->edge_w, w.vw1, w.vw2);
     } else {
       // more than two node types: local ids from global2local, membership from a bitmap
       HG_LAUNCH("build_member_bits", k_member_bits, dim3(gB), dim3(kBT), 0, s, g->part, g->k,
@@ -1268,7 +1287,7 @@ extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg
       HG_TRY(scan_exclusive_i32(w.keep, w.keep, E + 1, w.cnt + C_ESUB, w.scratch, s));
       HG_LAUNCH("build_edge_compact", k_edge_compact, dim3(gE), dim3(kBT), 0, s, g->src, g->dst,
                 (const int32_t*)out->global2local, g->rel, (const int32_t*)w.keep, E, (int32_t)R, w.kcsr, w.kcsc,
-                w.vsrc, w.vdst, w.veid);
+                w.vsrc, w.vdst, w.veid, g->edge_w, w.vw1, w.vw2);
     }
   } else {
     HG_TRY(fill_i32(w.cnt + C_ESUB, 0, 1, s));
@@ -1296,15 +1315,21 @@ extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg
     uint32_t* ko;
     int32_t *v1o, *v2o;
     const bool want_eid = out->csr_eid != nullptr;
-    HG_TRY(radix_sort_pairs(w.kcsr, w.kalt, w.vsrc, w.alt1, want_eid ? w.veid : nullptr,
-                            want_eid ? w.alt2 : nullptr, ES, bits, w.scratch, s, &ko, &v1o, &v2o, out->csr_col,
-                            want_eid ? out->csr_eid : nullptr));
+    // second value: the edge id if asked for, else the weight of a weighted graph
+    int32_t* v2 = want_eid ? w.veid : (weighted ? w.vw1 : nullptr);
+    int32_t* v2_final = want_eid ? out->csr_eid : (weighted ? reinterpret_cast<int32_t*>(out->csr_w) : nullptr);
+    HG_TRY(radix_sort_pairs(w.kcsr, w.kalt, w.vsrc, w.alt1, v2, v2 ? w.alt2 : nullptr, ES, bits, w.scratch, s, &ko,
+                            &v1o, &v2o, out->csr_col, v2_final));
     csr_keys = ko;
     if (ES > 0 && v1o != out->csr_col) {  // no pass ran (a single key value)
       HG_HIP_TRY(hipMemcpyAsync(out->csr_col, v1o, sizeof(int32_t) * ES, hipMemcpyDeviceToDevice, s));
-      if (want_eid)
-        HG_HIP_TRY(hipMemcpyAsync(out->csr_eid, v2o, sizeof(int32_t) * ES, hipMemcpyDeviceToDevice, s));
+      if (v2)
+        HG_HIP_TRY(hipMemcpyAsync(v2_final, v2o, sizeof(int32_t) * ES, hipMemcpyDeviceToDevice, s));
     }
+    // both edge ids and weights asked for: the weights through the edge ids
+    if (want_eid && weighted && ES > 0)
+      HG_LAUNCH("build_csr_w", k_gather_w, dim3(grid_for(ES)), dim3(kBT), 0, s, (const int32_t*)out->csr_eid,
+                g->edge_w, ES, out->csr_w);
     HG_TRY(fill_i32(w.rowcnt, 0, NQ + 1, s));
     if (ES > 0)
       HG_LAUNCH("build_row_count", k_row_count, dim3((unsigned)cdiv(ES, kRCChunk)), dim3(kBT), 0, s,
@@ -1318,11 +1343,16 @@ extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg
   {
     uint32_t* ko;
     int32_t *v1o, *v2o;
-    // the CSR keys stay where the CSR sort left them
-    HG_TRY(radix_sort_pairs(w.kcsc, csr_keys == w.kalt ? w.kcsr : w.kalt, w.vdst, w.alt3, nullptr, nullptr, ES,
-                            bits, w.scratch, s, &ko, &v1o, &v2o, out->csc_row, nullptr));
-    if (ES > 0 && v1o != out->csc_row)
+    // the CSR keys stay where the CSR sort left them; a weighted graph's
+    // weights ride along into csc_scale, which k_csc_scale divides in place
+    int32_t* wscale = reinterpret_cast<int32_t*>(out->csc_scale);
+    HG_TRY(radix_sort_pairs(w.kcsc, csr_keys == w.kalt ? w.kcsr : w.kalt, w.vdst, w.alt3, weighted ? w.vw2 : nullptr,
+                            weighted ? w.walt : nullptr, ES, bits, w.scratch, s, &ko, &v1o, &v2o, out->csc_row,
+                            weighted ? wscale : nullptr));
+    if (ES > 0 && v1o != out->csc_row) {
       HG_HIP_TRY(hipMemcpyAsync(out->csc_row, v1o, sizeof(int32_t) * ES, hipMemcpyDeviceToDevice, s));
+      if (weighted) HG_HIP_TRY(hipMemcpyAsync(wscale, v2o, sizeof(int32_t) * ES, hipMemcpyDeviceToDevice, s));
+    }
     HG_TRY(fill_i32(w.rowcnt, 0, NQ + 1, s));
     if (ES > 0)
       HG_LAUNCH("build_row_count", k_row_count, dim3((unsigned)cdiv(ES, kRCChunk)), dim3(kBT), 0, s,
@@ -1331,7 +1361,7 @@ extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg
     if (ES > 0)
       HG_LAUNCH("build_csc_scale", k_csc_scale, dim3(grid_for(ES)), dim3(kBT), 0, s,
                 (const uint32_t*)ko, (const int32_t*)out->csc_row, (const uint8_t*)w.digit,
-                (const int32_t*)out->csr_ptr, ES, (int32_t)R, out->csc_scale);
+                (const int32_t*)out->csr_ptr, ES, (int32_t)R, weighted ? 1 : 0, out->csc_scale);
   }
   // 8. plan: active-source lists and backward work items
   PlanLayout pl(N, E, R);
@@ -1404,5 +1434,6 @@ extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg
   out->plan_fwd_heavy = hc[C_FHEAVY];
   out->plan_fwd_parts = hc[C_FPARTS];
   out->plan_slot_rows = row_layout(NQ, hc[C_ASLOTS]) ? NQ : hc[C_ASLOTS];
+  out->weighted = weighted ? 1 : 0;
   return HG_OK;
 }

@@ -40,6 +40,7 @@ int validate_hgt(const hg_subgraph* s, const hg_hgt_desc* L) {
     return fail(HG_ERR_ARG, "relu, residual and lean must be 0 or 1");
   if (s->n_rel < 1 || s->n_ntype < 1) return fail(HG_ERR_ARG, "subgraph has no relations or node types");
   if (s->n_sub < 0 || s->e_sub < 0) return fail(HG_ERR_ARG, "subgraph sizes are negative");
+  if (s->weighted) return fail(HG_ERR_UNSUPPORTED, "attention layer: edge weights are not supported");
   return HG_OK;
 }
 

@@ -4,7 +4,8 @@
 // Graph Transformer" paragraph in relation-typed mean form):
 //   (c) MFMA transforms  Y_self = H W_self[t] + b[t]   per contiguous type range
 //                        Y[slot(i,r)] = H_i W_r         for i in S_r (active sources)
-//   (b) SpMM             z_j = Y_self[j] + sum_{edges i->j of relation r} Y[slot(i,r)] / deg_r(j)
+//   (b) SpMM             z_j = Y_self[j] + sum_{edges i->j of relation r} w_ij Y[slot(i,r)] / deg_r(j)
+//                        (w_ij = 1 without edge weights)
 //                        h'_j = ReLU(z_j) + h_j, ReLU mask saved as bits
 // Y holds one row per active (source, relation) pair, A rows in all (slots
 // numbered in CSC row order; the plan gives the slot of every CSR entry), or
@@ -44,8 +45,9 @@ namespace {
 template <int D, class T>
 __device__ __forceinline__ void fwd_gather(int64_t rb, int32_t R, int32_t p0, int32_t pe, int32_t beg, int32_t end,
                                            const int32_t* __restrict__ csr_ptr, const int32_t* __restrict__ csr_col,
-                                           const int32_t* __restrict__ csr_slot, const T* __restrict__ Y, int l,
-                                           int slot, int c0, float (&acc)[Elt<T>::EL]) {
+                                           const int32_t* __restrict__ csr_slot, const float* __restrict__ csr_w,
+                                           const T* __restrict__ Y, int l, int slot, int c0,
+                                           float (&acc)[Elt<T>::EL]) {
   constexpr int EL = Elt<T>::EL;
   constexpr int EPW = 64 / (D / EL);
   constexpr int U = 4;
@@ -65,7 +67,7 @@ __device__ __forceinline__ void fwd_gather(int64_t rb, int32_t R, int32_t p0, in
         }
       }
       rowi = csr_slot ? csr_slot[pos] : csr_col[pos] * R + r;
-      wgt = 1.0f / (float)(hi - lo);
+      wgt = (csr_w ? csr_w[pos] : 1.0f) / (float)(hi - lo);
     }
     const int cnt = (end - base) < 64 ? (end - base) : 64;
     for (int e = 0; e < cnt; e += EPW * U) {
@@ -124,6 +126,7 @@ template <int D, class T>
 __global__ void __launch_bounds__(256, (sizeof(T) == 2 || D <= 128) ? 8 : 4) k_spmm_fwd(int64_t n_sub, int32_t R, const int32_t* __restrict__ csr_ptr,
                                                   const int32_t* __restrict__ csr_col,
                                                   const int32_t* __restrict__ csr_slot,
+                                                  const float* __restrict__ csr_w,
                                                   const T* __restrict__ Y, const T* __restrict__ Yself,
                                                   const T* __restrict__ Hin, T* __restrict__ Hout,
                                                   uint32_t* __restrict__ mask, int relu, int residual) {
@@ -144,7 +147,7 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 2 || D <= 128) ? 8 : 4) k_s
     float acc[EL];
 #pragma unroll
     for (int q = 0; q < EL; ++q) acc[q] = 0.f;
-    fwd_gather<D, T>(rb, R, p0, pe, p0, pe, csr_ptr, csr_col, csr_slot, Y, l, slot, c0, acc);
+    fwd_gather<D, T>(rb, R, p0, pe, p0, pe, csr_ptr, csr_col, csr_slot, csr_w, Y, l, slot, c0, acc);
 #pragma unroll
     for (int o = LPR; o < 64; o <<= 1)
 #pragma unroll
@@ -159,7 +162,8 @@ template <int D, class T>
 __global__ void __launch_bounds__(256) k_spmm_fwd_part(int64_t n_items, const int4* __restrict__ items, int32_t R,
                                                        const int32_t* __restrict__ csr_ptr,
                                                        const int32_t* __restrict__ csr_col,
-                                                       const int32_t* __restrict__ csr_slot, const T* __restrict__ Y,
+                                                       const int32_t* __restrict__ csr_slot,
+                                                       const float* __restrict__ csr_w, const T* __restrict__ Y,
                                                        float* __restrict__ part) {
   constexpr int EL = Elt<T>::EL;
   constexpr int LPR = D / EL;
@@ -174,8 +178,8 @@ __global__ void __launch_bounds__(256) k_spmm_fwd_part(int64_t n_items, const in
     float acc[EL];
 #pragma unroll
     for (int q = 0; q < EL; ++q) acc[q] = 0.f;
-    fwd_gather<D, T>(rb, R, csr_ptr[rb], csr_ptr[rb + R], item.y, item.z, csr_ptr, csr_col, csr_slot, Y, l, slot, c0,
-                     acc);
+    fwd_gather<D, T>(rb, R, csr_ptr[rb], csr_ptr[rb + R], item.y, item.z, csr_ptr, csr_col, csr_slot, csr_w, Y, l,
+                     slot, c0, acc);
 #pragma unroll
     for (int o = LPR; o < 64; o <<= 1)
 #pragma unroll
@@ -526,15 +530,17 @@ int layer_fwd_impl(const hg_subgraph* s, const hg_layer_desc* L, const T* Hin, c
     HG_TRY((transform<D, T, false>("gemm_fwd_rel", n, W_rel + (int64_t)r * D * D, la, ep, st)));
     off += n;
   }
-  // (b) aggregation + epilogue; long destination rows by chunks
+  // (b) aggregation + epilogue; long destination rows by chunks; the edge
+  // weights of a weighted graph multiply the messages
+  const float* csr_w = s->weighted ? s->csr_w : nullptr;
   if (s->n_sub > 0)
     HG_LAUNCH("spmm_fwd", (k_spmm_fwd<D, T>), dim3(wave_grid(s->n_sub)), dim3(256), 0, st, s->n_sub, R,
-              (const int32_t*)s->csr_ptr, (const int32_t*)s->csr_col, pv.csr_slot, (const T*)w.Y, (const T*)w.Yself, Hin,
+              (const int32_t*)s->csr_ptr, (const int32_t*)s->csr_col, pv.csr_slot, csr_w, (const T*)w.Y, (const T*)w.Yself, Hin,
               Hout, mask, L->relu, L->residual);
   if (s->plan_fwd_heavy > 0) {
     HG_LAUNCH("spmm_fwd_part", (k_spmm_fwd_part<D, T>), dim3(wave_grid(s->plan_fwd_parts)), dim3(256), 0, st,
               (int64_t)s->plan_fwd_parts, pv.fwd_items, R, (const int32_t*)s->csr_ptr, (const int32_t*)s->csr_col,
-              pv.csr_slot, (const T*)w.Y, w.part);
+              pv.csr_slot, csr_w, (const T*)w.Y, w.part);
     HG_LAUNCH("spmm_fwd_merge", (k_spmm_fwd_merge<D, T>), dim3(wave_grid(s->plan_fwd_heavy)), dim3(256), 0, st,
               (int64_t)s->plan_fwd_heavy, pv.fwd_heavy, (const float*)w.part, (const T*)w.Yself, Hin, Hout, mask,
               L->relu, L->residual);

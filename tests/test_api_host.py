@@ -63,7 +63,6 @@ def _ov(**kw):
     (dict(n_nodes=2**30, n_rel=4), {}, api.HG_ERR_UNSUPPORTED),
     (dict(src=None), {}, api.HG_ERR_ARG),
     (dict(part=None), {}, api.HG_ERR_ARG),
-    (dict(edge_w=C.c_void_p(0x1000)), {}, api.HG_ERR_UNSUPPORTED),
     ({}, dict(budget_M=-1), api.HG_ERR_ARG),
     ({}, dict(key=7), api.HG_ERR_ARG),
     ({}, dict(key_dir=1), api.HG_ERR_UNSUPPORTED),
@@ -75,6 +74,22 @@ def test_build_validation(L, gkw, okw, code):
     assert L.hg_build_csr_workspace_size(C.byref(g), C.byref(o)) == 0
     assert L.hg_build_csr(C.byref(g), C.byref(o), C.byref(s), None, 0, None) == code
     assert len(api.last_error_detail()) > 0
+
+
+def test_weighted_build_needs_the_weight_output(L):
+    """Edge weights are accepted, and then the build writes the weight of
+    every CSR entry: a missing csr_w output is refused before any device work."""
+    fake = C.c_void_p(0x1000)
+    g, o = _graph(edge_w=fake), _ov()
+    assert L.hg_build_csr_workspace_size(C.byref(g), C.byref(o)) > \
+        L.hg_build_csr_workspace_size(C.byref(_graph()), C.byref(o))
+    s = api.SubgraphStruct()
+    for name in ("local2global", "global2local", "type_off", "overlap", "overlap_home", "overlap_rel", "csr_ptr",
+                 "csr_col", "csc_ptr", "csc_row", "csc_scale", "plan"):
+        setattr(s, name, fake)
+    s.plan_bytes = api.hg_plan_size(10, 5, 2)
+    assert L.hg_build_csr(C.byref(g), C.byref(o), C.byref(s), None, 0, None) == api.HG_ERR_ARG
+    assert "csr_w" in api.last_error_detail()
 
 
 def test_build_capacity_checks(L):
