@@ -162,8 +162,9 @@ int hg_node_keys(const hg_graph_desc* g, int32_t key, int32_t* keys, void* ws, s
  * Algorithm 1).  Local ids order the nodes by (node type, global id), so each
  * type is a contiguous range [type_off[t], type_off[t+1]).  Row (v, r) of the
  * CSR holds the in-edges of relation r of local node v (index v*n_rel + r),
- * entries in ascending original edge index; the CSC likewise holds
- * out-edges.  csc_scale[p] = w / deg_r(csc_row[p]), the mean-aggregation
+ * entries in ascending original edge index; row (v, r) of the CSC holds the
+ * out-edges of relation r of v, entries in ascending (destination, original
+ * edge index).  csc_scale[p] = w / deg_r(csc_row[p]), the mean-aggregation
  * weight (w = the entry's edge weight, 1 without weights), as a correctly
  * rounded float32 quotient.
  *

@@ -15,7 +15,8 @@ construction loop of Algorithm 1:
 4. the overlapping node set V_k u C_{k,M} (union equation) and its induced
    subgraph G[V~_k], relabelled in (node type, global id) order;
 5. per-relation CSR (destination-major) and CSC (source-major) of the induced
-   subgraph, entries of a row in ascending original edge index, and the CSC
+   subgraph, entries of a CSR row in ascending original edge index, entries
+   of a CSC row in ascending (destination, original edge index), and the CSC
    scale 1/deg_r(destination) as a float32 quotient (w_ij/deg_r(destination)
    for weighted edges, the message weight over the in-edge count, with the
    weight of every CSR entry);
@@ -183,7 +184,7 @@ def build(src, dst, rel, ntype, part, k: int, n_rel: int, n_ntype: int,
     csr_eid = eid[p]
 
     key_csc = src_l * r_count + rel_l
-    q = np.argsort(key_csc, kind="stable")
+    q = np.lexsort((eid, dst_l, key_csc))   # row, then destination, then edge index
     csc_counts = np.bincount(key_csc, minlength=nrows)
     csc_ptr = np.concatenate([[0], np.cumsum(csc_counts)])
     csc_row = dst_l[q]

@@ -85,6 +85,7 @@ def _brute_build(src, dst, rel, ntype, part, k, R, T, budget, key, theta, seed, 
     for eid, s, d, r in edges:
         csr_rows[d * R + r].append((s, eid))
         csc_rows[s * R + r].append((d, eid))
+    csc_rows = [sorted(row) for row in csc_rows]  # a CSC row by (destination, edge index)
     base_rel = {}
     for v in chosen:
         first = min(i for i in range(e) if (src[i] == v and dst[i] in base) or (dst[i] == v and src[i] in base))
