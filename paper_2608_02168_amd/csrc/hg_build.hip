@@ -221,6 +221,7 @@ inline unsigned agg_grid(int64_t n, int per_cu = 3) {
 // (64 KB, two blocks per compute unit) keeps far more of them than the
 // 2^11-slot tables of the passes that hold several tables at once.
 constexpr int kDegBits = 13, kDegSlots = 1 << kDegBits, kDegPerCu = 2;
+constexpr int kEpItems = 4;
 
 // Range checks and the candidates C_k: every node outside V_k joined to V_k
 // by an edge gets first[v] < n_edges -- in a dense build the smallest index of
@@ -248,21 +249,46 @@ __global__ void __launch_bounds__(kAggBT) k_edges_pass(const int32_t* __restrict
     fd.init();
   }
   __syncthreads();
-  GRID_STRIDE(e, n_edges) {
-    const int32_t s = src[e], d = dst[e];
-    const int r = rel[e];
-    if (s < 0 || s >= n_nodes || d < 0 || d >= n_nodes || r >= n_rel) {
-      atomicOr(&cnt[C_ERR], 1);
-      continue;
+  // kEpItems edges per thread and round (strided by the grid), every load of
+  // a round issued before the lookups that depend on it
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t e0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e0 < n_edges; e0 += kEpItems * stride) {
+    int32_t sv[kEpItems], dv[kEpItems];
+    bool ok[kEpItems], ps[kEpItems], pd[kEpItems];
+#pragma unroll
+    for (int j = 0; j < kEpItems; ++j) {
+      const int64_t e = e0 + j * stride;
+      sv[j] = dv[j] = 0;
+      ok[j] = false;
+      if (e < n_edges) {
+        sv[j] = src[e];
+        dv[j] = dst[e];
+        ok[j] = rel[e] < n_rel;
+      }
     }
-    const bool ps = bit_of(base_bits, s), pd = bit_of(base_bits, d);
-    if (count_all || (count_out && !ps)) deg.put((uint32_t)s, 1, outdeg);
-    if (exact) {
-      if (pd && !ps) fs.put((uint32_t)s, (int32_t)e, first);
-      if (ps && !pd) fd.put((uint32_t)d, (int32_t)e, first);
-    } else {
-      if (pd && !ps && first[s] != 0) first[s] = 0;
-      if (ps && !pd && first[d] != 0) first[d] = 0;
+#pragma unroll
+    for (int j = 0; j < kEpItems; ++j) {
+      const int64_t e = e0 + j * stride;
+      if (e < n_edges && !(ok[j] && sv[j] >= 0 && sv[j] < n_nodes && dv[j] >= 0 && dv[j] < n_nodes)) {
+        atomicOr(&cnt[C_ERR], 1);
+        ok[j] = false;
+      }
+      ps[j] = ok[j] && bit_of(base_bits, sv[j]);
+      pd[j] = ok[j] && bit_of(base_bits, dv[j]);
+    }
+#pragma unroll
+    for (int j = 0; j < kEpItems; ++j) {
+      if (!ok[j]) continue;
+      const int64_t e = e0 + j * stride;
+      const int32_t s = sv[j], d = dv[j];
+      if (count_all || (count_out && !ps[j])) deg.put((uint32_t)s, 1, outdeg);
+      if (exact) {
+        if (pd[j] && !ps[j]) fs.put((uint32_t)s, (int32_t)e, first);
+        if (ps[j] && !pd[j]) fd.put((uint32_t)d, (int32_t)e, first);
+      } else {
+        if (pd[j] && !ps[j] && first[s] != 0) first[s] = 0;
+        if (ps[j] && !pd[j] && first[d] != 0) first[d] = 0;
+      }
     }
   }
   __syncthreads();
@@ -506,19 +532,19 @@ __global__ void k_overlap_fill(const int32_t* __restrict__ l2g, const int32_t* _
 }
 
 // ---- induced edges from a rank table (node types 0 and 1) ------------------
-// Local ids order the node set by (type, gid).  For 64 consecutive gids an
+// Local ids order the node set by (type, gid).  For 32 consecutive gids an
 // entry holds the masks of their type-0 and type-1 members and the number of
-// type-0 and type-1 members before them (32 bytes per 64 nodes, 5 MB for 10M
+// type-0 and type-1 members before them (16 bytes per 32 nodes, 5 MB for 10M
 // nodes, where global2local takes 40 MB), so
 //   local(v) = pre0 + popc(mem0 below v)                          (type 0)
 //   local(v) = type_off[1] + pre1 + popc(mem1 below v)            (type 1)
-// and -1 outside the node set: one 32-byte lookup per endpoint.
+// and -1 outside the node set: one 16-byte load per endpoint.
 struct __align__(16) RankEnt {
-  uint64_t mem0, mem1;
-  uint32_t pre0, pre1, pad0, pad1;
+  uint32_t mem0, mem1, pre0, pre1;
 };
+constexpr int kRankGroup = 32;
 
-// Masks and member counts of every 64-node group (one wave per group).
+// Masks and member counts of every 32-node group (one wave per two groups).
 __global__ void __launch_bounds__(kBT) k_rank_bits(const int32_t* __restrict__ part, int32_t k,
                                                    const uint8_t* __restrict__ sel, const uint8_t* __restrict__ ntype,
                                                    int64_t n, RankEnt* __restrict__ rt, int32_t* __restrict__ c0,
@@ -526,13 +552,15 @@ __global__ void __launch_bounds__(kBT) k_rank_bits(const int32_t* __restrict__ p
   GRID_STRIDE(v, cdiv_dev(n, 64) * 64) {
     const bool in = v < n && (part[v] == k || sel[v]);
     const bool t1 = in && ntype[v] == 1;
-    const uint64_t m = __ballot(in), m1 = __ballot(t1);
-    if ((threadIdx.x & 63) == 0) {
-      const int64_t b = v >> 6;
-      rt[b].mem0 = m & ~m1;
-      rt[b].mem1 = m1;
-      c0[b] = (int32_t)__popcll(m & ~m1);
-      c1[b] = (int32_t)__popcll(m1);
+    const uint64_t m = __ballot(in), m1 = __ballot(t1), m0 = m & ~m1;
+    const int l = threadIdx.x & 63;
+    if (l < 2) {  // lane h writes group 2 (v / 64) + h, the half h of the wave's 64 nodes
+      const int64_t b = (v >> 6) * 2 + l;
+      const uint32_t g0 = (uint32_t)(m0 >> (32 * l)), g1 = (uint32_t)(m1 >> (32 * l));
+      rt[b].mem0 = g0;
+      rt[b].mem1 = g1;
+      c0[b] = __popc(g0);
+      c1[b] = __popc(g1);
     }
   }
 }
@@ -546,12 +574,10 @@ __global__ void k_rank_pack(const int32_t* __restrict__ pre0, const int32_t* __r
 }
 
 __device__ __forceinline__ int32_t rank_local(const RankEnt* __restrict__ rt, int32_t off1, int32_t v) {
-  const uint4* p = reinterpret_cast<const uint4*>(rt + (v >> 6));
-  const uint4 a = p[0], b = p[1];
-  const uint64_t mem0 = (uint64_t)a.x | ((uint64_t)a.y << 32), mem1 = (uint64_t)a.z | ((uint64_t)a.w << 32);
-  const uint64_t bit = 1ull << (v & 63), below = bit - 1ull;
-  if (mem0 & bit) return (int32_t)b.x + __popcll(mem0 & below);
-  if (mem1 & bit) return off1 + (int32_t)b.y + __popcll(mem1 & below);
+  const uint4 a = *reinterpret_cast<const uint4*>(rt + (v >> 5));
+  const uint32_t bit = 1u << (v & 31), below = bit - 1u;
+  if (a.x & bit) return (int32_t)a.z + __popc(a.x & below);
+  if (a.y & bit) return off1 + (int32_t)a.w + __popc(a.y & below);
   return -1;
 }
 
@@ -611,10 +637,8 @@ __global__ void __launch_bounds__(kBT) k_edge_ids(const int32_t* __restrict__ sr
 __global__ void __launch_bounds__(kBT) k_edge_emit(const int32_t* __restrict__ sl, const int32_t* __restrict__ dl,
                                                    const uint8_t* __restrict__ rel, int64_t n_edges, int32_t n_rel,
                                                    const int32_t* __restrict__ tile_off, uint32_t* __restrict__ kcsr,
-                                                   uint32_t* __restrict__ kcsc, int32_t* __restrict__ vsrc,
-                                                   int32_t* __restrict__ vdst, int32_t* __restrict__ veid,
-                                                   const float* __restrict__ edge_w, int32_t* __restrict__ vw1,
-                                                   int32_t* __restrict__ vw2) {
+                                                   int32_t* __restrict__ vsrc, int32_t* __restrict__ veid,
+                                                   const float* __restrict__ edge_w, int32_t* __restrict__ vw) {
   constexpr int NW = kBT / 64;
   __shared__ int32_t cnt[kERounds * NW];
   const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
@@ -649,13 +673,10 @@ __global__ void __launch_bounds__(kBT) k_edge_emit(const int32_t* __restrict__ s
     if ((bal[j] >> l) & 1ull) {
       const int64_t e = base + (int64_t)j * kBT + threadIdx.x;
       const int32_t p = t0 + cnt[j * NW + w] + (int32_t)__popcll(bal[j] & lt);
-      const uint32_t r = rel[e];
-      kcsr[p] = (uint32_t)b[j] * (uint32_t)n_rel + r;
-      kcsc[p] = (uint32_t)a[j] * (uint32_t)n_rel + r;
+      kcsr[p] = (uint32_t)b[j] * (uint32_t)n_rel + (uint32_t)rel[e];
       vsrc[p] = a[j];
-      vdst[p] = b[j];
-      veid[p] = (int32_t)e;
-      if (edge_w) vw1[p] = vw2[p] = __float_as_int(edge_w[e]);
+      if (veid) veid[p] = (int32_t)e;
+      if (vw) vw[p] = __float_as_int(edge_w[e]);
     }
   }
 }
@@ -689,21 +710,15 @@ __global__ void k_edge_keep(const int32_t* __restrict__ src, const int32_t* __re
 __global__ void k_edge_compact(const int32_t* __restrict__ src, const int32_t* __restrict__ dst,
                                const int32_t* __restrict__ g2l, const uint8_t* __restrict__ rel,
                                const int32_t* __restrict__ pos, int64_t n_edges, int32_t n_rel,
-                               uint32_t* __restrict__ kcsr, uint32_t* __restrict__ kcsc, int32_t* __restrict__ vsrc,
-                               int32_t* __restrict__ vdst, int32_t* __restrict__ veid,
-                               const float* __restrict__ edge_w, int32_t* __restrict__ vw1,
-                               int32_t* __restrict__ vw2) {
+                               uint32_t* __restrict__ kcsr, int32_t* __restrict__ vsrc, int32_t* __restrict__ veid,
+                               const float* __restrict__ edge_w, int32_t* __restrict__ vw) {
   GRID_STRIDE(e, n_edges) {
     const int32_t p = pos[e];
     if (pos[e + 1] != p) {
-      const int32_t s = g2l[src[e]], d = g2l[dst[e]];
-      const uint32_t r = rel[e];
-      kcsr[p] = (uint32_t)d * (uint32_t)n_rel + r;
-      kcsc[p] = (uint32_t)s * (uint32_t)n_rel + r;
-      vsrc[p] = s;
-      vdst[p] = d;
-      veid[p] = (int32_t)e;
-      if (edge_w) vw1[p] = vw2[p] = __float_as_int(edge_w[e]);
+      kcsr[p] = (uint32_t)g2l[dst[e]] * (uint32_t)n_rel + (uint32_t)rel[e];
+      vsrc[p] = g2l[src[e]];
+      if (veid) veid[p] = (int32_t)e;
+      if (vw) vw[p] = __float_as_int(edge_w[e]);
     }
   }
 }
@@ -769,27 +784,52 @@ __global__ void __launch_bounds__(kBT) k_row_count(const uint32_t* __restrict__ 
   }
 }
 
-// In-degree of every CSR row (dst, r) as one byte, 255 standing for "255 or
-// more": the CSC scales look their rows up at random, in a table a quarter
-// the size of csr_ptr (and a quarter of the lines).
-__global__ void k_deg_bytes(const int32_t* __restrict__ rowcnt, int64_t nq, uint8_t* __restrict__ deg8) {
-  GRID_STRIDE(q, nq) {
-    const int32_t c = rowcnt[q];
-    deg8[q] = (uint8_t)(c < 255 ? c : 255);
+// The CSC sort's input, taken from the CSR in its order: the key (source, r)
+// = csr_col[p] * R + r and, as the value, the destination with the in-degree
+// of its row, read from csr_ptr while the row is at hand (rows arrive in
+// order).  packed: value = destination | min(deg, 255) << 24 (destinations
+// below 2^24), which the sort's last pass unpacks into csc_row and the scale;
+// else the destination and, as a second value, the scale w / deg itself (a
+// correctly rounded float32 quotient; w = the entry's weight, or 1).  A
+// stable sort of this input by its key lists a CSC row by (destination,
+// original edge index).  Each thread takes kCiItems entries, one per round of
+// the block, all loads of a round issued before any store.
+constexpr int kCiItems = 4;
+__global__ void __launch_bounds__(kBT) k_csc_input(const uint32_t* __restrict__ kcsr,
+                                                   const int32_t* __restrict__ csr_col,
+                                                   const int32_t* __restrict__ csr_ptr,
+                                                   const float* __restrict__ csr_w, int64_t n, int32_t n_rel,
+                                                   int packed, uint32_t* __restrict__ kcsc, int32_t* __restrict__ v1,
+                                                   int32_t* __restrict__ v2) {
+  const int64_t base = (int64_t)blockIdx.x * (kBT * kCiItems) + threadIdx.x;
+  uint32_t key[kCiItems];
+  int32_t col[kCiItems], lo[kCiItems], hi[kCiItems];
+#pragma unroll
+  for (int j = 0; j < kCiItems; ++j) {
+    const int64_t p = base + (int64_t)j * kBT;
+    key[j] = p < n ? kcsr[p] : 0u;
+    col[j] = p < n ? csr_col[p] : 0;
   }
-}
-
-// csc_scale = w / deg_r(destination), an IEEE float32 quotient; w = 1, or the
-// entry's edge weight already sorted into scale (weighted graphs).
-__global__ void k_csc_scale(const uint32_t* __restrict__ kcsc, const int32_t* __restrict__ csc_row,
-                            const uint8_t* __restrict__ deg8, const int32_t* __restrict__ csr_ptr, int64_t n,
-                            int32_t n_rel, int weighted, float* __restrict__ scale) {
-  GRID_STRIDE(p, n) {
-    const int64_t row = (int64_t)csc_row[p] * n_rel + (int64_t)(kcsc[p] % (uint32_t)n_rel);
-    int32_t deg = deg8[row];
-    if (deg == 255) deg = csr_ptr[row + 1] - csr_ptr[row];
-    const float w = weighted ? scale[p] : 1.0f;
-    scale[p] = w / (float)deg;
+#pragma unroll
+  for (int j = 0; j < kCiItems; ++j) {
+    const int64_t p = base + (int64_t)j * kBT;
+    lo[j] = p < n ? csr_ptr[key[j]] : 0;
+    hi[j] = p < n ? csr_ptr[key[j] + 1] : 1;
+  }
+#pragma unroll
+  for (int j = 0; j < kCiItems; ++j) {
+    const int64_t p = base + (int64_t)j * kBT;
+    if (p < n) {
+      const uint32_t dst = key[j] / (uint32_t)n_rel, r = key[j] - dst * (uint32_t)n_rel;
+      const int32_t deg = hi[j] - lo[j];
+      kcsc[p] = (uint32_t)col[j] * (uint32_t)n_rel + r;
+      if (packed) {
+        v1[p] = (int32_t)(dst | ((uint32_t)(deg < 255 ? deg : 255) << 24));
+      } else {
+        v1[p] = (int32_t)dst;
+        v2[p] = __float_as_int((csr_w ? csr_w[p] : 1.0f) / (float)deg);
+      }
+    }
   }
 }
 
@@ -927,6 +967,10 @@ __global__ void k_csr_slot(const int32_t* __restrict__ csr_col, const uint32_t* 
   }
 }
 
+// The CSC sort packs destination and row degree into one value while the
+// destinations fit in 24 bits.
+constexpr int64_t kPackedMaxNodes = (int64_t)1 << 24;
+
 int bits_for(int64_t nvals) {
   int b = 0;
   while (b < 32 && ((int64_t)1 << b) < nvals) ++b;
@@ -941,7 +985,8 @@ struct BuildWs {
   SelectState* st;
   int32_t *keep, *vsrc, *vdst, *veid, *alt1, *alt2, *alt3, *rowcnt, *q_items, *q_heavy, *q_parts,
       *q_src, *scratch, *bcnt;
-  int32_t *vw1, *vw2, *walt;  // weighted graphs: edge weights (float bits) in edge order for each sort
+  int32_t* vw;                // weighted graphs: edge weights (float bits) of the kept edges in edge order
+  int32_t *vsc, *vsc_alt;     // unpacked CSC sort: the scales (float bits) and their ping-pong buffer
   uint32_t *kcsr, *kcsc, *kalt, *bbits, *mbits;
   RankEnt* rt;
   int32_t *rc0, *rc1, *tile_cnt;
@@ -961,9 +1006,10 @@ struct BuildWs {
     sel = a.template take<uint8_t>(N);
     bbits = a.template take<uint32_t>(N / 32 + 2);
     mbits = a.template take<uint32_t>(2 * (N / 64 + 1));
-    rt = a.template take<RankEnt>(N / 64 + 1);
-    rc0 = a.template take<int32_t>(N / 64 + 1);
-    rc1 = a.template take<int32_t>(N / 64 + 1);
+    // rank groups: cdiv(N, 64) * 2 <= N / 32 + 2
+    rt = a.template take<RankEnt>(N / kRankGroup + 2);
+    rc0 = a.template take<int32_t>(N / kRankGroup + 2);
+    rc1 = a.template take<int32_t>(N / kRankGroup + 2);
     tile_cnt = a.template take<int32_t>(E / kETile + 2);
     digit = a.template take<uint8_t>(NQ > N ? NQ : N);
     st = a.template take<SelectState>(1);
@@ -982,9 +1028,10 @@ struct BuildWs {
     q_heavy = a.template take<int32_t>(NQ);
     q_parts = a.template take<int32_t>(NQ);
     q_src = a.template take<int32_t>(NQ);
-    vw1 = a.template take<int32_t>(weighted ? E : 0);
-    vw2 = a.template take<int32_t>(weighted ? E : 0);
-    walt = a.template take<int32_t>(weighted ? E : 0);
+    vw = a.template take<int32_t>(weighted ? E : 0);
+    const bool unpacked = weighted || N >= kPackedMaxNodes;
+    vsc = a.template take<int32_t>(unpacked ? E : 0);
+    vsc_alt = a.template take<int32_t>(unpacked ? E : 0);
     int64_t sc = scan_scratch_elems(E + N + NQ + 1);
     int64_t rs = radix_scratch_elems(E > NQ ? E : NQ);
     scratch = a.template take<int32_t>(sc > rs ? sc : rs);
@@ -1170,6 +1217,7 @@ extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg
       (g->n_edges > 0 && (!out->csr_col || !out->csc_row || !out->csc_scale)))
     return fail(HG_ERR_ARG, "null output array");
   const bool weighted = g->edge_w != nullptr;
+  const bool want_eid = out->csr_eid != nullptr;
   if (weighted && g->n_edges > 0 && !out->csr_w) return fail(HG_ERR_ARG, "a weighted graph needs the csr_w output");
   const int64_t N = g->n_nodes, E = g->n_edges, R = g->n_rel, T = g->n_ntype;
   const size_t need_plan = hg_plan_size(N, E, (int32_t)R);
@@ -1260,9 +1308,11 @@ extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg
     HG_HIP_TRY(hipMemcpyAsync(&nb_host, w.cnt + C_BASE, sizeof(int32_t), hipMemcpyDeviceToHost, s));
     HG_HIP_TRY(hipStreamSynchronize(s));
     const bool dense = dense_build(nb_host, o->budget_M, N);
+    // the CSR sort carries the edge id if asked for, else a weighted graph's weight
+    const bool emit_w = weighted && !want_eid;
     if (T <= 2) {
-      const int64_t nb = N / 64 + 1, ntiles = cdiv(E, kETile);
-      HG_LAUNCH("build_rank_bits", k_rank_bits, dim3(grid_for(nb * 64)), dim3(kBT), 0, s, g->part, g->k,
+      const int64_t nb = cdiv(N, 64) * 2, ntiles = cdiv(E, kETile);
+      HG_LAUNCH("build_rank_bits", k_rank_bits, dim3(grid_for(nb * kRankGroup)), dim3(kBT), 0, s, g->part, g->k,
                 (const uint8_t*)w.sel, g->ntype, N, w.rt, w.rc0, w.rc1);
       HG_TRY(scan_exclusive_i32(w.rc0, w.rc0, nb, nullptr, w.scratch, s));
       HG_TRY(scan_exclusive_i32(w.rc1, w.rc1, nb, nullptr, w.scratch, s));
@@ -1274,8 +1324,8 @@ extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg
                 g->t_cut, E, dense ? 0 : 1, w.alt1, w.alt2, w.tile_cnt, w.first);
       HG_TRY(scan_exclusive_i32(w.tile_cnt, w.tile_cnt, ntiles, w.cnt + C_ESUB, w.scratch, s));
       HG_LAUNCH("build_edge_compact", k_edge_emit, dim3((unsigned)ntiles), dim3(kBT), 0, s, (const int32_t*)w.alt1,
-                (const int32_t*)w.alt2, g->rel, E, (int32_t)R, (const int32_t*)w.tile_cnt, w.kcsr, w.kcsc, w.vsrc,
-                w.vdst, w.veid, g->edge_w, w.vw1, w.vw2);
+                (const int32_t*)w.alt2, g->rel, E, (int32_t)R, (const int32_t*)w.tile_cnt, w.kcsr, w.vsrc,
+                want_eid ? w.veid : nullptr, g->edge_w, emit_w ? w.vw : nullptr);
     } else {
       // more than two node types: local ids from global2local, membership from a bitmap
       HG_LAUNCH("build_member_bits", k_member_bits, dim3(gB), dim3(kBT), 0, s, g->part, g->k,
@@ -1286,8 +1336,8 @@ extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg
       HG_TRY(fill_i32(w.keep + E, 0, 1, s));
       HG_TRY(scan_exclusive_i32(w.keep, w.keep, E + 1, w.cnt + C_ESUB, w.scratch, s));
       HG_LAUNCH("build_edge_compact", k_edge_compact, dim3(gE), dim3(kBT), 0, s, g->src, g->dst,
-                (const int32_t*)out->global2local, g->rel, (const int32_t*)w.keep, E, (int32_t)R, w.kcsr, w.kcsc,
-                w.vsrc, w.vdst, w.veid, g->edge_w, w.vw1, w.vw2);
+                (const int32_t*)out->global2local, g->rel, (const int32_t*)w.keep, E, (int32_t)R, w.kcsr, w.vsrc,
+                want_eid ? w.veid : nullptr, g->edge_w, emit_w ? w.vw : nullptr);
     }
   } else {
     HG_TRY(fill_i32(w.cnt + C_ESUB, 0, 1, s));
@@ -1308,15 +1358,14 @@ extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg
   HG_HIP_TRY(hipStreamSynchronize(s));
   const int64_t NS = hc[C_NSUB], ES = hc[C_ESUB];
   const int64_t NQ = NS * R;
-  // 7. CSR: stable sort by dst*R + r; CSC: stable sort by src*R + r
+  // 7. CSR: stable sort by dst*R + r; CSC: stable sort of the CSR-ordered entries by src*R + r
   const int bits = bits_for(NQ);
   uint32_t* csr_keys = w.kcsr;  // the CSR's sorted keys, kept for the slots of its entries
   {
     uint32_t* ko;
     int32_t *v1o, *v2o;
-    const bool want_eid = out->csr_eid != nullptr;
     // second value: the edge id if asked for, else the weight of a weighted graph
-    int32_t* v2 = want_eid ? w.veid : (weighted ? w.vw1 : nullptr);
+    int32_t* v2 = want_eid ? w.veid : (weighted ? w.vw : nullptr);
     int32_t* v2_final = want_eid ? out->csr_eid : (weighted ? reinterpret_cast<int32_t*>(out->csr_w) : nullptr);
     HG_TRY(radix_sort_pairs(w.kcsr, w.kalt, w.vsrc, w.alt1, v2, v2 ? w.alt2 : nullptr, ES, bits, w.scratch, s, &ko,
                             &v1o, &v2o, out->csr_col, v2_final));
@@ -1335,33 +1384,32 @@ extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg
       HG_LAUNCH("build_row_count", k_row_count, dim3((unsigned)cdiv(ES, kRCChunk)), dim3(kBT), 0, s,
                 (const uint32_t*)ko, ES, w.rowcnt);
     HG_TRY(scan_exclusive_i32(w.rowcnt, out->csr_ptr, NQ + 1, nullptr, w.scratch, s));
-    // row degrees as bytes for the CSC scales (w.digit is free until the plan)
-    if (ES > 0)
-      HG_LAUNCH("build_deg_bytes", k_deg_bytes, dim3(grid_for(NQ)), dim3(kBT), 0, s, (const int32_t*)w.rowcnt, NQ,
-                w.digit);
   }
   {
+    // the CSC sort's input from the CSR in its order (the CSR keys stay
+    // where the CSR sort left them, for the slots of its entries)
     uint32_t* ko;
     int32_t *v1o, *v2o;
-    // the CSR keys stay where the CSR sort left them; a weighted graph's
-    // weights ride along into csc_scale, which k_csc_scale divides in place
-    int32_t* wscale = reinterpret_cast<int32_t*>(out->csc_scale);
-    HG_TRY(radix_sort_pairs(w.kcsc, csr_keys == w.kalt ? w.kcsr : w.kalt, w.vdst, w.alt3, weighted ? w.vw2 : nullptr,
-                            weighted ? w.walt : nullptr, ES, bits, w.scratch, s, &ko, &v1o, &v2o, out->csc_row,
-                            weighted ? wscale : nullptr));
-    if (ES > 0 && v1o != out->csc_row) {
+    const bool packed = !weighted && NS < kPackedMaxNodes;
+    if (ES > 0)
+      HG_LAUNCH("build_csc_input", k_csc_input, dim3((unsigned)cdiv(ES, kBT * kCiItems)), dim3(kBT), 0, s,
+                (const uint32_t*)csr_keys, (const int32_t*)out->csr_col, (const int32_t*)out->csr_ptr,
+                weighted ? (const float*)out->csr_w : nullptr, ES, (int32_t)R, packed ? 1 : 0, w.kcsc, w.vdst,
+                packed ? nullptr : w.vsc);
+    int32_t* scale_bits = reinterpret_cast<int32_t*>(out->csc_scale);
+    const SortUnpack up{out->csr_ptr, (int32_t)R, out->csc_scale};
+    HG_TRY(radix_sort_pairs(w.kcsc, csr_keys == w.kalt ? w.kcsr : w.kalt, w.vdst, w.alt3, packed ? nullptr : w.vsc,
+                            packed ? nullptr : w.vsc_alt, ES, bits, w.scratch, s, &ko, &v1o, &v2o, out->csc_row,
+                            packed ? nullptr : scale_bits, packed ? &up : nullptr));
+    if (ES > 0 && v1o != out->csc_row) {  // no pass ran (unpacked, a single key value)
       HG_HIP_TRY(hipMemcpyAsync(out->csc_row, v1o, sizeof(int32_t) * ES, hipMemcpyDeviceToDevice, s));
-      if (weighted) HG_HIP_TRY(hipMemcpyAsync(wscale, v2o, sizeof(int32_t) * ES, hipMemcpyDeviceToDevice, s));
+      HG_HIP_TRY(hipMemcpyAsync(scale_bits, v2o, sizeof(int32_t) * ES, hipMemcpyDeviceToDevice, s));
     }
     HG_TRY(fill_i32(w.rowcnt, 0, NQ + 1, s));
     if (ES > 0)
       HG_LAUNCH("build_row_count", k_row_count, dim3((unsigned)cdiv(ES, kRCChunk)), dim3(kBT), 0, s,
                 (const uint32_t*)ko, ES, w.rowcnt);
     HG_TRY(scan_exclusive_i32(w.rowcnt, out->csc_ptr, NQ + 1, nullptr, w.scratch, s));
-    if (ES > 0)
-      HG_LAUNCH("build_csc_scale", k_csc_scale, dim3(grid_for(ES)), dim3(kBT), 0, s,
-                (const uint32_t*)ko, (const int32_t*)out->csc_row, (const uint8_t*)w.digit,
-                (const int32_t*)out->csr_ptr, ES, (int32_t)R, weighted ? 1 : 0, out->csc_scale);
   }
   // 8. plan: active-source lists and backward work items
   PlanLayout pl(N, E, R);

@@ -136,18 +136,30 @@ int64_t scan_scratch_elems(int64_t n);
 int scan_exclusive_i32(const int32_t* in, int32_t* out, int64_t n, int32_t* total_dev,
                        int32_t* scratch, hipStream_t s);
 
+// Last pass of the CSC sort: its value packs a destination (low 24 bits)
+// and the in-degree of the destination's row (high 8 bits, 255 = "255 or
+// more": read from csr_ptr); the pass writes the destination to v1_final and
+// the mean weight 1 / deg, a correctly rounded float32 quotient, to scale.
+// The row of an entry is destination * n_rel + key % n_rel.
+struct SortUnpack {
+  const int32_t* csr_ptr;
+  int32_t n_rel;
+  float* scale;
+};
+
 // Stable LSD radix sort of (key, value[, value2]) by the low `bits` bits of
 // key (uint32).  Ping-pong buffers must hold n elements; the result ends in
 // the *_out buffers.  v1_final / v2_final (may be NULL; n elements, distinct
 // from every other buffer) receive the values of the last pass directly, so
-// *v1_out == v1_final whenever at least one pass ran.  Scratch:
-// radix_scratch_elems(n).
+// *v1_out == v1_final whenever at least one pass ran.  With unpack (no v2,
+// v1_final given) at least one pass runs and its last pass unpacks v1 as
+// SortUnpack states.  Scratch: radix_scratch_elems(n).
 int64_t radix_scratch_elems(int64_t n);
 int radix_sort_pairs(uint32_t* keys, uint32_t* keys_alt, int32_t* v1, int32_t* v1_alt,
                      int32_t* v2, int32_t* v2_alt, int64_t n, int bits,
                      int32_t* scratch, hipStream_t s, uint32_t** keys_out,
                      int32_t** v1_out, int32_t** v2_out, int32_t* v1_final = nullptr,
-                     int32_t* v2_final = nullptr);
+                     int32_t* v2_final = nullptr, const SortUnpack* unpack = nullptr);
 
 // Stable partition of n items into `nbins` (<= 256) buckets by a digit array
 // (uint8, 255 = drop).  Writes out[off[bin] + rank] = val[i] and bin_off[0..nbins]

@@ -25,16 +25,19 @@ __device__ __forceinline__ int wave_incl_scan(int v) {
   return v;
 }
 
-// Exclusive block scan of one int per thread; returns the block total in *total.
+// Exclusive block scan of one int per thread (a block of kT threads); returns
+// the block total in *total.
+template <int kT = kThreads>
 __device__ __forceinline__ int block_excl_scan(int v, int* total) {
-  __shared__ int wsum[kWaves];
+  constexpr int kW = kT / kWave;
+  __shared__ int wsum[kW];
   const int w = threadIdx.x / kWave;
   int inc = wave_incl_scan(v);
   if (lane_id() == kWave - 1) wsum[w] = inc;
   __syncthreads();
   int off = 0, tot = 0;
 #pragma unroll
-  for (int i = 0; i < kWaves; ++i) {
+  for (int i = 0; i < kW; ++i) {
     int x = wsum[i];
     off += (i < w) ? x : 0;
     tot += x;
@@ -98,18 +101,21 @@ __global__ void k_scan_tiles(const int32_t* __restrict__ in, int32_t* __restrict
 // averages 32 items, so the scatter writes whole 128-byte lines.
 constexpr int kRItems = 32;
 constexpr int kRTile = kThreads * kRItems;
+// Key sorts take 512 threads per scatter block (16 items each): with one
+// value per key two blocks fit a compute unit's LDS, 16 waves in flight.
+constexpr int kKeyThreads = 512;
 
-// Digit histogram of one tile: hist[d * ntiles + tile].
-template <bool kDigitArray>
+// Digit histogram of one tile of kTN items: hist[d * ntiles + tile].
+template <bool kDigitArray, int kTN = kRTile>
 __global__ void k_radix_upsweep(const uint32_t* __restrict__ keys, const uint8_t* __restrict__ digits,
                                 int64_t n, int shift, uint32_t dmask, int32_t* __restrict__ hist,
                                 int64_t ntiles) {
   __shared__ int cnt[256];
   cnt[threadIdx.x] = 0;
   __syncthreads();
-  const int64_t base = (int64_t)blockIdx.x * kRTile;
+  const int64_t base = (int64_t)blockIdx.x * kTN;
 #pragma unroll 4
-  for (int j = 0; j < kRItems; ++j) {
+  for (int j = 0; j < kTN / kThreads; ++j) {
     int64_t i = base + (int64_t)j * kThreads + threadIdx.x;
     if (i < n) {
       uint32_t d = kDigitArray ? (uint32_t)digits[i] : ((keys[i] >> shift) & dmask);
@@ -130,35 +136,42 @@ __global__ void k_radix_upsweep(const uint32_t* __restrict__ keys, const uint8_t
 // order, so every digit's run lands in consecutive global addresses.
 // offs is the digit-major exclusive scan of the per-tile counts with the
 // grand total at offs[256 * ntiles].
-template <bool kDigitArray, bool kHasV2>
-__global__ void __launch_bounds__(256) k_radix_downsweep(
+// kUnpack: the CSC sort's last pass (SortUnpack): v1 packs the destination
+// and its row's in-degree; v1_out gets the destination, scale_out 1 / deg.
+// kT threads per block (a multiple of 256), tiles of kTN items, kTN / kT
+// items per thread.
+template <bool kDigitArray, bool kHasV2, bool kUnpack = false, int kT = kThreads, int kTN = kRTile>
+__global__ void __launch_bounds__(kT) k_radix_downsweep(
     const uint32_t* __restrict__ keys, const uint8_t* __restrict__ digits,
     const int32_t* __restrict__ v1, const int32_t* __restrict__ v2, int64_t n, int shift, uint32_t dmask,
     const int32_t* __restrict__ offs, int64_t ntiles, uint32_t* __restrict__ keys_out,
-    int32_t* __restrict__ v1_out, int32_t* __restrict__ v2_out) {
+    int32_t* __restrict__ v1_out, int32_t* __restrict__ v2_out, SortUnpack up = SortUnpack{nullptr, 1, nullptr}) {
+  constexpr int kW = kT / kWave, kI = kTN / kT;
   __shared__ int gbase[256];
   __shared__ int loff[256];
-  __shared__ int wcnt[kWaves][256];
-  __shared__ uint32_t sk[kDigitArray ? 1 : kRTile];
-  __shared__ int32_t sv1[kRTile];
-  __shared__ int32_t sv2[kHasV2 ? kRTile : 1];
-  __shared__ uint8_t sd[kRTile];
+  __shared__ uint16_t wcnt[kW][256];  // counts, then offsets, below kTN
+  __shared__ uint32_t sk[kDigitArray ? 1 : kTN];
+  __shared__ int32_t sv1[kTN];
+  __shared__ int32_t sv2[kHasV2 ? kTN : 1];
+  __shared__ uint8_t sd[kDigitArray ? kTN : 1];  // a key's digit is read off sk
   const int t = threadIdx.x;
   const int w = t / kWave;
   const int l = lane_id();
-  const int64_t fi = (int64_t)t * ntiles + blockIdx.x;
-  const int base = offs[fi];
-  const int cnt = offs[fi + 1] - base;
-  gbase[t] = base;
-#pragma unroll
-  for (int i = 0; i < kWaves; ++i) wcnt[i][t] = 0;
+  int cnt = 0;
+  if (t < 256) {
+    const int64_t fi = (int64_t)t * ntiles + blockIdx.x;
+    const int base = offs[fi];
+    cnt = offs[fi + 1] - base;
+    gbase[t] = base;
+  }
+  for (int q = t; q < kW * 256; q += kT) (&wcnt[0][0])[q] = 0;
   const uint64_t lt_mask = (l == 0) ? 0ull : (~0ull >> (kWave - l));
-  const int64_t wbase = (int64_t)blockIdx.x * kRTile + (int64_t)w * (kRItems * kWave);
+  const int64_t wbase = (int64_t)blockIdx.x * kTN + (int64_t)w * (kI * kWave);
   // all loads of the wave's slice first
-  uint32_t kd[kRItems];  // key, or digit
-  int32_t a1[kRItems], a2[kHasV2 ? kRItems : 1];
+  uint32_t kd[kI];  // key, or digit
+  int32_t a1[kI], a2[kHasV2 ? kI : 1];
 #pragma unroll
-  for (int j = 0; j < kRItems; ++j) {
+  for (int j = 0; j < kI; ++j) {
     const int64_t i = wbase + (int64_t)j * kWave + l;
     if (i < n) {
       kd[j] = kDigitArray ? (uint32_t)digits[i] : keys[i];
@@ -171,12 +184,12 @@ __global__ void __launch_bounds__(256) k_radix_downsweep(
     }
   }
   int lo = 0, kept = 0;
-  lo = block_excl_scan(cnt, &kept);  // includes a barrier: wcnt zeroing is visible after it
-  loff[t] = lo;
+  lo = block_excl_scan<kT>(cnt, &kept);  // includes a barrier: wcnt zeroing is visible after it
+  if (t < 256) loff[t] = lo;
   // ranks inside the wave
-  uint16_t rk[kRItems];
+  uint16_t rk[kI];
 #pragma unroll
-  for (int j = 0; j < kRItems; ++j) {
+  for (int j = 0; j < kI; ++j) {
     const int64_t i = wbase + (int64_t)j * kWave + l;
     const uint32_t d = kDigitArray ? kd[j] : ((kd[j] >> shift) & dmask);
     const bool valid = i < n && (!kDigitArray || d != 255u);
@@ -191,39 +204,51 @@ __global__ void __launch_bounds__(256) k_radix_downsweep(
     if (valid) r = wcnt[w][d] + __popcll(m & lt_mask);
     // every lane has read the counter before the group's leader advances it
     __builtin_amdgcn_wave_barrier();
-    if (valid && (m & lt_mask) == 0) wcnt[w][d] += __popcll(m);
+    if (valid && (m & lt_mask) == 0) wcnt[w][d] = (uint16_t)(wcnt[w][d] + __popcll(m));
     __builtin_amdgcn_wave_barrier();
     rk[j] = valid ? (uint16_t)r : (uint16_t)0xFFFFu;
   }
   __syncthreads();
   // per digit: exclusive prefix over the waves, added to the tile-local offset
-  {
+  if (t < 256) {
     int run = loff[t];
 #pragma unroll
-    for (int q = 0; q < kWaves; ++q) {
+    for (int q = 0; q < kW; ++q) {
       const int c = wcnt[q][t];
-      wcnt[q][t] = run;
+      wcnt[q][t] = (uint16_t)run;
       run += c;
     }
   }
   __syncthreads();
 #pragma unroll
-  for (int j = 0; j < kRItems; ++j) {
+  for (int j = 0; j < kI; ++j) {
     if (rk[j] != 0xFFFFu) {
       const uint32_t d = kDigitArray ? kd[j] : ((kd[j] >> shift) & dmask);
       const int lpos = wcnt[w][d] + rk[j];
       if (!kDigitArray) sk[lpos] = kd[j];
       sv1[lpos] = a1[j];
       if (kHasV2) sv2[lpos] = a2[j];
-      sd[lpos] = (uint8_t)d;
+      if (kDigitArray) sd[lpos] = (uint8_t)d;
     }
   }
   __syncthreads();
-  for (int idx = t; idx < kept; idx += kThreads) {
-    const int d = sd[idx];
+  for (int idx = t; idx < kept; idx += kT) {
+    const int d = kDigitArray ? (int)sd[idx] : (int)((sk[idx] >> shift) & dmask);
     const int pos = gbase[d] + (idx - loff[d]);
     if (!kDigitArray) keys_out[pos] = sk[idx];
-    v1_out[pos] = sv1[idx];
+    if (kUnpack) {
+      const uint32_t v = (uint32_t)sv1[idx];
+      const int32_t dst = (int32_t)(v & 0xFFFFFFu);
+      int32_t deg = (int32_t)(v >> 24);
+      if (deg == 255) {
+        const int64_t row = (int64_t)dst * up.n_rel + (int64_t)(sk[idx] % (uint32_t)up.n_rel);
+        deg = up.csr_ptr[row + 1] - up.csr_ptr[row];
+      }
+      v1_out[pos] = dst;
+      up.scale[pos] = 1.0f / (float)deg;
+    } else {
+      v1_out[pos] = sv1[idx];
+    }
     if (kHasV2) v2_out[pos] = sv2[idx];
   }
 }
@@ -278,10 +303,14 @@ int64_t radix_scratch_elems(int64_t n) {
 int radix_sort_pairs(uint32_t* keys, uint32_t* keys_alt, int32_t* v1, int32_t* v1_alt,
                      int32_t* v2, int32_t* v2_alt, int64_t n, int bits, int32_t* scratch,
                      hipStream_t s, uint32_t** keys_out, int32_t** v1_out, int32_t** v2_out,
-                     int32_t* v1_final, int32_t* v2_final) {
+                     int32_t* v1_final, int32_t* v2_final, const SortUnpack* unpack) {
   *keys_out = keys;
   *v1_out = v1;
   if (v2_out) *v2_out = v2;
+  if (unpack) {
+    if (v2 || !v1_final) return fail(HG_ERR_ARG, "radix_sort_pairs: unpack needs v1_final and no v2");
+    if (bits < 1) bits = 1;  // a single key value still takes the unpacking pass
+  }
   if (n <= 0 || bits <= 0) return HG_OK;
   const int64_t tiles = cdiv(n, kRTile);
   int32_t* hist = scratch;
@@ -299,14 +328,19 @@ int radix_sort_pairs(uint32_t* keys, uint32_t* keys_alt, int32_t* v1, int32_t* v
     HG_LAUNCH("radix_upsweep", (k_radix_upsweep<false>), dim3((unsigned)tiles), dim3(kThreads), 0, s,
               (const uint32_t*)ka, (const uint8_t*)nullptr, n, shift, dmask, hist, tiles);
     HG_TRY(scan_exclusive_i32(hist, hist, 256 * tiles, hist + 256 * tiles, sscr, s));
-    if (v2) {
-      HG_LAUNCH("radix_downsweep", (k_radix_downsweep<false, true>), dim3((unsigned)tiles),
-                dim3(kThreads), 0, s, (const uint32_t*)ka, (const uint8_t*)nullptr,
+    if (unpack && shift + 8 >= bits) {
+      HG_LAUNCH("radix_downsweep", (k_radix_downsweep<false, false, true, kKeyThreads>), dim3((unsigned)tiles),
+                dim3(kKeyThreads), 0, s, (const uint32_t*)ka, (const uint8_t*)nullptr,
+                (const int32_t*)a1, (const int32_t*)nullptr, n, shift, dmask,
+                (const int32_t*)hist, tiles, kb, b1, (int32_t*)nullptr, *unpack);
+    } else if (v2) {
+      HG_LAUNCH("radix_downsweep", (k_radix_downsweep<false, true, false, kKeyThreads>), dim3((unsigned)tiles),
+                dim3(kKeyThreads), 0, s, (const uint32_t*)ka, (const uint8_t*)nullptr,
                 (const int32_t*)a1, (const int32_t*)a2, n, shift, dmask, (const int32_t*)hist,
                 tiles, kb, b1, b2);
     } else {
-      HG_LAUNCH("radix_downsweep", (k_radix_downsweep<false, false>), dim3((unsigned)tiles),
-                dim3(kThreads), 0, s, (const uint32_t*)ka, (const uint8_t*)nullptr,
+      HG_LAUNCH("radix_downsweep", (k_radix_downsweep<false, false, false, kKeyThreads>), dim3((unsigned)tiles),
+                dim3(kKeyThreads), 0, s, (const uint32_t*)ka, (const uint8_t*)nullptr,
                 (const int32_t*)a1, (const int32_t*)nullptr, n, shift, dmask,
                 (const int32_t*)hist, tiles, kb, b1, (int32_t*)nullptr);
     }

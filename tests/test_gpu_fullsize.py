@@ -134,15 +134,13 @@ def test_fullsize_csr_csc_properties(full):
     cptr = sub.view("csc_ptr").cpu().numpy().astype(np.int64)
     assert np.array_equal(np.diff(cptr), cnt_csc)
     crow = sub.view("csc_row").cpu().numpy().astype(np.int64)
-    # exact order: the oracle's CSC lists the kept edges by (source row, edge
-    # index), i.e. its stable sort on the row key; one sort of the unique
-    # int64 key (row << 28 | position among the kept edges) gives that order
-    e_s = full.eid.shape[0]
-    assert e_s < (1 << 28) and nq < (1 << 35)
-    order = np.sort((key_csc << 28) | np.arange(e_s, dtype=np.int64)) & ((1 << 28) - 1)
-    assert np.array_equal(crow, full.dst_l[order])
+    # exact order: the oracle's CSC lists a row by (destination, edge index);
+    # entries equal in (row, destination) are parallel edges with equal
+    # outputs, so the sorted (row << 24 | destination) of the kept edges is the
+    # whole CSC (row, csc_row) sequence
+    assert ns < (1 << 24) and nq < (1 << 38)
     rows = np.repeat(np.arange(nq), cnt_csc)
-    del order
+    assert np.array_equal((rows << 24) | crow, np.sort((key_csc << 24) | full.dst_l))
     scale = sub.view("csc_scale").cpu().numpy()
     deg = cnt_csr[crow * R + (rows % R)].astype(np.float32)
     assert np.array_equal(scale.view(np.uint32), (np.float32(1.0) / deg).view(np.uint32))
