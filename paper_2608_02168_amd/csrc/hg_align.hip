@@ -222,7 +222,10 @@ __device__ __forceinline__ void quad_of(int q, int& qi, int& qj) {
 // the end-of-chunk arrays reuse the step buffers.
 template <int D, class T>
 struct GramLds {
-  static constexpr int kStepRows = D * sizeof(T) <= 512 ? 64 : 32;  // 64 KB of LDS per step at most
+  // steps of 64 rows up to 512-byte rows (128 KB of LDS at most), except at
+  // d = 256, whose ten Gram waves per view spill with two 32-row blocks per
+  // step (32-row steps: 1.6 against 3.3 ms per bf16 step)
+  static constexpr int kStepRows = (D * sizeof(T) <= 512 && D < 256) ? 64 : 32;
   static constexpr int kStep = 2 * kStepRows * D;               // elements of one step buffer
   static constexpr size_t kRows = 2 * (size_t)kStep * sizeof(T);  // both step buffers, bytes
   static constexpr size_t kTail = sizeof(double) * (128 * 25 + 1024 + 6 * D);
