@@ -244,3 +244,14 @@ def test_transform_layout_choice(n_rel):
     assert int(sub.c.plan_slot_rows) == (nq if nq <= 4 * A else A)
     assert (nq <= 4 * A) == (n_rel == 3)
 
+
+
+def test_build_beyond_24_bit_destinations():
+    """A subgraph of more than 2^24 nodes: a destination no longer fits the
+    24 bits the CSC sort packs next to its row degree, so the sort carries the
+    scale 1 / deg as a second value instead; the outputs are the same."""
+    cfg = synth.GraphConfig("wide", (1 << 24) + 50_000, 3_000_000, 3, 1.2, 50.0, 1 << 24, 40_000, seed=21)
+    _, ref, sub = run_both(cfg, 0, select.THETA_NONE, None)
+    assert sub.n_sub > (1 << 24)
+    assert int(ref.csc_row.max()) >= (1 << 24)
+    assert_same(ref, sub)
