@@ -420,22 +420,6 @@ __global__ void k_heavy_reduce(int64_t n_heavy, const int4* __restrict__ heavy,
   }
 }
 
-// y = bf16(x) on the rows whose CSC row of relation r is empty (the others
-// were written by that relation's dX pass): one thread per 4 columns.
-template <int D>
-__global__ void k_to_bf16_rest(const float* __restrict__ x, bf16_t* __restrict__ y, int64_t n_rows,
-                               const int32_t* __restrict__ csc_ptr, int32_t R, int32_t r) {
-  const int64_t total = n_rows * (D / 4);
-  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t row = e / (D / 4);
-    const int64_t q = row * R + r;
-    if (csc_ptr[q + 1] > csc_ptr[q]) continue;
-    const int64_t i = row * D + (e % (D / 4)) * 4;
-    const f32x4 v = *reinterpret_cast<const f32x4*>(x + i);
-    *reinterpret_cast<uint2*>(y + i) = uint2{pack2bf(v[0], v[1]), pack2bf(v[2], v[3])};
-  }
-}
-
 inline unsigned wave_grid(int64_t n_waves) {
   int64_t blocks = cdiv(n_waves, 4);
   const int64_t cap = (int64_t)num_cus() * 64;
@@ -558,7 +542,11 @@ int layer_bwd_impl(const hg_subgraph* s, const hg_layer_desc* L, const T* Hin, c
   if (!a.ok()) return fail(HG_ERR_CAPACITY, "backward workspace needs %zu bytes, got %zu", a.used, ws_bytes);
   const int32_t R = s->n_rel;
   const PlanView pv = plan_view(s);
-  float* dacc = (sizeof(T) == 4) ? reinterpret_cast<float*>(dHin) : w.dhacc;
+  // float32 rows: dH accumulates in place; bfloat16 rows: in a float32
+  // accumulator, each row written once in bf16 by the last pass reaching it
+  constexpr bool kBf = sizeof(T) == 2;
+  float* dacc = kBf ? w.dhacc : reinterpret_cast<float*>(dHin);
+  const int32_t* cptr = (const int32_t*)s->csc_ptr;
   // (c) dH = G (residual) + dZ W_self^T per type, float32 MFMA; the A-operand
   // load forms dZ = G * mask and also writes it out for the SpMM and dW_self
   for (int t = 0; t < s->n_ntype; ++t) {
@@ -568,8 +556,14 @@ int layer_bwd_impl(const hg_subgraph* s, const hg_layer_desc* L, const T* Hin, c
     // d = 128 are read again instead (held through the tile they would not
     // fit the registers beside the next tile's rows and the split operand)
     constexpr bool kFromA = !(D == 128 && sizeof(T) == 4);
-    StoreRows<D, float, T, kFromA> ep{dacc, rows_contig(lo), nullptr, L->residual ? G : nullptr};
-    HG_TRY((rows_f32<D, true>("gemm_bwd_dx_self", hi - lo, W_self + (int64_t)t * D * D, la, ep, st)));
+    if constexpr (kBf) {
+      StoreLast<D, T, kFromA> ep{reinterpret_cast<bf16_t*>(dHin), dacc, rows_contig(lo), nullptr,
+                                 L->residual ? G : nullptr, cptr, R, -1};
+      HG_TRY((rows_f32<D, true>("gemm_bwd_dx_self", hi - lo, W_self + (int64_t)t * D * D, la, ep, st)));
+    } else {
+      StoreRows<D, float, T, kFromA> ep{dacc, rows_contig(lo), nullptr, L->residual ? G : nullptr};
+      HG_TRY((rows_f32<D, true>("gemm_bwd_dx_self", hi - lo, W_self + (int64_t)t * D * D, la, ep, st)));
+    }
   }
   // (b) transposed SpMM into float32 dY
   if (s->plan_items > 0)
@@ -579,36 +573,20 @@ int layer_bwd_impl(const hg_subgraph* s, const hg_layer_desc* L, const T* Hin, c
   if (s->plan_heavy > 0)
     HG_LAUNCH("spmm_bwd_reduce", (k_heavy_reduce<D, float>), dim3(wave_grid(s->plan_heavy)), dim3(256), 0, st,
               (int64_t)s->plan_heavy, pv.heavy, (const double*)w.part, w.dY);
-  // (c) dH += dY_r W_r^T per relation, in relation order; for bfloat16 rows
-  // the relation with the most active sources goes last and writes its rows
-  // of dH in bf16 straight from the float32 accumulator, and only the other
-  // rows are converted afterwards
-  int32_t rlast = -1;
-  if constexpr (sizeof(T) == 2) {
-    rlast = 0;
-    for (int r = 1; r < R; ++r)
-      if (s->n_active[r] > s->n_active[rlast]) rlast = r;
-  }
+  // (c) dH += dY_r W_r^T per relation, in relation order
   std::vector<int64_t> act_off(R + 1, 0);
   for (int r = 0; r < R; ++r) act_off[r + 1] = act_off[r] + s->n_active[r];
-  for (int k = 0; k < R; ++k) {
-    const int r = (rlast < 0) ? k : (k < rlast ? k : (k < R - 1 ? k + 1 : rlast));
+  for (int r = 0; r < R; ++r) {
     const int64_t n = s->n_active[r], off = act_off[r];
     LoadRows<D, float> la{w.dY, rows_list(pv.act_slot + off)};
-    if (r == rlast) {
-      StoreRows<D, T, float> ep{dHin, rows_list(pv.active + off), nullptr, dacc};
+    if constexpr (kBf) {
+      StoreLast<D, float> ep{reinterpret_cast<bf16_t*>(dHin), dacc, rows_list(pv.active + off), nullptr, dacc, cptr,
+                             R, r};
       HG_TRY((rows_f32<D, true>("gemm_bwd_dx_rel", n, W_rel + (int64_t)r * D * D, la, ep, st)));
     } else {
       StoreRows<D, float, float> ep{dacc, rows_list(pv.active + off), nullptr, dacc};
       HG_TRY((rows_f32<D, true>("gemm_bwd_dx_rel", n, W_rel + (int64_t)r * D * D, la, ep, st)));
     }
-  }
-  if constexpr (sizeof(T) == 2) {
-    const int64_t n = s->n_sub * (int64_t)(D / 4);
-    if (n > 0)
-      HG_LAUNCH("dh_to_bf16", k_to_bf16_rest<D>, dim3((unsigned)(cdiv(n, 256) < 65536 ? cdiv(n, 256) : 65536)),
-                dim3(256), 0, st, (const float*)w.dhacc, reinterpret_cast<bf16_t*>(dHin), s->n_sub,
-                (const int32_t*)s->csc_ptr, R, rlast);
   }
   // (c) weight gradients, split-K
   for (int t = 0; t < s->n_ntype; ++t) {

@@ -472,6 +472,56 @@ struct StoreRows {
   }
 };
 
+// dH rows of a bfloat16 layer, each written once in bf16: the self pass and
+// the relation passes in relation order add into a float32 accumulator, and
+// the last pass that reaches a row writes it in bf16 instead.  Relation pass
+// r (r = -1: the self pass) is a row's last when the row has no CSC entries
+// of a relation after r: csc_ptr[i R + R] == csc_ptr[i R + r + 1].  The self
+// pass writes the accumulator of every row some relation pass reaches after
+// it, so each relation pass reads an initialised accumulator (its addend).
+template <int D, class TA = float, bool kAddendIsA = false>
+struct StoreLast {
+  static constexpr bool kAddA = kAddendIsA;
+  static constexpr bool kMask = false;
+  static constexpr bool kRowFlag = true;  // the kernel reads last(ro) once per row, early
+  bf16_t* out;          // [rows, D] final bf16 rows
+  float* accum;         // [rows, D] float32 accumulator rows
+  RowMap map;
+  const float* bias;    // [D] or null
+  const TA* addend;     // rows through the same map (the accumulator, or the residual), or null
+  const int32_t* csc_ptr;
+  int32_t n_rel, rel;   // rel = -1 for the self pass
+  __device__ __forceinline__ int64_t row(int64_t i) const { return map(i); }
+  __device__ __forceinline__ bool last(int64_t ro) const {
+    const int32_t* q = csc_ptr + ro * n_rel;
+    return q[n_rel] == q[rel + 1];
+  }
+  __device__ __forceinline__ f32x4 pre4(int64_t, int64_t ro, int c) const {
+    f32x4 v = bias ? *reinterpret_cast<const f32x4*>(bias + c) : f32x4{0.f, 0.f, 0.f, 0.f};
+    if (addend) v += Elt<TA>::load4(addend + ro * D + c);
+    return v;
+  }
+  __device__ __forceinline__ f32x4 bias4(int c) const {
+    return bias ? *reinterpret_cast<const f32x4*>(bias + c) : f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  __device__ __forceinline__ bool flag(int64_t ro) const { return last(ro); }
+  __device__ __forceinline__ void store4f(int64_t, int64_t ro, int c, f32x4 acc, f32x4 pre, bool is_last) const {
+    const f32x4 r = acc + pre;
+    if (is_last) {
+      *reinterpret_cast<uint2*>(out + ro * D + c) = uint2{pack2bf(r[0], r[1]), pack2bf(r[2], r[3])};
+    } else {
+      *reinterpret_cast<f32x4*>(accum + ro * D + c) = r;
+    }
+  }
+};
+
+// Epilogues with kRowFlag take a per-row flag, read once per row before the
+// products (flag(ro)), in their stores (store4f).
+template <class E, class = void>
+struct EpiRowFlag : std::false_type {};
+template <class E>
+struct EpiRowFlag<E, std::void_t<decltype(E::kRowFlag)>> : std::integral_constant<bool, E::kRowFlag> {};
+
 // ---- row GEMMs on the split-fp16 MFMA: shared shape ------------------------------
 // Block = 8 waves sharing one LDS copy of a column slice of op(W); a wave owns
 // 16 rows, a block 128 rows; persistent over tiles.  W is D x D; blockIdx.y
@@ -594,6 +644,8 @@ __global__ void __launch_bounds__(kGemmThreads, D > 128 ? 2 : 4) k_gemm_rows_pp(
     const bool live = i < n_rows;
     const int64_t ro = epi.map.template row_of<kListO>(ko);
     const int64_t ra = aload.map.template row_of<kListA>(ka);
+    bool rflag = false;
+    if constexpr (EpiRowFlag<Epi>::value) rflag = live && epi.flag(ro);
     // the row as MFMA operand: scaled by a power of two of its largest
     // magnitude (or of a bound of it: the stored row, for loaders whose
     // operand only zeroes elements of it), split in two
@@ -681,7 +733,13 @@ __global__ void __launch_bounds__(kGemmThreads, D > 128 ? 2 : 4) k_gemm_rows_pp(
         if (live && g == 0) epi.mask_word(ro, p, word);
       } else if (live) {
 #pragma unroll
-        for (int q = 0; q < NG; ++q) epi.store4(i, ro, col0 + 16 * (p * NG + q) + 4 * g, acc[q], pre[q]);
+        for (int q = 0; q < NG; ++q) {
+          if constexpr (EpiRowFlag<Epi>::value) {
+            epi.store4f(i, ro, col0 + 16 * (p * NG + q) + 4 * g, acc[q], pre[q], rflag);
+          } else {
+            epi.store4(i, ro, col0 + 16 * (p * NG + q) + 4 * g, acc[q], pre[q]);
+          }
+        }
       }
     }
   };
