@@ -1381,6 +1381,224 @@ static __global__ void k_sum_partials(const float* __restrict__ partial, int64_t
   out[i] = s;
 }
 
+// gemm_tn on v_mfma_f32_16x16x32_bf16 for plain feature rows at d = 128 and
+// 256 whose two operands have the same storage type (float32 x float32: each
+// element split once per block instead of by each wave that uses it, 2.64 ->
+// 2.2 ms per weight gradient of the 10M-row self transform; bf16 x bf16).
+// A bf16 x float32 product stays with k_gemm_tn_bf, which measured twice as
+// fast at d = 256 (its four independent waves per block keep more rows in
+// flight than a block synchronised per step).  The operands are staged in LDS
+// once per step.  A block computes one
+// 128 x 128 output tile (ti, tj) of its chunk (d = 256: four blocks per
+// chunk, as in k_gemm_tn_bf) in steps of 32 rows.  Threads 0-127 stage A,
+// 128-255 B: thread u takes rows 8 (u/32) .. + 7 of the step and features
+// 4 (u%32) .. + 3 of the tile, one raw load of 4 features per row, and
+// writes per feature the 8 rows' values as one uint4 of bf16 -- the MFMA's
+// 8 K slots of K group u/32 -- into LDS (float32 rows: the three bf16 parts
+// of split_bf3, each element split once per block instead of once per wave
+// that uses it).  The next step's rows are loaded while the waves multiply.
+// Wave w owns the 64 x 64 quadrant (w/2, w%2) of the tile; MFMA block
+// (bi, bj) covers tile rows 64 qi + 16 bi + m and columns 64 qj + 16 bj + n,
+// lane (c, g) supplying K group g of A row m = c and B column n = c, and
+// holding output (m = 4 g + v, n = c).  Part products of order <= 2,
+// smallest first, as in k_gemm_tn_bf.  Same outputs and chunking as
+// k_gemm_tn_bf (column sums of B in float32, rows in order per K group, the
+// four K groups summed in order).
+// A block barrier ordering LDS accesses only: global loads in flight (the
+// next step's rows) stay in flight across it.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+template <int D, class TA, class TB, bool kListA, bool kListB>
+__global__ void __launch_bounds__(256, 2) k_gemm_tn_lds(int64_t n_rows, int64_t kc, LoadRows<D, TA> la,
+                                                        LoadRows<D, TB> lb, float* __restrict__ partial,
+                                                        float* __restrict__ colsum) {
+  static_assert(D == 128 || D == 256, "gemm_tn_lds: d must be 128 or 256");
+  constexpr bool kSplitA = sizeof(TA) == 4, kSplitB = sizeof(TB) == 4;
+  constexpr int PA = kSplitA ? 3 : 1, PB = kSplitB ? 3 : 1;
+  constexpr int TT = 128;  // output tile edge
+  constexpr int S = 32;    // rows per step
+  __shared__ uint4 fa[PA][4][TT];
+  __shared__ uint4 fb[PB][4][TT];
+  __shared__ float cred[4][TT];
+  const int tid = threadIdx.x, w = tid >> 6, l = tid & 63;
+  const int g = l >> 4, c = l & 15;
+  int64_t chunk;
+  int ti, tj;
+  tn_block<D>(chunk, ti, tj);
+  const int64_t k_beg = chunk * kc;
+  if (k_beg >= n_rows) return;  // a padding block (the whole block)
+  const int64_t k_end = (k_beg + kc < n_rows) ? k_beg + kc : n_rows;
+  // staging role (uniform per wave)
+  const bool sb = tid >= 128;
+  const int u = tid & 127, sg = u >> 5, sf = 4 * (u & 31);
+  const int scol = (sb ? TT * tj : TT * ti) + sf;
+  // row keys of a step: list entries (loaded ahead) or the row index itself
+  // (both below 2^31)
+  int32_t kk[8];
+  auto keys = [&](int64_t k0) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      int64_t r = k0 + 8 * sg + e;
+      r = r < k_end ? r : k_end - 1;
+      if (sb) {
+        kk[e] = (int32_t)lb.map.template key<kListB>(r);
+      } else {
+        kk[e] = (int32_t)la.map.template key<kListA>(r);
+      }
+    }
+  };
+  uint4 rawa[8];  // 4 features of each of the 8 rows, as loaded (bf16 rows use .x and .y)
+  auto fetch = [&](int64_t k0, uint4 (&raw)[8]) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      raw[e] = uint4{0u, 0u, 0u, 0u};
+      if (k0 + 8 * sg + e < k_end) {
+        if (sb) {
+          const int64_t row = lb.map.template row_of<kListB>((typename RowMap::template Key<kListB>)kk[e]);
+          if constexpr (kSplitB) {
+            raw[e] = __builtin_bit_cast(uint4, lb.raw4b(row, scol));
+          } else {
+            const uint2 x = lb.raw4b(row, scol);
+            raw[e] = uint4{x.x, x.y, 0u, 0u};
+          }
+        } else {
+          const int64_t row = la.map.template row_of<kListA>((typename RowMap::template Key<kListA>)kk[e]);
+          if constexpr (kSplitA) {
+            raw[e] = __builtin_bit_cast(uint4, la.raw4b(row, scol));
+          } else {
+            const uint2 x = la.raw4b(row, scol);
+            raw[e] = uint4{x.x, x.y, 0u, 0u};
+          }
+        }
+      }
+    }
+  };
+  // feature q of rows 2p, 2p + 1 as one packed bf16 pair (bf16 rows)
+  auto pair_bf = [](const uint4 (&raw)[8], int p, int q) -> uint32_t {
+    const uint32_t a = (q < 2) ? raw[2 * p].x : raw[2 * p].y, b = (q < 2) ? raw[2 * p + 1].x : raw[2 * p + 1].y;
+    return (q & 1) ? ((a >> 16) | (b & 0xFFFF0000u)) : ((a & 0xFFFFu) | (b << 16));
+  };
+  auto value = [](const uint4 (&raw)[8], int e, int q, bool split) -> float {
+    if (split) return __uint_as_float(q == 0 ? raw[e].x : q == 1 ? raw[e].y : q == 2 ? raw[e].z : raw[e].w);
+    const uint32_t x = (q < 2) ? raw[e].x : raw[e].y;
+    return (q & 1) ? __uint_as_float(x & 0xFFFF0000u) : __uint_as_float(x << 16);
+  };
+  float bsum[4] = {0.f, 0.f, 0.f, 0.f};
+  // the raw rows -> fragments in LDS (and, for B, the column sums)
+  auto park = [&](const uint4 (&raw)[8]) {
+    if (sb) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) bsum[q] += value(raw, e, q, kSplitB);
+        if constexpr (kSplitB) {
+          uint32_t wv[3][4];
+#pragma unroll
+          for (int p = 0; p < 4; ++p) {
+            uint32_t part[3];
+            split_bf3(value(raw, 2 * p, q, true), value(raw, 2 * p + 1, q, true), part);
+#pragma unroll
+            for (int k = 0; k < 3; ++k) wv[k][p] = part[k];
+          }
+#pragma unroll
+          for (int k = 0; k < 3; ++k) fb[k][sg][sf + q] = uint4{wv[k][0], wv[k][1], wv[k][2], wv[k][3]};
+        } else {
+          fb[0][sg][sf + q] = uint4{pair_bf(raw, 0, q), pair_bf(raw, 1, q), pair_bf(raw, 2, q), pair_bf(raw, 3, q)};
+        }
+      }
+    } else {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        if constexpr (kSplitA) {
+          uint32_t wv[3][4];
+#pragma unroll
+          for (int p = 0; p < 4; ++p) {
+            uint32_t part[3];
+            split_bf3(value(raw, 2 * p, q, true), value(raw, 2 * p + 1, q, true), part);
+#pragma unroll
+            for (int k = 0; k < 3; ++k) wv[k][p] = part[k];
+          }
+#pragma unroll
+          for (int k = 0; k < 3; ++k) fa[k][sg][sf + q] = uint4{wv[k][0], wv[k][1], wv[k][2], wv[k][3]};
+        } else {
+          fa[0][sg][sf + q] = uint4{pair_bf(raw, 0, q), pair_bf(raw, 1, q), pair_bf(raw, 2, q), pair_bf(raw, 3, q)};
+        }
+      }
+    }
+  };
+  const int qi = w >> 1, qj = w & 1;
+  f32x4 acc[4][4];
+#pragma unroll
+  for (int bi = 0; bi < 4; ++bi)
+#pragma unroll
+    for (int bj = 0; bj < 4; ++bj) acc[bi][bj] = f32x4{0.f, 0.f, 0.f, 0.f};
+  constexpr int NJ = 4;  // column blocks whose B fragments are held at a time
+  auto compute = [&]() {
+#pragma unroll
+    for (int j0 = 0; j0 < 4; j0 += NJ) {
+      uint4 bq[NJ][PB];
+#pragma unroll
+      for (int jj = 0; jj < NJ; ++jj)
+#pragma unroll
+        for (int p = 0; p < PB; ++p) bq[jj][p] = fb[p][g][64 * qj + 16 * (j0 + jj) + c];
+#pragma unroll
+      for (int bi = 0; bi < 4; ++bi) {
+        uint4 aq[PA];
+#pragma unroll
+        for (int p = 0; p < PA; ++p) aq[p] = fa[p][g][64 * qi + 16 * bi + c];
+#pragma unroll
+        for (int jj = 0; jj < NJ; ++jj) {
+#pragma unroll
+          for (int ord = 2; ord >= 0; --ord)
+#pragma unroll
+            for (int pa = 0; pa < PA; ++pa) {
+              const int pb = ord - pa;
+              if (pb >= 0 && pb < PB) acc[bi][j0 + jj] = mfma_bf16(aq[pa], bq[jj][pb], acc[bi][j0 + jj]);
+            }
+        }
+      }
+    }
+  };
+  int64_t k0 = k_beg;
+  keys(k0);
+  fetch(k0, rawa);
+  keys(k0 + S);
+  for (;;) {
+    park(rawa);
+    lds_barrier();
+    const bool more = k0 + S < k_end;
+    if (more) {
+      fetch(k0 + S, rawa);  // the next step's rows arrive while the waves multiply
+      keys(k0 + 2 * S);
+    }
+    compute();
+    lds_barrier();
+    if (!more) break;
+    k0 += S;
+  }
+  float* out = partial + chunk * (int64_t)D * D;
+#pragma unroll
+  for (int bi = 0; bi < 4; ++bi)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int64_t i = TT * ti + 64 * qi + 16 * bi + 4 * g + v;
+#pragma unroll
+      for (int bj = 0; bj < 4; ++bj) out[i * D + TT * tj + 64 * qj + 16 * bj + c] = acc[bi][bj][v];
+    }
+  if (colsum && ti == 0) {
+    if (sb) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) cred[sg][sf + q] = bsum[q];
+    }
+    __syncthreads();
+    if (tid < TT) colsum[chunk * D + TT * tj + tid] = ((cred[0][tid] + cred[1][tid]) + cred[2][tid]) + cred[3][tid];
+  }
+}
+
 // Chunking of a K-reduction of n rows (deterministic in n): at most
 // kSplitPerCu chunks per compute unit, one resident block each.
 constexpr int kSplitPerCu = 2;
@@ -1432,8 +1650,16 @@ int launch_gemm_tn(const char* name, int64_t n_rows, LA la, LB lb, float* partia
     // plain feature rows: the bf16 MFMA kernel
     typedef typename std::remove_cv<typename std::remove_pointer<decltype(la.base)>::type>::type TA_;
     typedef typename std::remove_cv<typename std::remove_pointer<decltype(lb.base)>::type>::type TB_;
-#define HG_TN_BF(LA_, LB_) \
-  HG_LAUNCH(name, (k_gemm_tn_bf<D, TA_, TB_, LA_, LB_>), grid, dim3(256), 0, s, n_rows, kc, la, lb, partial, cs)
+#define HG_TN_BF(LA_, LB_)                                                                                 \
+  do {                                                                                                     \
+    if constexpr (D >= 128 && sizeof(TA_) == sizeof(TB_)) {                                              \
+      HG_LAUNCH(name, (k_gemm_tn_lds<D, TA_, TB_, LA_, LB_>), grid, dim3(256), 0, s, n_rows, kc, la, lb, partial, \
+                cs);                                                                                       \
+    } else {                                                                                               \
+      HG_LAUNCH(name, (k_gemm_tn_bf<D, TA_, TB_, LA_, LB_>), grid, dim3(256), 0, s, n_rows, kc, la, lb, partial, \
+                cs);                                                                                       \
+    }                                                                                                      \
+  } while (0)
     if (list_a && list_b) {
       HG_TN_BF(true, true);
     } else if (!list_a && !list_b) {
