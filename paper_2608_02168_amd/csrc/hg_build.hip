@@ -741,8 +741,21 @@ __global__ void __launch_bounds__(kBT) k_row_count(const uint32_t* __restrict__ 
   const int m = (int)((n - base) < kRCChunk ? (n - base) : kRCChunk);
   const int p0 = t * kRCItems;
   uint32_t k[kRCItems];
+  if (p0 + kRCItems <= m) {
+    // 16 consecutive keys as four 16-byte loads (chunks start 64-byte aligned)
+    const uint4* kp = reinterpret_cast<const uint4*>(keys + base + p0);
 #pragma unroll
-  for (int j = 0; j < kRCItems; ++j) k[j] = (p0 + j < m) ? keys[base + p0 + j] : 0u;
+    for (int j = 0; j < kRCItems / 4; ++j) {
+      const uint4 v = kp[j];
+      k[4 * j] = v.x;
+      k[4 * j + 1] = v.y;
+      k[4 * j + 2] = v.z;
+      k[4 * j + 3] = v.w;
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < kRCItems; ++j) k[j] = (p0 + j < m) ? keys[base + p0 + j] : 0u;
+  }
   uint32_t prev = (p0 > 0 && p0 - 1 < m) ? keys[base + p0 - 1] : ~k[0];
   int nf = 0;
 #pragma unroll
