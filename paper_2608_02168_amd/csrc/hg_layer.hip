@@ -552,10 +552,9 @@ int layer_bwd_impl(const hg_subgraph* s, const hg_layer_desc* L, const T* Hin, c
   for (int t = 0; t < s->n_ntype; ++t) {
     const int64_t lo = s->type_off_host[t], hi = s->type_off_host[t + 1];
     LoadMasked<D, T> la{G, mask, rows_contig(lo), w.dZ};
-    // the residual addend G is A's own rows before masking; float32 rows of
-    // d = 128 are read again instead (held through the tile they would not
-    // fit the registers beside the next tile's rows and the split operand)
-    constexpr bool kFromA = !(D == 128 && sizeof(T) == 4);
+    // the residual addend G is A's own rows before masking (float32 rows of
+    // d = 128 hold them with 256 VGPRs, one block per compute unit)
+    constexpr bool kFromA = true;
     if constexpr (kBf) {
       StoreLast<D, T, kFromA> ep{reinterpret_cast<bf16_t*>(dHin), dacc, rows_contig(lo), nullptr,
                                  L->residual ? G : nullptr, cptr, R, -1};

@@ -562,8 +562,8 @@ struct F32Slice {
 //    epilogue operands are loaded before their MFMAs and stored right after.
 // The loader's fetch_row issues the loads; operand4 turns them into MFMA
 // operands (mask, conversion) when they are used.
-template <int D, bool kTransW, class ALoad, class Epi, bool kListA, bool kListO, int NG>
-__global__ void __launch_bounds__(kGemmThreads, D > 128 ? 2 : 4) k_gemm_rows_pp(int64_t n_rows,
+template <int D, bool kTransW, class ALoad, class Epi, bool kListA, bool kListO, int NG, int kMinWaves = (D > 128 ? 2 : 4)>
+__global__ void __launch_bounds__(kGemmThreads, kMinWaves) k_gemm_rows_pp(int64_t n_rows,
                                                                             const float* __restrict__ W,
                                                                             ALoad aload, Epi epi) {
   static_assert(D == 64 || D == 128 || D == 256, "pipelined gemm_rows: d = 64, 128 or 256");
@@ -783,11 +783,15 @@ int launch_gemm_rows_pp(const char* name, int64_t n_rows, const float* W, ALoad 
   // and, as the residual addend, may stay live through the tile: one column
   // block per group keeps it within 128 VGPRs
   constexpr int NG = (ALoad::kTee && (D == 128 || (Epi::kAddA && sizeof(typename ALoad::Raw) == 16))) ? 1 : 2;
+  // float32 masked rows at d = 128 holding the residual addend: 256 VGPRs,
+  // one block per compute unit (the residual is not read a second time)
+  constexpr bool kWide = ALoad::kTee && Epi::kAddA && D == 128 && sizeof(typename ALoad::Raw) == 16;
+  constexpr int kMinWaves = (D > 128 || kWide) ? 2 : 4;
   constexpr int DN = F32Slice<D>::DN;
   const int64_t tiles = cdiv(n_rows, 16 * (kGemmThreads / 64));
   // LDS holds a D x DN slice of op(W): 64 KB up to d = 128 (two resident
   // blocks per compute unit), 128 KB at d = 256 (one)
-  const int64_t cap = (int64_t)num_cus() * (D > 128 ? 1 : kGemmPPBlocksPerCu);
+  const int64_t cap = (int64_t)num_cus() * ((D > 128 || kWide) ? 1 : kGemmPPBlocksPerCu);
   int64_t grid = tiles < cap ? tiles : cap;
   // two column slices: 2 blocks per tile group, groups in multiples of 8 (the
   // kernel's block -> (slice, group) map pairs blocks 16 q + x and 16 q + 8 + x)
@@ -796,7 +800,7 @@ int launch_gemm_rows_pp(const char* name, int64_t n_rows, const float* W, ALoad 
   const bool la = aload.map.list != nullptr, lo = epi.map.list != nullptr;
 #define HG_PP_LAUNCH(LA_, LO_)                                                                          \
   do {                                                                                                  \
-    auto kern = k_gemm_rows_pp<D, kTransW, ALoad, Epi, LA_, LO_, NG>;                                   \
+    auto kern = k_gemm_rows_pp<D, kTransW, ALoad, Epi, LA_, LO_, NG, kMinWaves>;                        \
     if (lds > 65536) {                                                                                  \
       static bool attr_set = false;                                                                     \
       if (!attr_set) {                                                                                  \
