@@ -695,8 +695,11 @@ __global__ void k_dmu_rows(int64_t n_rows, int32_t R, int32_t T, const int32_t* 
 // Source pass: one wave per work item (CSC row q = i * R + r or a chunk of
 // it, at slot item.x); Kt and Vt of the row are read once, Q and dh~
 // gathered per out-edge.
+// At most 128 VGPRs from four heads on: four waves per SIMD for the gathers
+// in flight (130 registers, three waves, made the pass 7% slower); one or
+// two heads would spill there.
 template <int D, int S>
-__global__ void __launch_bounds__(kAttnThreads) k_hgt_attn_bwd_src(
+__global__ void __launch_bounds__(kAttnThreads, S >= 4 ? 4 : 1) k_hgt_attn_bwd_src(
     int64_t n_items, const int4* __restrict__ items, const int32_t* __restrict__ slot_q, int32_t R, int32_t T,
     const int32_t* __restrict__ type_off,
     const int32_t* __restrict__ csc_row, const float* __restrict__ Q, const float* __restrict__ Kt,
