@@ -105,7 +105,13 @@ constexpr int kRTile = kThreads * kRItems;
 // value per key two blocks fit a compute unit's LDS, 16 waves in flight.
 constexpr int kKeyThreads = 512;
 
-// Digit histogram of one tile of kTN items: hist[d * ntiles + tile].
+// Digit histogram of one tile of kTN items: hist[d * ntiles + tile].  Keys
+// of a whole tile are read as 16-byte vectors (4 consecutive keys per thread
+// and load).  Sorted runs of one key (a hub's entries once the lower digits
+// are sorted) would send all 64 lanes of an LDS atomic to one counter, which
+// serialises it: a wave whose 256 keys of a load all carry the wave's first
+// digit adds them with one atomic, and a thread adds equal neighbours among
+// its 4 keys together.
 template <bool kDigitArray, int kTN = kRTile>
 __global__ void k_radix_upsweep(const uint32_t* __restrict__ keys, const uint8_t* __restrict__ digits,
                                 int64_t n, int shift, uint32_t dmask, int32_t* __restrict__ hist,
@@ -114,16 +120,59 @@ __global__ void k_radix_upsweep(const uint32_t* __restrict__ keys, const uint8_t
   cnt[threadIdx.x] = 0;
   __syncthreads();
   const int64_t base = (int64_t)blockIdx.x * kTN;
+  const bool vec = !kDigitArray && base + kTN <= n && (reinterpret_cast<uintptr_t>(keys) & 15u) == 0;
+  if (vec) {
+    constexpr int kV = kTN / (4 * kThreads);
+    const uint4* kp = reinterpret_cast<const uint4*>(keys + base);
+    uint4 v[kV];
+#pragma unroll
+    for (int j = 0; j < kV; ++j) v[j] = kp[j * kThreads + threadIdx.x];
+#pragma unroll
+    for (int j = 0; j < kV; ++j) {
+      const uint32_t d0 = (v[j].x >> shift) & dmask, d1 = (v[j].y >> shift) & dmask;
+      const uint32_t d2 = (v[j].z >> shift) & dmask, d3 = (v[j].w >> shift) & dmask;
+      const uint32_t lead = (uint32_t)__builtin_amdgcn_readfirstlane((int)d0);
+      if (__ballot(d0 == lead && d1 == lead && d2 == lead && d3 == lead) == ~0ull) {
+        if ((threadIdx.x & (kWave - 1)) == 0) atomicAdd(&cnt[lead], 4 * kWave);
+      } else {
+        uint32_t pd = d0;
+        int pc = 1;
+        const uint32_t dn[3] = {d1, d2, d3};
+#pragma unroll
+        for (int q = 0; q < 3; ++q) {
+          if (dn[q] == pd) {
+            ++pc;
+          } else {
+            atomicAdd(&cnt[pd], pc);
+            pd = dn[q];
+            pc = 1;
+          }
+        }
+        atomicAdd(&cnt[pd], pc);
+      }
+    }
+  } else {
 #pragma unroll 4
-  for (int j = 0; j < kTN / kThreads; ++j) {
-    int64_t i = base + (int64_t)j * kThreads + threadIdx.x;
-    if (i < n) {
-      uint32_t d = kDigitArray ? (uint32_t)digits[i] : ((keys[i] >> shift) & dmask);
-      if (!kDigitArray || d != 255u) atomicAdd(&cnt[d], 1);
+    for (int j = 0; j < kTN / kThreads; ++j) {
+      int64_t i = base + (int64_t)j * kThreads + threadIdx.x;
+      if (i < n) {
+        uint32_t d = kDigitArray ? (uint32_t)digits[i] : ((keys[i] >> shift) & dmask);
+        if (!kDigitArray || d != 255u) atomicAdd(&cnt[d], 1);
+      }
     }
   }
   __syncthreads();
   hist[(int64_t)threadIdx.x * ntiles + blockIdx.x] = cnt[threadIdx.x];
+}
+
+// Tile of a scatter block: blocks go round-robin over the 8 XCDs, so block b
+// runs on XCD b mod 8; XCD x takes the x-th eighth of the tiles in order.  A
+// digit's run of tile t continues in tile t + 1, so consecutive tiles on one
+// XCD complete each other's partly written lines in that XCD's L2 before
+// they are written back (tiles on different XCDs leave two partial lines).
+__device__ __forceinline__ int64_t xcd_tile(int64_t b, int64_t ntiles) {
+  const int64_t q = ntiles >> 3, r = ntiles & 7, x = b & 7, i = b >> 3;
+  return x * q + (x < r ? x : r) + i;
 }
 
 // Stable scatter of one tile, staged through LDS.  Wave w owns the 2048
@@ -157,16 +206,17 @@ __global__ void __launch_bounds__(kT) k_radix_downsweep(
   const int t = threadIdx.x;
   const int w = t / kWave;
   const int l = lane_id();
+  const int64_t tile = xcd_tile(blockIdx.x, ntiles);
   int cnt = 0;
   if (t < 256) {
-    const int64_t fi = (int64_t)t * ntiles + blockIdx.x;
+    const int64_t fi = (int64_t)t * ntiles + tile;
     const int base = offs[fi];
     cnt = offs[fi + 1] - base;
     gbase[t] = base;
   }
   for (int q = t; q < kW * 256; q += kT) (&wcnt[0][0])[q] = 0;
   const uint64_t lt_mask = (l == 0) ? 0ull : (~0ull >> (kWave - l));
-  const int64_t wbase = (int64_t)blockIdx.x * kTN + (int64_t)w * (kI * kWave);
+  const int64_t wbase = tile * kTN + (int64_t)w * (kI * kWave);
   // all loads of the wave's slice first
   uint32_t kd[kI];  // key, or digit
   int32_t a1[kI], a2[kHasV2 ? kI : 1];
