@@ -112,12 +112,14 @@ constexpr int kKeyThreads = 512;
 // serialises it: a wave whose 256 keys of a load all carry the wave's first
 // digit adds them with one atomic, and a thread adds equal neighbours among
 // its 4 keys together.
-template <bool kDigitArray, int kTN = kRTile>
+template <bool kDigitArray, int kTN = kRTile, int kBins = 256>
 __global__ void k_radix_upsweep(const uint32_t* __restrict__ keys, const uint8_t* __restrict__ digits,
                                 int64_t n, int shift, uint32_t dmask, int32_t* __restrict__ hist,
                                 int64_t ntiles) {
-  __shared__ int cnt[256];
-  cnt[threadIdx.x] = 0;
+  static_assert(kBins % kThreads == 0, "bins in whole rounds of the block");
+  __shared__ int cnt[kBins];
+#pragma unroll
+  for (int q = 0; q < kBins; q += kThreads) cnt[q + threadIdx.x] = 0;
   __syncthreads();
   const int64_t base = (int64_t)blockIdx.x * kTN;
   const bool vec = !kDigitArray && base + kTN <= n && (reinterpret_cast<uintptr_t>(keys) & 15u) == 0;
@@ -162,7 +164,8 @@ __global__ void k_radix_upsweep(const uint32_t* __restrict__ keys, const uint8_t
     }
   }
   __syncthreads();
-  hist[(int64_t)threadIdx.x * ntiles + blockIdx.x] = cnt[threadIdx.x];
+#pragma unroll
+  for (int q = 0; q < kBins; q += kThreads) hist[(int64_t)(q + threadIdx.x) * ntiles + blockIdx.x] = cnt[q + threadIdx.x];
 }
 
 // Tile of a scatter block: blocks go round-robin over the 8 XCDs, so block b
@@ -189,16 +192,19 @@ __device__ __forceinline__ int64_t xcd_tile(int64_t b, int64_t ntiles) {
 // and its row's in-degree; v1_out gets the destination, scale_out 1 / deg.
 // kT threads per block (a multiple of 256), tiles of kTN items, kTN / kT
 // items per thread.
-template <bool kDigitArray, bool kHasV2, bool kUnpack = false, int kT = kThreads, int kTN = kRTile>
+template <bool kDigitArray, bool kHasV2, bool kUnpack = false, int kT = kThreads, int kTN = kRTile, int kBins = 256>
 __global__ void __launch_bounds__(kT) k_radix_downsweep(
     const uint32_t* __restrict__ keys, const uint8_t* __restrict__ digits,
     const int32_t* __restrict__ v1, const int32_t* __restrict__ v2, int64_t n, int shift, uint32_t dmask,
     const int32_t* __restrict__ offs, int64_t ntiles, uint32_t* __restrict__ keys_out,
     int32_t* __restrict__ v1_out, int32_t* __restrict__ v2_out, SortUnpack up = SortUnpack{nullptr, 1, nullptr}) {
   constexpr int kW = kT / kWave, kI = kTN / kT;
-  __shared__ int gbase[256];
-  __shared__ int loff[256];
-  __shared__ uint16_t wcnt[kW][256];  // counts, then offsets, below kTN
+  constexpr int kBits = kBins == 512 ? 9 : 8;
+  static_assert(kBins == 256 || (kBins == 512 && !kDigitArray), "8- or 9-bit key digits");
+  static_assert(kT >= kBins, "one thread per digit");
+  __shared__ int gbase[kBins];
+  __shared__ int loff[kBins];
+  __shared__ uint16_t wcnt[kW][kBins];  // counts, then offsets, below kTN
   __shared__ uint32_t sk[kDigitArray ? 1 : kTN];
   __shared__ int32_t sv1[kTN];
   __shared__ int32_t sv2[kHasV2 ? kTN : 1];
@@ -208,13 +214,13 @@ __global__ void __launch_bounds__(kT) k_radix_downsweep(
   const int l = lane_id();
   const int64_t tile = xcd_tile(blockIdx.x, ntiles);
   int cnt = 0;
-  if (t < 256) {
+  if (t < kBins) {
     const int64_t fi = (int64_t)t * ntiles + tile;
     const int base = offs[fi];
     cnt = offs[fi + 1] - base;
     gbase[t] = base;
   }
-  for (int q = t; q < kW * 256; q += kT) (&wcnt[0][0])[q] = 0;
+  for (int q = t; q < kW * kBins; q += kT) (&wcnt[0][0])[q] = 0;
   const uint64_t lt_mask = (l == 0) ? 0ull : (~0ull >> (kWave - l));
   const int64_t wbase = tile * kTN + (int64_t)w * (kI * kWave);
   // all loads of the wave's slice first
@@ -235,7 +241,7 @@ __global__ void __launch_bounds__(kT) k_radix_downsweep(
   }
   int lo = 0, kept = 0;
   lo = block_excl_scan<kT>(cnt, &kept);  // includes a barrier: wcnt zeroing is visible after it
-  if (t < 256) loff[t] = lo;
+  if (t < kBins) loff[t] = lo;
   // ranks inside the wave
   uint16_t rk[kI];
 #pragma unroll
@@ -245,7 +251,7 @@ __global__ void __launch_bounds__(kT) k_radix_downsweep(
     const bool valid = i < n && (!kDigitArray || d != 255u);
     uint64_t m = __ballot(valid);
 #pragma unroll
-    for (int b = 0; b < 8; ++b) {
+    for (int b = 0; b < kBits; ++b) {
       const bool bit = (d >> b) & 1u;
       const uint64_t bal = __ballot(bit);
       m &= bit ? bal : ~bal;
@@ -260,7 +266,7 @@ __global__ void __launch_bounds__(kT) k_radix_downsweep(
   }
   __syncthreads();
   // per digit: exclusive prefix over the waves, added to the tile-local offset
-  if (t < 256) {
+  if (t < kBins) {
     int run = loff[t];
 #pragma unroll
     for (int q = 0; q < kW; ++q) {
@@ -346,9 +352,41 @@ int scan_exclusive_i32(const int32_t* in, int32_t* out, int64_t n, int32_t* tota
 
 int64_t radix_scratch_elems(int64_t n) {
   const int64_t tiles = cdiv(n > 0 ? n : 1, kRTile);
-  const int64_t h = 256 * tiles;
+  const int64_t h = 512 * tiles;
   return h + 1 + scan_scratch_elems(h) + 64;
 }
+
+namespace {
+
+// One LSD pass over the digit of nb (<= 9) bits at shift: tile histograms,
+// their digit-major scan, the stable scatter.
+template <int kBins>
+int radix_pass(const uint32_t* ka, uint32_t* kb, const int32_t* a1, int32_t* b1, const int32_t* a2, int32_t* b2,
+               int64_t n, int shift, uint32_t dmask, int32_t* scratch, hipStream_t s, const SortUnpack* unpack) {
+  const int64_t tiles = cdiv(n, kRTile);
+  int32_t* hist = scratch;
+  int32_t* sscr = scratch + kBins * tiles + 1;
+  HG_LAUNCH("radix_upsweep", (k_radix_upsweep<false, kRTile, kBins>), dim3((unsigned)tiles), dim3(kThreads), 0, s,
+            ka, (const uint8_t*)nullptr, n, shift, dmask, hist, tiles);
+  HG_TRY(scan_exclusive_i32(hist, hist, kBins * tiles, hist + kBins * tiles, sscr, s));
+  if (unpack) {
+    HG_LAUNCH("radix_downsweep", (k_radix_downsweep<false, false, true, kKeyThreads, kRTile, kBins>),
+              dim3((unsigned)tiles), dim3(kKeyThreads), 0, s, ka, (const uint8_t*)nullptr, a1,
+              (const int32_t*)nullptr, n, shift, dmask, (const int32_t*)hist, tiles, kb, b1, (int32_t*)nullptr,
+              *unpack);
+  } else if (a2) {
+    HG_LAUNCH("radix_downsweep", (k_radix_downsweep<false, true, false, kKeyThreads, kRTile, kBins>),
+              dim3((unsigned)tiles), dim3(kKeyThreads), 0, s, ka, (const uint8_t*)nullptr, a1, a2, n, shift, dmask,
+              (const int32_t*)hist, tiles, kb, b1, b2);
+  } else {
+    HG_LAUNCH("radix_downsweep", (k_radix_downsweep<false, false, false, kKeyThreads, kRTile, kBins>),
+              dim3((unsigned)tiles), dim3(kKeyThreads), 0, s, ka, (const uint8_t*)nullptr, a1,
+              (const int32_t*)nullptr, n, shift, dmask, (const int32_t*)hist, tiles, kb, b1, (int32_t*)nullptr);
+  }
+  return HG_OK;
+}
+
+}  // namespace
 
 int radix_sort_pairs(uint32_t* keys, uint32_t* keys_alt, int32_t* v1, int32_t* v1_alt,
                      int32_t* v2, int32_t* v2_alt, int64_t n, int bits, int32_t* scratch,
@@ -362,38 +400,30 @@ int radix_sort_pairs(uint32_t* keys, uint32_t* keys_alt, int32_t* v1, int32_t* v
     if (bits < 1) bits = 1;  // a single key value still takes the unpacking pass
   }
   if (n <= 0 || bits <= 0) return HG_OK;
-  const int64_t tiles = cdiv(n, kRTile);
-  int32_t* hist = scratch;
-  int32_t* sscr = scratch + 256 * tiles + 1;
+  // Digits of 8 or 9 bits, as few passes as 9-bit digits allow: P passes
+  // take P * 8 bits with 8-bit digits and the first bits - 8 P of them one
+  // bit more (26 bits: 9, 9, 8 in three passes instead of four).
+  const int passes = (bits + 8) / 9;
+  const int wide = bits > 8 * passes ? bits - 8 * passes : 0;
   uint32_t *ka = keys, *kb = keys_alt;
   int32_t *a1 = v1, *b1 = v1_alt, *a2 = v2, *b2 = v2_alt;
-  for (int shift = 0; shift < bits; shift += 8) {
-    const int nb = (bits - shift) < 8 ? (bits - shift) : 8;
+  int shift = 0;
+  for (int p = 0; p < passes; ++p) {
+    const int nb = p < wide ? 9 : (bits - shift < 8 ? bits - shift : 8);
     const uint32_t dmask = (1u << nb) - 1u;
+    const bool last = p == passes - 1;
     // the last pass writes the values straight into their final arrays
-    if (shift + 8 >= bits) {
+    if (last) {
       if (v1_final) b1 = v1_final;
       if (v2_final && v2) b2 = v2_final;
     }
-    HG_LAUNCH("radix_upsweep", (k_radix_upsweep<false>), dim3((unsigned)tiles), dim3(kThreads), 0, s,
-              (const uint32_t*)ka, (const uint8_t*)nullptr, n, shift, dmask, hist, tiles);
-    HG_TRY(scan_exclusive_i32(hist, hist, 256 * tiles, hist + 256 * tiles, sscr, s));
-    if (unpack && shift + 8 >= bits) {
-      HG_LAUNCH("radix_downsweep", (k_radix_downsweep<false, false, true, kKeyThreads>), dim3((unsigned)tiles),
-                dim3(kKeyThreads), 0, s, (const uint32_t*)ka, (const uint8_t*)nullptr,
-                (const int32_t*)a1, (const int32_t*)nullptr, n, shift, dmask,
-                (const int32_t*)hist, tiles, kb, b1, (int32_t*)nullptr, *unpack);
-    } else if (v2) {
-      HG_LAUNCH("radix_downsweep", (k_radix_downsweep<false, true, false, kKeyThreads>), dim3((unsigned)tiles),
-                dim3(kKeyThreads), 0, s, (const uint32_t*)ka, (const uint8_t*)nullptr,
-                (const int32_t*)a1, (const int32_t*)a2, n, shift, dmask, (const int32_t*)hist,
-                tiles, kb, b1, b2);
+    const SortUnpack* up = (unpack && last) ? unpack : nullptr;
+    if (nb > 8) {
+      HG_TRY(radix_pass<512>(ka, kb, a1, b1, a2, b2, n, shift, dmask, scratch, s, up));
     } else {
-      HG_LAUNCH("radix_downsweep", (k_radix_downsweep<false, false, false, kKeyThreads>), dim3((unsigned)tiles),
-                dim3(kKeyThreads), 0, s, (const uint32_t*)ka, (const uint8_t*)nullptr,
-                (const int32_t*)a1, (const int32_t*)nullptr, n, shift, dmask,
-                (const int32_t*)hist, tiles, kb, b1, (int32_t*)nullptr);
+      HG_TRY(radix_pass<256>(ka, kb, a1, b1, a2, b2, n, shift, dmask, scratch, s, up));
     }
+    shift += nb;
     uint32_t* tk = ka; ka = kb; kb = tk;
     int32_t* t1 = a1; a1 = b1; b1 = t1;
     int32_t* t2 = a2; a2 = b2; b2 = t2;
