@@ -264,9 +264,11 @@ struct LoadRows {
   }
   // per-K-block form: the row as stored, and the MFMA operand
   __device__ __forceinline__ f32x4 stored4(const RowRaw& r, int kb) const { return Elt<T>::cook4(r.x[kb]); }
+  __device__ __forceinline__ f32x4 stored4r(const Raw& r) const { return Elt<T>::cook4(r); }
   __device__ __forceinline__ f32x4 operand4(const RowRaw& r, int kb, int) const { return Elt<T>::cook4(r.x[kb]); }
   static constexpr bool kTee = false;
   static constexpr bool kBoundByStored = false;
+  static constexpr bool kHalf = sizeof(T) == 2;
   __device__ __forceinline__ void tee4(int64_t, int, int, f32x4) const {}
 };
 
@@ -403,6 +405,7 @@ struct LoadMasked {
     }
   }
   __device__ __forceinline__ f32x4 stored4(const RowRaw& r, int kb) const { return Elt<T>::cook4(r.x[kb]); }
+  __device__ __forceinline__ f32x4 stored4r(const Raw& r) const { return Elt<T>::cook4(r); }
   __device__ __forceinline__ f32x4 operand4(const RowRaw& r, int kb, int g) const {
     f32x4 x = Elt<T>::cook4(r.x[kb]);
     const uint32_t nib = r.m[kb >> 1] >> (16 * (kb & 1) + 4 * g);
@@ -413,6 +416,7 @@ struct LoadMasked {
   static constexpr bool kTee = true;
   // |operand| <= |stored| element by element (the mask only zeroes)
   static constexpr bool kBoundByStored = true;
+  static constexpr bool kHalf = sizeof(T) == 2;
   __device__ __forceinline__ void tee4(int64_t b, int kb, int g, f32x4 x) const {
     if (!tee) return;
     T* o = tee + b * D + 16 * kb + 4 * g;
@@ -517,6 +521,12 @@ struct StoreLast {
 
 // Epilogues with kRowFlag take a per-row flag, read once per row before the
 // products (flag(ro)), in their stores (store4f).
+// loaders whose rows are stored in a 16-bit type (kHalf)
+template <class L, class = void>
+struct HalfRows : std::false_type {};
+template <class L>
+struct HalfRows<L, std::void_t<decltype(L::kHalf)>> : std::integral_constant<bool, L::kHalf> {};
+
 template <class E, class = void>
 struct EpiRowFlag : std::false_type {};
 template <class E>
@@ -562,20 +572,28 @@ struct F32Slice {
 //    epilogue operands are loaded before their MFMAs and stored right after.
 // The loader's fetch_row issues the loads; operand4 turns them into MFMA
 // operands (mask, conversion) when they are used.
-template <int D, bool kTransW, class ALoad, class Epi, bool kListA, bool kListO, int NG, int kMinWaves = (D > 128 ? 2 : 4)>
-__global__ void __launch_bounds__(kGemmThreads, kMinWaves) k_gemm_rows_pp(int64_t n_rows,
-                                                                            const float* __restrict__ W,
-                                                                            ALoad aload, Epi epi) {
+// kT threads per block, kPF: the next tile's A rows loaded while the current
+// one is multiplied (else each wave loads its rows and waits for them, and
+// the other waves of the compute unit cover the wait: at d = 256 one block
+// of 1024 threads, four waves per SIMD, within 128 VGPRs).
+template <int D, bool kTransW, class ALoad, class Epi, bool kListA, bool kListO, int NG, int kMinWaves = (D > 128 ? 2 : 4),
+          int kT = kGemmThreads, bool kPF = true>
+__global__ void __launch_bounds__(kT, kMinWaves) k_gemm_rows_pp(int64_t n_rows, const float* __restrict__ W,
+                                                                ALoad aload, Epi epi) {
   static_assert(D == 64 || D == 128 || D == 256, "pipelined gemm_rows: d = 64, 128 or 256");
   constexpr int DN = F32Slice<D>::DN;
   constexpr int KB = D / 16, KB2 = D / 32, NB = DN / 16;
   static_assert(!Epi::kMask || D == DN, "mask words need the whole row in one block");
   static_assert(NB % NG == 0, "column groups must divide the column blocks");
   static_assert(!Epi::kAddA || !kListO, "an addend taken from A needs the output rows to be the A rows");
-  constexpr int kRowsPerTile = 16 * (kGemmThreads / 64);
+  // rows stored in bfloat16 are exact fp16 high parts after the power-of-two
+  // scaling (8 significant bits; elements below 2^-32 of the row's largest
+  // lose bits of order 2^-38 of it), so their remainder products are skipped
+  constexpr bool kHiOnly = HalfRows<ALoad>::value;
+  constexpr int kRowsPerTile = 16 * (kT / 64);
   constexpr int kFrag = KB2 * NB * 64;
   extern __shared__ uint4 wfr[];  // [kFrag] high parts, then [kFrag] low parts
-  constexpr int kWaves = kGemmThreads / 64;
+  constexpr int kWaves = kT / 64;
   __shared__ float wmax[kWaves + 1];  // per-wave maxima, then the unscale factor of op(W)
   const int tid = threadIdx.x;
   // Block -> (column slice, tile group).  With two slices the blocks that
@@ -588,7 +606,7 @@ __global__ void __launch_bounds__(kGemmThreads, kMinWaves) k_gemm_rows_pp(int64_
   // largest |w| of op(W) (= of W)
   {
     float m = 0.f;
-    for (int e = tid; e < D * D / 4; e += kGemmThreads) {
+    for (int e = tid; e < D * D / 4; e += kT) {
       const f32x4 v = *reinterpret_cast<const f32x4*>(W + 4 * e);
       m = fmaxf(m, fmaxf(fmaxf(fabsf(v[0]), fabsf(v[1])), fmaxf(fabsf(v[2]), fabsf(v[3]))));
     }
@@ -601,7 +619,7 @@ __global__ void __launch_bounds__(kGemmThreads, kMinWaves) k_gemm_rows_pp(int64_
     for (int q = 1; q < kWaves; ++q) m = fmaxf(m, wmax[q]);
     const uint32_t ew = split_exp(m);
     const float sw = split_scale(ew);
-    for (int e = tid; e < kFrag; e += kGemmThreads) {
+    for (int e = tid; e < kFrag; e += kT) {
       const int l = e & 63;
       const int nb = (e >> 6) % NB;
       const int kb2 = (e >> 6) / NB;
@@ -650,6 +668,10 @@ __global__ void __launch_bounds__(kGemmThreads, kMinWaves) k_gemm_rows_pp(int64_
     // magnitude (or of a bound of it: the stored row, for loaders whose
     // operand only zeroes elements of it), split in two
     uint4 xh[KB2], xlo[KB2];
+    // with two column slices, the addend's half of the row (picked once, so
+    // the other half's registers are free during the products)
+    constexpr bool kHalfAdd = Epi::kAddA && D == 2 * DN;
+    typename ALoad::Raw xadd[kHalfAdd ? NB : 1];
     float ux;
     {
       auto absmax4 = [](f32x4 v) { return fmaxf(fmaxf(fabsf(v[0]), fabsf(v[1])), fmaxf(fabsf(v[2]), fabsf(v[3]))); };
@@ -677,11 +699,29 @@ __global__ void __launch_bounds__(kGemmThreads, kMinWaves) k_gemm_rows_pp(int64_
           v[q] = a0[q] * sx;
           v[4 + q] = a1[q] * sx;
         }
-        split8(v, xh[kb2], xlo[kb2]);
+        if constexpr (kHalfAdd) {
+          // K blocks 2 kb2 and 2 kb2 + 1 hold output columns of slice 0 when
+          // kb2 < KB2 / 2, of slice 1 otherwise
+          if (2 * kb2 < NB) {
+            xadd[2 * kb2] = slice == 0 ? x.x[2 * kb2] : x.x[NB + 2 * kb2];
+            xadd[2 * kb2 + 1] = slice == 0 ? x.x[2 * kb2 + 1] : x.x[NB + 2 * kb2 + 1];
+          }
+        }
+        if constexpr (kHiOnly) {
+          uint32_t h[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) h[q] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(v[2 * q], v[2 * q + 1]));
+          xh[kb2] = uint4{h[0], h[1], h[2], h[3]};
+        } else {
+          split8(v, xh[kb2], xlo[kb2]);
+        }
       }
     }
 #pragma unroll
     for (int p = 0; p < NB / NG; ++p) {
+      // without prefetching (128 VGPRs) each column group's W fragments are
+      // read where they are used, not hoisted ahead of earlier groups
+      if constexpr (!kPF) __builtin_amdgcn_sched_barrier(0);
       f32x4 pre[NG];
 #pragma unroll
       for (int q = 0; q < NG; ++q) {
@@ -695,7 +735,7 @@ __global__ void __launch_bounds__(kGemmThreads, kMinWaves) k_gemm_rows_pp(int64_
             st = aload.stored4(x, p * NG + q);
           } else {
             static_assert(D == 2 * DN, "two column slices");
-            st = slice == 0 ? aload.stored4(x, p * NG + q) : aload.stored4(x, NB + p * NG + q);
+            st = aload.stored4r(xadd[p * NG + q]);
           }
           pre[q] = epi.addend ? epi.bias4(col) + st : epi.bias4(col);
         } else {
@@ -712,9 +752,15 @@ __global__ void __launch_bounds__(kGemmThreads, kMinWaves) k_gemm_rows_pp(int64_
           const int e = (kb2 * NB + p * NG + q) * 64 + l;
           const uint4 bh = wfr[e], bl = wfr[kFrag + e];
           acc[q] = mfma_f16(bh, xh[kb2], acc[q]);
-          acc[q] = mfma_f16(bh, xlo[kb2], acc[q]);
+          if constexpr (!kHiOnly) acc[q] = mfma_f16(bh, xlo[kb2], acc[q]);
           acc[q] = mfma_f16(bl, xh[kb2], acc[q]);
         }
+        // the residual's half row stays live through the products: W
+        // fragments are read at most four K blocks ahead
+        if constexpr (!kPF && kHalfAdd) {
+          if (kb2 % 4 == 3) __builtin_amdgcn_sched_barrier(0);
+        }
+
       }
 #pragma unroll
       for (int q = 0; q < NG; ++q) acc[q] = split_unscale4(acc[q], ux, uw);
@@ -745,6 +791,16 @@ __global__ void __launch_bounds__(kGemmThreads, kMinWaves) k_gemm_rows_pp(int64_
   };
   int64_t t = bgroup;
   if (t >= ntiles) return;
+  if constexpr (!kPF) {
+    for (; t < ntiles; t += G) {
+      const KA ka = aload.map.template key<kListA>(row_in(t));
+      const KO ko = epi.map.template key<kListO>(row_in(t));
+      RR x;
+      aload.fetch_row(aload.map.template row_of<kListA>(ka), g, x);
+      tile(t, x, ka, ko);
+    }
+    return;
+  }
   KA ka0 = aload.map.template key<kListA>(row_in(t));
   KA ka1 = aload.map.template key<kListA>(row_in(t + G));
   KO ko0 = epi.map.template key<kListO>(row_in(t));
@@ -782,13 +838,19 @@ int launch_gemm_rows_pp(const char* name, int64_t n_rows, const float* W, ALoad 
   // the masked loader's rows (with their mask words) are the largest prefetch
   // and, as the residual addend, may stay live through the tile: one column
   // block per group keeps it within 128 VGPRs
+  // d = 256: one block of 1024 threads per compute unit (its LDS slice of
+  // op(W) takes 128 KB), no prefetch, 128 VGPRs -- except float32 rows held
+  // as the residual addend (64 VGPRs on top of their split parts), which keep
+  // the 512-thread prefetching kernel
+  constexpr bool kBig = D == 256 && !(Epi::kAddA && sizeof(typename ALoad::Raw) == 16);
   constexpr int NG = (ALoad::kTee && (D == 128 || (Epi::kAddA && sizeof(typename ALoad::Raw) == 16))) ? 1 : 2;
   // float32 masked rows at d = 128 holding the residual addend: 256 VGPRs,
   // one block per compute unit (the residual is not read a second time)
   constexpr bool kWide = ALoad::kTee && Epi::kAddA && D == 128 && sizeof(typename ALoad::Raw) == 16;
-  constexpr int kMinWaves = (D > 128 || kWide) ? 2 : 4;
+  constexpr int kT = kBig ? 2 * kGemmThreads : kGemmThreads;
+  constexpr int kMinWaves = kBig ? 1 : ((D > 128 || kWide) ? 2 : 4);
   constexpr int DN = F32Slice<D>::DN;
-  const int64_t tiles = cdiv(n_rows, 16 * (kGemmThreads / 64));
+  const int64_t tiles = cdiv(n_rows, 16 * (kT / 64));
   // LDS holds a D x DN slice of op(W): 64 KB up to d = 128 (two resident
   // blocks per compute unit), 128 KB at d = 256 (one)
   const int64_t cap = (int64_t)num_cus() * ((D > 128 || kWide) ? 1 : kGemmPPBlocksPerCu);
@@ -800,7 +862,7 @@ int launch_gemm_rows_pp(const char* name, int64_t n_rows, const float* W, ALoad 
   const bool la = aload.map.list != nullptr, lo = epi.map.list != nullptr;
 #define HG_PP_LAUNCH(LA_, LO_)                                                                          \
   do {                                                                                                  \
-    auto kern = k_gemm_rows_pp<D, kTransW, ALoad, Epi, LA_, LO_, NG, kMinWaves>;                        \
+    auto kern = k_gemm_rows_pp<D, kTransW, ALoad, Epi, LA_, LO_, NG, kMinWaves, kT, !kBig>;             \
     if (lds > 65536) {                                                                                  \
       static bool attr_set = false;                                                                     \
       if (!attr_set) {                                                                                  \
@@ -809,7 +871,7 @@ int launch_gemm_rows_pp(const char* name, int64_t n_rows, const float* W, ALoad 
         attr_set = true;                                                                                \
       }                                                                                                 \
     }                                                                                                   \
-    HG_LAUNCH(name, kern, dim3((unsigned)grid), dim3(kGemmThreads), lds, s, n_rows, W, aload, epi);          \
+    HG_LAUNCH(name, kern, dim3((unsigned)grid), dim3(kT), lds, s, n_rows, W, aload, epi);                   \
   } while (0)
   if constexpr (Epi::kAddA) {
     // the addend is read from the A registers: output row i must be A row i
