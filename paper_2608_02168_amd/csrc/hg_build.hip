@@ -607,14 +607,19 @@ __global__ void __launch_bounds__(kBT) k_edge_ids(const int32_t* __restrict__ sr
     bool keep = false;
     if (e < n_edges) {
       const int32_t s = src[e], d = dst[e];
-      int32_t a = rank_local(rt, off1, s);
-      const int32_t b = rank_local(rt, off1, d);
+      // the destination's entry is looked up only for an edge whose source
+      // is in the node set (in a sparse build most are not), and neither for
+      // an edge after the snapshot cut in a dense one (a sparse build still
+      // needs such an edge for the base edges)
+      const bool late = ts && ts[e] > t_cut;
+      int32_t a = (late && !sparse) ? -1 : rank_local(rt, off1, s);
+      const int32_t b = a >= 0 ? rank_local(rt, off1, d) : -1;
       if (sparse && a >= 0 && b >= 0) {
         const bool ps = bit_of(base_bits, s), pd = bit_of(base_bits, d);
         if (pd && !ps) atomicMin(&first[s], (int32_t)e);
         if (ps && !pd) atomicMin(&first[d], (int32_t)e);
       }
-      if (ts && ts[e] > t_cut) a = -1;
+      if (late) a = -1;
       keep = a >= 0 && b >= 0;
       sl[e] = a;
       dl[e] = b;
