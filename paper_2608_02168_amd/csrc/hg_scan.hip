@@ -105,6 +105,18 @@ constexpr int kRTile = kThreads * kRItems;
 // value per key two blocks fit a compute unit's LDS, 16 waves in flight.
 constexpr int kKeyThreads = 512;
 
+// Tile of a block: blocks go round-robin over the 8 XCDs, so block b runs on
+// XCD b mod 8; XCD x takes the x-th eighth of the tiles in order.  The
+// histogram pass writes digit d of tile t next to that of tile t + 1, and in
+// the scatter pass a digit's run of tile t continues in tile t + 1, so
+// consecutive tiles on one XCD complete each other's partly written lines in
+// that XCD's L2 before they are written back (tiles on different XCDs leave
+// two partial lines).
+__device__ __forceinline__ int64_t xcd_tile(int64_t b, int64_t ntiles) {
+  const int64_t q = ntiles >> 3, r = ntiles & 7, x = b & 7, i = b >> 3;
+  return x * q + (x < r ? x : r) + i;
+}
+
 // Digit histogram of one tile of kTN items: hist[d * ntiles + tile].  Keys
 // of a whole tile are read as 16-byte vectors (4 consecutive keys per thread
 // and load).  Sorted runs of one key (a hub's entries once the lower digits
@@ -121,7 +133,8 @@ __global__ void k_radix_upsweep(const uint32_t* __restrict__ keys, const uint8_t
 #pragma unroll
   for (int q = 0; q < kBins; q += kThreads) cnt[q + threadIdx.x] = 0;
   __syncthreads();
-  const int64_t base = (int64_t)blockIdx.x * kTN;
+  const int64_t tile = xcd_tile(blockIdx.x, ntiles);
+  const int64_t base = tile * kTN;
   const bool vec = !kDigitArray && base + kTN <= n && (reinterpret_cast<uintptr_t>(keys) & 15u) == 0;
   if (vec) {
     constexpr int kV = kTN / (4 * kThreads);
@@ -165,17 +178,7 @@ __global__ void k_radix_upsweep(const uint32_t* __restrict__ keys, const uint8_t
   }
   __syncthreads();
 #pragma unroll
-  for (int q = 0; q < kBins; q += kThreads) hist[(int64_t)(q + threadIdx.x) * ntiles + blockIdx.x] = cnt[q + threadIdx.x];
-}
-
-// Tile of a scatter block: blocks go round-robin over the 8 XCDs, so block b
-// runs on XCD b mod 8; XCD x takes the x-th eighth of the tiles in order.  A
-// digit's run of tile t continues in tile t + 1, so consecutive tiles on one
-// XCD complete each other's partly written lines in that XCD's L2 before
-// they are written back (tiles on different XCDs leave two partial lines).
-__device__ __forceinline__ int64_t xcd_tile(int64_t b, int64_t ntiles) {
-  const int64_t q = ntiles >> 3, r = ntiles & 7, x = b & 7, i = b >> 3;
-  return x * q + (x < r ? x : r) + i;
+  for (int q = 0; q < kBins; q += kThreads) hist[(int64_t)(q + threadIdx.x) * ntiles + tile] = cnt[q + threadIdx.x];
 }
 
 // Stable scatter of one tile, staged through LDS.  Wave w owns the 2048
