@@ -30,7 +30,8 @@ constexpr int kTThreads = 512;
 constexpr int kTWaves = kTThreads / 64;
 constexpr int kTMat = kTD * kTP;
 constexpr int kTVec = 7 * kTMat;  // then r, bi0 + bh0, bi1 + bh1, bi2, bh2
-constexpr size_t kTLds = sizeof(float) * (7 * kTMat + 5 * kTD);
+constexpr int kTUnscale = kTVec + 5 * kTD;  // then the 7 matrices' unscale factors
+constexpr size_t kTLds = sizeof(float) * (7 * kTMat + 5 * kTD + 8);
 
 struct TParams {
   const float *Q, *r, *Wi, *bi, *Wh, *bh;
@@ -44,13 +45,40 @@ struct TCtxOut {
   T* c[kTMaxW];
 };
 
-// LDS: Q, Wi[0..2], Wh[0..2] (row-major, pitch kTP), then the vectors.
+// LDS: Q, Wi[0..2], Wh[0..2] (row-major, pitch kTP), each scaled by the
+// power of two that brings its largest magnitude into [2^14, 2^15) (the
+// split-fp16 products, see t_gemm), then the vectors, then the 7 factors
+// that undo the scalings.
 __device__ __forceinline__ void t_stage(float* lds, const TParams& p) {
   constexpr int kDD = kTD * kTD;
+  __shared__ float wmax[kTWaves][7];
+  auto src_of = [&](int m) { return m == 0 ? p.Q : (m < 4 ? p.Wi + (m - 1) * kDD : p.Wh + (m - 4) * kDD); };
+  {
+    // largest |w| of each matrix: wave w reduces matrix m over its lanes,
+    // the block over its waves
+    const int wv = threadIdx.x >> 6, l = threadIdx.x & 63;
+    for (int m = 0; m < 7; ++m) {
+      const float* src = src_of(m);
+      float mx = 0.f;
+      for (int e = wv * 64 + l; e < kDD; e += kTThreads) mx = fmaxf(mx, fabsf(src[e]));
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+      if (l == 0) wmax[wv][m] = mx;
+    }
+  }
+  __syncthreads();
   for (int e = threadIdx.x; e < 7 * kDD; e += kTThreads) {
     const int m = e / kDD, ij = e - m * kDD;
-    const float* src = m == 0 ? p.Q : (m < 4 ? p.Wi + (m - 1) * kDD : p.Wh + (m - 4) * kDD);
-    lds[m * kTMat + (ij / kTD) * kTP + (ij % kTD)] = src[ij];
+    float mx = wmax[0][m];
+#pragma unroll
+    for (int q = 1; q < kTWaves; ++q) mx = fmaxf(mx, wmax[q][m]);
+    lds[m * kTMat + (ij / kTD) * kTP + (ij % kTD)] = src_of(m)[ij] * split_scale(split_exp(mx));
+  }
+  if (threadIdx.x < 7) {
+    float mx = wmax[0][threadIdx.x];
+#pragma unroll
+    for (int q = 1; q < kTWaves; ++q) mx = fmaxf(mx, wmax[q][threadIdx.x]);
+    lds[kTUnscale + threadIdx.x] = split_unscale(split_exp(mx));
   }
   float* v = lds + kTVec;
   for (int c = threadIdx.x; c < kTD; c += kTThreads) {
@@ -67,31 +95,81 @@ __device__ __forceinline__ void t_stage(float* lds, const TParams& p) {
 
 __device__ __forceinline__ f32x4 t_vec4(const float* v, int col) { return *reinterpret_cast<const f32x4*>(v + col); }
 
-// acc += x . op(M) for the 64 x 64 matrix M in LDS: lane (c, g) supplies
-// x[row c][16 kb + 4 g + s] and op(M)[16 kb + 4 g + s][16 nb + c] at MFMA step
-// s of K block kb, and receives row c, columns 16 nb + 4 g .. + 3.
+// acc += x . op(M) for the 64 x 64 matrix M = matrix mat in LDS (scaled, see
+// t_stage; its factor undoes the scaling) on the split-fp16 MFMA (v_mfma_f32_16x16x32_f16,
+// three products per K block: the high parts of both factors and each
+// factor's remainder against the other's high part, as in the row GEMMs).
+// The row is scaled by the power of two of its largest magnitude (the four
+// lanes of row c agree by two xor shuffles).  K block kb2 of 32 takes the
+// lane's columns 16 (2 kb2) + 4 g .. + 3 (slots 0-3) and 16 (2 kb2 + 1) +
+// 4 g .. + 3 (slots 4-7); lane (c, g) supplies op(M)[k][16 nb + c] for the
+// same k and receives row c, columns 16 nb + 4 g .. + 3, the layout x is
+// held in, so one product feeds the next.  op(M) = M is read as 8 words
+// down a column, op(M) = M^T as two 16-byte words along a row (pitch 68:
+// neither conflicts), and split into fp16 parts as it is read.
 template <bool kTrans>
-__device__ __forceinline__ void t_gemm(const float* M, const f32x4 (&x)[4], f32x4 (&acc)[4], int g, int c) {
+__device__ __forceinline__ void t_gemm(const float* lds, int mat, const f32x4 (&x)[4], f32x4 (&acc)[4], int g,
+                                       int c) {
+  const float* M = lds + mat * kTMat;
+  const float uw = lds[kTUnscale + mat];
+  float mx = 0.f;
 #pragma unroll
-  for (int kb = 0; kb < 4; ++kb) {
-    // each K block's fragments are read right before its MFMAs (hoisting
-    // every read of every product ahead would exhaust the registers)
-    __builtin_amdgcn_sched_barrier(0);
-    f32x4 w[4];
+  for (int b = 0; b < 4; ++b)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) mx = fmaxf(mx, fabsf(x[b][v]));
+  mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+  mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+  const uint32_t ex = split_exp(mx);
+  const float sx = split_scale(ex), ux = split_unscale(ex);
+  uint4 xh[2], xl[2];
+#pragma unroll
+  for (int kb2 = 0; kb2 < 2; ++kb2) {
+    float v[8];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      v[q] = x[2 * kb2][q] * sx;
+      v[4 + q] = x[2 * kb2 + 1][q] * sx;
+    }
+    split8(v, xh[kb2], xl[kb2]);
+  }
+  f32x4 t[4];
+#pragma unroll
+  for (int nb = 0; nb < 4; ++nb) t[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int kb2 = 0; kb2 < 2; ++kb2) {
 #pragma unroll
     for (int nb = 0; nb < 4; ++nb) {
+      // each fragment is read and split right before its MFMAs (hoisting
+      // them all would exhaust the registers)
+      __builtin_amdgcn_sched_barrier(0);
+      float w[8];
       if constexpr (kTrans) {
-        w[nb] = *reinterpret_cast<const f32x4*>(M + (16 * nb + c) * kTP + 16 * kb + 4 * g);
+        const float* q = M + (16 * nb + c) * kTP + 32 * kb2 + 4 * g;
+        const f32x4 a = *reinterpret_cast<const f32x4*>(q), b = *reinterpret_cast<const f32x4*>(q + 16);
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+          w[s] = a[s];
+          w[4 + s] = b[s];
+        }
       } else {
-        const float* q = M + (16 * kb + 4 * g) * kTP + 16 * nb + c;
-        w[nb] = f32x4{q[0], q[kTP], q[2 * kTP], q[3 * kTP]};
+        const float* q = M + (32 * kb2 + 4 * g) * kTP + 16 * nb + c;
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+          w[s] = q[s * kTP];
+          w[4 + s] = q[(16 + s) * kTP];
+        }
       }
+      uint4 wh, wl;
+      split8(w, wh, wl);
+      t[nb] = mfma_f16(wh, xh[kb2], t[nb]);
+      t[nb] = mfma_f16(wh, xl[kb2], t[nb]);
+      t[nb] = mfma_f16(wl, xh[kb2], t[nb]);
     }
-#pragma unroll
-    for (int s = 0; s < 4; ++s)
-#pragma unroll
-      for (int nb = 0; nb < 4; ++nb) acc[nb] = mfma4(w[nb][s], x[kb][s], acc[nb]);
   }
+#pragma unroll
+  for (int nb = 0; nb < 4; ++nb)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) acc[nb][v] += (t[nb][v] * ux) * uw;
 }
 
 template <class T>
@@ -137,7 +215,7 @@ __device__ __forceinline__ float t_tanh(float x) {
 
 // E12 for the lane's row: u_k = tanh(c_k Q^T), a = softmax(r . u_k), Ht.
 template <int W, int WA>
-__device__ __forceinline__ void t_attend(const float* Ql, const float* rv, const f32x4 (&cx)[WA][4], float (&a)[WA],
+__device__ __forceinline__ void t_attend(const float* lds, const float* rv, const f32x4 (&cx)[WA][4], float (&a)[WA],
                                          f32x4 (&ht)[4], int g, int c) {
   t_zero(ht);
   if constexpr (W > 0) {
@@ -146,7 +224,7 @@ __device__ __forceinline__ void t_attend(const float* Ql, const float* rv, const
     for (int k = 0; k < W; ++k) {
       f32x4 acc[4];
       t_zero(acc);
-      t_gemm<true>(Ql, cx[k], acc, g, c);
+      t_gemm<true>(lds, 0, cx[k], acc, g, c);
       float part = 0.f;
 #pragma unroll
       for (int b = 0; b < 4; ++b) {
@@ -178,20 +256,20 @@ __device__ __forceinline__ void t_attend(const float* Ql, const float* rv, const
 // The gate pre-activations without biases: ar = h Wi0 + Ht Wh0,
 // az = h Wi1 + Ht Wh1, ain = h Wi2, ahn = Ht Wh2.
 template <int W>
-__device__ __forceinline__ void t_gates(const float* Wil, const float* Whl, const f32x4 (&x)[4], const f32x4 (&ht)[4],
+__device__ __forceinline__ void t_gates(const float* lds, const f32x4 (&x)[4], const f32x4 (&ht)[4],
                                         f32x4 (&ar)[4], f32x4 (&az)[4], f32x4 (&ain)[4], f32x4 (&ahn)[4], int g,
                                         int c) {
   t_zero(ar);
   t_zero(az);
   t_zero(ain);
   t_zero(ahn);
-  t_gemm<false>(Wil, x, ar, g, c);
-  t_gemm<false>(Wil + kTMat, x, az, g, c);
-  t_gemm<false>(Wil + 2 * kTMat, x, ain, g, c);
+  t_gemm<false>(lds, 1, x, ar, g, c);
+  t_gemm<false>(lds, 2, x, az, g, c);
+  t_gemm<false>(lds, 3, x, ain, g, c);
   if constexpr (W > 0) {
-    t_gemm<false>(Whl, ht, ar, g, c);
-    t_gemm<false>(Whl + kTMat, ht, az, g, c);
-    t_gemm<false>(Whl + 2 * kTMat, ht, ahn, g, c);
+    t_gemm<false>(lds, 4, ht, ar, g, c);
+    t_gemm<false>(lds, 5, ht, az, g, c);
+    t_gemm<false>(lds, 6, ht, ahn, g, c);
   }
 }
 
@@ -201,9 +279,6 @@ __global__ void __launch_bounds__(kTThreads) k_temporal_fwd(int64_t n, const T* 
   constexpr int WA = W > 0 ? W : 1;
   extern __shared__ float lds[];
   t_stage(lds, p);
-  const float* Ql = lds;
-  const float* Wil = lds + kTMat;
-  const float* Whl = lds + 4 * kTMat;
   const float* vec = lds + kTVec;
   const int l = lane64(), g = l >> 4, c = l & 15;
   const int64_t ntiles = (n + 15) / 16;
@@ -217,9 +292,9 @@ __global__ void __launch_bounds__(kTThreads) k_temporal_fwd(int64_t n, const T* 
     t_load(h, ri, g, x);
 #pragma unroll
     for (int k = 0; k < W; ++k) t_load(C.c[k], ri, g, cx[k]);
-    t_attend<W, WA>(Ql, vec, cx, a, ht, g, c);
+    t_attend<W, WA>(lds, vec, cx, a, ht, g, c);
     f32x4 ar[4], az[4], ain[4], ahn[4];
-    t_gates<W>(Wil, Whl, x, ht, ar, az, ain, ahn, g, c);
+    t_gates<W>(lds, x, ht, ar, az, ain, ahn, g, c);
     f32x4 out[4];
 #pragma unroll
     for (int b = 0; b < 4; ++b) {
@@ -253,9 +328,6 @@ __global__ void __launch_bounds__(kTThreads) k_temporal_bwd(int64_t n, const T* 
   extern __shared__ float lds[];
   __shared__ f32x4 red[kTWaves][16];
   t_stage(lds, p);
-  const float* Ql = lds;
-  const float* Wil = lds + kTMat;
-  const float* Whl = lds + 4 * kTMat;
   const float* vec = lds + kTVec;
   const int l = lane64(), g = l >> 4, c = l & 15;
   const int wv = threadIdx.x >> 6;
@@ -273,9 +345,9 @@ __global__ void __launch_bounds__(kTThreads) k_temporal_bwd(int64_t n, const T* 
 #pragma unroll
     for (int k = 0; k < W; ++k) t_load(C.c[k], ri, g, cx[k]);
     t_load(dH, ri, g, dy);
-    t_attend<W, WA>(Ql, vec, cx, a, ht, g, c);
+    t_attend<W, WA>(lds, vec, cx, a, ht, g, c);
     f32x4 ar[4], az[4], ain[4], ahn[4];
-    t_gates<W>(Wil, Whl, x, ht, ar, az, ain, ahn, g, c);
+    t_gates<W>(lds, x, ht, ar, az, ain, ahn, g, c);
     // gate gradients, in place of the pre-activations
     f32x4 dht[4];
 #pragma unroll
@@ -309,14 +381,14 @@ __global__ void __launch_bounds__(kTThreads) k_temporal_bwd(int64_t n, const T* 
     }
     f32x4 acc[4];
     t_zero(acc);
-    t_gemm<true>(Wil, ar, acc, g, c);
-    t_gemm<true>(Wil + kTMat, az, acc, g, c);
-    t_gemm<true>(Wil + 2 * kTMat, ain, acc, g, c);
+    t_gemm<true>(lds, 1, ar, acc, g, c);
+    t_gemm<true>(lds, 2, az, acc, g, c);
+    t_gemm<true>(lds, 3, ain, acc, g, c);
     if (live) t_store(dh, i, g, acc);
     if constexpr (W > 0) {
-      t_gemm<true>(Whl, ar, dht, g, c);
-      t_gemm<true>(Whl + kTMat, az, dht, g, c);
-      t_gemm<true>(Whl + 2 * kTMat, ahn, dht, g, c);
+      t_gemm<true>(lds, 4, ar, dht, g, c);
+      t_gemm<true>(lds, 5, az, dht, g, c);
+      t_gemm<true>(lds, 6, ahn, dht, g, c);
       // softmax backward: da_k = dHt . c_k, ds_k = a_k (da_k - sum_j a_j da_j).
       // The context rows are read again here and u_k = tanh(c_k Q^T) is
       // recomputed, rather than both kept live through the products above
@@ -342,7 +414,7 @@ __global__ void __launch_bounds__(kTThreads) k_temporal_bwd(int64_t n, const T* 
         const float dsl = live ? ds : 0.f;
         f32x4 dp[4];
         t_zero(dp);
-        t_gemm<true>(Ql, cx[k], dp, g, c);
+        t_gemm<true>(lds, 0, cx[k], dp, g, c);
 #pragma unroll
         for (int b = 0; b < 4; ++b) {
           const f32x4 r4 = t_vec4(vec, 16 * b + 4 * g);
@@ -359,7 +431,7 @@ __global__ void __launch_bounds__(kTThreads) k_temporal_bwd(int64_t n, const T* 
           t_load(dC.c[k], ri, g, o);
 #pragma unroll
           for (int b = 0; b < 4; ++b) o[b] += a[k] * dht[b];
-          t_gemm<false>(Ql, dp, o, g, c);
+          t_gemm<false>(lds, 0, dp, o, g, c);
           if (live) t_store(dC.c[k], i, g, o);
         }
       }

@@ -56,6 +56,22 @@ def test_build_bit_exact(case):
     assert_same(ref, sub)
 
 
+# The CSR/CSC sorts take digits of 9 bits where that saves a pass: keys of
+# 9 bits sort in one 9-bit pass, of 18 bits in two, and the CSC sort's last
+# pass (which unpacks each entry's destination and scale) then runs with a
+# 9-bit digit.  Subgraph sizes n_sub * R that give exactly those key widths.
+DIGIT_PLANS = {9: 0.012, 18: 6.0}
+
+
+@pytest.mark.parametrize("bits", sorted(DIGIT_PLANS))
+def test_build_bit_exact_nine_bit_digits(bits):
+    cfg = synth.scaled(synth.WORKLOADS["tiny"].graph, DIGIT_PLANS[bits])
+    _, ref, sub = run_both(cfg, 0, select.THETA_NONE, None)
+    nq = ref.n_sub * cfg.n_rel
+    assert (nq - 1).bit_length() == bits, nq
+    assert_same(ref, sub)
+
+
 def test_build_deterministic():
     cfg, key, theta, budget = CASES["tiny_hindex_budget_cut"]
     g, _, a = run_both(cfg, key, theta, budget)
