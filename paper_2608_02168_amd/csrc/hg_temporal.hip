@@ -46,9 +46,10 @@ struct TCtxOut {
 };
 
 // LDS: Q, Wi[0..2], Wh[0..2] (row-major, pitch kTP), each scaled by the
-// power of two that brings its largest magnitude into [2^14, 2^15) (the
-// split-fp16 products, see t_gemm), then the vectors, then the 7 factors
-// that undo the scalings.
+// power of two that brings its largest magnitude into [2^14, 2^15) and held
+// as split-fp16 pairs (one 32-bit word per weight: the fp16 high part, then
+// the fp16 remainder; see t_gemm), then the vectors, then the 7 factors that
+// undo the scalings.
 __device__ __forceinline__ void t_stage(float* lds, const TParams& p) {
   constexpr int kDD = kTD * kTD;
   __shared__ float wmax[kTWaves][7];
@@ -67,12 +68,19 @@ __device__ __forceinline__ void t_stage(float* lds, const TParams& p) {
     }
   }
   __syncthreads();
+  uint32_t* wl = reinterpret_cast<uint32_t*>(lds);
   for (int e = threadIdx.x; e < 7 * kDD; e += kTThreads) {
     const int m = e / kDD, ij = e - m * kDD;
     float mx = wmax[0][m];
 #pragma unroll
     for (int q = 1; q < kTWaves; ++q) mx = fmaxf(mx, wmax[q][m]);
-    lds[m * kTMat + (ij / kTD) * kTP + (ij % kTD)] = src_of(m)[ij] * split_scale(split_exp(mx));
+    // the scaled weight as its fp16 high part (low half) and the fp16
+    // remainder (high half), as split8 forms them
+    const float v = src_of(m)[ij] * split_scale(split_exp(mx));
+    const auto hp = __builtin_amdgcn_cvt_pkrtz(v, 0.f);
+    const auto lp = __builtin_amdgcn_cvt_pkrtz(v - (float)hp[0], 0.f);
+    wl[m * kTMat + (ij / kTD) * kTP + (ij % kTD)] =
+        (__builtin_bit_cast(uint32_t, hp) & 0xFFFFu) | (__builtin_bit_cast(uint32_t, lp) << 16);
   }
   if (threadIdx.x < 7) {
     float mx = wmax[0][threadIdx.x];
@@ -106,11 +114,12 @@ __device__ __forceinline__ f32x4 t_vec4(const float* v, int col) { return *reint
 // same k and receives row c, columns 16 nb + 4 g .. + 3, the layout x is
 // held in, so one product feeds the next.  op(M) = M is read as 8 words
 // down a column, op(M) = M^T as two 16-byte words along a row (pitch 68:
-// neither conflicts), and split into fp16 parts as it is read.
+// neither conflicts); each word holds a weight's two fp16 parts, which are
+// regrouped into the MFMA's high-part and remainder operands.
 template <bool kTrans>
 __device__ __forceinline__ void t_gemm(const float* lds, int mat, const f32x4 (&x)[4], f32x4 (&acc)[4], int g,
                                        int c) {
-  const float* M = lds + mat * kTMat;
+  const uint32_t* M = reinterpret_cast<const uint32_t*>(lds) + mat * kTMat;
   const float uw = lds[kTUnscale + mat];
   float mx = 0.f;
 #pragma unroll
@@ -142,25 +151,27 @@ __device__ __forceinline__ void t_gemm(const float* lds, int mat, const f32x4 (&
       // each fragment is read and split right before its MFMAs (hoisting
       // them all would exhaust the registers)
       __builtin_amdgcn_sched_barrier(0);
-      float w[8];
+      uint32_t w[8];
       if constexpr (kTrans) {
-        const float* q = M + (16 * nb + c) * kTP + 32 * kb2 + 4 * g;
-        const f32x4 a = *reinterpret_cast<const f32x4*>(q), b = *reinterpret_cast<const f32x4*>(q + 16);
-#pragma unroll
-        for (int s = 0; s < 4; ++s) {
-          w[s] = a[s];
-          w[4 + s] = b[s];
-        }
+        const uint32_t* q = M + (16 * nb + c) * kTP + 32 * kb2 + 4 * g;
+        const uint4 a = *reinterpret_cast<const uint4*>(q), b = *reinterpret_cast<const uint4*>(q + 16);
+        w[0] = a.x; w[1] = a.y; w[2] = a.z; w[3] = a.w;
+        w[4] = b.x; w[5] = b.y; w[6] = b.z; w[7] = b.w;
       } else {
-        const float* q = M + (32 * kb2 + 4 * g) * kTP + 16 * nb + c;
+        const uint32_t* q = M + (32 * kb2 + 4 * g) * kTP + 16 * nb + c;
 #pragma unroll
         for (int s = 0; s < 4; ++s) {
           w[s] = q[s * kTP];
           w[4 + s] = q[(16 + s) * kTP];
         }
       }
-      uint4 wh, wl;
-      split8(w, wh, wl);
+      uint32_t h[4], r[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        h[q] = (w[2 * q] & 0xFFFFu) | (w[2 * q + 1] << 16);
+        r[q] = (w[2 * q] >> 16) | (w[2 * q + 1] & 0xFFFF0000u);
+      }
+      const uint4 wh{h[0], h[1], h[2], h[3]}, wl{r[0], r[1], r[2], r[3]};
       t[nb] = mfma_f16(wh, xh[kb2], t[nb]);
       t[nb] = mfma_f16(wh, xl[kb2], t[nb]);
       t[nb] = mfma_f16(wl, xh[kb2], t[nb]);
