@@ -47,7 +47,8 @@
  *    with each float32 operand split into parts, a published way to recover
  *    float32 accuracy from 16-bit matrix units:
  *      row transforms (forward transforms, dX, the alignment's Grams and
- *      gradient): the fp16 high part plus the fp16 remainder of each value,
+ *      gradient, the temporal module's products with Q, Wi and Wh): the
+ *      fp16 high part plus the fp16 remainder of each value,
  *      after scaling the row (and W) by a power of two so that its largest
  *      magnitude lies in [2^14, 2^15), with three of the four part
  *      products formed (Ootomo and Yokota, "Recovering single precision
