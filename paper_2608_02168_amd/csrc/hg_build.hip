@@ -573,12 +573,12 @@ __global__ void k_rank_pack(const int32_t* __restrict__ pre0, const int32_t* __r
   }
 }
 
-__device__ __forceinline__ int32_t rank_local(const RankEnt* __restrict__ rt, int32_t off1, int32_t v) {
-  const uint4 a = *reinterpret_cast<const uint4*>(rt + (v >> 5));
+// The local id of v from its group's entry (already loaded), -1 outside.
+__device__ __forceinline__ int32_t rank_of(uint4 a, int32_t off1, int32_t v) {
   const uint32_t bit = 1u << (v & 31), below = bit - 1u;
-  if (a.x & bit) return (int32_t)a.z + __popc(a.x & below);
-  if (a.y & bit) return off1 + (int32_t)a.w + __popc(a.y & below);
-  return -1;
+  const int32_t r0 = (int32_t)a.z + __popc(a.x & below);
+  const int32_t r1 = off1 + (int32_t)a.w + __popc(a.y & below);
+  return (a.x & bit) ? r0 : ((a.y & bit) ? r1 : -1);
 }
 
 // Edges in tiles of kETile = 16 rounds of kBT consecutive edges (round j of a
@@ -586,45 +586,89 @@ __device__ __forceinline__ int32_t rank_local(const RankEnt* __restrict__ rt, in
 constexpr int kERounds = 16;
 constexpr int kETile = kBT * kERounds;
 
-// Local ids of both endpoints of every edge (-1 outside the node set; an edge
-// after the snapshot cut gets source -1) and the number of kept edges per
-// tile.  In a sparse build also the base edge of every selected node: the
-// smallest index of an edge of the node set joining it to V_k (atomic
-// minimum; the selected nodes are few and of small key).
+// The CSR entry of every kept edge at its edge index: key dst_local * R + r
+// and the source's local id (and the edge id or weight when the sort
+// carries one); a bit per edge, set when the edge is kept (both endpoints in
+// the node set, not after the snapshot cut: keep[e / 64] bit e % 64, one
+// ballot per wave and round); and the number of kept edges per tile.  When
+// every edge is kept the entries are the sort's input as they stand;
+// otherwise k_edge_emit compacts them.  In a sparse build also the base edge of every
+// selected node: the smallest index of an edge of the node set joining it to
+// V_k (atomic minimum; the selected nodes are few and of small key).
+template <bool kTs, bool kW>
 __global__ void __launch_bounds__(kBT) k_edge_ids(const int32_t* __restrict__ src, const int32_t* __restrict__ dst,
+                                                  const uint8_t* __restrict__ rel, int32_t n_rel,
                                                   const RankEnt* __restrict__ rt, const int32_t* __restrict__ type_off,
                                                   const uint32_t* __restrict__ base_bits, const int32_t* __restrict__ ts,
-                                                  int32_t t_cut, int64_t n_edges, int sparse, int32_t* __restrict__ sl,
-                                                  int32_t* __restrict__ dl, int32_t* __restrict__ tile_cnt,
-                                                  int32_t* __restrict__ first) {
+                                                  int32_t t_cut, int64_t n_edges, int sparse,
+                                                  uint32_t* __restrict__ kcsr, int32_t* __restrict__ vsrc,
+                                                  int32_t* __restrict__ veid, const float* __restrict__ edge_w,
+                                                  int32_t* __restrict__ vw, uint64_t* __restrict__ keep_bits,
+                                                  int32_t* __restrict__ tile_cnt, int32_t* __restrict__ first) {
   __shared__ int32_t wsum[kBT / 64];
   const int64_t base = (int64_t)blockIdx.x * kETile;
   const int32_t off1 = type_off[1];
   int32_t c = 0;
-#pragma unroll 4
-  for (int j = 0; j < kERounds; ++j) {
-    const int64_t e = base + (int64_t)j * kBT + threadIdx.x;
-    bool keep = false;
-    if (e < n_edges) {
-      const int32_t s = src[e], d = dst[e];
-      // the destination's entry is looked up only for an edge whose source
-      // is in the node set (in a sparse build most are not), and neither for
-      // an edge after the snapshot cut in a dense one (a sparse build still
-      // needs such an edge for the base edges)
-      const bool late = ts && ts[e] > t_cut;
-      int32_t a = (late && !sparse) ? -1 : rank_local(rt, off1, s);
-      const int32_t b = a >= 0 ? rank_local(rt, off1, d) : -1;
-      if (sparse && a >= 0 && b >= 0) {
-        const bool ps = bit_of(base_bits, s), pd = bit_of(base_bits, d);
-        if (pd && !ps) atomicMin(&first[s], (int32_t)e);
-        if (ps && !pd) atomicMin(&first[d], (int32_t)e);
-      }
-      if (late) a = -1;
-      keep = a >= 0 && b >= 0;
-      sl[e] = a;
-      dl[e] = b;
+  // kEiItems rounds at a time, each phase's loads issued for all of them
+  // before any is used: the endpoints (with relation, weight and timestamp),
+  // then the sources' rank entries, then the destinations' (looked up only
+  // for an edge whose source is in the node set -- in a sparse build most
+  // are not -- and neither for an edge after the snapshot cut in a dense
+  // build; a sparse build still needs such an edge for the base edges)
+  constexpr int kEiItems = 4;
+  for (int j0 = 0; j0 < kERounds; j0 += kEiItems) {
+    int32_t sv[kEiItems], dv[kEiItems], wv[kEiItems];
+    uint32_t rv[kEiItems];
+    bool in[kEiItems], late[kEiItems];
+#pragma unroll
+    for (int u = 0; u < kEiItems; ++u) {
+      // past the end: the last edge's loads, and nothing kept
+      const int64_t e = base + (int64_t)(j0 + u) * kBT + threadIdx.x;
+      in[u] = e < n_edges;
+      const int64_t ec = in[u] ? e : n_edges - 1;
+      sv[u] = src[ec];
+      dv[u] = dst[ec];
+      rv[u] = rel[ec];
+      wv[u] = kW ? __float_as_int(edge_w[ec]) : 0;
+      late[u] = kTs ? ts[ec] > t_cut : false;
     }
-    c += __popcll(__ballot(keep));
+    uint4 ra[kEiItems];
+#pragma unroll
+    for (int u = 0; u < kEiItems; ++u) {
+      ra[u] = uint4{0u, 0u, 0u, 0u};
+      if (in[u] && !(late[u] && !sparse)) ra[u] = *reinterpret_cast<const uint4*>(rt + (sv[u] >> 5));
+    }
+    int32_t a[kEiItems];
+#pragma unroll
+    for (int u = 0; u < kEiItems; ++u) a[u] = rank_of(ra[u], off1, sv[u]);
+    uint4 rb[kEiItems];
+#pragma unroll
+    for (int u = 0; u < kEiItems; ++u) {
+      rb[u] = uint4{0u, 0u, 0u, 0u};
+      if (a[u] >= 0) rb[u] = *reinterpret_cast<const uint4*>(rt + (dv[u] >> 5));
+    }
+#pragma unroll
+    for (int u = 0; u < kEiItems; ++u) {
+      const int64_t e = base + (int64_t)(j0 + u) * kBT + threadIdx.x;
+      const int32_t b = a[u] >= 0 ? rank_of(rb[u], off1, dv[u]) : -1;
+      if (sparse && a[u] >= 0 && b >= 0) {
+        const bool ps = bit_of(base_bits, sv[u]), pd = bit_of(base_bits, dv[u]);
+        if (pd && !ps) atomicMin(&first[sv[u]], (int32_t)e);
+        if (ps && !pd) atomicMin(&first[dv[u]], (int32_t)e);
+      }
+      const bool keep = !late[u] && a[u] >= 0 && b >= 0;
+      if (keep) {
+        kcsr[e] = (uint32_t)b * (uint32_t)n_rel + rv[u];
+        vsrc[e] = a[u];
+        if (veid) veid[e] = (int32_t)e;
+        if (kW) vw[e] = wv[u];
+      }
+      const uint64_t kb = __ballot(keep);
+      // the wave's 64 edges start at a multiple of 64 (tiles of kETile)
+      if ((threadIdx.x & 63) == 0 && base + (int64_t)(j0 + u) * kBT + (threadIdx.x & ~63) < n_edges)
+        keep_bits[(base + (int64_t)(j0 + u) * kBT + threadIdx.x) >> 6] = kb;
+      c += __popcll(kb);
+    }
   }
   if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = c;
   __syncthreads();
@@ -636,30 +680,25 @@ __global__ void __launch_bounds__(kBT) k_edge_ids(const int32_t* __restrict__ sr
   }
 }
 
-// Stable compaction of the kept edges of a tile at tile_off[tile] (exclusive
-// scan of the tile counts): the rank of a kept edge is the number of kept
-// edges before it in (round, wave, lane) order, i.e. in edge order.
-__global__ void __launch_bounds__(kBT) k_edge_emit(const int32_t* __restrict__ sl, const int32_t* __restrict__ dl,
-                                                   const uint8_t* __restrict__ rel, int64_t n_edges, int32_t n_rel,
-                                                   const int32_t* __restrict__ tile_off, uint32_t* __restrict__ kcsr,
-                                                   int32_t* __restrict__ vsrc, int32_t* __restrict__ veid,
-                                                   const float* __restrict__ edge_w, int32_t* __restrict__ vw) {
+// Stable compaction of the kept CSR entries of a tile at tile_off[tile]
+// (exclusive scan of the tile counts): the rank of a kept entry is the
+// number of kept entries before it in (round, wave, lane) order, i.e. in
+// edge order.  v2 / o2: the second sort value (edge id or weight), or null.
+__global__ void __launch_bounds__(kBT) k_edge_emit(const uint32_t* __restrict__ kin, const int32_t* __restrict__ v1,
+                                                   const int32_t* __restrict__ v2,
+                                                   const uint64_t* __restrict__ keep_bits, int64_t n_edges,
+                                                   const int32_t* __restrict__ tile_off, uint32_t* __restrict__ kout,
+                                                   int32_t* __restrict__ o1, int32_t* __restrict__ o2) {
   constexpr int NW = kBT / 64;
   __shared__ int32_t cnt[kERounds * NW];
   const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
   const uint64_t lt = (l == 0) ? 0ull : (~0ull >> (64 - l));
   const int64_t base = (int64_t)blockIdx.x * kETile;
-  int32_t a[kERounds], b[kERounds];
   uint64_t bal[kERounds];
 #pragma unroll
   for (int j = 0; j < kERounds; ++j) {
-    const int64_t e = base + (int64_t)j * kBT + threadIdx.x;
-    a[j] = b[j] = -1;
-    if (e < n_edges) {
-      a[j] = sl[e];
-      b[j] = dl[e];
-    }
-    bal[j] = __ballot(a[j] >= 0 && b[j] >= 0);
+    const int64_t e0 = base + (int64_t)j * kBT + 64 * w;
+    bal[j] = e0 < n_edges ? keep_bits[e0 >> 6] : 0ull;
     if (l == 0) cnt[j * NW + w] = (int32_t)__popcll(bal[j]);
   }
   __syncthreads();
@@ -678,10 +717,9 @@ __global__ void __launch_bounds__(kBT) k_edge_emit(const int32_t* __restrict__ s
     if ((bal[j] >> l) & 1ull) {
       const int64_t e = base + (int64_t)j * kBT + threadIdx.x;
       const int32_t p = t0 + cnt[j * NW + w] + (int32_t)__popcll(bal[j] & lt);
-      kcsr[p] = (uint32_t)b[j] * (uint32_t)n_rel + (uint32_t)rel[e];
-      vsrc[p] = a[j];
-      if (veid) veid[p] = (int32_t)e;
-      if (vw) vw[p] = __float_as_int(edge_w[e]);
+      kout[p] = kin[e];
+      o1[p] = v1[e];
+      if (v2) o2[p] = v2[e];
     }
   }
 }
@@ -1321,29 +1359,38 @@ extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg
             out->global2local, w.cnt);
   // 6. induced-subgraph edges in original order, and the base edges of the
   // selected nodes
+  // the CSR sort carries the edge id if asked for, else a weighted graph's weight
+  const bool emit_w = weighted && !want_eid;
+  // with at most two node types the CSR entries are formed in edge order and
+  // compacted only if some edge was dropped (below, once the count is known)
+  bool rank_path = false;
+  const int64_t ntiles = cdiv(E, kETile);
   if (E > 0) {
     int32_t nb_host = 0;
     HG_HIP_TRY(hipMemcpyAsync(&nb_host, w.cnt + C_BASE, sizeof(int32_t), hipMemcpyDeviceToHost, s));
     HG_HIP_TRY(hipStreamSynchronize(s));
     const bool dense = dense_build(nb_host, o->budget_M, N);
-    // the CSR sort carries the edge id if asked for, else a weighted graph's weight
-    const bool emit_w = weighted && !want_eid;
     if (T <= 2) {
-      const int64_t nb = cdiv(N, 64) * 2, ntiles = cdiv(E, kETile);
+      rank_path = true;
+      const int64_t nb = cdiv(N, 64) * 2;
       HG_LAUNCH("build_rank_bits", k_rank_bits, dim3(grid_for(nb * kRankGroup)), dim3(kBT), 0, s, g->part, g->k,
                 (const uint8_t*)w.sel, g->ntype, N, w.rt, w.rc0, w.rc1);
       HG_TRY(scan_exclusive_i32(w.rc0, w.rc0, nb, nullptr, w.scratch, s));
       HG_TRY(scan_exclusive_i32(w.rc1, w.rc1, nb, nullptr, w.scratch, s));
       HG_LAUNCH("build_rank_pack", k_rank_pack, dim3(grid_for(nb)), dim3(kBT), 0, s, (const int32_t*)w.rc0,
                 (const int32_t*)w.rc1, nb, w.rt);
-      // local ids land in the sort's ping-pong buffers (free until the sorts)
-      HG_LAUNCH("build_edge_ids", k_edge_ids, dim3((unsigned)ntiles), dim3(kBT), 0, s, g->src, g->dst,
-                (const RankEnt*)w.rt, (const int32_t*)out->type_off, (const uint32_t*)w.bbits, g->edge_ts,
-                g->t_cut, E, dense ? 0 : 1, w.alt1, w.alt2, w.tile_cnt, w.first);
+#define HG_EDGE_IDS(TS_, W_)                                                                                   \
+  HG_LAUNCH("build_edge_ids", (k_edge_ids<TS_, W_>), dim3((unsigned)ntiles), dim3(kBT), 0, s, g->src, g->dst,     \
+            g->rel, (int32_t)R, (const RankEnt*)w.rt, (const int32_t*)out->type_off, (const uint32_t*)w.bbits,    \
+            g->edge_ts, g->t_cut, E, dense ? 0 : 1, w.kcsr, w.vsrc, want_eid ? w.veid : nullptr, g->edge_w,       \
+            emit_w ? w.vw : nullptr, reinterpret_cast<uint64_t*>(w.keep), w.tile_cnt, w.first)
+      if (g->edge_ts) {
+        if (emit_w) HG_EDGE_IDS(true, true); else HG_EDGE_IDS(true, false);
+      } else {
+        if (emit_w) HG_EDGE_IDS(false, true); else HG_EDGE_IDS(false, false);
+      }
+#undef HG_EDGE_IDS
       HG_TRY(scan_exclusive_i32(w.tile_cnt, w.tile_cnt, ntiles, w.cnt + C_ESUB, w.scratch, s));
-      HG_LAUNCH("build_edge_compact", k_edge_emit, dim3((unsigned)ntiles), dim3(kBT), 0, s, (const int32_t*)w.alt1,
-                (const int32_t*)w.alt2, g->rel, E, (int32_t)R, (const int32_t*)w.tile_cnt, w.kcsr, w.vsrc,
-                want_eid ? w.veid : nullptr, g->edge_w, emit_w ? w.vw : nullptr);
     } else {
       // more than two node types: local ids from global2local, membership from a bitmap
       HG_LAUNCH("build_member_bits", k_member_bits, dim3(gB), dim3(kBT), 0, s, g->part, g->k,
@@ -1385,8 +1432,19 @@ extern "C" int hg_build_csr(const hg_graph_desc* g, const hg_overlap_desc* o, hg
     // second value: the edge id if asked for, else the weight of a weighted graph
     int32_t* v2 = want_eid ? w.veid : (weighted ? w.vw : nullptr);
     int32_t* v2_final = want_eid ? out->csr_eid : (weighted ? reinterpret_cast<int32_t*>(out->csr_w) : nullptr);
-    HG_TRY(radix_sort_pairs(w.kcsr, w.kalt, w.vsrc, w.alt1, v2, v2 ? w.alt2 : nullptr, ES, bits, w.scratch, s, &ko,
-                            &v1o, &v2o, out->csr_col, v2_final));
+    uint32_t *sk = w.kcsr, *sk_alt = w.kalt;
+    int32_t *s1 = w.vsrc, *s1_alt = w.alt1, *s2 = v2, *s2_alt = v2 ? w.alt2 : nullptr;
+    if (rank_path && ES < E) {
+      // some edges were dropped: compact the entries into the ping-pong buffers
+      HG_LAUNCH("build_edge_compact", k_edge_emit, dim3((unsigned)ntiles), dim3(kBT), 0, s, (const uint32_t*)w.kcsr,
+                (const int32_t*)w.vsrc, (const int32_t*)v2, (const uint64_t*)w.keep, E, (const int32_t*)w.tile_cnt,
+                w.kalt, w.alt1, v2 ? w.alt2 : nullptr);
+      std::swap(sk, sk_alt);
+      std::swap(s1, s1_alt);
+      std::swap(s2, s2_alt);
+    }
+    HG_TRY(radix_sort_pairs(sk, sk_alt, s1, s1_alt, s2, s2_alt, ES, bits, w.scratch, s, &ko, &v1o, &v2o,
+                            out->csr_col, v2_final));
     csr_keys = ko;
     if (ES > 0 && v1o != out->csr_col) {  // no pass ran (a single key value)
       HG_HIP_TRY(hipMemcpyAsync(out->csr_col, v1o, sizeof(int32_t) * ES, hipMemcpyDeviceToDevice, s));
