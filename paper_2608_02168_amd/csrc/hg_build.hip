@@ -254,27 +254,39 @@ __global__ void __launch_bounds__(kAggBT) k_edges_pass(const int32_t* __restrict
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t e0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e0 < n_edges; e0 += kEpItems * stride) {
     int32_t sv[kEpItems], dv[kEpItems];
+    uint32_t rv[kEpItems], ws[kEpItems], wd[kEpItems];
     bool ok[kEpItems], ps[kEpItems], pd[kEpItems];
+    // loads without branches (an index past the end reads the last edge and
+    // counts for nothing; an endpoint out of range reads word 0), so the
+    // loads of all items are in flight together
 #pragma unroll
     for (int j = 0; j < kEpItems; ++j) {
       const int64_t e = e0 + j * stride;
-      sv[j] = dv[j] = 0;
-      ok[j] = false;
-      if (e < n_edges) {
-        sv[j] = src[e];
-        dv[j] = dst[e];
-        ok[j] = rel[e] < n_rel;
-      }
+      const int64_t ec = e < n_edges ? e : n_edges - 1;
+      sv[j] = src[ec];
+      dv[j] = dst[ec];
+      rv[j] = rel[ec];
+    }
+    uint32_t is[kEpItems], id[kEpItems];
+#pragma unroll
+    for (int j = 0; j < kEpItems; ++j) {
+      const bool in_range = sv[j] >= 0 && sv[j] < n_nodes && dv[j] >= 0 && dv[j] < n_nodes;
+      is[j] = in_range ? (uint32_t)sv[j] >> 5 : 0u;
+      id[j] = in_range ? (uint32_t)dv[j] >> 5 : 0u;
+    }
+#pragma unroll
+    for (int j = 0; j < kEpItems; ++j) {
+      ws[j] = base_bits[is[j]];
+      wd[j] = base_bits[id[j]];
     }
 #pragma unroll
     for (int j = 0; j < kEpItems; ++j) {
       const int64_t e = e0 + j * stride;
-      if (e < n_edges && !(ok[j] && sv[j] >= 0 && sv[j] < n_nodes && dv[j] >= 0 && dv[j] < n_nodes)) {
-        atomicOr(&cnt[C_ERR], 1);
-        ok[j] = false;
-      }
-      ps[j] = ok[j] && bit_of(base_bits, sv[j]);
-      pd[j] = ok[j] && bit_of(base_bits, dv[j]);
+      const bool in_range = sv[j] >= 0 && sv[j] < n_nodes && dv[j] >= 0 && dv[j] < n_nodes;
+      ok[j] = e < n_edges && in_range && rv[j] < (uint32_t)n_rel;
+      if (e < n_edges && !ok[j]) atomicOr(&cnt[C_ERR], 1);
+      ps[j] = ok[j] && ((ws[j] >> (sv[j] & 31)) & 1u);
+      pd[j] = ok[j] && ((wd[j] >> (dv[j] & 31)) & 1u);
     }
 #pragma unroll
     for (int j = 0; j < kEpItems; ++j) {
@@ -310,13 +322,28 @@ __global__ void __launch_bounds__(kAggBT) k_all_outdeg(const int32_t* __restrict
   LdsAgg<false, kDegBits> deg{lk, lv};
   deg.init();
   __syncthreads();
-  GRID_STRIDE(e, n_edges) {
-    const int32_t s = src[e], d = dst[e];
-    if (s < 0 || s >= n_nodes || d < 0 || d >= n_nodes || rel[e] >= n_rel) {
-      atomicOr(&cnt[C_ERR], 1);
-      continue;
+  // kEpItems edges per thread and round, all their loads issued first
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t e0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e0 < n_edges; e0 += kEpItems * stride) {
+    int32_t sv[kEpItems], dv[kEpItems];
+    uint32_t rv[kEpItems];
+#pragma unroll
+    for (int j = 0; j < kEpItems; ++j) {
+      const int64_t e = e0 + j * stride;
+      const int64_t ec = e < n_edges ? e : n_edges - 1;
+      sv[j] = src[ec];
+      dv[j] = dst[ec];
+      rv[j] = rel[ec];
     }
-    deg.put((uint32_t)s, 1, outdeg);
+#pragma unroll
+    for (int j = 0; j < kEpItems; ++j) {
+      if (e0 + j * stride >= n_edges) continue;
+      if (sv[j] < 0 || sv[j] >= n_nodes || dv[j] < 0 || dv[j] >= n_nodes || rv[j] >= (uint32_t)n_rel) {
+        atomicOr(&cnt[C_ERR], 1);
+        continue;
+      }
+      deg.put((uint32_t)sv[j], 1, outdeg);
+    }
   }
   __syncthreads();
   deg.flush(outdeg);
