@@ -1489,6 +1489,12 @@ __global__ void __launch_bounds__(256, 2) k_gemm_tn_lds(int64_t n_rows, int64_t 
   constexpr int S = 32;    // rows per step
   __shared__ uint4 fa[PA][4][TT];
   __shared__ uint4 fb[PB][4][TT];
+  // feature f's fragment sits at f ^ ((f / 16) mod 4): a staging thread
+  // writes 4 consecutive features and its neighbours the next 4, so without
+  // the swizzle a store of 32 lanes hits each bank 8 times; with it the
+  // stores spread over all banks, and the 16 lanes of a fragment read still
+  // find a permutation of 16 consecutive slots
+  auto swz = [](int f) { return f ^ ((f >> 4) & 3); };
   __shared__ float cred[4][TT];
   const int tid = threadIdx.x, w = tid >> 6, l = tid & 63;
   const int g = l >> 4, c = l & 15;
@@ -1571,9 +1577,9 @@ __global__ void __launch_bounds__(256, 2) k_gemm_tn_lds(int64_t n_rows, int64_t 
             for (int k = 0; k < 3; ++k) wv[k][p] = part[k];
           }
 #pragma unroll
-          for (int k = 0; k < 3; ++k) fb[k][sg][sf + q] = uint4{wv[k][0], wv[k][1], wv[k][2], wv[k][3]};
+          for (int k = 0; k < 3; ++k) fb[k][sg][swz(sf + q)] = uint4{wv[k][0], wv[k][1], wv[k][2], wv[k][3]};
         } else {
-          fb[0][sg][sf + q] = uint4{pair_bf(raw, 0, q), pair_bf(raw, 1, q), pair_bf(raw, 2, q), pair_bf(raw, 3, q)};
+          fb[0][sg][swz(sf + q)] = uint4{pair_bf(raw, 0, q), pair_bf(raw, 1, q), pair_bf(raw, 2, q), pair_bf(raw, 3, q)};
         }
       }
     } else {
@@ -1589,9 +1595,9 @@ __global__ void __launch_bounds__(256, 2) k_gemm_tn_lds(int64_t n_rows, int64_t 
             for (int k = 0; k < 3; ++k) wv[k][p] = part[k];
           }
 #pragma unroll
-          for (int k = 0; k < 3; ++k) fa[k][sg][sf + q] = uint4{wv[k][0], wv[k][1], wv[k][2], wv[k][3]};
+          for (int k = 0; k < 3; ++k) fa[k][sg][swz(sf + q)] = uint4{wv[k][0], wv[k][1], wv[k][2], wv[k][3]};
         } else {
-          fa[0][sg][sf + q] = uint4{pair_bf(raw, 0, q), pair_bf(raw, 1, q), pair_bf(raw, 2, q), pair_bf(raw, 3, q)};
+          fa[0][sg][swz(sf + q)] = uint4{pair_bf(raw, 0, q), pair_bf(raw, 1, q), pair_bf(raw, 2, q), pair_bf(raw, 3, q)};
         }
       }
     }
@@ -1610,12 +1616,12 @@ __global__ void __launch_bounds__(256, 2) k_gemm_tn_lds(int64_t n_rows, int64_t 
 #pragma unroll
       for (int jj = 0; jj < NJ; ++jj)
 #pragma unroll
-        for (int p = 0; p < PB; ++p) bq[jj][p] = fb[p][g][64 * qj + 16 * (j0 + jj) + c];
+        for (int p = 0; p < PB; ++p) bq[jj][p] = fb[p][g][swz(64 * qj + 16 * (j0 + jj) + c)];
 #pragma unroll
       for (int bi = 0; bi < 4; ++bi) {
         uint4 aq[PA];
 #pragma unroll
-        for (int p = 0; p < PA; ++p) aq[p] = fa[p][g][64 * qi + 16 * bi + c];
+        for (int p = 0; p < PA; ++p) aq[p] = fa[p][g][swz(64 * qi + 16 * bi + c)];
 #pragma unroll
         for (int jj = 0; jj < NJ; ++jj) {
 #pragma unroll
