@@ -619,9 +619,10 @@ constexpr int kETile = kBT * kERounds;
 // the node set, not after the snapshot cut: keep[e / 64] bit e % 64, one
 // ballot per wave and round); and the number of kept edges per tile.  When
 // every edge is kept the entries are the sort's input as they stand;
-// otherwise k_edge_emit compacts them.  In a sparse build also the base edge of every
-// selected node: the smallest index of an edge of the node set joining it to
-// V_k (atomic minimum; the selected nodes are few and of small key).
+// otherwise k_edge_emit compacts them.  In a sparse build also the base edge
+// of every selected node: the smallest index of an edge of the node set
+// joining it to V_k (atomic minimum; the selected nodes are few and of small
+// key).
 template <bool kTs, bool kW>
 __global__ void __launch_bounds__(kBT) k_edge_ids(const int32_t* __restrict__ src, const int32_t* __restrict__ dst,
                                                   const uint8_t* __restrict__ rel, int32_t n_rel,

@@ -533,25 +533,27 @@ template <class E>
 struct EpiRowFlag<E, std::void_t<decltype(E::kRowFlag)>> : std::integral_constant<bool, E::kRowFlag> {};
 
 // ---- row GEMMs on the split-fp16 MFMA: shared shape ------------------------------
-// Block = 8 waves sharing one LDS copy of a column slice of op(W); a wave owns
-// 16 rows, a block 128 rows; persistent over tiles.  W is D x D; blockIdx.y
-// picks the column slice [DN*y, DN*y + DN) (DN = D for D <= 128, 128 for
-// D = 256).  Products on the split-fp16 MFMA (split8): each row is scaled by
-// the power of two of its largest magnitude, op(W) by that of its own; LDS
-// holds the slice in fragment order, uint4 element (kb2*NB + nb)*64 + lane
-// being op(W)[k][col0 + 16 nb + lane%16] for the lane's 8 K slots of K block
-// kb2 (columns 16 (2 kb2) + 4 (lane/16) .. + 3 and the same 16 further on),
-// high parts first, then the remainders.
+// Block = 8 waves (16 at d = 256) sharing one LDS copy of a column slice of
+// op(W); a wave owns 16 rows of a tile; persistent over tiles.  W is D x D;
+// the column slice is [DN s, DN s + DN) (DN = D for D <= 128, 128 for
+// D = 256; the block index picks s and the tile group, see the kernel).
+// Products on the split-fp16 MFMA (split8): each row is scaled by the power
+// of two of its largest magnitude, op(W) by that of its own; LDS holds the
+// slice in fragment order, uint4 element (kb2*NB + nb)*64 + lane being
+// op(W)[k][col0 + 16 nb + lane%16] for the lane's 8 K slots of K block kb2
+// (columns 16 (2 kb2) + 4 (lane/16) .. + 3 and the same 16 further on), high
+// parts first, then the remainders.
 constexpr int kGemmThreads = 512;
 template <int D>
 struct F32Slice {
   static constexpr int DN = D > 128 ? 128 : D;
 };
 
-// ---- gemm_rows, software-pipelined (d <= 128) ---------------------------------------
+// ---- gemm_rows on the split-fp16 MFMA ------------------------------------------------
 // Row GEMM on the split-fp16 MFMA (v_mfma_f32_16x16x32_f16, three products
-// per K block, see split8): tiles of 16 rows per wave, 8 waves per block,
-// persistent over tiles, op(W) staged once per block in LDS.
+// per K block, see split8): tiles of 16 rows per wave, 8 waves per block (16
+// without prefetching at d = 256, see the launcher), persistent over tiles,
+// op(W) staged once per block in LDS.
 //  - Layout.  The MFMA computes the transpose (W fragments as its A operand,
 //    the rows as its B operand), so lane (c, g) ends with 4 consecutive
 //    columns 16 nb + 4 g of row c and the epilogue moves 16 bytes per lane.

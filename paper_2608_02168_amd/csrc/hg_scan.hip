@@ -97,8 +97,9 @@ __global__ void k_scan_tiles(const int32_t* __restrict__ in, int32_t* __restrict
 }
 
 // ---- radix sort -------------------------------------------------------------
-// Tiles of 8192 items (32 per thread): a digit's run inside a tile then
-// averages 32 items, so the scatter writes whole 128-byte lines.
+// Tiles of 8192 items: a run of an 8-bit digit inside a tile then averages
+// 32 items (128 bytes of keys), of a 9-bit digit 16; runs that continue in
+// the next tile are completed in the same L2 (see xcd_tile).
 constexpr int kRItems = 32;
 constexpr int kRTile = kThreads * kRItems;
 // Key sorts take 512 threads per scatter block (16 items each): with one
